@@ -1,0 +1,257 @@
+/*
+ * paragan.h -- C ABI of libparagan, the MI355X (gfx950) hot path of ParaGAN's
+ * per-replica BigGAN training: spectrally normalised convolutions,
+ * class-conditional BatchNorm, ReLU, nearest-upsample / avg-pool, the
+ * self-attention block, the hinge loss and the D:G train step.
+ *
+ * The paper (ParaGAN, SoCC'24) trains BigGAN data-parallel: every replica
+ * runs the generator and discriminator forward and backward passes on its
+ * share of the batch, then synchronises gradients (Design, "Computation
+ * Model").  This library is that per-replica compute on one GPU.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Status: every call returns PARAGAN_OK (0) or a negative PARAGAN_E*
+ *   code.  Arguments are validated on the host before anything is enqueued:
+ *   on error nothing has been launched and paragan_last_error() names the
+ *   problem.  No C++ exception crosses the ABI.
+ * - Streams: all device work is enqueued on the hipStream_t given to
+ *   paragan_create(), in order.  Calls are asynchronous unless stated.
+ * - Memory: every device buffer is allocated and owned by the caller and
+ *   passed as a plain device pointer.  The library never allocates device
+ *   memory.  Sizes of the "saved" (forward -> backward) and "ws" (scratch)
+ *   buffers come from the *_sizes() queries and must be 256-byte aligned.
+ * - Activations are NHWC.  Their channel stride is the channel count
+ *   rounded up to a multiple of 32 (paragan_cpad()); padded channels hold
+ *   zeros on input and are written as zeros.  dtype PARAGAN_BF16 means
+ *   bfloat16 activations with fp32 accumulation; PARAGAN_F32 means fp32
+ *   throughout.
+ * - Parameters of a module (block or network) live in ONE flat fp32 buffer
+ *   in the order given by paragan_*_layout(); gradients and the Adam moments
+ *   use the same layout.  Convolution weights are [Cout][kh][kw][Cin],
+ *   linear weights [out][in], embeddings [classes][dim].  Spectral
+ *   normalisation keeps one persistent fp32 vector u (length = the weight's
+ *   row count, Cout) per SN weight in a separate flat "u" buffer, in
+ *   layout order; training-mode forwards update it in place.
+ * - Threading: a context is used by one host thread at a time.
+ */
+#ifndef PARAGAN_H
+#define PARAGAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  PARAGAN_OK = 0,
+  PARAGAN_EINVAL = -1,        /* bad argument: null pointer, bad shape, ... */
+  PARAGAN_EUNSUPPORTED = -2,  /* valid request this build does not handle */
+  PARAGAN_EWORKSPACE = -3,    /* a buffer is smaller than the query said */
+  PARAGAN_EHIP = -4,          /* a HIP runtime call failed */
+  PARAGAN_ENONFINITE = -5     /* train step produced a NaN/Inf loss */
+};
+
+enum { PARAGAN_F32 = 0, PARAGAN_BF16 = 1 };
+
+typedef struct paragan_ctx paragan_ctx;
+
+/* Create a context bound to `hip_stream` (a hipStream_t; NULL = the null
+ * stream) on the current device.  Checks that the device is gfx950. */
+int paragan_create(paragan_ctx** out, void* hip_stream);
+void paragan_destroy(paragan_ctx* ctx);
+/* Message of the last failed call on this context (or of the last failed
+ * paragan_create when ctx is NULL).  Valid until the next call. */
+const char* paragan_last_error(const paragan_ctx* ctx);
+/* Block until all work enqueued by this context has finished. */
+int paragan_sync(paragan_ctx* ctx);
+
+/* Channel stride of an activation tensor with c channels. */
+int64_t paragan_cpad(int64_t c);
+
+/* One entry of a parameter layout. */
+typedef struct {
+  char name[48];       /* e.g. "g0.conv1.w" */
+  int32_t ndim;
+  int64_t shape[4];
+  int64_t offset;      /* in floats, into the flat parameter buffer */
+  int64_t u_offset;    /* in floats, into the flat u buffer; -1 if no SN */
+} paragan_tensor_info;
+
+/* ---------------------------------------------------------------------
+ * Spectral normalisation (BigGAN's SN, as cited in Related Work): one
+ * power iteration per training forward,
+ *     v <- N(W^T u),  u <- N(W v),  sigma = u^T W v,   N(t) = t / max(|t|, eps),
+ * repeated n_iter times.  W: device fp32, row-major rows x cols (the
+ * weight viewed as (Cout, kh*kw*Cin)).  u: device fp32 [rows], read and
+ * overwritten.  v: device fp32 [cols], written.  sigma: device fp32 scalar,
+ * written.  rows, cols >= 1; n_iter >= 1.  ws: device scratch of
+ * paragan_sn_ws_size() bytes, 256-byte aligned.
+ * ------------------------------------------------------------------- */
+int paragan_sn_ws_size(int64_t rows, int64_t cols, size_t* ws_bytes);
+int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t rows,
+                          int64_t cols, float* u, float* v, float* sigma,
+                          int n_iter, float eps, void* ws);
+
+/* ---------------------------------------------------------------------
+ * BigGAN generator residual block (spec block of the benchmark
+ * model, Evaluation "Experiment Setup"):
+ *   y = conv3x3(ReLU(cBN2(h1))) + b2 + conv1x1(up2(x)) + bsc,
+ *   h1 = conv3x3(up2(ReLU(cBN1(x)))) + b1,
+ *   cBN_k(t) = (1 + cond Wg_k^T) * BN(t) + cond Wb_k^T  (batch statistics),
+ * every weight spectrally normalised.  x: [B][H][W][cpad(cin)], y:
+ * [B][2H][2W][cpad(cout)], cond: fp32 [B][dc].  Parameter order from
+ * paragan_gblock_layout(): bn1.gain bn1.bias conv1.w conv1.b bn2.gain
+ * bn2.bias conv2.w conv2.b sc.w sc.b.
+ * ------------------------------------------------------------------- */
+typedef struct {
+  int32_t B, H, W;       /* input batch and spatial size (H, W >= 1) */
+  int32_t cin, cout, dc; /* channels in/out, width of cond */
+  int32_t dtype;         /* PARAGAN_BF16 or PARAGAN_F32 */
+  int32_t n_power_iter;  /* >= 1 */
+  float bn_eps, sn_eps;
+} paragan_gblock_desc;
+
+int paragan_gblock_layout(const paragan_gblock_desc* d,
+                          paragan_tensor_info* out, int32_t cap,
+                          int32_t* count, int64_t* n_params, int64_t* n_u);
+int paragan_gblock_sizes(const paragan_gblock_desc* d, size_t* saved_bytes,
+                         size_t* ws_bytes);
+int paragan_gblock_check(const paragan_gblock_desc* d);
+/* Training forward: updates u, writes y and `saved` (read by bwd). */
+int paragan_gblock_fwd(paragan_ctx* ctx, const paragan_gblock_desc* d,
+                       const float* params, float* u, const void* x,
+                       const float* cond, void* y, void* saved, void* ws);
+/* Backward from dy ([B][2H][2W][cpad(cout)]): writes dx (x's shape),
+ * dcond (fp32 [B][dc]) and grads (flat, parameter layout; overwritten). */
+int paragan_gblock_bwd(paragan_ctx* ctx, const paragan_gblock_desc* d,
+                       const float* params, const void* x, const float* cond,
+                       const void* saved, const void* dy, void* dx,
+                       float* dcond, float* grads, void* ws);
+
+/* ---------------------------------------------------------------------
+ * BigGAN discriminator residual block:
+ *   h = conv3x3([ReLU](x)) + b1,  main = [avgpool2](conv3x3(ReLU(h)) + b2),
+ *   y = main + skip,  skip = conv1x1([avgpool2](x)) + bsc (learnable) or x.
+ * x: [B][H][W][cpad(cin)] (bf16, or fp32 images when cin <= 4 and
+ * x_f32), y: [B][H'][W'][cpad(cout)].  Parameters: conv1.w conv1.b
+ * conv2.w conv2.b [sc.w sc.b].
+ * ------------------------------------------------------------------- */
+typedef struct {
+  int32_t B, H, W, cin, cout;
+  int32_t preact;        /* ReLU on the input of conv1 */
+  int32_t downsample;    /* 2x2 avg-pool (H, W even) */
+  int32_t learnable_sc;  /* 1x1 conv skip; required if cin != cout or pooled */
+  int32_t dtype;
+  int32_t n_power_iter;
+  float sn_eps;
+} paragan_dblock_desc;
+
+int paragan_dblock_layout(const paragan_dblock_desc* d,
+                          paragan_tensor_info* out, int32_t cap,
+                          int32_t* count, int64_t* n_params, int64_t* n_u);
+int paragan_dblock_sizes(const paragan_dblock_desc* d, size_t* saved_bytes,
+                         size_t* ws_bytes);
+int paragan_dblock_check(const paragan_dblock_desc* d);
+int paragan_dblock_fwd(paragan_ctx* ctx, const paragan_dblock_desc* d,
+                       const float* params, float* u, const void* x, void* y,
+                       void* saved, void* ws);
+/* dx may be NULL (input gradient not wanted). */
+int paragan_dblock_bwd(paragan_ctx* ctx, const paragan_dblock_desc* d,
+                       const float* params, const void* x, const void* saved,
+                       const void* dy, void* dx, float* grads, void* ws);
+
+/* ---------------------------------------------------------------------
+ * Self-attention block (bf16 only):
+ *   theta = x Wt^T (C/8), phi = maxpool2(x Wp^T) (C/8), g = maxpool2(x Wg^T)
+ *   (C/2), P = softmax over keys of theta phi^T (no scaling),
+ *   y = x + gamma * (P g) Wo^T.  SN on Wt Wp Wg Wo; gamma has none.
+ * x, y: [B][H][W][cpad(C)], H and W even, C a multiple of 8.
+ * Parameters: theta phi g o gamma.
+ * ------------------------------------------------------------------- */
+typedef struct {
+  int32_t B, H, W, C;
+  int32_t n_power_iter;
+  float sn_eps;
+} paragan_attn_desc;
+
+int paragan_attn_layout(const paragan_attn_desc* d, paragan_tensor_info* out,
+                        int32_t cap, int32_t* count, int64_t* n_params,
+                        int64_t* n_u);
+int paragan_attn_sizes(const paragan_attn_desc* d, size_t* saved_bytes,
+                       size_t* ws_bytes);
+int paragan_attn_check(const paragan_attn_desc* d);
+int paragan_attn_fwd(paragan_ctx* ctx, const paragan_attn_desc* d,
+                     const float* params, float* u, const void* x, void* y,
+                     void* saved, void* ws);
+int paragan_attn_bwd(paragan_ctx* ctx, const paragan_attn_desc* d,
+                     const float* params, const void* x, const void* saved,
+                     const void* dy, void* dx, float* grads, void* ws);
+
+/* ---------------------------------------------------------------------
+ * Full BigGAN G+D train step.  The architecture is given by channel
+ * multipliers (BigGAN-128: ch 96, G 16,16,8,4,2,1, D 1,2,4,8,16,16 with the
+ * last D block not pooling, attention at 64x64, 1000 classes, z 120 split
+ * into 6 chunks of 20, shared class embedding 128).  One call runs n_D
+ * discriminator steps, each on concat(real_k, G(z_k, y_k)) with labels
+ * concat(yr_k, yf_k) (inputs sharing a weight are batched, Implementation
+ * "Hardware-Aware Layout Transformation"), then one generator step on
+ * (z_g, y_g); the D:G ratio n_D is the caller's (Numerical Optimizations,
+ * "Asynchronous Update Scheme").  Hinge loss, Adam on fp32 master weights.
+ * ------------------------------------------------------------------- */
+typedef struct {
+  int32_t img;          /* output resolution */
+  int32_t ch;           /* base width */
+  int32_t n_g;          /* generator blocks */
+  int32_t g_mult[10];   /* n_g + 1 entries: C0 mult, then each block's out */
+  int32_t n_d;          /* discriminator blocks */
+  int32_t d_mult[10];   /* n_d entries */
+  int32_t d_down[10];   /* n_d entries, 0/1 */
+  int32_t attn_res;     /* 0: none */
+  int32_t n_classes, dz, shared_dim;
+  int32_t B;            /* per-GPU batch (D steps see 2B images) */
+  int32_t n_power_iter;
+  float bn_eps, sn_eps;
+  float lr_g, lr_d, beta1, beta2, adam_eps;
+} paragan_biggan_desc;
+
+/* which = 0: generator, 1: discriminator. */
+int paragan_net_layout(const paragan_biggan_desc* d, int32_t which,
+                       paragan_tensor_info* out, int32_t cap, int32_t* count,
+                       int64_t* n_params, int64_t* n_u);
+int paragan_biggan_check(const paragan_biggan_desc* d);
+int paragan_train_step_ws_size(const paragan_biggan_desc* d, size_t* ws_bytes);
+
+typedef struct {
+  float* params;   /* flat fp32 master weights (updated by Adam) */
+  float* u;        /* flat SN vectors (updated by every forward) */
+  float* grads;    /* flat fp32: the last gradient computed (overwritten) */
+  float* adam_m;   /* flat fp32 Adam moments */
+  float* adam_v;
+  int64_t adam_t;  /* Adam steps taken so far (host; incremented) */
+} paragan_net_state;
+
+typedef struct {
+  /* n_D entries each: */
+  const float* const* x_real;   /* fp32 [B][img][img][3] images in [-1,1] */
+  const int32_t* const* y_real; /* [B] */
+  const float* const* z_fake;   /* fp32 [B][dz] */
+  const int32_t* const* y_fake; /* [B] */
+  const float* z_g;             /* fp32 [B][dz] for the generator step */
+  const int32_t* y_g;           /* [B] */
+} paragan_step_inputs;
+
+/* Runs the step on the context's stream and synchronises once at the end.
+ * losses_host: n_D + 1 floats (L_D per D step, then L_G).  Returns
+ * PARAGAN_ENONFINITE (after finishing the step) if a loss is not finite. */
+int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
+                       paragan_net_state* G, paragan_net_state* D,
+                       const paragan_step_inputs* in, int32_t n_D, void* ws,
+                       float* losses_host);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PARAGAN_H */

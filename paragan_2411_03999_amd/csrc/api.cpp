@@ -1,0 +1,318 @@
+// C ABI of libparagan (include/paragan.h): argument validation, buffer
+// planning, and dispatch into the block executors.  Every entry point
+// catches all exceptions and turns them into status codes.
+#include <cstring>
+
+#include "../../include/paragan.h"
+#include "blocks.hpp"
+
+using namespace pg;
+
+static std::string g_create_err;
+
+static int fail(paragan_ctx* ctx, int code, const std::string& msg) {
+  if (ctx) ctx->err = msg;
+  else g_create_err = msg;
+  return code;
+}
+
+#define PG_TRY(ctx, ...)                                   \
+  try {                                                    \
+    __VA_ARGS__;                                           \
+    return PARAGAN_OK;                                     \
+  } catch (const ::pg::Error& e) {                         \
+    return fail(ctx, e.code, e.msg);                       \
+  } catch (const std::exception& e) {                      \
+    return fail(ctx, PARAGAN_EINVAL, e.what());            \
+  } catch (...) {                                          \
+    return fail(ctx, PARAGAN_EINVAL, "unknown error");     \
+  }
+
+extern "C" {
+
+int paragan_create(paragan_ctx** out, void* hip_stream) {
+  if (!out) return fail(nullptr, PARAGAN_EINVAL, "paragan_create: out is NULL");
+  try {
+    int dev = 0;
+    PG_HIP(hipGetDevice(&dev));
+    hipDeviceProp_t p;
+    PG_HIP(hipGetDeviceProperties(&p, dev));
+    if (std::strncmp(p.gcnArchName, "gfx950", 6) != 0)
+      throw Error{PARAGAN_EUNSUPPORTED, std::string("paragan needs gfx950, found ") + p.gcnArchName};
+    auto* c = new paragan_ctx;
+    c->stream = (hipStream_t)hip_stream;
+    c->device = dev;
+    c->n_cu = p.multiProcessorCount;
+    *out = c;
+    return PARAGAN_OK;
+  } catch (const Error& e) {
+    return fail(nullptr, e.code, e.msg);
+  }
+}
+
+void paragan_destroy(paragan_ctx* ctx) { delete ctx; }
+
+const char* paragan_last_error(const paragan_ctx* ctx) {
+  return ctx ? ctx->err.c_str() : g_create_err.c_str();
+}
+
+int paragan_sync(paragan_ctx* ctx) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, PG_HIP(hipStreamSynchronize(ctx->stream)))
+}
+
+int64_t paragan_cpad(int64_t c) { return cpad(c); }
+
+}  // extern "C"
+
+// ------------------------------------------------------------ helpers
+static void need(const void* p, const char* what) {
+  if (!p) throw Error{PARAGAN_EINVAL, std::string(what) + " is NULL"};
+}
+static void aligned(const void* p, const char* what) {
+  if (((uintptr_t)p & 255) != 0) throw Error{PARAGAN_EINVAL, std::string(what) + " is not 256-byte aligned"};
+}
+
+static int export_layout(const Layout& L, paragan_tensor_info* out, int32_t cap, int32_t* count,
+                         int64_t* n_params, int64_t* n_u) {
+  if (count) *count = (int32_t)L.e.size();
+  if (n_params) *n_params = L.n_params;
+  if (n_u) *n_u = L.n_u;
+  if (out) {
+    if (cap < (int32_t)L.e.size()) return PARAGAN_EINVAL;
+    for (size_t i = 0; i < L.e.size(); ++i) {
+      const Entry& e = L.e[i];
+      paragan_tensor_info& t = out[i];
+      std::memset(&t, 0, sizeof(t));
+      std::strncpy(t.name, e.name.c_str(), sizeof(t.name) - 1);
+      t.ndim = (int32_t)e.shape.size();
+      for (size_t d = 0; d < e.shape.size() && d < 4; ++d) t.shape[d] = e.shape[d];
+      t.offset = e.offset;
+      t.u_offset = e.u_offset;
+    }
+  }
+  return PARAGAN_OK;
+}
+
+// ------------------------------------------------------------ G block
+static void gcheck(const paragan_gblock_desc* d) {
+  if (!d) throw Error{PARAGAN_EINVAL, "gblock: desc is NULL"};
+  PG_CHECK(d->B >= 1 && d->H >= 1 && d->W >= 1, "gblock: B, H, W must be >= 1");
+  PG_CHECK(d->cin >= 1 && d->cout >= 1 && d->dc >= 1, "gblock: cin, cout, dc must be >= 1");
+  PG_CHECK(d->dtype == PARAGAN_BF16 || d->dtype == PARAGAN_F32, "gblock: dtype must be PARAGAN_BF16 or PARAGAN_F32");
+  PG_CHECK(d->n_power_iter >= 1, "gblock: n_power_iter must be >= 1");
+  PG_CHECK(d->bn_eps > 0.f && d->sn_eps > 0.f, "gblock: eps must be > 0");
+  PG_CHECK((int64_t)d->B * 4 * d->H * d->W < (1LL << 31), "gblock: too many output pixels");
+}
+
+static GBlock make_g(const paragan_gblock_desc* d) {
+  GBlock g;
+  g.B = d->B; g.H = d->H; g.W = d->W; g.cin = d->cin; g.cout = d->cout; g.dc = d->dc;
+  g.npi = d->n_power_iter; g.f32 = d->dtype == PARAGAN_F32; g.bn_eps = d->bn_eps; g.sn_eps = d->sn_eps;
+  Arena a(nullptr);
+  g.plan_saved(a);
+  return g;
+}
+
+extern "C" int paragan_gblock_check(const paragan_gblock_desc* d) { PG_TRY(nullptr, gcheck(d)) }
+
+extern "C" int paragan_gblock_layout(const paragan_gblock_desc* d, paragan_tensor_info* out, int32_t cap,
+                                     int32_t* count, int64_t* n_params, int64_t* n_u) {
+  try {
+    gcheck(d);
+    return export_layout(gblock_layout(d->cin, d->cout, d->dc), out, cap, count, n_params, n_u);
+  } catch (const Error& e) {
+    return fail(nullptr, e.code, e.msg);
+  }
+}
+
+extern "C" int paragan_gblock_sizes(const paragan_gblock_desc* d, size_t* saved, size_t* ws) {
+  PG_TRY(nullptr, {
+    gcheck(d);
+    GBlock g = make_g(d);
+    Arena a(nullptr);
+    g.plan_saved(a);
+    if (saved) *saved = a.off;
+    int dev = 0, ncu = 256;
+    if (hipGetDevice(&dev) == hipSuccess) {
+      hipDeviceProp_t p;
+      if (hipGetDeviceProperties(&p, dev) == hipSuccess) ncu = p.multiProcessorCount;
+    }
+    if (ws) *ws = g.ws_size(ncu);
+  })
+}
+
+static size_t g_ws_for(paragan_ctx* ctx, const GBlock& g) { return g.ws_size(ctx->n_cu); }
+
+extern "C" int paragan_gblock_fwd(paragan_ctx* ctx, const paragan_gblock_desc* d, const float* params, float* u,
+                                  const void* x, const float* cond, void* y, void* saved, void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    gcheck(d);
+    need(params, "params"); need(u, "u"); need(x, "x"); need(cond, "cond"); need(y, "y");
+    need(saved, "saved"); need(ws, "ws");
+    aligned(saved, "saved"); aligned(ws, "ws");
+    GBlock g = make_g(d);
+    Arena a(saved);
+    g.plan_saved(a);
+    Layout L = gblock_layout(d->cin, d->cout, d->dc);
+    Params P{&L, "", params, u, nullptr};
+    Exec ex{ctx->stream, ctx->n_cu, ws, g_ws_for(ctx, g)};
+    g.fwd(ex, P, x, cond, y);
+  })
+}
+
+extern "C" int paragan_gblock_bwd(paragan_ctx* ctx, const paragan_gblock_desc* d, const float* params,
+                                  const void* x, const float* cond, const void* saved, const void* dy, void* dx,
+                                  float* dcond, float* grads, void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    gcheck(d);
+    need(params, "params"); need(x, "x"); need(cond, "cond"); need(saved, "saved"); need(dy, "dy");
+    need(dx, "dx"); need(dcond, "dcond"); need(grads, "grads"); need(ws, "ws");
+    aligned(saved, "saved"); aligned(ws, "ws");
+    GBlock g = make_g(d);
+    Arena a((void*)saved);
+    g.plan_saved(a);
+    Layout L = gblock_layout(d->cin, d->cout, d->dc);
+    Params P{&L, "", params, nullptr, grads};
+    Exec ex{ctx->stream, ctx->n_cu, ws, g_ws_for(ctx, g)};
+    g.bwd(ex, P, x, cond, dy, dx, dcond, false);
+  })
+}
+
+// ------------------------------------------------------------ D block
+static void dcheck(const paragan_dblock_desc* d) {
+  if (!d) throw Error{PARAGAN_EINVAL, "dblock: desc is NULL"};
+  PG_CHECK(d->B >= 1 && d->H >= 1 && d->W >= 1, "dblock: B, H, W must be >= 1");
+  PG_CHECK(d->cin >= 1 && d->cout >= 1, "dblock: cin, cout must be >= 1");
+  PG_CHECK(d->dtype == PARAGAN_BF16 || d->dtype == PARAGAN_F32, "dblock: dtype must be PARAGAN_BF16 or PARAGAN_F32");
+  PG_CHECK(d->n_power_iter >= 1, "dblock: n_power_iter must be >= 1");
+  PG_CHECK(d->sn_eps > 0.f, "dblock: sn_eps must be > 0");
+  PG_CHECK(!d->downsample || (d->H % 2 == 0 && d->W % 2 == 0), "dblock: pooling needs even H and W");
+  PG_CHECK(d->learnable_sc || (d->cin == d->cout && !d->downsample),
+           "dblock: an identity skip needs cin == cout and no pooling");
+  PG_CHECK((int64_t)d->B * d->H * d->W < (1LL << 31), "dblock: too many pixels");
+}
+
+static DBlock make_d(const paragan_dblock_desc* d) {
+  DBlock b;
+  b.B = d->B; b.H = d->H; b.W = d->W; b.cin = d->cin; b.cout = d->cout; b.npi = d->n_power_iter;
+  b.preact = d->preact != 0; b.down = d->downsample != 0; b.lsc = d->learnable_sc != 0;
+  b.f32 = d->dtype == PARAGAN_F32; b.sn_eps = d->sn_eps;
+  Arena a(nullptr);
+  b.plan_saved(a);
+  return b;
+}
+
+extern "C" int paragan_dblock_check(const paragan_dblock_desc* d) { PG_TRY(nullptr, dcheck(d)) }
+
+extern "C" int paragan_dblock_layout(const paragan_dblock_desc* d, paragan_tensor_info* out, int32_t cap,
+                                     int32_t* count, int64_t* n_params, int64_t* n_u) {
+  try {
+    dcheck(d);
+    return export_layout(dblock_layout(d->cin, d->cout, d->learnable_sc != 0), out, cap, count, n_params, n_u);
+  } catch (const Error& e) {
+    return fail(nullptr, e.code, e.msg);
+  }
+}
+
+static int device_cus() {
+  int dev = 0, ncu = 256;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    hipDeviceProp_t p;
+    if (hipGetDeviceProperties(&p, dev) == hipSuccess) ncu = p.multiProcessorCount;
+  }
+  return ncu;
+}
+
+extern "C" int paragan_dblock_sizes(const paragan_dblock_desc* d, size_t* saved, size_t* ws) {
+  PG_TRY(nullptr, {
+    dcheck(d);
+    DBlock b = make_d(d);
+    Arena a(nullptr);
+    b.plan_saved(a);
+    if (saved) *saved = a.off;
+    if (ws) *ws = b.ws_size(device_cus());
+  })
+}
+
+extern "C" int paragan_dblock_fwd(paragan_ctx* ctx, const paragan_dblock_desc* d, const float* params, float* u,
+                                  const void* x, void* y, void* saved, void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    dcheck(d);
+    need(params, "params"); need(u, "u"); need(x, "x"); need(y, "y"); need(saved, "saved"); need(ws, "ws");
+    aligned(saved, "saved"); aligned(ws, "ws");
+    DBlock b = make_d(d);
+    Arena a(saved);
+    b.plan_saved(a);
+    Layout L = dblock_layout(d->cin, d->cout, d->learnable_sc != 0);
+    Params P{&L, "", params, u, nullptr};
+    Exec ex{ctx->stream, ctx->n_cu, ws, b.ws_size(ctx->n_cu)};
+    b.fwd(ex, P, x, y);
+  })
+}
+
+extern "C" int paragan_dblock_bwd(paragan_ctx* ctx, const paragan_dblock_desc* d, const float* params,
+                                  const void* x, const void* saved, const void* dy, void* dx, float* grads,
+                                  void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    dcheck(d);
+    need(params, "params"); need(x, "x"); need(saved, "saved"); need(dy, "dy"); need(grads, "grads");
+    need(ws, "ws");
+    aligned(saved, "saved"); aligned(ws, "ws");
+    DBlock b = make_d(d);
+    Arena a((void*)saved);
+    b.plan_saved(a);
+    Layout L = dblock_layout(d->cin, d->cout, d->learnable_sc != 0);
+    Params P{&L, "", params, nullptr, grads};
+    Exec ex{ctx->stream, ctx->n_cu, ws, b.ws_size(ctx->n_cu)};
+    b.bwd(ex, P, x, dy, dx, false);
+  })
+}
+
+// ------------------------------------------------------------ SN
+extern "C" int paragan_sn_ws_size(int64_t rows, int64_t cols, size_t* ws_bytes) {
+  PG_TRY(nullptr, {
+    PG_CHECK(rows >= 1 && cols >= 1, "sn_ws_size: rows and cols must be >= 1");
+    need(ws_bytes, "ws_bytes");
+    *ws_bytes = sn_ws_bytes(rows, cols);
+  })
+}
+
+extern "C" int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t rows, int64_t cols, float* u,
+                                     float* v, float* sigma, int n_iter, float eps, void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    need(W, "W"); need(u, "u"); need(v, "v"); need(sigma, "sigma"); need(ws, "ws");
+    aligned(ws, "ws");
+    PG_CHECK(rows >= 1 && cols >= 1, "sn_power_iter: rows and cols must be >= 1");
+    PG_CHECK(n_iter >= 1, "sn_power_iter: n_iter must be >= 1");
+    PG_CHECK(eps > 0.f, "sn_power_iter: eps must be > 0");
+    PG_CHECK(rows < (1LL << 31) && cols < (1LL << 31), "sn_power_iter: matrix too large");
+    sn_power_iter(ctx->stream, W, rows, cols, u, v, sigma, n_iter, eps, ws);
+  })
+}
+
+// ------------------------------------------------------------ not yet built
+#define PG_UNSUPPORTED(ctx) \
+  return fail(ctx, PARAGAN_EUNSUPPORTED, "not implemented in this build")
+
+extern "C" int paragan_attn_layout(const paragan_attn_desc*, paragan_tensor_info*, int32_t, int32_t*, int64_t*,
+                                   int64_t*) { PG_UNSUPPORTED(nullptr); }
+extern "C" int paragan_attn_sizes(const paragan_attn_desc*, size_t*, size_t*) { PG_UNSUPPORTED(nullptr); }
+extern "C" int paragan_attn_check(const paragan_attn_desc*) { PG_UNSUPPORTED(nullptr); }
+extern "C" int paragan_attn_fwd(paragan_ctx* ctx, const paragan_attn_desc*, const float*, float*, const void*,
+                                void*, void*, void*) { PG_UNSUPPORTED(ctx); }
+extern "C" int paragan_attn_bwd(paragan_ctx* ctx, const paragan_attn_desc*, const float*, const void*,
+                                const void*, const void*, void*, float*, void*) { PG_UNSUPPORTED(ctx); }
+extern "C" int paragan_net_layout(const paragan_biggan_desc*, int32_t, paragan_tensor_info*, int32_t, int32_t*,
+                                  int64_t*, int64_t*) { PG_UNSUPPORTED(nullptr); }
+extern "C" int paragan_biggan_check(const paragan_biggan_desc*) { PG_UNSUPPORTED(nullptr); }
+extern "C" int paragan_train_step_ws_size(const paragan_biggan_desc*, size_t*) { PG_UNSUPPORTED(nullptr); }
+extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc*, paragan_net_state*,
+                                  paragan_net_state*, const paragan_step_inputs*, int32_t, void*, float*) {
+  PG_UNSUPPORTED(ctx);
+}

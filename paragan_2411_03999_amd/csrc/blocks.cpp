@@ -1,0 +1,452 @@
+// Residual-block executors: the order of kernel launches for the BigGAN
+// generator and discriminator blocks, forward and backward.
+#include "blocks.hpp"
+
+namespace pg {
+
+const Entry& Layout::get(const std::string& name) const {
+  for (const auto& x : e)
+    if (x.name == name) return x;
+  throw Error{-1, "layout: no parameter named " + name};
+}
+
+void Layout::add_prefixed(const std::string& prefix, const Layout& sub) {
+  for (const auto& x : sub.e) add(prefix + x.name, x.shape, x.sn);
+}
+
+Layout gblock_layout(int cin, int cout, int dc) {
+  Layout L;
+  L.add("bn1.gain", {cin, dc}, true);
+  L.add("bn1.bias", {cin, dc}, true);
+  L.add("conv1.w", {cout, 3, 3, cin}, true);
+  L.add("conv1.b", {cout}, false);
+  L.add("bn2.gain", {cout, dc}, true);
+  L.add("bn2.bias", {cout, dc}, true);
+  L.add("conv2.w", {cout, 3, 3, cout}, true);
+  L.add("conv2.b", {cout}, false);
+  L.add("sc.w", {cout, 1, 1, cin}, true);
+  L.add("sc.b", {cout}, false);
+  return L;
+}
+
+Layout dblock_layout(int cin, int cout, bool lsc) {
+  Layout L;
+  L.add("conv1.w", {cout, 3, 3, cin}, true);
+  L.add("conv1.b", {cout}, false);
+  L.add("conv2.w", {cout, 3, 3, cout}, true);
+  L.add("conv2.b", {cout}, false);
+  if (lsc) {
+    L.add("sc.w", {cout, 1, 1, cin}, true);
+    L.add("sc.b", {cout}, false);
+  }
+  return L;
+}
+
+Layout attn_layout(int c) {
+  Layout L;
+  L.add("theta", {c / 8, 1, 1, c}, true);
+  L.add("phi", {c / 8, 1, 1, c}, true);
+  L.add("g", {c / 2, 1, 1, c}, true);
+  L.add("o", {c, 1, 1, c / 2}, true);
+  L.add("gamma", {1}, false);
+  return L;
+}
+
+static int64_t cols_of(const Entry& e) { return e.numel() / e.shape[0]; }
+
+void sn_forward(const Exec& ex, const Params& P, const std::string& name, SNSlot& s, int npi, float eps) {
+  const Entry& e = P.ent(name);
+  sn_power_iter(ex.st, P.p + e.offset, e.shape[0], cols_of(e), P.u + e.u_offset, s.v, s.sigma, npi, eps,
+                ex.ws, s.u);
+}
+
+static void plan_sn(Arena& a, SNSlot& s, int64_t rows, int64_t cols) {
+  s.u = a.f32(rows);
+  s.v = a.f32(cols);
+  s.sigma = a.f32(1);
+}
+
+static size_t esz(bool f32) { return f32 ? 4 : 2; }
+
+// ======================================================================
+// generator block
+// ======================================================================
+static const char* kGSN[7] = {"bn1.gain", "bn1.bias", "conv1.w", "bn2.gain", "bn2.bias", "conv2.w", "sc.w"};
+
+void GBlock::plan_saved(Arena& a) {
+  Cip = (int)cpad(cin);
+  Cop = (int)cpad(cout);
+  const int64_t cols[7] = {dc, dc, 9LL * cin, dc, dc, 9LL * cout, cin};
+  const int64_t rows[7] = {cin, cin, cout, cout, cout, cout, cout};
+  for (int i = 0; i < 7; ++i) plan_sn(a, sn[i], rows[i], cols[i]);
+  const size_t e = esz(f32);
+  wp1 = a.bytes((size_t)Cop * 9 * Cip * e);
+  wp2 = a.bytes((size_t)Cop * 9 * Cop * e);
+  wpsc = a.bytes((size_t)Cop * Cip * e);
+  mean1 = a.f32(Cip); rstd1 = a.f32(Cip);
+  gain1 = a.f32((size_t)B * Cip); bias1 = a.f32((size_t)B * Cip); scale1 = a.f32((size_t)B * Cip);
+  mean2 = a.f32(Cop); rstd2 = a.f32(Cop);
+  gain2 = a.f32((size_t)B * Cop); bias2 = a.f32((size_t)B * Cop); scale2 = a.f32((size_t)B * Cop);
+  h1 = a.bytes((size_t)B * 4 * H * W * Cop * e);
+}
+
+struct GWsF {
+  void* sn;
+  void* bn;
+  float* skip;
+};
+struct GWsB {
+  void *wd1, *wd2, *wdsc;
+  float *dwp1, *dwp2, *dwpsc, *dlin;
+  void* wg;
+  size_t wg_bytes;
+  void* cs;
+  float *dxs, *da2, *da1;
+  void* dh1;
+  float *dg1, *db1, *dg2, *db2, *part;
+  void* bnb;
+};
+
+static size_t g_sn_ws(const GBlock& g) {
+  size_t m = 0;
+  const int64_t rc[7][2] = {{g.cin, g.dc}, {g.cin, g.dc}, {g.cout, 9LL * g.cin}, {g.cout, g.dc},
+                            {g.cout, g.dc}, {g.cout, 9LL * g.cout}, {g.cout, g.cin}};
+  for (auto& r : rc) m = std::max(m, sn_ws_bytes(r[0], r[1]));
+  return m;
+}
+
+static GWsF g_carve_f(const GBlock& g, Arena& a) {
+  GWsF w;
+  const int64_t M1 = (int64_t)g.B * g.H * g.W, M2 = 4 * M1;
+  w.sn = a.bytes(g_sn_ws(g));
+  w.bn = a.bytes(std::max(bn_stats_ws_bytes(M1, g.cin), bn_stats_ws_bytes(M2, g.cout)));
+  w.skip = a.f32((size_t)M1 * g.Cop);
+  return w;
+}
+
+static GWsB g_carve_b(const GBlock& g, Arena& a, int n_cu) {
+  GWsB w;
+  const int64_t M1 = (int64_t)g.B * g.H * g.W, M2 = 4 * M1;
+  const size_t e = esz(g.f32);
+  w.wd1 = a.bytes((size_t)g.Cip * 9 * g.Cop * e);
+  w.wd2 = a.bytes((size_t)g.Cop * 9 * g.Cop * e);
+  w.wdsc = a.bytes((size_t)g.Cip * g.Cop * e);
+  w.dwp1 = a.f32((size_t)g.Cop * 9 * g.Cip);
+  w.dwp2 = a.f32((size_t)g.Cop * 9 * g.Cop);
+  w.dwpsc = a.f32((size_t)g.Cop * g.Cip);
+  w.dlin = a.f32((size_t)std::max(g.cin, g.cout) * g.dc);
+  w.wg_bytes = std::max({conv_wgrad_ws(g.f32, M2, 3, g.Cip, g.Cop, n_cu),
+                         conv_wgrad_ws(g.f32, M2, 3, g.Cop, g.Cop, n_cu),
+                         conv_wgrad_ws(g.f32, M2, 1, g.Cip, g.Cop, n_cu)});
+  w.wg = a.bytes(w.wg_bytes);
+  w.cs = a.bytes(colsum_ws_bytes(M2, g.Cop));
+  w.dxs = a.f32((size_t)M1 * g.Cip);
+  w.da2 = a.f32((size_t)M2 * g.Cop);
+  w.da1 = a.f32((size_t)M2 * g.Cip);
+  w.dh1 = a.bytes((size_t)M2 * g.Cop * e);
+  w.dg1 = a.f32((size_t)g.B * g.Cip); w.db1 = a.f32((size_t)g.B * g.Cip);
+  w.dg2 = a.f32((size_t)g.B * g.Cop); w.db2 = a.f32((size_t)g.B * g.Cop);
+  w.part = a.f32(256);
+  w.bnb = a.bytes(std::max(bn_bwd_ws_bytes(g.B, 4 * g.H * g.W, g.cout), bn_bwd_ws_bytes(g.B, g.H * g.W, g.cin)));
+  return w;
+}
+
+size_t GBlock::ws_size(int n_cu) const {
+  Arena a(nullptr), b(nullptr);
+  g_carve_f(*this, a);
+  g_carve_b(*this, b, n_cu);
+  return std::max(a.off, b.off);
+}
+
+void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y) {
+  Arena a(ex.ws);
+  GWsF w = g_carve_f(*this, a);
+  Exec exs = ex;
+  exs.ws = w.sn;
+  for (int i = 0; i < 7; ++i) sn_forward(exs, P, kGSN[i], sn[i], npi, sn_eps);
+  pack_weight(ex.st, f32, P.w("conv1.w"), sn[2].sigma, cout, cin, 3, Cop, Cip, false, wp1);
+  pack_weight(ex.st, f32, P.w("conv2.w"), sn[5].sigma, cout, cout, 3, Cop, Cop, false, wp2);
+  pack_weight(ex.st, f32, P.w("sc.w"), sn[6].sigma, cout, cin, 1, Cop, Cip, false, wpsc);
+  const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
+  // cBN1 statistics and tables
+  bn_stats(ex.st, f32, x, M1, cin, Cip, bn_eps, mean1, rstd1, w.bn);
+  cbn_tables(ex.st, cond, dc, P.w("bn1.gain"), P.w("bn1.bias"), sn[0].sigma, sn[1].sigma, nullptr, nullptr,
+             rstd1, B, cin, Cip, gain1, bias1, scale1);
+  // h1 = conv3x3(up2(relu(cbn1(x)))) + b1
+  ConvIn in;
+  in.x = x; in.B = B; in.Hx = H; in.Wx = W; in.C = Cip;
+  in.gather = G_UP2; in.mean = mean1; in.scale = scale1; in.shift = bias1; in.tab_stride = Cip; in.relu = 1;
+  ConvOut o;
+  o.y = h1; o.y_f32 = f32; o.yC = Cop; o.n_real = cout; o.bias = P.w("conv1.b");
+  conv_fwd(ex.st, f32, in, 2 * H, 2 * W, 3, wp1, Cop, o);
+  // cBN2
+  bn_stats(ex.st, f32, h1, M2, cout, Cop, bn_eps, mean2, rstd2, w.bn);
+  cbn_tables(ex.st, cond, dc, P.w("bn2.gain"), P.w("bn2.bias"), sn[3].sigma, sn[4].sigma, nullptr, nullptr,
+             rstd2, B, cout, Cop, gain2, bias2, scale2);
+  // skip at low resolution (conv1x1 commutes with the nearest upsample)
+  ConvIn si;
+  si.x = x; si.B = B; si.Hx = H; si.Wx = W; si.C = Cip;
+  ConvOut so;
+  so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b");
+  conv_fwd(ex.st, f32, si, H, W, 1, wpsc, Cop, so);
+  // y = conv3x3(relu(cbn2(h1))) + b2 + up2(skip)
+  ConvIn i2;
+  i2.x = h1; i2.B = B; i2.Hx = 2 * H; i2.Wx = 2 * W; i2.C = Cop;
+  i2.mean = mean2; i2.scale = scale2; i2.shift = bias2; i2.tab_stride = Cop; i2.relu = 1;
+  ConvOut o2;
+  o2.y = y; o2.y_f32 = f32; o2.yC = Cop; o2.n_real = cout; o2.bias = P.w("conv2.b");
+  o2.res = w.skip; o2.res_f32 = 1; o2.res_mode = R_HALF; o2.resC = Cop;
+  conv_fwd(ex.st, f32, i2, 2 * H, 2 * W, 3, wp2, Cop, o2);
+}
+
+void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* cond, const void* dy, void* dx,
+                 float* dcond, bool dcond_acc) {
+  Arena a(ex.ws);
+  GWsB w = g_carve_b(*this, a, ex.n_cu);
+  const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
+  const int H2 = 2 * H, W2 = 2 * W;
+  pack_weight(ex.st, f32, P.w("conv1.w"), sn[2].sigma, cout, cin, 3, Cop, Cip, true, w.wd1);
+  pack_weight(ex.st, f32, P.w("conv2.w"), sn[5].sigma, cout, cout, 3, Cop, Cop, true, w.wd2);
+  pack_weight(ex.st, f32, P.w("sc.w"), sn[6].sigma, cout, cin, 1, Cop, Cip, true, w.wdsc);
+  // conv2: dW2, db2
+  GradIn gdy;
+  gdy.g = dy; gdy.Hs = H2; gdy.Ws = W2; gdy.C = Cop;
+  ConvIn a2;
+  a2.x = h1; a2.B = B; a2.Hx = H2; a2.Wx = W2; a2.C = Cop;
+  a2.mean = mean2; a2.scale = scale2; a2.shift = bias2; a2.tab_stride = Cop; a2.relu = 1;
+  conv_wgrad(ex.st, f32, gdy, a2, H2, W2, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
+  colsum(ex.st, f32, dy, M2, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
+  // skip: dWsc at full resolution against up2(x); dbsc = db2
+  ConvIn ax;
+  ax.x = x; ax.B = B; ax.Hx = H; ax.Wx = W; ax.C = Cip; ax.gather = G_UP2;
+  conv_wgrad(ex.st, f32, gdy, ax, H2, W2, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
+  colsum(ex.st, f32, dy, M2, cout, Cop, 1.f, P.gr("sc.b"), w.cs);
+  // dx_skip = Wsc^T sum2x2(dy)   (low resolution, fp32)
+  ConvIn dsp;
+  dsp.x = dy; dsp.B = B; dsp.Hx = H2; dsp.Wx = W2; dsp.C = Cop; dsp.gather = G_POOL2;
+  ConvOut dso;
+  dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = cin;
+  conv_fwd(ex.st, f32, dsp, H, W, 1, w.wdsc, Cip, dso);
+  // da2 = conv2^T dy (fp32)
+  ConvIn d2;
+  d2.x = dy; d2.B = B; d2.Hx = H2; d2.Wx = W2; d2.C = Cop;
+  ConvOut d2o;
+  d2o.y = w.da2; d2o.y_f32 = 1; d2o.yC = Cop; d2o.n_real = cout;
+  conv_fwd(ex.st, f32, d2, H2, W2, 3, w.wd2, Cop, d2o);
+  // cBN2 backward (through the ReLU) -> dh1
+  bn_bwd(ex.st, f32, w.da2, false, h1, B, H2, W2, cout, Cop, mean2, rstd2, gain2, bias2, Cop, nullptr, w.dh1,
+         w.dg2, w.db2, Cop, w.bnb);
+  // conv1: dW1, db1
+  GradIn gdh;
+  gdh.g = w.dh1; gdh.Hs = H2; gdh.Ws = W2; gdh.C = Cop;
+  ConvIn a1;
+  a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.gather = G_UP2;
+  a1.mean = mean1; a1.scale = scale1; a1.shift = bias1; a1.tab_stride = Cip; a1.relu = 1;
+  conv_wgrad(ex.st, f32, gdh, a1, H2, W2, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+  colsum(ex.st, f32, w.dh1, M2, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
+  // da1 (at 2x resolution; the BN backward sums 2x2)
+  ConvIn d1;
+  d1.x = w.dh1; d1.B = B; d1.Hx = H2; d1.Wx = W2; d1.C = Cop;
+  ConvOut d1o;
+  d1o.y = w.da1; d1o.y_f32 = 1; d1o.yC = Cip; d1o.n_real = cin;
+  conv_fwd(ex.st, f32, d1, H2, W2, 3, w.wd1, Cip, d1o);
+  bn_bwd(ex.st, f32, w.da1, true, x, B, H, W, cin, Cip, mean1, rstd1, gain1, bias1, Cip, w.dxs, dx, w.dg1,
+         w.db1, Cip, w.bnb);
+  // conditional-BN linear maps (+ their SN) and dcond
+  struct Lin { const char* name; float* dgb; int C; int slot; };
+  const Lin lins[4] = {{"bn1.gain", w.dg1, cin, 0}, {"bn1.bias", w.db1, cin, 1},
+                       {"bn2.gain", w.dg2, cout, 3}, {"bn2.bias", w.db2, cout, 4}};
+  const int Cps[4] = {Cip, Cip, Cop, Cop};
+  for (int i = 0; i < 4; ++i) {
+    const Lin& l = lins[i];
+    cbn_linear_bwd(ex.st, l.dgb, B, l.C, Cps[i], cond, dc, P.w(l.name), sn[l.slot].sigma, w.dlin, dcond,
+                   dcond_acc || i > 0);
+    sn_bwd(ex.st, w.dlin, P.w(l.name), sn[l.slot].u, sn[l.slot].v, sn[l.slot].sigma, l.C, dc, 1, dc, 1.f,
+           P.gr(l.name), w.part);
+  }
+  sn_bwd(ex.st, w.dwp1, P.w("conv1.w"), sn[2].u, sn[2].v, sn[2].sigma, cout, cin, 3, Cip, 1.f,
+         P.gr("conv1.w"), w.part);
+  sn_bwd(ex.st, w.dwp2, P.w("conv2.w"), sn[5].u, sn[5].v, sn[5].sigma, cout, cout, 3, Cop, 1.f,
+         P.gr("conv2.w"), w.part);
+  sn_bwd(ex.st, w.dwpsc, P.w("sc.w"), sn[6].u, sn[6].v, sn[6].sigma, cout, cin, 1, Cip, 1.f,
+         P.gr("sc.w"), w.part);
+}
+
+// ======================================================================
+// discriminator block
+// ======================================================================
+void DBlock::plan_saved(Arena& a) {
+  Cip = (int)cpad(cin);
+  Cop = (int)cpad(cout);
+  Ho = down ? H / 2 : H;
+  Wo = down ? W / 2 : W;
+  plan_sn(a, sn[0], cout, 9LL * cin);
+  plan_sn(a, sn[1], cout, 9LL * cout);
+  if (lsc) plan_sn(a, sn[2], cout, cin);
+  const size_t e = esz(f32);
+  wp1 = a.bytes((size_t)Cop * 9 * Cip * e);
+  wp2 = a.bytes((size_t)Cop * 9 * Cop * e);
+  if (lsc) wpsc = a.bytes((size_t)Cop * Cip * e);
+  h = a.bytes((size_t)B * H * W * Cop * e);
+}
+
+struct DWsF {
+  void* sn;
+  float* skip;
+};
+struct DWsB {
+  void *wd1, *wd2, *wdsc;
+  float *dwp1, *dwp2, *dwpsc;
+  void* wg;
+  size_t wg_bytes;
+  void* cs;
+  void* dh;
+  float* dxs;
+  float* part;
+};
+
+static DWsF d_carve_f(const DBlock& d, Arena& a) {
+  DWsF w;
+  size_t s = std::max(sn_ws_bytes(d.cout, 9LL * d.cin), sn_ws_bytes(d.cout, 9LL * d.cout));
+  if (d.lsc) s = std::max(s, sn_ws_bytes(d.cout, d.cin));
+  w.sn = a.bytes(s);
+  w.skip = d.lsc ? a.f32((size_t)d.B * d.Ho * d.Wo * d.Cop) : nullptr;
+  return w;
+}
+
+static DWsB d_carve_b(const DBlock& d, Arena& a, int n_cu) {
+  DWsB w;
+  const int64_t M = (int64_t)d.B * d.H * d.W, Mo = (int64_t)d.B * d.Ho * d.Wo;
+  const size_t e = esz(d.f32);
+  w.wd1 = a.bytes((size_t)d.Cip * 9 * d.Cop * e);
+  w.wd2 = a.bytes((size_t)d.Cop * 9 * d.Cop * e);
+  w.wdsc = d.lsc ? a.bytes((size_t)d.Cip * d.Cop * e) : nullptr;
+  w.dwp1 = a.f32((size_t)d.Cop * 9 * d.Cip);
+  w.dwp2 = a.f32((size_t)d.Cop * 9 * d.Cop);
+  w.dwpsc = d.lsc ? a.f32((size_t)d.Cop * d.Cip) : nullptr;
+  w.wg_bytes = std::max(conv_wgrad_ws(d.f32, M, 3, d.Cip, d.Cop, n_cu), conv_wgrad_ws(d.f32, M, 3, d.Cop, d.Cop, n_cu));
+  if (d.lsc) w.wg_bytes = std::max(w.wg_bytes, conv_wgrad_ws(d.f32, Mo, 1, d.Cip, d.Cop, n_cu));
+  w.wg = a.bytes(w.wg_bytes);
+  w.cs = a.bytes(colsum_ws_bytes(M, d.Cop));
+  w.dh = a.bytes((size_t)M * d.Cop * e);
+  w.dxs = d.lsc ? a.f32((size_t)Mo * d.Cip) : nullptr;
+  w.part = a.f32(256);
+  return w;
+}
+
+size_t DBlock::ws_size(int n_cu) const {
+  Arena a(nullptr), b(nullptr);
+  d_carve_f(*this, a);
+  d_carve_b(*this, b, n_cu);
+  return std::max(a.off, b.off);
+}
+
+void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
+  Arena a(ex.ws);
+  DWsF w = d_carve_f(*this, a);
+  Exec exs = ex;
+  exs.ws = w.sn;
+  sn_forward(exs, P, "conv1.w", sn[0], npi, sn_eps);
+  sn_forward(exs, P, "conv2.w", sn[1], npi, sn_eps);
+  if (lsc) sn_forward(exs, P, "sc.w", sn[2], npi, sn_eps);
+  pack_weight(ex.st, f32, P.w("conv1.w"), sn[0].sigma, cout, cin, 3, Cop, Cip, false, wp1);
+  pack_weight(ex.st, f32, P.w("conv2.w"), sn[1].sigma, cout, cout, 3, Cop, Cop, false, wp2);
+  if (lsc) pack_weight(ex.st, f32, P.w("sc.w"), sn[2].sigma, cout, cin, 1, Cop, Cip, false, wpsc);
+  // h = conv3x3([relu](x)) + b1
+  ConvIn i1;
+  i1.x = x; i1.B = B; i1.Hx = H; i1.Wx = W; i1.C = Cip; i1.relu = preact;
+  ConvOut o1;
+  o1.y = h; o1.y_f32 = f32; o1.yC = Cop; o1.n_real = cout; o1.bias = P.w("conv1.b");
+  conv_fwd(ex.st, f32, i1, H, W, 3, wp1, Cop, o1);
+  // skip = conv1x1([avgpool](x)) + bsc, fp32
+  if (lsc) {
+    ConvIn si;
+    si.x = x; si.B = B; si.Hx = H; si.Wx = W; si.C = Cip;
+    if (down) { si.gather = G_POOL2; si.gscale = 0.25f; }
+    ConvOut so;
+    so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b");
+    conv_fwd(ex.st, f32, si, Ho, Wo, 1, wpsc, Cop, so);
+  }
+  // y = [avgpool](conv3x3(relu(h)) + b2) + skip
+  ConvIn i2;
+  i2.x = h; i2.B = B; i2.Hx = H; i2.Wx = W; i2.C = Cop; i2.relu = 1;
+  ConvOut o2;
+  o2.y = y; o2.y_f32 = f32; o2.yC = Cop; o2.n_real = cout; o2.bias = P.w("conv2.b"); o2.pool = down;
+  o2.res_mode = R_SAME; o2.resC = Cop;
+  if (lsc) { o2.res = w.skip; o2.res_f32 = 1; }
+  else { o2.res = x; o2.res_f32 = f32; }
+  conv_fwd(ex.st, f32, i2, H, W, 3, wp2, Cop, o2);
+}
+
+void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool dx_f32) {
+  Arena a(ex.ws);
+  DWsB w = d_carve_b(*this, a, ex.n_cu);
+  const int64_t M = (int64_t)B * H * W, Mo = (int64_t)B * Ho * Wo;
+  pack_weight(ex.st, f32, P.w("conv1.w"), sn[0].sigma, cout, cin, 3, Cop, Cip, true, w.wd1);
+  pack_weight(ex.st, f32, P.w("conv2.w"), sn[1].sigma, cout, cout, 3, Cop, Cop, true, w.wd2);
+  if (lsc) pack_weight(ex.st, f32, P.w("sc.w"), sn[2].sigma, cout, cin, 1, Cop, Cip, true, w.wdsc);
+  // conv2 (its output gradient is dy, or dy/4 spread over 2x2 when pooled)
+  GradIn g2;
+  g2.g = dy; g2.Hs = Ho; g2.Ws = Wo; g2.C = Cop;
+  if (down) { g2.gather = G_UP2; g2.gscale = 0.25f; }
+  ConvIn a2;
+  a2.x = h; a2.B = B; a2.Hx = H; a2.Wx = W; a2.C = Cop; a2.relu = 1;
+  conv_wgrad(ex.st, f32, g2, a2, H, W, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
+  colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
+  // dh = (conv2^T dc2) * [h > 0]
+  ConvIn d2;
+  d2.x = dy; d2.B = B; d2.Hx = Ho; d2.Wx = Wo; d2.C = Cop;
+  if (down) { d2.gather = G_UP2; d2.gscale = 0.25f; }
+  ConvOut d2o;
+  d2o.y = w.dh; d2o.y_f32 = f32; d2o.yC = Cop; d2o.n_real = cout;
+  d2o.mask = h; d2o.mask_f32 = f32; d2o.maskC = Cop;
+  conv_fwd(ex.st, f32, d2, H, W, 3, w.wd2, Cop, d2o);
+  // conv1
+  GradIn g1;
+  g1.g = w.dh; g1.Hs = H; g1.Ws = W; g1.C = Cop;
+  ConvIn a1;
+  a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.relu = preact;
+  conv_wgrad(ex.st, f32, g1, a1, H, W, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+  colsum(ex.st, f32, w.dh, M, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
+  // skip
+  if (lsc) {
+    GradIn gs;
+    gs.g = dy; gs.Hs = Ho; gs.Ws = Wo; gs.C = Cop;
+    ConvIn as;
+    as.x = x; as.B = B; as.Hx = H; as.Wx = W; as.C = Cip;
+    if (down) { as.gather = G_POOL2; as.gscale = 0.25f; }
+    conv_wgrad(ex.st, f32, gs, as, Ho, Wo, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
+    colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("sc.b"), w.cs);
+    if (dx) {
+      ConvIn ds;
+      ds.x = dy; ds.B = B; ds.Hx = Ho; ds.Wx = Wo; ds.C = Cop;
+      ConvOut dso;
+      dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = cin;
+      conv_fwd(ex.st, f32, ds, Ho, Wo, 1, w.wdsc, Cip, dso);
+    }
+  }
+  if (dx) {
+    ConvIn d1;
+    d1.x = w.dh; d1.B = B; d1.Hx = H; d1.Wx = W; d1.C = Cop;
+    ConvOut d1o;
+    d1o.y = dx; d1o.y_f32 = dx_f32 || f32; d1o.yC = Cip; d1o.n_real = cin;
+    if (preact) { d1o.mask = x; d1o.mask_f32 = f32; d1o.maskC = Cip; }
+    if (lsc) {
+      d1o.res = w.dxs; d1o.res_f32 = 1; d1o.resC = Cip;
+      d1o.res_mode = down ? R_HALF : R_SAME;
+      d1o.res_scale = down ? 0.25f : 1.f;
+    } else {
+      d1o.res = dy; d1o.res_f32 = f32; d1o.resC = Cop; d1o.res_mode = R_SAME;
+    }
+    conv_fwd(ex.st, f32, d1, H, W, 3, w.wd1, Cip, d1o);
+  }
+  sn_bwd(ex.st, w.dwp1, P.w("conv1.w"), sn[0].u, sn[0].v, sn[0].sigma, cout, cin, 3, Cip, 1.f,
+         P.gr("conv1.w"), w.part);
+  sn_bwd(ex.st, w.dwp2, P.w("conv2.w"), sn[1].u, sn[1].v, sn[1].sigma, cout, cout, 3, Cop, 1.f,
+         P.gr("conv2.w"), w.part);
+  if (lsc)
+    sn_bwd(ex.st, w.dwpsc, P.w("sc.w"), sn[2].u, sn[2].v, sn[2].sigma, cout, cin, 1, Cip, 1.f,
+           P.gr("sc.w"), w.part);
+}
+
+}  // namespace pg

@@ -1,0 +1,141 @@
+// Host runtime: parameter layouts, buffer planning, and the residual-block
+// executors used by both the per-block C-ABI calls and the train step.
+#pragma once
+#include <string>
+#include <vector>
+
+#include "misc.hpp"
+
+namespace pg {
+
+// Sequential carving of a caller-owned buffer; with a null base it only
+// measures (the *_sizes() queries run the same plan with base == nullptr).
+struct Arena {
+  char* base;
+  size_t off = 0;
+  explicit Arena(void* b) : base((char*)b) {}
+  void* bytes(size_t n) {
+    const size_t o = off;
+    off = align256(off + n);
+    return base ? (void*)(base + o) : nullptr;
+  }
+  float* f32(size_t n) { return (float*)bytes(n * 4); }
+};
+
+struct Entry {
+  std::string name;
+  std::vector<int64_t> shape;
+  bool sn;
+  int64_t offset = 0, u_offset = -1;
+  int64_t numel() const {
+    int64_t n = 1;
+    for (auto s : shape) n *= s;
+    return n;
+  }
+};
+
+struct Layout {
+  std::vector<Entry> e;
+  int64_t n_params = 0, n_u = 0;
+  void add(const std::string& name, std::vector<int64_t> shape, bool sn) {
+    Entry x{name, shape, sn};
+    x.offset = n_params;
+    n_params += x.numel();
+    if (sn) {
+      x.u_offset = n_u;
+      n_u += shape[0];
+    }
+    e.push_back(x);
+  }
+  const Entry& get(const std::string& name) const;
+  void add_prefixed(const std::string& prefix, const Layout& sub);
+};
+
+Layout gblock_layout(int cin, int cout, int dc);
+Layout dblock_layout(int cin, int cout, bool lsc);
+Layout attn_layout(int c);
+
+// Parameters of one module resolved against flat buffers.
+struct Params {
+  const Layout* L;
+  std::string prefix;
+  const float* p;     // flat params
+  float* u;           // flat u
+  float* g;           // flat grads (may be null)
+  const float* w(const std::string& n) const { return p + L->get(prefix + n).offset; }
+  float* uu(const std::string& n) const { return u + L->get(prefix + n).u_offset; }
+  float* gr(const std::string& n) const { return g + L->get(prefix + n).offset; }
+  const Entry& ent(const std::string& n) const { return L->get(prefix + n); }
+};
+
+// One spectrally normalised weight: u, v and sigma of the last forward.
+struct SNSlot {
+  float* u = nullptr;
+  float* v = nullptr;
+  float* sigma = nullptr;
+};
+
+struct Exec {
+  hipStream_t st;
+  int n_cu;
+  void* ws;           // scratch shared by the steps of one block call
+  size_t ws_bytes;
+};
+
+// ----------------------------------------------------------- G block
+struct GBlock {
+  int B, H, W, cin, cout, dc, npi;
+  bool f32;
+  float bn_eps, sn_eps;
+  int Cip, Cop;
+  // saved by fwd for bwd
+  SNSlot sn[7];
+  void *wp1 = nullptr, *wp2 = nullptr, *wpsc = nullptr;
+  float *mean1, *rstd1, *gain1, *bias1, *scale1;
+  float *mean2, *rstd2, *gain2, *bias2, *scale2;
+  void* h1 = nullptr;
+  void plan_saved(Arena& a);
+  size_t ws_size(int n_cu) const;
+  void fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y);
+  // dcond_accumulate: add to dcond instead of overwriting it
+  void bwd(const Exec& ex, const Params& P, const void* x, const float* cond, const void* dy, void* dx,
+           float* dcond, bool dcond_accumulate);
+};
+
+// ----------------------------------------------------------- D block
+struct DBlock {
+  int B, H, W, cin, cout, npi;
+  bool preact, down, lsc, f32;
+  float sn_eps;
+  int Cip, Cop, Ho, Wo;
+  SNSlot sn[3];
+  void *wp1 = nullptr, *wp2 = nullptr, *wpsc = nullptr;
+  void* h = nullptr;
+  void plan_saved(Arena& a);
+  size_t ws_size(int n_cu) const;
+  void fwd(const Exec& ex, const Params& P, const void* x, void* y);
+  // dx may be null; dx_f32 writes an unrounded fp32 input gradient.
+  void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool dx_f32);
+};
+
+// ----------------------------------------------------------- attention
+struct Attn {
+  int B, H, W, C, npi;
+  float sn_eps;
+  int Cp, dk, dv, Nqkv;      // padded head dims; Nqkv = 2*dk + dv
+  SNSlot sn[4];
+  void *wqkv = nullptr, *wo = nullptr;   // packed fwd weights
+  void *qkv = nullptr;       // [B][H][W][Nqkv] bf16 projections (pre-pool)
+  void *kp = nullptr, *vp = nullptr, *vt = nullptr;   // pooled keys/values
+  void *o = nullptr;         // attention output [B][HW][dv] bf16
+  float* lse = nullptr;      // [B][HW]
+  void plan_saved(Arena& a);
+  size_t ws_size(int n_cu) const;
+  void fwd(const Exec& ex, const Params& P, const void* x, void* y);
+  void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx);
+};
+
+// SN of one weight into a slot (power iteration updates u in place).
+void sn_forward(const Exec& ex, const Params& P, const std::string& name, SNSlot& s, int npi, float eps);
+
+}  // namespace pg

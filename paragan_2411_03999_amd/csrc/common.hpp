@@ -1,0 +1,107 @@
+// Shared device/host helpers for libparagan (gfx950 only).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#define PG_DEV __device__ __forceinline__
+
+namespace pg {
+
+typedef uint16_t bf16_t;                                     // storage type
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));   // MFMA operand
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kCPad = 32;   // channel padding: the K depth of one bf16 MFMA step pair
+
+__host__ __device__ inline int64_t cpad(int64_t c) { return (c + kCPad - 1) / kCPad * kCPad; }
+__host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
+PG_DEV bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+PG_DEV float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// 8 packed bf16 in a uint4 <-> 8 floats
+PG_DEV void unpack8(const uint4& q, float* f) {
+  const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+PG_DEV uint4 pack8(const float* f) {
+  uint4 q;
+  q.x = (uint32_t)f2bf(f[0]) | ((uint32_t)f2bf(f[1]) << 16);
+  q.y = (uint32_t)f2bf(f[2]) | ((uint32_t)f2bf(f[3]) << 16);
+  q.z = (uint32_t)f2bf(f[4]) | ((uint32_t)f2bf(f[5]) << 16);
+  q.w = (uint32_t)f2bf(f[6]) | ((uint32_t)f2bf(f[7]) << 16);
+  return q;
+}
+
+// element load/store for the two activation types
+template <typename T> PG_DEV float ld(const T* p, int64_t i);
+template <> PG_DEV float ld<float>(const float* p, int64_t i) { return p[i]; }
+template <> PG_DEV float ld<bf16_t>(const bf16_t* p, int64_t i) { return bf2f(p[i]); }
+template <typename T> PG_DEV void st(T* p, int64_t i, float v);
+template <> PG_DEV void st<float>(float* p, int64_t i, float v) { p[i] = v; }
+template <> PG_DEV void st<bf16_t>(bf16_t* p, int64_t i, float v) { p[i] = f2bf(v); }
+// rounding to the storage precision of T (identity for fp32)
+template <typename T> PG_DEV float rnd(float v);
+template <> PG_DEV float rnd<float>(float v) { return v; }
+template <> PG_DEV float rnd<bf16_t>(float v) { return bf2f(f2bf(v)); }
+
+// wavefront reduction (64 lanes), result valid in every lane
+PG_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+PG_DEV double wave_sum_d(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace pg
+
+// ---------------------------------------------------------------- host side
+struct paragan_ctx {
+  hipStream_t stream = nullptr;
+  int device = 0;
+  int n_cu = 0;
+  std::string err;
+};
+
+namespace pg {
+
+struct Error {
+  int code;
+  std::string msg;
+};
+
+#define PG_HIP(call)                                                        \
+  do {                                                                      \
+    hipError_t e_ = (call);                                                 \
+    if (e_ != hipSuccess)                                                   \
+      throw ::pg::Error{-4, std::string(#call) + ": " + hipGetErrorString(e_)}; \
+  } while (0)
+
+#define PG_CHECK(cond, msg)                                                 \
+  do {                                                                      \
+    if (!(cond)) throw ::pg::Error{-1, std::string(msg)};                   \
+  } while (0)
+
+#define PG_LAUNCH_CHECK() PG_HIP(hipGetLastError())
+
+}  // namespace pg

@@ -1,0 +1,40 @@
+// Launchers of the bandwidth-bound kernels (misc.hip, heads.hip, attention.hip).
+#pragma once
+#include "ops.hpp"
+
+namespace pg {
+
+// spectral normalisation
+size_t sn_ws_bytes(int64_t rows, int64_t cols);
+// u_save (optional) receives a copy of the final u (kept for the backward).
+void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, float* u, float* v,
+                   float* sigma, int n_iter, float eps, void* ws, float* u_save = nullptr);
+void pack_weight(hipStream_t st, bool f32, const float* W, const float* sigma, int Cout, int Cin,
+                 int R, int Np, int Cp, bool dgrad, void* dst);
+// dW = (s*dWsn - <s*dWsn, W/sigma> u v^T) / sigma with s = extra_scale.
+void sn_bwd(hipStream_t st, const float* dwp, const float* W, const float* u, const float* v,
+            const float* sigma, int Cout, int Cin, int R, int Cp, float extra_scale, float* dW,
+            float* part);
+
+// out[c] = scale * sum_m x[m][c]
+size_t colsum_ws_bytes(int64_t M, int C);
+void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float scale, float* out,
+            void* ws);
+
+// batch norm
+size_t bn_stats_ws_bytes(int64_t M, int C);
+void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float eps, float* mean,
+              float* rstd, void* ws);
+void cbn_tables(hipStream_t st, const float* cond, int dc, const float* Wg, const float* Wb,
+                const float* sg, const float* sb, const float* gain_p, const float* bias_p,
+                const float* rstd, int B, int C, int Cp, float* gain, float* bias, float* scale);
+size_t bn_bwd_ws_bytes(int B, int HW, int C);
+void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x, int B, int H, int W,
+            int C, int Cp, const float* mean, const float* rstd, const float* gain, const float* bias,
+            int tab_stride, const float* res, void* dx, float* dgain, float* dbias, int dg_stride,
+            void* ws);
+void cbn_linear_bwd(hipStream_t st, const float* dgb, int B, int C, int Cp, const float* cond, int dc,
+                    const float* W, const float* sigma, float* dW, float* dcond, bool accumulate);
+void fill(hipStream_t st, float* p, int64_t n, float v);
+
+}  // namespace pg

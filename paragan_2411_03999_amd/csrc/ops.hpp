@@ -1,0 +1,66 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher enqueues on the
+// given stream and returns immediately; shapes are validated by the callers
+// (the C-ABI layer) before anything is launched.
+#pragma once
+#include "common.hpp"
+
+namespace pg {
+
+enum Gather { G_DIRECT = 0, G_UP2 = 1, G_POOL2 = 2 };
+enum ResMode { R_NONE = 0, R_SAME = 1, R_HALF = 2 };
+
+// The A operand of an implicit-GEMM convolution: an NHWC activation read
+// through a gather (direct, nearest 2x upsample, or 2x2 sum-pool), scaled,
+// optionally batch-normalised with per-(sample, channel) affine tables and
+// ReLU'd -- all applied while staging the operand, before the MMA.
+struct ConvIn {
+  const void* x = nullptr;
+  int B = 0, Hx = 0, Wx = 0, C = 0;   // source dims; C = channel stride (x32)
+  int gather = G_DIRECT;
+  float gscale = 1.f;
+  const float* mean = nullptr;        // [C]      (affine prologue)
+  const float* scale = nullptr;       // [B][C] or [C]
+  const float* shift = nullptr;
+  int tab_stride = 0;                 // C for per-sample tables, 0 for per-channel
+  int relu = 0;
+};
+
+// Epilogue: v = (acc * (*acc_scale) + bias[n]) * (mask > 0) + res_scale * res,
+// optionally 2x2 average-pooled (the output rows are then the pooled pixels).
+struct ConvOut {
+  void* y = nullptr;
+  int y_f32 = 0;
+  int yC = 0;                  // channel stride of y
+  int n_real = 0;              // channels >= n_real are written as 0
+  const float* bias = nullptr;
+  const float* acc_scale = nullptr;   // device scalar
+  int pool = 0;
+  const void* res = nullptr;
+  int res_f32 = 0, res_mode = R_NONE, resC = 0;
+  float res_scale = 1.f;
+  const void* mask = nullptr;         // same position as the output
+  int mask_f32 = 0, maskC = 0;
+};
+
+// y = conv_RxR(gathered/transformed x, w) on an H x W grid (stride 1, pad R/2).
+// w: packed [Np][R][R][in.C] in the activation type (bf16 or fp32).
+void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
+              const void* w, int Np, const ConvOut& out);
+
+// Gradient operand of a weight gradient: dy at the conv-output grid (H x W)
+// read directly or as a nearest-2x upsample of a half-resolution tensor.
+struct GradIn {
+  const void* g = nullptr;
+  int Hs = 0, Ws = 0, C = 0;   // source dims; C = channel stride (= Np)
+  int gather = G_DIRECT;       // G_DIRECT or G_UP2
+  float gscale = 1.f;          // applied to the result
+};
+
+// dw[n][r][s][c] = gscale * sum_m g[m][n] * A[m][(r,s,c)], A = im2col(in).
+// dw: fp32 [Np][R][R][in.C] (padded).  ws: scratch for split-M partials.
+size_t conv_wgrad_ws(bool f32, int64_t M, int R, int Cin, int Np, int n_cu);
+void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in,
+                int H, int W, int R, int Np, float* dw, void* ws, size_t ws_bytes,
+                int n_cu);
+
+}  // namespace pg

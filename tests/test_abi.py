@@ -1,0 +1,84 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+include/paragan.h declares, validates arguments on the host, and describes
+parameter layouts that match the oracle's (names, shapes, order)."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from oracle import biggan as O
+from oracle import blocks as OB
+from paragan_2411_03999_amd import lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(lib.LIB_PATH):
+        from paragan_2411_03999_amd.build import build
+        build()
+    return lib.load()
+
+
+def header_functions():
+    src = open(os.path.join(ROOT, "include", "paragan.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(paragan_\w+)\s*\(", src)))
+
+
+def test_exports_every_declared_function(L):
+    names = header_functions()
+    assert len(names) >= 25
+    for n in names:
+        assert hasattr(L, n), n
+        assert n in lib.exported_symbols(), n
+
+
+def test_cpad():
+    assert [lib.cpad(c) for c in (1, 3, 32, 33, 96, 148)] == [32, 32, 32, 64, 96, 160]
+
+
+def test_gblock_validation(L):
+    good = lib.GBlockDesc(4, 8, 8, 64, 64, 128, lib.F32, 1, 1e-5, 1e-12)
+    assert lib.paragan_gblock_check(good) == lib.OK
+    for field, bad in [("B", 0), ("cin", 0), ("dtype", 7), ("n_power_iter", 0), ("bn_eps", 0.0)]:
+        d = lib.GBlockDesc(4, 8, 8, 64, 64, 128, lib.F32, 1, 1e-5, 1e-12)
+        setattr(d, field, bad)
+        assert lib.paragan_gblock_check(d) == lib.EINVAL, field
+        assert L.paragan_last_error(None).decode()
+    assert L.paragan_gblock_check(None) == lib.EINVAL
+
+
+def test_dblock_validation(L):
+    ok = lib.DBlockDesc(2, 8, 8, 16, 32, 1, 1, 1, lib.BF16, 1, 1e-12)
+    assert lib.paragan_dblock_check(ok) == lib.OK
+    odd = lib.DBlockDesc(2, 7, 8, 16, 32, 1, 1, 1, lib.BF16, 1, 1e-12)
+    assert lib.paragan_dblock_check(odd) == lib.EINVAL           # pooling needs even H
+    ident = lib.DBlockDesc(2, 8, 8, 16, 32, 1, 0, 0, lib.BF16, 1, 1e-12)
+    assert lib.paragan_dblock_check(ident) == lib.EINVAL         # identity skip, cin != cout
+
+
+def test_entry_points_reject_null_context(L):
+    d = lib.DBlockDesc(2, 8, 8, 16, 32, 1, 1, 1, lib.BF16, 1, 1e-12)
+    assert L.paragan_dblock_fwd(None, C.byref(d), None, None, None, None, None, None) == lib.EINVAL
+    assert L.paragan_sn_power_iter(None, None, 1, 1, None, None, None, 1, 1e-12, None) == lib.EINVAL
+
+
+def test_layouts_match_oracle(L):
+    ents, npar, nu = lib.paragan_gblock_layout(lib.GBlockDesc(4, 8, 8, 64, 48, 148, lib.BF16, 1, 1e-5, 1e-12))
+    ref = OB.gblock_param_shapes(64, 48, 148)
+    assert [(e["name"], e["shape"]) for e in ents] == list(ref.items())
+    assert npar == sum(int(__import__("numpy").prod(s)) for s in ref.values())
+    sn = [e["name"] for e in ents if e["u_offset"] >= 0]
+    assert sn == list(OB.GBLOCK_SN)
+    for lsc in (0, 1):
+        ents, _, _ = lib.paragan_dblock_layout(lib.DBlockDesc(2, 8, 8, 32, 32, 1, lsc, lsc, lib.BF16, 1, 1e-12))
+        assert [(e["name"], e["shape"]) for e in ents] == list(OB.dblock_param_shapes(32, 32, lsc).items())
+
+
+def test_sizes_queries_need_no_gpu(L):
+    s, w = lib.paragan_dblock_sizes(lib.DBlockDesc(64, 32, 32, 256, 512, 1, 1, 1, lib.BF16, 1, 1e-12))
+    assert s > 0 and w > 0 and s % 256 == 0
+    assert lib.paragan_sn_ws_size(512, 2304) > 0
