@@ -5,6 +5,8 @@
 
 #include "../../include/paragan.h"
 #include "blocks.hpp"
+#include "net.hpp"
+#include <cmath>
 
 using namespace pg;
 
@@ -296,23 +298,139 @@ extern "C" int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t r
   })
 }
 
-// ------------------------------------------------------------ not yet built
-#define PG_UNSUPPORTED(ctx) \
-  return fail(ctx, PARAGAN_EUNSUPPORTED, "not implemented in this build")
+// ------------------------------------------------------------ attention
+static void acheck(const paragan_attn_desc* d) {
+  if (!d) throw Error{PARAGAN_EINVAL, "attn: desc is NULL"};
+  PG_CHECK(d->B >= 1 && d->H >= 2 && d->W >= 2 && d->H % 2 == 0 && d->W % 2 == 0,
+           "attn: B >= 1 and H, W even and >= 2");
+  PG_CHECK(d->C >= 8 && d->C % 8 == 0, "attn: C must be a multiple of 8");
+  PG_CHECK(d->C / 8 <= 32, "attn: C/8 query width above 32 is not supported");
+  const int64_t dv = cpad(d->C / 2);
+  PG_CHECK(dv == 32 || dv == 64 || dv == 96 || dv == 128, "attn: C/2 value width must pad to 32, 64, 96 or 128");
+  PG_CHECK(d->n_power_iter >= 1 && d->sn_eps > 0.f, "attn: bad n_power_iter / sn_eps");
+  PG_CHECK((int64_t)d->B * d->H * d->W < (1LL << 31), "attn: too many pixels");
+}
 
-extern "C" int paragan_attn_layout(const paragan_attn_desc*, paragan_tensor_info*, int32_t, int32_t*, int64_t*,
-                                   int64_t*) { PG_UNSUPPORTED(nullptr); }
-extern "C" int paragan_attn_sizes(const paragan_attn_desc*, size_t*, size_t*) { PG_UNSUPPORTED(nullptr); }
-extern "C" int paragan_attn_check(const paragan_attn_desc*) { PG_UNSUPPORTED(nullptr); }
-extern "C" int paragan_attn_fwd(paragan_ctx* ctx, const paragan_attn_desc*, const float*, float*, const void*,
-                                void*, void*, void*) { PG_UNSUPPORTED(ctx); }
-extern "C" int paragan_attn_bwd(paragan_ctx* ctx, const paragan_attn_desc*, const float*, const void*,
-                                const void*, const void*, void*, float*, void*) { PG_UNSUPPORTED(ctx); }
-extern "C" int paragan_net_layout(const paragan_biggan_desc*, int32_t, paragan_tensor_info*, int32_t, int32_t*,
-                                  int64_t*, int64_t*) { PG_UNSUPPORTED(nullptr); }
-extern "C" int paragan_biggan_check(const paragan_biggan_desc*) { PG_UNSUPPORTED(nullptr); }
-extern "C" int paragan_train_step_ws_size(const paragan_biggan_desc*, size_t*) { PG_UNSUPPORTED(nullptr); }
-extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc*, paragan_net_state*,
-                                  paragan_net_state*, const paragan_step_inputs*, int32_t, void*, float*) {
-  PG_UNSUPPORTED(ctx);
+static Attn make_a(const paragan_attn_desc* d) {
+  Attn t;
+  t.B = d->B; t.H = d->H; t.W = d->W; t.C = d->C; t.npi = d->n_power_iter; t.sn_eps = d->sn_eps;
+  Arena a(nullptr);
+  t.plan_saved(a);
+  return t;
+}
+
+extern "C" int paragan_attn_check(const paragan_attn_desc* d) { PG_TRY(nullptr, acheck(d)) }
+
+extern "C" int paragan_attn_layout(const paragan_attn_desc* d, paragan_tensor_info* out, int32_t cap,
+                                   int32_t* count, int64_t* n_params, int64_t* n_u) {
+  try {
+    acheck(d);
+    return export_layout(attn_layout(d->C), out, cap, count, n_params, n_u);
+  } catch (const Error& e) {
+    return fail(nullptr, e.code, e.msg);
+  }
+}
+
+extern "C" int paragan_attn_sizes(const paragan_attn_desc* d, size_t* saved, size_t* ws) {
+  PG_TRY(nullptr, {
+    acheck(d);
+    Attn t = make_a(d);
+    Arena a(nullptr);
+    t.plan_saved(a);
+    if (saved) *saved = a.off;
+    if (ws) *ws = t.ws_size(device_cus());
+  })
+}
+
+extern "C" int paragan_attn_fwd(paragan_ctx* ctx, const paragan_attn_desc* d, const float* params, float* u,
+                                const void* x, void* y, void* saved, void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    acheck(d);
+    need(params, "params"); need(u, "u"); need(x, "x"); need(y, "y"); need(saved, "saved"); need(ws, "ws");
+    aligned(saved, "saved"); aligned(ws, "ws");
+    Attn t = make_a(d);
+    Arena a(saved);
+    t.plan_saved(a);
+    Layout L = attn_layout(d->C);
+    Params P{&L, "", params, u, nullptr};
+    Exec ex{ctx->stream, ctx->n_cu, ws, t.ws_size(ctx->n_cu)};
+    t.fwd(ex, P, x, y);
+  })
+}
+
+extern "C" int paragan_attn_bwd(paragan_ctx* ctx, const paragan_attn_desc* d, const float* params, const void* x,
+                                const void* saved, const void* dy, void* dx, float* grads, void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    acheck(d);
+    need(params, "params"); need(x, "x"); need(saved, "saved"); need(dy, "dy"); need(dx, "dx");
+    need(grads, "grads"); need(ws, "ws");
+    aligned(saved, "saved"); aligned(ws, "ws");
+    Attn t = make_a(d);
+    Arena a((void*)saved);
+    t.plan_saved(a);
+    Layout L = attn_layout(d->C);
+    Params P{&L, "", params, nullptr, grads};
+    Exec ex{ctx->stream, ctx->n_cu, ws, t.ws_size(ctx->n_cu)};
+    t.bwd(ex, P, x, dy, dx, true);
+  })
+}
+
+// ------------------------------------------------------------ networks, step
+extern "C" int paragan_biggan_check(const paragan_biggan_desc* d) { PG_TRY(nullptr, check_arch(d)) }
+
+extern "C" int paragan_net_layout(const paragan_biggan_desc* d, int32_t which, paragan_tensor_info* out,
+                                  int32_t cap, int32_t* count, int64_t* n_params, int64_t* n_u) {
+  try {
+    check_arch(d);
+    PG_CHECK(which == 0 || which == 1, "net_layout: which must be 0 (G) or 1 (D)");
+    const Arch a = arch_from(d);
+    return export_layout(which == 0 ? g_layout(a) : d_layout(a), out, cap, count, n_params, n_u);
+  } catch (const Error& e) {
+    return fail(nullptr, e.code, e.msg);
+  }
+}
+
+extern "C" int paragan_train_step_ws_size(const paragan_biggan_desc* d, size_t* ws_bytes) {
+  PG_TRY(nullptr, {
+    check_arch(d);
+    need(ws_bytes, "ws_bytes");
+    *ws_bytes = train_step_ws(d, device_cus());
+  })
+}
+
+static void need_state(const paragan_net_state* s, const char* who) {
+  need(s, who);
+  need(s->params, "params"); need(s->u, "u"); need(s->grads, "grads");
+  need(s->adam_m, "adam_m"); need(s->adam_v, "adam_v");
+  PG_CHECK(s->adam_t >= 0, "adam_t must be >= 0");
+}
+
+extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G,
+                                  paragan_net_state* D, const paragan_step_inputs* in, int32_t n_D, void* ws,
+                                  float* losses_host) {
+  if (!ctx) return PARAGAN_EINVAL;
+  try {
+    check_arch(d);
+    need_state(G, "G");
+    need_state(D, "D");
+    need(in, "inputs"); need(ws, "ws"); need(losses_host, "losses_host");
+    aligned(ws, "ws");
+    PG_CHECK(n_D >= 1 && n_D <= 63, "train_step: n_D must be in [1, 63]");
+    need(in->x_real, "x_real"); need(in->y_real, "y_real"); need(in->z_fake, "z_fake"); need(in->y_fake, "y_fake");
+    for (int k = 0; k < n_D; ++k) {
+      need(in->x_real[k], "x_real[k]"); need(in->y_real[k], "y_real[k]");
+      need(in->z_fake[k], "z_fake[k]"); need(in->y_fake[k], "y_fake[k]");
+    }
+    need(in->z_g, "z_g"); need(in->y_g, "y_g");
+    train_step(ctx, d, G, D, in, n_D, ws, losses_host);
+    for (int k = 0; k <= n_D; ++k)
+      if (!std::isfinite(losses_host[k])) return fail(ctx, PARAGAN_ENONFINITE, "train_step: non-finite loss");
+    return PARAGAN_OK;
+  } catch (const Error& e) {
+    return fail(ctx, e.code, e.msg);
+  } catch (const std::exception& e) {
+    return fail(ctx, PARAGAN_EINVAL, e.what());
+  }
 }

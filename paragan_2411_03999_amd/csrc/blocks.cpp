@@ -261,14 +261,14 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
     const Lin& l = lins[i];
     cbn_linear_bwd(ex.st, l.dgb, B, l.C, Cps[i], cond, dc, P.w(l.name), sn[l.slot].sigma, w.dlin, dcond,
                    dcond_acc || i > 0);
-    sn_bwd(ex.st, w.dlin, P.w(l.name), sn[l.slot].u, sn[l.slot].v, sn[l.slot].sigma, l.C, dc, 1, dc, 1.f,
+    sn_bwd(ex.st, w.dlin, P.w(l.name), sn[l.slot].u, sn[l.slot].v, sn[l.slot].sigma, l.C, dc, 1, dc, nullptr,
            P.gr(l.name), w.part);
   }
-  sn_bwd(ex.st, w.dwp1, P.w("conv1.w"), sn[2].u, sn[2].v, sn[2].sigma, cout, cin, 3, Cip, 1.f,
+  sn_bwd(ex.st, w.dwp1, P.w("conv1.w"), sn[2].u, sn[2].v, sn[2].sigma, cout, cin, 3, Cip, nullptr,
          P.gr("conv1.w"), w.part);
-  sn_bwd(ex.st, w.dwp2, P.w("conv2.w"), sn[5].u, sn[5].v, sn[5].sigma, cout, cout, 3, Cop, 1.f,
+  sn_bwd(ex.st, w.dwp2, P.w("conv2.w"), sn[5].u, sn[5].v, sn[5].sigma, cout, cout, 3, Cop, nullptr,
          P.gr("conv2.w"), w.part);
-  sn_bwd(ex.st, w.dwpsc, P.w("sc.w"), sn[6].u, sn[6].v, sn[6].sigma, cout, cin, 1, Cip, 1.f,
+  sn_bwd(ex.st, w.dwpsc, P.w("sc.w"), sn[6].u, sn[6].v, sn[6].sigma, cout, cin, 1, Cip, nullptr,
          P.gr("sc.w"), w.part);
 }
 
@@ -378,7 +378,8 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   conv_fwd(ex.st, f32, i2, H, W, 3, wp2, Cop, o2);
 }
 
-void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool dx_f32) {
+void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool dx_f32,
+                 bool wgrad) {
   Arena a(ex.ws);
   DWsB w = d_carve_b(*this, a, ex.n_cu);
   const int64_t M = (int64_t)B * H * W, Mo = (int64_t)B * Ho * Wo;
@@ -391,8 +392,10 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   if (down) { g2.gather = G_UP2; g2.gscale = 0.25f; }
   ConvIn a2;
   a2.x = h; a2.B = B; a2.Hx = H; a2.Wx = W; a2.C = Cop; a2.relu = 1;
-  conv_wgrad(ex.st, f32, g2, a2, H, W, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
-  colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
+  if (wgrad) {
+    conv_wgrad(ex.st, f32, g2, a2, H, W, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
+    colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
+  }
   // dh = (conv2^T dc2) * [h > 0]
   ConvIn d2;
   d2.x = dy; d2.B = B; d2.Hx = Ho; d2.Wx = Wo; d2.C = Cop;
@@ -406,8 +409,10 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   g1.g = w.dh; g1.Hs = H; g1.Ws = W; g1.C = Cop;
   ConvIn a1;
   a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.relu = preact;
-  conv_wgrad(ex.st, f32, g1, a1, H, W, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
-  colsum(ex.st, f32, w.dh, M, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
+  if (wgrad) {
+    conv_wgrad(ex.st, f32, g1, a1, H, W, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+    colsum(ex.st, f32, w.dh, M, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
+  }
   // skip
   if (lsc) {
     GradIn gs;
@@ -415,8 +420,10 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     ConvIn as;
     as.x = x; as.B = B; as.Hx = H; as.Wx = W; as.C = Cip;
     if (down) { as.gather = G_POOL2; as.gscale = 0.25f; }
-    conv_wgrad(ex.st, f32, gs, as, Ho, Wo, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
-    colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("sc.b"), w.cs);
+    if (wgrad) {
+      conv_wgrad(ex.st, f32, gs, as, Ho, Wo, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
+      colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("sc.b"), w.cs);
+    }
     if (dx) {
       ConvIn ds;
       ds.x = dy; ds.B = B; ds.Hx = Ho; ds.Wx = Wo; ds.C = Cop;
@@ -440,12 +447,13 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     }
     conv_fwd(ex.st, f32, d1, H, W, 3, w.wd1, Cip, d1o);
   }
-  sn_bwd(ex.st, w.dwp1, P.w("conv1.w"), sn[0].u, sn[0].v, sn[0].sigma, cout, cin, 3, Cip, 1.f,
+  if (!wgrad) return;
+  sn_bwd(ex.st, w.dwp1, P.w("conv1.w"), sn[0].u, sn[0].v, sn[0].sigma, cout, cin, 3, Cip, nullptr,
          P.gr("conv1.w"), w.part);
-  sn_bwd(ex.st, w.dwp2, P.w("conv2.w"), sn[1].u, sn[1].v, sn[1].sigma, cout, cout, 3, Cop, 1.f,
+  sn_bwd(ex.st, w.dwp2, P.w("conv2.w"), sn[1].u, sn[1].v, sn[1].sigma, cout, cout, 3, Cop, nullptr,
          P.gr("conv2.w"), w.part);
   if (lsc)
-    sn_bwd(ex.st, w.dwpsc, P.w("sc.w"), sn[2].u, sn[2].v, sn[2].sigma, cout, cin, 1, Cip, 1.f,
+    sn_bwd(ex.st, w.dwpsc, P.w("sc.w"), sn[2].u, sn[2].v, sn[2].sigma, cout, cin, 1, Cip, nullptr,
            P.gr("sc.w"), w.part);
 }
 

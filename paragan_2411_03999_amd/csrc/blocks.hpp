@@ -114,8 +114,10 @@ struct DBlock {
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);
-  // dx may be null; dx_f32 writes an unrounded fp32 input gradient.
-  void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool dx_f32);
+  // dx may be null; dx_f32 writes an unrounded fp32 input gradient;
+  // wgrad = false computes the input gradient only (no parameter gradients).
+  void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool dx_f32,
+           bool wgrad = true);
 };
 
 // ----------------------------------------------------------- attention
@@ -126,13 +128,13 @@ struct Attn {
   SNSlot sn[4];
   void *wqkv = nullptr, *wo = nullptr;   // packed fwd weights
   void *qkv = nullptr;       // [B][H][W][Nqkv] bf16 projections (pre-pool)
-  void *kp = nullptr, *vp = nullptr, *vt = nullptr;   // pooled keys/values
+  void *kp = nullptr, *kt = nullptr, *vp = nullptr, *vt = nullptr;   // pooled keys/values
   void *o = nullptr;         // attention output [B][HW][dv] bf16
   float* lse = nullptr;      // [B][HW]
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);
-  void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx);
+  void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool wgrad = true);
 };
 
 // SN of one weight into a slot (power iteration updates u in place).

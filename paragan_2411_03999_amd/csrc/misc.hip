@@ -158,6 +158,30 @@ void pack_weight(hipStream_t st, bool f32, const float* W, const float* sigma, i
   PG_LAUNCH_CHECK();
 }
 
+// Transposed 1x1 pack into columns [col_off, col_off + Np) of a [Cp][ld]
+// matrix: dst[c][col_off + n] = W[n][c] / sigma (zero outside Cout x Cin).
+template <typename T>
+__global__ void k_pack_t(const float* W, const float* sigma, int Cout, int Cin, int Cp, int Np, int ld,
+                         int col_off, T* dst) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)Cp * Np) return;
+  const int n = (int)(i % Np), c = (int)(i / Np);
+  const float v = (n < Cout && c < Cin) ? W[(int64_t)n * Cin + c] / *sigma : 0.f;
+  st<T>(dst, (int64_t)c * ld + col_off + n, v);
+}
+
+void pack_weight_t(hipStream_t st, bool f32, const float* W, const float* sigma, int Cout, int Cin, int Cp,
+                   int Np, int ld, int col_off, void* dst) {
+  dim3 g((unsigned)cdiv((int64_t)Cp * Np, 256));
+  if (f32)
+    hipLaunchKernelGGL(k_pack_t<float>, g, dim3(256), 0, st, W, sigma, Cout, Cin, Cp, Np, ld, col_off,
+                       (float*)dst);
+  else
+    hipLaunchKernelGGL(k_pack_t<bf16_t>, g, dim3(256), 0, st, W, sigma, Cout, Cin, Cp, Np, ld, col_off,
+                       (bf16_t*)dst);
+  PG_LAUNCH_CHECK();
+}
+
 // SN backward.  dwp: dL/d(W/sigma) in the padded forward layout
 // [Np][R][R][Cp]; W: master [Cout][R][R][Cin].
 //   dW = (dWsn - <dWsn, W/sigma> u v^T) / sigma,  v indexed by (r, s, c).
@@ -177,8 +201,9 @@ __global__ void k_sn_dot_part(const float* dwp, const float* W, int Cout, int Ci
 
 __global__ void k_sn_bwd_apply(const float* dwp, const float* W, const float* u, const float* v,
                                const float* sigma, const float* part, int nparts, int Cout, int Cin,
-                               int RR, int Cp, float extra_scale, float* dW) {
+                               int RR, int Cp, const float* scale_p, float* dW) {
   __shared__ float dotsh;
+  const float extra_scale = scale_p ? *scale_p : 1.f;
   if (threadIdx.x == 0) {
     float d = 0.f;
     for (int j = 0; j < nparts; ++j) d += part[j];
@@ -198,14 +223,14 @@ __global__ void k_sn_bwd_apply(const float* dwp, const float* W, const float* u,
 }
 
 void sn_bwd(hipStream_t st, const float* dwp, const float* W, const float* u, const float* v,
-            const float* sigma, int Cout, int Cin, int R, int Cp, float extra_scale, float* dW,
+            const float* sigma, int Cout, int Cin, int R, int Cp, const float* scale, float* dW,
             float* part /* >= 256 floats */) {
   const int RR = R * R;
   const int64_t total = (int64_t)Cout * RR * Cin;
   const int nparts = (int)std::min<int64_t>(256, cdiv(total, 256));
   hipLaunchKernelGGL(k_sn_dot_part, dim3(nparts), dim3(256), 0, st, dwp, W, Cout, Cin, RR, Cp, part);
   hipLaunchKernelGGL(k_sn_bwd_apply, dim3((unsigned)cdiv(total, 256)), dim3(256), 0, st, dwp, W, u, v,
-                     sigma, part, nparts, Cout, Cin, RR, Cp, extra_scale, dW);
+                     sigma, part, nparts, Cout, Cin, RR, Cp, scale, dW);
   PG_LAUNCH_CHECK();
 }
 

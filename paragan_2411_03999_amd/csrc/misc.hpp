@@ -11,9 +11,12 @@ void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, f
                    float* sigma, int n_iter, float eps, void* ws, float* u_save = nullptr);
 void pack_weight(hipStream_t st, bool f32, const float* W, const float* sigma, int Cout, int Cin,
                  int R, int Np, int Cp, bool dgrad, void* dst);
-// dW = (s*dWsn - <s*dWsn, W/sigma> u v^T) / sigma with s = extra_scale.
+// dst[c][col_off + n] = W[n][c] / sigma for a 1x1 weight W [Cout][Cin]
+void pack_weight_t(hipStream_t st, bool f32, const float* W, const float* sigma, int Cout, int Cin, int Cp,
+                   int Np, int ld, int col_off, void* dst);
+// dW = (s*dWsn - <s*dWsn, W/sigma> u v^T) / sigma with s = *scale (1 if null).
 void sn_bwd(hipStream_t st, const float* dwp, const float* W, const float* u, const float* v,
-            const float* sigma, int Cout, int Cin, int R, int Cp, float extra_scale, float* dW,
+            const float* sigma, int Cout, int Cin, int R, int Cp, const float* scale, float* dW,
             float* part);
 
 // out[c] = scale * sum_m x[m][c]

@@ -1,0 +1,458 @@
+// BigGAN generator / discriminator executors and the G+D train step.
+//
+// One training iteration (Numerical Optimizations, "Asynchronous Update
+// Scheme": the D:G ratio is adjustable; here n_D discriminator updates per
+// generator update) runs entirely on the context's stream:
+//   D step k:  G forward on (z_k, y_k) writing the fake half of the D batch,
+//              D forward / hinge / backward on concat(real_k, fake_k) --
+//              inputs that share a weight go through one batched pass
+//              (Implementation, "Hardware-Aware Layout Transformation") --
+//              then Adam on D;
+//   G step:    G forward, D forward, hinge, D backward for the input
+//              gradient only, G backward, Adam on G.
+// Only one host synchronisation per call: the losses at the end.
+#include "net.hpp"
+
+#include <cstdio>
+
+namespace pg {
+
+Arch arch_from(const paragan_biggan_desc* d) {
+  Arch a;
+  a.img = d->img; a.ch = d->ch; a.n_g = d->n_g; a.n_d = d->n_d; a.attn_res = d->attn_res;
+  a.n_classes = d->n_classes; a.dz = d->dz; a.sd = d->shared_dim;
+  a.zc = d->n_g >= 0 ? d->dz / (d->n_g + 1) : 0;
+  a.dc = a.sd + a.zc;
+  for (int i = 0; i <= d->n_g && i < 10; ++i) a.g_mult.push_back(d->g_mult[i]);
+  for (int j = 0; j < d->n_d && j < 10; ++j) {
+    a.d_mult.push_back(d->d_mult[j]);
+    a.d_down.push_back(d->d_down[j]);
+  }
+  a.npi = d->n_power_iter; a.bn_eps = d->bn_eps; a.sn_eps = d->sn_eps;
+  return a;
+}
+
+std::vector<DSpec> d_specs(const Arch& a) {
+  std::vector<DSpec> v;
+  int res = a.img, cin = 3;
+  bool placed = false;
+  for (int j = 0; j < a.n_d; ++j) {
+    DSpec s;
+    s.cin = cin; s.cout = a.d_mult[j] * a.ch; s.H = res; s.W = res;
+    s.preact = j > 0; s.down = a.d_down[j] != 0; s.lsc = s.cin != s.cout || s.down;
+    res = s.down ? res / 2 : res;
+    s.attn = !placed && a.attn_res > 0 && res == a.attn_res;
+    placed = placed || s.attn;
+    v.push_back(s);
+    cin = s.cout;
+  }
+  return v;
+}
+
+static bool attn_width_ok(int C) {
+  const int dv = (int)cpad(C / 2);
+  return C % 8 == 0 && C / 8 <= 32 && (dv == 32 || dv == 64 || dv == 96 || dv == 128);
+}
+
+void check_arch(const paragan_biggan_desc* d) {
+  if (!d) throw Error{-1, "biggan: desc is NULL"};
+  PG_CHECK(d->n_g >= 1 && d->n_g <= 9, "biggan: n_g must be in [1, 9]");
+  PG_CHECK(d->n_d >= 1 && d->n_d <= 10, "biggan: n_d must be in [1, 10]");
+  PG_CHECK(d->ch >= 1 && d->B >= 1 && d->n_classes >= 1 && d->shared_dim >= 1, "biggan: ch, B, n_classes, shared_dim >= 1");
+  PG_CHECK(d->img == (4 << d->n_g), "biggan: img must equal 4 * 2^n_g");
+  PG_CHECK(d->dz >= d->n_g + 1 && d->dz % (d->n_g + 1) == 0, "biggan: dz must split into n_g + 1 equal chunks");
+  for (int i = 0; i <= d->n_g; ++i) PG_CHECK(d->g_mult[i] >= 1, "biggan: g_mult entries must be >= 1");
+  for (int j = 0; j < d->n_d; ++j) PG_CHECK(d->d_mult[j] >= 1, "biggan: d_mult entries must be >= 1");
+  PG_CHECK(d->n_power_iter >= 1 && d->bn_eps > 0 && d->sn_eps > 0 && d->adam_eps > 0, "biggan: bad eps / n_power_iter");
+  PG_CHECK(d->lr_g >= 0 && d->lr_d >= 0 && d->beta1 >= 0 && d->beta1 < 1 && d->beta2 >= 0 && d->beta2 < 1,
+           "biggan: bad optimiser settings");
+  PG_CHECK((int64_t)2 * d->B * d->img * d->img < (1LL << 31), "biggan: batch too large");
+  const Arch a = arch_from(d);
+  int res = a.img;
+  for (const DSpec& s : d_specs(a)) {
+    PG_CHECK(!s.down || (res % 2 == 0 && res >= 2), "biggan: a pooling D block needs an even resolution");
+    res = s.down ? res / 2 : res;
+    if (s.attn) PG_CHECK(attn_width_ok(s.cout) && res % 2 == 0, "biggan: unsupported D attention width");
+  }
+  for (int i = 0; i < a.n_g; ++i)
+    if ((4 << (i + 1)) == a.attn_res)
+      PG_CHECK(attn_width_ok(a.g_mult[i + 1] * a.ch), "biggan: unsupported G attention width");
+}
+
+Layout g_layout(const Arch& a) {
+  Layout L;
+  const int c0 = a.g_mult[0] * a.ch;
+  L.add("shared", {a.n_classes, a.sd}, false);
+  L.add("linear.w", {16LL * c0, a.zc}, true);
+  L.add("linear.b", {16LL * c0}, false);
+  for (int i = 0; i < a.n_g; ++i) {
+    const int cout = a.g_mult[i + 1] * a.ch;
+    L.add_prefixed("g" + std::to_string(i) + ".", gblock_layout(a.g_mult[i] * a.ch, cout, a.dc));
+    if ((4 << (i + 1)) == a.attn_res) L.add_prefixed("attn.", attn_layout(cout));
+  }
+  const int c = a.g_mult[a.n_g] * a.ch;
+  L.add("out_bn.gain", {c}, false);
+  L.add("out_bn.bias", {c}, false);
+  L.add("out_conv.w", {3, 3, 3, c}, true);
+  L.add("out_conv.b", {3}, false);
+  return L;
+}
+
+Layout d_layout(const Arch& a) {
+  Layout L;
+  const auto specs = d_specs(a);
+  for (int j = 0; j < (int)specs.size(); ++j) {
+    const DSpec& s = specs[j];
+    L.add_prefixed("d" + std::to_string(j) + ".", dblock_layout(s.cin, s.cout, s.lsc));
+    if (s.attn) L.add_prefixed("attn.", attn_layout(s.cout));
+  }
+  const int c = a.d_mult[a.n_d - 1] * a.ch;
+  L.add("head.w", {1, c}, true);
+  L.add("head.b", {1}, false);
+  L.add("embed", {a.n_classes, c}, true);
+  return L;
+}
+
+static Params sub(const Params& P, const std::string& prefix) {
+  Params q = P;
+  q.prefix = prefix;
+  return q;
+}
+
+static void plan_slot(Arena& s, SNSlot& slot, int64_t rows, int64_t cols) {
+  slot.u = s.f32(rows);
+  slot.v = s.f32(cols);
+  slot.sigma = s.f32(1);
+}
+
+// =================================================================== G
+void GNet::plan_saved(Arena& s) {
+  const Arch& a = a_;
+  const int c0 = a.g_mult[0] * a.ch;
+  plan_slot(s, lin_, 16LL * c0, a.zc);
+  cond_.clear();
+  for (int i = 0; i < a.n_g; ++i) cond_.push_back(s.f32((size_t)B_ * a.dc));
+  act_.clear();
+  blocks_.clear();
+  act_.push_back(s.bytes((size_t)B_ * 16 * cpad(c0) * 2));
+  in_.assign(1, act_[0]);
+  int res = 4;
+  for (int i = 0; i < a.n_g; ++i) {
+    GBlock g;
+    g.B = B_; g.H = res; g.W = res; g.cin = a.g_mult[i] * a.ch; g.cout = a.g_mult[i + 1] * a.ch;
+    g.dc = a.dc; g.npi = a.npi; g.f32 = false; g.bn_eps = a.bn_eps; g.sn_eps = a.sn_eps;
+    g.plan_saved(s);
+    blocks_.push_back(g);
+    res *= 2;
+    act_.push_back(s.bytes((size_t)B_ * res * res * cpad(g.cout) * 2));
+    if (res == a.attn_res) {
+      attn_after_ = i;
+      attn_.B = B_; attn_.H = res; attn_.W = res; attn_.C = g.cout; attn_.npi = a.npi; attn_.sn_eps = a.sn_eps;
+      attn_.plan_saved(s);
+      attn_out_ = s.bytes((size_t)B_ * res * res * cpad(g.cout) * 2);
+    }
+    in_.push_back(i == attn_after_ ? attn_out_ : act_[i + 1]);
+  }
+  const int c = a.g_mult[a.n_g] * a.ch;
+  const int cp = (int)cpad(c);
+  mean_ = s.f32(cp); rstd_ = s.f32(cp); gain_ = s.f32(cp); bias_ = s.f32(cp); scale_ = s.f32(cp);
+  plan_slot(s, out_, 3, 27LL * c);
+}
+
+struct GNetWs {
+  void *g0, *g1;       // ping-pong activation gradients (bf16)
+  float *da, *dw, *dlin, *dcond, *part;
+  void* head;
+  void* blk;           // block workspace
+  size_t blk_bytes;
+};
+
+static GNetWs gnet_carve(const Arch& a, int B, const std::vector<GBlock>& blocks, const Attn* attn, Arena& w,
+                         int n_cu) {
+  GNetWs r;
+  size_t maxact = (size_t)B * 16 * cpad(a.g_mult[0] * a.ch);
+  int res = 4;
+  size_t blk = 0;
+  for (const GBlock& g : blocks) {
+    res *= 2;
+    maxact = std::max(maxact, (size_t)B * res * res * std::max(cpad(g.cin), cpad(g.cout)));
+    blk = std::max(blk, g.ws_size(n_cu));
+  }
+  if (attn) blk = std::max(blk, attn->ws_size(n_cu));
+  const int c0 = a.g_mult[0] * a.ch;
+  const int c = a.g_mult[a.n_g] * a.ch;
+  const int64_t M = (int64_t)B * a.img * a.img;
+  blk = std::max({blk, sn_ws_bytes(16LL * c0, a.zc), sn_ws_bytes(3, 27LL * c), bn_stats_ws_bytes(M, c)});
+  r.g0 = w.bytes(maxact * 2);
+  r.g1 = w.bytes(maxact * 2);
+  r.da = w.f32((size_t)M * cpad(c));
+  r.dw = w.f32(27LL * c);
+  r.dlin = w.f32(16LL * c0 * a.zc);
+  r.dcond = w.f32((size_t)B * a.dc);
+  r.part = w.f32(256);
+  r.head = w.bytes(std::max(ghead_ws_bytes(M, c), bn_bwd_ws_bytes(B, a.img * a.img, c)));
+  r.blk_bytes = blk;
+  r.blk = w.bytes(blk);
+  return r;
+}
+
+size_t GNet::ws_size(int n_cu) {
+  Arena w(nullptr);
+  gnet_carve(a_, B_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, n_cu);
+  return w.off;
+}
+
+void GNet::fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img) {
+  const Arch& a = a_;
+  Arena w(ex.ws);
+  GNetWs r = gnet_carve(a, B_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
+  Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
+  const int c0 = a.g_mult[0] * a.ch;
+  sn_forward(eb, P, "linear.w", lin_, a.npi, a.sn_eps);
+  glin_fwd(ex.st, z, a.dz, a.zc, P.w("linear.w"), lin_.sigma, P.w("linear.b"), B_, c0, (int)cpad(c0), act_[0]);
+  const void* h = act_[0];
+  for (int i = 0; i < a.n_g; ++i) {
+    make_cond(ex.st, P.w("shared"), a.sd, y, z, a.dz, a.zc * (i + 1), a.zc, B_, cond_[i]);
+    blocks_[i].fwd(eb, sub(P, "g" + std::to_string(i) + "."), h, cond_[i], act_[i + 1]);
+    h = act_[i + 1];
+    if (i == attn_after_) {
+      attn_.fwd(eb, sub(P, "attn."), h, attn_out_);
+      h = attn_out_;
+    }
+  }
+  const int c = a.g_mult[a.n_g] * a.ch, cp = (int)cpad(c);
+  const int64_t M = (int64_t)B_ * a.img * a.img;
+  bn_stats(ex.st, false, h, M, c, cp, a.bn_eps, mean_, rstd_, r.blk);
+  cbn_tables(ex.st, nullptr, 0, nullptr, nullptr, nullptr, nullptr, P.w("out_bn.gain"), P.w("out_bn.bias"), rstd_,
+             1, c, cp, gain_, bias_, scale_);
+  sn_forward(eb, P, "out_conv.w", out_, a.npi, a.sn_eps);
+  ghead_fwd(ex.st, h, B_, a.img, a.img, c, cp, mean_, scale_, bias_, P.w("out_conv.w"), out_.sigma,
+            P.w("out_conv.b"), img);
+  img_ = img;
+}
+
+void GNet::bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, const float* dimg, int ldd) {
+  const Arch& a = a_;
+  Arena w(ex.ws);
+  GNetWs r = gnet_carve(a, B_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
+  Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
+  const int c = a.g_mult[a.n_g] * a.ch, cp = (int)cpad(c);
+  const void* x5 = in_[a.n_g];
+  ghead_bwd(ex.st, dimg, ldd, img_, x5, B_, a.img, a.img, c, cp, mean_, scale_, bias_, P.w("out_conv.w"),
+            out_.sigma, r.da, r.dw, P.gr("out_conv.b"), r.head);
+  sn_bwd(ex.st, r.dw, P.w("out_conv.w"), out_.u, out_.v, out_.sigma, 3, c, 3, c, nullptr, P.gr("out_conv.w"),
+         r.part);
+  void* gcur = r.g0;
+  void* gnext = r.g1;
+  bn_bwd(ex.st, false, r.da, false, x5, B_, a.img, a.img, c, cp, mean_, rstd_, gain_, bias_, 0, nullptr, gcur,
+         P.gr("out_bn.gain"), P.gr("out_bn.bias"), 0, r.head);
+  for (int i = a.n_g - 1; i >= 0; --i) {
+    if (i == attn_after_) {
+      attn_.bwd(eb, sub(P, "attn."), act_[i + 1], gcur, gnext);
+      std::swap(gcur, gnext);
+    }
+    blocks_[i].bwd(eb, sub(P, "g" + std::to_string(i) + "."), in_[i], cond_[i], gcur, gnext, r.dcond,
+                   i != a.n_g - 1);
+    std::swap(gcur, gnext);
+  }
+  const int c0 = a.g_mult[0] * a.ch;
+  glin_bwd(ex.st, gcur, z, a.dz, a.zc, B_, c0, (int)cpad(c0), r.dlin, P.gr("linear.b"));
+  sn_bwd(ex.st, r.dlin, P.w("linear.w"), lin_.u, lin_.v, lin_.sigma, 16 * c0, a.zc, 1, a.zc, nullptr,
+         P.gr("linear.w"), r.part);
+  shared_grad(ex.st, r.dcond, a.dc, y, B_, a.n_classes, a.sd, P.gr("shared"));
+}
+
+// =================================================================== D
+void DNet::plan_saved(Arena& s) {
+  const Arch& a = a_;
+  act_.clear();
+  blocks_.clear();
+  act_.push_back(s.bytes((size_t)N_ * a.img * a.img * 32 * 2));
+  in_.assign(1, act_[0]);
+  const auto specs = d_specs(a);
+  for (int j = 0; j < (int)specs.size(); ++j) {
+    const DSpec& sp = specs[j];
+    DBlock b;
+    b.B = N_; b.H = sp.H; b.W = sp.W; b.cin = sp.cin; b.cout = sp.cout; b.npi = a.npi;
+    b.preact = sp.preact; b.down = sp.down; b.lsc = sp.lsc; b.f32 = false; b.sn_eps = a.sn_eps;
+    b.plan_saved(s);
+    blocks_.push_back(b);
+    act_.push_back(s.bytes((size_t)N_ * b.Ho * b.Wo * cpad(sp.cout) * 2));
+    if (sp.attn) {
+      attn_after_ = j;
+      attn_.B = N_; attn_.H = b.Ho; attn_.W = b.Wo; attn_.C = sp.cout; attn_.npi = a.npi; attn_.sn_eps = a.sn_eps;
+      attn_.plan_saved(s);
+      attn_out_ = s.bytes((size_t)N_ * b.Ho * b.Wo * cpad(sp.cout) * 2);
+    }
+    in_.push_back(j == attn_after_ ? attn_out_ : act_[j + 1]);
+  }
+  const int c = a.d_mult[a.n_d - 1] * a.ch;
+  hs_ = s.f32((size_t)N_ * c);
+  plan_slot(s, head_, 1, c);
+  plan_slot(s, emb_, a.n_classes, c);
+}
+
+struct DNetWs {
+  void *g0, *g1;
+  float *dw, *dE, *part;
+  void* blk;
+  size_t blk_bytes;
+};
+
+static DNetWs dnet_carve(const Arch& a, int N, const std::vector<DBlock>& blocks, const Attn* attn, Arena& w,
+                         int n_cu) {
+  DNetWs r;
+  size_t maxact = 0, blk = 0;
+  for (const DBlock& b : blocks) {
+    maxact = std::max(maxact, (size_t)N * b.H * b.W * std::max(cpad(b.cin), cpad(b.cout)));
+    blk = std::max(blk, b.ws_size(n_cu));
+  }
+  if (attn) blk = std::max(blk, attn->ws_size(n_cu));
+  const int c = a.d_mult[a.n_d - 1] * a.ch;
+  blk = std::max({blk, sn_ws_bytes(1, c), sn_ws_bytes(a.n_classes, c)});
+  r.g0 = w.bytes(maxact * 2);
+  r.g1 = w.bytes(maxact * 2);
+  r.dw = w.f32(c);
+  r.dE = w.f32((size_t)a.n_classes * c);
+  r.part = w.f32(256);
+  r.blk_bytes = blk;
+  r.blk = w.bytes(blk);
+  return r;
+}
+
+size_t DNet::ws_size(int n_cu) {
+  Arena w(nullptr);
+  dnet_carve(a_, N_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, n_cu);
+  return w.off;
+}
+
+void DNet::fwd(const Exec& ex, const Params& P, const float* x, const int32_t* y, float* out) {
+  const Arch& a = a_;
+  Arena w(ex.ws);
+  DNetWs r = dnet_carve(a, N_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
+  Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
+  img_to_bf16(ex.st, x, (int64_t)N_ * a.img * a.img, 32, act_[0]);
+  const void* h = act_[0];
+  for (int j = 0; j < (int)blocks_.size(); ++j) {
+    blocks_[j].fwd(eb, sub(P, "d" + std::to_string(j) + "."), h, act_[j + 1]);
+    h = act_[j + 1];
+    if (j == attn_after_) {
+      attn_.fwd(eb, sub(P, "attn."), h, attn_out_);
+      h = attn_out_;
+    }
+  }
+  const DBlock& last = blocks_.back();
+  sn_forward(eb, P, "head.w", head_, a.npi, a.sn_eps);
+  sn_forward(eb, P, "embed", emb_, a.npi, a.sn_eps);
+  dhead_fwd(ex.st, h, N_, last.Ho * last.Wo, last.cout, last.Cop, y, P.w("head.w"), head_.sigma, P.w("head.b"),
+            P.w("embed"), emb_.sigma, hs_, out);
+}
+
+void DNet::bwd(const Exec& ex, const Params& P, const int32_t* y, const float* dout, float* dimg, bool wgrad) {
+  const Arch& a = a_;
+  Arena w(ex.ws);
+  DNetWs r = dnet_carve(a, N_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
+  Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
+  const DBlock& last = blocks_.back();
+  const int nb = (int)blocks_.size();
+  const void* xl = in_[nb];
+  void* gcur = r.g0;
+  void* gnext = r.g1;
+  dhead_bwd(ex.st, xl, N_, last.Ho * last.Wo, last.cout, last.Cop, y, dout, hs_, P.w("head.w"), head_.sigma,
+            P.w("embed"), emb_.sigma, a.n_classes, gcur, wgrad ? r.dw : nullptr, P.gr("head.b"), r.dE);
+  if (wgrad) {
+    sn_bwd(ex.st, r.dw, P.w("head.w"), head_.u, head_.v, head_.sigma, 1, last.cout, 1, last.cout, nullptr,
+           P.gr("head.w"), r.part);
+    sn_bwd(ex.st, r.dE, P.w("embed"), emb_.u, emb_.v, emb_.sigma, a.n_classes, last.cout, 1, last.cout, nullptr,
+           P.gr("embed"), r.part);
+  }
+  for (int j = nb - 1; j >= 0; --j) {
+    if (j == attn_after_) {
+      attn_.bwd(eb, sub(P, "attn."), act_[j + 1], gcur, gnext, wgrad);
+      std::swap(gcur, gnext);
+    }
+    void* dx = j > 0 ? gnext : (void*)dimg;
+    blocks_[j].bwd(eb, sub(P, "d" + std::to_string(j) + "."), in_[j], gcur, dx, j == 0, wgrad);
+    std::swap(gcur, gnext);
+  }
+}
+
+// =================================================================== step
+struct StepWs {
+  void* gsaved;
+  void* dsaved;
+  float *ximg, *logits, *dout, *dimg, *dloss;
+  int32_t* ylab;
+  void* net;
+  size_t net_bytes;
+};
+
+static StepWs step_carve(const Arch& a, int B, Arena& w, GNet& g, DNet& d2, DNet& d1, int n_cu) {
+  StepWs r;
+  Arena gs(w.base ? w.base + w.off : nullptr);
+  g.plan_saved(gs);
+  r.gsaved = w.bytes(gs.off);
+  Arena ds2(w.base ? w.base + w.off : nullptr), ds1(w.base ? w.base + w.off : nullptr);
+  d2.plan_saved(ds2);
+  d1.plan_saved(ds1);
+  r.dsaved = w.bytes(std::max(ds2.off, ds1.off));
+  const int64_t pix = (int64_t)a.img * a.img;
+  r.ximg = w.f32((size_t)2 * B * pix * 3);
+  r.ylab = (int32_t*)w.bytes((size_t)2 * B * 4);
+  r.logits = w.f32(2 * B);
+  r.dout = w.f32(2 * B);
+  r.dimg = w.f32((size_t)B * pix * 32);
+  r.dloss = w.f32(64);
+  r.net_bytes = std::max({g.ws_size(n_cu), d2.ws_size(n_cu), d1.ws_size(n_cu)});
+  r.net = w.bytes(r.net_bytes);
+  return r;
+}
+
+size_t train_step_ws(const paragan_biggan_desc* d, int n_cu) {
+  const Arch a = arch_from(d);
+  GNet g(a, d->B);
+  DNet d2(a, 2 * d->B), d1(a, d->B);
+  Arena w(nullptr);
+  step_carve(a, d->B, w, g, d2, d1, n_cu);
+  return w.off;
+}
+
+void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
+                const paragan_step_inputs* in, int n_D, void* ws, float* losses_host) {
+  const Arch a = arch_from(d);
+  const int B = d->B;
+  hipStream_t st = ctx->stream;
+  GNet g(a, B);
+  DNet d2(a, 2 * B), d1(a, B);
+  Arena w(ws);
+  StepWs r = step_carve(a, B, w, g, d2, d1, ctx->n_cu);
+  Exec ex{st, ctx->n_cu, r.net, r.net_bytes};
+  const Layout LG = g_layout(a), LD = d_layout(a);
+  Params PG{&LG, "", G->params, G->u, G->grads};
+  Params PD{&LD, "", D->params, D->u, D->grads};
+  const int64_t pix = (int64_t)a.img * a.img;
+  for (int k = 0; k < n_D; ++k) {
+    PG_HIP(hipMemcpyAsync(r.ximg, in->x_real[k], (size_t)B * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(r.ylab, in->y_real[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(r.ylab + B, in->y_fake[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
+    g.fwd(ex, PG, in->z_fake[k], in->y_fake[k], r.ximg + (size_t)B * pix * 3);
+    d2.fwd(ex, PD, r.ximg, r.ylab, r.logits);
+    hinge(st, r.logits, B, B, false, r.dout, r.dloss + k);
+    d2.bwd(ex, PD, r.ylab, r.dout, nullptr, true);
+    D->adam_t += 1;
+    adam(st, D->params, D->grads, D->adam_m, D->adam_v, LD.n_params, d->beta1, d->beta2, d->lr_d, d->adam_eps,
+         D->adam_t);
+  }
+  g.fwd(ex, PG, in->z_g, in->y_g, r.ximg);
+  d1.fwd(ex, PD, r.ximg, in->y_g, r.logits);
+  hinge(st, r.logits, 0, B, true, r.dout, r.dloss + n_D);
+  d1.bwd(ex, PD, in->y_g, r.dout, r.dimg, false);
+  g.bwd(ex, PG, in->z_g, in->y_g, r.dimg, 32);
+  G->adam_t += 1;
+  adam(st, G->params, G->grads, G->adam_m, G->adam_v, LG.n_params, d->beta1, d->beta2, d->lr_g, d->adam_eps,
+       G->adam_t);
+  PG_HIP(hipMemcpyAsync(losses_host, r.dloss, (size_t)(n_D + 1) * 4, hipMemcpyDeviceToHost, st));
+  PG_HIP(hipStreamSynchronize(st));
+}
+
+}  // namespace pg

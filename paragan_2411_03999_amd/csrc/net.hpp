@@ -1,0 +1,80 @@
+// BigGAN networks and the G+D train step (host runtime).
+#pragma once
+#include "../../include/paragan.h"
+#include "attn.hpp"
+#include "blocks.hpp"
+#include "heads.hpp"
+
+namespace pg {
+
+struct Arch {
+  int img, ch, n_g, n_d, attn_res, n_classes, dz, sd, zc, dc;
+  std::vector<int> g_mult, d_mult, d_down;
+  int npi;
+  float bn_eps, sn_eps;
+};
+
+Arch arch_from(const paragan_biggan_desc* d);
+void check_arch(const paragan_biggan_desc* d);
+Layout g_layout(const Arch& a);
+Layout d_layout(const Arch& a);
+
+struct DSpec {
+  int cin, cout, H, W;
+  bool preact, down, lsc, attn;
+};
+std::vector<DSpec> d_specs(const Arch& a);
+
+class GNet {
+ public:
+  GNet(const Arch& a, int B) : a_(a), B_(B) {}
+  void plan_saved(Arena& s);
+  size_t ws_size(int n_cu);
+  // img: fp32 [B][img][img][3]
+  void fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img);
+  // dimg: fp32 [B][img][img][ldd]
+  void bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, const float* dimg, int ldd);
+
+ private:
+  Arch a_;
+  int B_;
+  std::vector<GBlock> blocks_;
+  Attn attn_;
+  int attn_after_ = -1;
+  std::vector<void*> act_;     // act_[0]: linear output; act_[i+1]: output of block i
+  std::vector<void*> in_;      // in_[i]: input of block i (attention output after the attention block)
+  void* attn_out_ = nullptr;
+  std::vector<float*> cond_;
+  SNSlot lin_, out_;
+  float *mean_, *rstd_, *gain_, *bias_, *scale_;
+  float* img_ = nullptr;
+};
+
+class DNet {
+ public:
+  DNet(const Arch& a, int N) : a_(a), N_(N) {}
+  void plan_saved(Arena& s);
+  size_t ws_size(int n_cu);
+  // x: fp32 images [N][img][img][3]; out: fp32 logits [N]
+  void fwd(const Exec& ex, const Params& P, const float* x, const int32_t* y, float* out);
+  // wgrad = false: input gradient only (dimg fp32 [N][img][img][32])
+  void bwd(const Exec& ex, const Params& P, const int32_t* y, const float* dout, float* dimg, bool wgrad);
+
+ private:
+  Arch a_;
+  int N_;
+  std::vector<DBlock> blocks_;
+  Attn attn_;
+  int attn_after_ = -1;
+  std::vector<void*> act_;     // act_[0]: bf16 image; act_[j+1]: output of block j
+  std::vector<void*> in_;      // in_[j]: input of block j
+  void* attn_out_ = nullptr;
+  float* hs_ = nullptr;
+  SNSlot head_, emb_;
+};
+
+size_t train_step_ws(const paragan_biggan_desc* d, int n_cu);
+void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
+                const paragan_step_inputs* in, int n_D, void* ws, float* losses_host);
+
+}  // namespace pg

@@ -82,3 +82,44 @@ def test_sizes_queries_need_no_gpu(L):
     s, w = lib.paragan_dblock_sizes(lib.DBlockDesc(64, 32, 32, 256, 512, 1, 1, 1, lib.BF16, 1, 1e-12))
     assert s > 0 and w > 0 and s % 256 == 0
     assert lib.paragan_sn_ws_size(512, 2304) > 0
+
+
+def _desc(a, B=2):
+    d = lib.BigganDesc()
+    d.img, d.ch, d.n_g, d.n_d = a.img, a.ch, a.n_g, len(a.d_mult)
+    for i, m in enumerate(a.g_mult):
+        d.g_mult[i] = m
+    for j, (m, dn) in enumerate(zip(a.d_mult, a.d_down)):
+        d.d_mult[j], d.d_down[j] = m, dn
+    d.attn_res, d.n_classes, d.dz, d.shared_dim, d.B = a.attn_res, a.n_classes, a.dz, a.shared_dim, B
+    d.n_power_iter, d.bn_eps, d.sn_eps = 1, 1e-5, 1e-12
+    d.lr_g, d.lr_d, d.beta1, d.beta2, d.adam_eps = 1e-4, 4e-4, 0.0, 0.999, 1e-6
+    return d
+
+
+@pytest.mark.parametrize("arch", [O.biggan128, O.biggan512])
+def test_network_layouts_match_oracle(L, arch):
+    a = arch()
+    d = _desc(a)
+    assert lib.paragan_biggan_check(d) == lib.OK
+    for which, fn in ((0, O.g_layout), (1, O.d_layout)):
+        ents, npar, nu = lib.paragan_net_layout(d, which)
+        lay, sn = fn(a)
+        assert [(e["name"], e["shape"]) for e in ents] == list(lay.items())
+        assert [e["name"] for e in ents if e["u_offset"] >= 0] == sn
+    if arch is O.biggan128:
+        g = lib.paragan_net_layout(d, 0)[1]
+        dd = lib.paragan_net_layout(d, 1)[1]
+        assert g + dd == 158_416_358            # Table tab:GAN: 158.42M
+
+
+def test_biggan_validation(L):
+    a = O.biggan128()
+    d = _desc(a)
+    d.img = 64
+    assert lib.paragan_biggan_check(d) == lib.EINVAL          # img != 4 * 2^n_g
+    d = _desc(a)
+    d.dz = 121
+    assert lib.paragan_biggan_check(d) == lib.EINVAL          # z does not split evenly
+    d = _desc(a)
+    assert lib.paragan_train_step_ws_size(d) > 0

@@ -1,0 +1,77 @@
+"""GPU parity: the self-attention block vs the oracle (bf16 path)."""
+import numpy as np
+import pytest
+
+from oracle import blocks as OB
+from oracle.numerics import bf16
+from paragan_2411_03999_amd import lib
+from paragan_2411_03999_amd.synth import Stream, init_params, init_u
+
+from .parity import Report, check, need_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def f32(d):
+    return {k: np.asarray(v, np.float32).astype(np.float64) for k, v in d.items()}
+
+
+def run_attn(B, H, W, C, seed, gamma=0.7, weights="gaussian"):
+    torch = need_gpu()
+    s = Stream(seed)
+    shapes = OB.attn_param_shapes(C)
+    p = f32(init_params(shapes, s, weights=weights, attn_gamma=gamma))
+    u = f32(init_u(shapes, OB.ATTN_SN, s))
+    x = bf16(s.normal((B, H, W, C)))
+    dy = bf16(s.normal((B, H, W, C)))
+    print("attn case", dict(B=B, H=H, W=W, C=C, seed=seed), flush=True)
+    cfg = OB.BlockCfg(bf16=True)
+    y_r, u_r, cache = OB.attn_fwd(x, p, u, cfg)
+    dx_r, g_r = OB.attn_bwd(dy, cache, cfg)
+    d = lib.AttnDesc(B, H, W, C, 1, 1e-12)
+    ents, npar, nu = lib.paragan_attn_layout(d)
+    assert [(e["name"], e["shape"]) for e in ents] == list(shapes.items())
+    sb, wb = lib.paragan_attn_sizes(d)
+    ctx = lib.Context()
+    P = lib.flat_from_named(ents, npar, p)
+    U = lib.u_from_named(ents, nu, u)
+    X = lib.to_device_nhwc(x, lib.BF16)
+    Y = lib.empty_nhwc(B, H, W, C, lib.BF16)
+    saved, ws = lib.workspace(sb), lib.workspace(wb)
+    lib.paragan_attn_fwd(ctx, d, P, U, X, Y, saved, ws)
+    DX = lib.empty_nhwc(B, H, W, C, lib.BF16)
+    G = torch.zeros(npar, dtype=torch.float32, device="cuda")
+    lib.paragan_attn_bwd(ctx, d, P, X, saved, lib.to_device_nhwc(dy, lib.BF16), DX, G, ws)
+    torch.cuda.synchronize()
+    rep = Report()
+    check("y", lib.from_device_nhwc(Y, C), y_r, True, rep)
+    # the attention contribution alone (y - x), a sharper view of the core
+    check("y-x", lib.from_device_nhwc(Y, C) - x, y_r - x, True, rep)
+    gu = lib.named_u_from_flat(ents, U)
+    for k in OB.ATTN_SN:
+        check("u." + k, gu[k], u_r[k], False, rep)
+    gg = lib.named_from_flat(ents, G)
+    for k in shapes:
+        check("grad." + k, gg[k], g_r[k], True, rep)
+    check("dx", lib.from_device_nhwc(DX, C), dx_r, True, rep)
+    check("dx-dy", lib.from_device_nhwc(DX, C) - dy, dx_r - dy, True, rep)
+    rep.done()
+
+
+def test_attn_small_padded_keys():
+    # H = W = 6: 36 queries and 9 keys, both padded to 32 inside the kernels
+    run_attn(B=2, H=6, W=6, C=96, seed=201)
+
+
+def test_attn_g_width():
+    run_attn(B=2, H=8, W=8, C=192, seed=202)        # dv = 96
+
+
+def test_attn_d_width_64x64():
+    """The BigGAN-128 discriminator's attention shape: 64x64, C = 96."""
+    run_attn(B=2, H=64, W=64, C=96, seed=203)
+
+
+def test_attn_g_width_64x64():
+    """The BigGAN-128 generator's attention shape: 64x64, C = 192."""
+    run_attn(B=1, H=64, W=64, C=192, seed=204)
