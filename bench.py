@@ -1,0 +1,240 @@
+#!/usr/bin/env python3
+"""Benchmark: BigGAN-128 G+D train step on one MI355X.
+
+One step = one paragan_train_step call: n_D = 2 discriminator updates on
+concat(real, fake) batches of 2 x 256 images and one generator update on
+256 images (hinge loss, Adam), the configuration the paper trains BigGAN
+with at 2048 images per step over 8 accelerators (Evaluation, Table
+tab:abl_study).  images/sec = batch x steps / seconds (the generator batch,
+one step per generator update).
+
+Inputs are synthetic and seeded (real images uniform in [-1, 1], z ~ N(0, 1),
+labels uniform over 1000 classes), generated on the GPU and resident in HBM
+before the timed region.  Weights are random (N(0, 1/fan_in)); spectral
+normalisation makes the scale immaterial.
+
+The JSON line also carries:
+  roofline      the dominant kernel (most GPU time in the timed steps),
+                timed live with HIP events on the library's stream:
+                algorithmic FLOPs (real channels) / its launch time, against
+                the bf16 dense MFMA peak;
+  conv_mfma     all implicit-GEMM convolution launches together;
+  cpu_baseline  the float64 CPU oracle timed on this host on a bounded
+                sample (one train step at batch 1 on the same architecture).
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA (published)
+METRIC = "images/sec/GPU, BigGAN-128 G+D train step; conv MFMA util % of peak"
+
+ARCHS = {
+    # img, ch, g_mult, d_mult, d_down, attn_res, n_classes, dz, shared_dim
+    "biggan128": (128, 96, (16, 16, 8, 4, 2, 1), (1, 2, 4, 8, 16, 16), (1, 1, 1, 1, 1, 0), 64, 1000, 120, 128),
+    "biggan512": (512, 64, (16, 16, 8, 8, 4, 2, 1, 1), (1, 1, 2, 4, 8, 8, 16, 16), (1, 1, 1, 1, 1, 1, 1, 0), 64,
+                  1000, 128, 128),
+}
+
+
+def make_desc(lib, arch, B):
+    img, ch, gm, dm, dd, attn, ncls, dz, sd = ARCHS[arch]
+    d = lib.BigganDesc()
+    d.img, d.ch, d.n_g, d.n_d = img, ch, len(gm) - 1, len(dm)
+    for i, m in enumerate(gm):
+        d.g_mult[i] = m
+    for j, (m, dn) in enumerate(zip(dm, dd)):
+        d.d_mult[j], d.d_down[j] = m, dn
+    d.attn_res, d.n_classes, d.dz, d.shared_dim, d.B = attn, ncls, dz, sd, B
+    d.n_power_iter, d.bn_eps, d.sn_eps = 1, 1e-5, 1e-12
+    d.lr_g, d.lr_d, d.beta1, d.beta2, d.adam_eps = 1e-4, 4e-4, 0.0, 0.999, 1e-6
+    return d
+
+
+def device_net(torch, lib, ents, npar, nu, gen):
+    """Seeded random parameters, u vectors and zeroed Adam state on the GPU."""
+    P = torch.empty(npar, dtype=torch.float32, device="cuda")
+    for e in ents:
+        n = 1
+        for s in e["shape"]:
+            n *= s
+        view = P[e["offset"]:e["offset"] + n]
+        name = e["name"]
+        if name.endswith("gamma"):
+            view.fill_(0.5)
+        elif name.endswith("out_bn.gain"):
+            view.fill_(1.0)
+        elif len(e["shape"]) >= 2:
+            fan = n // e["shape"][0]
+            view.normal_(0.0, fan ** -0.5, generator=gen)
+        else:
+            view.normal_(0.0, 0.02, generator=gen)
+    U = torch.empty(max(nu, 1), dtype=torch.float32, device="cuda").normal_(generator=gen)
+    G = torch.zeros(npar, dtype=torch.float32, device="cuda")
+    M = torch.zeros(npar, dtype=torch.float32, device="cuda")
+    V = torch.zeros(npar, dtype=torch.float32, device="cuda")
+    st = lib.NetState(P.data_ptr(), U.data_ptr(), G.data_ptr(), M.data_ptr(), V.data_ptr(), 0)
+    return dict(P=P, U=U, G=G, M=M, V=V, state=st)
+
+
+def cpu_baseline(arch, B=1, n_D=2):
+    """Time the oracle (float64 numpy) on one train step at batch B."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import biggan as O
+    from paragan_2411_03999_amd.synth import Stream, init_params, init_u
+    img, ch, gm, dm, dd, attn, ncls, dz, sd = ARCHS[arch]
+    a = O.Arch(img, ch, gm, dm, dd, attn, ncls, dz, sd)
+    s = Stream(4004)
+    glay, gsn = O.g_layout(a)
+    dlay, dsn = O.d_layout(a)
+    gp, gu = init_params(glay, s, weights="gaussian"), init_u(glay, gsn, s)
+    dp, du = init_params(dlay, s, weights="gaussian"), init_u(dlay, dsn, s)
+    d_in = [(s.uniform((B, img, img, 3)), s.labels(B, ncls), s.normal((B, dz)), s.labels(B, ncls))
+            for _ in range(n_D)]
+    g_in = (s.normal((B, dz)), s.labels(B, ncls))
+    hp = O.HParams()
+    optG, optD = O.adam_init(gp), O.adam_init(dp)
+    t0 = time.perf_counter()
+    _, _, losses, _, _ = O.train_step(a, hp, (gp, gu), (dp, du), optG, optD, d_in, g_in)
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": B / dt, "unit": "images/sec", "cores": int(threads), "kind": "oracle",
+            "sample": "one %s G+D train step (n_D=%d) at batch %d, float64 numpy, %.1f s; finite losses: %s"
+                      % (arch, n_D, B, dt, bool(np.all(np.isfinite(losses))))}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--batch", type=int, default=256)
+    ap.add_argument("--n-d", type=int, default=2)
+    ap.add_argument("--arch", default="biggan128", choices=sorted(ARCHS))
+    ap.add_argument("--seed", type=int, default=1004)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-batch", type=int, default=1)
+    ap.add_argument("--kernels-out", default=None, help="write the per-kernel table (JSON) here")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only (--gpus %d requested); the multi-GPU data-parallel "
+              "path is a design, not code" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import ctypes as C
+
+    import torch
+
+    from paragan_2411_03999_amd import lib
+    lib.load()
+    torch.cuda.set_device(0)
+    B, n_D = args.batch, args.n_d
+    d = make_desc(lib, args.arch, B)
+    assert lib.paragan_biggan_check(d) == lib.OK
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(args.seed)
+    gents, gn, gnu = lib.paragan_net_layout(d, 0)
+    dents, dn, dnu = lib.paragan_net_layout(d, 1)
+    Gn = device_net(torch, lib, gents, gn, gnu, gen)
+    Dn = device_net(torch, lib, dents, dn, dnu, gen)
+    img = d.img
+    keep = []
+    for _ in range(n_D):
+        keep.append(torch.rand((B, img, img, 3), device="cuda", generator=gen) * 2 - 1)
+    for _ in range(n_D):
+        keep.append(torch.randint(0, d.n_classes, (B,), device="cuda", generator=gen, dtype=torch.int32))
+    for _ in range(n_D):
+        keep.append(torch.randn((B, d.dz), device="cuda", generator=gen))
+    for _ in range(n_D):
+        keep.append(torch.randint(0, d.n_classes, (B,), device="cuda", generator=gen, dtype=torch.int32))
+    keep.append(torch.randn((B, d.dz), device="cuda", generator=gen))
+    keep.append(torch.randint(0, d.n_classes, (B,), device="cuda", generator=gen, dtype=torch.int32))
+    ptr = [t.data_ptr() for t in keep]
+    arr = lambda lst: (C.c_void_p * n_D)(*lst)
+    inp = lib.StepInputs(arr(ptr[0:n_D]), arr(ptr[n_D:2 * n_D]), arr(ptr[2 * n_D:3 * n_D]),
+                         arr(ptr[3 * n_D:4 * n_D]), ptr[4 * n_D], ptr[4 * n_D + 1])
+    ws_bytes = lib.paragan_train_step_ws_size(d)
+    ws = lib.workspace(ws_bytes)
+    ctx = lib.Context()
+    losses = (C.c_float * (n_D + 1))()
+
+    def step():
+        rc = lib.paragan_train_step(ctx, d, Gn["state"], Dn["state"], inp, n_D, ws, losses)
+        if rc != lib.OK:
+            raise lib.ParaganError(rc, lib.load().paragan_last_error(ctx.h).decode())
+
+    print("bench: %s B=%d n_D=%d workspace %.1f GB, G %d params, D %d params"
+          % (args.arch, B, n_D, ws_bytes / 2 ** 30, gn, dn), file=sys.stderr, flush=True)
+    for i in range(args.warmup):
+        step()
+        print("bench: warmup step %d losses %s" % (i, list(losses)), file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    lib.paragan_profile(ctx, True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+    ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    lib.paragan_profile(ctx, False)
+    stats = lib.paragan_profile_read(ctx)
+    gpu_ms = ev0.elapsed_time(ev1)
+    secs = gpu_ms / 1e3
+    print("bench: %d steps in %.3f s (wall %.3f s), last losses %s" % (args.steps, secs, wall, list(losses)),
+          file=sys.stderr, flush=True)
+
+    stats.sort(key=lambda s: -s["total_ms"])
+    dom = stats[0]
+    achieved = dom["flops"] / (dom["total_ms"] / 1e3) / 1e12
+    conv = [s for s in stats if s["name"].startswith(("k_conv_mfma", "k_wgrad_mfma"))]
+    conv_ms = sum(s["total_ms"] for s in conv)
+    conv_tf = sum(s["flops"] for s in conv) / (conv_ms / 1e3) / 1e12 if conv_ms else 0.0
+    all_ms = sum(s["total_ms"] for s in stats)
+    if args.kernels_out:
+        with open(args.kernels_out, "w") as f:
+            json.dump(stats, f, indent=1)
+    for s in stats[:12]:
+        print("bench: %-40s %6d launches %9.2f ms %8.1f TFLOP/s" % (
+            s["name"], s["launches"], s["total_ms"], s["flops"] / max(s["total_ms"], 1e-9) / 1e9),
+            file=sys.stderr)
+    out = {
+        "metric": METRIC,
+        "value": B * args.steps / secs,
+        "unit": "images/sec",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": gpu_ms / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded uniform images, N(0,1) latents, uniform labels; random weights)",
+        "config": {"workload": "%s G+D train step, batch %d, %d D steps per G step, bf16 activations with fp32 "
+                               "accumulation, fp32 heads" % (args.arch, B, n_D),
+                   "batch": B, "n_D": n_D, "resolution": d.img},
+        "roofline": {"bound": "mfma", "kernel": dom["name"], "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "launches_per_step": dom["launches"] / args.steps},
+        "conv_mfma": {"achieved": conv_tf, "unit": "TFLOP/s", "frac_of_peak": conv_tf / PEAK_BF16_TFLOPS,
+                      "share_of_profiled_time": conv_ms / max(all_ms, 1e-9)},
+    }
+    if not args.no_cpu_baseline:
+        print("bench: timing the CPU oracle sample ...", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(args.arch, B=args.cpu_batch, n_D=n_D)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -251,6 +251,26 @@ int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
                        const paragan_step_inputs* in, int32_t n_D, void* ws,
                        float* losses_host);
 
+/* ---------------------------------------------------------------------
+ * Launch profiler (instrumentation for the roofline report).  When enabled,
+ * every convolution, weight-gradient and attention launch on the context's
+ * stream is bracketed by a HIP event pair and tagged with its kernel
+ * template instance and algorithmic FLOPs (real, unpadded channels).
+ * paragan_profile_read synchronises the stream, aggregates the records by
+ * kernel name into `out` (up to `cap` entries; *count = number of kernels)
+ * and clears them.  Off by default; costs two event records per launch.
+ * ------------------------------------------------------------------- */
+typedef struct {
+  char name[64];
+  int64_t launches;
+  double total_ms;
+  double flops;
+} paragan_kernel_stat;
+
+int paragan_profile(paragan_ctx* ctx, int enable);
+int paragan_profile_read(paragan_ctx* ctx, paragan_kernel_stat* out,
+                         int32_t cap, int32_t* count);
+
 #ifdef __cplusplus
 }
 #endif

@@ -12,6 +12,14 @@ using namespace pg;
 
 static std::string g_create_err;
 
+namespace {
+// binds the context's profiler to the launchers for the duration of a call
+struct ProfBind {
+  explicit ProfBind(paragan_ctx* c) { pg::t_prof = c ? &c->prof : nullptr; }
+  ~ProfBind() { pg::t_prof = nullptr; }
+};
+}  // namespace
+
 static int fail(paragan_ctx* ctx, int code, const std::string& msg) {
   if (ctx) ctx->err = msg;
   else g_create_err = msg;
@@ -149,6 +157,7 @@ static size_t g_ws_for(paragan_ctx* ctx, const GBlock& g) { return g.ws_size(ctx
 extern "C" int paragan_gblock_fwd(paragan_ctx* ctx, const paragan_gblock_desc* d, const float* params, float* u,
                                   const void* x, const float* cond, void* y, void* saved, void* ws) {
   if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
   PG_TRY(ctx, {
     gcheck(d);
     need(params, "params"); need(u, "u"); need(x, "x"); need(cond, "cond"); need(y, "y");
@@ -168,6 +177,7 @@ extern "C" int paragan_gblock_bwd(paragan_ctx* ctx, const paragan_gblock_desc* d
                                   const void* x, const float* cond, const void* saved, const void* dy, void* dx,
                                   float* dcond, float* grads, void* ws) {
   if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
   PG_TRY(ctx, {
     gcheck(d);
     need(params, "params"); need(x, "x"); need(cond, "cond"); need(saved, "saved"); need(dy, "dy");
@@ -242,6 +252,7 @@ extern "C" int paragan_dblock_sizes(const paragan_dblock_desc* d, size_t* saved,
 extern "C" int paragan_dblock_fwd(paragan_ctx* ctx, const paragan_dblock_desc* d, const float* params, float* u,
                                   const void* x, void* y, void* saved, void* ws) {
   if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
   PG_TRY(ctx, {
     dcheck(d);
     need(params, "params"); need(u, "u"); need(x, "x"); need(y, "y"); need(saved, "saved"); need(ws, "ws");
@@ -260,6 +271,7 @@ extern "C" int paragan_dblock_bwd(paragan_ctx* ctx, const paragan_dblock_desc* d
                                   const void* x, const void* saved, const void* dy, void* dx, float* grads,
                                   void* ws) {
   if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
   PG_TRY(ctx, {
     dcheck(d);
     need(params, "params"); need(x, "x"); need(saved, "saved"); need(dy, "dy"); need(grads, "grads");
@@ -287,6 +299,7 @@ extern "C" int paragan_sn_ws_size(int64_t rows, int64_t cols, size_t* ws_bytes) 
 extern "C" int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t rows, int64_t cols, float* u,
                                      float* v, float* sigma, int n_iter, float eps, void* ws) {
   if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
   PG_TRY(ctx, {
     need(W, "W"); need(u, "u"); need(v, "v"); need(sigma, "sigma"); need(ws, "ws");
     aligned(ws, "ws");
@@ -345,6 +358,7 @@ extern "C" int paragan_attn_sizes(const paragan_attn_desc* d, size_t* saved, siz
 extern "C" int paragan_attn_fwd(paragan_ctx* ctx, const paragan_attn_desc* d, const float* params, float* u,
                                 const void* x, void* y, void* saved, void* ws) {
   if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
   PG_TRY(ctx, {
     acheck(d);
     need(params, "params"); need(u, "u"); need(x, "x"); need(y, "y"); need(saved, "saved"); need(ws, "ws");
@@ -362,6 +376,7 @@ extern "C" int paragan_attn_fwd(paragan_ctx* ctx, const paragan_attn_desc* d, co
 extern "C" int paragan_attn_bwd(paragan_ctx* ctx, const paragan_attn_desc* d, const float* params, const void* x,
                                 const void* saved, const void* dy, void* dx, float* grads, void* ws) {
   if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
   PG_TRY(ctx, {
     acheck(d);
     need(params, "params"); need(x, "x"); need(saved, "saved"); need(dy, "dy"); need(dx, "dx");
@@ -411,6 +426,7 @@ extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d
                                   paragan_net_state* D, const paragan_step_inputs* in, int32_t n_D, void* ws,
                                   float* losses_host) {
   if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
   try {
     check_arch(d);
     need_state(G, "G");
@@ -433,4 +449,41 @@ extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d
   } catch (const std::exception& e) {
     return fail(ctx, PARAGAN_EINVAL, e.what());
   }
+}
+
+// ------------------------------------------------------------ profiler
+extern "C" int paragan_profile(paragan_ctx* ctx, int enable) {
+  if (!ctx) return PARAGAN_EINVAL;
+  ctx->prof.on = enable != 0;
+  return PARAGAN_OK;
+}
+
+extern "C" int paragan_profile_read(paragan_ctx* ctx, paragan_kernel_stat* out, int32_t cap, int32_t* count) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    need(count, "count");
+    PG_HIP(hipStreamSynchronize(ctx->stream));
+    std::vector<paragan_kernel_stat> agg;
+    for (auto& r : ctx->prof.recs) {
+      float ms = 0.f;
+      PG_HIP(hipEventElapsedTime(&ms, r.a, r.b));
+      paragan_kernel_stat* k = nullptr;
+      for (auto& x : agg)
+        if (r.name == x.name) k = &x;
+      if (!k) {
+        agg.push_back(paragan_kernel_stat{});
+        k = &agg.back();
+        std::strncpy(k->name, r.name.c_str(), sizeof(k->name) - 1);
+      }
+      k->launches += 1;
+      k->total_ms += ms;
+      k->flops += r.flops;
+      ctx->prof.pool.push_back(r.a);
+      ctx->prof.pool.push_back(r.b);
+    }
+    ctx->prof.recs.clear();
+    *count = (int32_t)agg.size();
+    if (out)
+      for (int32_t i = 0; i < *count && i < cap; ++i) out[i] = agg[i];
+  })
 }

@@ -400,16 +400,19 @@ void attn_transpose(hipStream_t st, const AttnDims& a, const void* src, int ld, 
 void attn_fwd_core(hipStream_t st, const AttnDims& a, const void* qkv, const void* kp, const void* vt, void* o,
                    float* lse) {
   dim3 grid((unsigned)cdiv(a.HWp, 128), a.B);
+  ProfScope prof(st);
   PG_DV_DISPATCH(a.dv, hipLaunchKernelGGL(k_attn_fwd<DVc>, grid, dim3(256), 0, st, (const bf16_t*)qkv, a.Nqkv,
                                           (const bf16_t*)kp, (const bf16_t*)vt, a.HW, a.L, a.Lp, a.HWp,
                                           (bf16_t*)o, lse));
   PG_LAUNCH_CHECK();
+  prof.done("k_attn_fwd<" + std::to_string(a.dv) + ">", 2.0 * a.B * (double)a.HW * a.L * (a.dk + a.dv));
 }
 
 void attn_bwd_core(hipStream_t st, const AttnDims& a, const void* qkv, const void* o, const void* dO,
                    const void* kp, const void* kt, const void* vp, const void* qt, const void* dOt,
                    const float* lse, float* Dv, void* dk, void* dvv, void* dqkv) {
   dim3 gq((unsigned)cdiv(a.HWp, 128), a.B), gk((unsigned)cdiv(a.Lp, 128), a.B);
+  ProfScope prof(st);
   PG_DV_DISPATCH(a.dv, {
     hipLaunchKernelGGL(k_attn_dq<DVc>, gq, dim3(256), 0, st, (const bf16_t*)qkv, a.Nqkv, (const bf16_t*)kp,
                        (const bf16_t*)kt, (const bf16_t*)vp, (const bf16_t*)dO, lse, Dv, a.HW, a.L, a.Lp, a.HWp,
@@ -418,6 +421,9 @@ void attn_bwd_core(hipStream_t st, const AttnDims& a, const void* qkv, const voi
                        (const bf16_t*)kp, (const bf16_t*)vp, (const bf16_t*)dO, (const bf16_t*)dOt, lse, Dv, a.HW,
                        a.L, a.Lp, a.HWp, (bf16_t*)dk, (bf16_t*)dvv);
   });
+  // dQ: 2 passes of S and dP plus dQ; dK/dV: S, dP, dV, dK
+  prof.done("k_attn_bwd<" + std::to_string(a.dv) + ">",
+            2.0 * a.B * (double)a.HW * a.L * (3 * a.dk + 4 * a.dv));
   const int64_t n = (int64_t)a.B * a.L * (a.dk + a.dv);
   hipLaunchKernelGGL(k_attn_pool_bwd, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, (const bf16_t*)qkv,
                      (const bf16_t*)dk, (const bf16_t*)dvv, a.B, a.H, a.W, a.Nqkv, a.dk, a.dv, a.Lp,

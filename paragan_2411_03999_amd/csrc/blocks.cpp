@@ -354,14 +354,14 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   if (lsc) pack_weight(ex.st, f32, P.w("sc.w"), sn[2].sigma, cout, cin, 1, Cop, Cip, false, wpsc);
   // h = conv3x3([relu](x)) + b1
   ConvIn i1;
-  i1.x = x; i1.B = B; i1.Hx = H; i1.Wx = W; i1.C = Cip; i1.relu = preact;
+  i1.x = x; i1.B = B; i1.Hx = H; i1.Wx = W; i1.C = Cip; i1.relu = preact; i1.c_real = cin;
   ConvOut o1;
   o1.y = h; o1.y_f32 = f32; o1.yC = Cop; o1.n_real = cout; o1.bias = P.w("conv1.b");
   conv_fwd(ex.st, f32, i1, H, W, 3, wp1, Cop, o1);
   // skip = conv1x1([avgpool](x)) + bsc, fp32
   if (lsc) {
     ConvIn si;
-    si.x = x; si.B = B; si.Hx = H; si.Wx = W; si.C = Cip;
+    si.x = x; si.B = B; si.Hx = H; si.Wx = W; si.C = Cip; si.c_real = cin;
     if (down) { si.gather = G_POOL2; si.gscale = 0.25f; }
     ConvOut so;
     so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b");
@@ -408,7 +408,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   GradIn g1;
   g1.g = w.dh; g1.Hs = H; g1.Ws = W; g1.C = Cop;
   ConvIn a1;
-  a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.relu = preact;
+  a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.relu = preact; a1.c_real = cin;
   if (wgrad) {
     conv_wgrad(ex.st, f32, g1, a1, H, W, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
     colsum(ex.st, f32, w.dh, M, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
@@ -418,7 +418,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     GradIn gs;
     gs.g = dy; gs.Hs = Ho; gs.Ws = Wo; gs.C = Cop;
     ConvIn as;
-    as.x = x; as.B = B; as.Hx = H; as.Wx = W; as.C = Cip;
+    as.x = x; as.B = B; as.Hx = H; as.Wx = W; as.C = Cip; as.c_real = cin;
     if (down) { as.gather = G_POOL2; as.gscale = 0.25f; }
     if (wgrad) {
       conv_wgrad(ex.st, f32, gs, as, Ho, Wo, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);

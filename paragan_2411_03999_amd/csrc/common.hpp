@@ -76,11 +76,61 @@ PG_DEV double wave_sum_d(double v) {
 }  // namespace pg
 
 // ---------------------------------------------------------------- host side
+#include <vector>
+
+namespace pg {
+// Opt-in launch profiler: an event pair around each instrumented launch on
+// the context's stream, with the launch's algorithmic FLOPs.  Read (and
+// reset) through paragan_profile_read once the stream is idle.
+struct ProfRec {
+  std::string name;
+  double flops;
+  hipEvent_t a, b;
+};
+struct Profiler {
+  bool on = false;
+  std::vector<ProfRec> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t ev() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e;
+    (void)hipEventCreate(&e);
+    return e;
+  }
+};
+// set by the C-ABI entry points for the duration of a call
+extern thread_local Profiler* t_prof;
+
+struct ProfScope {
+  Profiler* p;
+  hipStream_t st;
+  hipEvent_t a = nullptr;
+  ProfScope(hipStream_t s) : p(t_prof), st(s) {
+    if (p && p->on) {
+      a = p->ev();
+      (void)hipEventRecord(a, st);
+    }
+  }
+  void done(const std::string& name, double flops) {
+    if (!a) return;
+    hipEvent_t b = p->ev();
+    (void)hipEventRecord(b, st);
+    p->recs.push_back(ProfRec{name, flops, a, b});
+    a = nullptr;
+  }
+};
+}  // namespace pg
+
 struct paragan_ctx {
   hipStream_t stream = nullptr;
   int device = 0;
   int n_cu = 0;
   std::string err;
+  pg::Profiler prof;
 };
 
 namespace pg {

@@ -19,6 +19,8 @@
 
 namespace pg {
 
+thread_local Profiler* t_prof = nullptr;
+
 // ------------------------------------------------------------ A operand
 struct AOp {
   const void* x;
@@ -381,8 +383,19 @@ __global__ __launch_bounds__(256) void k_conv_simt(ConvK k) {
 }
 
 // --------------------------------------------------------------- launcher
+static std::string kname(const char* base, std::initializer_list<int> args) {
+  std::string n = std::string(base) + "<";
+  bool first = true;
+  for (int a : args) {
+    n += (first ? "" : ",") + std::to_string(a);
+    first = false;
+  }
+  return n + ">";
+}
+
+// returns the launched kernel's name (template instance)
 template <int WM, int WN, int TM, int TN>
-static void launch_mfma_cfg(hipStream_t s, ConvK& k, int gather, bool aff, bool relu) {
+static std::string launch_mfma_cfg(hipStream_t s, ConvK& k, int gather, bool aff, bool relu) {
   constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
   k.tiles_m = (int)cdiv(k.a.M, BM);
   k.tiles_n = (int)cdiv(k.Np, BN);
@@ -390,7 +403,7 @@ static void launch_mfma_cfg(hipStream_t s, ConvK& k, int gather, bool aff, bool 
 #define PG_CONV_CASE(G, A_, R_)                                                   \
   if (gather == G && aff == A_ && relu == R_) {                                   \
     hipLaunchKernelGGL((k_conv_mfma<WM, WN, TM, TN, G, A_, R_>), grid, block, 0, s, k); \
-    return;                                                                       \
+    return kname("k_conv_mfma", {WM, WN, TM, TN, G, A_, R_});                   \
   }
   PG_CONV_CASE(G_DIRECT, false, false)
   PG_CONV_CASE(G_DIRECT, false, true)
@@ -412,6 +425,8 @@ void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
   k.o = out;
   if (k.a.M == 0) return;
   const bool aff = in.mean != nullptr;
+  ProfScope prof(s);
+  const double flops = 2.0 * (double)k.a.M * out.n_real * R * R * (in.c_real ? in.c_real : in.C);
   if (f32) {
     k.cchunks = in.C / 16;
     k.ksteps = R * R * k.cchunks;
@@ -422,6 +437,7 @@ void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
   if (in.gather == G && aff == A_ && (bool)in.relu == R_) {                         \
     hipLaunchKernelGGL((k_conv_simt<G, A_, R_>), grid, block, 0, s, k);             \
     PG_LAUNCH_CHECK();                                                              \
+    prof.done(kname("k_conv_simt", {G, A_, R_}), flops);                            \
     return;                                                                         \
   }
     PG_SIMT_CASE(G_DIRECT, false, false)
@@ -437,15 +453,17 @@ void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
   k.ksteps = R * R * k.cchunks;
   // tile choice: 128x128 when N is a multiple of 128, else 256x96 / 128x64
   // shapes so that BigGAN's 96-multiple widths waste no MMA columns.
+  std::string name;
   if (Np % 128 == 0)
-    launch_mfma_cfg<2, 2, 2, 2>(s, k, in.gather, aff, in.relu);
+    name = launch_mfma_cfg<2, 2, 2, 2>(s, k, in.gather, aff, in.relu);
   else if (Np % 96 == 0)
-    launch_mfma_cfg<4, 1, 2, 3>(s, k, in.gather, aff, in.relu);
+    name = launch_mfma_cfg<4, 1, 2, 3>(s, k, in.gather, aff, in.relu);
   else if (Np <= 64)
-    launch_mfma_cfg<4, 1, 1, 2>(s, k, in.gather, aff, in.relu);
+    name = launch_mfma_cfg<4, 1, 1, 2>(s, k, in.gather, aff, in.relu);
   else
-    launch_mfma_cfg<2, 2, 2, 2>(s, k, in.gather, aff, in.relu);
+    name = launch_mfma_cfg<2, 2, 2, 2>(s, k, in.gather, aff, in.relu);
   PG_LAUNCH_CHECK();
+  prof.done(name, flops);
 }
 
 // ================================================================ wgrad
@@ -772,12 +790,15 @@ void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in, int 
   const bool aff = in.mean != nullptr;
   dim3 grid(k.splits * k.tiles_n * k.tiles_k), block(256);
   bool done = false;
+  ProfScope prof(s);
+  std::string name;
 #define PG_WG_CASE(G, A_, R_)                                                   \
   if (!done && in.gather == G && aff == A_ && (bool)in.relu == R_) {            \
     if (f32)                                                                    \
       hipLaunchKernelGGL((k_wgrad_simt<G, A_, R_>), grid, block, 0, s, k);      \
     else                                                                        \
       hipLaunchKernelGGL((k_wgrad_mfma<G, A_, R_>), grid, block, 0, s, k);      \
+    name = kname(f32 ? "k_wgrad_simt" : "k_wgrad_mfma", {G, A_, R_});            \
     done = true;                                                                \
   }
   PG_WG_CASE(G_DIRECT, false, false)
@@ -789,6 +810,7 @@ void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in, int 
 #undef PG_WG_CASE
   if (!done) throw Error{-2, "conv_wgrad: unsupported prologue combination"};
   PG_LAUNCH_CHECK();
+  prof.done(name, 2.0 * (double)k.a.M * (g.n_real ? g.n_real : Np) * R * R * (in.c_real ? in.c_real : in.C));
   if (k.splits > 1 || g.gscale != 1.f) {
     hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)cdiv(nout, 256)), dim3(256), 0, s,
                        k.part, k.splits, nout, g.gscale, dw);

@@ -24,7 +24,9 @@ void img_to_bf16(hipStream_t st, const float* img, int64_t npix, int Cp, void* o
 }
 
 // --------------------------------------------------- generator output layer
-// a = relu((x - mean) * scale + shift) (per channel), img = tanh(conv3x3(a) + b)
+// a = relu((x - mean) * scale + shift) (per channel), img = tanh(conv3x3(a) + b).
+// Each thread computes 4 horizontally adjacent pixels, so every staged
+// weight and every loaded input serves up to 4 outputs.
 __global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* x, int B, int H, int W, int C, int Cp,
                                                    const float* mean, const float* scale, const float* shift,
                                                    const float* Wt, const float* sigma, const float* bias,
@@ -40,35 +42,58 @@ __global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* x, int B, int H
     sm[2 * C + i] = shift[i];
   }
   __syncthreads();
-  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (p >= (int64_t)B * H * W) return;
-  const int w = (int)(p % W);
-  const int64_t t = p / W;
-  const int h = (int)(t % H);
-  const int b = (int)(t / H);
-  float acc[3] = {bias[0], bias[1], bias[2]};
+  const int Wq = (W + 3) / 4;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)B * H * Wq) return;
+  const int w0 = (int)(t % Wq) * 4;
+  const int64_t bh = t / Wq;
+  const int h = (int)(bh % H);
+  const int b = (int)(bh / H);
+  float acc[4][3];
+  for (int j = 0; j < 4; ++j)
+    for (int co = 0; co < 3; ++co) acc[j][co] = bias[co];
   for (int r = 0; r < 3; ++r) {
     const int ih = h + r - 1;
     if (ih < 0 || ih >= H) continue;
-    for (int s = 0; s < 3; ++s) {
-      const int iw = w + s - 1;
-      if (iw < 0 || iw >= W) continue;
-      const bf16_t* xr = x + (((int64_t)b * H + ih) * W + iw) * Cp;
-      const int tap = r * 3 + s;
-      for (int c = 0; c < C; c += 8) {
-        float f[8];
-        unpack8(*reinterpret_cast<const uint4*>(xr + c), f);
+    const bf16_t* xrow = x + ((int64_t)b * H + ih) * W * Cp;
+    for (int c = 0; c < C; c += 8) {
+      float a[6][8];
+#pragma unroll
+      for (int q = 0; q < 6; ++q) {
+        const int iw = w0 - 1 + q;
+        if (iw < 0 || iw >= W) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) a[q][e] = 0.f;
+          continue;
+        }
+        unpack8(*reinterpret_cast<const uint4*>(xrow + (int64_t)iw * Cp + c), a[q]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          a[q][e] = (c + e < C) ? fmaxf((a[q][e] - sm[c + e]) * sm[C + c + e] + sm[2 * C + c + e], 0.f) : 0.f;
+      }
+#pragma unroll
+      for (int s_ = 0; s_ < 3; ++s_)
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           if (c + e >= C) break;
-          const float a = fmaxf((f[e] - sm[c + e]) * sm[C + c + e] + sm[2 * C + c + e], 0.f);
+          const float w0_ = sw[(0 * 9 + r * 3 + s_) * C + c + e];
+          const float w1_ = sw[(1 * 9 + r * 3 + s_) * C + c + e];
+          const float w2_ = sw[(2 * 9 + r * 3 + s_) * C + c + e];
 #pragma unroll
-          for (int co = 0; co < 3; ++co) acc[co] = fmaf(a, sw[(co * 9 + tap) * C + c + e], acc[co]);
+          for (int j = 0; j < 4; ++j) {
+            const float av = a[j + s_][e];
+            acc[j][0] = fmaf(av, w0_, acc[j][0]);
+            acc[j][1] = fmaf(av, w1_, acc[j][1]);
+            acc[j][2] = fmaf(av, w2_, acc[j][2]);
+          }
         }
-      }
     }
   }
-  for (int co = 0; co < 3; ++co) img[p * 3 + co] = tanhf(acc[co]);
+  for (int j = 0; j < 4; ++j) {
+    if (w0 + j >= W) break;
+    const int64_t p = ((int64_t)b * H + h) * W + w0 + j;
+    for (int co = 0; co < 3; ++co) img[p * 3 + co] = tanhf(acc[j][co]);
+  }
 }
 
 // da[p][c] = sum_{tap, co} dt[p - tap][co] * W[co][tap][c] / sigma,
@@ -108,64 +133,93 @@ __global__ __launch_bounds__(256) void k_ghead_dgrad(const float* dimg, int ldd,
   da[i] = s_;
 }
 
-// per pixel chunk: part[chunk][co][tap][c] = sum dt[p][co] a[p + tap][c];
-// part[chunk][27C + co] = sum dt[p][co]   (bias)
+// Weight gradient of the output layer.  Per chunk of kHeadRows pixels:
+//   part[chunk][co][tap][c] = sum_p dt[p][co] a[p + tap][c],
+//   part[chunk][27C + co]   = sum_p dt[p][co]          (bias),
+// with dt = dimg (1 - img^2) staged in LDS; a thread owns (tap, c) pairs
+// (consecutive c across lanes: coalesced loads of x).  Chunks are then
+// summed in a fixed order.
+constexpr int kHeadRows = 512;
+
 __global__ __launch_bounds__(256) void k_ghead_wgrad(const float* dimg, int ldd, const float* img, const bf16_t* x,
                                                      int B, int H, int W, int C, int Cp, const float* mean,
-                                                     const float* scale, const float* shift, int rows_per,
-                                                     float* part) {
+                                                     const float* scale, const float* shift, float* part) {
+  __shared__ float sdt[kHeadRows][3];
   const int64_t M = (int64_t)B * H * W;
-  const int64_t p0 = (int64_t)blockIdx.x * rows_per;
-  const int64_t p1 = p0 + rows_per < M ? p0 + rows_per : M;
+  const int64_t p0 = (int64_t)blockIdx.x * kHeadRows;
+  const int np = (int)(p0 + kHeadRows < M ? kHeadRows : M - p0);
   const int nout = 27 * C + 3;
-  for (int o = threadIdx.x; o < nout; o += 256) {
-    float acc = 0.f;
-    if (o >= 27 * C) {
-      const int co = o - 27 * C;
-      for (int64_t p = p0; p < p1; ++p) {
-        const float y = img[p * 3 + co];
-        acc += dimg[p * ldd + co] * (1.f - y * y);
-      }
-    } else {
-      const int c = o % C;
-      const int tap = (o / C) % 9;
-      const int co = o / (9 * C);
-      const int r = tap / 3, s = tap % 3;
-      const float mu = mean[c], sc = scale[c], sh = shift[c];
-      for (int64_t p = p0; p < p1; ++p) {
-        const int w = (int)(p % W);
-        const int64_t t = p / W;
-        const int h = (int)(t % H);
-        const int b = (int)(t / H);
-        const int ih = h + r - 1, iw = w + s - 1;
-        if (ih < 0 || ih >= H || iw < 0 || iw >= W) continue;
-        const float y = img[p * 3 + co];
-        const float dt = dimg[p * ldd + co] * (1.f - y * y);
+  for (int i = threadIdx.x; i < np; i += 256) {
+    const int64_t p = p0 + i;
+    for (int co = 0; co < 3; ++co) {
+      const float y = img[p * 3 + co];
+      sdt[i][co] = dimg[p * ldd + co] * (1.f - y * y);
+    }
+  }
+  __syncthreads();
+  float* out = part + (int64_t)blockIdx.x * nout;
+  if (threadIdx.x < 3) {
+    float sb = 0.f;
+    for (int i = 0; i < np; ++i) sb += sdt[i][threadIdx.x];
+    out[27 * C + threadIdx.x] = sb;
+  }
+  const int w00 = (int)(p0 % W);
+  const int64_t t0 = p0 / W;
+  const int h00 = (int)(t0 % H);
+  const int b00 = (int)(t0 / H);
+  for (int k = threadIdx.x; k < 9 * C; k += 256) {
+    const int c = k % C, tap = k / C;
+    const int r = tap / 3, s_ = tap % 3;
+    const float mu = mean[c], sc = scale[c], sh = shift[c];
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f;
+    int b = b00, h = h00, w = w00;
+    for (int i = 0; i < np; ++i) {
+      const int ih = h + r - 1, iw = w + s_ - 1;
+      if (ih >= 0 && ih < H && iw >= 0 && iw < W) {
         const float a = fmaxf((bf2f(x[(((int64_t)b * H + ih) * W + iw) * Cp + c]) - mu) * sc + sh, 0.f);
-        acc = fmaf(dt, a, acc);
+        a0 = fmaf(sdt[i][0], a, a0);
+        a1 = fmaf(sdt[i][1], a, a1);
+        a2 = fmaf(sdt[i][2], a, a2);
+      }
+      if (++w == W) {
+        w = 0;
+        if (++h == H) { h = 0; ++b; }
       }
     }
-    part[(int64_t)blockIdx.x * nout + o] = acc;
+    out[(0 * 9 + tap) * C + c] = a0;
+    out[(1 * 9 + tap) * C + c] = a1;
+    out[(2 * 9 + tap) * C + c] = a2;
   }
 }
 
-__global__ void k_sum_parts(const float* part, int nparts, int n, float* out, float* out_tail, int ntail) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= n + ntail) return;
+// fixed-order sum of the chunk partials; the last 3 entries are the bias
+__global__ __launch_bounds__(1024) void k_ghead_fin(const float* part, int nch, int n, float* dw, float* dbias) {
+  __shared__ float sh[16][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int o = blockIdx.x * 64 + lane;
   float s = 0.f;
-  for (int j = 0; j < nparts; ++j) s += part[(int64_t)j * (n + ntail) + i];
-  if (i < n) out[i] = s;
-  else out_tail[i - n] = s;
+  if (o < n)
+    for (int j = wv; j < nch; j += 16) s += part[(int64_t)j * n + o];
+  sh[wv][lane] = s;
+  __syncthreads();
+  if (wv == 0 && o < n) {
+    float t = 0.f;
+    for (int i = 0; i < 16; ++i) t += sh[i][lane];
+    if (o < n - 3) dw[o] = t;
+    else dbias[o - (n - 3)] = t;
+  }
 }
 
-size_t ghead_ws_bytes(int64_t M, int C) { return align256((size_t)cdiv(M, 4096) * (27 * C + 3) * 4); }
+size_t ghead_ws_bytes(int64_t M, int C) { return align256((size_t)cdiv(M, kHeadRows) * (27 * C + 3) * 4); }
 
 void ghead_fwd(hipStream_t st, const void* x, int B, int H, int W, int C, int Cp, const float* mean,
                const float* scale, const float* shift, const float* Wt, const float* sigma, const float* bias,
                float* img) {
   const int64_t M = (int64_t)B * H * W;
   const size_t sh = (27 * C + 3 * C) * sizeof(float);
-  hipLaunchKernelGGL(k_ghead_fwd, dim3((unsigned)cdiv(M, 256)), dim3(256), sh, st, (const bf16_t*)x, B, H, W, C,
+  const int64_t nthr = (int64_t)B * H * ((W + 3) / 4);
+  (void)M;
+  hipLaunchKernelGGL(k_ghead_fwd, dim3((unsigned)cdiv(nthr, 256)), dim3(256), sh, st, (const bf16_t*)x, B, H, W, C,
                      Cp, mean, scale, shift, Wt, sigma, bias, img);
   PG_LAUNCH_CHECK();
 }
@@ -176,12 +230,11 @@ void ghead_bwd(hipStream_t st, const float* dimg, int ldd, const float* img, con
   const int64_t M = (int64_t)B * H * W;
   hipLaunchKernelGGL(k_ghead_dgrad, dim3((unsigned)cdiv(M * Cp, 256)), dim3(256), 27 * C * sizeof(float), st,
                      dimg, ldd, img, B, H, W, C, Cp, Wt, sigma, da);
-  const int rows_per = 4096;
-  const int nch = (int)cdiv(M, rows_per);
+  const int nch = (int)cdiv(M, kHeadRows);
   hipLaunchKernelGGL(k_ghead_wgrad, dim3(nch), dim3(256), 0, st, dimg, ldd, img, (const bf16_t*)x, B, H, W, C, Cp,
-                     mean, scale, shift, rows_per, (float*)ws);
-  hipLaunchKernelGGL(k_sum_parts, dim3((unsigned)cdiv(27 * C + 3, 256)), dim3(256), 0, st, (const float*)ws, nch,
-                     27 * C, dwsn, dbias, 3);
+                     mean, scale, shift, (float*)ws);
+  hipLaunchKernelGGL(k_ghead_fin, dim3((unsigned)cdiv(27 * C + 3, 64)), dim3(1024), 0, st, (const float*)ws, nch,
+                     27 * C + 3, dwsn, dbias);
   PG_LAUNCH_CHECK();
 }
 

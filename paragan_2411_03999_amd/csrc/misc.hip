@@ -235,107 +235,135 @@ void sn_bwd(hipStream_t st, const float* dwp, const float* W, const float* u, co
 }
 
 // ------------------------------------------------------ column sums
-// part[chunk][c] = sum over rows of the chunk; then out[c] = sum of chunks.
+// Two-level fixed-order reduction over rows.  Level 1: block (chunk of
+// kRows rows, 64 channels); its 4 waves take rows r = wave (mod 4), lanes
+// are consecutive channels (coalesced), the 4 wave sums combine in order.
+// Level 2: one block per 64 channels; 16 waves take chunks j = wave
+// (mod 16), combined in order.
+constexpr int kRows = 2048;
+
 template <typename T>
-__global__ void k_colsum_part(const T* x, int64_t M, int C, int ldc, int rows_per, float* part) {
-  const int64_t r0 = (int64_t)blockIdx.x * rows_per;
-  int64_t r1 = r0 + rows_per;
-  if (r1 > M) r1 = M;
-  for (int c = threadIdx.x; c < C; c += blockDim.x) {
-    float s = 0.f;
-    for (int64_t r = r0; r < r1; ++r) s += ld<T>(x, r * ldc + c);
-    part[(int64_t)blockIdx.x * C + c] = s;
-  }
-}
-__global__ void k_colsum_fin(const float* part, int nch, int C, float scale, float* out) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= C) return;
+__global__ __launch_bounds__(256) void k_colsum_part(const T* x, int64_t M, int C, int ldc, float* part) {
+  __shared__ float sh[4][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c = blockIdx.y * 64 + lane;
+  const int64_t r0 = (int64_t)blockIdx.x * kRows;
+  const int64_t r1 = r0 + kRows < M ? r0 + kRows : M;
   float s = 0.f;
-  for (int j = 0; j < nch; ++j) s += part[(int64_t)j * C + c];
-  out[c] = s * scale;
+  if (c < C)
+    for (int64_t r = r0 + wv; r < r1; r += 4) s += ld<T>(x, r * ldc + c);
+  sh[wv][lane] = s;
+  __syncthreads();
+  if (wv == 0 && c < C) part[(int64_t)blockIdx.x * C + c] = (sh[0][lane] + sh[1][lane]) + (sh[2][lane] + sh[3][lane]);
 }
 
-size_t colsum_ws_bytes(int64_t M, int C) {
-  return align256((size_t)cdiv(M, 256) * C * 4);
+__global__ __launch_bounds__(1024) void k_colsum_fin(const float* part, int nch, int C, float scale, float* out) {
+  __shared__ float sh[16][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  float s = 0.f;
+  if (c < C)
+    for (int j = wv; j < nch; j += 16) s += part[(int64_t)j * C + c];
+  sh[wv][lane] = s;
+  __syncthreads();
+  if (wv == 0 && c < C) {
+    float t = 0.f;
+    for (int i = 0; i < 16; ++i) t += sh[i][lane];
+    out[c] = t * scale;
+  }
 }
+
+size_t colsum_ws_bytes(int64_t M, int C) { return align256((size_t)cdiv(M, kRows) * C * 4); }
 
 void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float scale, float* out,
             void* ws) {
-  const int rows_per = 256;
-  const int nch = (int)cdiv(M, rows_per);
+  const int nch = (int)cdiv(M, kRows);
   float* part = (float*)ws;
-  const int nt = C >= 256 ? 256 : (int)cdiv(C, 64) * 64;
+  dim3 g1(nch, (unsigned)cdiv(C, 64));
   if (f32)
-    hipLaunchKernelGGL(k_colsum_part<float>, dim3(nch), dim3(nt), 0, st, (const float*)x, M, C, ldc,
-                       rows_per, part);
+    hipLaunchKernelGGL(k_colsum_part<float>, g1, dim3(256), 0, st, (const float*)x, M, C, ldc, part);
   else
-    hipLaunchKernelGGL(k_colsum_part<bf16_t>, dim3(nch), dim3(nt), 0, st, (const bf16_t*)x, M, C, ldc,
-                       rows_per, part);
-  hipLaunchKernelGGL(k_colsum_fin, dim3((unsigned)cdiv(C, 256)), dim3(256), 0, st, part, nch, C, scale,
-                     out);
+    hipLaunchKernelGGL(k_colsum_part<bf16_t>, g1, dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, part);
+  hipLaunchKernelGGL(k_colsum_fin, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, part, nch, C, scale, out);
   PG_LAUNCH_CHECK();
 }
 
 // ------------------------------------------------------- batch norm
-// Per-chunk (mean, M2) with two passes over the chunk, merged per channel in
-// chunk order with Chan's formula in fp64.
+// Per chunk of kRows rows: mean by a first pass, M2 = sum (x - mean)^2 by a
+// second (both fixed-order as in the column sums); chunks merge with Chan's
+// formula in fp64, in a fixed order.
 template <typename T>
-__global__ void k_bn_part(const T* x, int64_t M, int C, int ldc, int rows_per, float* pmean,
-                          float* pm2) {
-  const int64_t r0 = (int64_t)blockIdx.x * rows_per;
-  int64_t r1 = r0 + rows_per;
-  if (r1 > M) r1 = M;
-  const float n = (float)(r1 - r0);
-  for (int c = threadIdx.x; c < C; c += blockDim.x) {
-    float s = 0.f;
-    for (int64_t r = r0; r < r1; ++r) s += ld<T>(x, r * ldc + c);
-    const float mean = s / n;
-    float m2 = 0.f;
-    for (int64_t r = r0; r < r1; ++r) {
+__global__ __launch_bounds__(256) void k_bn_part(const T* x, int64_t M, int C, int ldc, float* pmean, float* pm2) {
+  __shared__ float sh[4][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c = blockIdx.y * 64 + lane;
+  const int64_t r0 = (int64_t)blockIdx.x * kRows;
+  const int64_t r1 = r0 + kRows < M ? r0 + kRows : M;
+  float s = 0.f;
+  if (c < C)
+    for (int64_t r = r0 + wv; r < r1; r += 4) s += ld<T>(x, r * ldc + c);
+  sh[wv][lane] = s;
+  __syncthreads();
+  const float mean = ((sh[0][lane] + sh[1][lane]) + (sh[2][lane] + sh[3][lane])) / (float)(r1 - r0);
+  __syncthreads();
+  float m2 = 0.f;
+  if (c < C)
+    for (int64_t r = r0 + wv; r < r1; r += 4) {
       const float d = ld<T>(x, r * ldc + c) - mean;
       m2 = fmaf(d, d, m2);
     }
+  sh[wv][lane] = m2;
+  __syncthreads();
+  if (wv == 0 && c < C) {
     pmean[(int64_t)blockIdx.x * C + c] = mean;
-    pm2[(int64_t)blockIdx.x * C + c] = m2;
+    pm2[(int64_t)blockIdx.x * C + c] = (sh[0][lane] + sh[1][lane]) + (sh[2][lane] + sh[3][lane]);
   }
 }
 
-__global__ void k_bn_fin(const float* pmean, const float* pm2, int nch, int64_t M, int rows_per, int C,
-                         float eps, float* mean, float* rstd) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= C) return;
+PG_DEV void chan_merge(double& n, double& mu, double& m2, double nb, double mb, double m2b) {
+  if (nb <= 0.0) return;
+  const double nn = n + nb;
+  const double d = mb - mu;
+  mu += d * nb / nn;
+  m2 += m2b + d * d * n * nb / nn;
+  n = nn;
+}
+
+__global__ __launch_bounds__(1024) void k_bn_fin(const float* pmean, const float* pm2, int nch, int64_t M, int C,
+                                                 float eps, float* mean, float* rstd) {
+  __shared__ double sn[16][64], smu[16][64], sm2[16][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
   double n = 0.0, mu = 0.0, m2 = 0.0;
-  for (int j = 0; j < nch; ++j) {
-    const double nb = (double)std::min<int64_t>(rows_per, M - (int64_t)j * rows_per);
-    const double mb = pmean[(int64_t)j * C + c];
-    const double d = mb - mu;
-    const double nn = n + nb;
-    mu += d * nb / nn;
-    m2 += pm2[(int64_t)j * C + c] + d * d * n * nb / nn;
-    n = nn;
+  if (c < C)
+    for (int j = wv; j < nch; j += 16) {
+      const double nb = (double)std::min<int64_t>(kRows, M - (int64_t)j * kRows);
+      chan_merge(n, mu, m2, nb, pmean[(int64_t)j * C + c], pm2[(int64_t)j * C + c]);
+    }
+  sn[wv][lane] = n; smu[wv][lane] = mu; sm2[wv][lane] = m2;
+  __syncthreads();
+  if (wv == 0 && c < C) {
+    double tn = 0.0, tmu = 0.0, tm2 = 0.0;
+    for (int i = 0; i < 16; ++i) chan_merge(tn, tmu, tm2, sn[i][lane], smu[i][lane], sm2[i][lane]);
+    mean[c] = (float)tmu;
+    rstd[c] = (float)(1.0 / sqrt(tm2 / tn + (double)eps));
   }
-  const double var = m2 / n;
-  mean[c] = (float)mu;
-  rstd[c] = (float)(1.0 / sqrt(var + (double)eps));
 }
 
-size_t bn_stats_ws_bytes(int64_t M, int C) { return 2 * align256((size_t)cdiv(M, 512) * C * 4); }
+size_t bn_stats_ws_bytes(int64_t M, int C) { return 2 * align256((size_t)cdiv(M, kRows) * C * 4); }
 
 void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float eps, float* mean,
               float* rstd, void* ws) {
-  const int rows_per = 512;
-  const int nch = (int)cdiv(M, rows_per);
+  const int nch = (int)cdiv(M, kRows);
   float* pmean = (float*)ws;
   float* pm2 = (float*)((char*)ws + align256((size_t)nch * C * 4));
-  const int nt = C >= 256 ? 256 : (int)cdiv(C, 64) * 64;
+  dim3 g1(nch, (unsigned)cdiv(C, 64));
   if (f32)
-    hipLaunchKernelGGL(k_bn_part<float>, dim3(nch), dim3(nt), 0, st, (const float*)x, M, C, ldc, rows_per,
-                       pmean, pm2);
+    hipLaunchKernelGGL(k_bn_part<float>, g1, dim3(256), 0, st, (const float*)x, M, C, ldc, pmean, pm2);
   else
-    hipLaunchKernelGGL(k_bn_part<bf16_t>, dim3(nch), dim3(nt), 0, st, (const bf16_t*)x, M, C, ldc,
-                       rows_per, pmean, pm2);
-  hipLaunchKernelGGL(k_bn_fin, dim3((unsigned)cdiv(C, 256)), dim3(256), 0, st, pmean, pm2, nch, M,
-                     rows_per, C, eps, mean, rstd);
+    hipLaunchKernelGGL(k_bn_part<bf16_t>, g1, dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, pmean, pm2);
+  hipLaunchKernelGGL(k_bn_fin, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, pmean, pm2, nch, M, C, eps, mean,
+                     rstd);
   PG_LAUNCH_CHECK();
 }
 

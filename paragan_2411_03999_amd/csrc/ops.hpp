@@ -23,6 +23,7 @@ struct ConvIn {
   const float* shift = nullptr;
   int tab_stride = 0;                 // C for per-sample tables, 0 for per-channel
   int relu = 0;
+  int c_real = 0;                     // real input channels (0: = C); for FLOP counts
 };
 
 // Epilogue: v = (acc * (*acc_scale) + bias[n]) * (mask > 0) + res_scale * res,
@@ -54,6 +55,7 @@ struct GradIn {
   int Hs = 0, Ws = 0, C = 0;   // source dims; C = channel stride (= Np)
   int gather = G_DIRECT;       // G_DIRECT or G_UP2
   float gscale = 1.f;          // applied to the result
+  int n_real = 0;              // real gradient channels (0: = Np); for FLOP counts
 };
 
 // dw[n][r][s][c] = gscale * sum_m g[m][n] * A[m][(r,s,c)], A = im2col(in).

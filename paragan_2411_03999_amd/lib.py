@@ -65,8 +65,15 @@ class StepInputs(C.Structure):
                 ("z_g", C.c_void_p), ("y_g", C.c_void_p)]
 
 
+class KernelStat(C.Structure):
+    _fields_ = [("name", C.c_char * 64), ("launches", C.c_int64), ("total_ms", C.c_double),
+                ("flops", C.c_double)]
+
+
 _P = C.c_void_p
 _SIGS = {
+    "paragan_profile": (C.c_int, [_P, C.c_int]),
+    "paragan_profile_read": (C.c_int, [_P, _P, C.c_int32, C.POINTER(C.c_int32)]),
     "paragan_create": (C.c_int, [C.POINTER(_P), _P]),
     "paragan_destroy": (None, [_P]),
     "paragan_last_error": (C.c_char_p, [_P]),
@@ -287,6 +294,20 @@ def paragan_train_step(ctx, desc, G, D, inputs, n_D, ws, losses):
     """G, D: NetState; inputs: StepInputs; losses: ctypes float array (n_D+1)."""
     return load().paragan_train_step(ctx.h, C.byref(desc), C.byref(G), C.byref(D), C.byref(inputs), n_D,
                                      _ptr(ws), losses)
+
+
+def paragan_profile(ctx, enable):
+    return ctx.check(load().paragan_profile(ctx.h, int(bool(enable))))
+
+
+def paragan_profile_read(ctx, cap=256):
+    """Per-kernel launch statistics since the last read (list of dicts);
+    the records are consumed."""
+    arr = (KernelStat * cap)()
+    n = C.c_int32()
+    ctx.check(load().paragan_profile_read(ctx.h, arr, cap, C.byref(n)))
+    return [dict(name=a.name.decode(), launches=a.launches, total_ms=a.total_ms, flops=a.flops)
+            for a in arr[:min(n.value, cap)]]
 
 
 # ---------------------------------------------------------- tensor marshalling
