@@ -88,6 +88,8 @@ void GBlock::plan_saved(Arena& a) {
   mean2 = a.f32(Cop); rstd2 = a.f32(Cop);
   gain2 = a.f32((size_t)B * Cop); bias2 = a.f32((size_t)B * Cop); scale2 = a.f32((size_t)B * Cop);
   h1 = a.bytes((size_t)B * 4 * H * W * Cop * e);
+  a1 = a.bytes((size_t)B * H * W * Cip * e);
+  a2 = a.bytes((size_t)B * 4 * H * W * Cop * e);
 }
 
 struct GWsF {
@@ -172,10 +174,10 @@ void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* co
   bn_stats(ex.st, f32, x, M1, cin, Cip, bn_eps, mean1, rstd1, w.bn);
   cbn_tables(ex.st, cond, dc, P.w("bn1.gain"), P.w("bn1.bias"), sn[0].sigma, sn[1].sigma, nullptr, nullptr,
              rstd1, B, cin, Cip, gain1, bias1, scale1);
-  // h1 = conv3x3(up2(relu(cbn1(x)))) + b1
+  // h1 = conv3x3(up2(a1)) + b1, a1 = relu(cbn1(x)) (stored once, bf16)
+  bn_apply(ex.st, f32, x, M1, H * W, cin, Cip, mean1, scale1, bias1, Cip, true, a1);
   ConvIn in;
-  in.x = x; in.B = B; in.Hx = H; in.Wx = W; in.C = Cip;
-  in.gather = G_UP2; in.mean = mean1; in.scale = scale1; in.shift = bias1; in.tab_stride = Cip; in.relu = 1;
+  in.x = a1; in.B = B; in.Hx = H; in.Wx = W; in.C = Cip; in.gather = G_UP2;
   ConvOut o;
   o.y = h1; o.y_f32 = f32; o.yC = Cop; o.n_real = cout; o.bias = P.w("conv1.b");
   conv_fwd(ex.st, f32, in, 2 * H, 2 * W, 3, wp1, Cop, o);
@@ -189,10 +191,10 @@ void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* co
   ConvOut so;
   so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b");
   conv_fwd(ex.st, f32, si, H, W, 1, wpsc, Cop, so);
-  // y = conv3x3(relu(cbn2(h1))) + b2 + up2(skip)
+  // y = conv3x3(a2) + b2 + up2(skip), a2 = relu(cbn2(h1))
+  bn_apply(ex.st, f32, h1, M2, 4 * H * W, cout, Cop, mean2, scale2, bias2, Cop, true, a2);
   ConvIn i2;
-  i2.x = h1; i2.B = B; i2.Hx = 2 * H; i2.Wx = 2 * W; i2.C = Cop;
-  i2.mean = mean2; i2.scale = scale2; i2.shift = bias2; i2.tab_stride = Cop; i2.relu = 1;
+  i2.x = a2; i2.B = B; i2.Hx = 2 * H; i2.Wx = 2 * W; i2.C = Cop;
   ConvOut o2;
   o2.y = y; o2.y_f32 = f32; o2.yC = Cop; o2.n_real = cout; o2.bias = P.w("conv2.b");
   o2.res = w.skip; o2.res_f32 = 1; o2.res_mode = R_HALF; o2.resC = Cop;
@@ -211,10 +213,9 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   // conv2: dW2, db2
   GradIn gdy;
   gdy.g = dy; gdy.Hs = H2; gdy.Ws = W2; gdy.C = Cop;
-  ConvIn a2;
-  a2.x = h1; a2.B = B; a2.Hx = H2; a2.Wx = W2; a2.C = Cop;
-  a2.mean = mean2; a2.scale = scale2; a2.shift = bias2; a2.tab_stride = Cop; a2.relu = 1;
-  conv_wgrad(ex.st, f32, gdy, a2, H2, W2, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
+  ConvIn ia2;
+  ia2.x = a2; ia2.B = B; ia2.Hx = H2; ia2.Wx = W2; ia2.C = Cop;
+  conv_wgrad(ex.st, f32, gdy, ia2, H2, W2, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
   colsum(ex.st, f32, dy, M2, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
   // skip: dWsc at full resolution against up2(x); dbsc = db2
   ConvIn ax;
@@ -239,10 +240,9 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   // conv1: dW1, db1
   GradIn gdh;
   gdh.g = w.dh1; gdh.Hs = H2; gdh.Ws = W2; gdh.C = Cop;
-  ConvIn a1;
-  a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.gather = G_UP2;
-  a1.mean = mean1; a1.scale = scale1; a1.shift = bias1; a1.tab_stride = Cip; a1.relu = 1;
-  conv_wgrad(ex.st, f32, gdh, a1, H2, W2, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+  ConvIn ia1;
+  ia1.x = a1; ia1.B = B; ia1.Hx = H; ia1.Wx = W; ia1.C = Cip; ia1.gather = G_UP2;
+  conv_wgrad(ex.st, f32, gdh, ia1, H2, W2, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
   colsum(ex.st, f32, w.dh1, M2, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
   // da1 (at 2x resolution; the BN backward sums 2x2)
   ConvIn d1;

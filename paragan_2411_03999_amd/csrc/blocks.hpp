@@ -94,6 +94,7 @@ struct GBlock {
   float *mean1, *rstd1, *gain1, *bias1, *scale1;
   float *mean2, *rstd2, *gain2, *bias2, *scale2;
   void* h1 = nullptr;
+  void *a1 = nullptr, *a2 = nullptr;   // relu(cbn1(x)), relu(cbn2(h1)): conv operands
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   void fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y);

@@ -49,6 +49,18 @@ PG_DEV uint4 pack8(const float* f) {
   return q;
 }
 
+// ReLU on 8 packed bf16 by their bit patterns: a negative bf16 is a negative
+// int16, so max(v, 0) as packed int16 zeroes exactly the negatives (and -0).
+typedef short short2v __attribute__((ext_vector_type(2)));
+PG_DEV uint32_t relu2_bits(uint32_t w) {
+  short2v v = __builtin_bit_cast(short2v, w);
+  v = __builtin_elementwise_max(v, (short2v){0, 0});
+  return __builtin_bit_cast(uint32_t, v);
+}
+PG_DEV uint4 relu8_bits(const uint4& q) {
+  return make_uint4(relu2_bits(q.x), relu2_bits(q.y), relu2_bits(q.z), relu2_bits(q.w));
+}
+
 // element load/store for the two activation types
 template <typename T> PG_DEV float ld(const T* p, int64_t i);
 template <> PG_DEV float ld<float>(const float* p, int64_t i) { return p[i]; }

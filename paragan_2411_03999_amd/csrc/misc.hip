@@ -367,6 +367,37 @@ void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc
   PG_LAUNCH_CHECK();
 }
 
+// a = [relu]((x - mean[c]) * scale[b][c] + shift[b][c]) stored in the
+// activation type: the BN(+ReLU) operand of the next convolution, computed
+// once per element instead of once per filter tap.  Padded channels get 0.
+template <typename T>
+__global__ void k_bn_apply(const T* x, int64_t M, int HW, int C, int Cp, const float* mean, const float* scale,
+                           const float* shift, int tab_stride, int relu, T* out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= M * Cp) return;
+  const int c = (int)(i % Cp);
+  float v = 0.f;
+  if (c < C) {
+    const int b = (int)((i / Cp) / HW);
+    const int64_t t = (int64_t)b * tab_stride + c;
+    v = (ld<T>(x, i) - mean[c]) * scale[t] + shift[t];
+    if (relu) v = fmaxf(v, 0.f);
+  }
+  st<T>(out, i, v);
+}
+
+void bn_apply(hipStream_t st, bool f32, const void* x, int64_t M, int HW, int C, int Cp, const float* mean,
+              const float* scale, const float* shift, int tab_stride, bool relu, void* out) {
+  dim3 g((unsigned)cdiv(M * Cp, 256));
+  if (f32)
+    hipLaunchKernelGGL(k_bn_apply<float>, g, dim3(256), 0, st, (const float*)x, M, HW, C, Cp, mean, scale, shift,
+                       tab_stride, (int)relu, (float*)out);
+  else
+    hipLaunchKernelGGL(k_bn_apply<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, M, HW, C, Cp, mean, scale,
+                       shift, tab_stride, (int)relu, (bf16_t*)out);
+  PG_LAUNCH_CHECK();
+}
+
 // Conditional-BN tables for the conv prologue and the backward pass:
 //   gain[b][c] = 1 + cond[b] . Wg[c] / sigma_g,  bias[b][c] = cond[b] . Wb[c] / sigma_b
 //   scale[b][c] = gain * rstd[c]   (prologue: (x - mean) * scale + bias)

@@ -28,6 +28,9 @@ void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, 
 size_t bn_stats_ws_bytes(int64_t M, int C);
 void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float eps, float* mean,
               float* rstd, void* ws);
+// out = [relu]((x - mean) * scale + shift), per-(sample, channel) tables
+void bn_apply(hipStream_t st, bool f32, const void* x, int64_t M, int HW, int C, int Cp, const float* mean,
+              const float* scale, const float* shift, int tab_stride, bool relu, void* out);
 void cbn_tables(hipStream_t st, const float* cond, int dc, const float* Wg, const float* Wb,
                 const float* sg, const float* sb, const float* gain_p, const float* bias_p,
                 const float* rstd, int B, int C, int Cp, float* gain, float* bias, float* scale);

@@ -35,6 +35,7 @@ struct ConvOut {
   int n_real = 0;              // channels >= n_real are written as 0
   const float* bias = nullptr;
   const float* acc_scale = nullptr;   // device scalar
+  float acc_mul = 1.f;                // host scalar (also multiplies acc)
   int pool = 0;
   const void* res = nullptr;
   int res_f32 = 0, res_mode = R_NONE, resC = 0;
