@@ -974,11 +974,18 @@ size_t conv_wgrad_ws(bool f32, int64_t M, int R, int Cin, int Np, int n_cu) {
   int tn, tk, sp;
   int64_t mps;
   wgrad_plan(f32, M, R, Cin, Np, n_cu, tn, tk, sp, mps);
-  return sp > 1 ? align256((size_t)sp * Np * R * R * Cin * 4) : 0;
+  const size_t legacy = sp > 1 ? align256((size_t)sp * Np * R * R * Cin * 4) : 0;
+  return f32 ? legacy : std::max(legacy, wgrad_tr_ws(M, R, Cin, Np, n_cu));
 }
 
 void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in, int H, int W,
                 int R, int Np, float* dw, void* ws, size_t ws_bytes, int n_cu) {
+  const double flops =
+      2.0 * (double)in.B * H * W * (g.n_real ? g.n_real : Np) * R * R * (in.c_real ? in.c_real : in.C);
+  if (!f32 && wgrad_tr_ok(g, in, H, W, R, Np)) {
+    if ((int64_t)in.B * H * W > 0) wgrad_tr(s, g, in, H, W, R, Np, dw, ws, ws_bytes, n_cu, flops);
+    return;
+  }
   WgK k;
   k.a = AOp{in.x, in.B, in.Hx, in.Wx, in.C, in.gscale, in.mean, in.scale, in.shift,
             in.tab_stride, H, W, R, R / 2, (int64_t)in.B * H * W};
@@ -1018,7 +1025,7 @@ void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in, int 
 #undef PG_WG_CASE
   if (!done) throw Error{-2, "conv_wgrad: unsupported prologue combination"};
   PG_LAUNCH_CHECK();
-  prof.done(name, 2.0 * (double)k.a.M * (g.n_real ? g.n_real : Np) * R * R * (in.c_real ? in.c_real : in.C));
+  prof.done(name, flops);
   if (k.splits > 1 || g.gscale != 1.f) {
     hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)cdiv(nout, 256)), dim3(256), 0, s,
                        k.part, k.splits, nout, g.gscale, dw);

@@ -3,6 +3,7 @@
 // (the C-ABI layer) before anything is launched.
 #pragma once
 #include "common.hpp"
+#include "fastdiv.hpp"
 
 namespace pg {
 
@@ -65,5 +66,13 @@ size_t conv_wgrad_ws(bool f32, int64_t M, int R, int Cin, int Np, int n_cu);
 void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in,
                 int H, int W, int R, int Np, float* dw, void* ws, size_t ws_bytes,
                 int n_cu);
+
+// bf16 weight gradient through LDS transpose reads (wgrad.hip), for direct or
+// upsampled operands without a BN-affine prologue.  wgrad_tr_ok tells whether
+// a call qualifies; conv_wgrad dispatches to it.
+bool wgrad_tr_ok(const GradIn& g, const ConvIn& in, int H, int W, int R, int Np);
+size_t wgrad_tr_ws(int64_t M, int R, int Cin, int Np, int n_cu);
+void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, int R, int Np, float* dw,
+              void* ws, size_t ws_bytes, int n_cu, double flops);
 
 }  // namespace pg

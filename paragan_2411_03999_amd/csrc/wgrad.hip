@@ -1,0 +1,373 @@
+// bf16 convolution weight gradients on gfx950 MFMA through LDS transpose reads.
+//
+//   dW[n][(r, s, c)] = sum over conv-grid pixels m of dY[m][n] * X~[m][(r, s, c)]
+//
+// where X~ is the im2col view of the activation (direct, or a nearest 2x
+// upsample of a half-resolution tensor, optionally ReLU'd) and dY the output
+// gradient (direct, or a nearest 2x upsample of a half-resolution gradient).
+// The reduction runs over pixels, which are the rows of both operands in
+// memory, so each MFMA operand is a transposed tile.  Here both tiles are
+// copied row-major into LDS unchanged (16-byte loads and stores) and the
+// transposition happens in the LDS read: ds_read_b64_tr_b16 hands each lane
+// four values of one column from four consecutive rows, and two such reads
+// form the eight-deep K slice of a v_mfma_f32_32x32x16_bf16 operand.
+//
+// LDS rows are swizzled in 64-byte blocks so that the 32 lanes of one
+// transpose read (four rows x 64 bytes) hit distinct banks of the 64-bank
+// LDS.  The pixel range is split over blocks; each split writes its own
+// partial sum and the splits are added in a fixed order (bitwise
+// reproducible, no float atomics).
+#include "ops.hpp"
+
+namespace pg {
+
+namespace {
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+constexpr int kMS = 32;   // pixels per pipeline stage (two MFMA K steps)
+
+// block swizzle of LDS row r for a row of NB 64-byte blocks: for four
+// consecutive rows the XOR puts their 64-byte spans on distinct banks
+template <int NB>
+PG_DEV int swz(int r) {
+  return NB % 4 == 0 ? (r & 3) : (NB % 4 == 2 ? ((r >> 1) & 1) : 0);
+}
+// element offset of (row r, element e) in a swizzled tile of P-element rows
+template <int P>
+PG_DEV int lds_off(int r, int e) {
+  constexpr int NB = P / 32;
+  return r * P + ((((e >> 5) ^ swz<NB>(r)) << 5) | (e & 31));
+}
+
+// Two transpose reads: 8 consecutive rows (the K slice) of one column.
+PG_DEV bf16x8 tr_pair(const bf16_t* base, int off_lo, int off_hi) {
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + off_lo));
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(base + off_hi));
+  const auto v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+struct WgTrK {
+  const bf16_t* g;   // gradient source, channel stride gC
+  const bf16_t* x;   // activation source [B][Hx][Wx][C]
+  int gC, Np, Kdim, C, R, pad;
+  int H, W;          // conv grid
+  int Hx, Wx;        // activation source dims
+  int Hs, Ws;        // gradient source dims (upsampled gradient)
+  int M;             // conv-grid pixels
+  FastDiv fdW, fdH, fdC, fdR;
+  int m_per_split, tiles_n, tiles_k;
+  float* part;       // [splits][Np][Kdim]
+};
+
+PG_DEV int remap_block(int bid, int total) {
+  // Blocks go round-robin to the 8 XCDs; give each XCD a contiguous run of
+  // the logical order (split-major), so tiles reading the same pixel range
+  // share that XCD's L2.
+  if ((total & 7) == 0) {
+    const int per = total >> 3;
+    return (bid & 7) * per + (bid >> 3);
+  }
+  return bid;
+}
+
+template <int WM, int WN, int TM, int TN, bool GUP, int XG, bool RELU>
+__global__ __launch_bounds__(256, 2) void k_wgrad_tr(WgTrK k) {
+  constexpr int BN = WM * TM * 32, BK = WN * TN * 32;
+  constexpr int GCH = BN / 8, XCH = BK / 8;   // 16-byte chunks per LDS row
+  constexpr int GIT = (kMS * GCH + 255) / 256, XIT = (kMS * XCH + 255) / 256;
+  __shared__ __attribute__((aligned(16))) bf16_t Gs[2][kMS * BN];
+  __shared__ __attribute__((aligned(16))) bf16_t Xs[2][kMS * BK];
+
+  const int tiles = k.tiles_n * k.tiles_k;
+  const int bid = remap_block(blockIdx.x, gridDim.x);
+  const int split = bid / tiles;
+  const int tile = bid - split * tiles;
+  const int tni = tile / k.tiles_k, tki = tile - tni * k.tiles_k;
+  const int n0 = tni * BN, k0 = tki * BK;
+  const int mbeg = split * k.m_per_split;
+  const int mend = min(mbeg + k.m_per_split, k.M);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  // ---- per-thread load slots (fixed across stages)
+  int g_row[GIT], g_col[GIT], g_lds[GIT];
+  bool g_on[GIT];
+#pragma unroll
+  for (int i = 0; i < GIT; ++i) {
+    const int id = tid + 256 * i;
+    const int row = id / GCH, ch = id - (id / GCH) * GCH;
+    g_on[i] = id < kMS * GCH && n0 + ch * 8 < k.Np;
+    g_row[i] = row;
+    g_col[i] = n0 + ch * 8;
+    g_lds[i] = lds_off<BN>(row < kMS ? row : 0, ch * 8);
+  }
+  int x_row[XIT], x_rs[XIT], x_c[XIT], x_lds[XIT];
+#pragma unroll
+  for (int i = 0; i < XIT; ++i) {
+    const int id = tid + 256 * i;
+    const int row = id / XCH, ch = id - (id / XCH) * XCH;
+    const int kc = k0 + ch * 8;
+    const bool on = id < kMS * XCH && kc < k.Kdim;
+    const int tap = (int)fdiv((uint32_t)kc, k.fdC);
+    const int c = kc - tap * k.C;
+    const int r = (int)fdiv((uint32_t)tap, k.fdR);
+    const int s = tap - r * k.R;
+    x_row[i] = row;
+    // tap offsets relative to the padding; an off slot gets an offset that
+    // fails every bounds check
+    x_rs[i] = on ? (((r - k.pad) & 0xffff) | ((s - k.pad) << 16)) : (0x4000 | (0x4000 << 16));
+    x_c[i] = c;
+    x_lds[i] = lds_off<BK>(row < kMS ? row : 0, ch * 8);
+  }
+
+  uint4 rg[GIT], rx[XIT];
+  auto load = [&](int mb) {
+#pragma unroll
+    for (int i = 0; i < GIT; ++i) {
+      const int m = mb + g_row[i];
+      rg[i] = make_uint4(0, 0, 0, 0);
+      if (g_on[i] && m < mend) {
+        int off;
+        if (!GUP) {
+          off = m * k.gC + g_col[i];
+        } else {
+          const int t = (int)fdiv((uint32_t)m, k.fdW);
+          const int ow = m - t * k.W;
+          const int b = (int)fdiv((uint32_t)t, k.fdH);
+          const int oh = t - b * k.H;
+          off = ((b * k.Hs + (oh >> 1)) * k.Ws + (ow >> 1)) * k.gC + g_col[i];
+        }
+        rg[i] = *reinterpret_cast<const uint4*>(k.g + off);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < XIT; ++i) {
+      const int m = mb + x_row[i];
+      rx[i] = make_uint4(0, 0, 0, 0);
+      const int t = (int)fdiv((uint32_t)m, k.fdW);
+      const int ow = m - t * k.W;
+      const int b = (int)fdiv((uint32_t)t, k.fdH);
+      const int oh = t - b * k.H;
+      const int ih = oh + (short)(x_rs[i] & 0xffff), iw = ow + (x_rs[i] >> 16);
+      if (m < mend && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W) {
+        const int sh = XG == G_UP2 ? (ih >> 1) : ih, sw = XG == G_UP2 ? (iw >> 1) : iw;
+        rx[i] = *reinterpret_cast<const uint4*>(k.x + ((b * k.Hx + sh) * k.Wx + sw) * k.C + x_c[i]);
+      }
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < GIT; ++i)
+      if (tid + 256 * i < kMS * GCH) *reinterpret_cast<uint4*>(&Gs[buf][g_lds[i]]) = rg[i];
+#pragma unroll
+    for (int i = 0; i < XIT; ++i)
+      if (tid + 256 * i < kMS * XCH)
+        *reinterpret_cast<uint4*>(&Xs[buf][x_lds[i]]) = RELU ? relu8_bits(rx[i]) : rx[i];
+  };
+
+  // ---- per-lane transpose-read offsets: source lane L of a 16-lane group
+  // addresses row 8*(L/32) + (L%16)/4 (+4 for the upper half of the K slice)
+  // and column 16*((L/16)%2) + 4*(L%4) of its 32-column MFMA tile.
+  const int rA = 8 * (lane >> 5) + ((lane & 15) >> 2);
+  const int cA = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int a_off[TM], b_off[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) a_off[i] = lds_off<BN>(rA, (wm * TM + i) * 32 + cA);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) b_off[j] = lds_off<BK>(rA, (wn * TN + j) * 32 + cA);
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nst = (mend - mbeg + kMS - 1) / kMS;
+  if (nst > 0) {
+    load(mbeg);
+    store(0);
+  }
+  __syncthreads();
+  int buf = 0;
+  for (int st = 0; st < nst; ++st) {
+    const bool more = st + 1 < nst;
+    if (more) load(mbeg + (st + 1) * kMS);
+    const bf16_t* gb = Gs[buf];
+    const bf16_t* xb = Xs[buf];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8 av[TM], bv[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) av[i] = tr_pair(gb, a_off[i] + kk * 16 * BN, a_off[i] + (kk * 16 + 4) * BN);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bv[j] = tr_pair(xb, b_off[j] + kk * 16 * BK, b_off[j] + (kk * 16 + 4) * BK);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) store(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+
+  float* part = k.part + (int64_t)split * k.Np * k.Kdim;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int kc = k0 + (wn * TN + j) * 32 + (lane & 31);
+      if (kc >= k.Kdim) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int n = n0 + (wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (n < k.Np) part[(int64_t)n * k.Kdim + kc] = acc[i][j][r];
+      }
+    }
+}
+
+// dw = scale * sum over splits, in split order
+__global__ void k_wgtr_reduce(const float* part, int splits, int64_t n, float scale, float* out) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int j = 0; j < splits; ++j) s += part[(int64_t)j * n + i];
+  out[i] = s * scale;
+}
+
+struct TrCfg {
+  int WM, WN, TM, TN;
+};
+constexpr TrCfg kTrCfgs[] = {{2, 2, 4, 2}, {2, 2, 2, 4}, {2, 2, 3, 3}, {1, 4, 3, 2}, {1, 4, 3, 3}, {2, 2, 2, 2}};
+
+struct TrPlan {
+  int cfg, tiles_n, tiles_k, splits, m_per_split;
+};
+
+// Tile shape with the least padded work (BigGAN widths are multiples of 96,
+// filter-tap K dims multiples of 288), then a split of the pixel range that
+// gives the chip ~4 blocks per CU, each split at least 1024 pixels long.
+TrPlan tr_plan(int64_t M, int R, int Cin, int Np, int n_cu) {
+  const int64_t K = (int64_t)R * R * Cin;
+  TrPlan p{0, 0, 0, 1, 0};
+  double best = 1e300;
+  for (int c = 0; c < (int)(sizeof(kTrCfgs) / sizeof(kTrCfgs[0])); ++c) {
+    const TrCfg& t = kTrCfgs[c];
+    const int bn = t.WM * t.TM * 32, bk = t.WN * t.TN * 32;
+    const double tiles = (double)cdiv(Np, bn) * cdiv(K, bk);
+    const double eff = t.TM * t.TN >= 8 ? 1.0 : (t.TM * t.TN >= 6 ? 0.92 : 0.8);
+    const double cost = tiles * bn * bk / eff;
+    if (cost < best * 0.999) {
+      best = cost;
+      p.cfg = c;
+    }
+  }
+  const TrCfg& t = kTrCfgs[p.cfg];
+  p.tiles_n = (int)cdiv(Np, t.WM * t.TM * 32);
+  p.tiles_k = (int)cdiv(K, t.WN * t.TN * 32);
+  const int64_t tiles = (int64_t)p.tiles_n * p.tiles_k;
+  int64_t sp = cdiv(4LL * n_cu, tiles);
+  sp = std::min<int64_t>(sp, std::max<int64_t>(1, M / 1024));
+  const int64_t cap = (512LL << 20) / (4 * (int64_t)Np * K);
+  sp = std::max<int64_t>(1, std::min<int64_t>(sp, cap));
+  p.m_per_split = (int)(cdiv(cdiv(M, sp), kMS) * kMS);
+  p.splits = (int)cdiv(M, p.m_per_split);
+  return p;
+}
+
+template <int WM, int WN, int TM, int TN>
+std::string launch_tr(hipStream_t s, const WgTrK& k, int blocks, bool gup, int xg, bool relu) {
+#define PG_WTR_CASE(GU, XG, RL)                                                                    \
+  if (gup == GU && xg == XG && relu == RL) {                                                       \
+    hipLaunchKernelGGL((k_wgrad_tr<WM, WN, TM, TN, GU, XG, RL>), dim3(blocks), dim3(256), 0, s, k); \
+    return "k_wgrad_tr<" + std::to_string(WM * TM * 32) + "x" + std::to_string(WN * TN * 32) +    \
+           "," #GU "," #XG "," #RL ">";                                                            \
+  }
+  PG_WTR_CASE(false, G_DIRECT, false)
+  PG_WTR_CASE(false, G_DIRECT, true)
+  PG_WTR_CASE(true, G_DIRECT, false)
+  PG_WTR_CASE(true, G_DIRECT, true)
+  PG_WTR_CASE(false, G_UP2, false)
+#undef PG_WTR_CASE
+  throw Error{-2, "wgrad_tr: unsupported gather combination"};
+}
+
+}  // namespace
+
+bool wgrad_tr_ok(const GradIn& g, const ConvIn& in, int H, int W, int R, int Np) {
+  if (in.mean || in.gather == G_POOL2 || in.gscale != 1.f) return false;
+  if (in.gather == G_UP2 && in.relu) return false;
+  if (g.gather != G_DIRECT && g.gather != G_UP2) return false;
+  const int64_t M = (int64_t)in.B * H * W;
+  const int64_t xs = (int64_t)in.B * in.Hx * in.Wx * in.C;
+  const int64_t gs = g.gather == G_DIRECT ? M * g.C : (int64_t)in.B * g.Hs * g.Ws * g.C;
+  return M < (1LL << 30) && xs < (1LL << 31) && gs < (1LL << 31) && in.C % 8 == 0 && g.C % 8 == 0 &&
+         Np % 8 == 0;
+}
+
+size_t wgrad_tr_ws(int64_t M, int R, int Cin, int Np, int n_cu) {
+  const TrPlan p = tr_plan(M, R, Cin, Np, n_cu);
+  return p.splits > 1 ? align256((size_t)p.splits * Np * R * R * Cin * 4) : 0;
+}
+
+void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, int R, int Np, float* dw,
+              void* ws, size_t ws_bytes, int n_cu, double flops) {
+  WgTrK k;
+  k.g = (const bf16_t*)g.g;
+  k.x = (const bf16_t*)in.x;
+  k.gC = g.C;
+  k.Np = Np;
+  k.Kdim = R * R * in.C;
+  k.C = in.C;
+  k.R = R;
+  k.pad = R / 2;
+  k.H = H;
+  k.W = W;
+  k.Hx = in.Hx;
+  k.Wx = in.Wx;
+  k.Hs = g.Hs;
+  k.Ws = g.Ws;
+  k.M = (int)((int64_t)in.B * H * W);
+  k.fdW = make_fastdiv(W);
+  k.fdH = make_fastdiv(H);
+  k.fdC = make_fastdiv(in.C);
+  k.fdR = make_fastdiv(R);
+  const TrPlan p = tr_plan(k.M, R, in.C, Np, n_cu);
+  k.m_per_split = p.m_per_split;
+  k.tiles_n = p.tiles_n;
+  k.tiles_k = p.tiles_k;
+  const int64_t nout = (int64_t)Np * k.Kdim;
+  const bool direct = p.splits == 1 && g.gscale == 1.f;
+  if (!direct && p.splits > 1 && (size_t)p.splits * nout * 4 > ws_bytes)
+    throw Error{-3, "conv_wgrad: workspace too small"};
+  k.part = direct || p.splits == 1 ? dw : (float*)ws;
+  const int blocks = p.splits * p.tiles_n * p.tiles_k;
+  const bool gup = g.gather == G_UP2;
+  std::string name;
+  ProfScope prof(s);
+  switch (p.cfg) {
+    case 0: name = launch_tr<2, 2, 4, 2>(s, k, blocks, gup, in.gather, in.relu); break;
+    case 1: name = launch_tr<2, 2, 2, 4>(s, k, blocks, gup, in.gather, in.relu); break;
+    case 2: name = launch_tr<2, 2, 3, 3>(s, k, blocks, gup, in.gather, in.relu); break;
+    case 3: name = launch_tr<1, 4, 3, 2>(s, k, blocks, gup, in.gather, in.relu); break;
+    case 4: name = launch_tr<1, 4, 3, 3>(s, k, blocks, gup, in.gather, in.relu); break;
+    default: name = launch_tr<2, 2, 2, 2>(s, k, blocks, gup, in.gather, in.relu); break;
+  }
+  PG_LAUNCH_CHECK();
+  prof.done(name, flops);
+  if (p.splits > 1 || g.gscale != 1.f) {
+    ProfScope pr(s);
+    hipLaunchKernelGGL(k_wgtr_reduce, dim3((unsigned)cdiv(nout, 256)), dim3(256), 0, s, k.part, p.splits,
+                       nout, g.gscale, dw);
+    PG_LAUNCH_CHECK();
+    pr.done("k_wgtr_reduce", 0.0);
+  }
+}
+
+}  // namespace pg
