@@ -197,7 +197,8 @@ def main():
     stats.sort(key=lambda s: -s["total_ms"])
     dom = stats[0]
     achieved = dom["flops"] / (dom["total_ms"] / 1e3) / 1e12
-    conv = [s for s in stats if s["name"].startswith(("k_conv_mfma", "k_wgrad_mfma"))]
+    conv = [s for s in stats if s["name"].startswith(("k_conv_", "k_wgrad_")) and s["flops"] > 0
+            and "simt" not in s["name"]]
     conv_ms = sum(s["total_ms"] for s in conv)
     conv_tf = sum(s["flops"] for s in conv) / (conv_ms / 1e3) / 1e12 if conv_ms else 0.0
     all_ms = sum(s["total_ms"] for s in stats)

@@ -311,161 +311,6 @@ __global__ __launch_bounds__(256, 2) void k_conv_mfma(ConvK k) {
   }
 }
 
-// ------------------------------------------- bf16 MFMA conv, streamlined K loop
-// For the direct and nearest-upsample gathers with a plain or ReLU operand.
-// The K loop runs tap-outer, channel-inner: a thread's source offsets for its
-// rows are computed once per tap and then advance by 32 channels per step;
-// weight offsets are linear in the step.  Every index fits in 32 bits (the
-// host checks the source tensor size).
-template <int WM, int WN, int TM, int TN, int GATHER, bool RELU>
-__global__ __launch_bounds__(256, 2) void k_conv_mfma2(ConvK k) {
-  constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
-  constexpr int LDA = 40;
-  constexpr int AP = BM / 64;
-  constexpr int BP = (BN * 4 + 255) / 256;
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LDA];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * LDA];
-
-  const AOp& a = k.a;
-  const int bid = remap_tile(blockIdx.x, k.tiles_m * k.tiles_n);
-  const int tmi = bid / k.tiles_n, tni = bid - tmi * k.tiles_n;
-  const int64_t m0 = (int64_t)tmi * BM;
-  const int n0 = tni * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int q = tid & 3;
-  const int quad = k.o.pool;
-  const int C = a.C, R = a.R, pad = a.pad;
-
-  int rb[AP], roh[AP], row_[AP];
-  bool rv[AP];
-#pragma unroll
-  for (int p = 0; p < AP; ++p) {
-    const int64_t m = m0 + (tid >> 2) + 64 * p;
-    rv[p] = m < a.M;
-    decode_m(rv[p] ? m : 0, a.H, a.W, quad, rb[p], roh[p], row_[p]);
-  }
-  const bf16_t* X = (const bf16_t*)a.x;
-  const bf16_t* Wt = (const bf16_t*)k.w;
-  // per-row state of the tap being loaded
-  int roff[AP];
-  bool rok[AP];
-  auto set_tap = [&](int tap) {
-    const int r = tap / R, s = tap - (tap / R) * R;
-#pragma unroll
-    for (int p = 0; p < AP; ++p) {
-      const int ih = roh[p] + r - pad, iw = row_[p] + s - pad;
-      rok[p] = rv[p] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-      const int sh = GATHER == G_UP2 ? (ih >> 1) : ih;
-      const int sw = GATHER == G_UP2 ? (iw >> 1) : iw;
-      roff[p] = rok[p] ? ((rb[p] * a.Hx + sh) * a.Wx + sw) * C + q * 8 : 0;
-    }
-  };
-  int woff[BP];
-  bool wok[BP];
-#pragma unroll
-  for (int p = 0; p < BP; ++p) {
-    const int idx = tid + 256 * p;
-    const int n = n0 + (idx >> 2);
-    wok[p] = idx < BN * 4 && n < k.Np;
-    woff[p] = wok[p] ? n * R * R * C + (idx & 3) * 8 : 0;
-  }
-  uint4 ra[AP], rw[BP];
-  int ld_tap = 0, ld_c0 = 0, ld_ks = 0;
-  set_tap(0);
-  auto load = [&]() {
-#pragma unroll
-    for (int p = 0; p < AP; ++p)
-      ra[p] = rok[p] ? *reinterpret_cast<const uint4*>(X + roff[p] + ld_c0) : make_uint4(0, 0, 0, 0);
-#pragma unroll
-    for (int p = 0; p < BP; ++p)
-      rw[p] = wok[p] ? *reinterpret_cast<const uint4*>(Wt + woff[p] + ld_ks * 32) : make_uint4(0, 0, 0, 0);
-    ++ld_ks;
-    ld_c0 += 32;
-    if (ld_c0 == C) {
-      ld_c0 = 0;
-      ++ld_tap;
-      if (ld_tap < R * R) set_tap(ld_tap);
-    }
-  };
-  auto store = [&](int buf) {
-#pragma unroll
-    for (int p = 0; p < AP; ++p)
-      *reinterpret_cast<uint4*>(&As[buf][((tid >> 2) + 64 * p) * LDA + q * 8]) = RELU ? relu8_bits(ra[p]) : ra[p];
-#pragma unroll
-    for (int p = 0; p < BP; ++p) {
-      const int idx = tid + 256 * p;
-      if (idx < BN * 4) *reinterpret_cast<uint4*>(&Bs[buf][(idx >> 2) * LDA + (idx & 3) * 8]) = rw[p];
-    }
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  load();
-  store(0);
-  __syncthreads();
-  int buf = 0;
-  for (int ks = 0; ks < k.ksteps; ++ks) {
-    const bool more = ks + 1 < k.ksteps;
-    if (more) load();
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      bf16x8 av[TM], bv[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-        av[i] = *reinterpret_cast<const bf16x8*>(
-            &As[buf][((wm * TM + i) * 32 + (lane & 31)) * LDA + kk * 16 + (lane >> 5) * 8]);
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bv[j] = *reinterpret_cast<const bf16x8*>(
-            &Bs[buf][((wn * TN + j) * 32 + (lane & 31)) * LDA + kk * 16 + (lane >> 5) * 8]);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) store(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
-  }
-
-  const float accs = (k.o.acc_scale ? *k.o.acc_scale : 1.f) * k.o.acc_mul;
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int col = n0 + (wn * TN + j) * 32 + (lane & 31);
-      if (col >= k.o.yC) continue;
-      const float bias = (k.o.bias && col < k.o.n_real) ? k.o.bias[col] : 0.f;
-      const int64_t rbase = m0 + (wm * TM + i) * 32 + 4 * (lane >> 5);
-      if (!k.o.pool) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int64_t m = rbase + 8 * (r >> 2) + (r & 3);
-          if (m < a.M) epi_store(k, m, col, acc[i][j][r] * accs + bias, a.H, a.W);
-        }
-      } else {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int64_t m = rbase + 8 * g;
-          if (m < a.M) {
-            const float v = 0.25f * ((acc[i][j][4 * g] + acc[i][j][4 * g + 1]) +
-                                     (acc[i][j][4 * g + 2] + acc[i][j][4 * g + 3]));
-            epi_store(k, m >> 2, col, v * accs + bias, a.H, a.W);
-          }
-        }
-      }
-    }
-  }
-}
-
 // ------------------------------------------------------------ fp32 SIMT conv
 template <int GATHER, bool AFF, bool RELU>
 __global__ __launch_bounds__(256) void k_conv_simt(ConvK k) {
@@ -545,25 +390,6 @@ __global__ __launch_bounds__(256) void k_conv_simt(ConvK k) {
 // --------------------------------------------------------------- launcher
 static std::string kname(const char* base, std::initializer_list<int> args);
 
-template <int WM, int WN, int TM, int TN>
-static std::string launch_mfma2_cfg(hipStream_t s, ConvK& k, int gather, bool relu) {
-  constexpr int BM = WM * TM * 32, BN = WN * TN * 32;
-  k.tiles_m = (int)cdiv(k.a.M, BM);
-  k.tiles_n = (int)cdiv(k.Np, BN);
-  dim3 grid(k.tiles_m * k.tiles_n), block(256);
-#define PG_CONV2_CASE(G, R_)                                                          \
-  if (gather == G && relu == R_) {                                                    \
-    hipLaunchKernelGGL((k_conv_mfma2<WM, WN, TM, TN, G, R_>), grid, block, 0, s, k);  \
-    return kname("k_conv_mfma2", {WM, WN, TM, TN, G, R_});                          \
-  }
-  PG_CONV2_CASE(G_DIRECT, false)
-  PG_CONV2_CASE(G_DIRECT, true)
-  PG_CONV2_CASE(G_UP2, false)
-  PG_CONV2_CASE(G_UP2, true)
-#undef PG_CONV2_CASE
-  throw Error{-2, "conv2: unsupported gather"};
-}
-
 static std::string kname(const char* base, std::initializer_list<int> args) {
   std::string n = std::string(base) + "<";
   bool first = true;
@@ -641,20 +467,15 @@ void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
       k.a.gscale = 1.f;
     }
   }
-  const bool fits32 = (int64_t)in.B * in.Hx * in.Wx * in.C < (1LL << 31) && (int64_t)Np * R * R * in.C < (1LL << 31);
-  if (!aff && in.gather != G_POOL2 && k.a.gscale == 1.f && fits32) {
-    std::string name;
-    if (Np % 128 == 0)
-      name = launch_mfma2_cfg<2, 2, 4, 2>(s, k, in.gather, in.relu);
-    else if (Np % 96 == 0)
-      name = launch_mfma2_cfg<4, 1, 2, 3>(s, k, in.gather, in.relu);
-    else if (Np <= 64)
-      name = launch_mfma2_cfg<4, 1, 1, 2>(s, k, in.gather, in.relu);
-    else
-      name = launch_mfma2_cfg<2, 2, 2, 2>(s, k, in.gather, in.relu);
-    PG_LAUNCH_CHECK();
-    prof.done(name, flops);
-    return;
+  {
+    ConvIn in2 = in;
+    in2.gscale = k.a.gscale;
+    if (conv_fwd_mfma_ok(in2, H, W, R, Np, k.o)) {
+      const std::string name = conv_fwd_mfma(s, in2, H, W, R, w, Np, k.o);
+      PG_LAUNCH_CHECK();
+      prof.done(name, flops);
+      return;
+    }
   }
   // tile choice: 128x128 when N is a multiple of 128, else 256x96 / 128x64
   // shapes so that BigGAN's 96-multiple widths waste no MMA columns.

@@ -50,6 +50,12 @@ struct ConvOut {
 void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
               const void* w, int Np, const ConvOut& out);
 
+// The MFMA convolution for direct / upsampled operands without a BN-affine
+// prologue (convfwd.hip); conv_fwd dispatches to it when conv_fwd_mfma_ok.
+bool conv_fwd_mfma_ok(const ConvIn& in, int H, int W, int R, int Np, const ConvOut& out);
+std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, const void* w, int Np,
+                          const ConvOut& out);
+
 // Gradient operand of a weight gradient: dy at the conv-output grid (H x W)
 // read directly or as a nearest-2x upsample of a half-resolution tensor.
 struct GradIn {
