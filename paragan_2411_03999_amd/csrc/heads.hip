@@ -24,75 +24,77 @@ void img_to_bf16(hipStream_t st, const float* img, int64_t npix, int Cp, void* o
 }
 
 // --------------------------------------------------- generator output layer
-// a = relu((x - mean) * scale + shift) (per channel), img = tanh(conv3x3(a) + b).
-// Each thread computes 4 horizontally adjacent pixels, so every staged
-// weight and every loaded input serves up to 4 outputs.
-__global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* x, int B, int H, int W, int C, int Cp,
-                                                   const float* mean, const float* scale, const float* shift,
-                                                   const float* Wt, const float* sigma, const float* bias,
+// a = relu((x - mean) * scale + shift) (per channel), img = tanh(conv3x3(a) / sigma + b),
+// all in fp32.  A block computes 128 pixels of one image row: per chunk of
+// 32 channels it stages the three input rows it needs, already normalised,
+// in LDS (each element transformed once), then each thread accumulates one
+// pixel over half of the chunk's channels with the weights read as
+// wave-uniform scalars; the two halves combine in a fixed order.
+constexpr int kHT = 128;
+constexpr int kHC = 32;
+
+__global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* __restrict__ x, int B, int H, int W, int C, int Cp,
+                                                   const float* __restrict__ mean, const float* __restrict__ scale,
+                                                   const float* __restrict__ shift, const float* __restrict__ Wt,
+                                                   const float* sigma, const float* __restrict__ bias,
                                                    float* img) {
-  extern __shared__ float sw[];   // [3][9][C] / sigma, then mean, scale, shift
-  const int n = 27 * C;
-  const float inv = 1.f / *sigma;
-  for (int i = threadIdx.x; i < n; i += 256) sw[i] = Wt[i] * inv;
-  float* sm = sw + n;
-  for (int i = threadIdx.x; i < C; i += 256) {
-    sm[i] = mean[i];
-    sm[C + i] = scale[i];
-    sm[2 * C + i] = shift[i];
-  }
-  __syncthreads();
-  const int Wq = (W + 3) / 4;
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (t >= (int64_t)B * H * Wq) return;
-  const int w0 = (int)(t % Wq) * 4;
-  const int64_t bh = t / Wq;
-  const int h = (int)(bh % H);
-  const int b = (int)(bh / H);
-  float acc[4][3];
-  for (int j = 0; j < 4; ++j)
-    for (int co = 0; co < 3; ++co) acc[j][co] = bias[co];
-  for (int r = 0; r < 3; ++r) {
-    const int ih = h + r - 1;
-    if (ih < 0 || ih >= H) continue;
-    const bf16_t* xrow = x + ((int64_t)b * H + ih) * W * Cp;
-    for (int c = 0; c < C; c += 8) {
-      float a[6][8];
+  __shared__ float As[3][kHT + 2][kHC + 1];
+  __shared__ float red[kHT][3];
+  const int tiles_w = (W + kHT - 1) / kHT;
+  const int bid = blockIdx.x;
+  const int tw = bid % tiles_w;
+  const int bh = bid / tiles_w;
+  const int h = bh % H, b = bh / H;
+  const int w0 = tw * kHT;
+  const int t = threadIdx.x, p = t & (kHT - 1);
+  const int half = __builtin_amdgcn_readfirstlane(t >> 7);
+  float acc[3] = {0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < C; c0 += kHC) {
+    __syncthreads();
+    for (int idx = t; idx < 3 * (kHT + 2) * 4; idx += 256) {
+      const int q = idx & 3;
+      const int pix = (idx >> 2) % (kHT + 2);
+      const int r = (idx >> 2) / (kHT + 2);
+      const int ih = h + r - 1, iw = w0 + pix - 1;
+      float v[8];
 #pragma unroll
-      for (int q = 0; q < 6; ++q) {
-        const int iw = w0 - 1 + q;
-        if (iw < 0 || iw >= W) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) a[q][e] = 0.f;
-          continue;
-        }
-        unpack8(*reinterpret_cast<const uint4*>(xrow + (int64_t)iw * Cp + c), a[q]);
-#pragma unroll
-        for (int e = 0; e < 8; ++e)
-          a[q][e] = (c + e < C) ? fmaxf((a[q][e] - sm[c + e]) * sm[C + c + e] + sm[2 * C + c + e], 0.f) : 0.f;
-      }
-#pragma unroll
-      for (int s_ = 0; s_ < 3; ++s_)
+      for (int e = 0; e < 8; ++e) v[e] = 0.f;
+      if (ih >= 0 && ih < H && iw >= 0 && iw < W) {
+        unpack8(*reinterpret_cast<const uint4*>(x + (((int64_t)b * H + ih) * W + iw) * Cp + c0 + q * 8), v);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          if (c + e >= C) break;
-          const float w0_ = sw[(0 * 9 + r * 3 + s_) * C + c + e];
-          const float w1_ = sw[(1 * 9 + r * 3 + s_) * C + c + e];
-          const float w2_ = sw[(2 * 9 + r * 3 + s_) * C + c + e];
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float av = a[j + s_][e];
-            acc[j][0] = fmaf(av, w0_, acc[j][0]);
-            acc[j][1] = fmaf(av, w1_, acc[j][1]);
-            acc[j][2] = fmaf(av, w2_, acc[j][2]);
-          }
+          const int c = c0 + q * 8 + e;
+          v[e] = c < C ? fmaxf((v[e] - mean[c]) * scale[c] + shift[c], 0.f) : 0.f;
         }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) As[r][pix][q * 8 + e] = v[e];
     }
+    __syncthreads();
+    const int cb = c0 + half * 16;
+    const int nc = min(16, C - cb);
+    for (int r = 0; r < 3; ++r)
+      for (int s_ = 0; s_ < 3; ++s_) {
+        const float* wr = Wt + (r * 3 + s_) * C + cb;
+        for (int cc = 0; cc < nc; ++cc) {
+          const float av = As[r][p + s_][half * 16 + cc];
+          acc[0] = fmaf(av, wr[cc], acc[0]);
+          acc[1] = fmaf(av, wr[9 * C + cc], acc[1]);
+          acc[2] = fmaf(av, wr[18 * C + cc], acc[2]);
+        }
+      }
   }
-  for (int j = 0; j < 4; ++j) {
-    if (w0 + j >= W) break;
-    const int64_t p = ((int64_t)b * H + h) * W + w0 + j;
-    for (int co = 0; co < 3; ++co) img[p * 3 + co] = tanhf(acc[j][co]);
+  if (half == 1) {
+    red[p][0] = acc[0];
+    red[p][1] = acc[1];
+    red[p][2] = acc[2];
+  }
+  __syncthreads();
+  if (half == 0 && w0 + p < W) {
+    const float inv = 1.f / *sigma;
+    const int64_t o = (((int64_t)b * H + h) * W + w0 + p) * 3;
+#pragma unroll
+    for (int co = 0; co < 3; ++co) img[o + co] = tanhf((acc[co] + red[p][co]) * inv + bias[co]);
   }
 }
 
@@ -215,12 +217,10 @@ size_t ghead_ws_bytes(int64_t M, int C) { return align256((size_t)cdiv(M, kHeadR
 void ghead_fwd(hipStream_t st, const void* x, int B, int H, int W, int C, int Cp, const float* mean,
                const float* scale, const float* shift, const float* Wt, const float* sigma, const float* bias,
                float* img) {
-  const int64_t M = (int64_t)B * H * W;
-  const size_t sh = (27 * C + 3 * C) * sizeof(float);
-  const int64_t nthr = (int64_t)B * H * ((W + 3) / 4);
-  (void)M;
-  hipLaunchKernelGGL(k_ghead_fwd, dim3((unsigned)cdiv(nthr, 256)), dim3(256), sh, st, (const bf16_t*)x, B, H, W, C,
-                     Cp, mean, scale, shift, Wt, sigma, bias, img);
+  const int64_t blocks = (int64_t)B * H * cdiv(W, kHT);
+  PG_CHECK(blocks < (1LL << 31) && Cp % 8 == 0, "ghead_fwd: shape");
+  hipLaunchKernelGGL(k_ghead_fwd, dim3((unsigned)blocks), dim3(256), 0, st, (const bf16_t*)x, B, H, W, C, Cp, mean,
+                     scale, shift, Wt, sigma, bias, img);
   PG_LAUNCH_CHECK();
 }
 

@@ -234,27 +234,111 @@ void sn_bwd(hipStream_t st, const float* dwp, const float* W, const float* u, co
   PG_LAUNCH_CHECK();
 }
 
-// ------------------------------------------------------ column sums
-// Two-level fixed-order reduction over rows.  Level 1: block (chunk of
-// kRows rows, 64 channels); its 4 waves take rows r = wave (mod 4), lanes
-// are consecutive channels (coalesced), the 4 wave sums combine in order.
-// Level 2: one block per 64 channels; 16 waves take chunks j = wave
-// (mod 16), combined in order.
-constexpr int kRows = 2048;
+// ------------------------------------------------ per-channel reductions
+// Column sums and batch-norm statistics over the rows (pixels) of an NHWC
+// tensor, in two fixed-order levels (bitwise reproducible, no atomics).
+// Level 1: a block takes a chunk of rows; a thread owns 8 consecutive
+// channels (one 16-byte bf16 load or two fp32 loads per row) of the rows
+// ro, ro + P, ... of the chunk, P threads sharing each channel group.  The
+// P partials per channel then combine in order through LDS.  Level 2 merges
+// the chunks.  Statistics use shifted sums per thread (shift = the thread's
+// first value, so the sums stay well conditioned) and Chan's parallel
+// variance formula for every merge.
+constexpr int kRowsPerThread = 32;
+
+struct RedShape {
+  int CC, P, rows_blk;
+};
+// C: channels reduced (real count); the reduction covers cpad(C) channels
+inline RedShape red_shape(int C) {
+  RedShape r;
+  r.CC = (int)(cpad(C) / 8);
+  r.P = std::max(1, 256 / r.CC);
+  r.rows_blk = r.P * kRowsPerThread;
+  return r;
+}
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_colsum_part(const T* x, int64_t M, int C, int ldc, float* part) {
-  __shared__ float sh[4][64];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int c = blockIdx.y * 64 + lane;
-  const int64_t r0 = (int64_t)blockIdx.x * kRows;
-  const int64_t r1 = r0 + kRows < M ? r0 + kRows : M;
-  float s = 0.f;
-  if (c < C)
-    for (int64_t r = r0 + wv; r < r1; r += 4) s += ld<T>(x, r * ldc + c);
-  sh[wv][lane] = s;
+PG_DEV void load8f(const T* p, float* v);
+template <>
+PG_DEV void load8f<bf16_t>(const bf16_t* p, float* v) {
+  unpack8(*reinterpret_cast<const uint4*>(p), v);
+}
+template <>
+PG_DEV void load8f<float>(const float* p, float* v) {
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+PG_DEV void chan_merge(double& n, double& mu, double& m2, double nb, double mb, double m2b) {
+  if (nb <= 0.0) return;
+  const double nn = n + nb;
+  const double d = mb - mu;
+  mu += d * nb / nn;
+  m2 += m2b + d * d * n * nb / nn;
+  n = nn;
+}
+
+// STATS: pa = chunk mean, pb = chunk M2; else pa = chunk sum.  [chunk][C]
+template <typename T, bool STATS>
+__global__ __launch_bounds__(256) void k_colred(const T* x, int64_t M, int C, int ldc, RedShape sh, float* pa,
+                                                float* pb) {
+  __shared__ float s_a[256 * 8], s_b[256 * 8];
+  __shared__ int s_n[256];
+  const int t = threadIdx.x;
+  const int cc = t % sh.CC, ro = t / sh.CC;
+  const int64_t r0 = (int64_t)blockIdx.x * sh.rows_blk;
+  const int64_t r1 = r0 + sh.rows_blk < M ? r0 + sh.rows_blk : M;
+  float sft[8], s1[8], s2[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) sft[e] = s1[e] = s2[e] = 0.f;
+  int n = 0;
+  if (ro < sh.P) {
+    for (int64_t r = r0 + ro; r < r1; r += sh.P) {
+      float v[8];
+      load8f<T>(x + r * ldc + cc * 8, v);
+      if (STATS && n == 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sft[e] = v[e];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float d = v[e] - sft[e];
+        s1[e] += d;
+        if (STATS) s2[e] = fmaf(d, d, s2[e]);
+      }
+      ++n;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    if (STATS) {
+      const float mu = n ? sft[e] + s1[e] / (float)n : 0.f;
+      s_a[t * 8 + e] = mu;
+      s_b[t * 8 + e] = n ? s2[e] - s1[e] * (s1[e] / (float)n) : 0.f;
+    } else {
+      s_a[t * 8 + e] = s1[e];
+    }
+  }
+  s_n[t] = n;
   __syncthreads();
-  if (wv == 0 && c < C) part[(int64_t)blockIdx.x * C + c] = (sh[0][lane] + sh[1][lane]) + (sh[2][lane] + sh[3][lane]);
+  for (int c = t; c < C; c += 256) {
+    const int g = c >> 3, e = c & 7;
+    if (STATS) {
+      double nn = 0.0, mu = 0.0, m2 = 0.0;
+      for (int j = 0; j < sh.P; ++j) {
+        const int u = j * sh.CC + g;
+        chan_merge(nn, mu, m2, (double)s_n[u], (double)s_a[u * 8 + e], (double)s_b[u * 8 + e]);
+      }
+      pa[(int64_t)blockIdx.x * C + c] = (float)mu;
+      pb[(int64_t)blockIdx.x * C + c] = (float)m2;
+    } else {
+      float sum = 0.f;
+      for (int j = 0; j < sh.P; ++j) sum += s_a[(j * sh.CC + g) * 8 + e];
+      pa[(int64_t)blockIdx.x * C + c] = sum;
+    }
+  }
 }
 
 __global__ __launch_bounds__(1024) void k_colsum_fin(const float* part, int nch, int C, float scale, float* out) {
@@ -273,71 +357,40 @@ __global__ __launch_bounds__(1024) void k_colsum_fin(const float* part, int nch,
   }
 }
 
-size_t colsum_ws_bytes(int64_t M, int C) { return align256((size_t)cdiv(M, kRows) * C * 4); }
+size_t colsum_ws_bytes(int64_t M, int C) {
+  return align256((size_t)cdiv(M, red_shape(C).rows_blk) * C * 4);
+}
 
 void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float scale, float* out,
             void* ws) {
-  const int nch = (int)cdiv(M, kRows);
+  if (M <= 0) {
+    fill(st, out, C, 0.f);
+    return;
+  }
+  const RedShape sh = red_shape(C);
+  PG_CHECK(ldc >= cpad(C) && ldc % 8 == 0, "colsum: channel stride");
+  const int nch = (int)cdiv(M, sh.rows_blk);
   float* part = (float*)ws;
-  dim3 g1(nch, (unsigned)cdiv(C, 64));
   if (f32)
-    hipLaunchKernelGGL(k_colsum_part<float>, g1, dim3(256), 0, st, (const float*)x, M, C, ldc, part);
+    hipLaunchKernelGGL((k_colred<float, false>), dim3(nch), dim3(256), 0, st, (const float*)x, M, C, ldc, sh, part,
+                       nullptr);
   else
-    hipLaunchKernelGGL(k_colsum_part<bf16_t>, g1, dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, part);
+    hipLaunchKernelGGL((k_colred<bf16_t, false>), dim3(nch), dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, sh,
+                       part, nullptr);
   hipLaunchKernelGGL(k_colsum_fin, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, part, nch, C, scale, out);
   PG_LAUNCH_CHECK();
 }
 
 // ------------------------------------------------------- batch norm
-// Per chunk of kRows rows: mean by a first pass, M2 = sum (x - mean)^2 by a
-// second (both fixed-order as in the column sums); chunks merge with Chan's
-// formula in fp64, in a fixed order.
-template <typename T>
-__global__ __launch_bounds__(256) void k_bn_part(const T* x, int64_t M, int C, int ldc, float* pmean, float* pm2) {
-  __shared__ float sh[4][64];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int c = blockIdx.y * 64 + lane;
-  const int64_t r0 = (int64_t)blockIdx.x * kRows;
-  const int64_t r1 = r0 + kRows < M ? r0 + kRows : M;
-  float s = 0.f;
-  if (c < C)
-    for (int64_t r = r0 + wv; r < r1; r += 4) s += ld<T>(x, r * ldc + c);
-  sh[wv][lane] = s;
-  __syncthreads();
-  const float mean = ((sh[0][lane] + sh[1][lane]) + (sh[2][lane] + sh[3][lane])) / (float)(r1 - r0);
-  __syncthreads();
-  float m2 = 0.f;
-  if (c < C)
-    for (int64_t r = r0 + wv; r < r1; r += 4) {
-      const float d = ld<T>(x, r * ldc + c) - mean;
-      m2 = fmaf(d, d, m2);
-    }
-  sh[wv][lane] = m2;
-  __syncthreads();
-  if (wv == 0 && c < C) {
-    pmean[(int64_t)blockIdx.x * C + c] = mean;
-    pm2[(int64_t)blockIdx.x * C + c] = (sh[0][lane] + sh[1][lane]) + (sh[2][lane] + sh[3][lane]);
-  }
-}
-
-PG_DEV void chan_merge(double& n, double& mu, double& m2, double nb, double mb, double m2b) {
-  if (nb <= 0.0) return;
-  const double nn = n + nb;
-  const double d = mb - mu;
-  mu += d * nb / nn;
-  m2 += m2b + d * d * n * nb / nn;
-  n = nn;
-}
-
-__global__ __launch_bounds__(1024) void k_bn_fin(const float* pmean, const float* pm2, int nch, int64_t M, int C,
-                                                 float eps, float* mean, float* rstd) {
+__global__ __launch_bounds__(1024) void k_bn_fin(const float* pmean, const float* pm2, int nch, int rows_blk,
+                                                 int64_t M, int C, float eps, float* mean, float* rstd) {
   __shared__ double sn[16][64], smu[16][64], sm2[16][64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int c = blockIdx.x * 64 + lane;
   double n = 0.0, mu = 0.0, m2 = 0.0;
   if (c < C)
     for (int j = wv; j < nch; j += 16) {
-      const double nb = (double)std::min<int64_t>(kRows, M - (int64_t)j * kRows);
+      const double nb = (double)std::min<int64_t>(rows_blk, M - (int64_t)j * rows_blk);
       chan_merge(n, mu, m2, nb, pmean[(int64_t)j * C + c], pm2[(int64_t)j * C + c]);
     }
   sn[wv][lane] = n; smu[wv][lane] = mu; sm2[wv][lane] = m2;
@@ -350,51 +403,84 @@ __global__ __launch_bounds__(1024) void k_bn_fin(const float* pmean, const float
   }
 }
 
-size_t bn_stats_ws_bytes(int64_t M, int C) { return 2 * align256((size_t)cdiv(M, kRows) * C * 4); }
+size_t bn_stats_ws_bytes(int64_t M, int C) {
+  return 2 * align256((size_t)cdiv(M, red_shape(C).rows_blk) * C * 4);
+}
 
 void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float eps, float* mean,
               float* rstd, void* ws) {
-  const int nch = (int)cdiv(M, kRows);
+  PG_CHECK(M > 0, "bn_stats: empty batch");
+  const RedShape sh = red_shape(C);
+  PG_CHECK(ldc >= cpad(C) && ldc % 8 == 0, "bn_stats: channel stride");
+  const int nch = (int)cdiv(M, sh.rows_blk);
   float* pmean = (float*)ws;
   float* pm2 = (float*)((char*)ws + align256((size_t)nch * C * 4));
-  dim3 g1(nch, (unsigned)cdiv(C, 64));
   if (f32)
-    hipLaunchKernelGGL(k_bn_part<float>, g1, dim3(256), 0, st, (const float*)x, M, C, ldc, pmean, pm2);
+    hipLaunchKernelGGL((k_colred<float, true>), dim3(nch), dim3(256), 0, st, (const float*)x, M, C, ldc, sh, pmean,
+                       pm2);
   else
-    hipLaunchKernelGGL(k_bn_part<bf16_t>, g1, dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, pmean, pm2);
-  hipLaunchKernelGGL(k_bn_fin, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, pmean, pm2, nch, M, C, eps, mean,
-                     rstd);
+    hipLaunchKernelGGL((k_colred<bf16_t, true>), dim3(nch), dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, sh,
+                       pmean, pm2);
+  hipLaunchKernelGGL(k_bn_fin, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, pmean, pm2, nch, sh.rows_blk, M, C,
+                     eps, mean, rstd);
   PG_LAUNCH_CHECK();
 }
 
 // a = [relu]((x - mean[c]) * scale[b][c] + shift[b][c]) stored in the
 // activation type: the BN(+ReLU) operand of the next convolution, computed
 // once per element instead of once per filter tap.  Padded channels get 0.
+// One thread per (pixel, 8 channels): 16-byte loads and stores.
 template <typename T>
-__global__ void k_bn_apply(const T* x, int64_t M, int HW, int C, int Cp, const float* mean, const float* scale,
-                           const float* shift, int tab_stride, int relu, T* out) {
+PG_DEV void store8f(T* p, const float* v);
+template <>
+PG_DEV void store8f<bf16_t>(bf16_t* p, const float* v) {
+  *reinterpret_cast<uint4*>(p) = pack8(v);
+}
+template <>
+PG_DEV void store8f<float>(float* p, const float* v) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_bn_apply(const T* x, int64_t n8, int CC, FastDiv fdCC, FastDiv fdHW,
+                                                  int C, const float* mean, const float* scale,
+                                                  const float* shift, int tab_stride, int relu, T* out) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= M * Cp) return;
-  const int c = (int)(i % Cp);
-  float v = 0.f;
-  if (c < C) {
-    const int b = (int)((i / Cp) / HW);
-    const int64_t t = (int64_t)b * tab_stride + c;
-    v = (ld<T>(x, i) - mean[c]) * scale[t] + shift[t];
-    if (relu) v = fmaxf(v, 0.f);
+  if (i >= n8) return;
+  const int p = (int)fdiv((uint32_t)i, fdCC);
+  const int c0 = ((int)i - p * CC) * 8;
+  const int b = (int)fdiv((uint32_t)p, fdHW);
+  float v[8];
+  load8f<T>(x + i * 8, v);
+  const int64_t tb = (int64_t)b * tab_stride;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int c = c0 + e;
+    float y = 0.f;
+    if (c < C) {
+      y = (v[e] - mean[c]) * scale[tb + c] + shift[tb + c];
+      if (relu) y = fmaxf(y, 0.f);
+    }
+    v[e] = y;
   }
-  st<T>(out, i, v);
+  store8f<T>(out + i * 8, v);
 }
 
 void bn_apply(hipStream_t st, bool f32, const void* x, int64_t M, int HW, int C, int Cp, const float* mean,
               const float* scale, const float* shift, int tab_stride, bool relu, void* out) {
-  dim3 g((unsigned)cdiv(M * Cp, 256));
+  const int CC = Cp / 8;
+  const int64_t n8 = M * CC;
+  if (n8 == 0) return;
+  PG_CHECK(Cp % 8 == 0 && n8 < (1LL << 31), "bn_apply: shape");
+  const FastDiv fdCC = make_fastdiv(CC), fdHW = make_fastdiv(HW);
+  dim3 g((unsigned)cdiv(n8, 256));
   if (f32)
-    hipLaunchKernelGGL(k_bn_apply<float>, g, dim3(256), 0, st, (const float*)x, M, HW, C, Cp, mean, scale, shift,
-                       tab_stride, (int)relu, (float*)out);
+    hipLaunchKernelGGL(k_bn_apply<float>, g, dim3(256), 0, st, (const float*)x, n8, CC, fdCC, fdHW, C, mean,
+                       scale, shift, tab_stride, (int)relu, (float*)out);
   else
-    hipLaunchKernelGGL(k_bn_apply<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, M, HW, C, Cp, mean, scale,
-                       shift, tab_stride, (int)relu, (bf16_t*)out);
+    hipLaunchKernelGGL(k_bn_apply<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, n8, CC, fdCC, fdHW, C, mean,
+                       scale, shift, tab_stride, (int)relu, (bf16_t*)out);
   PG_LAUNCH_CHECK();
 }
 
@@ -431,9 +517,86 @@ __global__ void k_cbn_tables(const float* cond, int dc, const float* Wg, const f
   scale[i] = c < C ? g * rstd[c] : 0.f;
 }
 
+// Small fp32 GEMM for the conditional-BN linear maps (B x dc by dc x C and
+// their transposes): C[i][j] = sum_k A(i, k) B(k, j) [/ *div] [+ C[i][j]],
+// A(i, k) = A[i * sai + k * sak], B(k, j) = B[k * sbk + j * sbj].  32 x 32
+// tiles through LDS, k in chunks of 32, fixed summation order.
+__global__ __launch_bounds__(256) void k_gemm_small(int M, int N, int K, const float* A, int64_t sai,
+                                                    int64_t sak, const float* Bm, int64_t sbk, int64_t sbj,
+                                                    float* Cm, int64_t ldc, const float* div, int acc) {
+  __shared__ float As[32][33], Bs[32][33];
+  const int i0 = blockIdx.y * 32, j0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  float c[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < K; k0 += 32) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = ty + 8 * q;
+      // the lane index runs along whichever dimension is contiguous
+      int ai, ak;
+      if (sak == 1) { ai = r; ak = tx; } else { ai = tx; ak = r; }
+      As[ai][ak] = (i0 + ai < M && k0 + ak < K) ? A[(i0 + ai) * sai + (int64_t)(k0 + ak) * sak] : 0.f;
+      int bk, bj;
+      if (sbj == 1) { bk = r; bj = tx; } else { bk = tx; bj = r; }
+      Bs[bk][bj] = (k0 + bk < K && j0 + bj < N) ? Bm[(int64_t)(k0 + bk) * sbk + (j0 + bj) * sbj] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int kk = 0; kk < 32; ++kk) {
+      const float b = Bs[kk][tx];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) c[q] = fmaf(As[ty + 8 * q][kk], b, c[q]);
+    }
+    __syncthreads();
+  }
+  const int j = j0 + tx;
+  if (j >= N) return;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = i0 + ty + 8 * q;
+    if (i >= M) continue;
+    float v = div ? c[q] / *div : c[q];
+    if (acc) v += Cm[(int64_t)i * ldc + j];
+    Cm[(int64_t)i * ldc + j] = v;
+  }
+}
+
+static void gemm_small(hipStream_t st, int M, int N, int K, const float* A, int64_t sai, int64_t sak,
+                       const float* Bm, int64_t sbk, int64_t sbj, float* Cm, int64_t ldc, const float* div,
+                       bool acc) {
+  if (M <= 0 || N <= 0) return;
+  hipLaunchKernelGGL(k_gemm_small, dim3((unsigned)cdiv(N, 32), (unsigned)cdiv(M, 32)), dim3(256), 0, st, M, N, K,
+                     A, sai, sak, Bm, sbk, sbj, Cm, ldc, div, (int)acc);
+}
+
+// gain = 1 + gain_raw, scale = gain * rstd; padded channels -> 0
+__global__ void k_cbn_fix(int B, int C, int Cp, const float* rstd, float* gain, float* bias, float* scale) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= B * Cp) return;
+  const int c = i % Cp;
+  if (c < C) {
+    const float g = 1.f + gain[i];
+    gain[i] = g;
+    scale[i] = g * rstd[c];
+  } else {
+    gain[i] = 0.f;
+    bias[i] = 0.f;
+    scale[i] = 0.f;
+  }
+}
+
 void cbn_tables(hipStream_t st, const float* cond, int dc, const float* Wg, const float* Wb,
                 const float* sg, const float* sb, const float* gain_p, const float* bias_p,
                 const float* rstd, int B, int C, int Cp, float* gain, float* bias, float* scale) {
+  if (cond) {
+    // gain_raw[b][c] = cond[b] . Wg[c] / sigma_g, bias[b][c] = cond[b] . Wb[c] / sigma_b
+    gemm_small(st, B, C, dc, cond, dc, 1, Wg, 1, dc, gain, Cp, sg, false);
+    gemm_small(st, B, C, dc, cond, dc, 1, Wb, 1, dc, bias, Cp, sb, false);
+    hipLaunchKernelGGL(k_cbn_fix, dim3((unsigned)cdiv((int64_t)B * Cp, 256)), dim3(256), 0, st, B, C, Cp, rstd,
+                       gain, bias, scale);
+    PG_LAUNCH_CHECK();
+    return;
+  }
   hipLaunchKernelGGL(k_cbn_tables, dim3((unsigned)cdiv((int64_t)B * Cp, 256)), dim3(256), 0, st, cond, dc,
                      Wg, Wb, sg, sb, gain_p, bias_p, rstd, B, C, Cp, gain, bias, scale);
   PG_LAUNCH_CHECK();
@@ -475,39 +638,62 @@ __global__ void k_bnb_reduce(const float* g, int g_up2, const T* x, int HW, int 
   }
 }
 
-// pass 2: dbias[b][c] = sum dz, dgain[b][c] = sum dz*xhat; per channel
-//   A[c] = sum_b gain[b][c] dbias[b][c] / N,  Bc[c] = sum_b gain[b][c] dgain[b][c] / N
-__global__ void k_bnb_fin(const float* p1, const float* p2, int nch, int B, int C, const float* gain,
-                          int tab_stride, int64_t N, float* dgain, float* dbias, float* A, float* Bc,
-                          int dg_stride) {
-  const int c = blockIdx.x * 256 + threadIdx.x;
-  if (c >= C) return;
-  float a = 0.f, bb = 0.f;
-  float ag = 0.f, ab = 0.f;   // per-channel totals (plain BN)
-  for (int b = 0; b < B; ++b) {
-    float s1 = 0.f, s2 = 0.f;
-    for (int j = 0; j < nch; ++j) {
-      const int64_t o = ((int64_t)b * nch + j) * C + c;
-      s1 += p1[o];
-      s2 += p2[o];
-    }
-    const float ga = gain[(int64_t)b * tab_stride + c];
-    a = fmaf(ga, s1, a);
-    bb = fmaf(ga, s2, bb);
-    if (dg_stride) {
-      dbias[(int64_t)b * dg_stride + c] = s1;
-      dgain[(int64_t)b * dg_stride + c] = s2;
-    } else {
+// pass 2a, per (sample, channel): s1 = sum of the chunk partials of dz,
+// s2 = of dz * xhat (fixed order), written over the first chunk's slot;
+// per-sample gain / bias gradients when dg_stride != 0.
+__global__ void k_bnb_fin1(float* p1, float* p2, int nch, int B, int C, float* dgain, float* dbias,
+                           int dg_stride) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)B * C) return;
+  const int b = (int)(i / C), c = (int)(i - (int64_t)b * C);
+  float s1 = 0.f, s2 = 0.f;
+  for (int j = 0; j < nch; ++j) {
+    const int64_t o = ((int64_t)b * nch + j) * C + c;
+    s1 += p1[o];
+    s2 += p2[o];
+  }
+  const int64_t o0 = (int64_t)b * nch * C + c;
+  p1[o0] = s1;
+  p2[o0] = s2;
+  if (dg_stride) {
+    dbias[(int64_t)b * dg_stride + c] = s1;
+    dgain[(int64_t)b * dg_stride + c] = s2;
+  }
+}
+
+// pass 2b, per channel: A = sum_b gain*s1 / N, Bc = sum_b gain*s2 / N (and the
+// plain-BN gain / bias gradients sum_b s2, sum_b s1); 16 waves stride the
+// samples, combined in order.
+__global__ __launch_bounds__(1024) void k_bnb_fin2(const float* p1, const float* p2, int nch, int B, int C,
+                                                   const float* gain, int tab_stride, int64_t N, float* dgain,
+                                                   float* dbias, float* A, float* Bc, int dg_stride) {
+  __shared__ float sh[4][16][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  float a = 0.f, bb = 0.f, ab = 0.f, ag = 0.f;
+  if (c < C)
+    for (int b = wv; b < B; b += 16) {
+      const int64_t o0 = (int64_t)b * nch * C + c;
+      const float s1 = p1[o0], s2 = p2[o0];
+      const float ga = gain[(int64_t)b * tab_stride + c];
+      a = fmaf(ga, s1, a);
+      bb = fmaf(ga, s2, bb);
       ab += s1;
       ag += s2;
     }
+  sh[0][wv][lane] = a; sh[1][wv][lane] = bb; sh[2][wv][lane] = ab; sh[3][wv][lane] = ag;
+  __syncthreads();
+  if (wv == 0 && c < C) {
+    float t[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int w = 0; w < 16; ++w)
+      for (int q = 0; q < 4; ++q) t[q] += sh[q][w][lane];
+    A[c] = t[0] / (float)N;
+    Bc[c] = t[1] / (float)N;
+    if (!dg_stride) {
+      dbias[c] = t[2];
+      dgain[c] = t[3];
+    }
   }
-  if (!dg_stride) {
-    dbias[c] = ab;
-    dgain[c] = ag;
-  }
-  A[c] = a / (float)N;
-  Bc[c] = bb / (float)N;
 }
 
 // pass 3: dx = rstd * (gain * dz - A - xhat * Bc) (+ res, at the same pixel)
@@ -566,7 +752,9 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
   else
     hipLaunchKernelGGL(k_bnb_reduce<bf16_t>, g1, dim3(nt), 0, st, g, (int)g_up2, (const bf16_t*)x, HW, H,
                        W, C, Cp, mean, rstd, gain, bias, tab_stride, rows_per, p1, p2);
-  hipLaunchKernelGGL(k_bnb_fin, dim3((unsigned)cdiv(C, 256)), dim3(256), 0, st, p1, p2, nch, B, C, gain,
+  hipLaunchKernelGGL(k_bnb_fin1, dim3((unsigned)cdiv((int64_t)B * C, 256)), dim3(256), 0, st, p1, p2, nch, B, C,
+                     dgain, dbias, dg_stride);
+  hipLaunchKernelGGL(k_bnb_fin2, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, p1, p2, nch, B, C, gain,
                      tab_stride, (int64_t)B * HW, dgain, dbias, A, Bc, dg_stride);
   const int64_t M = (int64_t)B * HW;
   dim3 g3((unsigned)cdiv(M * Cp, 256));
@@ -582,32 +770,11 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
 // Linear-map gradients of the conditional BN:
 //   dW[c][j] = sum_b dgb[b][c] cond[b][j]   (gradient of W/sigma; SN bwd follows)
 //   dcond[b][j] (+)= sum_c dgb[b][c] W[c][j] / sigma
-__global__ void k_cbn_lin_dw(const float* dgb, int B, int C, int Cp, const float* cond, int dc,
-                             float* dW) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= C * dc) return;
-  const int c = i / dc, j = i % dc;
-  float s = 0.f;
-  for (int b = 0; b < B; ++b) s = fmaf(dgb[(int64_t)b * Cp + c], cond[(int64_t)b * dc + j], s);
-  dW[i] = s;
-}
-__global__ void k_cbn_lin_dcond(const float* dgb, int B, int C, int Cp, const float* W, const float* sigma,
-                                int dc, int accumulate, float* dcond) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= B * dc) return;
-  const int b = i / dc, j = i % dc;
-  float s = 0.f;
-  for (int c = 0; c < C; ++c) s = fmaf(dgb[(int64_t)b * Cp + c], W[(int64_t)c * dc + j], s);
-  s = s / *sigma;
-  dcond[i] = accumulate ? dcond[i] + s : s;
-}
-
 void cbn_linear_bwd(hipStream_t st, const float* dgb, int B, int C, int Cp, const float* cond, int dc,
                     const float* W, const float* sigma, float* dW, float* dcond, bool accumulate) {
-  hipLaunchKernelGGL(k_cbn_lin_dw, dim3((unsigned)cdiv((int64_t)C * dc, 256)), dim3(256), 0, st, dgb, B, C,
-                     Cp, cond, dc, dW);
-  hipLaunchKernelGGL(k_cbn_lin_dcond, dim3((unsigned)cdiv((int64_t)B * dc, 256)), dim3(256), 0, st, dgb, B,
-                     C, Cp, W, sigma, dc, (int)accumulate, dcond);
+  // dW[c][j] = sum_b dgb[b][c] cond[b][j];  dcond[b][j] (+)= sum_c dgb[b][c] W[c][j] / sigma
+  gemm_small(st, C, dc, B, dgb, 1, Cp, cond, dc, 1, dW, dc, nullptr, false);
+  gemm_small(st, B, dc, C, dgb, Cp, 1, W, dc, 1, dcond, dc, sigma, accumulate);
   PG_LAUNCH_CHECK();
 }
 
