@@ -288,6 +288,8 @@ void DBlock::plan_saved(Arena& a) {
   wp2 = a.bytes((size_t)Cop * 9 * Cop * e);
   if (lsc) wpsc = a.bytes((size_t)Cop * Cip * e);
   h = a.bytes((size_t)B * H * W * Cop * e);
+  // the pooled block input, operand of the downsampling 1x1 skip
+  xp = lsc && down ? a.bytes((size_t)B * Ho * Wo * Cip * e) : nullptr;
 }
 
 struct DWsF {
@@ -362,7 +364,10 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   if (lsc) {
     ConvIn si;
     si.x = x; si.B = B; si.Hx = H; si.Wx = W; si.C = Cip; si.c_real = cin;
-    if (down) { si.gather = G_POOL2; si.gscale = 0.25f; }
+    if (down) {
+      avgpool2(ex.st, f32, x, B, H, W, Cip, xp);
+      si.x = xp; si.Hx = Ho; si.Wx = Wo;
+    }
     ConvOut so;
     so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b");
     conv_fwd(ex.st, f32, si, Ho, Wo, 1, wpsc, Cop, so);
@@ -419,7 +424,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     gs.g = dy; gs.Hs = Ho; gs.Ws = Wo; gs.C = Cop;
     ConvIn as;
     as.x = x; as.B = B; as.Hx = H; as.Wx = W; as.C = Cip; as.c_real = cin;
-    if (down) { as.gather = G_POOL2; as.gscale = 0.25f; }
+    if (down) { as.x = xp; as.Hx = Ho; as.Wx = Wo; }
     if (wgrad) {
       conv_wgrad(ex.st, f32, gs, as, Ho, Wo, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
       colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("sc.b"), w.cs);

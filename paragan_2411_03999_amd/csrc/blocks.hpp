@@ -112,6 +112,7 @@ struct DBlock {
   SNSlot sn[3];
   void *wp1 = nullptr, *wp2 = nullptr, *wpsc = nullptr;
   void* h = nullptr;
+  void* xp = nullptr;   // 2x2 average of the input (downsampling learnable skip)
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);

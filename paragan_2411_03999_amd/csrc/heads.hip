@@ -40,6 +40,7 @@ __global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* __restrict__ x,
                                                    float* img) {
   __shared__ float As[3][kHT + 2][kHC + 1];
   __shared__ float red[kHT][3];
+  __shared__ float tab[3][kHC];
   const int tiles_w = (W + kHT - 1) / kHT;
   const int bid = blockIdx.x;
   const int tw = bid % tiles_w;
@@ -50,6 +51,13 @@ __global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* __restrict__ x,
   const int half = __builtin_amdgcn_readfirstlane(t >> 7);
   float acc[3] = {0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < C; c0 += kHC) {
+    __syncthreads();
+    if (t < kHC) {
+      const int c = c0 + t;
+      tab[0][t] = c < C ? mean[c] : 0.f;
+      tab[1][t] = c < C ? scale[c] : 0.f;
+      tab[2][t] = c < C ? shift[c] : 0.f;
+    }
     __syncthreads();
     for (int idx = t; idx < 3 * (kHT + 2) * 4; idx += 256) {
       const int q = idx & 3;
@@ -63,8 +71,8 @@ __global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* __restrict__ x,
         unpack8(*reinterpret_cast<const uint4*>(x + (((int64_t)b * H + ih) * W + iw) * Cp + c0 + q * 8), v);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const int c = c0 + q * 8 + e;
-          v[e] = c < C ? fmaxf((v[e] - mean[c]) * scale[c] + shift[c], 0.f) : 0.f;
+          const int cl = q * 8 + e;
+          v[e] = c0 + cl < C ? fmaxf((v[e] - tab[0][cl]) * tab[1][cl] + tab[2][cl], 0.f) : 0.f;
         }
       }
 #pragma unroll
@@ -72,17 +80,35 @@ __global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* __restrict__ x,
     }
     __syncthreads();
     const int cb = c0 + half * 16;
-    const int nc = min(16, C - cb);
-    for (int r = 0; r < 3; ++r)
-      for (int s_ = 0; s_ < 3; ++s_) {
-        const float* wr = Wt + (r * 3 + s_) * C + cb;
-        for (int cc = 0; cc < nc; ++cc) {
-          const float av = As[r][p + s_][half * 16 + cc];
-          acc[0] = fmaf(av, wr[cc], acc[0]);
-          acc[1] = fmaf(av, wr[9 * C + cc], acc[1]);
-          acc[2] = fmaf(av, wr[18 * C + cc], acc[2]);
+    if (cb + 16 <= C) {
+#pragma unroll
+      for (int r = 0; r < 3; ++r)
+#pragma unroll
+        for (int s_ = 0; s_ < 3; ++s_) {
+          const float* wr = Wt + (r * 3 + s_) * C + cb;
+          float av[16];
+#pragma unroll
+          for (int cc = 0; cc < 16; ++cc) av[cc] = As[r][p + s_][half * 16 + cc];
+#pragma unroll
+          for (int cc = 0; cc < 16; ++cc) {
+            acc[0] = fmaf(av[cc], wr[cc], acc[0]);
+            acc[1] = fmaf(av[cc], wr[9 * C + cc], acc[1]);
+            acc[2] = fmaf(av[cc], wr[18 * C + cc], acc[2]);
+          }
         }
-      }
+    } else {
+      const int nc = max(0, C - cb);
+      for (int r = 0; r < 3; ++r)
+        for (int s_ = 0; s_ < 3; ++s_) {
+          const float* wr = Wt + (r * 3 + s_) * C + cb;
+          for (int cc = 0; cc < nc; ++cc) {
+            const float av = As[r][p + s_][half * 16 + cc];
+            acc[0] = fmaf(av, wr[cc], acc[0]);
+            acc[1] = fmaf(av, wr[9 * C + cc], acc[1]);
+            acc[2] = fmaf(av, wr[18 * C + cc], acc[2]);
+          }
+        }
+    }
   }
   if (half == 1) {
     red[p][0] = acc[0];

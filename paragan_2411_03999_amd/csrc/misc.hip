@@ -451,18 +451,17 @@ __global__ __launch_bounds__(256) void k_bn_apply(const T* x, int64_t n8, int CC
   const int p = (int)fdiv((uint32_t)i, fdCC);
   const int c0 = ((int)i - p * CC) * 8;
   const int b = (int)fdiv((uint32_t)p, fdHW);
-  float v[8];
+  float v[8], mu[8], sc[8], sh[8];
   load8f<T>(x + i * 8, v);
   const int64_t tb = (int64_t)b * tab_stride;
+  load8f<float>(mean + c0, mu);
+  load8f<float>(scale + tb + c0, sc);
+  load8f<float>(shift + tb + c0, sh);
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const int c = c0 + e;
-    float y = 0.f;
-    if (c < C) {
-      y = (v[e] - mean[c]) * scale[tb + c] + shift[tb + c];
-      if (relu) y = fmaxf(y, 0.f);
-    }
-    v[e] = y;
+    float y = (v[e] - mu[e]) * sc[e] + sh[e];
+    if (relu) y = fmaxf(y, 0.f);
+    v[e] = c0 + e < C ? y : 0.f;
   }
   store8f<T>(out + i * 8, v);
 }
@@ -472,7 +471,8 @@ void bn_apply(hipStream_t st, bool f32, const void* x, int64_t M, int HW, int C,
   const int CC = Cp / 8;
   const int64_t n8 = M * CC;
   if (n8 == 0) return;
-  PG_CHECK(Cp % 8 == 0 && n8 < (1LL << 31), "bn_apply: shape");
+  PG_CHECK(Cp % 8 == 0 && tab_stride % 8 == 0 && n8 < (1LL << 31), "bn_apply: shape");
+  PG_CHECK(((uintptr_t)mean | (uintptr_t)scale | (uintptr_t)shift) % 16 == 0, "bn_apply: table alignment");
   const FastDiv fdCC = make_fastdiv(CC), fdHW = make_fastdiv(HW);
   dim3 g((unsigned)cdiv(n8, 256));
   if (f32)
@@ -775,6 +775,53 @@ void cbn_linear_bwd(hipStream_t st, const float* dgb, int B, int C, int Cp, cons
   // dW[c][j] = sum_b dgb[b][c] cond[b][j];  dcond[b][j] (+)= sum_c dgb[b][c] W[c][j] / sigma
   gemm_small(st, C, dc, B, dgb, 1, Cp, cond, dc, 1, dW, dc, nullptr, false);
   gemm_small(st, B, dc, C, dgb, Cp, 1, W, dc, 1, dcond, dc, sigma, accumulate);
+  PG_LAUNCH_CHECK();
+}
+
+// 2x2 average pool, 8 channels per thread
+template <typename T>
+__global__ __launch_bounds__(256) void k_avgpool2(const T* x, int64_t n8, int CC, FastDiv fdCC, FastDiv fdWo,
+                                                  int Ho, int Wo, T* out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n8) return;
+  const int p = (int)fdiv((uint32_t)i, fdCC);
+  const int cc = (int)i - p * CC;
+  const int t = (int)fdiv((uint32_t)p, fdWo);
+  const int j = p - t * Wo;           // t = b * Ho + i
+  const int64_t W2 = 2LL * Wo;
+  const int64_t r0 = (2LL * t) * W2 + 2 * j;   // (b, 2i, 2j) as a pixel of the input
+  const int64_t Cp = (int64_t)CC * 8;
+  float a[8], v[8];
+  load8f<T>(x + r0 * Cp + cc * 8, a);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = a[e];
+  load8f<T>(x + (r0 + 1) * Cp + cc * 8, a);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] += a[e];
+  load8f<T>(x + (r0 + W2) * Cp + cc * 8, a);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] += a[e];
+  load8f<T>(x + (r0 + W2 + 1) * Cp + cc * 8, a);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (v[e] + a[e]) * 0.25f;
+  (void)Ho;
+  store8f<T>(out + i * 8, v);
+}
+
+void avgpool2(hipStream_t st, bool f32, const void* x, int B, int H, int W, int Cp, void* out) {
+  PG_CHECK(H % 2 == 0 && W % 2 == 0 && Cp % 8 == 0, "avgpool2: shape");
+  const int Ho = H / 2, Wo = W / 2, CC = Cp / 8;
+  const int64_t n8 = (int64_t)B * Ho * Wo * CC;
+  if (n8 == 0) return;
+  PG_CHECK(n8 < (1LL << 31), "avgpool2: size");
+  const FastDiv fdCC = make_fastdiv(CC), fdWo = make_fastdiv(Wo);
+  dim3 g((unsigned)cdiv(n8, 256));
+  if (f32)
+    hipLaunchKernelGGL(k_avgpool2<float>, g, dim3(256), 0, st, (const float*)x, n8, CC, fdCC, fdWo, Ho, Wo,
+                       (float*)out);
+  else
+    hipLaunchKernelGGL(k_avgpool2<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, n8, CC, fdCC, fdWo, Ho, Wo,
+                       (bf16_t*)out);
   PG_LAUNCH_CHECK();
 }
 

@@ -28,7 +28,8 @@ void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, 
 size_t bn_stats_ws_bytes(int64_t M, int C);
 void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float eps, float* mean,
               float* rstd, void* ws);
-// out = [relu]((x - mean) * scale + shift), per-(sample, channel) tables
+// out = [relu]((x - mean) * scale + shift), per-(sample, channel) tables;
+// mean has Cp entries and each table row (stride tab_stride) Cp, 16-byte aligned
 void bn_apply(hipStream_t st, bool f32, const void* x, int64_t M, int HW, int C, int Cp, const float* mean,
               const float* scale, const float* shift, int tab_stride, bool relu, void* out);
 void cbn_tables(hipStream_t st, const float* cond, int dc, const float* Wg, const float* Wb,
@@ -42,5 +43,8 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
 void cbn_linear_bwd(hipStream_t st, const float* dgb, int B, int C, int Cp, const float* cond, int dc,
                     const float* W, const float* sigma, float* dW, float* dcond, bool accumulate);
 void fill(hipStream_t st, float* p, int64_t n, float v);
+// out[b][i][j][c] = ((x[2i][2j] + x[2i][2j+1]) + x[2i+1][2j]) + x[2i+1][2j+1]) / 4, in the
+// activation type (NHWC, channel stride Cp; H and W even)
+void avgpool2(hipStream_t st, bool f32, const void* x, int B, int H, int W, int Cp, void* out);
 
 }  // namespace pg
