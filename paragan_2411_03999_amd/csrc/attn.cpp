@@ -31,15 +31,13 @@ void Attn::plan_saved(Arena& a) {
   wo = a.bytes((size_t)Cp * dv * 2);
   qkv = a.bytes((size_t)B * d.HW * Nqkv * 2);
   kp = a.bytes((size_t)B * d.Lp * dk * 2);
-  kt = a.bytes((size_t)B * d.Lp * dk * 2);
   vp = a.bytes((size_t)B * d.Lp * dv * 2);
-  vt = a.bytes((size_t)B * d.Lp * dv * 2);
   o = a.bytes((size_t)B * d.HW * dv * 2);
   lse = a.f32((size_t)B * d.HWp);
 }
 
 struct AWsB {
-  void *wdq, *wdo, *dO, *dOt, *qt, *dk, *dvv, *dqkv, *wg;
+  void *wdq, *wdo, *dO, *dk, *dvv, *dqkv, *wg;
   float *Dv, *dwq, *dwo, *part;
   size_t wg_bytes;
 };
@@ -51,8 +49,6 @@ static AWsB a_carve_b(const Attn& t, Arena& a, int n_cu) {
   w.wdq = a.bytes((size_t)t.Cp * t.Nqkv * 2);
   w.wdo = a.bytes((size_t)t.dv * t.Cp * 2);
   w.dO = a.bytes((size_t)M * t.dv * 2);
-  w.dOt = a.bytes((size_t)t.B * t.dv * d.HWp * 2);
-  w.qt = a.bytes((size_t)t.B * t.dk * d.HWp * 2);
   w.dk = a.bytes((size_t)t.B * d.Lp * t.dk * 2);
   w.dvv = a.bytes((size_t)t.B * d.Lp * t.dv * 2);
   w.dqkv = a.bytes((size_t)M * t.Nqkv * 2);
@@ -90,8 +86,8 @@ void Attn::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   ConvOut po;
   po.y = qkv; po.yC = Nqkv; po.n_real = Nqkv;
   conv_fwd(ex.st, false, in, H, W, 1, wqkv, Nqkv, po);
-  attn_pool(ex.st, d, qkv, kp, kt, vp, vt);
-  attn_fwd_core(ex.st, d, qkv, kp, vt, o, lse);
+  attn_pool(ex.st, d, qkv, kp, vp);
+  attn_fwd_core(ex.st, d, qkv, kp, vp, o, lse);
   ConvIn oi;
   oi.x = o; oi.B = B; oi.Hx = H; oi.Wx = W; oi.C = dv;
   ConvOut oo;
@@ -122,9 +118,7 @@ void Attn::bwd(const Exec& ex, const Params& P, const void* x, const void* dy, v
   ConvOut dOo;
   dOo.y = w.dO; dOo.yC = dv; dOo.n_real = dv; dOo.acc_scale = gamma;
   conv_fwd(ex.st, false, di, H, W, 1, w.wdo, dv, dOo);
-  attn_transpose(ex.st, d, qkv, Nqkv, 0, dk, w.qt);
-  attn_transpose(ex.st, d, w.dO, dv, 0, dv, w.dOt);
-  attn_bwd_core(ex.st, d, qkv, o, w.dO, kp, kt, vp, w.qt, w.dOt, lse, w.Dv, w.dk, w.dvv, w.dqkv);
+  attn_bwd_core(ex.st, d, qkv, w.dO, kp, vp, lse, w.Dv, w.dk, w.dvv, w.dqkv);
   // projections
   GradIn gq;
   gq.g = w.dqkv; gq.Hs = H; gq.Ws = W; gq.C = Nqkv;

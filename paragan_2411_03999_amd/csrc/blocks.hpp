@@ -130,9 +130,9 @@ struct Attn {
   SNSlot sn[4];
   void *wqkv = nullptr, *wo = nullptr;   // packed fwd weights
   void *qkv = nullptr;       // [B][H][W][Nqkv] bf16 projections (pre-pool)
-  void *kp = nullptr, *kt = nullptr, *vp = nullptr, *vt = nullptr;   // pooled keys/values
+  void *kp = nullptr, *vp = nullptr;   // pooled keys / values
   void *o = nullptr;         // attention output [B][HW][dv] bf16
-  float* lse = nullptr;      // [B][HW]
+  float* lse = nullptr;      // [B][HWp] log2-sum-exp2 of the scores
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);

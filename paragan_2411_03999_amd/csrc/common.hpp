@@ -22,12 +22,13 @@ __host__ __device__ inline int64_t cpad(int64_t c) { return (c + kCPad - 1) / kC
 __host__ __device__ inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
-// fp32 -> bf16, round to nearest even; NaN stays a (quiet) NaN.
-PG_DEV bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
+// fp32 -> bf16, round to nearest even (NaN stays NaN): gfx950's
+// v_cvt_pk_bf16_f32, two values per instruction.
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+PG_DEV bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+PG_DEV uint32_t f2bf2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2v));
 }
 PG_DEV float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
@@ -41,12 +42,7 @@ PG_DEV void unpack8(const uint4& q, float* f) {
   }
 }
 PG_DEV uint4 pack8(const float* f) {
-  uint4 q;
-  q.x = (uint32_t)f2bf(f[0]) | ((uint32_t)f2bf(f[1]) << 16);
-  q.y = (uint32_t)f2bf(f[2]) | ((uint32_t)f2bf(f[3]) << 16);
-  q.z = (uint32_t)f2bf(f[4]) | ((uint32_t)f2bf(f[5]) << 16);
-  q.w = (uint32_t)f2bf(f[6]) | ((uint32_t)f2bf(f[7]) << 16);
-  return q;
+  return make_uint4(f2bf2(f[0], f[1]), f2bf2(f[2], f[3]), f2bf2(f[4], f[5]), f2bf2(f[6], f[7]));
 }
 
 // ReLU on 8 packed bf16 by their bit patterns: a negative bf16 is a negative

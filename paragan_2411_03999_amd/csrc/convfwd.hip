@@ -99,8 +99,7 @@ PG_DEV void epi4(const ConvOut& o, int mo, int ridx, int n, float* v, float accs
   if (o.y_f32) {
     *reinterpret_cast<float4*>((float*)o.y + yi) = make_float4(v[0], v[1], v[2], v[3]);
   } else {
-    const uint2 q = make_uint2((uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16),
-                               (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16));
+    const uint2 q = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
     *reinterpret_cast<uint2*>((bf16_t*)o.y + yi) = q;
   }
 }
