@@ -304,7 +304,49 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
 
   Stager<4, 1> sk;
   Stager<NCV, (32 * NCV + 255) / 256> sv;
-  for (int pass = 0; pass < 2; ++pass) {
+  // one 32-key block of a pass; PASS and TAIL are compile-time so the
+  // per-element work has no branches
+  auto block = [&](auto pass_c, auto tail_c, const bf16_t* ks, const bf16_t* vs, int k0) {
+    constexpr int PASS = decltype(pass_c)::value;
+    constexpr bool TAIL = decltype(tail_c)::value;
+    f32x16 s[QT], dp[QT];
+#pragma unroll
+    for (int u = 0; u < QT; ++u)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) { s[u][r] = 0.f; dp[u][r] = 0.f; }
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const bf16x8 ka = ld_row<4>(ks, lq, 16 * t + 8 * g);
+#pragma unroll
+      for (int u = 0; u < QT; ++u) s[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[u][t], s[u], 0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < DV / 16; ++t) {
+      const bf16x8 va = ld_row<NCV>(vs, lq, 16 * t + 8 * g);
+#pragma unroll
+      for (int u = 0; u < QT; ++u) dp[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, db[u][t], dp[u], 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < QT; ++u) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float p = exp2_(fmaf(s[u][r], kL2E, -lq2[u]));
+        if (TAIL) p = k0 + acc_row(r, g) < L ? p : 0.f;
+        if (PASS == 0) dd[u] = fmaf(p, dp[u][r], dd[u]);
+        else s[u][r] = p * (dp[u][r] - dd[u]);
+      }
+    }
+    if (PASS == 1) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const bf16x8 ka = ld_tr<4>(ks, t, 0, lane);
+#pragma unroll
+        for (int u = 0; u < QT; ++u)
+          acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, pack_regs(s[u], t), acc[u], 0, 0, 0);
+      }
+    }
+  };
+  auto run = [&](auto pass_c) {
     sk.load(K, DK, 0, Lp, tid);
     sv.load(V, DV, 0, Lp, tid);
     __syncthreads();
@@ -318,46 +360,10 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
         sk.load(K, DK, k0 + 32, Lp, tid);
         sv.load(V, DV, k0 + 32, Lp, tid);
       }
-      const bf16_t* ks = Ks[buf];
-      const bf16_t* vs = Vs[buf];
-      f32x16 s[QT], dp[QT];
-#pragma unroll
-      for (int u = 0; u < QT; ++u)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) { s[u][r] = 0.f; dp[u][r] = 0.f; }
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const bf16x8 ka = ld_row<4>(ks, lq, 16 * t + 8 * g);
-#pragma unroll
-        for (int u = 0; u < QT; ++u) s[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qb[u][t], s[u], 0, 0, 0);
-      }
-#pragma unroll
-      for (int t = 0; t < DV / 16; ++t) {
-        const bf16x8 va = ld_row<NCV>(vs, lq, 16 * t + 8 * g);
-#pragma unroll
-        for (int u = 0; u < QT; ++u) dp[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, db[u][t], dp[u], 0, 0, 0);
-      }
-      const bool tail = k0 + 32 > L;
-#pragma unroll
-      for (int u = 0; u < QT; ++u) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          float p = exp2_(fmaf(s[u][r], kL2E, -lq2[u]));
-          if (tail && k0 + acc_row(r, g) >= L) p = 0.f;
-          if (!qv[u]) p = 0.f;
-          if (pass == 0) dd[u] = fmaf(p, dp[u][r], dd[u]);
-          else s[u][r] = p * (dp[u][r] - dd[u]);
-        }
-      }
-      if (pass == 1) {
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const bf16x8 ka = ld_tr<4>(ks, t, 0, lane);
-#pragma unroll
-          for (int u = 0; u < QT; ++u)
-            acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, pack_regs(s[u], t), acc[u], 0, 0, 0);
-        }
-      }
+      if (k0 + 32 > L)
+        block(pass_c, std::integral_constant<bool, true>(), Ks[buf], Vs[buf], k0);
+      else
+        block(pass_c, std::integral_constant<bool, false>(), Ks[buf], Vs[buf], k0);
       if (more) {
         sk.store(Ks[buf ^ 1], tid);
         sv.store(Vs[buf ^ 1], tid);
@@ -365,15 +371,17 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
       __syncthreads();
       buf ^= 1;
     }
-    if (pass == 0) {
+  };
+  // invalid queries have zero Q and dO rows and lse2 0: their dS rows are
+  // dropped at the store and their Dv is written as 0
+  run(std::integral_constant<int, 0>());
 #pragma unroll
-      for (int u = 0; u < QT; ++u) {
-        dd[u] = dd[u] + __shfl_xor(dd[u], 32, 64);
-        const int q = qw + 32 * u + lq;
-        if (g == 0 && q < HWp) Dv[(int64_t)b * HWp + q] = qv[u] ? dd[u] : 0.f;
-      }
-    }
+  for (int u = 0; u < QT; ++u) {
+    dd[u] = dd[u] + __shfl_xor(dd[u], 32, 64);
+    const int q = qw + 32 * u + lq;
+    if (g == 0 && q < HWp) Dv[(int64_t)b * HWp + q] = qv[u] ? dd[u] : 0.f;
   }
+  run(std::integral_constant<int, 1>());
 #pragma unroll
   for (int u = 0; u < QT; ++u) {
     const int q = qw + 32 * u + lq;
