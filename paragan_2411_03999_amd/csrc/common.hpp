@@ -45,6 +45,18 @@ PG_DEV uint4 pack8(const float* f) {
   return make_uint4(f2bf2(f[0], f[1]), f2bf2(f[2], f[3]), f2bf2(f[4], f[5]), f2bf2(f[6], f[7]));
 }
 
+// Raw buffer loads (gfx9 buffer resource: base, byte size, raw 32-bit
+// dwords).  A byte offset at or beyond the size reads zeros without touching
+// memory, so out-of-range rows need no branch: they get kOOB.
+constexpr uint32_t kOOB = 0xF0000000u;        // offsets from here on are out of range
+constexpr int64_t kBufMax = 0xF0000000LL;      // largest buffer (bytes) addressable this way
+PG_DEV __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)(uint32_t)bytes, 0x00020000);
+}
+PG_DEV uint4 buf_ld16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+}
+
 // ReLU on 8 packed bf16 by their bit patterns: a negative bf16 is a negative
 // int16, so max(v, 0) as packed int16 zeroes exactly the negatives (and -0).
 typedef short short2v __attribute__((ext_vector_type(2)));

@@ -22,6 +22,7 @@ namespace {
 struct CfK {
   const bf16_t* x;
   const bf16_t* w;
+  int64_t x_bytes, w_bytes;
   int Hx, Wx, C;        // activation source (C = channel stride)
   int H, W, R, pad;     // conv grid
   int M, Np, ksteps;
@@ -59,7 +60,7 @@ PG_DEV void pix_of(const CfK& k, int m, bool quad, int& b, int& oh, int& ow) {
   }
 }
 
-PG_DEV void load4(const void* p, bool f32, int64_t i, float* v) {
+PG_DEV void load4(const void* p, bool f32, int i, float* v) {
   if (f32) {
     const float4 q = *reinterpret_cast<const float4*>((const float*)p + i);
     v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
@@ -72,36 +73,12 @@ PG_DEV void load4(const void* p, bool f32, int64_t i, float* v) {
   }
 }
 
-// bias, ReLU mask, residual and store of 4 consecutive channels n..n+3 of
-// output pixel mo (residual pixel ridx)
-PG_DEV void epi4(const ConvOut& o, int mo, int ridx, int n, float* v, float accs) {
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const float bias = (o.bias && n + e < o.n_real) ? o.bias[n + e] : 0.f;
-    v[e] = v[e] * accs + bias;
-  }
-  if (o.mask) {
-    float mk[4];
-    load4(o.mask, o.mask_f32, (int64_t)mo * o.maskC + n, mk);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] = mk[e] > 0.f ? v[e] : 0.f;
-  }
-  if (o.res_mode != R_NONE) {
-    float rv[4];
-    load4(o.res, o.res_f32, (int64_t)ridx * o.resC + n, rv);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) v[e] += o.res_scale * rv[e];
-  }
-#pragma unroll
-  for (int e = 0; e < 4; ++e)
-    if (n + e >= o.n_real) v[e] = 0.f;
-  const int64_t yi = (int64_t)mo * o.yC + n;
-  if (o.y_f32) {
-    *reinterpret_cast<float4*>((float*)o.y + yi) = make_float4(v[0], v[1], v[2], v[3]);
-  } else {
-    const uint2 q = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
-    *reinterpret_cast<uint2*>((bf16_t*)o.y + yi) = q;
-  }
+// value of lane ^ 1 / lane ^ 2 (DPP quad permutations [1,0,3,2] / [2,3,0,1])
+PG_DEV float dpp_xor1(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+}
+PG_DEV float dpp_xor2(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
 }
 
 // swizzled element offset of (row r, 16-byte chunk c) in a tile of 32-element rows
@@ -132,27 +109,27 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
     rv[p] = m < k.M;
     pix_of(k, rv[p] ? m : 0, quad, rb[p], roh[p], row_[p]);
   }
-  int roff[AP];
-  bool rok[AP];
+  // byte offsets of this thread's 16-byte chunks (kOOB: reads zeros)
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(k.x, k.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(k.w, k.w_bytes);
+  uint32_t roff[AP];
   auto set_tap = [&](int tap) {
     const int r = tap / R, s = tap - (tap / R) * R;
 #pragma unroll
     for (int p = 0; p < AP; ++p) {
       const int ih = roh[p] + r - pad, iw = row_[p] + s - pad;
-      rok[p] = rv[p] && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W;
+      const bool ok = rv[p] && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W;
       const int sh = GATHER == G_UP2 ? (ih >> 1) : ih;
       const int sw = GATHER == G_UP2 ? (iw >> 1) : iw;
-      roff[p] = rok[p] ? ((rb[p] * k.Hx + sh) * k.Wx + sw) * C + q * 8 : 0;
+      roff[p] = ok ? (uint32_t)(((rb[p] * k.Hx + sh) * k.Wx + sw) * C + q * 8) * 2u : kOOB;
     }
   };
-  int woff[BP];
-  bool wok[BP];
+  uint32_t woff[BP];
 #pragma unroll
   for (int p = 0; p < BP; ++p) {
     const int idx = tid + 256 * p;
     const int n = n0 + (idx >> 2);
-    wok[p] = idx < BN * 4 && n < k.Np;
-    woff[p] = wok[p] ? n * R * R * C + (idx & 3) * 8 : 0;
+    woff[p] = idx < BN * 4 && n < k.Np ? (uint32_t)(n * R * R * C + (idx & 3) * 8) * 2u : kOOB;
   }
   // LDS staging offsets (fixed across steps)
   int xst[AP], wst[BP];
@@ -169,11 +146,9 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   set_tap(0);
   auto load = [&]() {
 #pragma unroll
-    for (int p = 0; p < AP; ++p)
-      ra[p] = rok[p] ? *reinterpret_cast<const uint4*>(k.x + roff[p] + ld_c0) : make_uint4(0, 0, 0, 0);
+    for (int p = 0; p < AP; ++p) ra[p] = buf_ld16(xr, roff[p] + 2u * ld_c0);
 #pragma unroll
-    for (int p = 0; p < BP; ++p)
-      rw[p] = wok[p] ? *reinterpret_cast<const uint4*>(k.w + woff[p] + ld_ks * 32) : make_uint4(0, 0, 0, 0);
+    for (int p = 0; p < BP; ++p) rw[p] = buf_ld16(wr, woff[p] + 64u * ld_ks);
     ++ld_ks;
     ld_c0 += 32;
     if (ld_c0 == C) {
@@ -232,38 +207,74 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
     buf ^= 1;
   }
 
-  // ---- epilogue: lane holds channels 8g + 4h + (0..3) of pixel m
+  // ---- epilogue: lane holds channels 8g + 4h + (0..3) of pixel m.
+  // Per pixel tile: 32-bit element offsets of the output, mask and residual
+  // rows (the host guarantees they fit); per channel group: the bias.
   const ConvOut& o = k.o;
   const float accs = (o.acc_scale ? *o.acc_scale : 1.f) * o.acc_mul;
+  int yo[TM], mko[TM], ro[TM];
+  bool wr_ok[TM];
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
     const int m = m0 + (wm * TM + j) * 32 + lr;
     const bool mv = m < k.M;
     const int mo = quad ? (m >> 2) : m;
+    wr_ok[j] = mv && (!quad || (lr & 3) == 0);
+    yo[j] = mo * o.yC;
+    mko[j] = mo * o.maskC;
     int ridx = mo;
     if (o.res_mode == R_HALF) {
-      int b, oh, ow;
-      pix_of(k, mv ? m : 0, false, b, oh, ow);
-      ridx = (b * (k.H >> 1) + (oh >> 1)) * (k.W >> 1) + (ow >> 1);
+      int bb, oh, ow;
+      pix_of(k, mv ? m : 0, false, bb, oh, ow);
+      ridx = (bb * (k.H >> 1) + (oh >> 1)) * (k.W >> 1) + (ow >> 1);
     }
+    ro[j] = ridx * o.resC;
+  }
 #pragma unroll
-    for (int i = 0; i < TN; ++i) {
+  for (int i = 0; i < TN; ++i) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int n = n0 + (wn * TN + i) * 32 + 8 * g + 4 * h;
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const int n = n0 + (wn * TN + i) * 32 + 8 * g4 + 4 * h;
+      float bias[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bias[e] = (o.bias && n + e < o.n_real) ? o.bias[n + e] : 0.f;
+      const bool n_ok = n < o.yC;
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g + e];
+        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g4 + e];
         if (quad) {
           // 2x2 average over the four consecutive rows (lanes) of a window
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float t = v[e] + __shfl_xor(v[e], 1, 64);
-            v[e] = 0.25f * (t + __shfl_xor(t, 2, 64));
+            const float t = v[e] + dpp_xor1(v[e]);
+            v[e] = 0.25f * (t + dpp_xor2(t));
           }
         }
-        if (!mv || n >= o.yC || (quad && (lr & 3))) continue;
-        epi4(o, mo, ridx, n, v, accs);
+        if (!(wr_ok[j] && n_ok)) continue;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = v[e] * accs + bias[e];
+        if (o.mask) {
+          float mk[4];
+          load4(o.mask, o.mask_f32, mko[j] + n, mk);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = mk[e] > 0.f ? v[e] : 0.f;
+        }
+        if (o.res_mode != R_NONE) {
+          float rv[4];
+          load4(o.res, o.res_f32, ro[j] + n, rv);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += o.res_scale * rv[e];
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (n + e >= o.n_real) v[e] = 0.f;
+        if (o.y_f32) {
+          *reinterpret_cast<float4*>((float*)o.y + (yo[j] + n)) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          *reinterpret_cast<uint2*>((bf16_t*)o.y + (yo[j] + n)) = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
+        }
       }
     }
   }
@@ -300,6 +311,7 @@ bool conv_fwd_mfma_ok(const ConvIn& in, int H, int W, int R, int Np, const ConvO
   const int64_t ws = (int64_t)Np * R * R * in.C;
   const int cmax = std::max({o.yC, o.resC, o.maskC});
   if (M >= (1LL << 31) || xs >= (1LL << 31) || ws >= (1LL << 31) || Mo * cmax >= (1LL << 31)) return false;
+  if (2 * xs >= kBufMax || 2 * ws >= kBufMax) return false;
   if (o.yC % 4 || (o.res_mode != R_NONE && o.resC % 4) || (o.mask && o.maskC % 4)) return false;
   if (!aligned16(o.y) || (o.res && !aligned16(o.res)) || (o.mask && !aligned16(o.mask))) return false;
   if (o.pool && o.res_mode == R_HALF) return false;
@@ -312,6 +324,8 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   CfK k;
   k.x = (const bf16_t*)in.x;
   k.w = (const bf16_t*)w;
+  k.x_bytes = 2LL * in.B * in.Hx * in.Wx * in.C;
+  k.w_bytes = 2LL * Np * R * R * in.C;
   k.Hx = in.Hx;
   k.Wx = in.Wx;
   k.C = in.C;

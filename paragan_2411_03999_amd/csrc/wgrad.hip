@@ -52,6 +52,7 @@ PG_DEV bf16x8 tr_pair(const bf16_t* base, int off_lo, int off_hi) {
 struct WgTrK {
   const bf16_t* g;   // gradient source, channel stride gC
   const bf16_t* x;   // activation source [B][Hx][Wx][C]
+  int64_t g_bytes, x_bytes;
   int gC, Np, Kdim, C, R, pad;
   int H, W;          // conv grid
   int Hx, Wx;        // activation source dims
@@ -124,38 +125,35 @@ __global__ __launch_bounds__(256, 2) void k_wgrad_tr(WgTrK k) {
   }
 
   uint4 rg[GIT], rx[XIT];
+  const __amdgpu_buffer_rsrc_t gr = make_rsrc(k.g, k.g_bytes);
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(k.x, k.x_bytes);
   auto load = [&](int mb) {
 #pragma unroll
     for (int i = 0; i < GIT; ++i) {
       const int m = mb + g_row[i];
-      rg[i] = make_uint4(0, 0, 0, 0);
-      if (g_on[i] && m < mend) {
-        int off;
-        if (!GUP) {
-          off = m * k.gC + g_col[i];
-        } else {
-          const int t = (int)fdiv((uint32_t)m, k.fdW);
-          const int ow = m - t * k.W;
-          const int b = (int)fdiv((uint32_t)t, k.fdH);
-          const int oh = t - b * k.H;
-          off = ((b * k.Hs + (oh >> 1)) * k.Ws + (ow >> 1)) * k.gC + g_col[i];
-        }
-        rg[i] = *reinterpret_cast<const uint4*>(k.g + off);
+      int off;
+      if (!GUP) {
+        off = m * k.gC + g_col[i];
+      } else {
+        const int t = (int)fdiv((uint32_t)m, k.fdW);
+        const int ow = m - t * k.W;
+        const int b = (int)fdiv((uint32_t)t, k.fdH);
+        const int oh = t - b * k.H;
+        off = ((b * k.Hs + (oh >> 1)) * k.Ws + (ow >> 1)) * k.gC + g_col[i];
       }
+      rg[i] = buf_ld16(gr, g_on[i] && m < mend ? 2u * (uint32_t)off : kOOB);
     }
 #pragma unroll
     for (int i = 0; i < XIT; ++i) {
       const int m = mb + x_row[i];
-      rx[i] = make_uint4(0, 0, 0, 0);
       const int t = (int)fdiv((uint32_t)m, k.fdW);
       const int ow = m - t * k.W;
       const int b = (int)fdiv((uint32_t)t, k.fdH);
       const int oh = t - b * k.H;
       const int ih = oh + (short)(x_rs[i] & 0xffff), iw = ow + (x_rs[i] >> 16);
-      if (m < mend && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W) {
-        const int sh = XG == G_UP2 ? (ih >> 1) : ih, sw = XG == G_UP2 ? (iw >> 1) : iw;
-        rx[i] = *reinterpret_cast<const uint4*>(k.x + ((b * k.Hx + sh) * k.Wx + sw) * k.C + x_c[i]);
-      }
+      const bool ok = m < mend && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W;
+      const int sh = XG == G_UP2 ? (ih >> 1) : ih, sw = XG == G_UP2 ? (iw >> 1) : iw;
+      rx[i] = buf_ld16(xr, ok ? 2u * (uint32_t)(((b * k.Hx + sh) * k.Wx + sw) * k.C + x_c[i]) : kOOB);
     }
   };
   auto store = [&](int buf) {
@@ -307,8 +305,8 @@ bool wgrad_tr_ok(const GradIn& g, const ConvIn& in, int H, int W, int R, int Np)
   const int64_t M = (int64_t)in.B * H * W;
   const int64_t xs = (int64_t)in.B * in.Hx * in.Wx * in.C;
   const int64_t gs = g.gather == G_DIRECT ? M * g.C : (int64_t)in.B * g.Hs * g.Ws * g.C;
-  return M < (1LL << 30) && xs < (1LL << 31) && gs < (1LL << 31) && in.C % 8 == 0 && g.C % 8 == 0 &&
-         Np % 8 == 0;
+  return M < (1LL << 30) && xs < (1LL << 31) && gs < (1LL << 31) && 2 * xs < kBufMax && 2 * gs < kBufMax &&
+         in.C % 8 == 0 && g.C % 8 == 0 && Np % 8 == 0;
 }
 
 size_t wgrad_tr_ws(int64_t M, int R, int Cin, int Np, int n_cu) {
@@ -321,6 +319,8 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   WgTrK k;
   k.g = (const bf16_t*)g.g;
   k.x = (const bf16_t*)in.x;
+  k.x_bytes = 2LL * in.B * in.Hx * in.Wx * in.C;
+  k.g_bytes = 2LL * (g.gather == G_DIRECT ? (int64_t)in.B * H * W : (int64_t)in.B * g.Hs * g.Ws) * g.C;
   k.gC = g.C;
   k.Np = Np;
   k.Kdim = R * R * in.C;
