@@ -123,6 +123,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batch", type=int, default=1)
     ap.add_argument("--kernels-out", default=None, help="write the per-kernel table (JSON) here")
+    ap.add_argument("--detail", action="store_true",
+                    help="profile per GEMM shape (names carry [M,N,K]); the roofline is then per shape")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only (--gpus %d requested); the multi-GPU data-parallel "
@@ -177,7 +179,7 @@ def main():
         step()
         print("bench: warmup step %d losses %s" % (i, list(losses)), file=sys.stderr, flush=True)
     torch.cuda.synchronize()
-    lib.paragan_profile(ctx, True)
+    lib.paragan_profile(ctx, 2 if args.detail else 1)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     ev0.record()
@@ -205,8 +207,8 @@ def main():
     if args.kernels_out:
         with open(args.kernels_out, "w") as f:
             json.dump(stats, f, indent=1)
-    for s in stats[:12]:
-        print("bench: %-40s %6d launches %9.2f ms %8.1f TFLOP/s" % (
+    for s in stats[:(60 if args.detail else 12)]:
+        print("bench: %-62s %6d launches %9.2f ms %8.1f TFLOP/s" % (
             s["name"], s["launches"], s["total_ms"], s["flops"] / max(s["total_ms"], 1e-9) / 1e9),
             file=sys.stderr)
     out = {

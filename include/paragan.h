@@ -259,6 +259,10 @@ int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
  * paragan_profile_read synchronises the stream, aggregates the records by
  * kernel name into `out` (up to `cap` entries; *count = number of kernels)
  * and clears them.  Off by default; costs two event records per launch.
+ * enable = 1 turns it on; enable = 2 also appends each convolution and
+ * weight-gradient launch's GEMM shape "[M,N,K]" to its name (rows =
+ * pixels, N = padded output channels, K = padded taps x input channels),
+ * so launches of one template instance aggregate per shape; 0 turns it off.
  * ------------------------------------------------------------------- */
 typedef struct {
   char name[64];

@@ -455,6 +455,7 @@ extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d
 extern "C" int paragan_profile(paragan_ctx* ctx, int enable) {
   if (!ctx) return PARAGAN_EINVAL;
   ctx->prof.on = enable != 0;
+  ctx->prof.detail = enable == 2;
   return PARAGAN_OK;
 }
 

@@ -109,6 +109,7 @@ struct ProfRec {
 };
 struct Profiler {
   bool on = false;
+  bool detail = false;   // tag each record with its GEMM shape
   std::vector<ProfRec> recs;
   std::vector<hipEvent_t> pool;
   hipEvent_t ev() {
@@ -141,6 +142,12 @@ struct ProfScope {
     (void)hipEventRecord(b, st);
     p->recs.push_back(ProfRec{name, flops, a, b});
     a = nullptr;
+  }
+  // as done(), with the launch's GEMM shape appended in detail mode
+  void done(const std::string& name, double flops, int64_t m, int64_t n, int64_t k) {
+    if (!a) return;
+    if (!p->detail) return done(name, flops);
+    done(name + "[" + std::to_string(m) + "," + std::to_string(n) + "," + std::to_string(k) + "]", flops);
   }
 };
 }  // namespace pg

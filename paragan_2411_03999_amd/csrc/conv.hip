@@ -473,7 +473,7 @@ void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
     if (conv_fwd_mfma_ok(in2, H, W, R, Np, k.o)) {
       const std::string name = conv_fwd_mfma(s, in2, H, W, R, w, Np, k.o);
       PG_LAUNCH_CHECK();
-      prof.done(name, flops);
+      prof.done(name, flops, k.a.M, Np, (int64_t)R * R * in.C);
       return;
     }
   }
@@ -489,7 +489,7 @@ void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
   else
     name = launch_mfma_cfg<2, 2, 2, 2>(s, k, in.gather, aff, in.relu);
   PG_LAUNCH_CHECK();
-  prof.done(name, flops);
+  prof.done(name, flops, k.a.M, Np, (int64_t)R * R * in.C);
 }
 
 // ================================================================ wgrad
@@ -846,7 +846,7 @@ void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in, int 
 #undef PG_WG_CASE
   if (!done) throw Error{-2, "conv_wgrad: unsupported prologue combination"};
   PG_LAUNCH_CHECK();
-  prof.done(name, flops);
+  prof.done(name, flops, k.a.M, Np, k.Kdim);
   if (k.splits > 1 || g.gscale != 1.f) {
     hipLaunchKernelGGL(k_split_reduce, dim3((unsigned)cdiv(nout, 256)), dim3(256), 0, s,
                        k.part, k.splits, nout, g.gscale, dw);

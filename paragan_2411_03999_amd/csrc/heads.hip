@@ -25,198 +25,310 @@ void img_to_bf16(hipStream_t st, const float* img, int64_t npix, int Cp, void* o
 
 // --------------------------------------------------- generator output layer
 // a = relu((x - mean) * scale + shift) (per channel), img = tanh(conv3x3(a) / sigma + b),
-// all in fp32.  A block computes 128 pixels of one image row: per chunk of
-// 32 channels it stages the three input rows it needs, already normalised,
-// in LDS (each element transformed once), then each thread accumulates one
-// pixel over half of the chunk's channels with the weights read as
-// wave-uniform scalars; the two halves combine in a fixed order.
-constexpr int kHT = 128;
-constexpr int kHC = 32;
+// all in fp32 on the vector ALUs (three output channels leave nothing for a
+// matrix unit to tile).  A block computes a 16-row x 64-column output tile:
+// per chunk of 8 channels it stages the haloed input tile, normalised once
+// per element, in LDS as [row][channel][column]; each lane then owns one
+// column of a 4-row strip (its wave's rows), so every staged value it reads
+// feeds up to 4 pixels x 3 outputs.  Weights sit in LDS as [c][27] and are
+// read as wave-wide broadcasts.
+constexpr int kFR = 16;   // output rows per block (4 waves x 4-row strips)
+constexpr int kFC = 64;   // output columns per block (one per lane)
+constexpr int kFK = 8;    // channels per staged chunk
 
 __global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* __restrict__ x, int B, int H, int W, int C, int Cp,
                                                    const float* __restrict__ mean, const float* __restrict__ scale,
                                                    const float* __restrict__ shift, const float* __restrict__ Wt,
-                                                   const float* sigma, const float* __restrict__ bias,
-                                                   float* img) {
-  __shared__ float As[3][kHT + 2][kHC + 1];
-  __shared__ float red[kHT][3];
-  __shared__ float tab[3][kHC];
-  const int tiles_w = (W + kHT - 1) / kHT;
-  const int bid = blockIdx.x;
+                                                   const float* __restrict__ sigma, const float* __restrict__ bias,
+                                                   float* __restrict__ img) {
+  __shared__ float L[kFR + 2][kFK][kFC + 2];
+  extern __shared__ float4 wsh4[];     // [C][7] float4: the 27 weights of channel c, then padding
+  float* wsh = reinterpret_cast<float*>(wsh4);
+  for (int i = threadIdx.x; i < 28 * C; i += 256) {
+    const int c = i / 28, k = i - c * 28;
+    wsh[i] = k < 27 ? Wt[k * C + c] : 0.f;
+  }
+  const int tiles_w = (W + kFC - 1) / kFC, tiles_h = (H + kFR - 1) / kFR;
+  int bid = blockIdx.x;
   const int tw = bid % tiles_w;
-  const int bh = bid / tiles_w;
-  const int h = bh % H, b = bh / H;
-  const int w0 = tw * kHT;
-  const int t = threadIdx.x, p = t & (kHT - 1);
-  const int half = __builtin_amdgcn_readfirstlane(t >> 7);
-  float acc[3] = {0.f, 0.f, 0.f};
-  for (int c0 = 0; c0 < C; c0 += kHC) {
+  bid /= tiles_w;
+  const int th = bid % tiles_h;
+  const int b = bid / tiles_h;
+  const int h0 = th * kFR, w0 = tw * kFC;
+  const int t = threadIdx.x, tx = t & 63;
+  const int ty = __builtin_amdgcn_readfirstlane(t >> 6);
+  float acc[4][3];
+#pragma unroll
+  for (int o = 0; o < 4; ++o) acc[o][0] = acc[o][1] = acc[o][2] = 0.f;
+  for (int c0 = 0; c0 < C; c0 += kFK) {
     __syncthreads();
-    if (t < kHC) {
-      const int c = c0 + t;
-      tab[0][t] = c < C ? mean[c] : 0.f;
-      tab[1][t] = c < C ? scale[c] : 0.f;
-      tab[2][t] = c < C ? shift[c] : 0.f;
-    }
-    __syncthreads();
-    for (int idx = t; idx < 3 * (kHT + 2) * 4; idx += 256) {
-      const int q = idx & 3;
-      const int pix = (idx >> 2) % (kHT + 2);
-      const int r = (idx >> 2) / (kHT + 2);
-      const int ih = h + r - 1, iw = w0 + pix - 1;
+    for (int idx = t; idx < (kFR + 2) * (kFC + 2); idx += 256) {
+      const int r = idx / (kFC + 2), col = idx - r * (kFC + 2);
+      const int ih = h0 + r - 1, iw = w0 + col - 1;
       float v[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) v[e] = 0.f;
-      if (ih >= 0 && ih < H && iw >= 0 && iw < W) {
-        unpack8(*reinterpret_cast<const uint4*>(x + (((int64_t)b * H + ih) * W + iw) * Cp + c0 + q * 8), v);
+      if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W) {
+        unpack8(*reinterpret_cast<const uint4*>(x + (((int64_t)b * H + ih) * W + iw) * Cp + c0), v);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
-          const int cl = q * 8 + e;
-          v[e] = c0 + cl < C ? fmaxf((v[e] - tab[0][cl]) * tab[1][cl] + tab[2][cl], 0.f) : 0.f;
+          const int c = c0 + e;
+          v[e] = c < C ? fmaxf((v[e] - mean[c]) * scale[c] + shift[c], 0.f) : 0.f;
         }
       }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) As[r][pix][q * 8 + e] = v[e];
+      for (int e = 0; e < 8; ++e) L[r][e][col] = v[e];
     }
     __syncthreads();
-    const int cb = c0 + half * 16;
-    if (cb + 16 <= C) {
+    const int nk = min(kFK, C - c0);
 #pragma unroll
-      for (int r = 0; r < 3; ++r)
+    for (int cc = 0; cc < kFK; ++cc) {
+      if (cc >= nk) break;
+      float w[28];
+#pragma unroll
+      for (int q = 0; q < 7; ++q) {
+        const float4 f = wsh4[(c0 + cc) * 7 + q];
+        w[4 * q] = f.x; w[4 * q + 1] = f.y; w[4 * q + 2] = f.z; w[4 * q + 3] = f.w;
+      }
+#pragma unroll
+      for (int rr = 0; rr < 6; ++rr)
 #pragma unroll
         for (int s_ = 0; s_ < 3; ++s_) {
-          const float* wr = Wt + (r * 3 + s_) * C + cb;
-          float av[16];
+          const float v = L[4 * ty + rr][cc][tx + s_];
 #pragma unroll
-          for (int cc = 0; cc < 16; ++cc) av[cc] = As[r][p + s_][half * 16 + cc];
+          for (int o = 0; o < 4; ++o) {
+            const int r = rr - o;
+            if (r >= 0 && r <= 2) {
 #pragma unroll
-          for (int cc = 0; cc < 16; ++cc) {
-            acc[0] = fmaf(av[cc], wr[cc], acc[0]);
-            acc[1] = fmaf(av[cc], wr[9 * C + cc], acc[1]);
-            acc[2] = fmaf(av[cc], wr[18 * C + cc], acc[2]);
-          }
-        }
-    } else {
-      const int nc = max(0, C - cb);
-      for (int r = 0; r < 3; ++r)
-        for (int s_ = 0; s_ < 3; ++s_) {
-          const float* wr = Wt + (r * 3 + s_) * C + cb;
-          for (int cc = 0; cc < nc; ++cc) {
-            const float av = As[r][p + s_][half * 16 + cc];
-            acc[0] = fmaf(av, wr[cc], acc[0]);
-            acc[1] = fmaf(av, wr[9 * C + cc], acc[1]);
-            acc[2] = fmaf(av, wr[18 * C + cc], acc[2]);
+              for (int co = 0; co < 3; ++co) acc[o][co] = fmaf(v, w[co * 9 + r * 3 + s_], acc[o][co]);
+            }
           }
         }
     }
   }
-  if (half == 1) {
-    red[p][0] = acc[0];
-    red[p][1] = acc[1];
-    red[p][2] = acc[2];
-  }
-  __syncthreads();
-  if (half == 0 && w0 + p < W) {
-    const float inv = 1.f / *sigma;
-    const int64_t o = (((int64_t)b * H + h) * W + w0 + p) * 3;
+  const float inv = 1.f / *sigma;
+  const int ow = w0 + tx;
 #pragma unroll
-    for (int co = 0; co < 3; ++co) img[o + co] = tanhf((acc[co] + red[p][co]) * inv + bias[co]);
+  for (int o = 0; o < 4; ++o) {
+    const int oh = h0 + 4 * ty + o;
+    if (oh < H && ow < W) {
+      const int64_t q = (((int64_t)b * H + oh) * W + ow) * 3;
+#pragma unroll
+      for (int co = 0; co < 3; ++co) img[q + co] = tanhf(acc[o][co] * inv + bias[co]);
+    }
   }
 }
 
 // da[p][c] = sum_{tap, co} dt[p - tap][co] * W[co][tap][c] / sigma,
-// dt = dimg * (1 - img^2).   dimg has channel stride ldd (>= 3).
-__global__ __launch_bounds__(256) void k_ghead_dgrad(const float* dimg, int ldd, const float* img, int B, int H,
-                                                     int W, int C, int Cp, const float* Wt, const float* sigma,
-                                                     float* da) {
-  extern __shared__ float sw[];
-  const int n = 27 * C;
+// dt = dimg * (1 - img^2) (dimg has channel stride ldd >= 3).  A block
+// computes a 2-row x 64-column tile of pixels, all Cp channels: dt of the
+// haloed tile is staged in LDS once ([row][col][4], one 16-byte read per
+// position), the weights as [tap*3][Cp] scaled by 1/sigma (zero for
+// channels >= C).  A work item is 4 consecutive channels x 4 consecutive
+// pixels of a row: 432 FMAs per 18 + 27 LDS reads, one 16-byte store per
+// pixel (lanes run over channels, so the stores are contiguous).
+constexpr int kDR = 2;     // output rows per block
+constexpr int kDC = 64;    // output columns per block
+
+__global__ __launch_bounds__(256) void k_ghead_dgrad(const float* __restrict__ dimg, int ldd,
+                                                     const float* __restrict__ img, int B, int H, int W, int C,
+                                                     int Cp, const float* __restrict__ Wt,
+                                                     const float* __restrict__ sigma, float* __restrict__ da) {
+  __shared__ float4 dts[kDR + 2][kDC + 2];
+  extern __shared__ float4 wsd4[];    // [27][Cp / 4]
+  float* wsd = reinterpret_cast<float*>(wsd4);
   const float inv = 1.f / *sigma;
-  for (int i = threadIdx.x; i < n; i += 256) sw[i] = Wt[i] * inv;
-  __syncthreads();
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (int64_t)B * H * W * Cp) return;
-  const int c = (int)(i % Cp);
-  const int64_t p = i / Cp;
-  if (c >= C) { da[i] = 0.f; return; }
-  const int w = (int)(p % W);
-  const int64_t t = p / W;
-  const int h = (int)(t % H);
-  const int b = (int)(t / H);
-  float s_ = 0.f;
-  for (int r = 0; r < 3; ++r) {
-    const int oh = h - r + 1;
-    if (oh < 0 || oh >= H) continue;
-    for (int s = 0; s < 3; ++s) {
-      const int ow = w - s + 1;
-      if (ow < 0 || ow >= W) continue;
-      const int64_t q = ((int64_t)b * H + oh) * W + ow;
-      for (int co = 0; co < 3; ++co) {
-        const float y = img[q * 3 + co];
-        const float dt = dimg[q * ldd + co] * (1.f - y * y);
-        s_ = fmaf(dt, sw[(co * 9 + r * 3 + s) * C + c], s_);
-      }
-    }
+  for (int i = threadIdx.x; i < 27 * Cp; i += 256) {
+    const int k = i / Cp, c = i - k * Cp;
+    wsd[i] = c < C ? Wt[k * C + c] * inv : 0.f;
   }
-  da[i] = s_;
+  const int tiles_w = (W + kDC - 1) / kDC, tiles_h = (H + kDR - 1) / kDR;
+  int bid = blockIdx.x;
+  const int tw = bid % tiles_w;
+  bid /= tiles_w;
+  const int th = bid % tiles_h;
+  const int b = bid / tiles_h;
+  const int h0 = th * kDR, w0 = tw * kDC;
+  for (int idx = threadIdx.x; idx < (kDR + 2) * (kDC + 2); idx += 256) {
+    const int r = idx / (kDC + 2), col = idx - r * (kDC + 2);
+    const int oh = h0 + r - 1, ow = w0 + col - 1;
+    float4 d = make_float4(0.f, 0.f, 0.f, 0.f);
+    if ((unsigned)oh < (unsigned)H && (unsigned)ow < (unsigned)W) {
+      const int64_t q = ((int64_t)b * H + oh) * W + ow;
+      const float y0 = img[q * 3], y1 = img[q * 3 + 1], y2 = img[q * 3 + 2];
+      d.x = dimg[q * ldd] * (1.f - y0 * y0);
+      d.y = dimg[q * ldd + 1] * (1.f - y1 * y1);
+      d.z = dimg[q * ldd + 2] * (1.f - y2 * y2);
+    }
+    dts[r][col] = d;
+  }
+  __syncthreads();
+  const int ncg = Cp >> 2;
+  const int items = ncg * kDR * (kDC / 4);
+  for (int it = threadIdx.x; it < items; it += 256) {
+    const int cg = it % ncg, pq = it / ncg;
+    const int rr = pq / (kDC / 4), cq = pq - rr * (kDC / 4);
+    const int oh = h0 + rr, ow0 = w0 + 4 * cq;
+    if (oh >= H || ow0 >= W) continue;
+    float acc[4][4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[p][e] = 0.f;
+    // output pixel (oh, ow0 + p) takes dt at (oh - r + 1, ow0 + p - s + 1) =
+    // staged position (rr + 2 - r, 4 cq + p + 2 - s)
+#pragma unroll
+    for (int r = 0; r < 3; ++r) {
+      float4 d[6];
+#pragma unroll
+      for (int j = 0; j < 6; ++j) d[j] = dts[rr + 2 - r][4 * cq + j];
+#pragma unroll
+      for (int s_ = 0; s_ < 3; ++s_)
+#pragma unroll
+        for (int co = 0; co < 3; ++co) {
+          const float4 wv = wsd4[(co * 9 + r * 3 + s_) * ncg + cg];
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            const float4 dd = d[p + 2 - s_];
+            const float dv = co == 0 ? dd.x : (co == 1 ? dd.y : dd.z);
+            acc[p][0] = fmaf(dv, wv.x, acc[p][0]);
+            acc[p][1] = fmaf(dv, wv.y, acc[p][1]);
+            acc[p][2] = fmaf(dv, wv.z, acc[p][2]);
+            acc[p][3] = fmaf(dv, wv.w, acc[p][3]);
+          }
+        }
+    }
+    const int64_t q0 = ((int64_t)b * H + oh) * W + ow0;
+#pragma unroll
+    for (int p = 0; p < 4; ++p)
+      *reinterpret_cast<float4*>(da + (q0 + p) * Cp + 4 * cg) = make_float4(acc[p][0], acc[p][1], acc[p][2], acc[p][3]);
+  }
 }
 
-// Weight gradient of the output layer.  Per chunk of kHeadRows pixels:
-//   part[chunk][co][tap][c] = sum_p dt[p][co] a[p + tap][c],
-//   part[chunk][27C + co]   = sum_p dt[p][co]          (bias),
-// with dt = dimg (1 - img^2) staged in LDS; a thread owns (tap, c) pairs
-// (consecutive c across lanes: coalesced loads of x).  Chunks are then
-// summed in a fixed order.
-constexpr int kHeadRows = 512;
+// Weight gradient of the output layer:
+//   dW[co][r][s][c] = sum_p dt[p][co] a[p + (r - 1, s - 1)][c],  db[co] = sum_p dt[p][co],
+// with a = relu(bn(x)) recomputed from x and dt = dimg (1 - img^2).  A
+// block takes kWR output rows of one image; a thread owns 4 channels and
+// walks whole rows (rows strip, strip + S, ... of the block), sliding a
+// 3x3 window of a (4 channels per position) in registers: one new column
+// of 3 loads per pixel feeds 108 FMAs.  The S strips then combine in a
+// fixed order through LDS, one output channel at a time, into the block's
+// partial; blocks are summed in order by k_ghead_fin.
+constexpr int kWR = 16;    // output rows per block
 
-__global__ __launch_bounds__(256) void k_ghead_wgrad(const float* dimg, int ldd, const float* img, const bf16_t* x,
-                                                     int B, int H, int W, int C, int Cp, const float* mean,
-                                                     const float* scale, const float* shift, float* part) {
-  __shared__ float sdt[kHeadRows][3];
-  const int64_t M = (int64_t)B * H * W;
-  const int64_t p0 = (int64_t)blockIdx.x * kHeadRows;
-  const int np = (int)(p0 + kHeadRows < M ? kHeadRows : M - p0);
-  const int nout = 27 * C + 3;
-  for (int i = threadIdx.x; i < np; i += 256) {
-    const int64_t p = p0 + i;
-    for (int co = 0; co < 3; ++co) {
-      const float y = img[p * 3 + co];
-      sdt[i][co] = dimg[p * ldd + co] * (1.f - y * y);
+__global__ __launch_bounds__(256) void k_ghead_wgrad(const float* __restrict__ dimg, int ldd,
+                                                     const float* __restrict__ img, const bf16_t* __restrict__ x,
+                                                     int B, int H, int W, int C, int Cp,
+                                                     const float* __restrict__ mean, const float* __restrict__ scale,
+                                                     const float* __restrict__ shift, float* __restrict__ part) {
+  extern __shared__ float red[];      // [S][9 * Cp] strip partials of one output channel
+  const int ncg = Cp >> 2;
+  const int S = 256 / ncg;            // strips (threads beyond S * ncg idle)
+  const int tiles_h = (H + kWR - 1) / kWR;
+  const int b = blockIdx.x / tiles_h, h0 = (blockIdx.x % tiles_h) * kWR;
+  const int h1 = min(H, h0 + kWR);
+  const int t = threadIdx.x;
+  const int cg = t % ncg, strip = t / ncg;
+  const bool active = strip < S;
+  const int c = 4 * cg;
+  float mu[4], sc[4], sh[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const bool ok = active && c + e < C;
+    mu[e] = ok ? mean[c + e] : 0.f;
+    sc[e] = ok ? scale[c + e] : 0.f;   // zero scale and shift: a = 0 for padded channels
+    sh[e] = ok ? shift[c + e] : 0.f;
+  }
+  float acc[3][9][4];
+#pragma unroll
+  for (int co = 0; co < 3; ++co)
+#pragma unroll
+    for (int k = 0; k < 9; ++k)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) acc[co][k][e] = 0.f;
+  float bsum[3] = {0.f, 0.f, 0.f};
+  // a at (row, col) for this thread's 4 channels (zero outside the image)
+  auto load_a = [&](int row, int col, float* v) {
+    if ((unsigned)row < (unsigned)H && (unsigned)col < (unsigned)W) {
+      const uint2 q = *reinterpret_cast<const uint2*>(x + (((int64_t)b * H + row) * W + col) * Cp + c);
+      const float f[4] = {__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xffff0000u),
+                          __uint_as_float(q.y << 16), __uint_as_float(q.y & 0xffff0000u)};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = fmaxf((f[e] - mu[e]) * sc[e] + sh[e], 0.f);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = 0.f;
     }
+  };
+  if (active) {
+    for (int h = h0 + strip; h < h1; h += S) {
+      // window columns w-1, w, w+1 of rows h-1, h, h+1
+      float win[3][3][4];
+#pragma unroll
+      for (int r = 0; r < 3; ++r) {
+        load_a(h + r - 1, -1, win[r][0]);
+        load_a(h + r - 1, 0, win[r][1]);
+      }
+      for (int w = 0; w < W; ++w) {
+#pragma unroll
+        for (int r = 0; r < 3; ++r) load_a(h + r - 1, w + 1, win[r][2]);
+        const int64_t q = ((int64_t)b * H + h) * W + w;
+        float dt[3];
+#pragma unroll
+        for (int co = 0; co < 3; ++co) {
+          const float y = img[q * 3 + co];
+          dt[co] = dimg[q * ldd + co] * (1.f - y * y);
+          bsum[co] += dt[co];
+        }
+#pragma unroll
+        for (int co = 0; co < 3; ++co)
+#pragma unroll
+          for (int r = 0; r < 3; ++r)
+#pragma unroll
+            for (int s_ = 0; s_ < 3; ++s_)
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                acc[co][r * 3 + s_][e] = fmaf(dt[co], win[r][s_][e], acc[co][r * 3 + s_][e]);
+#pragma unroll
+        for (int r = 0; r < 3; ++r)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            win[r][0][e] = win[r][1][e];
+            win[r][1][e] = win[r][2][e];
+          }
+      }
+    }
+  }
+  const int nout = 27 * C + 3;
+  float* out = part + (int64_t)blockIdx.x * nout;
+#pragma unroll
+  for (int co = 0; co < 3; ++co) {
+    __syncthreads();
+    if (active)
+#pragma unroll
+      for (int k = 0; k < 9; ++k)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) red[strip * 9 * Cp + k * Cp + c + e] = acc[co][k][e];
+    __syncthreads();
+    for (int i = t; i < 9 * C; i += 256) {
+      const int k = i / C, cc = i - k * C;
+      float v = 0.f;
+      for (int j = 0; j < S; ++j) v += red[j * 9 * Cp + k * Cp + cc];
+      out[(co * 9 + k) * C + cc] = v;
+    }
+  }
+  // bias: every strip's lane cg == 0 holds its rows' sums
+  __syncthreads();
+  if (active && cg == 0) {
+    red[strip * 3] = bsum[0];
+    red[strip * 3 + 1] = bsum[1];
+    red[strip * 3 + 2] = bsum[2];
   }
   __syncthreads();
-  float* out = part + (int64_t)blockIdx.x * nout;
-  if (threadIdx.x < 3) {
-    float sb = 0.f;
-    for (int i = 0; i < np; ++i) sb += sdt[i][threadIdx.x];
-    out[27 * C + threadIdx.x] = sb;
-  }
-  const int w00 = (int)(p0 % W);
-  const int64_t t0 = p0 / W;
-  const int h00 = (int)(t0 % H);
-  const int b00 = (int)(t0 / H);
-  for (int k = threadIdx.x; k < 9 * C; k += 256) {
-    const int c = k % C, tap = k / C;
-    const int r = tap / 3, s_ = tap % 3;
-    const float mu = mean[c], sc = scale[c], sh = shift[c];
-    float a0 = 0.f, a1 = 0.f, a2 = 0.f;
-    int b = b00, h = h00, w = w00;
-    for (int i = 0; i < np; ++i) {
-      const int ih = h + r - 1, iw = w + s_ - 1;
-      if (ih >= 0 && ih < H && iw >= 0 && iw < W) {
-        const float a = fmaxf((bf2f(x[(((int64_t)b * H + ih) * W + iw) * Cp + c]) - mu) * sc + sh, 0.f);
-        a0 = fmaf(sdt[i][0], a, a0);
-        a1 = fmaf(sdt[i][1], a, a1);
-        a2 = fmaf(sdt[i][2], a, a2);
-      }
-      if (++w == W) {
-        w = 0;
-        if (++h == H) { h = 0; ++b; }
-      }
-    }
-    out[(0 * 9 + tap) * C + c] = a0;
-    out[(1 * 9 + tap) * C + c] = a1;
-    out[(2 * 9 + tap) * C + c] = a2;
+  if (t < 3) {
+    float v = 0.f;
+    for (int j = 0; j < S; ++j) v += red[j * 3 + t];
+    out[27 * C + t] = v;
   }
 }
 
@@ -238,27 +350,34 @@ __global__ __launch_bounds__(1024) void k_ghead_fin(const float* part, int nch, 
   }
 }
 
-size_t ghead_ws_bytes(int64_t M, int C) { return align256((size_t)cdiv(M, kHeadRows) * (27 * C + 3) * 4); }
+static int64_t ghead_wgrad_blocks(int B, int H) { return (int64_t)B * cdiv(H, kWR); }
+
+size_t ghead_ws_bytes(int B, int H, int C) { return align256((size_t)ghead_wgrad_blocks(B, H) * (27 * C + 3) * 4); }
 
 void ghead_fwd(hipStream_t st, const void* x, int B, int H, int W, int C, int Cp, const float* mean,
                const float* scale, const float* shift, const float* Wt, const float* sigma, const float* bias,
                float* img) {
-  const int64_t blocks = (int64_t)B * H * cdiv(W, kHT);
-  PG_CHECK(blocks < (1LL << 31) && Cp % 8 == 0, "ghead_fwd: shape");
-  hipLaunchKernelGGL(k_ghead_fwd, dim3((unsigned)blocks), dim3(256), 0, st, (const bf16_t*)x, B, H, W, C, Cp, mean,
-                     scale, shift, Wt, sigma, bias, img);
+  const int64_t blocks = (int64_t)B * cdiv(H, kFR) * cdiv(W, kFC);
+  PG_CHECK(blocks < (1LL << 31) && Cp % 8 == 0 && C <= Cp && C <= 512, "ghead_fwd: shape");
+  hipLaunchKernelGGL(k_ghead_fwd, dim3((unsigned)blocks), dim3(256), 28 * C * sizeof(float), st, (const bf16_t*)x,
+                     B, H, W, C, Cp, mean, scale, shift, Wt, sigma, bias, img);
   PG_LAUNCH_CHECK();
 }
 
 void ghead_bwd(hipStream_t st, const float* dimg, int ldd, const float* img, const void* x, int B, int H, int W,
                int C, int Cp, const float* mean, const float* scale, const float* shift, const float* Wt,
                const float* sigma, float* da, float* dwsn, float* dbias, void* ws) {
-  const int64_t M = (int64_t)B * H * W;
-  hipLaunchKernelGGL(k_ghead_dgrad, dim3((unsigned)cdiv(M * Cp, 256)), dim3(256), 27 * C * sizeof(float), st,
-                     dimg, ldd, img, B, H, W, C, Cp, Wt, sigma, da);
-  const int nch = (int)cdiv(M, kHeadRows);
-  hipLaunchKernelGGL(k_ghead_wgrad, dim3(nch), dim3(256), 0, st, dimg, ldd, img, (const bf16_t*)x, B, H, W, C, Cp,
-                     mean, scale, shift, (float*)ws);
+  PG_CHECK(W % 4 == 0 && Cp % 4 == 0 && C <= Cp && Cp <= 1024, "ghead_bwd: shape");
+  const int64_t dblocks = (int64_t)B * cdiv(H, kDR) * cdiv(W, kDC);
+  PG_CHECK(dblocks < (1LL << 31), "ghead_bwd: shape");
+  hipLaunchKernelGGL(k_ghead_dgrad, dim3((unsigned)dblocks), dim3(256), 27 * Cp * sizeof(float), st, dimg, ldd,
+                     img, B, H, W, C, Cp, Wt, sigma, da);
+  const int nch = (int)ghead_wgrad_blocks(B, H);
+  const int S = 256 / (Cp / 4);
+  const size_t red_bytes = (size_t)S * 9 * Cp * sizeof(float);
+  PG_CHECK(S >= 1 && red_bytes <= 64 * 1024, "ghead_bwd: channels");
+  hipLaunchKernelGGL(k_ghead_wgrad, dim3(nch), dim3(256), red_bytes, st, dimg, ldd, img, (const bf16_t*)x, B, H, W,
+                     C, Cp, mean, scale, shift, (float*)ws);
   hipLaunchKernelGGL(k_ghead_fin, dim3((unsigned)cdiv(27 * C + 3, 64)), dim3(1024), 0, st, (const float*)ws, nch,
                      27 * C + 3, dwsn, dbias);
   PG_LAUNCH_CHECK();

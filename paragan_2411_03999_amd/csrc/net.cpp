@@ -190,7 +190,7 @@ static GNetWs gnet_carve(const Arch& a, int B, const std::vector<GBlock>& blocks
   r.dlin = w.f32(16LL * c0 * a.zc);
   r.dcond = w.f32((size_t)B * a.dc);
   r.part = w.f32(256);
-  r.head = w.bytes(std::max(ghead_ws_bytes(M, c), bn_bwd_ws_bytes(B, a.img * a.img, c)));
+  r.head = w.bytes(std::max(ghead_ws_bytes(B, a.img, c), bn_bwd_ws_bytes(B, a.img * a.img, c)));
   r.blk_bytes = blk;
   r.blk = w.bytes(blk);
   return r;

@@ -360,7 +360,7 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
     default: name = launch_tr<2, 2, 2, 2>(s, k, blocks, gup, in.gather, in.relu); break;
   }
   PG_LAUNCH_CHECK();
-  prof.done(name, flops);
+  prof.done(name, flops, k.M, Np, k.Kdim);
   if (p.splits > 1 || g.gscale != 1.f) {
     ProfScope pr(s);
     hipLaunchKernelGGL(k_wgtr_reduce, dim3((unsigned)cdiv(nout, 256)), dim3(256), 0, s, k.part, p.splits,

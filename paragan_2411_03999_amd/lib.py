@@ -297,10 +297,11 @@ def paragan_train_step(ctx, desc, G, D, inputs, n_D, ws, losses):
 
 
 def paragan_profile(ctx, enable):
-    return ctx.check(load().paragan_profile(ctx.h, int(bool(enable))))
+    """enable: 0 off, 1 on, 2 on with per-launch GEMM shapes in the names."""
+    return ctx.check(load().paragan_profile(ctx.h, int(enable)))
 
 
-def paragan_profile_read(ctx, cap=256):
+def paragan_profile_read(ctx, cap=1024):
     """Per-kernel launch statistics since the last read (list of dicts);
     the records are consumed."""
     arr = (KernelStat * cap)()
