@@ -55,17 +55,15 @@ static AWsB a_carve_b(const Attn& t, Arena& a, int n_cu) {
   w.Dv = a.f32((size_t)t.B * d.HWp);
   w.dwq = a.f32((size_t)t.Nqkv * t.Cp);
   w.dwo = a.f32((size_t)t.Cp * t.dv);
-  w.part = a.f32(256);
+  w.part = a.f32(256 * kSnGroupMax);
   w.wg_bytes = std::max(conv_wgrad_ws(false, M, 1, t.dv, t.Cp, n_cu), conv_wgrad_ws(false, M, 1, t.Cp, t.Nqkv, n_cu));
   w.wg = a.bytes(w.wg_bytes);
   return w;
 }
 
 size_t Attn::ws_size(int n_cu) const {
-  size_t sn_b = 0;
-  const int64_t rows[4] = {C / 8, C / 8, C / 2, C};
-  const int64_t cols[4] = {C, C, C, C / 2};
-  for (int i = 0; i < 4; ++i) sn_b = std::max(sn_b, sn_ws_bytes(rows[i], cols[i]));
+  const int64_t rc[4][2] = {{C / 8, C}, {C / 8, C}, {C / 2, C}, {C, C / 2}};
+  const size_t sn_b = sn_group_ws(rc, 4);
   Arena b(nullptr);
   a_carve_b(*this, b, n_cu);
   return std::max(align256(sn_b), b.off);
@@ -75,12 +73,14 @@ static const char* kASN[4] = {"theta", "phi", "g", "o"};
 
 void Attn::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   const AttnDims d = dims(*this);
-  for (int i = 0; i < 4; ++i) sn_forward(ex, P, kASN[i], sn[i], npi, sn_eps);
-  pack_weight(ex.st, false, P.w("theta"), sn[0].sigma, C / 8, C, 1, dk, Cp, false, wqkv);
-  pack_weight(ex.st, false, P.w("phi"), sn[1].sigma, C / 8, C, 1, dk, Cp, false, (char*)wqkv + (size_t)dk * Cp * 2);
-  pack_weight(ex.st, false, P.w("g"), sn[2].sigma, C / 2, C, 1, dv, Cp, false,
-              (char*)wqkv + (size_t)2 * dk * Cp * 2);
-  pack_weight(ex.st, false, P.w("o"), sn[3].sigma, C, C / 2, 1, Cp, dv, false, wo);
+  SnJob jobs[4];
+  for (int i = 0; i < 4; ++i) jobs[i] = sn_job(P, kASN[i], sn[i]);
+  sn_power_iter_group(ex.st, jobs, 4, npi, sn_eps, ex.ws);
+  const PackJob pk[4] = {{P.w("theta"), sn[0].sigma, wqkv, C / 8, C, 1, dk, Cp, false},
+                         {P.w("phi"), sn[1].sigma, (char*)wqkv + (size_t)dk * Cp * 2, C / 8, C, 1, dk, Cp, false},
+                         {P.w("g"), sn[2].sigma, (char*)wqkv + (size_t)2 * dk * Cp * 2, C / 2, C, 1, dv, Cp, false},
+                         {P.w("o"), sn[3].sigma, wo, C, C / 2, 1, Cp, dv, false}};
+  pack_group(ex.st, false, pk, 4);
   ConvIn in;
   in.x = x; in.B = B; in.Hx = H; in.Wx = W; in.C = Cp;
   ConvOut po;
@@ -135,13 +135,11 @@ void Attn::bwd(const Exec& ex, const Params& P, const void* x, const void* dy, v
   conv_fwd(ex.st, false, qi, H, W, 1, w.wdq, Cp, xo);
   (void)M;
   if (!wgrad) return;
-  sn_bwd(ex.st, w.dwq, P.w("theta"), sn[0].u, sn[0].v, sn[0].sigma, C / 8, C, 1, Cp, nullptr, P.gr("theta"),
-         w.part);
-  sn_bwd(ex.st, w.dwq + (size_t)dk * Cp, P.w("phi"), sn[1].u, sn[1].v, sn[1].sigma, C / 8, C, 1, Cp, nullptr,
-         P.gr("phi"), w.part);
-  sn_bwd(ex.st, w.dwq + (size_t)2 * dk * Cp, P.w("g"), sn[2].u, sn[2].v, sn[2].sigma, C / 2, C, 1, Cp, nullptr,
-         P.gr("g"), w.part);
-  sn_bwd(ex.st, w.dwo, P.w("o"), sn[3].u, sn[3].v, sn[3].sigma, C, C / 2, 1, dv, gamma, P.gr("o"), w.part);
+  const SnBwdJob jobs[4] = {sn_bwd_job(P, "theta", sn[0], w.dwq, 1, Cp, nullptr),
+                            sn_bwd_job(P, "phi", sn[1], w.dwq + (size_t)dk * Cp, 1, Cp, nullptr),
+                            sn_bwd_job(P, "g", sn[2], w.dwq + (size_t)2 * dk * Cp, 1, Cp, nullptr),
+                            sn_bwd_job(P, "o", sn[3], w.dwo, 1, dv, gamma)};
+  sn_bwd_group(ex.st, jobs, 4, w.part);
 }
 
 }  // namespace pg

@@ -55,9 +55,26 @@ Layout attn_layout(int c) {
 static int64_t cols_of(const Entry& e) { return e.numel() / e.shape[0]; }
 
 void sn_forward(const Exec& ex, const Params& P, const std::string& name, SNSlot& s, int npi, float eps) {
+  const SnJob j = sn_job(P, name, s);
+  sn_power_iter_group(ex.st, &j, 1, npi, eps, ex.ws);
+}
+
+SnJob sn_job(const Params& P, const std::string& name, SNSlot& s) {
   const Entry& e = P.ent(name);
-  sn_power_iter(ex.st, P.p + e.offset, e.shape[0], cols_of(e), P.u + e.u_offset, s.v, s.sigma, npi, eps,
-                ex.ws, s.u);
+  return SnJob{P.p + e.offset, e.shape[0], cols_of(e), P.u + e.u_offset, s.v, s.sigma, s.u};
+}
+
+size_t sn_group_ws(const int64_t (*rc)[2], int n) {
+  size_t t = 0;
+  for (int i = 0; i < n; ++i) t += sn_ws_bytes(rc[i][0], rc[i][1]);
+  return t;
+}
+
+SnBwdJob sn_bwd_job(const Params& P, const std::string& name, const SNSlot& s, const float* dwp, int R, int Cp,
+                    const float* scale) {
+  const Entry& e = P.ent(name);
+  return SnBwdJob{dwp, P.p + e.offset, s.u, s.v, s.sigma, scale, P.g + e.offset, (int)e.shape[0],
+                  (int)(cols_of(e) / (R * R)), R, Cp};
 }
 
 static void plan_sn(Arena& a, SNSlot& s, int64_t rows, int64_t cols) {
@@ -99,7 +116,7 @@ struct GWsF {
 };
 struct GWsB {
   void *wd1, *wd2, *wdsc;
-  float *dwp1, *dwp2, *dwpsc, *dlin;
+  float *dwp1, *dwp2, *dwpsc, *dlin[4];
   void* wg;
   size_t wg_bytes;
   void* cs;
@@ -110,11 +127,9 @@ struct GWsB {
 };
 
 static size_t g_sn_ws(const GBlock& g) {
-  size_t m = 0;
   const int64_t rc[7][2] = {{g.cin, g.dc}, {g.cin, g.dc}, {g.cout, 9LL * g.cin}, {g.cout, g.dc},
                             {g.cout, g.dc}, {g.cout, 9LL * g.cout}, {g.cout, g.cin}};
-  for (auto& r : rc) m = std::max(m, sn_ws_bytes(r[0], r[1]));
-  return m;
+  return sn_group_ws(rc, 7);
 }
 
 static GWsF g_carve_f(const GBlock& g, Arena& a) {
@@ -136,7 +151,7 @@ static GWsB g_carve_b(const GBlock& g, Arena& a, int n_cu) {
   w.dwp1 = a.f32((size_t)g.Cop * 9 * g.Cip);
   w.dwp2 = a.f32((size_t)g.Cop * 9 * g.Cop);
   w.dwpsc = a.f32((size_t)g.Cop * g.Cip);
-  w.dlin = a.f32((size_t)std::max(g.cin, g.cout) * g.dc);
+  for (int i = 0; i < 4; ++i) w.dlin[i] = a.f32((size_t)(i < 2 ? g.cin : g.cout) * g.dc);
   w.wg_bytes = std::max({conv_wgrad_ws(g.f32, M2, 3, g.Cip, g.Cop, n_cu),
                          conv_wgrad_ws(g.f32, M2, 3, g.Cop, g.Cop, n_cu),
                          conv_wgrad_ws(g.f32, M2, 1, g.Cip, g.Cop, n_cu)});
@@ -148,7 +163,7 @@ static GWsB g_carve_b(const GBlock& g, Arena& a, int n_cu) {
   w.dh1 = a.bytes((size_t)M2 * g.Cop * e);
   w.dg1 = a.f32((size_t)g.B * g.Cip); w.db1 = a.f32((size_t)g.B * g.Cip);
   w.dg2 = a.f32((size_t)g.B * g.Cop); w.db2 = a.f32((size_t)g.B * g.Cop);
-  w.part = a.f32(256);
+  w.part = a.f32(256 * kSnGroupMax);
   w.bnb = a.bytes(std::max(bn_bwd_ws_bytes(g.B, 4 * g.H * g.W, g.cout), bn_bwd_ws_bytes(g.B, g.H * g.W, g.cin)));
   return w;
 }
@@ -163,12 +178,13 @@ size_t GBlock::ws_size(int n_cu) const {
 void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y) {
   Arena a(ex.ws);
   GWsF w = g_carve_f(*this, a);
-  Exec exs = ex;
-  exs.ws = w.sn;
-  for (int i = 0; i < 7; ++i) sn_forward(exs, P, kGSN[i], sn[i], npi, sn_eps);
-  pack_weight(ex.st, f32, P.w("conv1.w"), sn[2].sigma, cout, cin, 3, Cop, Cip, false, wp1);
-  pack_weight(ex.st, f32, P.w("conv2.w"), sn[5].sigma, cout, cout, 3, Cop, Cop, false, wp2);
-  pack_weight(ex.st, f32, P.w("sc.w"), sn[6].sigma, cout, cin, 1, Cop, Cip, false, wpsc);
+  SnJob jobs[7];
+  for (int i = 0; i < 7; ++i) jobs[i] = sn_job(P, kGSN[i], sn[i]);
+  sn_power_iter_group(ex.st, jobs, 7, npi, sn_eps, w.sn);
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, wp1, cout, cin, 3, Cop, Cip, false},
+                         {P.w("conv2.w"), sn[5].sigma, wp2, cout, cout, 3, Cop, Cop, false},
+                         {P.w("sc.w"), sn[6].sigma, wpsc, cout, cin, 1, Cop, Cip, false}};
+  pack_group(ex.st, f32, pk, 3);
   const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
   // cBN1 statistics and tables
   bn_stats(ex.st, f32, x, M1, cin, Cip, bn_eps, mean1, rstd1, w.bn);
@@ -207,9 +223,10 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   GWsB w = g_carve_b(*this, a, ex.n_cu);
   const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
   const int H2 = 2 * H, W2 = 2 * W;
-  pack_weight(ex.st, f32, P.w("conv1.w"), sn[2].sigma, cout, cin, 3, Cop, Cip, true, w.wd1);
-  pack_weight(ex.st, f32, P.w("conv2.w"), sn[5].sigma, cout, cout, 3, Cop, Cop, true, w.wd2);
-  pack_weight(ex.st, f32, P.w("sc.w"), sn[6].sigma, cout, cin, 1, Cop, Cip, true, w.wdsc);
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, w.wd1, cout, cin, 3, Cop, Cip, true},
+                         {P.w("conv2.w"), sn[5].sigma, w.wd2, cout, cout, 3, Cop, Cop, true},
+                         {P.w("sc.w"), sn[6].sigma, w.wdsc, cout, cin, 1, Cop, Cip, true}};
+  pack_group(ex.st, f32, pk, 3);
   // conv2: dW2, db2
   GradIn gdy;
   gdy.g = dy; gdy.Hs = H2; gdy.Ws = W2; gdy.C = Cop;
@@ -257,19 +274,17 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   const Lin lins[4] = {{"bn1.gain", w.dg1, cin, 0}, {"bn1.bias", w.db1, cin, 1},
                        {"bn2.gain", w.dg2, cout, 3}, {"bn2.bias", w.db2, cout, 4}};
   const int Cps[4] = {Cip, Cip, Cop, Cop};
+  SnBwdJob jobs[7];
   for (int i = 0; i < 4; ++i) {
     const Lin& l = lins[i];
-    cbn_linear_bwd(ex.st, l.dgb, B, l.C, Cps[i], cond, dc, P.w(l.name), sn[l.slot].sigma, w.dlin, dcond,
+    cbn_linear_bwd(ex.st, l.dgb, B, l.C, Cps[i], cond, dc, P.w(l.name), sn[l.slot].sigma, w.dlin[i], dcond,
                    dcond_acc || i > 0);
-    sn_bwd(ex.st, w.dlin, P.w(l.name), sn[l.slot].u, sn[l.slot].v, sn[l.slot].sigma, l.C, dc, 1, dc, nullptr,
-           P.gr(l.name), w.part);
+    jobs[i] = sn_bwd_job(P, l.name, sn[l.slot], w.dlin[i], 1, dc, nullptr);
   }
-  sn_bwd(ex.st, w.dwp1, P.w("conv1.w"), sn[2].u, sn[2].v, sn[2].sigma, cout, cin, 3, Cip, nullptr,
-         P.gr("conv1.w"), w.part);
-  sn_bwd(ex.st, w.dwp2, P.w("conv2.w"), sn[5].u, sn[5].v, sn[5].sigma, cout, cout, 3, Cop, nullptr,
-         P.gr("conv2.w"), w.part);
-  sn_bwd(ex.st, w.dwpsc, P.w("sc.w"), sn[6].u, sn[6].v, sn[6].sigma, cout, cin, 1, Cip, nullptr,
-         P.gr("sc.w"), w.part);
+  jobs[4] = sn_bwd_job(P, "conv1.w", sn[2], w.dwp1, 3, Cip, nullptr);
+  jobs[5] = sn_bwd_job(P, "conv2.w", sn[5], w.dwp2, 3, Cop, nullptr);
+  jobs[6] = sn_bwd_job(P, "sc.w", sn[6], w.dwpsc, 1, Cip, nullptr);
+  sn_bwd_group(ex.st, jobs, 7, w.part);
 }
 
 // ======================================================================
@@ -309,9 +324,8 @@ struct DWsB {
 
 static DWsF d_carve_f(const DBlock& d, Arena& a) {
   DWsF w;
-  size_t s = std::max(sn_ws_bytes(d.cout, 9LL * d.cin), sn_ws_bytes(d.cout, 9LL * d.cout));
-  if (d.lsc) s = std::max(s, sn_ws_bytes(d.cout, d.cin));
-  w.sn = a.bytes(s);
+  const int64_t rc[3][2] = {{d.cout, 9LL * d.cin}, {d.cout, 9LL * d.cout}, {d.cout, d.cin}};
+  w.sn = a.bytes(sn_group_ws(rc, d.lsc ? 3 : 2));
   w.skip = d.lsc ? a.f32((size_t)d.B * d.Ho * d.Wo * d.Cop) : nullptr;
   return w;
 }
@@ -332,7 +346,7 @@ static DWsB d_carve_b(const DBlock& d, Arena& a, int n_cu) {
   w.cs = a.bytes(colsum_ws_bytes(M, d.Cop));
   w.dh = a.bytes((size_t)M * d.Cop * e);
   w.dxs = d.lsc ? a.f32((size_t)Mo * d.Cip) : nullptr;
-  w.part = a.f32(256);
+  w.part = a.f32(256 * kSnGroupMax);
   return w;
 }
 
@@ -346,14 +360,14 @@ size_t DBlock::ws_size(int n_cu) const {
 void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   Arena a(ex.ws);
   DWsF w = d_carve_f(*this, a);
-  Exec exs = ex;
-  exs.ws = w.sn;
-  sn_forward(exs, P, "conv1.w", sn[0], npi, sn_eps);
-  sn_forward(exs, P, "conv2.w", sn[1], npi, sn_eps);
-  if (lsc) sn_forward(exs, P, "sc.w", sn[2], npi, sn_eps);
-  pack_weight(ex.st, f32, P.w("conv1.w"), sn[0].sigma, cout, cin, 3, Cop, Cip, false, wp1);
-  pack_weight(ex.st, f32, P.w("conv2.w"), sn[1].sigma, cout, cout, 3, Cop, Cop, false, wp2);
-  if (lsc) pack_weight(ex.st, f32, P.w("sc.w"), sn[2].sigma, cout, cin, 1, Cop, Cip, false, wpsc);
+  const int nsn = lsc ? 3 : 2;
+  const SnJob jobs[3] = {sn_job(P, "conv1.w", sn[0]), sn_job(P, "conv2.w", sn[1]),
+                         lsc ? sn_job(P, "sc.w", sn[2]) : SnJob{}};
+  sn_power_iter_group(ex.st, jobs, nsn, npi, sn_eps, w.sn);
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, wp1, cout, cin, 3, Cop, Cip, false},
+                         {P.w("conv2.w"), sn[1].sigma, wp2, cout, cout, 3, Cop, Cop, false},
+                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, wpsc, cout, cin, 1, Cop, Cip, false}};
+  pack_group(ex.st, f32, pk, nsn);
   // h = conv3x3([relu](x)) + b1
   ConvIn i1;
   i1.x = x; i1.B = B; i1.Hx = H; i1.Wx = W; i1.C = Cip; i1.relu = preact; i1.c_real = cin;
@@ -388,9 +402,10 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   Arena a(ex.ws);
   DWsB w = d_carve_b(*this, a, ex.n_cu);
   const int64_t M = (int64_t)B * H * W, Mo = (int64_t)B * Ho * Wo;
-  pack_weight(ex.st, f32, P.w("conv1.w"), sn[0].sigma, cout, cin, 3, Cop, Cip, true, w.wd1);
-  pack_weight(ex.st, f32, P.w("conv2.w"), sn[1].sigma, cout, cout, 3, Cop, Cop, true, w.wd2);
-  if (lsc) pack_weight(ex.st, f32, P.w("sc.w"), sn[2].sigma, cout, cin, 1, Cop, Cip, true, w.wdsc);
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, w.wd1, cout, cin, 3, Cop, Cip, true},
+                         {P.w("conv2.w"), sn[1].sigma, w.wd2, cout, cout, 3, Cop, Cop, true},
+                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, w.wdsc, cout, cin, 1, Cop, Cip, true}};
+  pack_group(ex.st, f32, pk, lsc ? 3 : 2);
   // conv2 (its output gradient is dy, or dy/4 spread over 2x2 when pooled)
   GradIn g2;
   g2.g = dy; g2.Hs = Ho; g2.Ws = Wo; g2.C = Cop;
@@ -453,13 +468,10 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     conv_fwd(ex.st, f32, d1, H, W, 3, w.wd1, Cip, d1o);
   }
   if (!wgrad) return;
-  sn_bwd(ex.st, w.dwp1, P.w("conv1.w"), sn[0].u, sn[0].v, sn[0].sigma, cout, cin, 3, Cip, nullptr,
-         P.gr("conv1.w"), w.part);
-  sn_bwd(ex.st, w.dwp2, P.w("conv2.w"), sn[1].u, sn[1].v, sn[1].sigma, cout, cout, 3, Cop, nullptr,
-         P.gr("conv2.w"), w.part);
-  if (lsc)
-    sn_bwd(ex.st, w.dwpsc, P.w("sc.w"), sn[2].u, sn[2].v, sn[2].sigma, cout, cin, 1, Cip, nullptr,
-           P.gr("sc.w"), w.part);
+  const SnBwdJob jobs[3] = {sn_bwd_job(P, "conv1.w", sn[0], w.dwp1, 3, Cip, nullptr),
+                            sn_bwd_job(P, "conv2.w", sn[1], w.dwp2, 3, Cop, nullptr),
+                            lsc ? sn_bwd_job(P, "sc.w", sn[2], w.dwpsc, 1, Cip, nullptr) : SnBwdJob{}};
+  sn_bwd_group(ex.st, jobs, lsc ? 3 : 2, w.part);
 }
 
 }  // namespace pg

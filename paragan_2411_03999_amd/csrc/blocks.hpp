@@ -141,5 +141,14 @@ struct Attn {
 
 // SN of one weight into a slot (power iteration updates u in place).
 void sn_forward(const Exec& ex, const Params& P, const std::string& name, SNSlot& s, int npi, float eps);
+// Group job descriptors: the power iteration of a named weight into a slot
+// (persistent u in place, the slot keeps a copy), and its backward writing
+// the weight's gradient from dwp (dL/d(W/sigma), padded layout, channel
+// stride Cp) scaled by *scale (1 if null).
+SnJob sn_job(const Params& P, const std::string& name, SNSlot& s);
+SnBwdJob sn_bwd_job(const Params& P, const std::string& name, const SNSlot& s, const float* dwp, int R, int Cp,
+                    const float* scale);
+// workspace of a group of (rows, cols) weights
+size_t sn_group_ws(const int64_t (*rc)[2], int n);
 
 }  // namespace pg

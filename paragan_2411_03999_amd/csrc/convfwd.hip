@@ -9,10 +9,15 @@
 // 4-channel vectors and stores 8 bytes (bf16) or 16 bytes (fp32) per lane.
 //
 // K loop: tap-outer, channel-inner; a thread's source offsets are computed
-// once per tap and advance by 32 channels per step.  Double-buffered LDS
-// with one barrier per step; 64-byte LDS rows (32 bf16 of K) with the
-// 16-byte chunks XOR-swizzled by row so that both the staging stores and
-// the MFMA operand reads are free of bank conflicts.
+// once per tap and advance by 32 channels per step.  Operand tiles move
+// from HBM straight into LDS (buffer loads with an LDS destination: lane l
+// of a wave writes 16 bytes at M0 + 16 l, no registers or LDS stores
+// involved) through a ring of three stages, so the loads of step k + 2 are
+// in flight while step k computes; one barrier per step.  LDS rows are 64
+// bytes (32 bf16 of K) with the 16-byte chunks XOR-swizzled by row, which
+// keeps the MFMA operand reads free of bank conflicts; the swizzle is
+// realised by choosing which source chunk each lane loads.  A ReLU on the
+// activation operand is applied to the fragments as they leave LDS.
 #include "ops.hpp"
 
 namespace pg {
@@ -84,71 +89,135 @@ PG_DEV float dpp_xor2(float v) {
 // swizzled element offset of (row r, 16-byte chunk c) in a tile of 32-element rows
 PG_DEV int sw_off(int r, int c) { return r * 32 + 8 * (c ^ ((r >> 2) & 3)); }
 
+// Byte address in LDS of a pointer into a __shared__ array, made
+// wave-uniform (it becomes the M0 base of a direct load).
+PG_DEV uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)(p));
+}
+
+// 16 bytes per lane from a buffer straight into LDS at M0 + 16 * lane (an
+// out-of-range offset writes zeros).  Issued as inline assembly so that the
+// compiler's wait-count insertion does not treat the stores into the other
+// stages of the ring as hazards for every LDS read; their completion is
+// waited for explicitly (wait_barrier), which is correct because the main
+// loop issues no other vector-memory instructions.
+// The byte address is voff (per lane) + soff (uniform).
+PG_DEV void lds_load16(uint32_t lds_base, uint32_t voff, uint32_t soff, __amdgpu_buffer_rsrc_t r) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(lds_base), "v"(voff),
+               "s"(r), "s"(soff)
+               : "memory", "m0");
+}
+
+// Wait until at most N of this wave's vector-memory loads are outstanding
+// and all of its LDS reads have completed, then barrier: one statement, so
+// nothing the compiler schedules can slip between the wait and the barrier.
+template <int N>
+PG_DEV void wait_barrier();
+#define PG_WAIT_BARRIER(N)                                                          \
+  template <>                                                                       \
+  PG_DEV void wait_barrier<N>() {                                                   \
+    asm volatile("s_waitcnt vmcnt(" #N ") lgkmcnt(0)\n\ts_barrier" ::: "memory");   \
+  }
+PG_WAIT_BARRIER(0)
+PG_WAIT_BARRIER(1)
+PG_WAIT_BARRIER(2)
+PG_WAIT_BARRIER(3)
+PG_WAIT_BARRIER(4)
+PG_WAIT_BARRIER(5)
+PG_WAIT_BARRIER(6)
+PG_WAIT_BARRIER(7)
+PG_WAIT_BARRIER(8)
+PG_WAIT_BARRIER(9)
+PG_WAIT_BARRIER(10)
+PG_WAIT_BARRIER(11)
+PG_WAIT_BARRIER(12)
+#undef PG_WAIT_BARRIER
+
+// One K step of a wave: operand fragments of one LDS stage through the MFMAs.
+template <int TN, int TM, bool RELU>
+PG_DEV void conv_step(const bf16_t* xs, const bf16_t* ws, int xbase, int wbase, int rd0, int rd1,
+                      f32x16 (&acc)[TN][TM]) {
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+    const int rd = kk ? rd1 : rd0;
+    bf16x8 wv[TN], xv[TM];
+#pragma unroll
+    for (int i = 0; i < TN; ++i) wv[i] = *reinterpret_cast<const bf16x8*>(ws + wbase + i * 32 * 32 + rd);
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      if (RELU) {
+        const uint4 q = relu8_bits(*reinterpret_cast<const uint4*>(xs + xbase + j * 32 * 32 + rd));
+        xv[j] = __builtin_bit_cast(bf16x8, q);
+      } else {
+        xv[j] = *reinterpret_cast<const bf16x8*>(xs + xbase + j * 32 * 32 + rd);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int j = 0; j < TM; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[i], xv[j], acc[i][j], 0, 0, 0);
+  }
+}
+
 template <int WN, int WM, int TN, int TM, int GATHER, bool RELU>
 __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
-  constexpr int AP = BM / 64;                  // pixel rows per thread
-  constexpr int BP = (BN * 4 + 255) / 256;     // weight chunks per thread
-  __shared__ __attribute__((aligned(16))) bf16_t Xs[2][BM * 32];
-  __shared__ __attribute__((aligned(16))) bf16_t Ws[2][BN * 32];
+  constexpr int AP = BM / 64;                  // activation wave loads per wave per step (16 rows each)
+  constexpr int WR = (BN + 63) / 64 * 64;      // weight rows held in LDS (whole wave loads)
+  constexpr int BP = WR / 64;                  // weight wave loads per wave per step
+  constexpr int NS = 3;                        // stages of the LDS ring
+  __shared__ __attribute__((aligned(16))) bf16_t Xs[NS][BM * 32];
+  __shared__ __attribute__((aligned(16))) bf16_t Ws[NS][WR * 32];
 
   const int bid = remap_tile2(blockIdx.x, k.tiles_m * k.tiles_n);
   const int tmi = bid / k.tiles_n, tni = bid - tmi * k.tiles_n;
   const int m0 = tmi * BM, n0 = tni * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave / WM, wm = wave % WM;
-  const int q = tid & 3;
   const bool quad = k.o.pool;
   const int C = k.C, R = k.R, pad = k.pad;
 
+  // Load j of this wave covers tile rows 16 (4 j + wave) .. + 15; lane l
+  // fills row + l / 4, LDS chunk l % 4, which in the swizzled layout holds
+  // source chunk (l % 4) ^ ((row / 4) % 4) = (l % 4) ^ ((l / 16) % 4).
+  const int lrow = lane >> 2;
+  const uint32_t lchunk = (uint32_t)((lane & 3) ^ ((lane >> 4) & 3));
   int rb[AP], roh[AP], row_[AP];
   bool rv[AP];
 #pragma unroll
-  for (int p = 0; p < AP; ++p) {
-    const int m = m0 + (tid >> 2) + 64 * p;
-    rv[p] = m < k.M;
-    pix_of(k, rv[p] ? m : 0, quad, rb[p], roh[p], row_[p]);
+  for (int j = 0; j < AP; ++j) {
+    const int m = m0 + 16 * (4 * j + wave) + lrow;
+    rv[j] = m < k.M;
+    pix_of(k, rv[j] ? m : 0, quad, rb[j], roh[j], row_[j]);
   }
-  // byte offsets of this thread's 16-byte chunks (kOOB: reads zeros)
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(k.x, k.x_bytes);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(k.w, k.w_bytes);
   uint32_t roff[AP];
   auto set_tap = [&](int tap) {
     const int r = tap / R, s = tap - (tap / R) * R;
 #pragma unroll
-    for (int p = 0; p < AP; ++p) {
-      const int ih = roh[p] + r - pad, iw = row_[p] + s - pad;
-      const bool ok = rv[p] && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W;
+    for (int j = 0; j < AP; ++j) {
+      const int ih = roh[j] + r - pad, iw = row_[j] + s - pad;
+      const bool ok = rv[j] && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W;
       const int sh = GATHER == G_UP2 ? (ih >> 1) : ih;
       const int sw = GATHER == G_UP2 ? (iw >> 1) : iw;
-      roff[p] = ok ? (uint32_t)(((rb[p] * k.Hx + sh) * k.Wx + sw) * C + q * 8) * 2u : kOOB;
+      roff[j] = ok ? (uint32_t)(((rb[j] * k.Hx + sh) * k.Wx + sw) * C) * 2u + 16u * lchunk : kOOB;
     }
   };
   uint32_t woff[BP];
 #pragma unroll
-  for (int p = 0; p < BP; ++p) {
-    const int idx = tid + 256 * p;
-    const int n = n0 + (idx >> 2);
-    woff[p] = idx < BN * 4 && n < k.Np ? (uint32_t)(n * R * R * C + (idx & 3) * 8) * 2u : kOOB;
-  }
-  // LDS staging offsets (fixed across steps)
-  int xst[AP], wst[BP];
-#pragma unroll
-  for (int p = 0; p < AP; ++p) xst[p] = sw_off((tid >> 2) + 64 * p, q);
-#pragma unroll
-  for (int p = 0; p < BP; ++p) {
-    const int idx = tid + 256 * p;
-    wst[p] = idx < BN * 4 ? sw_off(idx >> 2, idx & 3) : 0;
+  for (int j = 0; j < BP; ++j) {
+    const int row = 16 * (4 * j + wave) + lrow;
+    const int n = n0 + row;
+    woff[j] = row < BN && n < k.Np ? (uint32_t)(n * R * R * C) * 2u + 16u * lchunk : kOOB;
   }
 
-  uint4 ra[AP], rw[BP];
+  // producer position (tap, channel offset, step)
   int ld_tap = 0, ld_c0 = 0, ld_ks = 0;
   set_tap(0);
-  auto load = [&]() {
-#pragma unroll
-    for (int p = 0; p < AP; ++p) ra[p] = buf_ld16(xr, roff[p] + 2u * ld_c0);
-#pragma unroll
-    for (int p = 0; p < BP; ++p) rw[p] = buf_ld16(wr, woff[p] + 64u * ld_ks);
+  auto advance = [&]() {
     ++ld_ks;
     ld_c0 += 32;
     if (ld_c0 == C) {
@@ -157,19 +226,24 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
       if (ld_tap < R * R) set_tap(ld_tap);
     }
   };
-  auto store = [&](int buf) {
+  // LDS bases of this wave's loads in stage 0 (stage s adds s * stage size)
+  const uint32_t xl0 = lds_addr(&Xs[0][16 * wave * 32]), wl0 = lds_addr(&Ws[0][16 * wave * 32]);
+  auto issue = [&](int stage) {
+    const uint32_t coff = __builtin_amdgcn_readfirstlane(2u * (uint32_t)ld_c0);
+    const uint32_t wk = __builtin_amdgcn_readfirstlane(64u * (uint32_t)ld_ks);
+    const uint32_t xl = xl0 + (uint32_t)stage * (BM * 64), wl = wl0 + (uint32_t)stage * (WR * 64);
 #pragma unroll
-    for (int p = 0; p < AP; ++p)
-      *reinterpret_cast<uint4*>(&Xs[buf][xst[p]]) = RELU ? relu8_bits(ra[p]) : ra[p];
+    for (int j = 0; j < AP; ++j) lds_load16(xl + j * 4096u, roff[j], coff, xr);
 #pragma unroll
-    for (int p = 0; p < BP; ++p)
-      if (tid + 256 * p < BN * 4) *reinterpret_cast<uint4*>(&Ws[buf][wst[p]]) = rw[p];
+    for (int j = 0; j < BP; ++j) lds_load16(wl + j * 4096u, woff[j], wk, wr);
+    advance();
   };
 
   // operand read offsets: row (tile base + lane%32), chunk 2*kk + lane/32
   const int lr = lane & 31, f = (lr >> 2) & 3, h = lane >> 5;
   const int rd0 = lr * 32 + 8 * ((0 + h) ^ f);
   const int rd1 = lr * 32 + 8 * ((2 + h) ^ f);
+  const int xbase = wm * TM * 32 * 32, wbase = wn * TN * 32 * 32;
 
   f32x16 acc[TN][TM];
 #pragma unroll
@@ -179,33 +253,38 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  load();
-  store(0);
-  __syncthreads();
-  int buf = 0;
-  for (int ks = 0; ks < k.ksteps; ++ks) {
-    const bool more = ks + 1 < k.ksteps;
-    if (more) load();
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int rd = kk ? rd1 : rd0;
-      bf16x8 wv[TN], xv[TM];
-#pragma unroll
-      for (int i = 0; i < TN; ++i)
-        wv[i] = *reinterpret_cast<const bf16x8*>(&Ws[buf][(wn * TN + i) * 32 * 32 + rd]);
-#pragma unroll
-      for (int j = 0; j < TM; ++j)
-        xv[j] = *reinterpret_cast<const bf16x8*>(&Xs[buf][(wm * TM + j) * 32 * 32 + rd]);
-#pragma unroll
-      for (int i = 0; i < TN; ++i)
-#pragma unroll
-        for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[i], xv[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) store(buf ^ 1);
-    __syncthreads();
-    buf ^= 1;
+  const int ksteps = k.ksteps;
+  issue(0);
+  if (ksteps > 1) issue(1);
+  // Step ks computes stage ks % 3 and refills stage (ks + 2) % 3, last read
+  // in step ks - 1.  Before the barrier this wave's loads of step ks have
+  // landed (those of ks + 1 may still fly) and its reads of step ks - 1 are
+  // done; past it, every wave's loads of step ks are visible and no wave
+  // still reads the stage being refilled.
+  // main loop: three steps per trip with compile-time stages (constant LDS
+  // addresses), every step refilling a stage; then at most four tail steps.
+  int ks = 0;
+  for (; ks + 4 < ksteps; ks += 3) {
+    wait_barrier<AP + BP>();
+    issue(2);
+    conv_step<TN, TM, RELU>(Xs[0], Ws[0], xbase, wbase, rd0, rd1, acc);
+    wait_barrier<AP + BP>();
+    issue(0);
+    conv_step<TN, TM, RELU>(Xs[1], Ws[1], xbase, wbase, rd0, rd1, acc);
+    wait_barrier<AP + BP>();
+    issue(1);
+    conv_step<TN, TM, RELU>(Xs[2], Ws[2], xbase, wbase, rd0, rd1, acc);
   }
+  auto tail = [&](int s, int cur, int nxt) {
+    if (s + 1 < ksteps) wait_barrier<AP + BP>();
+    else wait_barrier<0>();
+    if (s + 2 < ksteps) issue(nxt);
+    conv_step<TN, TM, RELU>(Xs[cur], Ws[cur], xbase, wbase, rd0, rd1, acc);
+  };
+  if (ks < ksteps) tail(ks, 0, 2);
+  if (ks + 1 < ksteps) tail(ks + 1, 1, 0);
+  if (ks + 2 < ksteps) tail(ks + 2, 2, 1);
+  if (ks + 3 < ksteps) tail(ks + 3, 0, 2);
 
   // ---- epilogue: lane holds channels 8g + 4h + (0..3) of pixel m.
   // Per pixel tile: 32-bit element offsets of the output, mask and residual

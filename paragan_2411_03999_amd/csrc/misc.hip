@@ -33,129 +33,287 @@ PG_DEV double block_sum_d(double v, double* sh) {
 }
 
 // ------------------------------------------------ spectral normalisation
-// part[rc][c] = sum_{r in chunk rc} W[r][c] u[r]
-__global__ void k_sn_wtu(const float* W, const float* u, int64_t rows, int64_t cols, int rchunk,
-                         float* part) {
-  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t r0 = (int64_t)blockIdx.y * rchunk;
-  if (c >= cols) return;
-  int64_t r1 = r0 + rchunk;
-  if (r1 > rows) r1 = rows;
-  float s = 0.f;
-  for (int64_t r = r0; r < r1; ++r) s = fmaf(W[r * cols + c], u[r], s);
-  part[(int64_t)blockIdx.y * cols + c] = s;
+// The power iteration of every SN weight of a module runs as one group:
+// one launch per phase for all of its weights (a module has up to
+// kSnGroupMax), each launch finding its weight from a block-offset table
+// passed by value with the job descriptors.
+//   phase 1  part[j][c] = sum_{r in row chunk j} W[r][c] u[r]
+//   phase 2  t[c] = sum_j part[j][c] (in order), and per-block partials of |t|^2
+//   phase 3  s'[r] = W[r] . t                                              (a wave per row)
+//   phase 4  (a block per weight) v = t / max(|t|, eps), s = s' / max(|t|, eps),
+//            u = s / max(|s|, eps), sigma = u . s
+// (W v = (W t) / max(|t|, eps) exactly; only the rounding order differs from
+// normalising t first.)  Row chunks are sized so that phase 2 sums at most
+// 16 partials per column.
+struct SnJobK {
+  const float* W;
+  float *u, *v, *sigma, *u_save, *part, *s;
+  double* tsq;          // per-block partials of |t|^2 (ceil(cols / 256))
+  int rows, cols, rchunk, nrc;
+};
+struct SnGroupK {
+  SnJobK j[kSnGroupMax];
+  int n;
+  int off[kSnGroupMax + 1];   // first block of each job in this launch
+};
+
+PG_DEV int find_job(const int* off, int n, int bid) {
+  int i = 0;
+  while (i + 1 < n && bid >= off[i + 1]) ++i;
+  return i;
 }
 
-// v = t / max(|t|, eps), t[c] = sum over row chunks (in order)
-__global__ void k_sn_finish_v(const float* part, int nrc, int64_t cols, float eps, float* v) {
-  __shared__ double sh[16];
-  double ss = 0.0;
-  for (int64_t c = threadIdx.x; c < cols; c += 1024) {
-    float t = 0.f;
-    for (int j = 0; j < nrc; ++j) t += part[(int64_t)j * cols + c];
-    v[c] = t;
-    ss += (double)t * t;
+__global__ __launch_bounds__(256) void k_sng_wtu(SnGroupK g) {
+  const int i = find_job(g.off, g.n, blockIdx.x);
+  const SnJobK& J = g.j[i];
+  const int lb = blockIdx.x - g.off[i];
+  const int cb = (J.cols + 255) >> 8;
+  const int rc = lb / cb;
+  const int c = (lb - rc * cb) * 256 + threadIdx.x;
+  if (c >= J.cols) return;
+  const int r0 = rc * J.rchunk, r1 = min(r0 + J.rchunk, J.rows);
+  const float* W = J.W + (int64_t)r0 * J.cols + c;
+  const int64_t ld = J.cols;
+  // four independent chains: four rows in flight per thread
+  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+  int r = r0;
+  for (; r + 4 <= r1; r += 4, W += 4 * ld) {
+    s0 = fmaf(W[0], J.u[r], s0);
+    s1 = fmaf(W[ld], J.u[r + 1], s1);
+    s2 = fmaf(W[2 * ld], J.u[r + 2], s2);
+    s3 = fmaf(W[3 * ld], J.u[r + 3], s3);
   }
-  const double tot = block_sum_d<1024>(ss, sh);
-  const float inv = 1.f / fmaxf((float)sqrt(tot), eps);
-  for (int64_t c = threadIdx.x; c < cols; c += 1024) v[c] = v[c] * inv;
+  for (; r < r1; ++r, W += ld) s0 = fmaf(W[0], J.u[r], s0);
+  J.part[(int64_t)rc * J.cols + c] = (s0 + s1) + (s2 + s3);
 }
 
-// s[r] = W[r] . v   (one wave per row)
-__global__ void k_sn_wv(const float* W, const float* v, int64_t rows, int64_t cols, float* s) {
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+__global__ __launch_bounds__(256) void k_sng_t(SnGroupK g) {
+  __shared__ double sh[4];
+  const int i = find_job(g.off, g.n, blockIdx.x);
+  const SnJobK& J = g.j[i];
+  const int lb = blockIdx.x - g.off[i];
+  const int c = lb * 256 + threadIdx.x;
+  float t = 0.f;
+  if (c < J.cols) {
+    for (int j = 0; j < J.nrc; ++j) t += J.part[(int64_t)j * J.cols + c];
+    J.v[c] = t;
+  }
+  const double ss = block_sum_d<256>((double)t * t, sh);
+  if (threadIdx.x == 0) J.tsq[lb] = ss;
+}
+
+__global__ __launch_bounds__(256) void k_sng_wv(SnGroupK g) {
+  const int i = find_job(g.off, g.n, blockIdx.x);
+  const SnJobK& J = g.j[i];
+  const int r = (blockIdx.x - g.off[i]) * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
-  if (r >= rows) return;
-  float acc = 0.f;
-  for (int64_t c = lane; c < cols; c += 64) acc = fmaf(W[r * cols + c], v[c], acc);
-  acc = wave_sum(acc);
-  if (lane == 0) s[r] = acc;
+  if (r >= J.rows) return;
+  const float* W = J.W + (int64_t)r * J.cols;
+  float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+  int c = lane;
+  for (; c + 192 < J.cols; c += 256) {
+    a0 = fmaf(W[c], J.v[c], a0);
+    a1 = fmaf(W[c + 64], J.v[c + 64], a1);
+    a2 = fmaf(W[c + 128], J.v[c + 128], a2);
+    a3 = fmaf(W[c + 192], J.v[c + 192], a3);
+  }
+  for (; c < J.cols; c += 64) a0 = fmaf(W[c], J.v[c], a0);
+  const float acc = wave_sum((a0 + a1) + (a2 + a3));
+  if (lane == 0) J.s[r] = acc;
 }
 
-// u = s / max(|s|, eps); sigma = u . s
-__global__ void k_sn_finish_u(const float* s, int64_t rows, float eps, float* u, float* u_save,
-                              float* sigma) {
+__global__ __launch_bounds__(1024) void k_sng_u(SnGroupK g, float eps) {
   __shared__ double sh[16];
+  __shared__ float inv_t_sh;
+  const SnJobK& J = g.j[blockIdx.x];
+  if (threadIdx.x == 0) {
+    double tt = 0.0;
+    const int nb = (J.cols + 255) >> 8;
+    for (int b = 0; b < nb; ++b) tt += J.tsq[b];
+    inv_t_sh = 1.f / fmaxf((float)sqrt(tt), eps);
+  }
+  __syncthreads();
+  const float inv_t = inv_t_sh;
+  for (int c = threadIdx.x; c < J.cols; c += 1024) J.v[c] = J.v[c] * inv_t;
   double ss = 0.0;
-  for (int64_t r = threadIdx.x; r < rows; r += 1024) ss += (double)s[r] * s[r];
+  for (int r = threadIdx.x; r < J.rows; r += 1024) {
+    const float sr = J.s[r] * inv_t;
+    ss += (double)sr * sr;
+  }
   const double tot = block_sum_d<1024>(ss, sh);
   const float inv = 1.f / fmaxf((float)sqrt(tot), eps);
   double sg = 0.0;
-  for (int64_t r = threadIdx.x; r < rows; r += 1024) {
-    const float un = s[r] * inv;
-    u[r] = un;
-    if (u_save) u_save[r] = un;
-    sg += (double)un * s[r];
+  for (int r = threadIdx.x; r < J.rows; r += 1024) {
+    const float sr = J.s[r] * inv_t;
+    const float un = sr * inv;
+    J.u[r] = un;
+    if (J.u_save) J.u_save[r] = un;
+    sg += (double)un * sr;
   }
   const double sgt = block_sum_d<1024>(sg, sh);
-  if (threadIdx.x == 0) *sigma = (float)sgt;
+  if (threadIdx.x == 0) *J.sigma = (float)sgt;
 }
 
-static int sn_rchunk(int64_t rows) { return rows > 4096 ? 256 : (rows > 256 ? 64 : 16); }
+static void sn_chunks(int64_t rows, int& rchunk, int& nrc) {
+  nrc = (int)std::min<int64_t>(16, cdiv(rows, 16));
+  rchunk = (int)cdiv(rows, nrc);
+  nrc = (int)cdiv(rows, rchunk);
+}
 
-size_t sn_ws_bytes(int64_t rows, int64_t cols) {
-  const int64_t nrc = cdiv(rows, sn_rchunk(rows));
-  return align256((size_t)nrc * cols * 4) + align256((size_t)rows * 4);
+static size_t sn_job_ws(int64_t rows, int64_t cols) {
+  int rc, nrc;
+  sn_chunks(rows, rc, nrc);
+  return align256((size_t)nrc * cols * 4) + align256((size_t)rows * 4) + align256((size_t)cdiv(cols, 256) * 8);
+}
+
+size_t sn_ws_bytes(int64_t rows, int64_t cols) { return sn_job_ws(rows, cols); }
+
+size_t sn_group_ws_bytes(const SnJob* jobs, int n) {
+  size_t t = 0;
+  for (int i = 0; i < n; ++i) t += sn_job_ws(jobs[i].rows, jobs[i].cols);
+  return t;
+}
+
+void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws) {
+  PG_CHECK(n >= 1 && n <= kSnGroupMax, "sn group: 1..8 weights");
+  SnGroupK g{};
+  g.n = n;
+  char* w = (char*)ws;
+  for (int i = 0; i < n; ++i) {
+    const SnJob& a = jobs[i];
+    PG_CHECK(a.rows >= 1 && a.cols >= 1 && a.rows < (1LL << 31) && a.cols < (1LL << 31), "sn group: shape");
+    SnJobK& k = g.j[i];
+    k.W = a.W; k.u = a.u; k.v = a.v; k.sigma = a.sigma; k.u_save = nullptr;
+    k.rows = (int)a.rows; k.cols = (int)a.cols;
+    sn_chunks(a.rows, k.rchunk, k.nrc);
+    k.part = (float*)w;
+    k.s = (float*)(w + align256((size_t)k.nrc * a.cols * 4));
+    k.tsq = (double*)(w + align256((size_t)k.nrc * a.cols * 4) + align256((size_t)a.rows * 4));
+    w += sn_job_ws(a.rows, a.cols);
+  }
+  int b1 = 0, b2 = 0, b3 = 0;
+  int o1[kSnGroupMax + 1], o2[kSnGroupMax + 1], o3[kSnGroupMax + 1];
+  for (int i = 0; i < n; ++i) {
+    o1[i] = b1;
+    o2[i] = b2;
+    o3[i] = b3;
+    b1 += (int)cdiv(g.j[i].cols, 256) * g.j[i].nrc;
+    b2 += (int)cdiv(g.j[i].cols, 256);
+    b3 += (int)cdiv(g.j[i].rows, 4);
+  }
+  o1[n] = b1;
+  o2[n] = b2;
+  o3[n] = b3;
+  for (int it = 0; it < n_iter; ++it) {
+    if (it + 1 == n_iter)
+      for (int i = 0; i < n; ++i) g.j[i].u_save = jobs[i].u_save;
+    std::copy(o1, o1 + n + 1, g.off);
+    hipLaunchKernelGGL(k_sng_wtu, dim3(b1), dim3(256), 0, st, g);
+    std::copy(o2, o2 + n + 1, g.off);
+    hipLaunchKernelGGL(k_sng_t, dim3(b2), dim3(256), 0, st, g);
+    std::copy(o3, o3 + n + 1, g.off);
+    hipLaunchKernelGGL(k_sng_wv, dim3(b3), dim3(256), 0, st, g);
+    hipLaunchKernelGGL(k_sng_u, dim3(n), dim3(1024), 0, st, g, eps);
+  }
+  PG_LAUNCH_CHECK();
 }
 
 void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, float* u, float* v,
                    float* sigma, int n_iter, float eps, void* ws, float* u_save) {
-  const int rc = sn_rchunk(rows);
-  const int nrc = (int)cdiv(rows, rc);
-  float* part = (float*)ws;
-  float* s = (float*)((char*)ws + align256((size_t)nrc * cols * 4));
-  for (int it = 0; it < n_iter; ++it) {
-    hipLaunchKernelGGL(k_sn_wtu, dim3((unsigned)cdiv(cols, 256), nrc), dim3(256), 0, st, W, u, rows,
-                       cols, rc, part);
-    hipLaunchKernelGGL(k_sn_finish_v, dim3(1), dim3(1024), 0, st, part, nrc, cols, eps, v);
-    hipLaunchKernelGGL(k_sn_wv, dim3((unsigned)cdiv(rows, 4)), dim3(256), 0, st, W, v, rows, cols, s);
-    hipLaunchKernelGGL(k_sn_finish_u, dim3(1), dim3(1024), 0, st, s, rows, eps, u,
-                       it + 1 == n_iter ? u_save : nullptr, sigma);
-  }
-  PG_LAUNCH_CHECK();
+  const SnJob j{W, rows, cols, u, v, sigma, u_save};
+  sn_power_iter_group(st, &j, 1, n_iter, eps, ws);
 }
 
-// Pack W/sigma into the conv operand layouts.
-//  forward: dst[n][r][s][c]  ([Np][R][R][Cp]),  n < Cout, c < Cin
+// Pack W/sigma into the conv operand layouts, every weight of a group in
+// one launch.
+//  forward: dst[n][r][s][c]  ([Np][R][R][Cp]),  n < Cout, c < Cin (else 0)
 //  dgrad:   dst[c][r][s][n]  ([Cp][R][R][Np]) = W[n][R-1-r][R-1-s][c]
+// The forward layout is a padded copy (a thread per element, both sides
+// contiguous along c); the dgrad layout transposes (n, c) per tap through
+// a 32 x 32 LDS tile so that reads run along c and writes along n.
+struct PackJobK {
+  const float* W;
+  const float* sigma;
+  void* dst;
+  int Cout, Cin, R, Np, Cp, dgrad;
+};
+struct PackGroupK {
+  PackJobK j[kSnGroupMax];
+  int n;
+  int off[kSnGroupMax + 1];
+};
+
 template <typename T>
-__global__ void k_pack(const float* W, const float* sigma, int Cout, int Cin, int R, int Np, int Cp,
-                       int dgrad, T* dst) {
-  const int64_t total = (int64_t)(dgrad ? Cp : Np) * R * R * (dgrad ? Np : Cp);
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= total) return;
-  const float inv_s = 1.f / *sigma;
-  float v = 0.f;
-  if (!dgrad) {
-    const int c = (int)(i % Cp);
-    const int64_t t = i / Cp;
-    const int tap = (int)(t % (R * R));
-    const int n = (int)(t / (R * R));
-    if (n < Cout && c < Cin) v = W[((int64_t)n * R * R + tap) * Cin + c] / *sigma;
-  } else {
-    const int n = (int)(i % Np);
-    const int64_t t = i / Np;
-    const int tap = (int)(t % (R * R));
-    const int c = (int)(t / (R * R));
-    const int r = tap / R, s = tap % R;
-    const int ftap = (R - 1 - r) * R + (R - 1 - s);
-    if (n < Cout && c < Cin) v = W[((int64_t)n * R * R + ftap) * Cin + c] / *sigma;
+__global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
+  __shared__ float tile[32][33];
+  const int i = find_job(g.off, g.n, blockIdx.x);
+  const PackJobK& J = g.j[i];
+  const int lb = blockIdx.x - g.off[i];
+  const int RR = J.R * J.R;
+  const float inv = 1.f / *J.sigma;
+  T* dst = (T*)J.dst;
+  if (!J.dgrad) {
+    // 32-bit indices (the host checks the sizes): four consecutive channels per thread
+    const int e = (lb * 256 + (int)threadIdx.x) * 4;
+    if (e >= J.Np * RR * J.Cp) return;
+    const int t = e / J.Cp;     // n * RR + tap
+    const int c = e - t * J.Cp;
+    const int n = t / RR;
+    const float* src = J.W + (int64_t)t * J.Cin;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float v = (n < J.Cout && c + q < J.Cin) ? src[c + q] * inv : 0.f;
+      st<T>(dst, (int64_t)e + q, v);
+    }
+    return;
   }
-  (void)inv_s;
-  st<T>(dst, i, v);
+  const int tn = (J.Np + 31) >> 5, tc = (J.Cp + 31) >> 5;
+  const int tap = lb / (tn * tc);
+  const int rem = lb - tap * tn * tc;
+  const int n0 = (rem / tc) * 32, c0 = (rem % tc) * 32;
+  const int r = tap / J.R, s_ = tap - r * J.R;
+  const int ftap = (J.R - 1 - r) * J.R + (J.R - 1 - s_);
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int n = n0 + ty + 8 * k, c = c0 + tx;
+    tile[ty + 8 * k][tx] = (n < J.Cout && c < J.Cin) ? J.W[((int64_t)n * RR + ftap) * J.Cin + c] * inv : 0.f;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int c = c0 + ty + 8 * k, n = n0 + tx;
+    if (c < J.Cp && n < J.Np) st<T>(dst, ((int64_t)c * RR + tap) * J.Np + n, tile[tx][ty + 8 * k]);
+  }
+}
+
+void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
+  PG_CHECK(n >= 1 && n <= kSnGroupMax, "pack group: 1..8 weights");
+  PackGroupK g{};
+  g.n = n;
+  int64_t b = 0;
+  for (int i = 0; i < n; ++i) {
+    const PackJob& a = jobs[i];
+    g.j[i] = PackJobK{a.W, a.sigma, a.dst, a.Cout, a.Cin, a.R, a.Np, a.Cp, a.dgrad ? 1 : 0};
+    g.off[i] = (int)b;
+    const int RR = a.R * a.R;
+    PG_CHECK(a.Cp % 4 == 0 && (int64_t)a.Np * RR * a.Cp < (1LL << 31) &&
+             (int64_t)a.Cout * RR * a.Cin < (1LL << 31), "pack group: shape");
+    b += a.dgrad ? (int64_t)RR * cdiv(a.Np, 32) * cdiv(a.Cp, 32) : cdiv((int64_t)a.Np * RR * a.Cp, 1024);
+    PG_CHECK(b < (1LL << 31), "pack group: too large");
+  }
+  g.off[n] = (int)b;
+  if (f32)
+    hipLaunchKernelGGL(k_pack_group<float>, dim3((unsigned)b), dim3(256), 0, st, g);
+  else
+    hipLaunchKernelGGL(k_pack_group<bf16_t>, dim3((unsigned)b), dim3(256), 0, st, g);
+  PG_LAUNCH_CHECK();
 }
 
 void pack_weight(hipStream_t st, bool f32, const float* W, const float* sigma, int Cout, int Cin,
                  int R, int Np, int Cp, bool dgrad, void* dst) {
-  const int64_t total = (int64_t)Np * R * R * Cp;
-  dim3 g((unsigned)cdiv(total, 256));
-  if (f32)
-    hipLaunchKernelGGL(k_pack<float>, g, dim3(256), 0, st, W, sigma, Cout, Cin, R, Np, Cp, (int)dgrad,
-                       (float*)dst);
-  else
-    hipLaunchKernelGGL(k_pack<bf16_t>, g, dim3(256), 0, st, W, sigma, Cout, Cin, R, Np, Cp, (int)dgrad,
-                       (bf16_t*)dst);
-  PG_LAUNCH_CHECK();
+  const PackJob j{W, sigma, dst, Cout, Cin, R, Np, Cp, dgrad};
+  pack_group(st, f32, &j, 1);
 }
 
 // Transposed 1x1 pack into columns [col_off, col_off + Np) of a [Cp][ld]
@@ -182,56 +340,96 @@ void pack_weight_t(hipStream_t st, bool f32, const float* W, const float* sigma,
   PG_LAUNCH_CHECK();
 }
 
-// SN backward.  dwp: dL/d(W/sigma) in the padded forward layout
-// [Np][R][R][Cp]; W: master [Cout][R][R][Cin].
-//   dW = (dWsn - <dWsn, W/sigma> u v^T) / sigma,  v indexed by (r, s, c).
-__global__ void k_sn_dot_part(const float* dwp, const float* W, int Cout, int Cin, int RR, int Cp,
-                              float* part) {
+// SN backward, every weight of a group in two launches.  dwp: dL/d(W/sigma)
+// in the padded forward layout [Np][R][R][Cp]; W: master [Cout][R][R][Cin].
+//   dW = (s dWsn - s <dWsn, W/sigma> u v^T) / sigma,  s = *scale (1 if null),
+// v indexed by (r, s, c).  Launch 1 forms fixed-order block partials of
+// <dWsn, W>; launch 2 sums a weight's partials (the same order in every
+// block) and applies the update elementwise.
+constexpr int kSnbParts = 256;
+
+struct SnBwdJobK {
+  const float *dwp, *W, *u, *v, *sigma, *scale;
+  float *dW, *part;
+  int Cout, Cin, RR, Cp, nparts;
+};
+struct SnBwdGroupK {
+  SnBwdJobK j[kSnGroupMax];
+  int n;
+  int off[kSnGroupMax + 1];
+};
+
+__global__ __launch_bounds__(256) void k_sngb_dot(SnBwdGroupK g) {
   __shared__ float sh[4];
-  const int64_t total = (int64_t)Cout * RR * Cin;
+  const int i = find_job(g.off, g.n, blockIdx.x);
+  const SnBwdJobK& J = g.j[i];
+  const int lb = blockIdx.x - g.off[i];
+  const int total = J.Cout * J.RR * J.Cin;      // < 2^31 (host-checked)
   float acc = 0.f;
-  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
-    const int c = (int)(i % Cin);
-    const int64_t t = i / Cin;
-    acc = fmaf(dwp[t * Cp + c], W[i], acc);
+  for (int e = lb * 256 + (int)threadIdx.x; e < total; e += J.nparts * 256) {
+    const int t = e / J.Cin;
+    const int c = e - t * J.Cin;
+    acc = fmaf(J.dwp[(int64_t)t * J.Cp + c], J.W[e], acc);
   }
   const float s = block_sum<256>(acc, sh);
-  if (threadIdx.x == 0) part[blockIdx.x] = s;
+  if (threadIdx.x == 0) J.part[lb] = s;
 }
 
-__global__ void k_sn_bwd_apply(const float* dwp, const float* W, const float* u, const float* v,
-                               const float* sigma, const float* part, int nparts, int Cout, int Cin,
-                               int RR, int Cp, const float* scale_p, float* dW) {
-  __shared__ float dotsh;
-  const float extra_scale = scale_p ? *scale_p : 1.f;
-  if (threadIdx.x == 0) {
-    float d = 0.f;
-    for (int j = 0; j < nparts; ++j) d += part[j];
-    dotsh = d / *sigma;      // <dWsn, W/sigma>
+__global__ __launch_bounds__(256) void k_sngb_apply(SnBwdGroupK g) {
+  __shared__ float sh[4];
+  const int i = find_job(g.off, g.n, blockIdx.x);
+  const SnBwdJobK& J = g.j[i];
+  const int lb = blockIdx.x - g.off[i];
+  const float p = (int)threadIdx.x < J.nparts ? J.part[threadIdx.x] : 0.f;
+  const float sig = *J.sigma;
+  const float extra = J.scale ? *J.scale : 1.f;
+  const float dot = block_sum<256>(p, sh) / sig * extra;   // s <dWsn, W/sigma>
+  const float inv = 1.f / sig;
+  const int total = J.Cout * J.RR * J.Cin;
+  const int e = lb * 256 + (int)threadIdx.x;
+  if (e >= total) return;
+  const int t = e / J.Cin;        // n * RR + tap
+  const int c = e - t * J.Cin;
+  const int n = t / J.RR;
+  const int k = e - n * J.RR * J.Cin;   // column index (tap, c)
+  J.dW[e] = (extra * J.dwp[(int64_t)t * J.Cp + c] - dot * J.u[n] * J.v[k]) * inv;
+}
+
+void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part) {
+  PG_CHECK(n >= 1 && n <= kSnGroupMax, "sn bwd group: 1..8 weights");
+  SnBwdGroupK g{};
+  g.n = n;
+  SnBwdGroupK g2;
+  int b1 = 0;
+  int64_t b2 = 0;
+  for (int i = 0; i < n; ++i) {
+    const SnBwdJob& a = jobs[i];
+    const int64_t total = (int64_t)a.Cout * a.R * a.R * a.Cin;
+    PG_CHECK(total < (1LL << 31) && (int64_t)a.Cout * a.R * a.R * a.Cp < (1LL << 40), "sn bwd group: shape");
+    const int np = (int)std::max<int64_t>(1, std::min<int64_t>(kSnbParts, cdiv(total, 256 * 16)));
+    g.j[i] = SnBwdJobK{a.dwp, a.W, a.u, a.v, a.sigma, a.scale, a.dW, part + (int64_t)i * kSnbParts,
+                       a.Cout, a.Cin, a.R * a.R, a.Cp, np};
+    g.off[i] = b1;
+    b1 += np;
   }
-  __syncthreads();
-  const float dot = dotsh * extra_scale;
-  const float inv = 1.f / *sigma;
-  const int64_t total = (int64_t)Cout * RR * Cin;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= total) return;
-  const int c = (int)(i % Cin);
-  const int64_t t = i / Cin;        // n * RR + tap
-  const int n = (int)(t / RR);
-  const int64_t k = i - (int64_t)n * RR * Cin;   // column index (tap, c)
-  dW[i] = (extra_scale * dwp[t * Cp + c] - dot * u[n] * v[k]) * inv;
+  g.off[n] = b1;
+  g2 = g;
+  for (int i = 0; i < n; ++i) {
+    g2.off[i] = (int)b2;
+    b2 += cdiv((int64_t)g.j[i].Cout * g.j[i].RR * g.j[i].Cin, 256);
+  }
+  g2.off[n] = (int)b2;
+  PG_CHECK(b2 < (1LL << 31), "sn bwd group: too large");
+  hipLaunchKernelGGL(k_sngb_dot, dim3(b1), dim3(256), 0, st, g);
+  hipLaunchKernelGGL(k_sngb_apply, dim3((unsigned)b2), dim3(256), 0, st, g2);
+  PG_LAUNCH_CHECK();
 }
 
 void sn_bwd(hipStream_t st, const float* dwp, const float* W, const float* u, const float* v,
             const float* sigma, int Cout, int Cin, int R, int Cp, const float* scale, float* dW,
             float* part /* >= 256 floats */) {
-  const int RR = R * R;
-  const int64_t total = (int64_t)Cout * RR * Cin;
-  const int nparts = (int)std::min<int64_t>(256, cdiv(total, 256));
-  hipLaunchKernelGGL(k_sn_dot_part, dim3(nparts), dim3(256), 0, st, dwp, W, Cout, Cin, RR, Cp, part);
-  hipLaunchKernelGGL(k_sn_bwd_apply, dim3((unsigned)cdiv(total, 256)), dim3(256), 0, st, dwp, W, u, v,
-                     sigma, part, nparts, Cout, Cin, RR, Cp, scale, dW);
-  PG_LAUNCH_CHECK();
+  const SnBwdJob j{dwp, W, u, v, sigma, scale, dW, Cout, Cin, R, Cp};
+  sn_bwd_group(st, &j, 1, part);
 }
 
 // ------------------------------------------------ per-channel reductions

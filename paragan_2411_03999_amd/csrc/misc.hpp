@@ -6,6 +6,31 @@ namespace pg {
 
 // spectral normalisation
 size_t sn_ws_bytes(int64_t rows, int64_t cols);
+// Grouped forms: every SN weight of a module through one launch per phase.
+constexpr int kSnGroupMax = 8;
+struct SnJob {
+  const float* W;       // [rows][cols] fp32
+  int64_t rows, cols;
+  float *u, *v, *sigma; // u updated in place; v, sigma written
+  float* u_save;        // optional copy of the final u
+};
+size_t sn_group_ws_bytes(const SnJob* jobs, int n);
+void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws);
+struct PackJob {
+  const float* W;
+  const float* sigma;
+  void* dst;
+  int Cout, Cin, R, Np, Cp;
+  bool dgrad;
+};
+void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n);
+struct SnBwdJob {
+  const float *dwp, *W, *u, *v, *sigma, *scale;
+  float* dW;
+  int Cout, Cin, R, Cp;
+};
+// part: >= 256 floats per job
+void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part);
 // u_save (optional) receives a copy of the final u (kept for the backward).
 void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, float* u, float* v,
                    float* sigma, int n_iter, float eps, void* ws, float* u_save = nullptr);
