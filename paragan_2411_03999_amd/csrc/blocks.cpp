@@ -238,7 +238,8 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   ConvIn ax;
   ax.x = x; ax.B = B; ax.Hx = H; ax.Wx = W; ax.C = Cip; ax.gather = G_UP2;
   conv_wgrad(ex.st, f32, gdy, ax, H2, W2, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
-  colsum(ex.st, f32, dy, M2, cout, Cop, 1.f, P.gr("sc.b"), w.cs);
+  // both biases add to the block output: their gradients are the same column sum of dy
+  PG_HIP(hipMemcpyAsync(P.gr("sc.b"), P.gr("conv2.b"), (size_t)cout * 4, hipMemcpyDeviceToDevice, ex.st));
   // dx_skip = Wsc^T sum2x2(dy)   (low resolution, fp32)
   ConvIn dsp;
   dsp.x = dy; dsp.B = B; dsp.Hx = H2; dsp.Wx = W2; dsp.C = Cop; dsp.gather = G_POOL2;
@@ -442,7 +443,8 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     if (down) { as.x = xp; as.Hx = Ho; as.Wx = Wo; }
     if (wgrad) {
       conv_wgrad(ex.st, f32, gs, as, Ho, Wo, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
-      colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("sc.b"), w.cs);
+      // both biases add to the block output (after the pool): the same column sum of dy
+      PG_HIP(hipMemcpyAsync(P.gr("sc.b"), P.gr("conv2.b"), (size_t)cout * 4, hipMemcpyDeviceToDevice, ex.st));
     }
     if (dx) {
       ConvIn ds;

@@ -439,20 +439,23 @@ void sn_bwd(hipStream_t st, const float* dwp, const float* W, const float* u, co
 // channels (one 16-byte bf16 load or two fp32 loads per row) of the rows
 // ro, ro + P, ... of the chunk, P threads sharing each channel group.  The
 // P partials per channel then combine in order through LDS.  Level 2 merges
-// the chunks.  Statistics use shifted sums per thread (shift = the thread's
+// the chunks.  Chunks are sized so that there are at most kMaxChunks of
+// them: enough blocks to fill the chip, few partials for level 2.  Statistics use shifted sums per thread (shift = the thread's
 // first value, so the sums stay well conditioned) and Chan's parallel
 // variance formula for every merge.
-constexpr int kRowsPerThread = 32;
+constexpr int kRowsPerThread = 32;   // minimum rows per thread
+constexpr int kMaxChunks = 1024;
 
 struct RedShape {
   int CC, P, rows_blk;
 };
-// C: channels reduced (real count); the reduction covers cpad(C) channels
-inline RedShape red_shape(int C) {
+// C: channels reduced (real count); the reduction covers cpad(C) channels of M rows
+inline RedShape red_shape(int C, int64_t M) {
   RedShape r;
   r.CC = (int)(cpad(C) / 8);
   r.P = std::max(1, 256 / r.CC);
-  r.rows_blk = r.P * kRowsPerThread;
+  const int64_t rpt = std::max<int64_t>(kRowsPerThread, cdiv(M, (int64_t)kMaxChunks * r.P));
+  r.rows_blk = (int)(r.P * rpt);
   return r;
 }
 
@@ -556,7 +559,7 @@ __global__ __launch_bounds__(1024) void k_colsum_fin(const float* part, int nch,
 }
 
 size_t colsum_ws_bytes(int64_t M, int C) {
-  return align256((size_t)cdiv(M, red_shape(C).rows_blk) * C * 4);
+  return align256((size_t)cdiv(M, red_shape(C, M).rows_blk) * C * 4);
 }
 
 void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float scale, float* out,
@@ -565,7 +568,7 @@ void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, 
     fill(st, out, C, 0.f);
     return;
   }
-  const RedShape sh = red_shape(C);
+  const RedShape sh = red_shape(C, M);
   PG_CHECK(ldc >= cpad(C) && ldc % 8 == 0, "colsum: channel stride");
   const int nch = (int)cdiv(M, sh.rows_blk);
   float* part = (float*)ws;
@@ -602,13 +605,13 @@ __global__ __launch_bounds__(1024) void k_bn_fin(const float* pmean, const float
 }
 
 size_t bn_stats_ws_bytes(int64_t M, int C) {
-  return 2 * align256((size_t)cdiv(M, red_shape(C).rows_blk) * C * 4);
+  return 2 * align256((size_t)cdiv(M, red_shape(C, M).rows_blk) * C * 4);
 }
 
 void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, float eps, float* mean,
               float* rstd, void* ws) {
   PG_CHECK(M > 0, "bn_stats: empty batch");
-  const RedShape sh = red_shape(C);
+  const RedShape sh = red_shape(C, M);
   PG_CHECK(ldc >= cpad(C) && ldc % 8 == 0, "bn_stats: channel stride");
   const int nch = (int)cdiv(M, sh.rows_blk);
   float* pmean = (float*)ws;
@@ -803,36 +806,95 @@ void cbn_tables(hipStream_t st, const float* cond, int dc, const float* Wg, cons
 // BN backward, pass 1: per (sample, channel) sums over the sample's pixels of
 //   dz = g * [bn(x) > 0]  and  dz * xhat,  xhat = (x - mean) * rstd,
 // where g is the gradient of ReLU(BN(x)) (fp32; optionally given at 2x
-// resolution and summed over 2x2 -- the upsample's adjoint).
+// resolution and summed over 2x2 -- the upsample's adjoint).  Blocks are
+// (chunk of a sample's pixels, sample); a thread owns 8 channels of the
+// pixels ro, ro + P, ... of the chunk (16-byte loads), and the P partials
+// of each channel combine in order through LDS.
+struct BnbShape {
+  int CC, P, nchs, rows;   // channel groups, phases, chunks per sample, rows per chunk
+};
+inline BnbShape bnb_shape(int B, int HW, int C) {
+  BnbShape s;
+  s.CC = (int)(cpad(C) / 8);
+  s.P = std::max(1, 256 / s.CC);
+  const int maxch = std::max(1, HW / (s.P * kRowsPerThread));
+  s.nchs = std::min(maxch, std::max(1, kMaxChunks / B));
+  s.rows = (int)cdiv(HW, s.nchs);
+  s.nchs = (int)cdiv(HW, s.rows);
+  return s;
+}
+
+// 8 fp32 gradient values of pixel r (of HW) of sample b at channel c0, read
+// directly or as the 2x2 sum at twice the resolution
+PG_DEV void load_g8(const float* g, int g_up2, int64_t m, int b, int r, FastDiv fdW, int H, int W, int Cp, int c0,
+                    float* v) {
+  if (!g_up2) {
+    load8f<float>(g + m * Cp + c0, v);
+    return;
+  }
+  const int h = (int)fdiv((uint32_t)r, fdW), w = r - h * W;
+  const int64_t base = (((int64_t)b * 2 * H + 2 * h) * 2 * W + 2 * w) * Cp + c0;
+  const int64_t dn = (int64_t)2 * W * Cp;
+  float a[8], c[8], d[8];
+  load8f<float>(g + base, v);
+  load8f<float>(g + base + Cp, a);
+  load8f<float>(g + base + dn, c);
+  load8f<float>(g + base + dn + Cp, d);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (v[e] + a[e]) + (c[e] + d[e]);
+}
+
 template <typename T>
-__global__ void k_bnb_reduce(const float* g, int g_up2, const T* x, int HW, int H, int W, int C, int Cp,
-                             const float* mean, const float* rstd, const float* gain, const float* bias,
-                             int tab_stride, int rows_per, float* p1, float* p2) {
+__global__ __launch_bounds__(256) void k_bnb_reduce(const float* g, int g_up2, const T* x, int HW, int H, int W,
+                                                    FastDiv fdW, int C, int Cp, const float* mean,
+                                                    const float* rstd, const float* gain, const float* bias,
+                                                    int tab_stride, BnbShape sh, float* p1, float* p2) {
+  __shared__ float s_a[256 * 8], s_b[256 * 8];
   const int b = blockIdx.y;
-  const int r0 = blockIdx.x * rows_per;
-  const int r1 = min(r0 + rows_per, HW);
-  for (int c = threadIdx.x; c < C; c += blockDim.x) {
-    const float mu = mean[c], rs = rstd[c];
-    const float ga = gain[(int64_t)b * tab_stride + c], be = bias[(int64_t)b * tab_stride + c];
-    float s1 = 0.f, s2 = 0.f;
-    for (int r = r0; r < r1; ++r) {
+  const int t = threadIdx.x;
+  const int cg = t % sh.CC, ph = t / sh.CC;
+  const int c0 = cg * 8;
+  const int r0 = blockIdx.x * sh.rows;
+  const int r1 = min(r0 + sh.rows, HW);
+  float s1[8], s2[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) s1[e] = s2[e] = 0.f;
+  if (ph < sh.P) {
+    float mu[8], rs[8], ga[8], be[8];
+    load8f<float>(mean + c0, mu);
+    load8f<float>(rstd + c0, rs);
+    load8f<float>(gain + (int64_t)b * tab_stride + c0, ga);
+    load8f<float>(bias + (int64_t)b * tab_stride + c0, be);
+    for (int r = r0 + ph; r < r1; r += sh.P) {
       const int64_t m = (int64_t)b * HW + r;
-      const float xh = (ld<T>(x, m * Cp + c) - mu) * rs;
-      float gv;
-      if (!g_up2) {
-        gv = g[m * Cp + c];
-      } else {
-        const int h = r / W, w = r % W;
-        const int64_t base = (((int64_t)b * 2 * H + 2 * h) * 2 * W + 2 * w) * Cp + c;
-        gv = (g[base] + g[base + Cp]) + (g[base + (int64_t)2 * W * Cp] + g[base + (int64_t)2 * W * Cp + Cp]);
+      float xv[8], gv[8];
+      load8f<T>(x + m * Cp + c0, xv);
+      load_g8(g, g_up2, m, b, r, fdW, H, W, Cp, c0, gv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xh = (xv[e] - mu[e]) * rs[e];
+        const float dz = (ga[e] * xh + be[e] > 0.f) ? gv[e] : 0.f;
+        s1[e] += dz;
+        s2[e] = fmaf(dz, xh, s2[e]);
       }
-      const float dz = (ga * xh + be > 0.f) ? gv : 0.f;
-      s1 += dz;
-      s2 = fmaf(dz, xh, s2);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    s_a[t * 8 + e] = s1[e];
+    s_b[t * 8 + e] = s2[e];
+  }
+  __syncthreads();
+  for (int c = t; c < C; c += 256) {
+    const int gi = c >> 3, e = c & 7;
+    float a1 = 0.f, a2 = 0.f;
+    for (int j = 0; j < sh.P; ++j) {
+      a1 += s_a[(j * sh.CC + gi) * 8 + e];
+      a2 += s_b[(j * sh.CC + gi) * 8 + e];
     }
     const int64_t o = ((int64_t)b * gridDim.x + blockIdx.x) * C + c;
-    p1[o] = s1;
-    p2[o] = s2;
+    p1[o] = a1;
+    p2[o] = a2;
   }
 }
 
@@ -894,41 +956,46 @@ __global__ __launch_bounds__(1024) void k_bnb_fin2(const float* p1, const float*
   }
 }
 
-// pass 3: dx = rstd * (gain * dz - A - xhat * Bc) (+ res, at the same pixel)
+// pass 3: dx = rstd * (gain * dz - A - xhat * Bc) (+ res, at the same pixel);
+// a thread per (pixel, 8 channels), 16-byte loads and stores.
 template <typename T>
-__global__ void k_bnb_apply(const float* g, int g_up2, const T* x, int64_t M, int HW, int H, int W, int C,
-                            int Cp, const float* mean, const float* rstd, const float* gain,
-                            const float* bias, int tab_stride, const float* A, const float* Bc,
-                            const float* res, T* dx) {
+__global__ __launch_bounds__(256) void k_bnb_apply(const float* g, int g_up2, const T* x, int64_t n8, int CC,
+                                                   FastDiv fdCC, FastDiv fdHW, FastDiv fdW, int HW, int H, int W,
+                                                   int C, int Cp, const float* mean, const float* rstd,
+                                                   const float* gain, const float* bias, int tab_stride,
+                                                   const float* A, const float* Bc, const float* res, T* dx) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= M * Cp) return;
-  const int c = (int)(i % Cp);
-  const int64_t m = i / Cp;
-  float out = 0.f;
-  if (c < C) {
-    const int b = (int)(m / HW);
-    const int r = (int)(m - (int64_t)b * HW);
-    const float xh = (ld<T>(x, i) - mean[c]) * rstd[c];
-    const float ga = gain[(int64_t)b * tab_stride + c], be = bias[(int64_t)b * tab_stride + c];
-    float gv;
-    if (!g_up2) {
-      gv = g[i];
-    } else {
-      const int h = r / W, w = r % W;
-      const int64_t base = (((int64_t)b * 2 * H + 2 * h) * 2 * W + 2 * w) * Cp + c;
-      gv = (g[base] + g[base + Cp]) + (g[base + (int64_t)2 * W * Cp] + g[base + (int64_t)2 * W * Cp + Cp]);
-    }
-    const float dz = (ga * xh + be > 0.f) ? gv : 0.f;
-    out = rstd[c] * (ga * dz - A[c] - xh * Bc[c]);
-    if (res) out += res[i];
+  if (i >= n8) return;
+  const int p = (int)fdiv((uint32_t)i, fdCC);
+  const int c0 = ((int)i - p * CC) * 8;
+  const int b = (int)fdiv((uint32_t)p, fdHW);
+  const int r = p - b * HW;
+  float xv[8], gv[8], mu[8], rs[8], ga[8], be[8], aa[8], bb[8];
+  load8f<T>(x + (int64_t)p * Cp + c0, xv);
+  load_g8(g, g_up2, p, b, r, fdW, H, W, Cp, c0, gv);
+  load8f<float>(mean + c0, mu);
+  load8f<float>(rstd + c0, rs);
+  load8f<float>(gain + (int64_t)b * tab_stride + c0, ga);
+  load8f<float>(bias + (int64_t)b * tab_stride + c0, be);
+  load8f<float>(A + c0, aa);
+  load8f<float>(Bc + c0, bb);
+  float rv[8];
+  if (res) load8f<float>(res + (int64_t)p * Cp + c0, rv);
+  float out[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float xh = (xv[e] - mu[e]) * rs[e];
+    const float dz = (ga[e] * xh + be[e] > 0.f) ? gv[e] : 0.f;
+    float o = rs[e] * (ga[e] * dz - aa[e] - xh * bb[e]);
+    if (res) o += rv[e];
+    out[e] = c0 + e < C ? o : 0.f;
   }
-  st<T>(dx, i, out);
+  store8f<T>(dx + (int64_t)p * Cp + c0, out);
 }
 
 size_t bn_bwd_ws_bytes(int B, int HW, int C) {
-  const int rows_per = 1024;
-  const int nch = (int)cdiv(HW, rows_per);
-  return 2 * align256((size_t)B * nch * C * 4) + 2 * align256((size_t)C * 4);
+  const BnbShape sh = bnb_shape(B, HW, C);
+  return 2 * align256((size_t)B * sh.nchs * C * 4) + 2 * align256((size_t)cpad(C) * 4);
 }
 
 void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x, int B, int H, int W,
@@ -936,32 +1003,39 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
             int tab_stride, const float* res, void* dx, float* dgain, float* dbias, int dg_stride,
             void* ws) {
   const int HW = H * W;
-  const int rows_per = 1024;
-  const int nch = (int)cdiv(HW, rows_per);
+  const BnbShape sh = bnb_shape(B, HW, C);
+  PG_CHECK(Cp % 8 == 0 && Cp >= cpad(C) && tab_stride % 8 == 0, "bn_bwd: channel layout");
+  PG_CHECK(((uintptr_t)mean | (uintptr_t)rstd | (uintptr_t)gain | (uintptr_t)bias | (uintptr_t)g) % 16 == 0,
+           "bn_bwd: alignment");
+  const int nch = sh.nchs;
   float* p1 = (float*)ws;
   float* p2 = (float*)((char*)p1 + align256((size_t)B * nch * C * 4));
   float* A = (float*)((char*)p2 + align256((size_t)B * nch * C * 4));
-  float* Bc = (float*)((char*)A + align256((size_t)C * 4));
-  const int nt = C >= 256 ? 256 : (int)cdiv(C, 64) * 64;
+  float* Bc = (float*)((char*)A + align256((size_t)cpad(C) * 4));
+  const FastDiv fdW = make_fastdiv(W);
   dim3 g1(nch, B);
   if (f32)
-    hipLaunchKernelGGL(k_bnb_reduce<float>, g1, dim3(nt), 0, st, g, (int)g_up2, (const float*)x, HW, H, W,
-                       C, Cp, mean, rstd, gain, bias, tab_stride, rows_per, p1, p2);
+    hipLaunchKernelGGL(k_bnb_reduce<float>, g1, dim3(256), 0, st, g, (int)g_up2, (const float*)x, HW, H, W, fdW,
+                       C, Cp, mean, rstd, gain, bias, tab_stride, sh, p1, p2);
   else
-    hipLaunchKernelGGL(k_bnb_reduce<bf16_t>, g1, dim3(nt), 0, st, g, (int)g_up2, (const bf16_t*)x, HW, H,
-                       W, C, Cp, mean, rstd, gain, bias, tab_stride, rows_per, p1, p2);
+    hipLaunchKernelGGL(k_bnb_reduce<bf16_t>, g1, dim3(256), 0, st, g, (int)g_up2, (const bf16_t*)x, HW, H, W, fdW,
+                       C, Cp, mean, rstd, gain, bias, tab_stride, sh, p1, p2);
   hipLaunchKernelGGL(k_bnb_fin1, dim3((unsigned)cdiv((int64_t)B * C, 256)), dim3(256), 0, st, p1, p2, nch, B, C,
                      dgain, dbias, dg_stride);
   hipLaunchKernelGGL(k_bnb_fin2, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, p1, p2, nch, B, C, gain,
                      tab_stride, (int64_t)B * HW, dgain, dbias, A, Bc, dg_stride);
   const int64_t M = (int64_t)B * HW;
-  dim3 g3((unsigned)cdiv(M * Cp, 256));
+  const int CC = Cp / 8;
+  const int64_t n8 = M * CC;
+  PG_CHECK(n8 < (1LL << 31) && M < (1LL << 31), "bn_bwd: too large");
+  dim3 g3((unsigned)cdiv(n8, 256));
+  const FastDiv fdCC = make_fastdiv(CC), fdHW = make_fastdiv(HW);
   if (f32)
-    hipLaunchKernelGGL(k_bnb_apply<float>, g3, dim3(256), 0, st, g, (int)g_up2, (const float*)x, M, HW, H,
-                       W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (float*)dx);
+    hipLaunchKernelGGL(k_bnb_apply<float>, g3, dim3(256), 0, st, g, (int)g_up2, (const float*)x, n8, CC, fdCC,
+                       fdHW, fdW, HW, H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (float*)dx);
   else
-    hipLaunchKernelGGL(k_bnb_apply<bf16_t>, g3, dim3(256), 0, st, g, (int)g_up2, (const bf16_t*)x, M, HW,
-                       H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (bf16_t*)dx);
+    hipLaunchKernelGGL(k_bnb_apply<bf16_t>, g3, dim3(256), 0, st, g, (int)g_up2, (const bf16_t*)x, n8, CC, fdCC,
+                       fdHW, fdW, HW, H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (bf16_t*)dx);
   PG_LAUNCH_CHECK();
 }
 
