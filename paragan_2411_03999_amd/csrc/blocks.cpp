@@ -122,7 +122,7 @@ struct GWsB {
   void* cs;
   float *dxs, *da2, *da1;
   void* dh1;
-  float *dg1, *db1, *dg2, *db2, *part;
+  float *dg1, *db1, *dg2, *db2, *part, *lin;
   void* bnb;
 };
 
@@ -164,6 +164,7 @@ static GWsB g_carve_b(const GBlock& g, Arena& a, int n_cu) {
   w.dg1 = a.f32((size_t)g.B * g.Cip); w.db1 = a.f32((size_t)g.B * g.Cip);
   w.dg2 = a.f32((size_t)g.B * g.Cop); w.db2 = a.f32((size_t)g.B * g.Cop);
   w.part = a.f32(256 * kSnGroupMax);
+  w.lin = (float*)a.bytes(cbn_linear_bwd_ws_bytes(g.B, g.dc));
   w.bnb = a.bytes(std::max(bn_bwd_ws_bytes(g.B, 4 * g.H * g.W, g.cout), bn_bwd_ws_bytes(g.B, g.H * g.W, g.cin)));
   return w;
 }
@@ -279,7 +280,7 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   for (int i = 0; i < 4; ++i) {
     const Lin& l = lins[i];
     cbn_linear_bwd(ex.st, l.dgb, B, l.C, Cps[i], cond, dc, P.w(l.name), sn[l.slot].sigma, w.dlin[i], dcond,
-                   dcond_acc || i > 0);
+                   dcond_acc || i > 0, w.lin);
     jobs[i] = sn_bwd_job(P, l.name, sn[l.slot], w.dlin[i], 1, dc, nullptr);
   }
   jobs[4] = sn_bwd_job(P, "conv1.w", sn[2], w.dwp1, 3, Cip, nullptr);

@@ -721,25 +721,29 @@ __global__ void k_cbn_tables(const float* cond, int dc, const float* Wg, const f
 // Small fp32 GEMM for the conditional-BN linear maps (B x dc by dc x C and
 // their transposes): C[i][j] = sum_k A(i, k) B(k, j) [/ *div] [+ C[i][j]],
 // A(i, k) = A[i * sai + k * sak], B(k, j) = B[k * sbk + j * sbj].  32 x 32
-// tiles through LDS, k in chunks of 32, fixed summation order.
+// tiles through LDS, k in chunks of 32, fixed summation order.  With a
+// split of K (blockIdx.z; part != nullptr) each split writes its raw sums
+// to part[z][M][N] and k_gemm_reduce adds them in split order.
 __global__ __launch_bounds__(256) void k_gemm_small(int M, int N, int K, const float* A, int64_t sai,
                                                     int64_t sak, const float* Bm, int64_t sbk, int64_t sbj,
-                                                    float* Cm, int64_t ldc, const float* div, int acc) {
+                                                    float* Cm, int64_t ldc, const float* div, int acc, int kper,
+                                                    float* part) {
   __shared__ float As[32][33], Bs[32][33];
   const int i0 = blockIdx.y * 32, j0 = blockIdx.x * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const int kb = blockIdx.z * kper, ke = min(K, kb + kper);
   float c[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int k0 = 0; k0 < K; k0 += 32) {
+  for (int k0 = kb; k0 < ke; k0 += 32) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int r = ty + 8 * q;
       // the lane index runs along whichever dimension is contiguous
       int ai, ak;
       if (sak == 1) { ai = r; ak = tx; } else { ai = tx; ak = r; }
-      As[ai][ak] = (i0 + ai < M && k0 + ak < K) ? A[(i0 + ai) * sai + (int64_t)(k0 + ak) * sak] : 0.f;
+      As[ai][ak] = (i0 + ai < M && k0 + ak < ke) ? A[(i0 + ai) * sai + (int64_t)(k0 + ak) * sak] : 0.f;
       int bk, bj;
       if (sbj == 1) { bk = r; bj = tx; } else { bk = tx; bj = r; }
-      Bs[bk][bj] = (k0 + bk < K && j0 + bj < N) ? Bm[(int64_t)(k0 + bk) * sbk + (j0 + bj) * sbj] : 0.f;
+      Bs[bk][bj] = (k0 + bk < ke && j0 + bj < N) ? Bm[(int64_t)(k0 + bk) * sbk + (j0 + bj) * sbj] : 0.f;
     }
     __syncthreads();
 #pragma unroll 8
@@ -756,18 +760,43 @@ __global__ __launch_bounds__(256) void k_gemm_small(int M, int N, int K, const f
   for (int q = 0; q < 4; ++q) {
     const int i = i0 + ty + 8 * q;
     if (i >= M) continue;
+    if (part) {
+      part[((int64_t)blockIdx.z * M + i) * N + j] = c[q];
+      continue;
+    }
     float v = div ? c[q] / *div : c[q];
     if (acc) v += Cm[(int64_t)i * ldc + j];
     Cm[(int64_t)i * ldc + j] = v;
   }
 }
 
+__global__ void k_gemm_reduce(int M, int N, int splits, const float* part, float* Cm, int64_t ldc,
+                              const float* div, int acc) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (int64_t)M * N) return;
+  const int i = (int)(e / N), j = (int)(e - (int64_t)i * N);
+  float sum = 0.f;
+  for (int z = 0; z < splits; ++z) sum += part[(int64_t)z * M * N + e];
+  float v = div ? sum / *div : sum;
+  if (acc) v += Cm[(int64_t)i * ldc + j];
+  Cm[(int64_t)i * ldc + j] = v;
+}
+
 static void gemm_small(hipStream_t st, int M, int N, int K, const float* A, int64_t sai, int64_t sak,
                        const float* Bm, int64_t sbk, int64_t sbj, float* Cm, int64_t ldc, const float* div,
-                       bool acc) {
+                       bool acc, float* part = nullptr, int splits = 1) {
   if (M <= 0 || N <= 0) return;
-  hipLaunchKernelGGL(k_gemm_small, dim3((unsigned)cdiv(N, 32), (unsigned)cdiv(M, 32)), dim3(256), 0, st, M, N, K,
-                     A, sai, sak, Bm, sbk, sbj, Cm, ldc, div, (int)acc);
+  if (!part || splits <= 1) {
+    hipLaunchKernelGGL(k_gemm_small, dim3((unsigned)cdiv(N, 32), (unsigned)cdiv(M, 32)), dim3(256), 0, st, M, N, K,
+                       A, sai, sak, Bm, sbk, sbj, Cm, ldc, div, (int)acc, K, (float*)nullptr);
+    return;
+  }
+  const int kper = (int)cdiv(cdiv(K, splits), 32) * 32;
+  splits = (int)cdiv(K, kper);
+  hipLaunchKernelGGL(k_gemm_small, dim3((unsigned)cdiv(N, 32), (unsigned)cdiv(M, 32), (unsigned)splits), dim3(256),
+                     0, st, M, N, K, A, sai, sak, Bm, sbk, sbj, Cm, ldc, div, (int)acc, kper, part);
+  hipLaunchKernelGGL(k_gemm_reduce, dim3((unsigned)cdiv((int64_t)M * N, 256)), dim3(256), 0, st, M, N, splits, part,
+                     Cm, ldc, div, (int)acc);
 }
 
 // gain = 1 + gain_raw, scale = gain * rstd; padded channels -> 0
@@ -1042,11 +1071,15 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
 // Linear-map gradients of the conditional BN:
 //   dW[c][j] = sum_b dgb[b][c] cond[b][j]   (gradient of W/sigma; SN bwd follows)
 //   dcond[b][j] (+)= sum_c dgb[b][c] W[c][j] / sigma
+size_t cbn_linear_bwd_ws_bytes(int B, int dc) { return align256((size_t)kLinSplits * B * dc * 4); }
+
 void cbn_linear_bwd(hipStream_t st, const float* dgb, int B, int C, int Cp, const float* cond, int dc,
-                    const float* W, const float* sigma, float* dW, float* dcond, bool accumulate) {
+                    const float* W, const float* sigma, float* dW, float* dcond, bool accumulate, float* ws) {
   // dW[c][j] = sum_b dgb[b][c] cond[b][j];  dcond[b][j] (+)= sum_c dgb[b][c] W[c][j] / sigma
   gemm_small(st, C, dc, B, dgb, 1, Cp, cond, dc, 1, dW, dc, nullptr, false);
-  gemm_small(st, B, dc, C, dgb, Cp, 1, W, dc, 1, dcond, dc, sigma, accumulate);
+  // K = C is long and M x N = B x dc small: split K for parallelism
+  const int splits = ws ? (int)std::min<int64_t>(kLinSplits, cdiv(C, 128)) : 1;
+  gemm_small(st, B, dc, C, dgb, Cp, 1, W, dc, 1, dcond, dc, sigma, accumulate, ws, splits);
   PG_LAUNCH_CHECK();
 }
 

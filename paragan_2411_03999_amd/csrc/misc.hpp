@@ -65,8 +65,11 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
             int C, int Cp, const float* mean, const float* rstd, const float* gain, const float* bias,
             int tab_stride, const float* res, void* dx, float* dgain, float* dbias, int dg_stride,
             void* ws);
+// ws: cbn_linear_bwd_ws_bytes() of scratch for a split-K dcond (may be null)
+constexpr int kLinSplits = 8;
+size_t cbn_linear_bwd_ws_bytes(int B, int dc);
 void cbn_linear_bwd(hipStream_t st, const float* dgb, int B, int C, int Cp, const float* cond, int dc,
-                    const float* W, const float* sigma, float* dW, float* dcond, bool accumulate);
+                    const float* W, const float* sigma, float* dW, float* dcond, bool accumulate, float* ws);
 void fill(hipStream_t st, float* p, int64_t n, float v);
 // out[b][i][j][c] = ((x[2i][2j] + x[2i][2j+1]) + x[2i+1][2j]) + x[2i+1][2j+1]) / 4, in the
 // activation type (NHWC, channel stride Cp; H and W even)

@@ -60,6 +60,7 @@ struct WgTrK {
   int M;             // conv-grid pixels
   FastDiv fdW, fdH, fdC, fdR;
   int m_per_split, tiles_n, tiles_k;
+  float scale;       // applied to the sums written (1 when splits are reduced later)
   float* part;       // [splits][Np][Kdim]
 };
 
@@ -225,18 +226,38 @@ __global__ __launch_bounds__(256, 2) void k_wgrad_tr(WgTrK k) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int n = n0 + (wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (n < k.Np) part[(int64_t)n * k.Kdim + kc] = acc[i][j][r];
+        if (n < k.Np) part[(int64_t)n * k.Kdim + kc] = acc[i][j][r] * k.scale;
       }
     }
 }
 
-// dw = scale * sum over splits, in split order
+// dw = scale * sum over splits, in split order (few splits: a thread per output)
 __global__ void k_wgtr_reduce(const float* part, int splits, int64_t n, float scale, float* out) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   float s = 0.f;
   for (int j = 0; j < splits; ++j) s += part[(int64_t)j * n + i];
   out[i] = s * scale;
+}
+
+// Many splits: 64 outputs per block, 16 waves each summing every 16th split,
+// then the 16 sums in wave order (a fixed order, as above).
+__global__ __launch_bounds__(1024) void k_wgtr_reduce_wide(const float* part, int splits, int64_t n, float scale,
+                                                           float* out) {
+  __shared__ float sh[16][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int64_t i = (int64_t)blockIdx.x * 64 + lane;
+  float s = 0.f;
+  if (i < n)
+    for (int j = wv; j < splits; j += 16) s += part[(int64_t)j * n + i];
+  sh[wv][lane] = s;
+  __syncthreads();
+  if (wv == 0 && i < n) {
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < 16; ++w) t += sh[w][lane];
+    out[i] = t * scale;
+  }
 }
 
 struct TrCfg {
@@ -343,10 +364,10 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   k.tiles_n = p.tiles_n;
   k.tiles_k = p.tiles_k;
   const int64_t nout = (int64_t)Np * k.Kdim;
-  const bool direct = p.splits == 1 && g.gscale == 1.f;
-  if (!direct && p.splits > 1 && (size_t)p.splits * nout * 4 > ws_bytes)
-    throw Error{-3, "conv_wgrad: workspace too small"};
-  k.part = direct || p.splits == 1 ? dw : (float*)ws;
+  if (p.splits > 1 && (size_t)p.splits * nout * 4 > ws_bytes) throw Error{-3, "conv_wgrad: workspace too small"};
+  // a single split writes the scaled result itself; several leave unscaled partials
+  k.part = p.splits == 1 ? dw : (float*)ws;
+  k.scale = p.splits == 1 ? g.gscale : 1.f;
   const int blocks = p.splits * p.tiles_n * p.tiles_k;
   const bool gup = g.gather == G_UP2;
   std::string name;
@@ -361,10 +382,14 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   }
   PG_LAUNCH_CHECK();
   prof.done(name, flops, k.M, Np, k.Kdim);
-  if (p.splits > 1 || g.gscale != 1.f) {
+  if (p.splits > 1) {
     ProfScope pr(s);
-    hipLaunchKernelGGL(k_wgtr_reduce, dim3((unsigned)cdiv(nout, 256)), dim3(256), 0, s, k.part, p.splits,
-                       nout, g.gscale, dw);
+    if (p.splits <= 8)
+      hipLaunchKernelGGL(k_wgtr_reduce, dim3((unsigned)cdiv(nout, 256)), dim3(256), 0, s, k.part, p.splits, nout,
+                         g.gscale, dw);
+    else
+      hipLaunchKernelGGL(k_wgtr_reduce_wide, dim3((unsigned)cdiv(nout, 64)), dim3(1024), 0, s, k.part, p.splits,
+                         nout, g.gscale, dw);
     PG_LAUNCH_CHECK();
     pr.done("k_wgtr_reduce", 0.0);
   }
