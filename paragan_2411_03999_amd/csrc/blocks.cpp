@@ -182,9 +182,9 @@ void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* co
   SnJob jobs[7];
   for (int i = 0; i < 7; ++i) jobs[i] = sn_job(P, kGSN[i], sn[i]);
   sn_power_iter_group(ex.st, jobs, 7, npi, sn_eps, w.sn);
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, wp1, cout, cin, 3, Cop, Cip, false},
-                         {P.w("conv2.w"), sn[5].sigma, wp2, cout, cout, 3, Cop, Cop, false},
-                         {P.w("sc.w"), sn[6].sigma, wpsc, cout, cin, 1, Cop, Cip, false}};
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, wp1, cout, cin, 3, Cop, Cip, kPackFwd},
+                         {P.w("conv2.w"), sn[5].sigma, wp2, cout, cout, 3, Cop, Cop, kPackFwd},
+                         {P.w("sc.w"), sn[6].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
   pack_group(ex.st, f32, pk, 3);
   const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
   // cBN1 statistics and tables
@@ -224,9 +224,9 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   GWsB w = g_carve_b(*this, a, ex.n_cu);
   const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
   const int H2 = 2 * H, W2 = 2 * W;
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, w.wd1, cout, cin, 3, Cop, Cip, true},
-                         {P.w("conv2.w"), sn[5].sigma, w.wd2, cout, cout, 3, Cop, Cop, true},
-                         {P.w("sc.w"), sn[6].sigma, w.wdsc, cout, cin, 1, Cop, Cip, true}};
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, w.wd1, cout, cin, 3, Cop, Cip, kPackDgrad},
+                         {P.w("conv2.w"), sn[5].sigma, w.wd2, cout, cout, 3, Cop, Cop, kPackDgrad},
+                         {P.w("sc.w"), sn[6].sigma, w.wdsc, cout, cin, 1, Cop, Cip, kPackDgrad}};
   pack_group(ex.st, f32, pk, 3);
   // conv2: dW2, db2
   GradIn gdy;
@@ -302,7 +302,8 @@ void DBlock::plan_saved(Arena& a) {
   if (lsc) plan_sn(a, sn[2], cout, cin);
   const size_t e = esz(f32);
   wp1 = a.bytes((size_t)Cop * 9 * Cip * e);
-  wp2 = a.bytes((size_t)Cop * 9 * Cop * e);
+  // a downsampling bf16 block keeps conv2 as the pre-pooled stride-2 4x4 filter
+  wp2 = a.bytes((size_t)Cop * (s2conv() ? 16 : 9) * Cop * e);
   if (lsc) wpsc = a.bytes((size_t)Cop * Cip * e);
   h = a.bytes((size_t)B * H * W * Cop * e);
   // the pooled block input, operand of the downsampling 1x1 skip
@@ -366,9 +367,9 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   const SnJob jobs[3] = {sn_job(P, "conv1.w", sn[0]), sn_job(P, "conv2.w", sn[1]),
                          lsc ? sn_job(P, "sc.w", sn[2]) : SnJob{}};
   sn_power_iter_group(ex.st, jobs, nsn, npi, sn_eps, w.sn);
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, wp1, cout, cin, 3, Cop, Cip, false},
-                         {P.w("conv2.w"), sn[1].sigma, wp2, cout, cout, 3, Cop, Cop, false},
-                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, wpsc, cout, cin, 1, Cop, Cip, false}};
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, wp1, cout, cin, 3, Cop, Cip, kPackFwd},
+                         {P.w("conv2.w"), sn[1].sigma, wp2, cout, cout, 3, Cop, Cop, s2conv() ? kPackPool4 : kPackFwd},
+                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
   pack_group(ex.st, f32, pk, nsn);
   // h = conv3x3([relu](x)) + b1
   ConvIn i1;
@@ -388,7 +389,8 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
     so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b");
     conv_fwd(ex.st, f32, si, Ho, Wo, 1, wpsc, Cop, so);
   }
-  // y = [avgpool](conv3x3(relu(h)) + b2) + skip
+  // y = [avgpool](conv3x3(relu(h)) + b2) + skip; with downsampling in bf16 the
+  // pool is folded into the filter: a stride-2 4x4 conv at the pooled pixels
   ConvIn i2;
   i2.x = h; i2.B = B; i2.Hx = H; i2.Wx = W; i2.C = Cop; i2.relu = 1;
   ConvOut o2;
@@ -396,7 +398,13 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   o2.res_mode = R_SAME; o2.resC = Cop;
   if (lsc) { o2.res = w.skip; o2.res_f32 = 1; }
   else { o2.res = x; o2.res_f32 = f32; }
-  conv_fwd(ex.st, f32, i2, H, W, 3, wp2, Cop, o2);
+  if (s2conv()) {
+    i2.gather = G_S2;
+    o2.pool = 0;
+    conv_fwd(ex.st, f32, i2, Ho, Wo, 4, wp2, Cop, o2);
+  } else {
+    conv_fwd(ex.st, f32, i2, H, W, 3, wp2, Cop, o2);
+  }
 }
 
 void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool dx_f32,
@@ -404,9 +412,9 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   Arena a(ex.ws);
   DWsB w = d_carve_b(*this, a, ex.n_cu);
   const int64_t M = (int64_t)B * H * W, Mo = (int64_t)B * Ho * Wo;
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, w.wd1, cout, cin, 3, Cop, Cip, true},
-                         {P.w("conv2.w"), sn[1].sigma, w.wd2, cout, cout, 3, Cop, Cop, true},
-                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, w.wdsc, cout, cin, 1, Cop, Cip, true}};
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, w.wd1, cout, cin, 3, Cop, Cip, kPackDgrad},
+                         {P.w("conv2.w"), sn[1].sigma, w.wd2, cout, cout, 3, Cop, Cop, kPackDgrad},
+                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, w.wdsc, cout, cin, 1, Cop, Cip, kPackDgrad}};
   pack_group(ex.st, f32, pk, lsc ? 3 : 2);
   // conv2 (its output gradient is dy, or dy/4 spread over 2x2 when pooled)
   GradIn g2;

@@ -113,6 +113,8 @@ struct DBlock {
   void *wp1 = nullptr, *wp2 = nullptr, *wpsc = nullptr;
   void* h = nullptr;
   void* xp = nullptr;   // 2x2 average of the input (downsampling learnable skip)
+  // conv2 + 2x2 average pool as one stride-2 4x4 conv (bf16 downsampling blocks)
+  bool s2conv() const { return down && !f32; }
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);

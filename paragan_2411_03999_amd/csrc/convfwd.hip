@@ -1,5 +1,6 @@
 // Implicit-GEMM convolution (forward and data gradient) on gfx950 MFMA for
-// the direct and nearest-upsample gathers with a plain or ReLU'd operand.
+// the direct, nearest-upsample and stride-2 gathers with a plain or ReLU'd
+// operand.
 //
 // GEMM: rows = output channels n (the packed weights, K contiguous), columns
 // = output pixels m (the im2col of the activation, gathered on the fly), K =
@@ -199,8 +200,12 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
     const int r = tap / R, s = tap - (tap / R) * R;
 #pragma unroll
     for (int j = 0; j < AP; ++j) {
-      const int ih = roh[j] + r - pad, iw = row_[j] + s - pad;
-      const bool ok = rv[j] && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W;
+      // source row / column: the conv-grid position plus the tap (twice the
+      // position for the stride-2 gather, whose source is twice the grid)
+      const int ih = (GATHER == G_S2 ? 2 * roh[j] : roh[j]) + r - pad;
+      const int iw = (GATHER == G_S2 ? 2 * row_[j] : row_[j]) + s - pad;
+      const int hb = GATHER == G_S2 ? k.Hx : k.H, wb = GATHER == G_S2 ? k.Wx : k.W;
+      const bool ok = rv[j] && (unsigned)ih < (unsigned)hb && (unsigned)iw < (unsigned)wb;
       const int sh = GATHER == G_UP2 ? (ih >> 1) : ih;
       const int sw = GATHER == G_UP2 ? (iw >> 1) : iw;
       roff[j] = ok ? (uint32_t)(((rb[j] * k.Hx + sh) * k.Wx + sw) * C) * 2u + 16u * lchunk : kOOB;
@@ -374,6 +379,8 @@ std::string launch_cfg(hipStream_t s, CfK& k, int gather, bool relu) {
   PG_CF_CASE(G_DIRECT, true)
   PG_CF_CASE(G_UP2, false)
   PG_CF_CASE(G_UP2, true)
+  PG_CF_CASE(G_S2, false)
+  PG_CF_CASE(G_S2, true)
 #undef PG_CF_CASE
   throw Error{-2, "conv_fwd: unsupported gather"};
 }
@@ -395,6 +402,7 @@ bool conv_fwd_mfma_ok(const ConvIn& in, int H, int W, int R, int Np, const ConvO
   if (!aligned16(o.y) || (o.res && !aligned16(o.res)) || (o.mask && !aligned16(o.mask))) return false;
   if (o.pool && o.res_mode == R_HALF) return false;
   if (o.pool && (H % 2 || W % 2)) return false;
+  if (in.gather == G_S2 && (R != 4 || in.Hx != 2 * H || in.Wx != 2 * W)) return false;
   return true;
 }
 
@@ -411,7 +419,7 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   k.H = H;
   k.W = W;
   k.R = R;
-  k.pad = R / 2;
+  k.pad = in.gather == G_S2 ? 1 : R / 2;
   k.M = (int)((int64_t)in.B * H * W);
   k.Np = Np;
   k.ksteps = R * R * (in.C / 32);

@@ -228,6 +228,8 @@ void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, f
 // one launch.
 //  forward: dst[n][r][s][c]  ([Np][R][R][Cp]),  n < Cout, c < Cin (else 0)
 //  dgrad:   dst[c][r][s][n]  ([Cp][R][R][Np]) = W[n][R-1-r][R-1-s][c]
+//  pool4:   dst[n][u][v][c]  ([Np][4][4][Cp]) = 1/4 sum over a, b in {0, 1}
+//           of W[n][u-a][v-b][c] (terms inside the 3x3 filter only)
 // The forward layout is a padded copy (a thread per element, both sides
 // contiguous along c); the dgrad layout transposes (n, c) per tap through
 // a 32 x 32 LDS tile so that reads run along c and writes along n.
@@ -235,7 +237,7 @@ struct PackJobK {
   const float* W;
   const float* sigma;
   void* dst;
-  int Cout, Cin, R, Np, Cp, dgrad;
+  int Cout, Cin, R, Np, Cp, mode;
 };
 struct PackGroupK {
   PackJobK j[kSnGroupMax];
@@ -252,7 +254,30 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
   const int RR = J.R * J.R;
   const float inv = 1.f / *J.sigma;
   T* dst = (T*)J.dst;
-  if (!J.dgrad) {
+  if (J.mode == kPackPool4) {
+    // four consecutive channels of one (n, u, v) per thread
+    const int e = (lb * 256 + (int)threadIdx.x) * 4;
+    if (e >= J.Np * 16 * J.Cp) return;
+    const int t = e / J.Cp;     // n * 16 + u * 4 + v
+    const int c = e - t * J.Cp;
+    const int n = t >> 4, u = (t >> 2) & 3, v = t & 3;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float acc = 0.f;
+      if (n < J.Cout && c + q < J.Cin) {
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int b2 = 0; b2 < 2; ++b2) {
+            const int r = u - a, s_ = v - b2;
+            if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) acc += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + c + q];
+          }
+      }
+      st<T>(dst, (int64_t)e + q, acc * (0.25f * inv));
+    }
+    return;
+  }
+  if (J.mode == kPackFwd) {
     // 32-bit indices (the host checks the sizes): four consecutive channels per thread
     const int e = (lb * 256 + (int)threadIdx.x) * 4;
     if (e >= J.Np * RR * J.Cp) return;
@@ -294,12 +319,14 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
   int64_t b = 0;
   for (int i = 0; i < n; ++i) {
     const PackJob& a = jobs[i];
-    g.j[i] = PackJobK{a.W, a.sigma, a.dst, a.Cout, a.Cin, a.R, a.Np, a.Cp, a.dgrad ? 1 : 0};
+    g.j[i] = PackJobK{a.W, a.sigma, a.dst, a.Cout, a.Cin, a.R, a.Np, a.Cp, a.mode};
     g.off[i] = (int)b;
     const int RR = a.R * a.R;
-    PG_CHECK(a.Cp % 4 == 0 && (int64_t)a.Np * RR * a.Cp < (1LL << 31) &&
+    const int RRd = a.mode == kPackPool4 ? 16 : RR;   // taps of the packed filter
+    PG_CHECK(a.mode != kPackPool4 || a.R == 3, "pack group: pool4 packs a 3x3 filter");
+    PG_CHECK(a.Cp % 4 == 0 && (int64_t)a.Np * RRd * a.Cp < (1LL << 31) &&
              (int64_t)a.Cout * RR * a.Cin < (1LL << 31), "pack group: shape");
-    b += a.dgrad ? (int64_t)RR * cdiv(a.Np, 32) * cdiv(a.Cp, 32) : cdiv((int64_t)a.Np * RR * a.Cp, 1024);
+    b += a.mode == kPackDgrad ? (int64_t)RR * cdiv(a.Np, 32) * cdiv(a.Cp, 32) : cdiv((int64_t)a.Np * RRd * a.Cp, 1024);
     PG_CHECK(b < (1LL << 31), "pack group: too large");
   }
   g.off[n] = (int)b;
@@ -312,7 +339,7 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
 
 void pack_weight(hipStream_t st, bool f32, const float* W, const float* sigma, int Cout, int Cin,
                  int R, int Np, int Cp, bool dgrad, void* dst) {
-  const PackJob j{W, sigma, dst, Cout, Cin, R, Np, Cp, dgrad};
+  const PackJob j{W, sigma, dst, Cout, Cin, R, Np, Cp, dgrad ? kPackDgrad : kPackFwd};
   pack_group(st, f32, &j, 1);
 }
 

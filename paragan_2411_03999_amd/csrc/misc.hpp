@@ -16,12 +16,16 @@ struct SnJob {
 };
 size_t sn_group_ws_bytes(const SnJob* jobs, int n);
 void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws);
+// mode: kPackFwd [Np][R][R][Cp]; kPackDgrad [Cp][R][R][Np] flipped taps;
+// kPackPool4 [Np][4][4][Cp], the 3x3 filter (R = 3) convolved with the 2x2
+// averaging box: the stride-2 filter of conv3x3 followed by avgpool2.
+enum PackMode { kPackFwd = 0, kPackDgrad = 1, kPackPool4 = 2 };
 struct PackJob {
   const float* W;
   const float* sigma;
   void* dst;
   int Cout, Cin, R, Np, Cp;
-  bool dgrad;
+  int mode;
 };
 void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n);
 struct SnBwdJob {

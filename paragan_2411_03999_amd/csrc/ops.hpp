@@ -7,7 +7,11 @@
 
 namespace pg {
 
-enum Gather { G_DIRECT = 0, G_UP2 = 1, G_POOL2 = 2 };
+// Operand gathers of the implicit-GEMM convolutions.  G_S2 reads the
+// source at stride 2 (a 4 x 4, pad-1 filter over a source of twice the conv
+// grid's size): a 3x3 conv followed by a 2x2 average pool, evaluated at the
+// pooled pixels only with the pre-pooled 4 x 4 weights (2.25x fewer MACs).
+enum Gather { G_DIRECT = 0, G_UP2 = 1, G_POOL2 = 2, G_S2 = 3 };
 enum ResMode { R_NONE = 0, R_SAME = 1, R_HALF = 2 };
 
 // The A operand of an implicit-GEMM convolution: an NHWC activation read
