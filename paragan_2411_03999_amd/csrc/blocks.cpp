@@ -145,7 +145,8 @@ static GWsB g_carve_b(const GBlock& g, Arena& a, int n_cu) {
   GWsB w;
   const int64_t M1 = (int64_t)g.B * g.H * g.W, M2 = 4 * M1;
   const size_t e = esz(g.f32);
-  w.wd1 = a.bytes((size_t)g.Cip * 9 * g.Cop * e);
+  // bf16: conv1's data gradient as the stride-2 4x4 filter (16 taps)
+  w.wd1 = a.bytes((size_t)g.Cip * (g.f32 ? 9 : 16) * g.Cop * e);
   w.wd2 = a.bytes((size_t)g.Cop * 9 * g.Cop * e);
   w.wdsc = a.bytes((size_t)g.Cip * g.Cop * e);
   w.dwp1 = a.f32((size_t)g.Cop * 9 * g.Cip);
@@ -224,7 +225,8 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   GWsB w = g_carve_b(*this, a, ex.n_cu);
   const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
   const int H2 = 2 * H, W2 = 2 * W;
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, w.wd1, cout, cin, 3, Cop, Cip, kPackDgrad},
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, w.wd1, cout, cin, 3, Cop, Cip,
+                          f32 ? kPackDgrad : kPackDgradSum4},
                          {P.w("conv2.w"), sn[5].sigma, w.wd2, cout, cout, 3, Cop, Cop, kPackDgrad},
                          {P.w("sc.w"), sn[6].sigma, w.wdsc, cout, cin, 1, Cop, Cip, kPackDgrad}};
   pack_group(ex.st, f32, pk, 3);
@@ -263,13 +265,20 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   ia1.x = a1; ia1.B = B; ia1.Hx = H; ia1.Wx = W; ia1.C = Cip; ia1.gather = G_UP2;
   conv_wgrad(ex.st, f32, gdh, ia1, H2, W2, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
   colsum(ex.st, f32, w.dh1, M2, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
-  // da1 (at 2x resolution; the BN backward sums 2x2)
+  // da1 = the 2x2 sum (the upsample's adjoint) of conv1^T dh1: in bf16 one
+  // stride-2 4x4 conv straight to the low resolution; in fp32 at 2x
+  // resolution, summed by the BN backward
   ConvIn d1;
   d1.x = w.dh1; d1.B = B; d1.Hx = H2; d1.Wx = W2; d1.C = Cop;
   ConvOut d1o;
   d1o.y = w.da1; d1o.y_f32 = 1; d1o.yC = Cip; d1o.n_real = cin;
-  conv_fwd(ex.st, f32, d1, H2, W2, 3, w.wd1, Cip, d1o);
-  bn_bwd(ex.st, f32, w.da1, true, x, B, H, W, cin, Cip, mean1, rstd1, gain1, bias1, Cip, w.dxs, dx, w.dg1,
+  if (!f32) {
+    d1.gather = G_S2;
+    conv_fwd(ex.st, f32, d1, H, W, 4, w.wd1, Cip, d1o);
+  } else {
+    conv_fwd(ex.st, f32, d1, H2, W2, 3, w.wd1, Cip, d1o);
+  }
+  bn_bwd(ex.st, f32, w.da1, f32, x, B, H, W, cin, Cip, mean1, rstd1, gain1, bias1, Cip, w.dxs, dx, w.dg1,
          w.db1, Cip, w.bnb);
   // conditional-BN linear maps (+ their SN) and dcond
   struct Lin { const char* name; float* dgb; int C; int slot; };

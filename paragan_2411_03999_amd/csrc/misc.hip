@@ -230,6 +230,8 @@ void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, f
 //  dgrad:   dst[c][r][s][n]  ([Cp][R][R][Np]) = W[n][R-1-r][R-1-s][c]
 //  pool4:   dst[n][u][v][c]  ([Np][4][4][Cp]) = 1/4 sum over a, b in {0, 1}
 //           of W[n][u-a][v-b][c] (terms inside the 3x3 filter only)
+//  dsum4:   dst[c][u][v][n]  ([Cp][4][4][Np]) = sum over a, b in {0, 1}
+//           of W[n][2-u+a][2-v+b][c] (terms inside the filter only)
 // The forward layout is a padded copy (a thread per element, both sides
 // contiguous along c); the dgrad layout transposes (n, c) per tap through
 // a 32 x 32 LDS tile so that reads run along c and writes along n.
@@ -292,23 +294,40 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     }
     return;
   }
+  // transposing modes: (n, c) tiles of 32 x 32 per destination tap through LDS
   const int tn = (J.Np + 31) >> 5, tc = (J.Cp + 31) >> 5;
   const int tap = lb / (tn * tc);
   const int rem = lb - tap * tn * tc;
   const int n0 = (rem / tc) * 32, c0 = (rem % tc) * 32;
-  const int r = tap / J.R, s_ = tap - r * J.R;
-  const int ftap = (J.R - 1 - r) * J.R + (J.R - 1 - s_);
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const int DR = J.mode == kPackDgradSum4 ? 4 : J.R;   // taps per row of the destination filter
+  const int u = tap / DR, v = tap - u * DR;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int n = n0 + ty + 8 * k, c = c0 + tx;
-    tile[ty + 8 * k][tx] = (n < J.Cout && c < J.Cin) ? J.W[((int64_t)n * RR + ftap) * J.Cin + c] * inv : 0.f;
+    float val = 0.f;
+    if (n < J.Cout && c < J.Cin) {
+      if (J.mode == kPackDgradSum4) {
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+          for (int b2 = 0; b2 < 2; ++b2) {
+            const int r = 2 - u + a, s_ = 2 - v + b2;
+            if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) val += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + c];
+          }
+      } else {
+        const int ftap = (J.R - 1 - u) * J.R + (J.R - 1 - v);
+        val = J.W[((int64_t)n * RR + ftap) * J.Cin + c];
+      }
+    }
+    tile[ty + 8 * k][tx] = val * inv;
   }
   __syncthreads();
+  const int DRR = DR * DR;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int c = c0 + ty + 8 * k, n = n0 + tx;
-    if (c < J.Cp && n < J.Np) st<T>(dst, ((int64_t)c * RR + tap) * J.Np + n, tile[tx][ty + 8 * k]);
+    if (c < J.Cp && n < J.Np) st<T>(dst, ((int64_t)c * DRR + tap) * J.Np + n, tile[tx][ty + 8 * k]);
   }
 }
 
@@ -322,11 +341,13 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
     g.j[i] = PackJobK{a.W, a.sigma, a.dst, a.Cout, a.Cin, a.R, a.Np, a.Cp, a.mode};
     g.off[i] = (int)b;
     const int RR = a.R * a.R;
-    const int RRd = a.mode == kPackPool4 ? 16 : RR;   // taps of the packed filter
-    PG_CHECK(a.mode != kPackPool4 || a.R == 3, "pack group: pool4 packs a 3x3 filter");
+    const bool four = a.mode == kPackPool4 || a.mode == kPackDgradSum4;
+    const int RRd = four ? 16 : RR;   // taps of the packed filter
+    PG_CHECK(!four || a.R == 3, "pack group: the 4x4 modes pack a 3x3 filter");
     PG_CHECK(a.Cp % 4 == 0 && (int64_t)a.Np * RRd * a.Cp < (1LL << 31) &&
              (int64_t)a.Cout * RR * a.Cin < (1LL << 31), "pack group: shape");
-    b += a.mode == kPackDgrad ? (int64_t)RR * cdiv(a.Np, 32) * cdiv(a.Cp, 32) : cdiv((int64_t)a.Np * RRd * a.Cp, 1024);
+    const bool tr = a.mode == kPackDgrad || a.mode == kPackDgradSum4;
+    b += tr ? (int64_t)RRd * cdiv(a.Np, 32) * cdiv(a.Cp, 32) : cdiv((int64_t)a.Np * RRd * a.Cp, 1024);
     PG_CHECK(b < (1LL << 31), "pack group: too large");
   }
   g.off[n] = (int)b;

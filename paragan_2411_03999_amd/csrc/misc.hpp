@@ -18,8 +18,12 @@ size_t sn_group_ws_bytes(const SnJob* jobs, int n);
 void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws);
 // mode: kPackFwd [Np][R][R][Cp]; kPackDgrad [Cp][R][R][Np] flipped taps;
 // kPackPool4 [Np][4][4][Cp], the 3x3 filter (R = 3) convolved with the 2x2
-// averaging box: the stride-2 filter of conv3x3 followed by avgpool2.
-enum PackMode { kPackFwd = 0, kPackDgrad = 1, kPackPool4 = 2 };
+// averaging box: the stride-2 filter of conv3x3 followed by avgpool2;
+// kPackDgradSum4 [Cp][4][4][Np], the flipped transposed 3x3 filter convolved
+// with the 2x2 summing box: the stride-2 filter of the data gradient of
+// conv3x3 after a nearest 2x upsample (conv3x3^T, then the upsample's
+// adjoint, the 2x2 sum).
+enum PackMode { kPackFwd = 0, kPackDgrad = 1, kPackPool4 = 2, kPackDgradSum4 = 3 };
 struct PackJob {
   const float* W;
   const float* sigma;
