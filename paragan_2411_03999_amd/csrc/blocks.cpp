@@ -97,7 +97,8 @@ void GBlock::plan_saved(Arena& a) {
   const int64_t rows[7] = {cin, cin, cout, cout, cout, cout, cout};
   for (int i = 0; i < 7; ++i) plan_sn(a, sn[i], rows[i], cols[i]);
   const size_t e = esz(f32);
-  wp1 = a.bytes((size_t)Cop * 9 * Cip * e);
+  // bf16: conv1 over the upsample as four 2x2 sub-pixel filters (16 taps)
+  wp1 = a.bytes((size_t)Cop * (f32 ? 9 : 16) * Cip * e);
   wp2 = a.bytes((size_t)Cop * 9 * Cop * e);
   wpsc = a.bytes((size_t)Cop * Cip * e);
   mean1 = a.f32(Cip); rstd1 = a.f32(Cip);
@@ -183,7 +184,7 @@ void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* co
   SnJob jobs[7];
   for (int i = 0; i < 7; ++i) jobs[i] = sn_job(P, kGSN[i], sn[i]);
   sn_power_iter_group(ex.st, jobs, 7, npi, sn_eps, w.sn);
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, wp1, cout, cin, 3, Cop, Cip, kPackFwd},
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, wp1, cout, cin, 3, Cop, Cip, f32 ? kPackFwd : kPackSub},
                          {P.w("conv2.w"), sn[5].sigma, wp2, cout, cout, 3, Cop, Cop, kPackFwd},
                          {P.w("sc.w"), sn[6].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
   pack_group(ex.st, f32, pk, 3);
@@ -198,7 +199,13 @@ void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* co
   in.x = a1; in.B = B; in.Hx = H; in.Wx = W; in.C = Cip; in.gather = G_UP2;
   ConvOut o;
   o.y = h1; o.y_f32 = f32; o.yC = Cop; o.n_real = cout; o.bias = P.w("conv1.b");
-  conv_fwd(ex.st, f32, in, 2 * H, 2 * W, 3, wp1, Cop, o);
+  if (!f32) {
+    // bf16: the four sub-pixel 2x2 convs over a1 itself
+    in.gather = G_SUB;
+    conv_fwd(ex.st, f32, in, H, W, 2, wp1, Cop, o);
+  } else {
+    conv_fwd(ex.st, f32, in, 2 * H, 2 * W, 3, wp1, Cop, o);
+  }
   // cBN2
   bn_stats(ex.st, f32, h1, M2, cout, Cop, bn_eps, mean2, rstd2, w.bn);
   cbn_tables(ex.st, cond, dc, P.w("bn2.gain"), P.w("bn2.bias"), sn[3].sigma, sn[4].sigma, nullptr, nullptr,
@@ -347,7 +354,8 @@ static DWsB d_carve_b(const DBlock& d, Arena& a, int n_cu) {
   const int64_t M = (int64_t)d.B * d.H * d.W, Mo = (int64_t)d.B * d.Ho * d.Wo;
   const size_t e = esz(d.f32);
   w.wd1 = a.bytes((size_t)d.Cip * 9 * d.Cop * e);
-  w.wd2 = a.bytes((size_t)d.Cop * 9 * d.Cop * e);
+  // with the pooled conv2: its data gradient as four sub-pixel 2x2 filters
+  w.wd2 = a.bytes((size_t)d.Cop * (d.subdgrad() ? 16 : 9) * d.Cop * e);
   w.wdsc = d.lsc ? a.bytes((size_t)d.Cip * d.Cop * e) : nullptr;
   w.dwp1 = a.f32((size_t)d.Cop * 9 * d.Cip);
   w.dwp2 = a.f32((size_t)d.Cop * 9 * d.Cop);
@@ -422,7 +430,8 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   DWsB w = d_carve_b(*this, a, ex.n_cu);
   const int64_t M = (int64_t)B * H * W, Mo = (int64_t)B * Ho * Wo;
   const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, w.wd1, cout, cin, 3, Cop, Cip, kPackDgrad},
-                         {P.w("conv2.w"), sn[1].sigma, w.wd2, cout, cout, 3, Cop, Cop, kPackDgrad},
+                         {P.w("conv2.w"), sn[1].sigma, w.wd2, cout, cout, 3, Cop, Cop,
+                          subdgrad() ? kPackSubDgrad : kPackDgrad},
                          {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, w.wdsc, cout, cin, 1, Cop, Cip, kPackDgrad}};
   pack_group(ex.st, f32, pk, lsc ? 3 : 2);
   // conv2 (its output gradient is dy, or dy/4 spread over 2x2 when pooled)
@@ -442,7 +451,13 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   ConvOut d2o;
   d2o.y = w.dh; d2o.y_f32 = f32; d2o.yC = Cop; d2o.n_real = cout;
   d2o.mask = h; d2o.mask_f32 = f32; d2o.maskC = Cop;
-  conv_fwd(ex.st, f32, d2, H, W, 3, w.wd2, Cop, d2o);
+  if (subdgrad()) {
+    // conv2^T over up2(dy) / 4 as the four sub-pixel 2x2 convs over dy
+    d2.gather = G_SUB;
+    conv_fwd(ex.st, f32, d2, Ho, Wo, 2, w.wd2, Cop, d2o);
+  } else {
+    conv_fwd(ex.st, f32, d2, H, W, 3, w.wd2, Cop, d2o);
+  }
   // conv1
   GradIn g1;
   g1.g = w.dh; g1.Hs = H; g1.Ws = W; g1.C = Cop;

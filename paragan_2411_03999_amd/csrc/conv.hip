@@ -433,7 +433,9 @@ void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
   if (k.a.M == 0) return;
   const bool aff = in.mean != nullptr;
   ProfScope prof(s);
-  const double flops = 2.0 * (double)k.a.M * out.n_real * R * R * (in.c_real ? in.c_real : in.C);
+  // (the sub-pixel gather runs four parity classes over the M source pixels)
+  const double flops = 2.0 * (double)k.a.M * out.n_real * R * R * (in.c_real ? in.c_real : in.C) *
+                       (in.gather == G_SUB ? 4 : 1);
   if (f32) {
     k.cchunks = in.C / 16;
     k.ksteps = R * R * k.cchunks;

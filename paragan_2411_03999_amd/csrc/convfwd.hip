@@ -1,6 +1,6 @@
 // Implicit-GEMM convolution (forward and data gradient) on gfx950 MFMA for
-// the direct, nearest-upsample and stride-2 gathers with a plain or ReLU'd
-// operand.
+// the direct, nearest-upsample, stride-2 and sub-pixel gathers with a plain
+// or ReLU'd operand.
 //
 // GEMM: rows = output channels n (the packed weights, K contiguous), columns
 // = output pixels m (the im2col of the activation, gathered on the fly), K =
@@ -178,6 +178,9 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave / WM, wm = wave % WM;
   const bool quad = k.o.pool;
+  // sub-pixel parity class (a, b) of this block's output pixels
+  const int par = GATHER == G_SUB ? (int)blockIdx.y : 0;
+  const int pa = par >> 1, pb = par & 1;
   const int C = k.C, R = k.R, pad = k.pad;
 
   // Load j of this wave covers tile rows 16 (4 j + wave) .. + 15; lane l
@@ -202,8 +205,8 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
     for (int j = 0; j < AP; ++j) {
       // source row / column: the conv-grid position plus the tap (twice the
       // position for the stride-2 gather, whose source is twice the grid)
-      const int ih = (GATHER == G_S2 ? 2 * roh[j] : roh[j]) + r - pad;
-      const int iw = (GATHER == G_S2 ? 2 * row_[j] : row_[j]) + s - pad;
+      const int ih = GATHER == G_S2 ? 2 * roh[j] + r - pad : (GATHER == G_SUB ? roh[j] + r - 1 + pa : roh[j] + r - pad);
+      const int iw = GATHER == G_S2 ? 2 * row_[j] + s - pad : (GATHER == G_SUB ? row_[j] + s - 1 + pb : row_[j] + s - pad);
       const int hb = GATHER == G_S2 ? k.Hx : k.H, wb = GATHER == G_S2 ? k.Wx : k.W;
       const bool ok = rv[j] && (unsigned)ih < (unsigned)hb && (unsigned)iw < (unsigned)wb;
       const int sh = GATHER == G_UP2 ? (ih >> 1) : ih;
@@ -216,7 +219,8 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   for (int j = 0; j < BP; ++j) {
     const int row = 16 * (4 * j + wave) + lrow;
     const int n = n0 + row;
-    woff[j] = row < BN && n < k.Np ? (uint32_t)(n * R * R * C) * 2u + 16u * lchunk : kOOB;
+    // (the sub-pixel gather keeps one filter per parity, [4][Np][2][2][C])
+    woff[j] = row < BN && n < k.Np ? (uint32_t)((par * k.Np + n) * R * R * C) * 2u + 16u * lchunk : kOOB;
   }
 
   // producer position (tap, channel offset, step)
@@ -302,7 +306,13 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   for (int j = 0; j < TM; ++j) {
     const int m = m0 + (wm * TM + j) * 32 + lr;
     const bool mv = m < k.M;
-    const int mo = quad ? (m >> 2) : m;
+    int mo = quad ? (m >> 2) : m;
+    if (GATHER == G_SUB) {
+      // source-grid pixel (b, i, j) -> output pixel (b, 2i + a, 2j + b) of the 2x grid
+      int bb, ii, jj;
+      pix_of(k, mv ? m : 0, false, bb, ii, jj);
+      mo = (bb * 2 * k.H + 2 * ii + pa) * (2 * k.W) + 2 * jj + pb;
+    }
     wr_ok[j] = mv && (!quad || (lr & 3) == 0);
     yo[j] = mo * o.yC;
     mko[j] = mo * o.maskC;
@@ -369,7 +379,7 @@ std::string launch_cfg(hipStream_t s, CfK& k, int gather, bool relu) {
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
   k.tiles_m = (int)cdiv(k.M, BM);
   k.tiles_n = (int)cdiv(k.Np, BN);
-  dim3 grid(k.tiles_m * k.tiles_n), block(256);
+  dim3 grid(k.tiles_m * k.tiles_n, gather == G_SUB ? 4 : 1), block(256);
 #define PG_CF_CASE(G, R_)                                                             \
   if (gather == G && relu == R_) {                                                    \
     hipLaunchKernelGGL((k_conv_fwd<WN, WM, TN, TM, G, R_>), grid, block, 0, s, k);    \
@@ -381,6 +391,7 @@ std::string launch_cfg(hipStream_t s, CfK& k, int gather, bool relu) {
   PG_CF_CASE(G_UP2, true)
   PG_CF_CASE(G_S2, false)
   PG_CF_CASE(G_S2, true)
+  PG_CF_CASE(G_SUB, false)
 #undef PG_CF_CASE
   throw Error{-2, "conv_fwd: unsupported gather"};
 }
@@ -403,6 +414,9 @@ bool conv_fwd_mfma_ok(const ConvIn& in, int H, int W, int R, int Np, const ConvO
   if (o.pool && o.res_mode == R_HALF) return false;
   if (o.pool && (H % 2 || W % 2)) return false;
   if (in.gather == G_S2 && (R != 4 || in.Hx != 2 * H || in.Wx != 2 * W)) return false;
+  if (in.gather == G_SUB &&
+      (R != 2 || in.relu || in.Hx != H || in.Wx != W || o.pool || o.res_mode != R_NONE || 4 * Mo * cmax >= (1LL << 31)))
+    return false;
   return true;
 }
 
@@ -412,7 +426,7 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   k.x = (const bf16_t*)in.x;
   k.w = (const bf16_t*)w;
   k.x_bytes = 2LL * in.B * in.Hx * in.Wx * in.C;
-  k.w_bytes = 2LL * Np * R * R * in.C;
+  k.w_bytes = 2LL * Np * R * R * in.C * (in.gather == G_SUB ? 4 : 1);
   k.Hx = in.Hx;
   k.Wx = in.Wx;
   k.C = in.C;

@@ -232,6 +232,11 @@ void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, f
 //           of W[n][u-a][v-b][c] (terms inside the 3x3 filter only)
 //  dsum4:   dst[c][u][v][n]  ([Cp][4][4][Np]) = sum over a, b in {0, 1}
 //           of W[n][2-u+a][2-v+b][c] (terms inside the filter only)
+//  sub:     dst[p][n][du][dv][c] ([4][Np][2][2][Cp]), p = 2a + b, = sum of
+//           W[n][r][s][c] over r in S(a, du), s in S(b, dv), where S(a, 0) =
+//           [0, a] and S(a, 1) = [1 + a, 2]
+//  subdg:   dst[p][c][du][dv][n] ([4][Cp][2][2][Np]) = the same sums of
+//           W[n][2-r][2-s][c]
 // The forward layout is a padded copy (a thread per element, both sides
 // contiguous along c); the dgrad layout transposes (n, c) per tap through
 // a 32 x 32 LDS tile so that reads run along c and writes along n.
@@ -279,6 +284,26 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     }
     return;
   }
+  if (J.mode == kPackSub) {
+    // four consecutive channels of one (p, n, du, dv) per thread
+    const int e = (lb * 256 + (int)threadIdx.x) * 4;
+    if (e >= 4 * J.Np * 4 * J.Cp) return;
+    const int t = e / J.Cp;   // (p * Np + n) * 4 + du * 2 + dv
+    const int c = e - t * J.Cp;
+    const int dv = t & 1, du = (t >> 1) & 1, pn = t >> 2;
+    const int p = pn / J.Np, n = pn - p * J.Np;
+    const int a = p >> 1, b2 = p & 1;
+    const int r0 = du ? 1 + a : 0, r1 = du ? 2 : a, s0 = dv ? 1 + b2 : 0, s1 = dv ? 2 : b2;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float acc = 0.f;
+      if (n < J.Cout && c + q < J.Cin)
+        for (int r = r0; r <= r1; ++r)
+          for (int s_ = s0; s_ <= s1; ++s_) acc += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + c + q];
+      st<T>(dst, (int64_t)e + q, acc * inv);
+    }
+    return;
+  }
   if (J.mode == kPackFwd) {
     // 32-bit indices (the host checks the sizes): four consecutive channels per thread
     const int e = (lb * 256 + (int)threadIdx.x) * 4;
@@ -300,8 +325,10 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
   const int rem = lb - tap * tn * tc;
   const int n0 = (rem / tc) * 32, c0 = (rem % tc) * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  const int DR = J.mode == kPackDgradSum4 ? 4 : J.R;   // taps per row of the destination filter
-  const int u = tap / DR, v = tap - u * DR;
+  const int DR = J.mode == kPackDgradSum4 ? 4 : (J.mode == kPackSubDgrad ? 2 : J.R);   // destination taps per row
+  const int DRR = DR * DR;
+  const int p = tap / DRR, ptap = tap - p * DRR;   // parity class (sub-pixel mode), tap within it
+  const int u = ptap / DR, v = ptap - u * DR;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int n = n0 + ty + 8 * k, c = c0 + tx;
@@ -315,6 +342,11 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
             const int r = 2 - u + a, s_ = 2 - v + b2;
             if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) val += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + c];
           }
+      } else if (J.mode == kPackSubDgrad) {
+        const int a = p >> 1, b2 = p & 1;
+        const int r0 = u ? 1 + a : 0, r1 = u ? 2 : a, s0 = v ? 1 + b2 : 0, s1 = v ? 2 : b2;
+        for (int r = r0; r <= r1; ++r)
+          for (int s_ = s0; s_ <= s1; ++s_) val += J.W[((int64_t)n * 9 + (2 - r) * 3 + (2 - s_)) * J.Cin + c];
       } else {
         const int ftap = (J.R - 1 - u) * J.R + (J.R - 1 - v);
         val = J.W[((int64_t)n * RR + ftap) * J.Cin + c];
@@ -323,11 +355,10 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     tile[ty + 8 * k][tx] = val * inv;
   }
   __syncthreads();
-  const int DRR = DR * DR;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int c = c0 + ty + 8 * k, n = n0 + tx;
-    if (c < J.Cp && n < J.Np) st<T>(dst, ((int64_t)c * DRR + tap) * J.Np + n, tile[tx][ty + 8 * k]);
+    if (c < J.Cp && n < J.Np) st<T>(dst, (((int64_t)p * J.Cp + c) * DRR + ptap) * J.Np + n, tile[tx][ty + 8 * k]);
   }
 }
 
@@ -342,11 +373,12 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
     g.off[i] = (int)b;
     const int RR = a.R * a.R;
     const bool four = a.mode == kPackPool4 || a.mode == kPackDgradSum4;
-    const int RRd = four ? 16 : RR;   // taps of the packed filter
-    PG_CHECK(!four || a.R == 3, "pack group: the 4x4 modes pack a 3x3 filter");
+    const bool sub = a.mode == kPackSub || a.mode == kPackSubDgrad;
+    const int RRd = four || sub ? 16 : RR;   // taps of the packed filter (all parities)
+    PG_CHECK(!(four || sub) || a.R == 3, "pack group: the 4x4 and sub-pixel modes pack a 3x3 filter");
     PG_CHECK(a.Cp % 4 == 0 && (int64_t)a.Np * RRd * a.Cp < (1LL << 31) &&
              (int64_t)a.Cout * RR * a.Cin < (1LL << 31), "pack group: shape");
-    const bool tr = a.mode == kPackDgrad || a.mode == kPackDgradSum4;
+    const bool tr = a.mode == kPackDgrad || a.mode == kPackDgradSum4 || a.mode == kPackSubDgrad;
     b += tr ? (int64_t)RRd * cdiv(a.Np, 32) * cdiv(a.Cp, 32) : cdiv((int64_t)a.Np * RRd * a.Cp, 1024);
     PG_CHECK(b < (1LL << 31), "pack group: too large");
   }

@@ -23,7 +23,13 @@ void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, f
 // with the 2x2 summing box: the stride-2 filter of the data gradient of
 // conv3x3 after a nearest 2x upsample (conv3x3^T, then the upsample's
 // adjoint, the 2x2 sum).
-enum PackMode { kPackFwd = 0, kPackDgrad = 1, kPackPool4 = 2, kPackDgradSum4 = 3 };
+// kPackSub [4][Np][2][2][Cp]: per parity (a, b) of the output pixels of a
+// 3x3 conv over a nearest 2x upsample, the 2x2 filter on the source whose
+// taps sum the 3x3 taps landing on one source pixel (rows r in [0, a] for
+// tap 0 and [1 + a, 2] for tap 1, columns likewise);
+// kPackSubDgrad [4][Cp][2][2][Np]: the same for the flipped transposed
+// filter (the data gradient of conv3x3 through a 2x2 average pool).
+enum PackMode { kPackFwd = 0, kPackDgrad = 1, kPackPool4 = 2, kPackDgradSum4 = 3, kPackSub = 4, kPackSubDgrad = 5 };
 struct PackJob {
   const float* W;
   const float* sigma;

@@ -11,7 +11,12 @@ namespace pg {
 // source at stride 2 (a 4 x 4, pad-1 filter over a source of twice the conv
 // grid's size): a 3x3 conv followed by a 2x2 average pool, evaluated at the
 // pooled pixels only with the pre-pooled 4 x 4 weights (2.25x fewer MACs).
-enum Gather { G_DIRECT = 0, G_UP2 = 1, G_POOL2 = 2, G_S2 = 3 };
+// G_SUB evaluates a 3x3 conv over the nearest 2x upsample of the source as
+// four 2x2 convs over the source itself, one per parity class (a, b) of the
+// output pixels (2i + a, 2j + b), with the 3x3 taps that fall on the same
+// source pixel summed (2.25x fewer MACs); the rows are source-grid pixels,
+// blockIdx.y the parity, and the epilogue writes the upsampled position.
+enum Gather { G_DIRECT = 0, G_UP2 = 1, G_POOL2 = 2, G_S2 = 3, G_SUB = 4 };
 enum ResMode { R_NONE = 0, R_SAME = 1, R_HALF = 2 };
 
 // The A operand of an implicit-GEMM convolution: an NHWC activation read

@@ -100,21 +100,25 @@ def rel_l2(g, r):
     return float(np.linalg.norm(np.asarray(g) - np.asarray(r)) / max(np.linalg.norm(np.asarray(r)), 1e-30))
 
 
-def pooled_conv_perturbed(a, dp, seed):
-    """The discriminator weights with every pooling block's conv2 filter moved
-    by the rounding the GPU applies after folding the 2x2 average pool into
-    it: each tap of the stride-2 4x4 filter is rounded to bf16 once (relative
-    error uniform in +-2^-8, bf16 having 8 significant bits), where the
-    definition rounds the 3x3 filter.  A pooled tap averages up to four 3x3
-    taps, so moving each 3x3 tap by a relative uniform +-2^-7 gives the pooled
-    taps about the same spread."""
+def folded_filters_perturbed(a, gp, dp, seed):
+    """The weights with every filter the GPU folds before rounding moved by
+    that rounding.  The folded filters are each pooling D block's conv2 (the
+    2x2 average folded in: a stride-2 4x4 filter) and each G block's conv1
+    (the nearest upsample folded in: four 2x2 sub-pixel filters).  Each
+    folded tap sums up to four 3x3 taps and is rounded to bf16 once (relative
+    error up to 2^-8, bf16 having 8 significant bits), where the definition
+    rounds the 3x3 filter; moving each 3x3 tap by a relative uniform +-2^-7
+    gives the folded taps at least that spread."""
     rng = np.random.default_rng(seed)
-    out = dict(dp)
+    g2, d2 = dict(gp), dict(dp)
     for j, down in enumerate(a.d_down):
         if down:
             w = dp["d%d.conv2.w" % j]
-            out["d%d.conv2.w" % j] = w * (1 + 2.0 ** -7 * rng.uniform(-1, 1, w.shape))
-    return out
+            d2["d%d.conv2.w" % j] = w * (1 + 2.0 ** -7 * rng.uniform(-1, 1, w.shape))
+    for i in range(a.n_g):
+        w = gp["g%d.conv1.w" % i]
+        g2["g%d.conv1.w" % i] = w * (1 + 2.0 ** -7 * rng.uniform(-1, 1, w.shape))
+    return g2, d2
 
 
 def run_step(a, B, n_D, seed, calibrated):
@@ -145,24 +149,27 @@ def run_step(a, B, n_D, seed, calibrated):
     optG, optD = O.adam_init(gp), O.adam_init(dp)
     Gr, Dr, loss_r, gd_r, gg_r = O.train_step(a, hp, (gp, gu), (dp, du), optG, optD, d_in, g_in)
     sens = {}
-    if not calibrated and any(a.d_down):
-        # ReLU masks near zero may flip between the two rounding points of the
-        # pooled conv2 filter: the oracle's own movement under that perturbation
-        # (max-abs metric, as the checks below) bounds what a flip can do
-        optG2, optD2 = O.adam_init(gp), O.adam_init(dp)
-        _, _, _, gd2, gg2 = O.train_step(a, hp, (gp, gu), (pooled_conv_perturbed(a, dp, seed), du), optG2, optD2,
-                                         d_in, g_in)
-        sens.update({"gG." + k: norm_maxabs(gg2[k], gg_r[k]) for k in glay})
-        sens.update({"gD." + k: norm_maxabs(gd2[k], gd_r[k]) for k in dlay})
+    # ReLU masks near zero may flip between the two rounding points of the
+    # filters the GPU folds: the oracle's own movement when they move by that
+    # rounding bounds what a flip can do (max-abs metric for the strict
+    # checks, relative L2 for the calibrated ones)
+    metric = rel_l2 if calibrated else norm_maxabs
+    gp2, dp2 = folded_filters_perturbed(a, gp, dp, seed)
+    optG2, optD2 = O.adam_init(gp2), O.adam_init(dp2)
+    _, _, _, gd2, gg2 = O.train_step(a, hp, (gp2, gu), (dp2, du), optG2, optD2, d_in, g_in)
+    sens.update({"gG." + k: metric(gg2[k], gg_r[k]) for k in glay})
+    sens.update({"gD." + k: metric(gd2[k], gd_r[k]) for k in dlay})
     if calibrated:
-        # the oracle's own movement when its real images move by 1e-5
-        # (about one bf16 flip in 300 values): the chaos floor of this net
+        # and its movement when its real images move by 1e-5 (about one bf16
+        # flip in 300 values): the chaos floor of this net; the larger counts
         rng = np.random.default_rng(seed)
         d_in2 = [(x * (1 + 1e-5 * rng.standard_normal(x.shape)), yr, z, yf) for x, yr, z, yf in d_in]
         optG2, optD2 = O.adam_init(gp), O.adam_init(dp)
         _, _, _, gd2, gg2 = O.train_step(a, hp, (gp, gu), (dp, du), optG2, optD2, d_in2, g_in)
-        sens.update({"gG." + k: rel_l2(gg2[k], gg_r[k]) for k in glay})
-        sens.update({"gD." + k: rel_l2(gd2[k], gd_r[k]) for k in dlay})
+        for k in glay:
+            sens["gG." + k] = max(sens["gG." + k], rel_l2(gg2[k], gg_r[k]))
+        for k in dlay:
+            sens["gD." + k] = max(sens["gD." + k], rel_l2(gd2[k], gd_r[k]))
     rep = Report()
     lg = np.array(list(losses))
     print("losses gpu", lg, "oracle", loss_r, flush=True)
@@ -176,12 +183,10 @@ def run_step(a, B, n_D, seed, calibrated):
             if calibrated:
                 tol = max(TOL_BF16, 3 * sens[tag + k])
                 rep.add(tag + k, rel_l2(got[k], ref[k]), tol)
-            elif sens:
+            else:
                 assert np.all(np.isfinite(got[k])), tag + k
                 rep.add(tag + k, norm_maxabs(got[k], ref[k]), max(TOL_BF16, 3 * sens[tag + k]))
                 rep.err[tag + k + ".sens"] = sens[tag + k]
-            else:
-                check(tag + k, got[k], ref[k], True, rep)
     gu_new = lib.named_u_from_flat(gents, G.U)
     for k in gsn:
         check("uG." + k, gu_new[k], Gr[1][k], False, rep)
@@ -220,5 +225,6 @@ def test_train_step_minimal_strict(n_D):
 
 def test_train_step_small_biggan_calibrated():
     """Every component (attention in both nets, identity skips) at a
-    tolerance calibrated by the oracle's own chaos floor (see run_step)."""
+    tolerance calibrated by the oracle's own chaos floor and its movement
+    under the folded filters' rounding (see run_step)."""
     run_step(small_arch(), B=4, n_D=2, seed=302, calibrated=True)
