@@ -332,7 +332,7 @@ struct DWsF {
 };
 struct DWsB {
   void *wd1, *wd2, *wdsc;
-  float *dwp1, *dwp2, *dwpsc;
+  float *dwp1, *dwp2, *dwpsc, *dwp2s;
   void* wg;
   size_t wg_bytes;
   void* cs;
@@ -360,7 +360,10 @@ static DWsB d_carve_b(const DBlock& d, Arena& a, int n_cu) {
   w.dwp1 = a.f32((size_t)d.Cop * 9 * d.Cip);
   w.dwp2 = a.f32((size_t)d.Cop * 9 * d.Cop);
   w.dwpsc = d.lsc ? a.f32((size_t)d.Cop * d.Cip) : nullptr;
+  // the pooled conv2's gradient in its stride-2 4x4 form, folded to 3x3 after
+  w.dwp2s = d.s2conv() ? a.f32((size_t)d.Cop * 16 * d.Cop) : nullptr;
   w.wg_bytes = std::max(conv_wgrad_ws(d.f32, M, 3, d.Cip, d.Cop, n_cu), conv_wgrad_ws(d.f32, M, 3, d.Cop, d.Cop, n_cu));
+  if (d.s2conv()) w.wg_bytes = std::max(w.wg_bytes, conv_wgrad_ws(d.f32, Mo, 4, d.Cop, d.Cop, n_cu));
   if (d.lsc) w.wg_bytes = std::max(w.wg_bytes, conv_wgrad_ws(d.f32, Mo, 1, d.Cip, d.Cop, n_cu));
   w.wg = a.bytes(w.wg_bytes);
   w.cs = a.bytes(colsum_ws_bytes(M, d.Cop));
@@ -441,7 +444,18 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   ConvIn a2;
   a2.x = h; a2.B = B; a2.Hx = H; a2.Wx = W; a2.C = Cop; a2.relu = 1;
   if (wgrad) {
-    conv_wgrad(ex.st, f32, g2, a2, H, W, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
+    if (s2conv()) {
+      // the gradient of the stride-2 4x4 form: pooled dy against relu(h) read
+      // at stride 2, then folded back onto the 3x3 filter
+      GradIn g2s;
+      g2s.g = dy; g2s.Hs = Ho; g2s.Ws = Wo; g2s.C = Cop;
+      ConvIn a2s = a2;
+      a2s.gather = G_S2;
+      conv_wgrad(ex.st, f32, g2s, a2s, Ho, Wo, 4, Cop, w.dwp2s, w.wg, w.wg_bytes, ex.n_cu);
+      fold_pool4_wgrad(ex.st, w.dwp2s, Cop, Cop, w.dwp2);
+    } else {
+      conv_wgrad(ex.st, f32, g2, a2, H, W, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
+    }
     colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
   }
   // dh = (conv2^T dc2) * [h > 0]

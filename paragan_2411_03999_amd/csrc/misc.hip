@@ -420,6 +420,28 @@ void pack_weight_t(hipStream_t st, bool f32, const float* W, const float* sigma,
   PG_LAUNCH_CHECK();
 }
 
+// Weight gradient of a 3x3 filter from that of its pooled stride-2 4x4 form
+// (W4 = W * box / 4): dw[n][r][s][c] = 1/4 sum over a, b in {0, 1} of
+// dw4[n][r+a][s+b][c]; both fp32 in the padded [Np][taps][Cp] layouts.
+__global__ void k_fold_pool4(const float* dw4, int Np, int Cp, float* dw) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)Np * 9 * Cp) return;
+  const int c = (int)(i % Cp);
+  const int64_t t = i / Cp;
+  const int tap = (int)(t % 9), n = (int)(t / 9);
+  const int r = tap / 3, s_ = tap % 3;
+  const float* src = dw4 + (int64_t)n * 16 * Cp + c;
+  const float v = (src[(r * 4 + s_) * Cp] + src[(r * 4 + s_ + 1) * Cp]) +
+                  (src[((r + 1) * 4 + s_) * Cp] + src[((r + 1) * 4 + s_ + 1) * Cp]);
+  dw[i] = 0.25f * v;
+}
+
+void fold_pool4_wgrad(hipStream_t st, const float* dw4, int Np, int Cp, float* dw) {
+  hipLaunchKernelGGL(k_fold_pool4, dim3((unsigned)cdiv((int64_t)Np * 9 * Cp, 256)), dim3(256), 0, st, dw4, Np, Cp,
+                     dw);
+  PG_LAUNCH_CHECK();
+}
+
 // SN backward, every weight of a group in two launches.  dwp: dL/d(W/sigma)
 // in the padded forward layout [Np][R][R][Cp]; W: master [Cout][R][R][Cin].
 //   dW = (s dWsn - s <dWsn, W/sigma> u v^T) / sigma,  s = *scale (1 if null),

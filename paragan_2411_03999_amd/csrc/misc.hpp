@@ -45,6 +45,9 @@ struct SnBwdJob {
 };
 // part: >= 256 floats per job
 void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part);
+// dw[n][r][s][c] (3x3) = 1/4 sum_{a,b in {0,1}} dw4[n][r+a][s+b][c]: the gradient
+// of a 3x3 filter from that of its pooled stride-2 4x4 form
+void fold_pool4_wgrad(hipStream_t st, const float* dw4, int Np, int Cp, float* dw);
 // u_save (optional) receives a copy of the final u (kept for the backward).
 void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, float* u, float* v,
                    float* sigma, int n_iter, float eps, void* ws, float* u_save = nullptr);

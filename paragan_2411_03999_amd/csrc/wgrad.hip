@@ -2,9 +2,11 @@
 //
 //   dW[n][(r, s, c)] = sum over conv-grid pixels m of dY[m][n] * X~[m][(r, s, c)]
 //
-// where X~ is the im2col view of the activation (direct, or a nearest 2x
-// upsample of a half-resolution tensor, optionally ReLU'd) and dY the output
-// gradient (direct, or a nearest 2x upsample of a half-resolution gradient).
+// where X~ is the im2col view of the activation (direct, a nearest 2x
+// upsample of a half-resolution tensor, or read at stride 2 for a 4x4 filter
+// over a tensor of twice the grid's size; optionally ReLU'd) and dY the
+// output gradient (direct, or a nearest 2x upsample of a half-resolution
+// gradient).
 // The reduction runs over pixels, which are the rows of both operands in
 // memory, so each MFMA operand is a transposed tile.  Here both tiles are
 // copied row-major into LDS unchanged (16-byte loads and stores) and the
@@ -151,8 +153,10 @@ __global__ __launch_bounds__(256, 2) void k_wgrad_tr(WgTrK k) {
       const int ow = m - t * k.W;
       const int b = (int)fdiv((uint32_t)t, k.fdH);
       const int oh = t - b * k.H;
-      const int ih = oh + (short)(x_rs[i] & 0xffff), iw = ow + (x_rs[i] >> 16);
-      const bool ok = m < mend && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W;
+      const int ih = (XG == G_S2 ? 2 * oh : oh) + (short)(x_rs[i] & 0xffff);
+      const int iw = (XG == G_S2 ? 2 * ow : ow) + (x_rs[i] >> 16);
+      const int hb = XG == G_S2 ? k.Hx : k.H, wb = XG == G_S2 ? k.Wx : k.W;
+      const bool ok = m < mend && (unsigned)ih < (unsigned)hb && (unsigned)iw < (unsigned)wb;
       const int sh = XG == G_UP2 ? (ih >> 1) : ih, sw = XG == G_UP2 ? (iw >> 1) : iw;
       rx[i] = buf_ld16(xr, ok ? 2u * (uint32_t)(((b * k.Hx + sh) * k.Wx + sw) * k.C + x_c[i]) : kOOB);
     }
@@ -313,6 +317,7 @@ std::string launch_tr(hipStream_t s, const WgTrK& k, int blocks, bool gup, int x
   PG_WTR_CASE(true, G_DIRECT, false)
   PG_WTR_CASE(true, G_DIRECT, true)
   PG_WTR_CASE(false, G_UP2, false)
+  PG_WTR_CASE(false, G_S2, true)
 #undef PG_WTR_CASE
   throw Error{-2, "wgrad_tr: unsupported gather combination"};
 }
@@ -322,6 +327,7 @@ std::string launch_tr(hipStream_t s, const WgTrK& k, int blocks, bool gup, int x
 bool wgrad_tr_ok(const GradIn& g, const ConvIn& in, int H, int W, int R, int Np) {
   if (in.mean || in.gather == G_POOL2 || in.gscale != 1.f) return false;
   if (in.gather == G_UP2 && in.relu) return false;
+  if (in.gather == G_S2 && (R != 4 || in.Hx != 2 * H || in.Wx != 2 * W || g.gather != G_DIRECT)) return false;
   if (g.gather != G_DIRECT && g.gather != G_UP2) return false;
   const int64_t M = (int64_t)in.B * H * W;
   const int64_t xs = (int64_t)in.B * in.Hx * in.Wx * in.C;
@@ -347,7 +353,7 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   k.Kdim = R * R * in.C;
   k.C = in.C;
   k.R = R;
-  k.pad = R / 2;
+  k.pad = in.gather == G_S2 ? 1 : R / 2;
   k.H = H;
   k.W = W;
   k.Hx = in.Hx;
