@@ -33,6 +33,31 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA (published)
+
+# HBM bytes per launch of a kernel, from two rocprofv3 --pmc passes over
+# "bench.py --steps 1 --warmup 1 --no-cpu-baseline --copy-probe" (FETCH_SIZE,
+# then WRITE_SIZE, KiB per dispatch, averaged over the kernel's dispatches),
+# each scaled by what the counter reads for the 1 GiB copy probe (FETCH_SIZE
+# reads 0.5 GiB for it: x2.0; WRITE_SIZE reads 1 GiB: x1.0).  Valid only for
+# the kernel source they were taken on (sha1 prefix of the file).
+TRAFFIC = {
+    "k_conv_fwd<128x256,G_DIRECT,false>": {"fetch": 2.0 * 425926.2 * 1024, "write": 251009.7 * 1024,
+                                            "source": "paragan_2411_03999_amd/csrc/convfwd.hip",
+                                            "sha1": "f83cdf409b3b"},
+}
+
+
+def traffic_of(name):
+    """Measured HBM bytes per launch of kernel `name`, or None when none were
+    taken or its source has changed since."""
+    import hashlib
+    t = TRAFFIC.get(name)
+    if not t:
+        return None
+    with open(os.path.join(ROOT, t["source"]), "rb") as f:
+        if hashlib.sha1(f.read()).hexdigest()[:12] != t["sha1"]:
+            return None
+    return t["fetch"] + t["write"]
 METRIC = "images/sec/GPU, BigGAN-128 G+D train step; conv MFMA util % of peak"
 
 ARCHS = {
@@ -55,6 +80,41 @@ def make_desc(lib, arch, B):
     d.n_power_iter, d.bn_eps, d.sn_eps = 1, 1e-5, 1e-12
     d.lr_g, d.lr_d, d.beta1, d.beta2, d.adam_eps = 1e-4, 4e-4, 0.0, 0.999, 1e-6
     return d
+
+
+def model_flops(arch):
+    """Model FLOPs per image of one G fwd (g) and one D fwd (d), as the network
+    defines them: 2 MACs per multiply-add of every conv and linear at its own
+    resolution (G skips at the upsampled resolution, D skips conv-then-pool),
+    the attention matmuls and the output conv; padding not counted.  Returns
+    (g, d, conv_g, conv_d), the last two over conv layers only."""
+    img, ch, gm, dm, dd, attn, ncls, dz, sd = ARCHS[arch]
+    conv_g = 0.0
+    H = 4
+    for i in range(len(gm) - 1):
+        cin, cout = gm[i] * ch, gm[i + 1] * ch
+        Ho = 2 * H
+        conv_g += 2.0 * Ho * Ho * cout * (9 * cin + 9 * cout + cin)
+        H = Ho
+    conv_g += 2.0 * img * img * 3 * 9 * gm[-1] * ch           # output conv (fp32)
+    conv_d = 0.0
+    H, cin = img, 3
+    for m, down in zip(dm, dd):
+        cout = m * ch
+        skip = cin if (cin != cout or down) else 0
+        conv_d += 2.0 * H * H * cout * (9 * cin + 9 * cout + skip)
+        H, cin = (H // 2 if down else H), cout
+    def attn_flops(c, hw):
+        L = hw // 4
+        return 2.0 * hw * (2 * (c // 8) * c + (c // 2) * c + c * (c // 2)) + 2.0 * hw * L * (c // 8 + c // 2)
+    # attention at attn x attn: in G after the block producing that resolution, in D after the first block
+    gc = [gm[i + 1] * ch for i in range(len(gm) - 1)]
+    gres = [8 * 2 ** i for i in range(len(gm) - 1)]
+    g = conv_g + (attn_flops(gc[gres.index(attn)], attn * attn) if attn in gres else 0.0)
+    d = conv_d + attn_flops(dm[0] * ch, attn * attn)
+    g += 2.0 * (dz // len(gm)) * 16 * gm[0] * ch                # z linear
+    d += 2.0 * 2 * dm[-1] * ch                                  # head + projection
+    return g, d, conv_g, conv_d
 
 
 def device_net(torch, lib, ents, npar, nu, gen):
@@ -123,6 +183,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-batch", type=int, default=1)
     ap.add_argument("--kernels-out", default=None, help="write the per-kernel table (JSON) here")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="before the timed steps, copy 1 GiB device to device once: the known-size "
+                         "reference for scaling the FETCH_SIZE / WRITE_SIZE counters")
     ap.add_argument("--detail", action="store_true",
                     help="profile per GEMM shape (names carry [M,N,K]); the roofline is then per shape")
     args = ap.parse_args()
@@ -179,6 +242,12 @@ def main():
         step()
         print("bench: warmup step %d losses %s" % (i, list(losses)), file=sys.stderr, flush=True)
     torch.cuda.synchronize()
+    if args.copy_probe:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     lib.paragan_profile(ctx, 2 if args.detail else 1)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -211,6 +280,14 @@ def main():
         print("bench: %-62s %6d launches %9.2f ms %8.1f TFLOP/s" % (
             s["name"], s["launches"], s["total_ms"], s["flops"] / max(s["total_ms"], 1e-9) / 1e9),
             file=sys.stderr)
+    # model FLOPs of one step per image: G fwd in each D step and in the G
+    # step, G bwd (2x fwd); D fwd+bwd on 2 images per D step, D fwd + input
+    # gradient (1x fwd) in the G step
+    g, dfw, conv_g, conv_d = model_flops(args.arch)
+    per_img = (n_D + 3) * g + (6 * n_D + 2) * dfw
+    conv_per_img = (n_D + 3) * conv_g + (6 * n_D + 2) * conv_d
+    model_tf = per_img * B * args.steps / secs / 1e12
+    conv_model_tf = conv_per_img * B * args.steps / (conv_ms / 1e3) / 1e12 if conv_ms else 0.0
     out = {
         "metric": METRIC,
         "value": B * args.steps / secs,
@@ -228,10 +305,16 @@ def main():
                                "accumulation, fp32 heads" % (args.arch, B, n_D),
                    "batch": B, "n_D": n_D, "resolution": d.img},
         "roofline": {"bound": "mfma", "kernel": dom["name"], "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
-                     "launches_per_step": dom["launches"] / args.steps},
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic_of(dom["name"]),
+                     "launches_per_step": dom["launches"] / args.steps,
+                     "avg_launch_us": dom["total_ms"] / dom["launches"] * 1e3,
+                     "flops_per_launch": dom["flops"] / dom["launches"]},
         "conv_mfma": {"achieved": conv_tf, "unit": "TFLOP/s", "frac_of_peak": conv_tf / PEAK_BF16_TFLOPS,
-                      "share_of_profiled_time": conv_ms / max(all_ms, 1e-9)},
+                      "share_of_profiled_time": conv_ms / max(all_ms, 1e-9),
+                      "flops": "executed (the folded pool / upsample filters do fewer MACs than the model)"},
+        "model": {"gflop_per_image": per_img / 1e9, "step_tflops": model_tf, "step_frac_of_peak":
+                  model_tf / PEAK_BF16_TFLOPS, "conv_gflop_per_image": conv_per_img / 1e9,
+                  "conv_tflops": conv_model_tf, "conv_frac_of_peak": conv_model_tf / PEAK_BF16_TFLOPS},
     }
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle sample ...", file=sys.stderr, flush=True)
