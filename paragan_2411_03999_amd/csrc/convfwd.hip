@@ -5,9 +5,11 @@
 // GEMM: rows = output channels n (the packed weights, K contiguous), columns
 // = output pixels m (the im2col of the activation, gathered on the fly), K =
 // taps x input channels.  With the weights as the MFMA A operand each lane's
-// accumulator holds four consecutive output channels of one pixel, so the
-// epilogue (bias, ReLU mask, residual, 2x2 average pool, scale) works on
-// 4-channel vectors and stores 8 bytes (bf16) or 16 bytes (fp32) per lane.
+// accumulator holds four consecutive output channels of one pixel.  The
+// epilogue (scale, bias, ReLU mask, residual) restages each wave's results
+// through LDS so that a lane owns eight consecutive channels of one pixel and
+// consecutive lanes walk a pixel's channel run: every store is 16 (bf16) or
+// 32 (fp32) contiguous bytes and a wave writes whole cache lines.
 //
 // K loop: tap-outer, channel-inner; a thread's source offsets are computed
 // once per tap and advance by 32 channels per step.  Operand tiles move
@@ -32,7 +34,7 @@ struct CfK {
   int Hx, Wx, C;        // activation source (C = channel stride)
   int H, W, R, pad;     // conv grid
   int M, Np, ksteps;
-  FastDiv fdW, fdH, fdW2, fdH2;
+  FastDiv fdW, fdH;
   int tiles_m, tiles_n;
   ConvOut o;
 };
@@ -47,44 +49,30 @@ PG_DEV int remap_tile2(int bid, int total) {
   return bid;
 }
 
-// conv-grid position of output row m (quad-ordered rows list the four
-// pixels of each 2x2 pooling window consecutively)
-PG_DEV void pix_of(const CfK& k, int m, bool quad, int& b, int& oh, int& ow) {
-  if (!quad) {
-    const int t = (int)fdiv((uint32_t)m, k.fdW);
-    ow = m - t * k.W;
-    b = (int)fdiv((uint32_t)t, k.fdH);
-    oh = t - b * k.H;
-  } else {
-    const int qd = m & 3, p = m >> 2;
-    const int t = (int)fdiv((uint32_t)p, k.fdW2);
-    const int pw = p - t * (k.W >> 1);
-    b = (int)fdiv((uint32_t)t, k.fdH2);
-    const int ph = t - b * (k.H >> 1);
-    oh = 2 * ph + (qd >> 1);
-    ow = 2 * pw + (qd & 1);
-  }
+// conv-grid position (b, oh, ow) of output row m
+PG_DEV void pix_of(const CfK& k, int m, int& b, int& oh, int& ow) {
+  const int t = (int)fdiv((uint32_t)m, k.fdW);
+  ow = m - t * k.W;
+  b = (int)fdiv((uint32_t)t, k.fdH);
+  oh = t - b * k.H;
 }
 
-PG_DEV void load4(const void* p, bool f32, int i, float* v) {
+// eight consecutive values (16-byte aligned bf16 or 32-byte aligned fp32)
+PG_DEV void load8(const void* p, bool f32, int i, float* v) {
   if (f32) {
-    const float4 q = *reinterpret_cast<const float4*>((const float*)p + i);
-    v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    const float4 a = *reinterpret_cast<const float4*>((const float*)p + i);
+    const float4 b = *reinterpret_cast<const float4*>((const float*)p + i + 4);
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
   } else {
-    const uint2 q = *reinterpret_cast<const uint2*>((const bf16_t*)p + i);
-    v[0] = __uint_as_float(q.x << 16);
-    v[1] = __uint_as_float(q.x & 0xffff0000u);
-    v[2] = __uint_as_float(q.y << 16);
-    v[3] = __uint_as_float(q.y & 0xffff0000u);
+    const uint4 q = *reinterpret_cast<const uint4*>((const bf16_t*)p + i);
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      v[2 * t] = __uint_as_float(w[t] << 16);
+      v[2 * t + 1] = __uint_as_float(w[t] & 0xffff0000u);
+    }
   }
-}
-
-// value of lane ^ 1 / lane ^ 2 (DPP quad permutations [1,0,3,2] / [2,3,0,1])
-PG_DEV float dpp_xor1(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
-}
-PG_DEV float dpp_xor2(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
 }
 
 // swizzled element offset of (row r, 16-byte chunk c) in a tile of 32-element rows
@@ -168,8 +156,12 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   constexpr int WR = (BN + 63) / 64 * 64;      // weight rows held in LDS (whole wave loads)
   constexpr int BP = WR / 64;                  // weight wave loads per wave per step
   constexpr int NS = 3;                        // stages of the LDS ring
-  __shared__ __attribute__((aligned(16))) bf16_t Xs[NS][BM * 32];
-  __shared__ __attribute__((aligned(16))) bf16_t Ws[NS][WR * 32];
+  constexpr int RING = NS * (BM + WR) * 32;    // bf16 elements of the operand ring
+  constexpr int SROW = TN * 32 + 4;            // epilogue staging: floats per pixel row
+  constexpr int STG = 4 * 32 * SROW * 2;       // (4 waves x 32 pixels, in bf16 elements)
+  __shared__ __attribute__((aligned(16))) bf16_t lds[RING > STG ? RING : STG];
+  bf16_t(*const Xs)[BM * 32] = reinterpret_cast<bf16_t(*)[BM * 32]>(lds);
+  bf16_t(*const Ws)[WR * 32] = reinterpret_cast<bf16_t(*)[WR * 32]>(lds + NS * BM * 32);
 
   const int bid = remap_tile2(blockIdx.x, k.tiles_m * k.tiles_n);
   const int tmi = bid / k.tiles_n, tni = bid - tmi * k.tiles_n;
@@ -177,7 +169,6 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave / WM, wm = wave % WM;
-  const bool quad = k.o.pool;
   // sub-pixel parity class (a, b) of this block's output pixels
   const int par = GATHER == G_SUB ? (int)blockIdx.y : 0;
   const int pa = par >> 1, pb = par & 1;
@@ -194,7 +185,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   for (int j = 0; j < AP; ++j) {
     const int m = m0 + 16 * (4 * j + wave) + lrow;
     rv[j] = m < k.M;
-    pix_of(k, rv[j] ? m : 0, quad, rb[j], roh[j], row_[j]);
+    pix_of(k, rv[j] ? m : 0, rb[j], roh[j], row_[j]);
   }
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(k.x, k.x_bytes);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(k.w, k.w_bytes);
@@ -295,80 +286,78 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   if (ks + 2 < ksteps) tail(ks + 2, 2, 1);
   if (ks + 3 < ksteps) tail(ks + 3, 0, 2);
 
-  // ---- epilogue: lane holds channels 8g + 4h + (0..3) of pixel m.
-  // Per pixel tile: 32-bit element offsets of the output, mask and residual
-  // rows (the host guarantees they fit); per channel group: the bias.
+  // ---- epilogue, 32 pixels of a wave at a time.  The MFMA layout (lane l:
+  // channels 8 g + 4 (l / 32) + 0..3 of pixel l % 32) goes to this wave's
+  // fp32 staging rows; read back, lane l takes chunk c = 64 t + l, i.e. the
+  // eight channels 8 (c % NQ) .. + 7 of pixel c / NQ.
+  constexpr int NQ = TN * 4;                   // 8-channel chunks per pixel
   const ConvOut& o = k.o;
   const float accs = (o.acc_scale ? *o.acc_scale : 1.f) * o.acc_mul;
-  int yo[TM], mko[TM], ro[TM];
-  bool wr_ok[TM];
+  float* const stg = reinterpret_cast<float*>(lds) + wave * 32 * SROW;
+  const int nw = n0 + wn * TN * 32;
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
-    const int m = m0 + (wm * TM + j) * 32 + lr;
-    const bool mv = m < k.M;
-    int mo = quad ? (m >> 2) : m;
-    if (GATHER == G_SUB) {
-      // source-grid pixel (b, i, j) -> output pixel (b, 2i + a, 2j + b) of the 2x grid
-      int bb, ii, jj;
-      pix_of(k, mv ? m : 0, false, bb, ii, jj);
-      mo = (bb * 2 * k.H + 2 * ii + pa) * (2 * k.W) + 2 * jj + pb;
-    }
-    wr_ok[j] = mv && (!quad || (lr & 3) == 0);
-    yo[j] = mo * o.yC;
-    mko[j] = mo * o.maskC;
-    int ridx = mo;
-    if (o.res_mode == R_HALF) {
-      int bb, oh, ow;
-      pix_of(k, mv ? m : 0, false, bb, oh, ow);
-      ridx = (bb * (k.H >> 1) + (oh >> 1)) * (k.W >> 1) + (ow >> 1);
-    }
-    ro[j] = ridx * o.resC;
-  }
+    // (first pass: every wave is done with the ring; later: this wave has
+    // read back the previous pass)
+    __syncthreads();
 #pragma unroll
-  for (int i = 0; i < TN; ++i) {
+    for (int i = 0; i < TN; ++i)
 #pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const int n = n0 + (wn * TN + i) * 32 + 8 * g4 + 4 * h;
-      float bias[4];
+      for (int g4 = 0; g4 < 4; ++g4)
+        *reinterpret_cast<float4*>(stg + lr * SROW + i * 32 + 8 * g4 + 4 * h) =
+            make_float4(acc[i][j][4 * g4], acc[i][j][4 * g4 + 1], acc[i][j][4 * g4 + 2], acc[i][j][4 * g4 + 3]);
+    __syncthreads();
+    const int mb = m0 + (wm * TM + j) * 32;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) bias[e] = (o.bias && n + e < o.n_real) ? o.bias[n + e] : 0.f;
-      const bool n_ok = n < o.yC;
+    for (int t = 0; t < NQ / 2; ++t) {
+      const int c = 64 * t + lane, p = c / NQ, q = c - p * NQ;
+      const int m = mb + p, n = nw + 8 * q;
+      if (m >= k.M || n >= o.yC) continue;
+      float v[8];
+      {
+        const float4 a = *reinterpret_cast<const float4*>(stg + p * SROW + 8 * q);
+        const float4 b = *reinterpret_cast<const float4*>(stg + p * SROW + 8 * q + 4);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+      }
 #pragma unroll
-      for (int j = 0; j < TM; ++j) {
-        float v[4];
+      for (int e = 0; e < 8; ++e) v[e] = v[e] * accs + ((o.bias && n + e < o.n_real) ? o.bias[n + e] : 0.f);
+      int mo = m;
+      if (GATHER == G_SUB) {
+        // source-grid pixel (b, i, j) -> output pixel (b, 2i + a, 2j + b) of the 2x grid
+        int bb, ii, jj;
+        pix_of(k, m, bb, ii, jj);
+        mo = (bb * 2 * k.H + 2 * ii + pa) * (2 * k.W) + 2 * jj + pb;
+      }
+      if (o.mask) {
+        float mk[8];
+        load8(o.mask, o.mask_f32, mo * o.maskC + n, mk);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * g4 + e];
-        if (quad) {
-          // 2x2 average over the four consecutive rows (lanes) of a window
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float t = v[e] + dpp_xor1(v[e]);
-            v[e] = 0.25f * (t + dpp_xor2(t));
-          }
+        for (int e = 0; e < 8; ++e) v[e] = mk[e] > 0.f ? v[e] : 0.f;
+      }
+      if (o.res_mode != R_NONE) {
+        int ridx = mo;
+        if (o.res_mode == R_HALF) {
+          int bb, oh, ow;
+          pix_of(k, m, bb, oh, ow);
+          ridx = (bb * (k.H >> 1) + (oh >> 1)) * (k.W >> 1) + (ow >> 1);
         }
-        if (!(wr_ok[j] && n_ok)) continue;
+        float rv8[8];
+        load8(o.res, o.res_f32, ridx * o.resC + n, rv8);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = v[e] * accs + bias[e];
-        if (o.mask) {
-          float mk[4];
-          load4(o.mask, o.mask_f32, mko[j] + n, mk);
+        for (int e = 0; e < 8; ++e) v[e] += o.res_scale * rv8[e];
+      }
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = mk[e] > 0.f ? v[e] : 0.f;
-        }
-        if (o.res_mode != R_NONE) {
-          float rv[4];
-          load4(o.res, o.res_f32, ro[j] + n, rv);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] += o.res_scale * rv[e];
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (n + e >= o.n_real) v[e] = 0.f;
-        if (o.y_f32) {
-          *reinterpret_cast<float4*>((float*)o.y + (yo[j] + n)) = make_float4(v[0], v[1], v[2], v[3]);
-        } else {
-          *reinterpret_cast<uint2*>((bf16_t*)o.y + (yo[j] + n)) = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
-        }
+      for (int e = 0; e < 8; ++e)
+        if (n + e >= o.n_real) v[e] = 0.f;
+      const int yo = mo * o.yC + n;
+      if (o.y_f32) {
+        float* yp = (float*)o.y + yo;
+        *reinterpret_cast<float4*>(yp) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(yp + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      } else {
+        *reinterpret_cast<uint4*>((bf16_t*)o.y + yo) =
+            make_uint4(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]), f2bf2(v[4], v[5]), f2bf2(v[6], v[7]));
       }
     }
   }
@@ -403,19 +392,18 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 bool conv_fwd_mfma_ok(const ConvIn& in, int H, int W, int R, int Np, const ConvOut& o) {
   if (in.mean || in.gather == G_POOL2 || in.gscale != 1.f) return false;
   const int64_t M = (int64_t)in.B * H * W;
-  const int64_t Mo = o.pool ? M / 4 : M;
+  const int64_t Mo = M;
   const int64_t xs = (int64_t)in.B * in.Hx * in.Wx * in.C;
   const int64_t ws = (int64_t)Np * R * R * in.C;
   const int cmax = std::max({o.yC, o.resC, o.maskC});
   if (M >= (1LL << 31) || xs >= (1LL << 31) || ws >= (1LL << 31) || Mo * cmax >= (1LL << 31)) return false;
   if (2 * xs >= kBufMax || 2 * ws >= kBufMax) return false;
-  if (o.yC % 4 || (o.res_mode != R_NONE && o.resC % 4) || (o.mask && o.maskC % 4)) return false;
+  // (the epilogue moves 8-channel runs; 2x2 pooling is left to the general kernel)
+  if (o.pool || o.yC % 8 || (o.res_mode != R_NONE && o.resC % 8) || (o.mask && o.maskC % 8)) return false;
   if (!aligned16(o.y) || (o.res && !aligned16(o.res)) || (o.mask && !aligned16(o.mask))) return false;
-  if (o.pool && o.res_mode == R_HALF) return false;
-  if (o.pool && (H % 2 || W % 2)) return false;
   if (in.gather == G_S2 && (R != 4 || in.Hx != 2 * H || in.Wx != 2 * W)) return false;
   if (in.gather == G_SUB &&
-      (R != 2 || in.relu || in.Hx != H || in.Wx != W || o.pool || o.res_mode != R_NONE || 4 * Mo * cmax >= (1LL << 31)))
+      (R != 2 || in.relu || in.Hx != H || in.Wx != W || o.res_mode != R_NONE || 4 * Mo * cmax >= (1LL << 31)))
     return false;
   return true;
 }
@@ -439,8 +427,6 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   k.ksteps = R * R * (in.C / 32);
   k.fdW = make_fastdiv(W);
   k.fdH = make_fastdiv(H);
-  k.fdW2 = make_fastdiv(std::max(1, W / 2));
-  k.fdH2 = make_fastdiv(std::max(1, H / 2));
   k.o = out;
   // Tile choice (measured on the BigGAN shapes in the train step): 128 x 256
   // for multiples of 128, 96 x 256 for the other multiples of 96, and 96 x
