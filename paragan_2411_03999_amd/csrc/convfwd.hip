@@ -120,6 +120,34 @@ PG_WAIT_BARRIER(9)
 PG_WAIT_BARRIER(10)
 PG_WAIT_BARRIER(11)
 PG_WAIT_BARRIER(12)
+PG_WAIT_BARRIER(13)
+PG_WAIT_BARRIER(14)
+PG_WAIT_BARRIER(15)
+PG_WAIT_BARRIER(16)
+PG_WAIT_BARRIER(17)
+PG_WAIT_BARRIER(18)
+PG_WAIT_BARRIER(19)
+PG_WAIT_BARRIER(20)
+PG_WAIT_BARRIER(21)
+PG_WAIT_BARRIER(22)
+PG_WAIT_BARRIER(23)
+PG_WAIT_BARRIER(24)
+PG_WAIT_BARRIER(25)
+PG_WAIT_BARRIER(26)
+PG_WAIT_BARRIER(27)
+PG_WAIT_BARRIER(28)
+PG_WAIT_BARRIER(29)
+PG_WAIT_BARRIER(30)
+PG_WAIT_BARRIER(31)
+PG_WAIT_BARRIER(32)
+PG_WAIT_BARRIER(33)
+PG_WAIT_BARRIER(34)
+PG_WAIT_BARRIER(35)
+PG_WAIT_BARRIER(36)
+PG_WAIT_BARRIER(37)
+PG_WAIT_BARRIER(38)
+PG_WAIT_BARRIER(39)
+PG_WAIT_BARRIER(40)
 #undef PG_WAIT_BARRIER
 
 // One K step of a wave: operand fragments of one LDS stage through the MFMAs.
@@ -149,13 +177,27 @@ PG_DEV void conv_step(const bf16_t* xs, const bf16_t* ws, int xbase, int wbase, 
   }
 }
 
-template <int WN, int WM, int TN, int TM, int GATHER, bool RELU>
+// Runtime form of wait_barrier for the ring's drain (n = 0 .. 4 steps of
+// L loads each may stay in flight).
+template <int L>
+PG_DEV void wait_barrier_steps(int n) {
+  switch (n) {
+    case 0: wait_barrier<0>(); break;
+    case 1: wait_barrier<L>(); break;
+    case 2: wait_barrier<2 * L>(); break;
+    case 3: wait_barrier<3 * L>(); break;
+    default: wait_barrier<4 * L>(); break;
+  }
+}
+
+template <int WN, int WM, int TN, int TM, int NS, int GATHER, bool RELU>
 __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
   constexpr int AP = BM / 64;                  // activation wave loads per wave per step (16 rows each)
   constexpr int WR = (BN + 63) / 64 * 64;      // weight rows held in LDS (whole wave loads)
   constexpr int BP = WR / 64;                  // weight wave loads per wave per step
-  constexpr int NS = 3;                        // stages of the LDS ring
+  constexpr int LPS = AP + BP;                 // loads per wave per step
+  static_assert(NS >= 3 && NS <= 6, "ring depth");
   constexpr int RING = NS * (BM + WR) * 32;    // bf16 elements of the operand ring
   constexpr int SROW = TN * 32 + 4;            // epilogue staging: floats per pixel row
   constexpr int STG = 4 * 32 * SROW * 2;       // (4 waves x 32 pixels, in bf16 elements)
@@ -254,37 +296,33 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
   const int ksteps = k.ksteps;
-  issue(0);
-  if (ksteps > 1) issue(1);
-  // Step ks computes stage ks % 3 and refills stage (ks + 2) % 3, last read
-  // in step ks - 1.  Before the barrier this wave's loads of step ks have
-  // landed (those of ks + 1 may still fly) and its reads of step ks - 1 are
-  // done; past it, every wave's loads of step ks are visible and no wave
-  // still reads the stage being refilled.
-  // main loop: three steps per trip with compile-time stages (constant LDS
-  // addresses), every step refilling a stage; then at most four tail steps.
+  // Ring of NS stages: the loads of step s go to stage s % NS and are issued
+  // NS - 1 steps ahead.  Step ks first waits until its own loads have landed
+  // (those of the up to NS - 2 later steps may still fly) and this wave's
+  // reads of step ks - 1 are done, then barriers: past it every wave's loads
+  // of step ks are visible and no wave still reads stage (ks - 1) % NS, which
+  // it refills with step ks + NS - 1.
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < ksteps) issue(s);
   int ks = 0;
-  for (; ks + 4 < ksteps; ks += 3) {
-    wait_barrier<AP + BP>();
-    issue(2);
-    conv_step<TN, TM, RELU>(Xs[0], Ws[0], xbase, wbase, rd0, rd1, acc);
-    wait_barrier<AP + BP>();
-    issue(0);
-    conv_step<TN, TM, RELU>(Xs[1], Ws[1], xbase, wbase, rd0, rd1, acc);
-    wait_barrier<AP + BP>();
-    issue(1);
-    conv_step<TN, TM, RELU>(Xs[2], Ws[2], xbase, wbase, rd0, rd1, acc);
+  // steady state, NS steps per trip with compile-time stages (constant LDS
+  // addresses), every step refilling a stage
+  for (; ks + 2 * NS - 2 < ksteps; ks += NS) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      wait_barrier<(NS - 2) * LPS>();
+      issue((s + NS - 1) % NS);
+      conv_step<TN, TM, RELU>(Xs[s], Ws[s], xbase, wbase, rd0, rd1, acc);
+    }
   }
-  auto tail = [&](int s, int cur, int nxt) {
-    if (s + 1 < ksteps) wait_barrier<AP + BP>();
-    else wait_barrier<0>();
-    if (s + 2 < ksteps) issue(nxt);
-    conv_step<TN, TM, RELU>(Xs[cur], Ws[cur], xbase, wbase, rd0, rd1, acc);
-  };
-  if (ks < ksteps) tail(ks, 0, 2);
-  if (ks + 1 < ksteps) tail(ks + 1, 1, 0);
-  if (ks + 2 < ksteps) tail(ks + 2, 2, 1);
-  if (ks + 3 < ksteps) tail(ks + 3, 0, 2);
+  // drain: at most 2 NS - 2 steps, the last NS - 1 of them issuing nothing
+  for (; ks < ksteps; ++ks) {
+    const int st = ks % NS;
+    wait_barrier_steps<LPS>(min(NS - 2, ksteps - 1 - ks));
+    if (ks + NS - 1 < ksteps) issue((st + NS - 1) % NS);
+    conv_step<TN, TM, RELU>(Xs[st], Ws[st], xbase, wbase, rd0, rd1, acc);
+  }
 
   // ---- epilogue, 32 pixels of a wave at a time.  The MFMA layout (lane l:
   // channels 8 g + 4 (l / 32) + 0..3 of pixel l % 32) goes to this wave's
@@ -363,7 +401,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   }
 }
 
-template <int WN, int WM, int TN, int TM>
+template <int WN, int WM, int TN, int TM, int NS = 3>
 std::string launch_cfg(hipStream_t s, CfK& k, int gather, bool relu) {
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
   k.tiles_m = (int)cdiv(k.M, BM);
@@ -371,8 +409,8 @@ std::string launch_cfg(hipStream_t s, CfK& k, int gather, bool relu) {
   dim3 grid(k.tiles_m * k.tiles_n, gather == G_SUB ? 4 : 1), block(256);
 #define PG_CF_CASE(G, R_)                                                             \
   if (gather == G && relu == R_) {                                                    \
-    hipLaunchKernelGGL((k_conv_fwd<WN, WM, TN, TM, G, R_>), grid, block, 0, s, k);    \
-    return "k_conv_fwd<" + std::to_string(BN) + "x" + std::to_string(BM) + "," #G "," #R_ ">"; \
+    hipLaunchKernelGGL((k_conv_fwd<WN, WM, TN, TM, NS, G, R_>), grid, block, 0, s, k); \
+    return "k_conv_fwd<" + std::to_string(BN) + "x" + std::to_string(BM) + (NS == 3 ? "" : "/" + std::to_string(NS)) + "," #G "," #R_ ">"; \
   }
   PG_CF_CASE(G_DIRECT, false)
   PG_CF_CASE(G_DIRECT, true)
@@ -428,13 +466,16 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   k.fdW = make_fastdiv(W);
   k.fdH = make_fastdiv(H);
   k.o = out;
-  // Tile choice (measured on the BigGAN shapes in the train step): 128 x 256
-  // for multiples of 128, 96 x 256 for the other multiples of 96, and 96 x
-  // 128 for exactly 96 channels (except over the upsample gather).
+  // Tile choice (measured on the BigGAN shapes in the train step): the
+  // largest per-wave tile whose width divides the channel count.  128 x 256
+  // for multiples of 128 (128 x 128 for exactly 128: the 1x1 attention
+  // projections, K <= 192), 192 x 128 for multiples of 192, 96 x 256 for the
+  // other multiples of 96, 32 x 256 and 64 x 256 for narrow outputs.
+  if (Np == 128) return launch_cfg<2, 2, 2, 2>(s, k, in.gather, in.relu);
   if (Np % 128 == 0) return launch_cfg<2, 2, 2, 4>(s, k, in.gather, in.relu);
-  if (Np % 96 == 0)
-    return Np == 96 && in.gather != G_UP2 ? launch_cfg<1, 4, 3, 1>(s, k, in.gather, in.relu)
-                                          : launch_cfg<1, 4, 3, 2>(s, k, in.gather, in.relu);
+  if (Np % 192 == 0) return launch_cfg<2, 2, 3, 2>(s, k, in.gather, in.relu);
+  if (Np % 96 == 0) return launch_cfg<1, 4, 3, 2>(s, k, in.gather, in.relu);
+  if (Np <= 32) return launch_cfg<1, 4, 1, 2>(s, k, in.gather, in.relu);
   if (Np <= 64) return launch_cfg<1, 4, 2, 2>(s, k, in.gather, in.relu);
   return launch_cfg<2, 2, 2, 2>(s, k, in.gather, in.relu);
 }
