@@ -201,7 +201,8 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   constexpr int RING = NS * (BM + WR) * 32;    // bf16 elements of the operand ring
   constexpr int SROW = TN * 32 + 4;            // epilogue staging: floats per pixel row
   constexpr int STG = 4 * 32 * SROW * 2;       // (4 waves x 32 pixels, in bf16 elements)
-  __shared__ __attribute__((aligned(16))) bf16_t lds[RING > STG ? RING : STG];
+  constexpr int EPI = STG + 2 * BN;            // staging + the block's bias (fp32)
+  __shared__ __attribute__((aligned(16))) bf16_t lds[RING > EPI ? RING : EPI];
   bf16_t(*const Xs)[BM * 32] = reinterpret_cast<bf16_t(*)[BM * 32]>(lds);
   bf16_t(*const Ws)[WR * 32] = reinterpret_cast<bf16_t(*)[WR * 32]>(lds + NS * BM * 32);
 
@@ -332,12 +333,17 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   const ConvOut& o = k.o;
   const float accs = (o.acc_scale ? *o.acc_scale : 1.f) * o.acc_mul;
   float* const stg = reinterpret_cast<float*>(lds) + wave * 32 * SROW;
+  // the block's bias, past every wave's staging rows
+  float* const bsh = reinterpret_cast<float*>(lds) + 4 * 32 * SROW;
   const int nw = n0 + wn * TN * 32;
+  const float* const bw = bsh + wn * TN * 32;
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
     // (first pass: every wave is done with the ring; later: this wave has
     // read back the previous pass)
     __syncthreads();
+    if (j == 0)
+      for (int t = tid; t < BN; t += 256) bsh[t] = (o.bias && n0 + t < o.n_real) ? o.bias[n0 + t] : 0.f;
 #pragma unroll
     for (int i = 0; i < TN; ++i)
 #pragma unroll
@@ -358,8 +364,13 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
         v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
         v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
       }
+      {
+        const float4 a = *reinterpret_cast<const float4*>(bw + 8 * q);
+        const float4 b = *reinterpret_cast<const float4*>(bw + 8 * q + 4);
+        const float bv[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = v[e] * accs + ((o.bias && n + e < o.n_real) ? o.bias[n + e] : 0.f);
+        for (int e = 0; e < 8; ++e) v[e] = v[e] * accs + bv[e];
+      }
       int mo = m;
       if (GATHER == G_SUB) {
         // source-grid pixel (b, i, j) -> output pixel (b, 2i + a, 2j + b) of the 2x grid
