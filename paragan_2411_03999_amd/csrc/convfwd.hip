@@ -191,16 +191,20 @@ PG_DEV void wait_barrier_steps(int n) {
 }
 
 template <int WN, int WM, int TN, int TM, int NS, int GATHER, bool RELU>
-__global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
+__global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k) {
+  constexpr int NW = WN * WM;                  // waves per block (4 or 8)
+  constexpr int NT = NW * 64;
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
-  constexpr int AP = BM / 64;                  // activation wave loads per wave per step (16 rows each)
-  constexpr int WR = (BN + 63) / 64 * 64;      // weight rows held in LDS (whole wave loads)
-  constexpr int BP = WR / 64;                  // weight wave loads per wave per step
+  constexpr int RG = 16 * NW;                  // tile rows covered by one load of every wave
+  static_assert(BM % RG == 0, "activation rows must be whole block loads");
+  constexpr int AP = BM / RG;                  // activation wave loads per wave per step (16 rows each)
+  constexpr int WR = (BN + RG - 1) / RG * RG;  // weight rows held in LDS (whole block loads)
+  constexpr int BP = WR / RG;                  // weight wave loads per wave per step
   constexpr int LPS = AP + BP;                 // loads per wave per step
   static_assert(NS >= 3 && NS <= 6, "ring depth");
   constexpr int RING = NS * (BM + WR) * 32;    // bf16 elements of the operand ring
   constexpr int SROW = TN * 32 + 4;            // epilogue staging: floats per pixel row
-  constexpr int STG = 4 * 32 * SROW * 2;       // (4 waves x 32 pixels, in bf16 elements)
+  constexpr int STG = NW * 32 * SROW * 2;      // (NW waves x 32 pixels, in bf16 elements)
   constexpr int EPI = STG + 2 * BN;            // staging + the block's bias (fp32)
   __shared__ __attribute__((aligned(16))) bf16_t lds[RING > EPI ? RING : EPI];
   bf16_t(*const Xs)[BM * 32] = reinterpret_cast<bf16_t(*)[BM * 32]>(lds);
@@ -217,7 +221,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   const int pa = par >> 1, pb = par & 1;
   const int C = k.C, R = k.R, pad = k.pad;
 
-  // Load j of this wave covers tile rows 16 (4 j + wave) .. + 15; lane l
+  // Load j of this wave covers tile rows 16 (NW j + wave) .. + 15; lane l
   // fills row + l / 4, LDS chunk l % 4, which in the swizzled layout holds
   // source chunk (l % 4) ^ ((row / 4) % 4) = (l % 4) ^ ((l / 16) % 4).
   const int lrow = lane >> 2;
@@ -226,7 +230,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   bool rv[AP];
 #pragma unroll
   for (int j = 0; j < AP; ++j) {
-    const int m = m0 + 16 * (4 * j + wave) + lrow;
+    const int m = m0 + 16 * (NW * j + wave) + lrow;
     rv[j] = m < k.M;
     pix_of(k, rv[j] ? m : 0, rb[j], roh[j], row_[j]);
   }
@@ -251,7 +255,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   uint32_t woff[BP];
 #pragma unroll
   for (int j = 0; j < BP; ++j) {
-    const int row = 16 * (4 * j + wave) + lrow;
+    const int row = 16 * (NW * j + wave) + lrow;
     const int n = n0 + row;
     // (the sub-pixel gather keeps one filter per parity, [4][Np][2][2][C])
     woff[j] = row < BN && n < k.Np ? (uint32_t)((par * k.Np + n) * R * R * C) * 2u + 16u * lchunk : kOOB;
@@ -276,9 +280,9 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
     const uint32_t wk = __builtin_amdgcn_readfirstlane(64u * (uint32_t)ld_ks);
     const uint32_t xl = xl0 + (uint32_t)stage * (BM * 64), wl = wl0 + (uint32_t)stage * (WR * 64);
 #pragma unroll
-    for (int j = 0; j < AP; ++j) lds_load16(xl + j * 4096u, roff[j], coff, xr);
+    for (int j = 0; j < AP; ++j) lds_load16(xl + j * (NW * 1024u), roff[j], coff, xr);
 #pragma unroll
-    for (int j = 0; j < BP; ++j) lds_load16(wl + j * 4096u, woff[j], wk, wr);
+    for (int j = 0; j < BP; ++j) lds_load16(wl + j * (NW * 1024u), woff[j], wk, wr);
     advance();
   };
 
@@ -334,7 +338,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
   const float accs = (o.acc_scale ? *o.acc_scale : 1.f) * o.acc_mul;
   float* const stg = reinterpret_cast<float*>(lds) + wave * 32 * SROW;
   // the block's bias, past every wave's staging rows
-  float* const bsh = reinterpret_cast<float*>(lds) + 4 * 32 * SROW;
+  float* const bsh = reinterpret_cast<float*>(lds) + NW * 32 * SROW;
   const int nw = n0 + wn * TN * 32;
   const float* const bw = bsh + wn * TN * 32;
 #pragma unroll
@@ -343,7 +347,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
     // read back the previous pass)
     __syncthreads();
     if (j == 0)
-      for (int t = tid; t < BN; t += 256) bsh[t] = (o.bias && n0 + t < o.n_real) ? o.bias[n0 + t] : 0.f;
+      for (int t = tid; t < BN; t += NT) bsh[t] = (o.bias && n0 + t < o.n_real) ? o.bias[n0 + t] : 0.f;
 #pragma unroll
     for (int i = 0; i < TN; ++i)
 #pragma unroll
@@ -396,9 +400,11 @@ __global__ __launch_bounds__(256, 2) void k_conv_fwd(CfK k) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] += o.res_scale * rv8[e];
       }
+      if (n + 8 > o.n_real) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (n + e >= o.n_real) v[e] = 0.f;
+        for (int e = 0; e < 8; ++e)
+          if (n + e >= o.n_real) v[e] = 0.f;
+      }
       const int yo = mo * o.yC + n;
       if (o.y_f32) {
         float* yp = (float*)o.y + yo;
@@ -417,7 +423,7 @@ std::string launch_cfg(hipStream_t s, CfK& k, int gather, bool relu) {
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
   k.tiles_m = (int)cdiv(k.M, BM);
   k.tiles_n = (int)cdiv(k.Np, BN);
-  dim3 grid(k.tiles_m * k.tiles_n, gather == G_SUB ? 4 : 1), block(256);
+  dim3 grid(k.tiles_m * k.tiles_n, gather == G_SUB ? 4 : 1), block(64 * WN * WM);
 #define PG_CF_CASE(G, R_)                                                             \
   if (gather == G && relu == R_) {                                                    \
     hipLaunchKernelGGL((k_conv_fwd<WN, WM, TN, TM, NS, G, R_>), grid, block, 0, s, k); \
@@ -477,11 +483,19 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   k.fdW = make_fastdiv(W);
   k.fdH = make_fastdiv(H);
   k.o = out;
-  // Tile choice (measured on the BigGAN shapes in the train step): the
-  // largest per-wave tile whose width divides the channel count.  128 x 256
-  // for multiples of 128 (128 x 128 for exactly 128: the 1x1 attention
-  // projections, K <= 192), 192 x 128 for multiples of 192, 96 x 256 for the
-  // other multiples of 96, 32 x 256 and 64 x 256 for narrow outputs.
+  // Tile choice (measured on the BigGAN shapes in the train step).  For
+  // multiples of 256 channels an eight-wave block (one per CU) on a 256 x
+  // 256 tile halves the operand bytes per MFMA of the four-wave 128 x 256
+  // tile, and wins whenever its blocks come in whole rounds over the CUs
+  // (the last round at least three quarters full); with a ragged last round
+  // the four-wave tiles, two per CU, spread better.  Otherwise: 128 x 256
+  // for multiples of 128 (128 x 128 for exactly 128, the 1x1 attention
+  // projections with K <= 192), 192 x 128 for multiples of 192, 96 x 256
+  // for the other multiples of 96, and 32 / 64 x 256 for narrow outputs.
+  const int64_t tiles8 = cdiv(k.M, 256) * (Np / 256) * (in.gather == G_SUB ? 4 : 1);
+  const int64_t last8 = tiles8 % 256;
+  if (Np % 256 == 0 && tiles8 >= 192 && (last8 == 0 || last8 >= 192))
+    return launch_cfg<2, 4, 4, 2>(s, k, in.gather, in.relu);
   if (Np == 128) return launch_cfg<2, 2, 2, 2>(s, k, in.gather, in.relu);
   if (Np % 128 == 0) return launch_cfg<2, 2, 2, 4>(s, k, in.gather, in.relu);
   if (Np % 192 == 0) return launch_cfg<2, 2, 3, 2>(s, k, in.gather, in.relu);
