@@ -149,7 +149,7 @@ static GWsB g_carve_b(const GBlock& g, Arena& a, int n_cu) {
   // bf16: conv1's data gradient as the stride-2 4x4 filter (16 taps)
   w.wd1 = a.bytes((size_t)g.Cip * (g.f32 ? 9 : 16) * g.Cop * e);
   w.wd2 = a.bytes((size_t)g.Cop * 9 * g.Cop * e);
-  w.wdsc = a.bytes((size_t)g.Cip * g.Cop * e);
+  w.wdsc = a.bytes((size_t)g.Cip * g.Cop * e * (g.f32 ? 1 : 4));
   w.dwp1 = a.f32((size_t)g.Cop * 9 * g.Cip);
   w.dwp2 = a.f32((size_t)g.Cop * 9 * g.Cop);
   w.dwpsc = a.f32((size_t)g.Cop * g.Cip);
@@ -235,7 +235,8 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, w.wd1, cout, cin, 3, Cop, Cip,
                           f32 ? kPackDgrad : kPackDgradSum4},
                          {P.w("conv2.w"), sn[5].sigma, w.wd2, cout, cout, 3, Cop, Cop, kPackDgrad},
-                         {P.w("sc.w"), sn[6].sigma, w.wdsc, cout, cin, 1, Cop, Cip, kPackDgrad}};
+                         {P.w("sc.w"), sn[6].sigma, w.wdsc, cout, cin, 1, Cop, Cip,
+                          f32 ? kPackDgrad : kPackDgradRep4}};
   pack_group(ex.st, f32, pk, 3);
   // conv2: dW2, db2
   GradIn gdy;
@@ -250,12 +251,13 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   conv_wgrad(ex.st, f32, gdy, ax, H2, W2, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
   // both biases add to the block output: their gradients are the same column sum of dy
   PG_HIP(hipMemcpyAsync(P.gr("sc.b"), P.gr("conv2.b"), (size_t)cout * 4, hipMemcpyDeviceToDevice, ex.st));
-  // dx_skip = Wsc^T sum2x2(dy)   (low resolution, fp32)
+  // dx_skip = Wsc^T sum2x2(dy)   (low resolution, fp32); in bf16 one
+  // stride-2 2x2 conv with Wsc^T on every tap
   ConvIn dsp;
-  dsp.x = dy; dsp.B = B; dsp.Hx = H2; dsp.Wx = W2; dsp.C = Cop; dsp.gather = G_POOL2;
+  dsp.x = dy; dsp.B = B; dsp.Hx = H2; dsp.Wx = W2; dsp.C = Cop; dsp.gather = f32 ? G_POOL2 : G_S2;
   ConvOut dso;
   dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = cin;
-  conv_fwd(ex.st, f32, dsp, H, W, 1, w.wdsc, Cip, dso);
+  conv_fwd(ex.st, f32, dsp, H, W, f32 ? 1 : 2, w.wdsc, Cip, dso);
   // da2 = conv2^T dy (fp32)
   ConvIn d2;
   d2.x = dy; d2.B = B; d2.Hx = H2; d2.Wx = W2; d2.C = Cop;

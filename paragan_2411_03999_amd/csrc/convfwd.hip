@@ -456,7 +456,7 @@ bool conv_fwd_mfma_ok(const ConvIn& in, int H, int W, int R, int Np, const ConvO
   // (the epilogue moves 8-channel runs; 2x2 pooling is left to the general kernel)
   if (o.pool || o.yC % 8 || (o.res_mode != R_NONE && o.resC % 8) || (o.mask && o.maskC % 8)) return false;
   if (!aligned16(o.y) || (o.res && !aligned16(o.res)) || (o.mask && !aligned16(o.mask))) return false;
-  if (in.gather == G_S2 && (R != 4 || in.Hx != 2 * H || in.Wx != 2 * W)) return false;
+  if (in.gather == G_S2 && ((R != 4 && R != 2) || in.Hx != 2 * H || in.Wx != 2 * W)) return false;
   if (in.gather == G_SUB &&
       (R != 2 || in.relu || in.Hx != H || in.Wx != W || o.res_mode != R_NONE || 4 * Mo * cmax >= (1LL << 31)))
     return false;
@@ -476,7 +476,7 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   k.H = H;
   k.W = W;
   k.R = R;
-  k.pad = in.gather == G_S2 ? 1 : R / 2;
+  k.pad = in.gather == G_S2 ? (R - 2) / 2 : R / 2;
   k.M = (int)((int64_t)in.B * H * W);
   k.Np = Np;
   k.ksteps = R * R * (in.C / 32);

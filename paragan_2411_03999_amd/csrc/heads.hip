@@ -10,15 +10,23 @@
 namespace pg {
 
 // fp32 [N][H][W][3] images -> bf16 [N][H][W][Cp] (channels >= 3 zero)
-__global__ void k_img_to_bf16(const float* img, int64_t npix, int Cp, bf16_t* out) {
+// one thread per 16-byte chunk (8 channels) of a pixel: the first chunk
+// holds the three colours, the rest are zeros
+__global__ void k_img_to_bf16(const float* img, int64_t npix, int q, bf16_t* out) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= npix * Cp) return;
-  const int c = (int)(i % Cp);
-  const int64_t p = i / Cp;
-  out[i] = c < 3 ? f2bf(img[p * 3 + c]) : (bf16_t)0;
+  if (i >= npix * q) return;
+  const int64_t p = i / q;
+  uint4 v = make_uint4(0u, 0u, 0u, 0u);
+  if (i == p * q) {
+    v.x = f2bf2(img[p * 3], img[p * 3 + 1]);
+    v.y = f2bf2(img[p * 3 + 2], 0.f);
+  }
+  reinterpret_cast<uint4*>(out)[i] = v;
 }
 void img_to_bf16(hipStream_t st, const float* img, int64_t npix, int Cp, void* out) {
-  hipLaunchKernelGGL(k_img_to_bf16, dim3((unsigned)cdiv(npix * Cp, 256)), dim3(256), 0, st, img, npix, Cp,
+  PG_CHECK(Cp % 8 == 0 && Cp >= 8 && ((uintptr_t)out & 15) == 0, "img_to_bf16: layout");
+  const int q = Cp / 8;
+  hipLaunchKernelGGL(k_img_to_bf16, dim3((unsigned)cdiv(npix * q, 256)), dim3(256), 0, st, img, npix, q,
                      (bf16_t*)out);
   PG_LAUNCH_CHECK();
 }
@@ -60,26 +68,49 @@ __global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* __restrict__ x,
   float acc[4][3];
 #pragma unroll
   for (int o = 0; o < 4; ++o) acc[o][0] = acc[o][1] = acc[o][2] = 0.f;
+  // The haloed tile's raw 8-channel vectors of the next chunk are fetched
+  // into registers before the current chunk is computed, so their latency
+  // hides behind the FMAs; staging normalises them into LDS.
+  constexpr int kNP = ((kFR + 2) * (kFC + 2) + 255) / 256;   // tile positions per thread
+  uint4 raw[kNP];
+  uint32_t inside = 0;   // bit j: position j lies inside the image
+#pragma unroll
+  for (int j = 0; j < kNP; ++j) {
+    const int idx = t + 256 * j;
+    const int r = idx / (kFC + 2), col = idx - r * (kFC + 2);
+    const int ih = h0 + r - 1, iw = w0 + col - 1;
+    if (idx < (kFR + 2) * (kFC + 2) && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W) inside |= 1u << j;
+  }
+  auto fetch = [&](int c0) {
+#pragma unroll
+    for (int j = 0; j < kNP; ++j) {
+      const int idx = t + 256 * j;
+      const int r = idx / (kFC + 2), col = idx - r * (kFC + 2);
+      raw[j] = (inside >> j) & 1
+                   ? *reinterpret_cast<const uint4*>(x + (((int64_t)b * H + h0 + r - 1) * W + w0 + col - 1) * Cp + c0)
+                   : make_uint4(0u, 0u, 0u, 0u);
+    }
+  };
+  fetch(0);
   for (int c0 = 0; c0 < C; c0 += kFK) {
     __syncthreads();
-    for (int idx = t; idx < (kFR + 2) * (kFC + 2); idx += 256) {
+#pragma unroll
+    for (int j = 0; j < kNP; ++j) {
+      const int idx = t + 256 * j;
+      if (idx >= (kFR + 2) * (kFC + 2)) break;
       const int r = idx / (kFC + 2), col = idx - r * (kFC + 2);
-      const int ih = h0 + r - 1, iw = w0 + col - 1;
       float v[8];
+      unpack8(raw[j], v);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = 0.f;
-      if ((unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W) {
-        unpack8(*reinterpret_cast<const uint4*>(x + (((int64_t)b * H + ih) * W + iw) * Cp + c0), v);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int c = c0 + e;
-          v[e] = c < C ? fmaxf((v[e] - mean[c]) * scale[c] + shift[c], 0.f) : 0.f;
-        }
+      for (int e = 0; e < 8; ++e) {
+        const int c = c0 + e;
+        v[e] = ((inside >> j) & 1) && c < C ? fmaxf((v[e] - mean[c]) * scale[c] + shift[c], 0.f) : 0.f;
       }
 #pragma unroll
       for (int e = 0; e < 8; ++e) L[r][e][col] = v[e];
     }
     __syncthreads();
+    if (c0 + kFK < C) fetch(c0 + kFK);
     const int nk = min(kFK, C - c0);
 #pragma unroll
     for (int cc = 0; cc < kFK; ++cc) {

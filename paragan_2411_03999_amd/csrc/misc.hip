@@ -237,6 +237,7 @@ void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, f
 //           [0, a] and S(a, 1) = [1 + a, 2]
 //  subdg:   dst[p][c][du][dv][n] ([4][Cp][2][2][Np]) = the same sums of
 //           W[n][2-r][2-s][c]
+//  rep4:    dst[c][u][v][n]  ([Cp][2][2][Np]) = W[n][c] (a 1x1 filter)
 // The forward layout is a padded copy (a thread per element, both sides
 // contiguous along c); the dgrad layout transposes (n, c) per tap through
 // a 32 x 32 LDS tile so that reads run along c and writes along n.
@@ -325,7 +326,7 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
   const int rem = lb - tap * tn * tc;
   const int n0 = (rem / tc) * 32, c0 = (rem % tc) * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
-  const int DR = J.mode == kPackDgradSum4 ? 4 : (J.mode == kPackSubDgrad ? 2 : J.R);   // destination taps per row
+  const int DR = J.mode == kPackDgradSum4 ? 4 : (J.mode == kPackSubDgrad || J.mode == kPackDgradRep4 ? 2 : J.R);
   const int DRR = DR * DR;
   const int p = tap / DRR, ptap = tap - p * DRR;   // parity class (sub-pixel mode), tap within it
   const int u = ptap / DR, v = ptap - u * DR;
@@ -347,6 +348,8 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
         const int r0 = u ? 1 + a : 0, r1 = u ? 2 : a, s0 = v ? 1 + b2 : 0, s1 = v ? 2 : b2;
         for (int r = r0; r <= r1; ++r)
           for (int s_ = s0; s_ <= s1; ++s_) val += J.W[((int64_t)n * 9 + (2 - r) * 3 + (2 - s_)) * J.Cin + c];
+      } else if (J.mode == kPackDgradRep4) {
+        val = J.W[(int64_t)n * J.Cin + c];
       } else {
         const int ftap = (J.R - 1 - u) * J.R + (J.R - 1 - v);
         val = J.W[((int64_t)n * RR + ftap) * J.Cin + c];
@@ -374,11 +377,13 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
     const int RR = a.R * a.R;
     const bool four = a.mode == kPackPool4 || a.mode == kPackDgradSum4;
     const bool sub = a.mode == kPackSub || a.mode == kPackSubDgrad;
-    const int RRd = four || sub ? 16 : RR;   // taps of the packed filter (all parities)
+    const bool rep = a.mode == kPackDgradRep4;
+    const int RRd = four || sub ? 16 : (rep ? 4 : RR);   // taps of the packed filter (all parities)
     PG_CHECK(!(four || sub) || a.R == 3, "pack group: the 4x4 and sub-pixel modes pack a 3x3 filter");
+    PG_CHECK(!rep || a.R == 1, "pack group: the 2x2 replication packs a 1x1 filter");
     PG_CHECK(a.Cp % 4 == 0 && (int64_t)a.Np * RRd * a.Cp < (1LL << 31) &&
              (int64_t)a.Cout * RR * a.Cin < (1LL << 31), "pack group: shape");
-    const bool tr = a.mode == kPackDgrad || a.mode == kPackDgradSum4 || a.mode == kPackSubDgrad;
+    const bool tr = a.mode == kPackDgrad || a.mode == kPackDgradSum4 || a.mode == kPackSubDgrad || rep;
     b += tr ? (int64_t)RRd * cdiv(a.Np, 32) * cdiv(a.Cp, 32) : cdiv((int64_t)a.Np * RRd * a.Cp, 1024);
     PG_CHECK(b < (1LL << 31), "pack group: too large");
   }

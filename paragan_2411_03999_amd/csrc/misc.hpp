@@ -29,7 +29,13 @@ void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, f
 // tap 0 and [1 + a, 2] for tap 1, columns likewise);
 // kPackSubDgrad [4][Cp][2][2][Np]: the same for the flipped transposed
 // filter (the data gradient of conv3x3 through a 2x2 average pool).
-enum PackMode { kPackFwd = 0, kPackDgrad = 1, kPackPool4 = 2, kPackDgradSum4 = 3, kPackSub = 4, kPackSubDgrad = 5 };
+// kPackDgradRep4 [Cp][2][2][Np]: the transposed 1x1 filter (R = 1) on all
+// four taps of a 2x2 window: the stride-2 filter of a 1x1 data gradient
+// taken on the 2x2 sum of its input.
+enum PackMode {
+  kPackFwd = 0, kPackDgrad = 1, kPackPool4 = 2, kPackDgradSum4 = 3, kPackSub = 4, kPackSubDgrad = 5,
+  kPackDgradRep4 = 6
+};
 struct PackJob {
   const float* W;
   const float* sigma;

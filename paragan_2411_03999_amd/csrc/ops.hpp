@@ -10,7 +10,9 @@ namespace pg {
 // Operand gathers of the implicit-GEMM convolutions.  G_S2 reads the
 // source at stride 2 (a 4 x 4, pad-1 filter over a source of twice the conv
 // grid's size): a 3x3 conv followed by a 2x2 average pool, evaluated at the
-// pooled pixels only with the pre-pooled 4 x 4 weights (2.25x fewer MACs).
+// pooled pixels only with the pre-pooled 4 x 4 weights (2.25x fewer MACs);
+// with a 2 x 2, pad-0 filter it is a 1x1 conv over the 2x2 sums of the
+// source, read once without materialising the sums.
 // G_SUB evaluates a 3x3 conv over the nearest 2x upsample of the source as
 // four 2x2 convs over the source itself, one per parity class (a, b) of the
 // output pixels (2i + a, 2j + b), with the 3x3 taps that fall on the same
