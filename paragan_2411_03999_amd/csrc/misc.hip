@@ -254,8 +254,31 @@ struct PackGroupK {
 };
 
 template <typename T>
+PG_DEV void store8f(T* p, const float* v);
+template <>
+PG_DEV void store8f<bf16_t>(bf16_t* p, const float* v) {
+  *reinterpret_cast<uint4*>(p) = pack8(v);
+}
+template <>
+PG_DEV void store8f<float>(float* p, const float* v) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+template <typename T>
+PG_DEV void store4f(T* p, const float* v);
+template <>
+PG_DEV void store4f<bf16_t>(bf16_t* p, const float* v) {
+  *reinterpret_cast<uint2*>(p) = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
+}
+template <>
+PG_DEV void store4f<float>(float* p, const float* v) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+
+template <typename T>
 __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
-  __shared__ float tile[32][33];
+  __shared__ float tile[64][65];
   const int i = find_job(g.off, g.n, blockIdx.x);
   const PackJobK& J = g.j[i];
   const int lb = blockIdx.x - g.off[i];
@@ -306,62 +329,86 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     return;
   }
   if (J.mode == kPackFwd) {
-    // 32-bit indices (the host checks the sizes): four consecutive channels per thread
-    const int e = (lb * 256 + (int)threadIdx.x) * 4;
+    // 32-bit indices (the host checks the sizes): eight consecutive channels per thread
+    const int e = (lb * 256 + (int)threadIdx.x) * 8;
     if (e >= J.Np * RR * J.Cp) return;
     const int t = e / J.Cp;     // n * RR + tap
     const int c = e - t * J.Cp;
     const int n = t / RR;
     const float* src = J.W + (int64_t)t * J.Cin;
+    float v[8];
+    if (n < J.Cout && (J.Cin & 3) == 0 && c + 8 <= J.Cin) {
+      const float4 a = *reinterpret_cast<const float4*>(src + c), b = *reinterpret_cast<const float4*>(src + c + 4);
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    } else {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float v = (n < J.Cout && c + q < J.Cin) ? src[c + q] * inv : 0.f;
-      st<T>(dst, (int64_t)e + q, v);
+      for (int q = 0; q < 8; ++q) v[q] = (n < J.Cout && c + q < J.Cin) ? src[c + q] : 0.f;
     }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) v[q] *= inv;
+    store8f<T>(dst + e, v);
     return;
   }
-  // transposing modes: (n, c) tiles of 32 x 32 per destination tap through LDS
-  const int tn = (J.Np + 31) >> 5, tc = (J.Cp + 31) >> 5;
+  // transposing modes: (n, c) tiles of 64 x 64 per destination tap through
+  // LDS; a thread reads four consecutive c of four rows n and writes four
+  // consecutive n of four rows c
+  const int tn = (J.Np + 63) >> 6, tc = (J.Cp + 63) >> 6;
   const int tap = lb / (tn * tc);
   const int rem = lb - tap * tn * tc;
-  const int n0 = (rem / tc) * 32, c0 = (rem % tc) * 32;
-  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const int n0 = (rem / tc) * 64, c0 = (rem % tc) * 64;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
   const int DR = J.mode == kPackDgradSum4 ? 4 : (J.mode == kPackSubDgrad || J.mode == kPackDgradRep4 ? 2 : J.R);
   const int DRR = DR * DR;
   const int p = tap / DRR, ptap = tap - p * DRR;   // parity class (sub-pixel mode), tap within it
   const int u = ptap / DR, v = ptap - u * DR;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const int n = n0 + ty + 8 * k, c = c0 + tx;
-    float val = 0.f;
-    if (n < J.Cout && c < J.Cin) {
+    const int n = n0 + ty + 16 * k, cb = c0 + 4 * tx;
+    float val[4] = {0.f, 0.f, 0.f, 0.f};
+    if (n < J.Cout) {
       if (J.mode == kPackDgradSum4) {
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int q = 0; q < 4; ++q)
+          if (cb + q < J.Cin)
 #pragma unroll
-          for (int b2 = 0; b2 < 2; ++b2) {
-            const int r = 2 - u + a, s_ = 2 - v + b2;
-            if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) val += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + c];
-          }
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+              for (int b2 = 0; b2 < 2; ++b2) {
+                const int r = 2 - u + a, s_ = 2 - v + b2;
+                if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) val[q] += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + cb + q];
+              }
       } else if (J.mode == kPackSubDgrad) {
         const int a = p >> 1, b2 = p & 1;
         const int r0 = u ? 1 + a : 0, r1 = u ? 2 : a, s0 = v ? 1 + b2 : 0, s1 = v ? 2 : b2;
-        for (int r = r0; r <= r1; ++r)
-          for (int s_ = s0; s_ <= s1; ++s_) val += J.W[((int64_t)n * 9 + (2 - r) * 3 + (2 - s_)) * J.Cin + c];
-      } else if (J.mode == kPackDgradRep4) {
-        val = J.W[(int64_t)n * J.Cin + c];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (cb + q < J.Cin)
+            for (int r = r0; r <= r1; ++r)
+              for (int s_ = s0; s_ <= s1; ++s_) val[q] += J.W[((int64_t)n * 9 + (2 - r) * 3 + (2 - s_)) * J.Cin + cb + q];
       } else {
-        const int ftap = (J.R - 1 - u) * J.R + (J.R - 1 - v);
-        val = J.W[((int64_t)n * RR + ftap) * J.Cin + c];
+        const int ftap = J.mode == kPackDgradRep4 ? 0 : (J.R - 1 - u) * J.R + (J.R - 1 - v);
+        const float* src = J.W + ((int64_t)n * RR + ftap) * J.Cin + cb;
+        if ((J.Cin & 3) == 0 && cb + 4 <= J.Cin) {
+          const float4 f = *reinterpret_cast<const float4*>(src);
+          val[0] = f.x; val[1] = f.y; val[2] = f.z; val[3] = f.w;
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) val[q] = cb + q < J.Cin ? src[q] : 0.f;
+        }
       }
     }
-    tile[ty + 8 * k][tx] = val * inv;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) tile[ty + 16 * k][4 * tx + q] = val[q] * inv;
   }
   __syncthreads();
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
-    const int c = c0 + ty + 8 * k, n = n0 + tx;
-    if (c < J.Cp && n < J.Np) st<T>(dst, (((int64_t)p * J.Cp + c) * DRR + ptap) * J.Np + n, tile[tx][ty + 8 * k]);
+    const int c = c0 + ty + 16 * k, nb = n0 + 4 * tx;
+    if (c < J.Cp && nb < J.Np) {
+      const float w4[4] = {tile[4 * tx][ty + 16 * k], tile[4 * tx + 1][ty + 16 * k], tile[4 * tx + 2][ty + 16 * k],
+                           tile[4 * tx + 3][ty + 16 * k]};
+      store4f<T>(dst + (((int64_t)p * J.Cp + c) * DRR + ptap) * J.Np + nb, w4);
+    }
   }
 }
 
@@ -384,7 +431,10 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
     PG_CHECK(a.Cp % 4 == 0 && (int64_t)a.Np * RRd * a.Cp < (1LL << 31) &&
              (int64_t)a.Cout * RR * a.Cin < (1LL << 31), "pack group: shape");
     const bool tr = a.mode == kPackDgrad || a.mode == kPackDgradSum4 || a.mode == kPackSubDgrad || rep;
-    b += tr ? (int64_t)RRd * cdiv(a.Np, 32) * cdiv(a.Cp, 32) : cdiv((int64_t)a.Np * RRd * a.Cp, 1024);
+    PG_CHECK(!tr || a.Np % 4 == 0, "pack group: transposed rows of 4");
+    PG_CHECK(tr || a.Cp % 8 == 0, "pack group: rows of 8");
+    b += tr ? (int64_t)RRd * cdiv(a.Np, 64) * cdiv(a.Cp, 64)
+            : (a.mode == kPackFwd ? cdiv((int64_t)a.Np * RRd * a.Cp, 2048) : cdiv((int64_t)a.Np * RRd * a.Cp, 1024));
     PG_CHECK(b < (1LL << 31), "pack group: too large");
   }
   g.off[n] = (int)b;
@@ -603,13 +653,9 @@ __global__ __launch_bounds__(256) void k_colred(const T* x, int64_t M, int C, in
   for (int e = 0; e < 8; ++e) sft[e] = s1[e] = s2[e] = 0.f;
   int n = 0;
   if (ro < sh.P) {
-    for (int64_t r = r0 + ro; r < r1; r += sh.P) {
-      float v[8];
-      load8f<T>(x + r * ldc + cc * 8, v);
-      if (STATS && n == 0) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sft[e] = v[e];
-      }
+    int64_t r = r0 + ro;
+    if (STATS && r < r1) load8f<T>(x + r * ldc + cc * 8, sft);
+    auto add = [&](const float* v) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float d = v[e] - sft[e];
@@ -617,6 +663,19 @@ __global__ __launch_bounds__(256) void k_colred(const T* x, int64_t M, int C, in
         if (STATS) s2[e] = fmaf(d, d, s2[e]);
       }
       ++n;
+    };
+    // four rows in flight per thread, accumulated in row order
+    for (; r + 3 * sh.P < r1; r += 4 * sh.P) {
+      float v[4][8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) load8f<T>(x + (r + u * sh.P) * ldc + cc * 8, v[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add(v[u]);
+    }
+    for (; r < r1; r += sh.P) {
+      float v[8];
+      load8f<T>(x + r * ldc + cc * 8, v);
+      add(v);
     }
   }
 #pragma unroll
@@ -738,18 +797,6 @@ void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc
 // activation type: the BN(+ReLU) operand of the next convolution, computed
 // once per element instead of once per filter tap.  Padded channels get 0.
 // One thread per (pixel, 8 channels): 16-byte loads and stores.
-template <typename T>
-PG_DEV void store8f(T* p, const float* v);
-template <>
-PG_DEV void store8f<bf16_t>(bf16_t* p, const float* v) {
-  *reinterpret_cast<uint4*>(p) = pack8(v);
-}
-template <>
-PG_DEV void store8f<float>(float* p, const float* v) {
-  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
-}
-
 template <typename T>
 __global__ __launch_bounds__(256) void k_bn_apply(const T* x, int64_t n8, int CC, FastDiv fdCC, FastDiv fdHW,
                                                   int C, const float* mean, const float* scale,
@@ -1001,11 +1048,7 @@ __global__ __launch_bounds__(256) void k_bnb_reduce(const float* g, int g_up2, c
     load8f<float>(rstd + c0, rs);
     load8f<float>(gain + (int64_t)b * tab_stride + c0, ga);
     load8f<float>(bias + (int64_t)b * tab_stride + c0, be);
-    for (int r = r0 + ph; r < r1; r += sh.P) {
-      const int64_t m = (int64_t)b * HW + r;
-      float xv[8], gv[8];
-      load8f<T>(x + m * Cp + c0, xv);
-      load_g8(g, g_up2, m, b, r, fdW, H, W, Cp, c0, gv);
+    auto add = [&](const float* xv, const float* gv) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float xh = (xv[e] - mu[e]) * rs[e];
@@ -1013,6 +1056,27 @@ __global__ __launch_bounds__(256) void k_bnb_reduce(const float* g, int g_up2, c
         s1[e] += dz;
         s2[e] = fmaf(dz, xh, s2[e]);
       }
+    };
+    int r = r0 + ph;
+    // four rows in flight per thread, accumulated in row order
+    for (; r + 3 * sh.P < r1; r += 4 * sh.P) {
+      float xv[4][8], gv[4][8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int ru = r + u * sh.P;
+        const int64_t m = (int64_t)b * HW + ru;
+        load8f<T>(x + m * Cp + c0, xv[u]);
+        load_g8(g, g_up2, m, b, ru, fdW, H, W, Cp, c0, gv[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) add(xv[u], gv[u]);
+    }
+    for (; r < r1; r += sh.P) {
+      const int64_t m = (int64_t)b * HW + r;
+      float xv[8], gv[8];
+      load8f<T>(x + m * Cp + c0, xv);
+      load_g8(g, g_up2, m, b, r, fdW, H, W, Cp, c0, gv);
+      add(xv, gv);
     }
   }
 #pragma unroll
