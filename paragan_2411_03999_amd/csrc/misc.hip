@@ -708,18 +708,20 @@ __global__ __launch_bounds__(256) void k_colred(const T* x, int64_t M, int C, in
   }
 }
 
+// fixed-order sum of the chunk partials: 16 channels per block, 64 lane
+// groups summing every 64th chunk, then the 64 group sums in order
 __global__ __launch_bounds__(1024) void k_colsum_fin(const float* part, int nch, int C, float scale, float* out) {
-  __shared__ float sh[16][64];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + lane;
+  __shared__ float sp[64][16];
+  const int cl = threadIdx.x & 15, grp = threadIdx.x >> 4;
+  const int c = blockIdx.x * 16 + cl;
   float s = 0.f;
   if (c < C)
-    for (int j = wv; j < nch; j += 16) s += part[(int64_t)j * C + c];
-  sh[wv][lane] = s;
+    for (int j = grp; j < nch; j += 64) s += part[(int64_t)j * C + c];
+  sp[grp][cl] = s;
   __syncthreads();
-  if (wv == 0 && c < C) {
+  if (grp == 0 && c < C) {
     float t = 0.f;
-    for (int i = 0; i < 16; ++i) t += sh[i][lane];
+    for (int i = 0; i < 64; ++i) t += sp[i][cl];
     out[c] = t * scale;
   }
 }
@@ -744,29 +746,50 @@ void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, 
   else
     hipLaunchKernelGGL((k_colred<bf16_t, false>), dim3(nch), dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, sh,
                        part, nullptr);
-  hipLaunchKernelGGL(k_colsum_fin, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, part, nch, C, scale, out);
+  hipLaunchKernelGGL(k_colsum_fin, dim3((unsigned)cdiv(C, 16)), dim3(1024), 0, st, part, nch, C, scale, out);
   PG_LAUNCH_CHECK();
 }
 
 // ------------------------------------------------------- batch norm
+// Merge of the chunk statistics, per channel c: with n_j rows, mean m_j and
+// M2_j per chunk, mean = sum n_j m_j / M and M2 = sum (M2_j + n_j (m_j -
+// mean)^2) -- two passes in fp64, no division per chunk.  A block takes 16
+// channels; its 64 lane groups (lane / 16 + 4 wave) sum every 64th chunk,
+// and the 64 group sums combine in group order.
 __global__ __launch_bounds__(1024) void k_bn_fin(const float* pmean, const float* pm2, int nch, int rows_blk,
                                                  int64_t M, int C, float eps, float* mean, float* rstd) {
-  __shared__ double sn[16][64], smu[16][64], sm2[16][64];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int c = blockIdx.x * 64 + lane;
-  double n = 0.0, mu = 0.0, m2 = 0.0;
-  if (c < C)
-    for (int j = wv; j < nch; j += 16) {
-      const double nb = (double)std::min<int64_t>(rows_blk, M - (int64_t)j * rows_blk);
-      chan_merge(n, mu, m2, nb, pmean[(int64_t)j * C + c], pm2[(int64_t)j * C + c]);
-    }
-  sn[wv][lane] = n; smu[wv][lane] = mu; sm2[wv][lane] = m2;
+  __shared__ double sp[64][16];
+  __shared__ double smu[16];
+  const int cl = threadIdx.x & 15, grp = threadIdx.x >> 4;
+  const int c = blockIdx.x * 16 + cl;
+  const bool on = c < C;
+  auto nrows = [&](int j) { return (double)std::min<int64_t>(rows_blk, M - (int64_t)j * rows_blk); };
+  double s = 0.0;
+  if (on)
+    for (int j = grp; j < nch; j += 64) s += nrows(j) * (double)pmean[(int64_t)j * C + c];
+  sp[grp][cl] = s;
   __syncthreads();
-  if (wv == 0 && c < C) {
-    double tn = 0.0, tmu = 0.0, tm2 = 0.0;
-    for (int i = 0; i < 16; ++i) chan_merge(tn, tmu, tm2, sn[i][lane], smu[i][lane], sm2[i][lane]);
-    mean[c] = (float)tmu;
-    rstd[c] = (float)(1.0 / sqrt(tm2 / tn + (double)eps));
+  if (grp == 0) {
+    double t = 0.0;
+    for (int i = 0; i < 64; ++i) t += sp[i][cl];
+    smu[cl] = t / (double)M;
+  }
+  __syncthreads();
+  const double mu = smu[cl];
+  double q = 0.0;
+  if (on)
+    for (int j = grp; j < nch; j += 64) {
+      const double d = (double)pmean[(int64_t)j * C + c] - mu;
+      q += (double)pm2[(int64_t)j * C + c] + nrows(j) * d * d;
+    }
+  __syncthreads();
+  sp[grp][cl] = q;
+  __syncthreads();
+  if (grp == 0 && on) {
+    double t = 0.0;
+    for (int i = 0; i < 64; ++i) t += sp[i][cl];
+    mean[c] = (float)mu;
+    rstd[c] = (float)(1.0 / sqrt(t / (double)M + (double)eps));
   }
 }
 
@@ -788,7 +811,7 @@ void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc
   else
     hipLaunchKernelGGL((k_colred<bf16_t, true>), dim3(nch), dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, sh,
                        pmean, pm2);
-  hipLaunchKernelGGL(k_bn_fin, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, pmean, pm2, nch, sh.rows_blk, M, C,
+  hipLaunchKernelGGL(k_bn_fin, dim3((unsigned)cdiv(C, 16)), dim3(1024), 0, st, pmean, pm2, nch, sh.rows_blk, M, C,
                      eps, mean, rstd);
   PG_LAUNCH_CHECK();
 }
@@ -953,19 +976,51 @@ static void gemm_small(hipStream_t st, int M, int N, int K, const float* A, int6
                      Cm, ldc, div, (int)acc);
 }
 
-// gain = 1 + gain_raw, scale = gain * rstd; padded channels -> 0
-__global__ void k_cbn_fix(int B, int C, int Cp, const float* rstd, float* gain, float* bias, float* scale) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= B * Cp) return;
-  const int c = i % Cp;
-  if (c < C) {
-    const float g = 1.f + gain[i];
-    gain[i] = g;
-    scale[i] = g * rstd[c];
-  } else {
-    gain[i] = 0.f;
-    bias[i] = 0.f;
-    scale[i] = 0.f;
+// Both conditional-BN linear maps of one BN in one launch (blockIdx.z: 0
+// gain, 1 bias), written as the tables the conv prologue and BN backward use:
+//   gain[b][c] = 1 + cond[b] . Wg[c] / sigma_g,  scale = gain * rstd[c],
+//   bias[b][c] = cond[b] . Wb[c] / sigma_b,  zeros for c >= C (up to Cp).
+// Same 32 x 32 tiling and summation order as k_gemm_small.
+__global__ __launch_bounds__(256) void k_cbn_lin(int B, int C, int Cp, int dc, const float* cond, const float* Wg,
+                                                 const float* Wb, const float* sg, const float* sb,
+                                                 const float* rstd, float* gain, float* bias, float* scale) {
+  __shared__ float As[32][33], Bs[32][33];
+  const bool isg = blockIdx.z == 0;
+  const float* Wm = isg ? Wg : Wb;
+  const int i0 = blockIdx.y * 32, j0 = blockIdx.x * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  float c[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < dc; k0 += 32) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = ty + 8 * q;
+      As[r][tx] = (i0 + r < B && k0 + tx < dc) ? cond[(int64_t)(i0 + r) * dc + k0 + tx] : 0.f;
+      Bs[tx][r] = (k0 + tx < dc && j0 + r < C) ? Wm[(int64_t)(j0 + r) * dc + k0 + tx] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int kk = 0; kk < 32; ++kk) {
+      const float b = Bs[kk][tx];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) c[q] = fmaf(As[ty + 8 * q][kk], b, c[q]);
+    }
+    __syncthreads();
+  }
+  const int j = j0 + tx;
+  if (j >= Cp) return;
+  const float sig = *(isg ? sg : sb);
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = i0 + ty + 8 * q;
+    if (i >= B) continue;
+    const int64_t o = (int64_t)i * Cp + j;
+    if (isg) {
+      const float g = j < C ? 1.f + c[q] / sig : 0.f;
+      gain[o] = g;
+      scale[o] = j < C ? g * rstd[j] : 0.f;
+    } else {
+      bias[o] = j < C ? c[q] / sig : 0.f;
+    }
   }
 }
 
@@ -974,10 +1029,8 @@ void cbn_tables(hipStream_t st, const float* cond, int dc, const float* Wg, cons
                 const float* rstd, int B, int C, int Cp, float* gain, float* bias, float* scale) {
   if (cond) {
     // gain_raw[b][c] = cond[b] . Wg[c] / sigma_g, bias[b][c] = cond[b] . Wb[c] / sigma_b
-    gemm_small(st, B, C, dc, cond, dc, 1, Wg, 1, dc, gain, Cp, sg, false);
-    gemm_small(st, B, C, dc, cond, dc, 1, Wb, 1, dc, bias, Cp, sb, false);
-    hipLaunchKernelGGL(k_cbn_fix, dim3((unsigned)cdiv((int64_t)B * Cp, 256)), dim3(256), 0, st, B, C, Cp, rstd,
-                       gain, bias, scale);
+    hipLaunchKernelGGL(k_cbn_lin, dim3((unsigned)cdiv(Cp, 32), (unsigned)cdiv(B, 32), 2), dim3(256), 0, st, B, C, Cp,
+                       dc, cond, Wg, Wb, sg, sb, rstd, gain, bias, scale);
     PG_LAUNCH_CHECK();
     return;
   }
