@@ -79,23 +79,24 @@ PG_DEV void load8(const void* p, bool f32, int i, float* v) {
 // swizzled element offset of (row r, 16-byte chunk c) in a tile of 32-element rows
 PG_DEV int sw_off(int r, int c) { return r * 32 + 8 * (c ^ ((r >> 2) & 3)); }
 
-// One K step of a wave: operand fragments of one LDS stage through the MFMAs.
-template <int TN, int TM, bool RELU>
-PG_DEV void conv_step(const bf16_t* xs, const bf16_t* ws, int xbase, int wbase, int rd0, int rd1,
+// One K step of a wave (KS channels): operand fragments of one LDS stage
+// through the MFMAs, KS / 16 of them per output tile.
+template <int TN, int TM, bool RELU, int KS>
+PG_DEV void conv_step(const bf16_t* xs, const bf16_t* ws, int xbase, int wbase, const int (&rdo)[KS / 16],
                       f32x16 (&acc)[TN][TM]) {
 #pragma unroll
-  for (int kk = 0; kk < 2; ++kk) {
-    const int rd = kk ? rd1 : rd0;
+  for (int kk = 0; kk < KS / 16; ++kk) {
+    const int rd = rdo[kk];
     bf16x8 wv[TN], xv[TM];
 #pragma unroll
-    for (int i = 0; i < TN; ++i) wv[i] = *reinterpret_cast<const bf16x8*>(ws + wbase + i * 32 * 32 + rd);
+    for (int i = 0; i < TN; ++i) wv[i] = *reinterpret_cast<const bf16x8*>(ws + wbase + i * 32 * KS + rd);
 #pragma unroll
     for (int j = 0; j < TM; ++j) {
       if (RELU) {
-        const uint4 q = relu8_bits(*reinterpret_cast<const uint4*>(xs + xbase + j * 32 * 32 + rd));
+        const uint4 q = relu8_bits(*reinterpret_cast<const uint4*>(xs + xbase + j * 32 * KS + rd));
         xv[j] = __builtin_bit_cast(bf16x8, q);
       } else {
-        xv[j] = *reinterpret_cast<const bf16x8*>(xs + xbase + j * 32 * 32 + rd);
+        xv[j] = *reinterpret_cast<const bf16x8*>(xs + xbase + j * 32 * KS + rd);
       }
     }
 #pragma unroll
@@ -106,25 +107,28 @@ PG_DEV void conv_step(const bf16_t* xs, const bf16_t* ws, int xbase, int wbase, 
   }
 }
 
-template <int WN, int WM, int TN, int TM, int NS, int GATHER, bool RELU>
+template <int WN, int WM, int TN, int TM, int NS, int KS, int GATHER, bool RELU>
 __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k) {
   constexpr int NW = WN * WM;                  // waves per block (4 or 8)
   constexpr int NT = NW * 64;
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
-  constexpr int RG = 16 * NW;                  // tile rows covered by one load of every wave
+  static_assert(KS == 32 || KS == 64, "channels per step");
+  constexpr int CH = KS / 8;                   // 16-byte chunks per LDS row
+  constexpr int RPL = 64 / CH;                 // rows filled by one wave load (1 KB)
+  constexpr int RG = RPL * NW;                 // tile rows covered by one load of every wave
   static_assert(BM % RG == 0, "activation rows must be whole block loads");
-  constexpr int AP = BM / RG;                  // activation wave loads per wave per step (16 rows each)
+  constexpr int AP = BM / RG;                  // activation wave loads per wave per step
   constexpr int WR = (BN + RG - 1) / RG * RG;  // weight rows held in LDS (whole block loads)
   constexpr int BP = WR / RG;                  // weight wave loads per wave per step
   constexpr int LPS = AP + BP;                 // loads per wave per step
-  static_assert(NS >= 3 && NS <= 6, "ring depth");
-  constexpr int RING = NS * (BM + WR) * 32;    // bf16 elements of the operand ring
+  static_assert(NS >= 2 && NS <= 6, "ring depth");
+  constexpr int RING = NS * (BM + WR) * KS;    // bf16 elements of the operand ring
   constexpr int SROW = TN * 32 + 4;            // epilogue staging: floats per pixel row
   constexpr int STG = NW * 32 * SROW * 2;      // (NW waves x 32 pixels, in bf16 elements)
   constexpr int EPI = STG + 2 * BN;            // staging + the block's bias (fp32)
   __shared__ __attribute__((aligned(16))) bf16_t lds[RING > EPI ? RING : EPI];
-  bf16_t(*const Xs)[BM * 32] = reinterpret_cast<bf16_t(*)[BM * 32]>(lds);
-  bf16_t(*const Ws)[WR * 32] = reinterpret_cast<bf16_t(*)[WR * 32]>(lds + NS * BM * 32);
+  bf16_t(*const Xs)[BM * KS] = reinterpret_cast<bf16_t(*)[BM * KS]>(lds);
+  bf16_t(*const Ws)[WR * KS] = reinterpret_cast<bf16_t(*)[WR * KS]>(lds + NS * BM * KS);
 
   const int bid = remap_tile2(blockIdx.x, k.tiles_m * k.tiles_n);
   const int tmi = bid / k.tiles_n, tni = bid - tmi * k.tiles_n;
@@ -137,16 +141,21 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
   const int pa = par >> 1, pb = par & 1;
   const int C = k.C, R = k.R, pad = k.pad;
 
-  // Load j of this wave covers tile rows 16 (NW j + wave) .. + 15; lane l
-  // fills row + l / 4, LDS chunk l % 4, which in the swizzled layout holds
-  // source chunk (l % 4) ^ ((row / 4) % 4) = (l % 4) ^ ((l / 16) % 4).
-  const int lrow = lane >> 2;
-  const uint32_t lchunk = (uint32_t)((lane & 3) ^ ((lane >> 4) & 3));
+  // Load j of this wave covers tile rows RPL (NW j + wave) .. + RPL - 1;
+  // lane l fills row + l / CH, LDS chunk l % CH, which in the swizzled
+  // layout holds source chunk (l % CH) ^ swz(row): rows of 64 bytes swizzle
+  // by (row / 4) % 4, rows of 128 bytes by (row / 2) % 8 (bits of the row
+  // that a load's base, a multiple of RPL, leaves alone apart from bit 3,
+  // whose value -- the parity of NW j + wave -- is that of wave).
+  const int lrow = lane / CH;
+  const int lrow_all = RPL * wave + lrow;      // row of load 0 (same swizzle for every load)
+  const uint32_t lchunk =
+      (uint32_t)((lane % CH) ^ (KS == 32 ? ((lrow_all >> 2) & 3) : ((lrow_all >> 1) & 7)));
   int rb[AP], roh[AP], row_[AP];
   bool rv[AP];
 #pragma unroll
   for (int j = 0; j < AP; ++j) {
-    const int m = m0 + 16 * (NW * j + wave) + lrow;
+    const int m = m0 + RPL * (NW * j + wave) + lrow;
     rv[j] = m < k.M;
     pix_of(k, rv[j] ? m : 0, rb[j], roh[j], row_[j]);
   }
@@ -171,7 +180,7 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
   uint32_t woff[BP];
 #pragma unroll
   for (int j = 0; j < BP; ++j) {
-    const int row = 16 * (NW * j + wave) + lrow;
+    const int row = RPL * (NW * j + wave) + lrow;
     const int n = n0 + row;
     // (the sub-pixel gather keeps one filter per parity, [4][Np][2][2][C])
     woff[j] = row < BN && n < k.Np ? (uint32_t)((par * k.Np + n) * R * R * C) * 2u + 16u * lchunk : kOOB;
@@ -182,7 +191,7 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
   set_tap(0);
   auto advance = [&]() {
     ++ld_ks;
-    ld_c0 += 32;
+    ld_c0 += KS;
     if (ld_c0 == C) {
       ld_c0 = 0;
       ++ld_tap;
@@ -190,11 +199,11 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
     }
   };
   // LDS bases of this wave's loads in stage 0 (stage s adds s * stage size)
-  const uint32_t xl0 = lds_addr(&Xs[0][16 * wave * 32]), wl0 = lds_addr(&Ws[0][16 * wave * 32]);
+  const uint32_t xl0 = lds_addr(&Xs[0][RPL * wave * KS]), wl0 = lds_addr(&Ws[0][RPL * wave * KS]);
   auto issue = [&](int stage) {
     const uint32_t coff = __builtin_amdgcn_readfirstlane(2u * (uint32_t)ld_c0);
-    const uint32_t wk = __builtin_amdgcn_readfirstlane(64u * (uint32_t)ld_ks);
-    const uint32_t xl = xl0 + (uint32_t)stage * (BM * 64), wl = wl0 + (uint32_t)stage * (WR * 64);
+    const uint32_t wk = __builtin_amdgcn_readfirstlane(2u * KS * (uint32_t)ld_ks);
+    const uint32_t xl = xl0 + (uint32_t)stage * (BM * KS * 2), wl = wl0 + (uint32_t)stage * (WR * KS * 2);
 #pragma unroll
     for (int j = 0; j < AP; ++j) lds_load16(xl + j * (NW * 1024u), roff[j], coff, xr);
 #pragma unroll
@@ -203,10 +212,12 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
   };
 
   // operand read offsets: row (tile base + lane%32), chunk 2*kk + lane/32
-  const int lr = lane & 31, f = (lr >> 2) & 3, h = lane >> 5;
-  const int rd0 = lr * 32 + 8 * ((0 + h) ^ f);
-  const int rd1 = lr * 32 + 8 * ((2 + h) ^ f);
-  const int xbase = wm * TM * 32 * 32, wbase = wn * TN * 32 * 32;
+  const int lr = lane & 31, h = lane >> 5;
+  const int f = KS == 32 ? ((lr >> 2) & 3) : ((lr >> 1) & 7);
+  int rdo[KS / 16];
+#pragma unroll
+  for (int kk = 0; kk < KS / 16; ++kk) rdo[kk] = lr * KS + 8 * ((2 * kk + h) ^ f);
+  const int xbase = wm * TM * 32 * KS, wbase = wn * TN * 32 * KS;
 
   f32x16 acc[TN][TM];
 #pragma unroll
@@ -232,9 +243,9 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
   for (; ks + 2 * NS - 2 < ksteps; ks += NS) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      wait_barrier<(NS - 2) * LPS>();
+      wait_barrier<vm_cap((NS - 2) * LPS)>();
       issue((s + NS - 1) % NS);
-      conv_step<TN, TM, RELU>(Xs[s], Ws[s], xbase, wbase, rd0, rd1, acc);
+      conv_step<TN, TM, RELU, KS>(Xs[s], Ws[s], xbase, wbase, rdo, acc);
     }
   }
   // drain: at most 2 NS - 2 steps, the last NS - 1 of them issuing nothing
@@ -242,7 +253,7 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
     const int st = ks % NS;
     wait_barrier_steps<LPS>(min(NS - 2, ksteps - 1 - ks));
     if (ks + NS - 1 < ksteps) issue((st + NS - 1) % NS);
-    conv_step<TN, TM, RELU>(Xs[st], Ws[st], xbase, wbase, rd0, rd1, acc);
+    conv_step<TN, TM, RELU, KS>(Xs[st], Ws[st], xbase, wbase, rdo, acc);
   }
 
   // ---- epilogue, 32 pixels of a wave at a time.  The MFMA layout (lane l:
@@ -334,16 +345,19 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
   }
 }
 
-template <int WN, int WM, int TN, int TM, int NS = 3>
+template <int WN, int WM, int TN, int TM, int NS = 3, int KS = 32>
 std::string launch_cfg(hipStream_t s, CfK& k, int gather, bool relu) {
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
+  if (k.C % KS) throw Error{-2, "conv_fwd: channels per step"};
+  k.ksteps = k.R * k.R * (k.C / KS);
   k.tiles_m = (int)cdiv(k.M, BM);
   k.tiles_n = (int)cdiv(k.Np, BN);
   dim3 grid(k.tiles_m * k.tiles_n, gather == G_SUB ? 4 : 1), block(64 * WN * WM);
 #define PG_CF_CASE(G, R_)                                                             \
   if (gather == G && relu == R_) {                                                    \
-    hipLaunchKernelGGL((k_conv_fwd<WN, WM, TN, TM, NS, G, R_>), grid, block, 0, s, k); \
-    return "k_conv_fwd<" + std::to_string(BN) + "x" + std::to_string(BM) + (NS == 3 ? "" : "/" + std::to_string(NS)) + "," #G "," #R_ ">"; \
+    hipLaunchKernelGGL((k_conv_fwd<WN, WM, TN, TM, NS, KS, G, R_>), grid, block, 0, s, k); \
+    return "k_conv_fwd<" + std::to_string(BN) + "x" + std::to_string(BM) + (KS == 32 ? "" : "k" + std::to_string(KS)) + \
+           (NS == 3 ? "" : "/" + std::to_string(NS)) + "," #G "," #R_ ">"; \
   }
   PG_CF_CASE(G_DIRECT, false)
   PG_CF_CASE(G_DIRECT, true)

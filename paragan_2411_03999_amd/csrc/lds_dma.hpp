@@ -74,18 +74,43 @@ PG_WAIT_BARRIER(37)
 PG_WAIT_BARRIER(38)
 PG_WAIT_BARRIER(39)
 PG_WAIT_BARRIER(40)
+PG_WAIT_BARRIER(41)
+PG_WAIT_BARRIER(42)
+PG_WAIT_BARRIER(43)
+PG_WAIT_BARRIER(44)
+PG_WAIT_BARRIER(45)
+PG_WAIT_BARRIER(46)
+PG_WAIT_BARRIER(47)
+PG_WAIT_BARRIER(48)
+PG_WAIT_BARRIER(49)
+PG_WAIT_BARRIER(50)
+PG_WAIT_BARRIER(51)
+PG_WAIT_BARRIER(52)
+PG_WAIT_BARRIER(53)
+PG_WAIT_BARRIER(54)
+PG_WAIT_BARRIER(55)
+PG_WAIT_BARRIER(56)
+PG_WAIT_BARRIER(57)
+PG_WAIT_BARRIER(58)
+PG_WAIT_BARRIER(59)
+PG_WAIT_BARRIER(60)
+PG_WAIT_BARRIER(61)
+PG_WAIT_BARRIER(62)
+PG_WAIT_BARRIER(63)
 #undef PG_WAIT_BARRIER
 
 // Runtime form of wait_barrier for the ring's drain (n = 0 .. 4 steps of
-// L loads each may stay in flight).
+// L loads each may stay in flight; the counter's limit of 63 only makes the
+// wait stricter).
+constexpr int vm_cap(int n) { return n < 63 ? n : 63; }
 template <int L>
 PG_DEV void wait_barrier_steps(int n) {
   switch (n) {
     case 0: wait_barrier<0>(); break;
-    case 1: wait_barrier<L>(); break;
-    case 2: wait_barrier<2 * L>(); break;
-    case 3: wait_barrier<3 * L>(); break;
-    default: wait_barrier<4 * L>(); break;
+    case 1: wait_barrier<vm_cap(L)>(); break;
+    case 2: wait_barrier<vm_cap(2 * L)>(); break;
+    case 3: wait_barrier<vm_cap(3 * L)>(); break;
+    default: wait_barrier<vm_cap(4 * L)>(); break;
   }
 }
 
