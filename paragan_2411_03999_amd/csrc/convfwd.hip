@@ -107,6 +107,104 @@ PG_DEV void conv_step(const bf16_t* xs, const bf16_t* ws, int xbase, int wbase, 
   }
 }
 
+// Epilogue of the conv kernels, 32 pixels of a wave at a time.  The MFMA
+// layout (lane l: channels 8 g + 4 (l / 32) + 0..3 of pixel l % 32) goes to
+// this wave's fp32 staging rows in LDS; read back, lane l takes chunk c =
+// 64 t + l, i.e. the eight channels 8 (c % NQ) .. + 7 of pixel c / NQ.
+// Rows are the block's BM = WM TM 32 consecutive output pixels from m0; the
+// caller has no LDS reads of its operands left in flight past the first
+// barrier here.
+template <int WN, int WM, int TN, int TM, int GATHER>
+PG_DEV void conv_epilogue(const CfK& k, f32x16 (&acc)[TN][TM], bf16_t* lds, int m0, int n0, int wn, int wm,
+                          int wave, int lane, int pa, int pb) {
+  constexpr int NW = WN * WM, NT = NW * 64, BN = WN * TN * 32;
+  constexpr int SROW = TN * 32 + 4;            // staging floats per pixel row
+  const int tid = wave * 64 + lane, lr = lane & 31, h = lane >> 5;
+  constexpr int NQ = TN * 4;                   // 8-channel chunks per pixel
+  const ConvOut& o = k.o;
+  const float accs = (o.acc_scale ? *o.acc_scale : 1.f) * o.acc_mul;
+  float* const stg = reinterpret_cast<float*>(lds) + wave * 32 * SROW;
+  // the block's bias, past every wave's staging rows
+  float* const bsh = reinterpret_cast<float*>(lds) + NW * 32 * SROW;
+  const int nw = n0 + wn * TN * 32;
+  const float* const bw = bsh + wn * TN * 32;
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    // (first pass: every wave is done with the ring; later: this wave has
+    // read back the previous pass)
+    __syncthreads();
+    if (j == 0)
+      for (int t = tid; t < BN; t += NT) bsh[t] = (o.bias && n0 + t < o.n_real) ? o.bias[n0 + t] : 0.f;
+#pragma unroll
+    for (int i = 0; i < TN; ++i)
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4)
+        *reinterpret_cast<float4*>(stg + lr * SROW + i * 32 + 8 * g4 + 4 * h) =
+            make_float4(acc[i][j][4 * g4], acc[i][j][4 * g4 + 1], acc[i][j][4 * g4 + 2], acc[i][j][4 * g4 + 3]);
+    __syncthreads();
+    const int mb = m0 + (wm * TM + j) * 32;
+#pragma unroll
+    for (int t = 0; t < NQ / 2; ++t) {
+      const int c = 64 * t + lane, p = c / NQ, q = c - p * NQ;
+      const int m = mb + p, n = nw + 8 * q;
+      if (m >= k.M || n >= o.yC) continue;
+      float v[8];
+      {
+        const float4 a = *reinterpret_cast<const float4*>(stg + p * SROW + 8 * q);
+        const float4 b = *reinterpret_cast<const float4*>(stg + p * SROW + 8 * q + 4);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+      }
+      {
+        const float4 a = *reinterpret_cast<const float4*>(bw + 8 * q);
+        const float4 b = *reinterpret_cast<const float4*>(bw + 8 * q + 4);
+        const float bv[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = v[e] * accs + bv[e];
+      }
+      int mo = m;
+      if (GATHER == G_SUB) {
+        // source-grid pixel (b, i, j) -> output pixel (b, 2i + a, 2j + b) of the 2x grid
+        int bb, ii, jj;
+        pix_of(k, m, bb, ii, jj);
+        mo = (bb * 2 * k.H + 2 * ii + pa) * (2 * k.W) + 2 * jj + pb;
+      }
+      if (o.mask) {
+        float mk[8];
+        load8(o.mask, o.mask_f32, mo * o.maskC + n, mk);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = mk[e] > 0.f ? v[e] : 0.f;
+      }
+      if (o.res_mode != R_NONE) {
+        int ridx = mo;
+        if (o.res_mode == R_HALF) {
+          int bb, oh, ow;
+          pix_of(k, m, bb, oh, ow);
+          ridx = (bb * (k.H >> 1) + (oh >> 1)) * (k.W >> 1) + (ow >> 1);
+        }
+        float rv8[8];
+        load8(o.res, o.res_f32, ridx * o.resC + n, rv8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] += o.res_scale * rv8[e];
+      }
+      if (n + 8 > o.n_real) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (n + e >= o.n_real) v[e] = 0.f;
+      }
+      const int yo = mo * o.yC + n;
+      if (o.y_f32) {
+        float* yp = (float*)o.y + yo;
+        *reinterpret_cast<float4*>(yp) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(yp + 4) = make_float4(v[4], v[5], v[6], v[7]);
+      } else {
+        *reinterpret_cast<uint4*>((bf16_t*)o.y + yo) =
+            make_uint4(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]), f2bf2(v[4], v[5]), f2bf2(v[6], v[7]));
+      }
+    }
+  }
+}
+
 template <int WN, int WM, int TN, int TM, int NS, int KS, int GATHER, bool RELU>
 __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k) {
   constexpr int NW = WN * WM;                  // waves per block (4 or 8)
@@ -256,93 +354,176 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
     conv_step<TN, TM, RELU, KS>(Xs[st], Ws[st], xbase, wbase, rdo, acc);
   }
 
-  // ---- epilogue, 32 pixels of a wave at a time.  The MFMA layout (lane l:
-  // channels 8 g + 4 (l / 32) + 0..3 of pixel l % 32) goes to this wave's
-  // fp32 staging rows; read back, lane l takes chunk c = 64 t + l, i.e. the
-  // eight channels 8 (c % NQ) .. + 7 of pixel c / NQ.
-  constexpr int NQ = TN * 4;                   // 8-channel chunks per pixel
-  const ConvOut& o = k.o;
-  const float accs = (o.acc_scale ? *o.acc_scale : 1.f) * o.acc_mul;
-  float* const stg = reinterpret_cast<float*>(lds) + wave * 32 * SROW;
-  // the block's bias, past every wave's staging rows
-  float* const bsh = reinterpret_cast<float*>(lds) + NW * 32 * SROW;
-  const int nw = n0 + wn * TN * 32;
-  const float* const bw = bsh + wn * TN * 32;
+  conv_epilogue<WN, WM, TN, TM, GATHER>(k, acc, lds, m0, n0, wn, wm, wave, lane, pa, pb);
+}
+
+// Halo variant for the 3x3, pad-1 convolution over the direct gather,
+// used when a block tile is TR = BM / W whole image rows of one image.  The
+// loop runs over 32-channel chunks outside and the nine taps inside: per
+// chunk, the tile's rows plus a one-pixel border -- a (TR + 2) x (W + 2)
+// patch -- move into LDS once (double-buffered, the next chunk's patch
+// issued at the chunk's first tap), and every tap reads its operand rows
+// out of the patch at offset (r, s), so the activation crosses the load
+// path once per chunk instead of nine times.  The weights of each tap step
+// come through a three-stage ring as in k_conv_fwd; with nine steps per
+// chunk the stage of tap t is t % 3.  Patch rows keep the 64-byte row
+// layout and swizzle of k_conv_fwd, indexed by patch pixel.
+template <int WN, int WM, int TN, int TM, int PPX, bool RELU>
+__global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k) {
+  constexpr int NW = WN * WM;
+  constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
+  constexpr int RG = 16 * NW;                  // rows covered by one load of every wave
+  constexpr int WR = (BN + RG - 1) / RG * RG, BP = WR / RG;
+  static_assert(PPX % RG == 0, "patch rows are whole block loads");
+  constexpr int PLW = PPX / RG;                // patch loads per wave per chunk
+  constexpr int PATCH = PPX * 32, WST = WR * 32;   // bf16 elements
+  constexpr int RING = 2 * PATCH + 3 * WST;
+  constexpr int SROW = TN * 32 + 4;
+  constexpr int EPI = NW * 32 * SROW * 2 + 2 * BN;
+  __shared__ __attribute__((aligned(16))) bf16_t lds[RING > EPI ? RING : EPI];
+
+  const int bid = remap_tile2(blockIdx.x, k.tiles_m * k.tiles_n);
+  const int tmi = bid / k.tiles_n, tni = bid - tmi * k.tiles_n;
+  const int m0 = tmi * BM, n0 = tni * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wn = wave / WM, wm = wave % WM;
+  const int C = k.C, H = k.H, W = k.W, PC = W + 2;
+  // the tile: rows tr0 .. tr0 + TR - 1 of image b (the host checks that W
+  // divides BM and BM / W divides H)
+  const int TR = BM / W;
+  const int t0 = (int)fdiv((uint32_t)m0, k.fdW);
+  const int b = (int)fdiv((uint32_t)t0, k.fdH), tr0 = t0 - b * H;
+  const int npx = (TR + 2) * PC;
+
+  // loads: load j of this wave covers rows 16 (NW j + wave) .. + 15 of the
+  // patch (pixels) or of the weight tile; lane l fills row + l / 4, LDS
+  // chunk l % 4 = source chunk (l % 4) ^ ((l / 16) % 4)
+  const int lrow = lane >> 2;
+  const uint32_t lchunk = (uint32_t)((lane & 3) ^ ((lane >> 4) & 3));
+  uint32_t poff[PLW];
+#pragma unroll
+  for (int j = 0; j < PLW; ++j) {
+    const int q = 16 * (NW * j + wave) + lrow;
+    const int pr = q / PC, pc = q - pr * PC;
+    const int ih = tr0 - 1 + pr, iw = pc - 1;
+    const bool ok = q < npx && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
+    poff[j] = ok ? (uint32_t)(((b * H + ih) * W + iw) * C) * 2u + 16u * lchunk : kOOB;
+  }
+  uint32_t woff[BP];
+#pragma unroll
+  for (int j = 0; j < BP; ++j) {
+    const int row = 16 * (NW * j + wave) + lrow;
+    const int n = n0 + row;
+    woff[j] = row < BN && n < k.Np ? (uint32_t)(n * 9 * C) * 2u + 16u * lchunk : kOOB;
+  }
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(k.x, k.x_bytes);
+  const __amdgpu_buffer_rsrc_t wr = make_rsrc(k.w, k.w_bytes);
+  const uint32_t pl0 = lds_addr(lds + 16 * wave * 32), wl0 = lds_addr(lds + 2 * PATCH + 16 * wave * 32);
+  // chunk c's patch into buffer buf
+  auto issue_patch = [&](int buf, int c) {
+    const uint32_t coff = __builtin_amdgcn_readfirstlane(64u * (uint32_t)c);
+    const uint32_t pl = pl0 + (uint32_t)buf * (PATCH * 2);
+#pragma unroll
+    for (int j = 0; j < PLW; ++j) lds_load16(pl + j * (NW * 1024u), poff[j], coff, xr);
+  };
+  // weights of step s (chunk s / 9, tap s % 9) into stage st
+  auto issue_w = [&](int st, int step) {
+    const int c = step / 9, t = step - 9 * c;
+    const uint32_t wk = __builtin_amdgcn_readfirstlane(2u * (uint32_t)(t * C + 32 * c));
+    const uint32_t wl = wl0 + (uint32_t)st * (WST * 2);
+#pragma unroll
+    for (int j = 0; j < BP; ++j) lds_load16(wl + j * (NW * 1024u), woff[j], wk, wr);
+  };
+
+  // operand reads: weight rows as in k_conv_fwd; activation fragment j of
+  // this wave holds tile pixels p = (wm TM + j) 32 + lane % 32, read at
+  // patch pixel q0 + r PC + s for tap (r, s), q0 = (p / W) PC + p % W
+  const int lr = lane & 31, h = lane >> 5;
+  const int f = (lr >> 2) & 3;
+  const int rdw[2] = {lr * 32 + 8 * ((0 + h) ^ f), lr * 32 + 8 * ((2 + h) ^ f)};
+  const int wbase = wn * TN * 32 * 32;
+  int q0[TM];
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
-    // (first pass: every wave is done with the ring; later: this wave has
-    // read back the previous pass)
-    __syncthreads();
-    if (j == 0)
-      for (int t = tid; t < BN; t += NT) bsh[t] = (o.bias && n0 + t < o.n_real) ? o.bias[n0 + t] : 0.f;
+    const int p = (wm * TM + j) * 32 + lr;
+    const int ty = (int)fdiv((uint32_t)p, k.fdW);
+    q0[j] = ty * PC + (p - ty * W);
+  }
+
+  f32x16 acc[TN][TM];
 #pragma unroll
-    for (int i = 0; i < TN; ++i)
+  for (int i = 0; i < TN; ++i)
 #pragma unroll
-      for (int g4 = 0; g4 < 4; ++g4)
-        *reinterpret_cast<float4*>(stg + lr * SROW + i * 32 + 8 * g4 + 4 * h) =
-            make_float4(acc[i][j][4 * g4], acc[i][j][4 * g4 + 1], acc[i][j][4 * g4 + 2], acc[i][j][4 * g4 + 3]);
-    __syncthreads();
-    const int mb = m0 + (wm * TM + j) * 32;
+    for (int j = 0; j < TM; ++j)
 #pragma unroll
-    for (int t = 0; t < NQ / 2; ++t) {
-      const int c = 64 * t + lane, p = c / NQ, q = c - p * NQ;
-      const int m = mb + p, n = nw + 8 * q;
-      if (m >= k.M || n >= o.yC) continue;
-      float v[8];
-      {
-        const float4 a = *reinterpret_cast<const float4*>(stg + p * SROW + 8 * q);
-        const float4 b = *reinterpret_cast<const float4*>(stg + p * SROW + 8 * q + 4);
-        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-        v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-      }
-      {
-        const float4 a = *reinterpret_cast<const float4*>(bw + 8 * q);
-        const float4 b = *reinterpret_cast<const float4*>(bw + 8 * q + 4);
-        const float bv[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  // Issue order: P(0) W(0) W(1), then at step s W(s + 2) and, at a chunk's
+  // first tap, P(c + 1).  Step s waits until W(s) -- and with it every
+  // earlier load, P(c) among them -- has landed; still in flight may be
+  // W(s + 1) and, at taps 1 and 2, P(c + 1).  The barrier then also
+  // guarantees that no wave reads weight stage (s - 1) % 3 or patch buffer
+  // (c + 1) % 2 (last read in chunk c - 1) any more before they refill.
+  const int nch = C / 32, S = 9 * nch;
+  issue_patch(0, 0);
+  issue_w(0, 0);
+  if (S > 1) issue_w(1, 1);
+  for (int c = 0; c < nch; ++c) {
+    const bf16_t* Pc = lds + (c & 1) * PATCH;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = v[e] * accs + bv[e];
-      }
-      int mo = m;
-      if (GATHER == G_SUB) {
-        // source-grid pixel (b, i, j) -> output pixel (b, 2i + a, 2j + b) of the 2x grid
-        int bb, ii, jj;
-        pix_of(k, m, bb, ii, jj);
-        mo = (bb * 2 * k.H + 2 * ii + pa) * (2 * k.W) + 2 * jj + pb;
-      }
-      if (o.mask) {
-        float mk[8];
-        load8(o.mask, o.mask_f32, mo * o.maskC + n, mk);
+    for (int t = 0; t < 9; ++t) {
+      const int s = 9 * c + t;
+      const bool wmore = s + 1 < S;
+      const bool pmore = (t == 1 || t == 2) && c + 1 < nch;
+      if (wmore && pmore) wait_barrier<vm_cap(BP + PLW)>();
+      else if (wmore) wait_barrier<BP>();
+      else if (pmore) wait_barrier<PLW>();
+      else wait_barrier<0>();
+      if (s + 2 < S) issue_w((t + 2) % 3, s + 2);
+      if (t == 0 && c + 1 < nch) issue_patch((c + 1) & 1, c + 1);
+      const int qoff = (t / 3) * PC + (t % 3);
+      const bf16_t* Wt = lds + 2 * PATCH + (t % 3) * WST;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] = mk[e] > 0.f ? v[e] : 0.f;
-      }
-      if (o.res_mode != R_NONE) {
-        int ridx = mo;
-        if (o.res_mode == R_HALF) {
-          int bb, oh, ow;
-          pix_of(k, m, bb, oh, ow);
-          ridx = (bb * (k.H >> 1) + (oh >> 1)) * (k.W >> 1) + (ow >> 1);
+      for (int kk = 0; kk < 2; ++kk) {
+        bf16x8 wv[TN], xv[TM];
+#pragma unroll
+        for (int i = 0; i < TN; ++i) wv[i] = *reinterpret_cast<const bf16x8*>(Wt + wbase + i * 32 * 32 + rdw[kk]);
+#pragma unroll
+        for (int j = 0; j < TM; ++j) {
+          const int q = q0[j] + qoff;
+          const uint4 v = *reinterpret_cast<const uint4*>(Pc + q * 32 + 8 * ((2 * kk + h) ^ ((q >> 2) & 3)));
+          xv[j] = __builtin_bit_cast(bf16x8, RELU ? relu8_bits(v) : v);
         }
-        float rv8[8];
-        load8(o.res, o.res_f32, ridx * o.resC + n, rv8);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) v[e] += o.res_scale * rv8[e];
-      }
-      if (n + 8 > o.n_real) {
+        for (int i = 0; i < TN; ++i)
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          if (n + e >= o.n_real) v[e] = 0.f;
-      }
-      const int yo = mo * o.yC + n;
-      if (o.y_f32) {
-        float* yp = (float*)o.y + yo;
-        *reinterpret_cast<float4*>(yp) = make_float4(v[0], v[1], v[2], v[3]);
-        *reinterpret_cast<float4*>(yp + 4) = make_float4(v[4], v[5], v[6], v[7]);
-      } else {
-        *reinterpret_cast<uint4*>((bf16_t*)o.y + yo) =
-            make_uint4(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]), f2bf2(v[4], v[5]), f2bf2(v[6], v[7]));
+          for (int j = 0; j < TM; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[i], xv[j], acc[i][j], 0, 0, 0);
       }
     }
   }
+  conv_epilogue<WN, WM, TN, TM, G_DIRECT>(k, acc, lds, m0, n0, wn, wm, wave, lane, 0, 0);
+}
+
+template <int WN, int WM, int TN, int TM, int PPX>
+std::string launch_halo(hipStream_t s, CfK& k, bool relu) {
+  constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
+  k.tiles_m = (int)cdiv(k.M, BM);
+  k.tiles_n = (int)cdiv(k.Np, BN);
+  k.ksteps = 9 * (k.C / 32);
+  dim3 grid(k.tiles_m * k.tiles_n), block(64 * WN * WM);
+  const std::string name = "k_conv_halo<" + std::to_string(BN) + "x" + std::to_string(BM) + (relu ? ",true>" : ",false>");
+  if (relu)
+    hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, true>), grid, block, 0, s, k);
+  else
+    hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, false>), grid, block, 0, s, k);
+  return name;
+}
+// patch pixels of a BM-pixel tile of whole rows of a W-wide image (0: not eligible)
+inline int halo_patch(int BM, int H, int W) {
+  if (W < 16 || BM % W || H % (BM / W)) return 0;
+  return (BM / W + 2) * (W + 2);
 }
 
 template <int WN, int WM, int TN, int TM, int NS = 3, int KS = 32>
@@ -422,10 +603,23 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   // for multiples of 128 (128 x 128 for exactly 128, the 1x1 attention
   // projections with K <= 192), 192 x 128 for multiples of 192, 96 x 256
   // for the other multiples of 96, and 32 / 64 x 256 for narrow outputs.
+  // Direct 3x3 convs whose tiles are whole image rows take the halo kernel
+  // (each activation chunk loaded once for all nine taps) on the 256 x 256
+  // and 192 x 128 tiles, and for 96 channels on an eight-wave 96 x 512 tile,
+  // whose weight loads the wider tile amortises (measured: on the four-wave
+  // 128 x 256 tile the patch addressing of its four pixel fragments costs
+  // more than the loads it saves).
+  const bool halo = in.gather == G_DIRECT && R == 3;
+  auto fits = [&](int bm, int ppx) {
+    const int np = halo_patch(bm, H, W);
+    return halo && np > 0 && np <= ppx;
+  };
   const int64_t tiles8 = cdiv(k.M, 256) * (Np / 256) * (in.gather == G_SUB ? 4 : 1);
   const int64_t last8 = tiles8 % 256;
   if (Np % 256 == 0 && tiles8 >= 192 && (last8 == 0 || last8 >= 192))
-    return launch_cfg<2, 4, 4, 2>(s, k, in.gather, in.relu);
+    return fits(256, 384) ? launch_halo<2, 4, 4, 2, 384>(s, k, in.relu) : launch_cfg<2, 4, 4, 2>(s, k, in.gather, in.relu);
+  if (Np % 192 == 0 && fits(128, 320)) return launch_halo<2, 2, 3, 2, 320>(s, k, in.relu);
+  if (Np == 96 && fits(512, 896)) return launch_halo<1, 8, 3, 2, 896>(s, k, in.relu);
   if (Np == 128) return launch_cfg<2, 2, 2, 2>(s, k, in.gather, in.relu);
   if (Np % 128 == 0) return launch_cfg<2, 2, 2, 4>(s, k, in.gather, in.relu);
   if (Np % 192 == 0) return launch_cfg<2, 2, 3, 2>(s, k, in.gather, in.relu);
