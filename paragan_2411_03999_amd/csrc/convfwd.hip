@@ -357,19 +357,24 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
   conv_epilogue<WN, WM, TN, TM, GATHER>(k, acc, lds, m0, n0, wn, wm, wave, lane, pa, pb);
 }
 
-// Halo variant for the 3x3, pad-1 convolution over the direct gather,
-// used when a block tile is TR = BM / W whole image rows of one image.  The
-// loop runs over 32-channel chunks outside and the nine taps inside: per
-// chunk, the tile's rows plus a one-pixel border -- a (TR + 2) x (W + 2)
-// patch -- move into LDS once (double-buffered, the next chunk's patch
-// issued at the chunk's first tap), and every tap reads its operand rows
-// out of the patch at offset (r, s), so the activation crosses the load
-// path once per chunk instead of nine times.  The weights of each tap step
-// come through a three-stage ring as in k_conv_fwd; with nine steps per
-// chunk the stage of tap t is t % 3.  Patch rows keep the 64-byte row
-// layout and swizzle of k_conv_fwd, indexed by patch pixel.
-template <int WN, int WM, int TN, int TM, int PPX, bool RELU>
+// Halo variant for the 3x3, pad-1 convolution over the direct gather
+// (GK = G_DIRECT, nine taps) and for the sub-pixel gather (GK = G_SUB, the
+// four 2x2 taps of one parity class over the source grid), used when a
+// block tile is TR = BM / W whole image rows of one image.  The loop runs
+// over 32-channel chunks outside and the T taps inside: per chunk, the
+// tile's rows plus a one-pixel border -- a (TR + 2) x (W + 2) patch -- move
+// into LDS once (double-buffered, the next chunk's patch issued at the
+// chunk's first tap), and every tap reads its operand rows out of the patch
+// at its offset, so the activation crosses the load path once per chunk
+// instead of once per tap.  The weights of each tap step come through a
+// ring of NSW stages as in k_conv_fwd; T is a multiple of NSW, so the stage
+// of tap t is t % NSW.  Patch rows keep the 64-byte row layout and swizzle
+// of k_conv_fwd, indexed by patch pixel.
+template <int WN, int WM, int TN, int TM, int PPX, int GK, bool RELU>
 __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k) {
+  static_assert(GK == G_DIRECT || GK == G_SUB, "halo gathers");
+  constexpr int T = GK == G_SUB ? 4 : 9;       // taps per chunk
+  constexpr int NSW = GK == G_SUB ? 2 : 3;     // weight ring stages
   constexpr int NW = WN * WM;
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
   constexpr int RG = 16 * NW;                  // rows covered by one load of every wave
@@ -377,7 +382,7 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
   static_assert(PPX % RG == 0, "patch rows are whole block loads");
   constexpr int PLW = PPX / RG;                // patch loads per wave per chunk
   constexpr int PATCH = PPX * 32, WST = WR * 32;   // bf16 elements
-  constexpr int RING = 2 * PATCH + 3 * WST;
+  constexpr int RING = 2 * PATCH + NSW * WST;
   constexpr int SROW = TN * 32 + 4;
   constexpr int EPI = NW * 32 * SROW * 2 + 2 * BN;
   __shared__ __attribute__((aligned(16))) bf16_t lds[RING > EPI ? RING : EPI];
@@ -388,6 +393,9 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave / WM, wm = wave % WM;
+  // sub-pixel parity class (a, b) of this block's output pixels
+  const int par = GK == G_SUB ? (int)blockIdx.y : 0;
+  const int pa = par >> 1, pb = par & 1;
   const int C = k.C, H = k.H, W = k.W, PC = W + 2;
   // the tile: rows tr0 .. tr0 + TR - 1 of image b (the host checks that W
   // divides BM and BM / W divides H)
@@ -415,7 +423,8 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
   for (int j = 0; j < BP; ++j) {
     const int row = 16 * (NW * j + wave) + lrow;
     const int n = n0 + row;
-    woff[j] = row < BN && n < k.Np ? (uint32_t)(n * 9 * C) * 2u + 16u * lchunk : kOOB;
+    // (the sub-pixel filters are [4][Np][2][2][C], one per parity)
+    woff[j] = row < BN && n < k.Np ? (uint32_t)((par * k.Np + n) * T * C) * 2u + 16u * lchunk : kOOB;
   }
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(k.x, k.x_bytes);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(k.w, k.w_bytes);
@@ -427,9 +436,9 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
 #pragma unroll
     for (int j = 0; j < PLW; ++j) lds_load16(pl + j * (NW * 1024u), poff[j], coff, xr);
   };
-  // weights of step s (chunk s / 9, tap s % 9) into stage st
+  // weights of step s (chunk s / T, tap s % T) into stage st
   auto issue_w = [&](int st, int step) {
-    const int c = step / 9, t = step - 9 * c;
+    const int c = step / T, t = step - T * c;
     const uint32_t wk = __builtin_amdgcn_readfirstlane(2u * (uint32_t)(t * C + 32 * c));
     const uint32_t wl = wl0 + (uint32_t)st * (WST * 2);
 #pragma unroll
@@ -438,7 +447,8 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
 
   // operand reads: weight rows as in k_conv_fwd; activation fragment j of
   // this wave holds tile pixels p = (wm TM + j) 32 + lane % 32, read at
-  // patch pixel q0 + r PC + s for tap (r, s), q0 = (p / W) PC + p % W
+  // patch pixel q0 + r PC + s for tap offset (r, s), q0 = (p / W) PC + p % W
+  // (direct: tap t at (t / 3, t % 3); sub-pixel: (t / 2 + a, t % 2 + b))
   const int lr = lane & 31, h = lane >> 5;
   const int f = (lr >> 2) & 3;
   const int rdw[2] = {lr * 32 + 8 * ((0 + h) ^ f), lr * 32 + 8 * ((2 + h) ^ f)};
@@ -459,31 +469,34 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // Issue order: P(0) W(0) W(1), then at step s W(s + 2) and, at a chunk's
-  // first tap, P(c + 1).  Step s waits until W(s) -- and with it every
-  // earlier load, P(c) among them -- has landed; still in flight may be
-  // W(s + 1) and, at taps 1 and 2, P(c + 1).  The barrier then also
-  // guarantees that no wave reads weight stage (s - 1) % 3 or patch buffer
-  // (c + 1) % 2 (last read in chunk c - 1) any more before they refill.
-  const int nch = C / 32, S = 9 * nch;
+  // Issue order: P(0) W(0) .. W(NSW - 2), then at step s W(s + NSW - 1)
+  // and, at a chunk's first tap, P(c + 1).  Step s waits until W(s) -- and
+  // with it every earlier load, P(c) among them -- has landed; still in
+  // flight may be W(s + 1) .. W(s + NSW - 2) and, at taps 1 .. NSW - 1,
+  // P(c + 1).  The barrier then also guarantees that no wave reads weight
+  // stage (s - 1) % NSW or patch buffer (c + 1) % 2 (last read in chunk
+  // c - 1) any more before they refill.
+  static_assert(T % NSW == 0 && NSW <= 3, "ring stage of a tap");
+  const int nch = C / 32, S = T * nch;
   issue_patch(0, 0);
-  issue_w(0, 0);
-  if (S > 1) issue_w(1, 1);
+#pragma unroll
+  for (int st = 0; st < NSW - 1; ++st)
+    if (st < S) issue_w(st, st);
   for (int c = 0; c < nch; ++c) {
     const bf16_t* Pc = lds + (c & 1) * PATCH;
 #pragma unroll
-    for (int t = 0; t < 9; ++t) {
-      const int s = 9 * c + t;
-      const bool wmore = s + 1 < S;
-      const bool pmore = (t == 1 || t == 2) && c + 1 < nch;
+    for (int t = 0; t < T; ++t) {
+      const int s = T * c + t;
+      const bool wmore = NSW == 3 && s + 1 < S;
+      const bool pmore = t >= 1 && t <= NSW - 1 && c + 1 < nch;
       if (wmore && pmore) wait_barrier<vm_cap(BP + PLW)>();
       else if (wmore) wait_barrier<BP>();
       else if (pmore) wait_barrier<PLW>();
       else wait_barrier<0>();
-      if (s + 2 < S) issue_w((t + 2) % 3, s + 2);
+      if (s + NSW - 1 < S) issue_w((t + NSW - 1) % NSW, s + NSW - 1);
       if (t == 0 && c + 1 < nch) issue_patch((c + 1) & 1, c + 1);
-      const int qoff = (t / 3) * PC + (t % 3);
-      const bf16_t* Wt = lds + 2 * PATCH + (t % 3) * WST;
+      const int qoff = GK == G_SUB ? ((t >> 1) + pa) * PC + (t & 1) + pb : (t / 3) * PC + (t % 3);
+      const bf16_t* Wt = lds + 2 * PATCH + (t % NSW) * WST;
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         bf16x8 wv[TN], xv[TM];
@@ -503,21 +516,27 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
       }
     }
   }
-  conv_epilogue<WN, WM, TN, TM, G_DIRECT>(k, acc, lds, m0, n0, wn, wm, wave, lane, 0, 0);
+  conv_epilogue<WN, WM, TN, TM, GK>(k, acc, lds, m0, n0, wn, wm, wave, lane, pa, pb);
 }
 
-template <int WN, int WM, int TN, int TM, int PPX>
+template <int WN, int WM, int TN, int TM, int PPX, int GK>
 std::string launch_halo(hipStream_t s, CfK& k, bool relu) {
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
   k.tiles_m = (int)cdiv(k.M, BM);
   k.tiles_n = (int)cdiv(k.Np, BN);
-  k.ksteps = 9 * (k.C / 32);
-  dim3 grid(k.tiles_m * k.tiles_n), block(64 * WN * WM);
-  const std::string name = "k_conv_halo<" + std::to_string(BN) + "x" + std::to_string(BM) + (relu ? ",true>" : ",false>");
-  if (relu)
-    hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, true>), grid, block, 0, s, k);
-  else
-    hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, false>), grid, block, 0, s, k);
+  k.ksteps = (GK == G_SUB ? 4 : 9) * (k.C / 32);
+  dim3 grid(k.tiles_m * k.tiles_n, GK == G_SUB ? 4 : 1), block(64 * WN * WM);
+  const std::string name = "k_conv_halo<" + std::to_string(BN) + "x" + std::to_string(BM) +
+                           (GK == G_SUB ? ",G_SUB" : "") + (relu ? ",true>" : ",false>");
+  if constexpr (GK == G_DIRECT) {
+    if (relu)
+      hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, G_DIRECT, true>), grid, block, 0, s, k);
+    else
+      hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, G_DIRECT, false>), grid, block, 0, s, k);
+  } else {
+    if (relu) throw Error{-2, "conv_fwd: no ReLU'd operand for the sub-pixel gather"};
+    hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, GK, false>), grid, block, 0, s, k);
+  }
   return name;
 }
 // patch pixels of a BM-pixel tile of whole rows of a W-wide image (0: not eligible)
@@ -617,9 +636,22 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   const int64_t tiles8 = cdiv(k.M, 256) * (Np / 256) * (in.gather == G_SUB ? 4 : 1);
   const int64_t last8 = tiles8 % 256;
   if (Np % 256 == 0 && tiles8 >= 192 && (last8 == 0 || last8 >= 192))
-    return fits(256, 384) ? launch_halo<2, 4, 4, 2, 384>(s, k, in.relu) : launch_cfg<2, 4, 4, 2>(s, k, in.gather, in.relu);
-  if (Np % 192 == 0 && fits(128, 320)) return launch_halo<2, 2, 3, 2, 320>(s, k, in.relu);
-  if (Np == 96 && fits(512, 896)) return launch_halo<1, 8, 3, 2, 896>(s, k, in.relu);
+    return fits(256, 384) ? launch_halo<2, 4, 4, 2, 384, G_DIRECT>(s, k, in.relu)
+                          : launch_cfg<2, 4, 4, 2>(s, k, in.gather, in.relu);
+  if (Np % 192 == 0 && fits(128, 320)) return launch_halo<2, 2, 3, 2, 320, G_DIRECT>(s, k, in.relu);
+  if (Np == 96 && fits(512, 896)) return launch_halo<1, 8, 3, 2, 896, G_DIRECT>(s, k, in.relu);
+  // sub-pixel convs (a 2x2 filter per parity over the source grid) share the
+  // patch logic, over a 96 x 256 tile and, for K = 4 C of at least 1536
+  // (3072 for multiples of 128, which otherwise take 128 x 256), a 192 x 128
+  // one (measured: shorter K loses to the ring kernel)
+  const bool hsub = in.gather == G_SUB && R == 2;
+  auto fits_sub = [&](int bm, int ppx) {
+    const int np = halo_patch(bm, H, W);
+    return hsub && np > 0 && np <= ppx;
+  };
+  if (Np % 192 == 0 && in.C >= (Np % 128 == 0 ? 768 : 384) && fits_sub(128, 320))
+    return launch_halo<2, 2, 3, 2, 320, G_SUB>(s, k, false);
+  if (Np == 96 && fits_sub(256, 448)) return launch_halo<1, 4, 3, 2, 448, G_SUB>(s, k, false);
   if (Np == 128) return launch_cfg<2, 2, 2, 2>(s, k, in.gather, in.relu);
   if (Np % 128 == 0) return launch_cfg<2, 2, 2, 4>(s, k, in.gather, in.relu);
   if (Np % 192 == 0) return launch_cfg<2, 2, 3, 2>(s, k, in.gather, in.relu);
