@@ -108,30 +108,43 @@ struct Stager {
 // ------------------------------------------------------------- pooling
 // Max over each 2x2 window (first maximum in (dh, dw) row-major order wins)
 // of the phi and g channels; writes K and V, rows >= L zero.
+// 2x2 max pool of the key / value projections, 8 channels per thread
+// (16-byte loads and stores); ties keep the first of the window in row
+// order; rows l >= L of the padded outputs are zero.
 __global__ void k_attn_pool(const bf16_t* qkv, int B, int H, int W, int Nqkv, int dk, int dv, int Lp, bf16_t* kp,
                             bf16_t* vp) {
   const int L = (H / 2) * (W / 2);
-  const int nch = dk + dv;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (int64_t)B * Lp * nch) return;
-  const int c = (int)(i % nch);
-  const int64_t t = i / nch;
-  const int l = (int)(t % Lp);
-  const int b = (int)(t / Lp);
-  bf16_t best = 0;
+  const int ng = (dk + dv) / 8;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= B * Lp * ng) return;
+  const int g = i % ng, t = i / ng;
+  const int l = t % Lp, b = t / Lp;
+  const int c = 8 * g;
+  uint4 best = make_uint4(0u, 0u, 0u, 0u);
   if (l < L) {
-    const int ph = l / (W / 2), pw = l % (W / 2);
-    float bv = 0.f;
+    const int ph = l / (W / 2), pw = l - ph * (W / 2);
+    float bv[8];
+#pragma unroll
     for (int d = 0; d < 4; ++d) {
       const int h = 2 * ph + (d >> 1), w = 2 * pw + (d & 1);
-      const bf16_t v = qkv[(((int64_t)b * H + h) * W + w) * Nqkv + dk + c];
-      if (d == 0 || bf2f(v) > bv) { bv = bf2f(v); best = v; }
+      const uint4 q = *reinterpret_cast<const uint4*>(qkv + ((int64_t)(b * H + h) * W + w) * Nqkv + dk + c);
+      float v[8];
+      unpack8(q, v);
+      uint32_t* bw = reinterpret_cast<uint32_t*>(&best);
+      const uint32_t* qw = reinterpret_cast<const uint32_t*>(&q);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (d == 0 || v[e] > bv[e]) {
+          bv[e] = v[e];
+          const uint32_t half = (qw[e >> 1] >> (16 * (e & 1))) & 0xffffu;
+          bw[e >> 1] = (bw[e >> 1] & ~(0xffffu << (16 * (e & 1)))) | (half << (16 * (e & 1)));
+        }
     }
   }
   if (c < dk)
-    kp[((int64_t)b * Lp + l) * dk + c] = best;
+    *reinterpret_cast<uint4*>(kp + ((int64_t)b * Lp + l) * dk + c) = best;
   else
-    vp[((int64_t)b * Lp + l) * dv + c - dk] = best;
+    *reinterpret_cast<uint4*>(vp + ((int64_t)b * Lp + l) * dv + c - dk) = best;
 }
 
 // ------------------------------------------------------------- forward
@@ -508,28 +521,46 @@ __global__ __launch_bounds__(256, 2) void k_attn_dkv(const bf16_t* qkv, int Nqkv
 
 // Max-pool backward: route dK / dV to the window's argmax (recomputed from
 // the forward projections with the same tie rule), zeros elsewhere.
+// its backward, 8 channels per thread: the gradient goes to the window's
+// (first) maximum, zeros elsewhere
 __global__ void k_attn_pool_bwd(const bf16_t* qkv, const bf16_t* dk, const bf16_t* dvv, int B, int H, int W,
                                 int Nqkv, int dkw, int dvw, int Lp, bf16_t* dqkv) {
-  const int nch = dkw + dvw;
+  const int ng = (dkw + dvw) / 8;
   const int L = (H / 2) * (W / 2);
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (int64_t)B * L * nch) return;
-  const int c = (int)(i % nch);
-  const int64_t t = i / nch;
-  const int l = (int)(t % L);
-  const int b = (int)(t / L);
-  const int ph = l / (W / 2), pw = l % (W / 2);
-  int arg = 0;
-  float bv = 0.f;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= B * L * ng) return;
+  const int g = i % ng, t = i / ng;
+  const int l = t % L, b = t / L;
+  const int c = 8 * g;
+  const int ph = l / (W / 2), pw = l - ph * (W / 2);
+  int arg[8];
+  float bv[8];
+#pragma unroll
   for (int d = 0; d < 4; ++d) {
     const int h = 2 * ph + (d >> 1), w = 2 * pw + (d & 1);
-    const float v = bf2f(qkv[(((int64_t)b * H + h) * W + w) * Nqkv + dkw + c]);
-    if (d == 0 || v > bv) { bv = v; arg = d; }
+    float v[8];
+    unpack8(*reinterpret_cast<const uint4*>(qkv + ((int64_t)(b * H + h) * W + w) * Nqkv + dkw + c), v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (d == 0 || v[e] > bv[e]) {
+        bv[e] = v[e];
+        arg[e] = d;
+      }
   }
-  const bf16_t gv = c < dkw ? dk[((int64_t)b * Lp + l) * dkw + c] : dvv[((int64_t)b * Lp + l) * dvw + c - dkw];
+  const uint4 gq = c < dkw ? *reinterpret_cast<const uint4*>(dk + ((int64_t)b * Lp + l) * dkw + c)
+                           : *reinterpret_cast<const uint4*>(dvv + ((int64_t)b * Lp + l) * dvw + c - dkw);
+  const uint32_t* gw = reinterpret_cast<const uint32_t*>(&gq);
+#pragma unroll
   for (int d = 0; d < 4; ++d) {
     const int h = 2 * ph + (d >> 1), w = 2 * pw + (d & 1);
-    dqkv[(((int64_t)b * H + h) * W + w) * Nqkv + dkw + c] = d == arg ? gv : (bf16_t)0;
+    uint32_t o[4];
+#pragma unroll
+    for (int k2 = 0; k2 < 4; ++k2) {
+      const uint32_t lo = arg[2 * k2] == d ? (gw[k2] & 0xffffu) : 0u;
+      const uint32_t hi = arg[2 * k2 + 1] == d ? (gw[k2] & 0xffff0000u) : 0u;
+      o[k2] = lo | hi;
+    }
+    *reinterpret_cast<uint4*>(dqkv + ((int64_t)(b * H + h) * W + w) * Nqkv + dkw + c) = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
@@ -555,7 +586,9 @@ __global__ void k_attn_dgamma(const bf16_t* wo, const float* dwo, int64_t n, flo
   }
 
 void attn_pool(hipStream_t st, const AttnDims& a, const void* qkv, void* kp, void* vp) {
-  const int64_t n = (int64_t)a.B * a.Lp * (a.dk + a.dv);
+  PG_CHECK(a.dk % 8 == 0 && a.dv % 8 == 0 && a.Nqkv % 8 == 0, "attention pool: 8-channel groups");
+  const int64_t n = (int64_t)a.B * a.Lp * ((a.dk + a.dv) / 8);
+  PG_CHECK(n < (1LL << 31) && (int64_t)a.B * a.H * a.W * a.Nqkv < (1LL << 31), "attention pool: size");
   hipLaunchKernelGGL(k_attn_pool, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, (const bf16_t*)qkv, a.B, a.H,
                      a.W, a.Nqkv, a.dk, a.dv, a.Lp, (bf16_t*)kp, (bf16_t*)vp);
   PG_LAUNCH_CHECK();
@@ -593,7 +626,9 @@ void attn_bwd_core(hipStream_t st, const AttnDims& a, const void* qkv, const voi
   // dQ: 2 passes of S and dP plus dQ; dK/dV: S, dP, dV, dK
   prof.done("k_attn_bwd<" + std::to_string(a.dv) + ">",
             2.0 * a.B * (double)a.HW * a.L * (3 * a.dk + 4 * a.dv));
-  const int64_t n = (int64_t)a.B * a.L * (a.dk + a.dv);
+  const int64_t n = (int64_t)a.B * a.L * ((a.dk + a.dv) / 8);
+  PG_CHECK(a.dv % 8 == 0 && n < (1LL << 31) && (int64_t)a.B * a.H * a.W * a.Nqkv < (1LL << 31),
+           "attention pool: size");
   hipLaunchKernelGGL(k_attn_pool_bwd, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, (const bf16_t*)qkv,
                      (const bf16_t*)dk, (const bf16_t*)dvv, a.B, a.H, a.W, a.Nqkv, a.dk, a.dv, a.Lp,
                      (bf16_t*)dqkv);
