@@ -478,25 +478,51 @@ __global__ void k_dhead_dx(const bf16_t* x, int N, int HW, int C, int Cp, const 
 
 // dw[c] = sum_b dout[b] hs[b][c];  dbias = sum_b dout[b];
 // dE[k][c] = sum_{b: y_b = k} dout[b] hs[b][c]
-__global__ void k_dhead_dw(const float* hs, const float* dout, const int32_t* y, int N, int C, int n_classes,
-                           float* dw, float* dbias, float* dE) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < C) {
-    float s = 0.f;
-    for (int b = 0; b < N; ++b) s = fmaf(dout[b], hs[(int64_t)b * C + i], s);
-    dw[i] = s;
+// D head parameter gradients.  Linear weight dw[c] = sum_b dout[b] hs[b][c]
+// (16 waves per 64 channels, every 16th sample each, then the 16 sums in
+// wave order) and dbias = sum_b dout[b]; the projection embedding, one block
+// per class k: dE[k][c] = sum over the samples b of class k, in order, of
+// dout[b] hs[b][c] (zero for a class with no sample).
+__global__ __launch_bounds__(1024) void k_dhead_dw(const float* hs, const float* dout, int N, int C, float* dw,
+                                                   float* dbias) {
+  __shared__ float sh[16][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  float s = 0.f;
+  if (c < C)
+    for (int b = wv; b < N; b += 16) s = fmaf(dout[b], hs[(int64_t)b * C + c], s);
+  sh[wv][lane] = s;
+  __syncthreads();
+  if (wv == 0 && c < C) {
+    float t = 0.f;
+    for (int i = 0; i < 16; ++i) t += sh[i][lane];
+    dw[c] = t;
   }
-  if (i == 0) {
-    float s = 0.f;
-    for (int b = 0; b < N; ++b) s += dout[b];
-    dbias[0] = s;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    float t = 0.f;
+    for (int b = 0; b < N; ++b) t += dout[b];
+    dbias[0] = t;
   }
-  if (i < (int64_t)n_classes * C) {
-    const int k = (int)(i / C), c = (int)(i % C);
-    float s = 0.f;
+}
+__global__ __launch_bounds__(256) void k_dhead_de(const float* hs, const float* dout, const int32_t* y, int N, int C,
+                                                  float* dE) {
+  __shared__ int ys[1024], list[1024];
+  __shared__ int cnt;
+  const int k = blockIdx.x;
+  for (int b = threadIdx.x; b < N; b += 256) ys[b] = y[b];
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int n = 0;
     for (int b = 0; b < N; ++b)
-      if (y[b] == k) s = fmaf(dout[b], hs[(int64_t)b * C + c], s);
-    dE[i] = s;
+      if (ys[b] == k) list[n++] = b;
+    cnt = n;
+  }
+  __syncthreads();
+  const int n = cnt;
+  for (int c = threadIdx.x; c < C; c += 256) {
+    float s = 0.f;
+    for (int i = 0; i < n; ++i) s = fmaf(dout[list[i]], hs[(int64_t)list[i] * C + c], s);
+    dE[(int64_t)k * C + c] = s;
   }
 }
 
@@ -518,9 +544,9 @@ void dhead_bwd(hipStream_t st, const void* x, int N, int HW, int C, int Cp, cons
   hipLaunchKernelGGL(k_dhead_dx, dim3((unsigned)cdiv((int64_t)N * HW * Cp, 256)), dim3(256), 0, st,
                      (const bf16_t*)x, N, HW, C, Cp, y, dout, w, sw, E, se, (bf16_t*)dx);
   if (dw) {
-    const int64_t n = std::max<int64_t>((int64_t)n_classes * C, C);
-    hipLaunchKernelGGL(k_dhead_dw, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, st, hs, dout, y, N, C, n_classes,
-                       dw, dbias, dE);
+    PG_CHECK(N <= 1024, "dhead: batch of at most 1024");
+    hipLaunchKernelGGL(k_dhead_dw, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, hs, dout, N, C, dw, dbias);
+    hipLaunchKernelGGL(k_dhead_de, dim3((unsigned)n_classes), dim3(256), 0, st, hs, dout, y, N, C, dE);
   }
   PG_LAUNCH_CHECK();
 }
@@ -537,40 +563,81 @@ __global__ void k_make_cond(const float* shared, int sd, const int32_t* y, const
 }
 
 // h0[b][(h*4+w)][c] = z[b][0:zc] . W[o] / sigma + bias[o],  o = (h*4+w)*C0 + c
-__global__ void k_glin_fwd(const float* z, int dz, int zc, const float* Wt, const float* sigma, const float* bias,
-                           int B, int C0, int C0p, bf16_t* h0) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (int64_t)B * 16 * C0p) return;
-  const int c = (int)(i % C0p);
-  const int64_t t = i / C0p;
-  const int hw = (int)(t % 16);
-  const int b = (int)(t / 16);
-  float v = 0.f;
-  if (c < C0) {
-    const int o = hw * C0 + c;
-    float s = 0.f;
-    for (int j = 0; j < zc; ++j) s = fmaf(z[(int64_t)b * dz + j], Wt[(int64_t)o * zc + j], s);
-    v = s / *sigma + bias[o];
+// h0[b][hw][c] = z_chunk[b] . W[hw*C0 + c] / sigma + bias (bf16; c >= C0
+// zero).  A block takes 256 consecutive outputs (hw, c) of 16 samples with
+// their weight rows and z chunks staged in LDS (zc <= 32).
+constexpr int kZcMax = 32;
+__global__ __launch_bounds__(256) void k_glin_fwd(const float* z, int dz, int zc, const float* Wt,
+                                                  const float* sigma, const float* bias, int B, int C0, int C0p,
+                                                  bf16_t* h0) {
+  __shared__ float ws[256][kZcMax + 1], zs[16][kZcMax + 1];
+  const int t = threadIdx.x;
+  const int o0 = blockIdx.x * 256, b0 = blockIdx.y * 16;
+  const int nop = 16 * C0p;
+  for (int e = t; e < 256 * zc; e += 256) {
+    const int oo = e / zc, j = e - oo * zc;
+    const int op = o0 + oo, hw = op / C0p, c = op - hw * C0p;
+    ws[oo][j] = op < nop && c < C0 ? Wt[(int64_t)(hw * C0 + c) * zc + j] : 0.f;
   }
-  h0[i] = f2bf(v);
+  for (int e = t; e < 16 * zc; e += 256) {
+    const int bb = e / zc, j = e - bb * zc;
+    zs[bb][j] = b0 + bb < B ? z[(int64_t)(b0 + bb) * dz + j] : 0.f;
+  }
+  __syncthreads();
+  const int op = o0 + t;
+  if (op >= nop) return;
+  const int hw = op / C0p, c = op - hw * C0p;
+  const float sg = *sigma;
+  for (int bb = 0; bb < 16 && b0 + bb < B; ++bb) {
+    float v = 0.f;
+    if (c < C0) {
+      float acc = 0.f;
+      for (int j = 0; j < zc; ++j) acc = fmaf(zs[bb][j], ws[t][j], acc);
+      v = acc / sg + bias[hw * C0 + c];
+    }
+    h0[((int64_t)(b0 + bb) * 16 + hw) * C0p + c] = f2bf(v);
+  }
 }
 
 // dW[o][j] = sum_b dh0[b][o] z[b][j]  (gradient of W/sigma);  dbias[o] = sum_b dh0[b][o]
-__global__ void k_glin_bwd(const bf16_t* dh0, const float* z, int dz, int zc, int B, int C0, int C0p, float* dW,
-                           float* dbias) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t no = 16LL * C0;
-  if (i >= no * (zc + 1)) return;
-  const int64_t o = i / (zc + 1);
-  const int j = (int)(i % (zc + 1));
-  const int hw = (int)(o / C0), c = (int)(o % C0);
-  float s = 0.f;
-  for (int b = 0; b < B; ++b) {
-    const float g = bf2f(dh0[((int64_t)b * 16 + hw) * C0p + c]);
-    s = j < zc ? fmaf(g, z[(int64_t)b * dz + j], s) : s + g;
+// A block takes 64 outputs (one per lane) with 16 waves, wave w summing the
+// samples w, w + 16, ... with all zc + 1 sums in registers; the 16 partial
+// sums then combine in wave order through LDS, one column at a time.
+__global__ __launch_bounds__(1024) void k_glin_bwd(const bf16_t* dh0, const float* z, int dz, int zc, int B, int C0,
+                                                   int C0p, float* dW, float* dbias) {
+  __shared__ float part[16][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int o = blockIdx.x * 64 + lane;
+  const int no = 16 * C0;
+  const bool on = o < no;
+  const int hw = on ? o / C0 : 0, c = on ? o - hw * C0 : 0;
+  float acc[kZcMax + 1];
+#pragma unroll
+  for (int j = 0; j <= kZcMax; ++j) acc[j] = 0.f;
+  if (on)
+    for (int b = wv; b < B; b += 16) {
+      const float g = bf2f(dh0[((int64_t)b * 16 + hw) * C0p + c]);
+      const float* zb = z + (int64_t)b * dz;
+#pragma unroll
+      for (int j = 0; j < kZcMax; ++j)
+        if (j < zc) acc[j] = fmaf(g, zb[j], acc[j]);
+      acc[kZcMax] += g;
+    }
+  for (int j = 0; j <= zc; ++j) {
+    float v = 0.f;
+#pragma unroll
+    for (int jj = 0; jj <= kZcMax; ++jj)
+      if (jj == (j == zc ? kZcMax : j)) v = acc[jj];
+    __syncthreads();
+    part[wv][lane] = v;
+    __syncthreads();
+    if (wv == 0 && on) {
+      float t = 0.f;
+      for (int i = 0; i < 16; ++i) t += part[i][lane];
+      if (j < zc) dW[(int64_t)o * zc + j] = t;
+      else dbias[o] = t;
+    }
   }
-  if (j < zc) dW[o * zc + j] = s;
-  else dbias[o] = s;
 }
 
 // dshared[k][d] = sum_{b: y_b = k} dcond[b][d]   (d < sd)
@@ -594,15 +661,17 @@ void make_cond(hipStream_t st, const float* shared, int sd, const int32_t* y, co
 
 void glin_fwd(hipStream_t st, const float* z, int dz, int zc, const float* Wt, const float* sigma,
               const float* bias, int B, int C0, int C0p, void* h0) {
-  hipLaunchKernelGGL(k_glin_fwd, dim3((unsigned)cdiv((int64_t)B * 16 * C0p, 256)), dim3(256), 0, st, z, dz, zc, Wt,
-                     sigma, bias, B, C0, C0p, (bf16_t*)h0);
+  PG_CHECK(zc >= 1 && zc <= kZcMax && (int64_t)B * 16 * C0p < (1LL << 31), "glin: z chunk of 1..32");
+  hipLaunchKernelGGL(k_glin_fwd, dim3((unsigned)cdiv(16LL * C0p, 256), (unsigned)cdiv(B, 16)), dim3(256), 0, st, z, dz,
+                     zc, Wt, sigma, bias, B, C0, C0p, (bf16_t*)h0);
   PG_LAUNCH_CHECK();
 }
 
 void glin_bwd(hipStream_t st, const void* dh0, const float* z, int dz, int zc, int B, int C0, int C0p, float* dW,
               float* dbias) {
-  hipLaunchKernelGGL(k_glin_bwd, dim3((unsigned)cdiv(16LL * C0 * (zc + 1), 256)), dim3(256), 0, st,
-                     (const bf16_t*)dh0, z, dz, zc, B, C0, C0p, dW, dbias);
+  PG_CHECK(zc >= 1 && zc <= kZcMax, "glin: z chunk of 1..32");
+  hipLaunchKernelGGL(k_glin_bwd, dim3((unsigned)cdiv(16LL * C0, 64)), dim3(1024), 0, st, (const bf16_t*)dh0, z, dz,
+                     zc, B, C0, C0p, dW, dbias);
   PG_LAUNCH_CHECK();
 }
 
