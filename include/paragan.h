@@ -191,6 +191,41 @@ int paragan_attn_bwd(paragan_ctx* ctx, const paragan_attn_desc* d,
                      const void* dy, void* dx, float* grads, void* ws);
 
 /* ---------------------------------------------------------------------
+ * Generator output layer (the last generator layer of the model,
+ * Evaluation "Experiment Setup"; kept in fp32 arithmetic by the paper's
+ * mixed-precision placement, Design "System Optimizations"):
+ *   a = ReLU(gain * BN(x) + bias)   (batch statistics over B, H, W),
+ *   img = tanh(conv3x3(a, W / sigma(W)) + b)   (3 output channels),
+ * with SN on W.  x: bf16 [B][H][W][cpad(C)]; img: fp32 [B][H][W][3].
+ * Shapes: cpad(C) <= 128 and W a multiple of 4 (paragan_gout_check says
+ * whether W also fits the weight-gradient tile; every W up to 704 does).
+ * Parameters: out_bn.gain out_bn.bias out_conv.w out_conv.b.
+ * ------------------------------------------------------------------- */
+typedef struct {
+  int32_t B, H, W, C;
+  int32_t n_power_iter;
+  float bn_eps, sn_eps;
+} paragan_gout_desc;
+
+int paragan_gout_layout(const paragan_gout_desc* d, paragan_tensor_info* out,
+                        int32_t cap, int32_t* count, int64_t* n_params,
+                        int64_t* n_u);
+int paragan_gout_sizes(const paragan_gout_desc* d, size_t* saved_bytes,
+                       size_t* ws_bytes);
+int paragan_gout_check(const paragan_gout_desc* d);
+/* Training forward: updates u, writes img and `saved` (read by bwd). */
+int paragan_gout_fwd(paragan_ctx* ctx, const paragan_gout_desc* d,
+                     const float* params, float* u, const void* x, float* img,
+                     void* saved, void* ws);
+/* Backward from dimg (fp32 [B][H][W][3]); img is this layer's forward
+ * output.  Writes dx (bf16, x's shape) and grads (flat, parameter layout;
+ * overwritten). */
+int paragan_gout_bwd(paragan_ctx* ctx, const paragan_gout_desc* d,
+                     const float* params, const void* x, const float* img,
+                     const void* saved, const float* dimg, void* dx,
+                     float* grads, void* ws);
+
+/* ---------------------------------------------------------------------
  * Full BigGAN G+D train step.  The architecture is given by channel
  * multipliers (BigGAN-128: ch 96, G 16,16,8,4,2,1, D 1,2,4,8,16,16 with the
  * last D block not pooling, attention at 64x64, 1000 classes, z 120 split

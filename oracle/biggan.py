@@ -168,6 +168,38 @@ def _put(dst, prefix, src):
 # --------------------------------------------------------------------------
 # generator
 # --------------------------------------------------------------------------
+def g_out_fwd(x5, p, u, cfg, bn_eps):
+    """Generator output layer, fp32 (model: Architecture; the last layer in
+    full precision: Design, "System Optimizations"): BN with batch
+    statistics and an affine gain / bias -> ReLU -> SN conv3x3 to 3 channels
+    (+ bias) -> tanh.  Reads out_bn.gain, out_bn.bias, out_conv.w and
+    out_conv.b of p.  Returns the image, the new u of out_conv.w and the
+    cache for g_out_bwd."""
+    bn, cbn = L.cbn_fwd(x5, p["out_bn.gain"][None, :], p["out_bn.bias"][None, :],
+                        bn_eps)
+    act = L.relu(bn)
+    wo, sto = spectral(p, u, "out_conv.w", cfg)
+    img = np.tanh(L.conv2d(act, wo, p["out_conv.b"]))
+    return img, sto[0], dict(bn=bn, cbn=cbn, act=act, wo=wo, sto=sto, img=img)
+
+
+def g_out_bwd(dimg, c):
+    """dimg (N, H, W, 3) -> (gradient of the layer's input, gradients of its
+    four parameters)."""
+    grads = {}
+    dt = dimg * (1.0 - c["img"] ** 2)
+    dwo = L.conv2d_wgrad(dt, c["act"], 3)
+    grads["out_conv.b"] = L.bias_grad(dt)
+    un, v, s = c["sto"]
+    grads["out_conv.w"] = L.sn_bwd(dwo, c["wo"], un, v, s)
+    dact = L.conv2d_dgrad(dt, c["wo"])
+    dbn = dact * (c["bn"] > 0)
+    dh, dgain, dbias = L.cbn_bwd(dbn, c["cbn"])
+    grads["out_bn.gain"] = dgain[0]
+    grads["out_bn.bias"] = dbias[0]
+    return dh, grads
+
+
 def g_fwd(a, hp, p, u, z, y):
     """z (N, dz), y (N,) int -> image (N, img, img, 3) in [-1, 1]."""
     R = rounder(hp.bf16)
@@ -197,15 +229,8 @@ def g_fwd(a, hp, p, u, z, y):
             _put(u_new, "attn.", ua)
             caches.append(("a", ca))
     # output layer, fp32
-    x5 = h
-    bn, cbn = L.cbn_fwd(x5, p["out_bn.gain"][None, :], p["out_bn.bias"][None, :],
-                        hp.bn_eps)
-    act = L.relu(bn)
-    wo, sto = spectral(p, u, "out_conv.w", cfg)
-    u_new["out_conv.w"] = sto[0]
-    img = np.tanh(L.conv2d(act, wo, p["out_conv.b"]))
-    cache = dict(zs=zs, y=y, emb=emb, wl=wl, stl=stl, caches=caches, bn=bn,
-                 cbn=cbn, act=act, wo=wo, sto=sto, img=img)
+    img, u_new["out_conv.w"], hc = g_out_fwd(h, p, u, cfg, hp.bn_eps)
+    cache = dict(zs=zs, y=y, emb=emb, wl=wl, stl=stl, caches=caches, **hc)
     return img, u_new, cache
 
 
@@ -214,17 +239,7 @@ def g_bwd(a, hp, p, dimg, cache):
     R = rounder(hp.bf16)
     cfg = hp.block()
     c = cache
-    grads = {}
-    dt = dimg * (1.0 - c["img"] ** 2)
-    dwo = L.conv2d_wgrad(dt, c["act"], 3)
-    grads["out_conv.b"] = L.bias_grad(dt)
-    un, v, s = c["sto"]
-    grads["out_conv.w"] = L.sn_bwd(dwo, c["wo"], un, v, s)
-    dact = L.conv2d_dgrad(dt, c["wo"])
-    dbn = dact * (c["bn"] > 0)
-    dh, dgain, dbias = L.cbn_bwd(dbn, c["cbn"])
-    grads["out_bn.gain"] = dgain[0]
-    grads["out_bn.bias"] = dbias[0]
+    dh, grads = g_out_bwd(dimg, c)
     dh = R(dh)
     n = dimg.shape[0]
     demb = np.zeros((n, a.shared_dim))

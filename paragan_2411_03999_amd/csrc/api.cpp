@@ -392,6 +392,82 @@ extern "C" int paragan_attn_bwd(paragan_ctx* ctx, const paragan_attn_desc* d, co
   })
 }
 
+// ------------------------------------------------------------ generator output layer
+static void ocheck(const paragan_gout_desc* d) {
+  if (!d) throw Error{PARAGAN_EINVAL, "gout: desc is NULL"};
+  PG_CHECK(d->B >= 1 && d->H >= 1 && d->W >= 1 && d->C >= 1, "gout: B, H, W, C >= 1");
+  PG_CHECK(ghead_shape_ok(d->W, d->C), "gout: needs cpad(C) <= 128, W a multiple of 4 and W small enough for the "
+                                       "weight-gradient tile");
+  PG_CHECK(d->n_power_iter >= 1 && d->bn_eps > 0.f && d->sn_eps > 0.f, "gout: bad n_power_iter / eps");
+  PG_CHECK((int64_t)d->B * d->H * d->W < (1LL << 31), "gout: too many pixels");
+}
+
+static GOut make_o(const paragan_gout_desc* d) {
+  GOut g;
+  g.B = d->B; g.H = d->H; g.W = d->W; g.C = d->C; g.npi = d->n_power_iter;
+  g.bn_eps = d->bn_eps; g.sn_eps = d->sn_eps;
+  return g;
+}
+
+extern "C" int paragan_gout_check(const paragan_gout_desc* d) { PG_TRY(nullptr, ocheck(d)) }
+
+extern "C" int paragan_gout_layout(const paragan_gout_desc* d, paragan_tensor_info* out, int32_t cap,
+                                   int32_t* count, int64_t* n_params, int64_t* n_u) {
+  try {
+    ocheck(d);
+    return export_layout(gout_layout(d->C), out, cap, count, n_params, n_u);
+  } catch (const Error& e) {
+    return fail(nullptr, e.code, e.msg);
+  }
+}
+
+extern "C" int paragan_gout_sizes(const paragan_gout_desc* d, size_t* saved, size_t* ws) {
+  PG_TRY(nullptr, {
+    ocheck(d);
+    GOut g = make_o(d);
+    Arena a(nullptr);
+    g.plan_saved(a);
+    if (saved) *saved = a.off;
+    if (ws) *ws = g.ws_size();
+  })
+}
+
+extern "C" int paragan_gout_fwd(paragan_ctx* ctx, const paragan_gout_desc* d, const float* params, float* u,
+                                const void* x, float* img, void* saved, void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
+  PG_TRY(ctx, {
+    ocheck(d);
+    need(params, "params"); need(u, "u"); need(x, "x"); need(img, "img"); need(saved, "saved"); need(ws, "ws");
+    aligned(saved, "saved"); aligned(ws, "ws");
+    GOut g = make_o(d);
+    Arena a(saved);
+    g.plan_saved(a);
+    Layout L = gout_layout(d->C);
+    Params P{&L, "", params, u, nullptr};
+    g.fwd(Exec{ctx->stream, ctx->n_cu, ws, g.ws_size()}, P, x, img);
+  })
+}
+
+extern "C" int paragan_gout_bwd(paragan_ctx* ctx, const paragan_gout_desc* d, const float* params, const void* x,
+                                const float* img, const void* saved, const float* dimg, void* dx, float* grads,
+                                void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
+  PG_TRY(ctx, {
+    ocheck(d);
+    need(params, "params"); need(x, "x"); need(img, "img"); need(saved, "saved"); need(dimg, "dimg");
+    need(dx, "dx"); need(grads, "grads"); need(ws, "ws");
+    aligned(saved, "saved"); aligned(ws, "ws");
+    GOut g = make_o(d);
+    Arena a((void*)saved);
+    g.plan_saved(a);
+    Layout L = gout_layout(d->C);
+    Params P{&L, "", params, nullptr, grads};
+    g.bwd(Exec{ctx->stream, ctx->n_cu, ws, g.ws_size()}, P, x, img, dimg, 3, dx);
+  })
+}
+
 // ------------------------------------------------------------ networks, step
 extern "C" int paragan_biggan_check(const paragan_biggan_desc* d) { PG_TRY(nullptr, check_arch(d)) }
 

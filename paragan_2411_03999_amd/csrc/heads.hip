@@ -32,120 +32,137 @@ void img_to_bf16(hipStream_t st, const float* img, int64_t npix, int Cp, void* o
 }
 
 // --------------------------------------------------- generator output layer
-// a = relu((x - mean) * scale + shift) (per channel), img = tanh(conv3x3(a) / sigma + b),
-// all in fp32 on the vector ALUs (three output channels leave nothing for a
-// matrix unit to tile).  A block computes a 16-row x 64-column output tile:
-// per chunk of 8 channels it stages the haloed input tile, normalised once
-// per element, in LDS as [row][channel][column]; each lane then owns one
-// column of a 4-row strip (its wave's rows), so every staged value it reads
-// feeds up to 4 pixels x 3 outputs.  Weights sit in LDS as [c][27] and are
-// read as wave-wide broadcasts.
-constexpr int kFR = 16;   // output rows per block (4 waves x 4-row strips)
-constexpr int kFC = 64;   // output columns per block (one per lane)
-constexpr int kFK = 8;    // channels per staged chunk
+// a = relu((x - mean) * scale + shift) per channel; img = tanh(conv3x3(a) / sigma + b).
+// Forward and weight gradient run on the fp32 matrix cores
+// (v_mfma_f32_32x32x2_f32: fp32 operands and accumulation, so the last layer
+// keeps full precision).  The 27 filter columns n = co * 9 + r * 3 + s (27 of
+// a 32-wide tile) are the N side of both products; the 3x3 window turns into
+// 9-term gathers around them.
+constexpr int kHR = 16;     // output rows per forward block
+constexpr int kZS = 33;     // LDS floats per Z position (odd: conflict-free gathers)
+constexpr int kZP = 130;    // Z positions per ring row: 128 output columns + 2 halo
 
-__global__ __launch_bounds__(256) void k_ghead_fwd(const bf16_t* __restrict__ x, int B, int H, int W, int C, int Cp,
-                                                   const float* __restrict__ mean, const float* __restrict__ scale,
-                                                   const float* __restrict__ shift, const float* __restrict__ Wt,
-                                                   const float* __restrict__ sigma, const float* __restrict__ bias,
-                                                   float* __restrict__ img) {
-  __shared__ float L[kFR + 2][kFK][kFC + 2];
-  extern __shared__ float4 wsh4[];     // [C][7] float4: the 27 weights of channel c, then padding
-  float* wsh = reinterpret_cast<float*>(wsh4);
-  for (int i = threadIdx.x; i < 28 * C; i += 256) {
-    const int c = i / 28, k = i - c * 28;
-    wsh[i] = k < 27 ? Wt[k * C + c] : 0.f;
+PG_DEV f32x16 mfma_f32(float a, float b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+// output columns per forward block: whole rows up to 128, else 126 (so the
+// Z columns of a block, its columns plus a halo, fit four 32-position tiles)
+static int ghead_cols(int W) { return W <= 128 ? W : 126; }
+
+// Forward.  Z[q][n] = sum_c a[q][c] W[n][c] for every input position q (K =
+// the channels, each input value read once), then img[p][co] = tanh(sum_{r,s}
+// Z[p + (r - 1, s - 1)][co * 9 + r * 3 + s] / sigma + b[co]).  A block takes
+// kHR output rows x ghead_cols(W) output columns of one image and walks its Z
+// rows top to bottom: each of the 4 waves computes one 32-position tile of a
+// Z row into a 3-row LDS ring (rows outside the image are never read), then
+// the block gathers the output row whose three Z rows are present.  A wave
+// loads its x values for the next Z row before the current row's products.
+// A lane of the product holds position l % 32 and channels 16 j + 8 (l / 32)
+// + 0..7 of chunk j: one 16-byte load feeds 8 products.
+template <int CK>   // CK = Cp / 16
+__global__ __launch_bounds__(256, 2) void k_ghead_fwd(const bf16_t* __restrict__ x, int H, int W, int C, int TC,
+                                                      const float* __restrict__ mean, const float* __restrict__ scale,
+                                                      const float* __restrict__ shift, const float* __restrict__ Wt,
+                                                      const float* __restrict__ sigma, const float* __restrict__ bias,
+                                                      float* __restrict__ img) {
+  constexpr int Cp = 16 * CK;
+  __shared__ float Zs[3][kZP][kZS];
+  __shared__ float Wl[CK * 512];          // [j][k][s][n] = W[n][16 j + 8 k + s], zero for n >= 27, c >= C
+  __shared__ float4 cst[3][Cp / 4];       // mean, scale, shift (zero for padded channels)
+  const int tid = threadIdx.x, lane = tid & 63, kh = lane >> 5, ln = lane & 31;
+  const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  for (int i = tid; i < CK * 512; i += 256) {
+    const int n = i & 31, s = (i >> 5) & 7, k = (i >> 8) & 1, j = i >> 9;
+    const int c = 16 * j + 8 * k + s;
+    Wl[i] = n < 27 && c < C ? Wt[n * C + c] : 0.f;
   }
-  const int tiles_w = (W + kFC - 1) / kFC, tiles_h = (H + kFR - 1) / kFR;
+  for (int c = tid; c < Cp; c += 256) {
+    const bool ok = c < C;
+    reinterpret_cast<float*>(cst[0])[c] = ok ? mean[c] : 0.f;
+    reinterpret_cast<float*>(cst[1])[c] = ok ? scale[c] : 0.f;
+    reinterpret_cast<float*>(cst[2])[c] = ok ? shift[c] : 0.f;
+  }
+  const int ncb = (W + TC - 1) / TC, nrb = (H + kHR - 1) / kHR;
   int bid = blockIdx.x;
-  const int tw = bid % tiles_w;
-  bid /= tiles_w;
-  const int th = bid % tiles_h;
-  const int b = bid / tiles_h;
-  const int h0 = th * kFR, w0 = tw * kFC;
-  const int t = threadIdx.x, tx = t & 63;
-  const int ty = __builtin_amdgcn_readfirstlane(t >> 6);
-  float acc[4][3];
+  const int cb = bid % ncb;
+  bid /= ncb;
+  const int rb = bid % nrb;
+  const int b = bid / nrb;
+  const int w0 = cb * TC, h0 = rb * kHR;
+  const int w1 = min(W, w0 + TC), h1 = min(H, h0 + kHR);
+  const int zc0 = max(0, w0 - 1), zc1 = min(W, w1 + 1);   // Z columns the block needs
+  const bool has_tile = 32 * wv < zc1 - zc0;
+  const int zw = zc0 + 32 * wv + ln;                        // this lane's Z column
+  const bool col_ok = zw < zc1;
+  uint4 xr[CK];
+  auto fetch = [&](int zr) {
+    const bool ok = col_ok && zr >= 0 && zr < H;
+    const int64_t off = ok ? (((int64_t)b * H + zr) * W + zw) * Cp + 8 * kh : 0;
 #pragma unroll
-  for (int o = 0; o < 4; ++o) acc[o][0] = acc[o][1] = acc[o][2] = 0.f;
-  // The haloed tile's raw 8-channel vectors of the next chunk are fetched
-  // into registers before the current chunk is computed, so their latency
-  // hides behind the FMAs; staging normalises them into LDS.
-  constexpr int kNP = ((kFR + 2) * (kFC + 2) + 255) / 256;   // tile positions per thread
-  uint4 raw[kNP];
-  uint32_t inside = 0;   // bit j: position j lies inside the image
-#pragma unroll
-  for (int j = 0; j < kNP; ++j) {
-    const int idx = t + 256 * j;
-    const int r = idx / (kFC + 2), col = idx - r * (kFC + 2);
-    const int ih = h0 + r - 1, iw = w0 + col - 1;
-    if (idx < (kFR + 2) * (kFC + 2) && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W) inside |= 1u << j;
-  }
-  auto fetch = [&](int c0) {
-#pragma unroll
-    for (int j = 0; j < kNP; ++j) {
-      const int idx = t + 256 * j;
-      const int r = idx / (kFC + 2), col = idx - r * (kFC + 2);
-      raw[j] = (inside >> j) & 1
-                   ? *reinterpret_cast<const uint4*>(x + (((int64_t)b * H + h0 + r - 1) * W + w0 + col - 1) * Cp + c0)
-                   : make_uint4(0u, 0u, 0u, 0u);
-    }
+    for (int j = 0; j < CK; ++j)
+      xr[j] = ok ? *reinterpret_cast<const uint4*>(x + off + 16 * j) : make_uint4(0u, 0u, 0u, 0u);
   };
-  fetch(0);
-  for (int c0 = 0; c0 < C; c0 += kFK) {
-    __syncthreads();
+  const float inv = 1.f / *sigma;
+  const int nz = h1 - h0 + 2;   // Z rows h0 - 1 .. h1
+  fetch(h0 - 1);
+  __syncthreads();
+  for (int t = 0; t < nz; ++t) {
+    const int zr = h0 - 1 + t;
+    uint4 cur[CK];
 #pragma unroll
-    for (int j = 0; j < kNP; ++j) {
-      const int idx = t + 256 * j;
-      if (idx >= (kFR + 2) * (kFC + 2)) break;
-      const int r = idx / (kFC + 2), col = idx - r * (kFC + 2);
-      float v[8];
-      unpack8(raw[j], v);
+    for (int j = 0; j < CK; ++j) cur[j] = xr[j];
+    if (t + 1 < nz) fetch(zr + 1);
+    if (has_tile && zr >= 0 && zr < H) {
+      f32x16 acc;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int c = c0 + e;
-        v[e] = ((inside >> j) & 1) && c < C ? fmaxf((v[e] - mean[c]) * scale[c] + shift[c], 0.f) : 0.f;
+      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+      for (int j = 0; j < CK; ++j) {
+        float v[8];
+        unpack8(cur[j], v);
+        const int q4 = 4 * j + 2 * kh;   // float4 index of channel 16 j + 8 kh
+        const float4 m0 = cst[0][q4], m1 = cst[0][q4 + 1];
+        const float4 s0 = cst[1][q4], s1 = cst[1][q4 + 1];
+        const float4 f0 = cst[2][q4], f1 = cst[2][q4 + 1];
+        const float mu[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
+        const float sc[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        const float sh[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+          const float a = col_ok ? fmaxf((v[s] - mu[s]) * sc[s] + sh[s], 0.f) : 0.f;
+          acc = mfma_f32(a, Wl[((2 * j + kh) * 8 + s) * 32 + ln], acc);
+        }
       }
+      // lane: Z[position row 8 (r / 4) + 4 kh + r % 4 of the tile][n = ln]
+      float* zs = &Zs[t % 3][0][0];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) L[r][e][col] = v[e];
+      for (int r = 0; r < 16; ++r) {
+        const int w = zc0 + 32 * wv + 8 * (r >> 2) + 4 * kh + (r & 3);
+        if (w < zc1) zs[(w - w0 + 1) * kZS + ln] = acc[r];
+      }
     }
-    __syncthreads();
-    if (c0 + kFK < C) fetch(c0 + kFK);
-    const int nk = min(kFK, C - c0);
+    if (t >= 2) {
+      // output row oh = zr - 1: its Z rows oh - 1 .. oh + 1 sit in ring slots (t - 2 .. t) % 3
+      __syncthreads();
+      const int oh = zr - 1, ncol = w1 - w0;
+      for (int it = tid; it < 3 * ncol; it += 256) {
+        const int co = it / ncol, pc = it - co * ncol;
+        const int ow = w0 + pc;
+        float sum = 0.f;
 #pragma unroll
-    for (int cc = 0; cc < kFK; ++cc) {
-      if (cc >= nk) break;
-      float w[28];
+        for (int r = 0; r < 3; ++r) {
+          const int ih = oh - 1 + r;
+          if ((unsigned)ih >= (unsigned)H) continue;
+          const float* zs = &Zs[(t - 2 + r) % 3][0][0];
 #pragma unroll
-      for (int q = 0; q < 7; ++q) {
-        const float4 f = wsh4[(c0 + cc) * 7 + q];
-        w[4 * q] = f.x; w[4 * q + 1] = f.y; w[4 * q + 2] = f.z; w[4 * q + 3] = f.w;
-      }
-#pragma unroll
-      for (int rr = 0; rr < 6; ++rr)
-#pragma unroll
-        for (int s_ = 0; s_ < 3; ++s_) {
-          const float v = L[4 * ty + rr][cc][tx + s_];
-#pragma unroll
-          for (int o = 0; o < 4; ++o) {
-            const int r = rr - o;
-            if (r >= 0 && r <= 2) {
-#pragma unroll
-              for (int co = 0; co < 3; ++co) acc[o][co] = fmaf(v, w[co * 9 + r * 3 + s_], acc[o][co]);
-            }
+          for (int s = 0; s < 3; ++s) {
+            const int iw = ow - 1 + s;
+            if ((unsigned)iw < (unsigned)W) sum += zs[(iw - w0 + 1) * kZS + co * 9 + r * 3 + s];
           }
         }
-    }
-  }
-  const float inv = 1.f / *sigma;
-  const int ow = w0 + tx;
-#pragma unroll
-  for (int o = 0; o < 4; ++o) {
-    const int oh = h0 + 4 * ty + o;
-    if (oh < H && ow < W) {
-      const int64_t q = (((int64_t)b * H + oh) * W + ow) * 3;
-#pragma unroll
-      for (int co = 0; co < 3; ++co) img[q + co] = tanhf(acc[o][co] * inv + bias[co]);
+        img[(((int64_t)b * H + oh) * W + ow) * 3 + co] = tanhf(sum * inv + bias[co]);
+      }
+      __syncthreads();
     }
   }
 }
@@ -237,129 +254,170 @@ __global__ __launch_bounds__(256) void k_ghead_dgrad(const float* __restrict__ d
 }
 
 // Weight gradient of the output layer:
-//   dW[co][r][s][c] = sum_p dt[p][co] a[p + (r - 1, s - 1)][c],  db[co] = sum_p dt[p][co],
-// with a = relu(bn(x)) recomputed from x and dt = dimg (1 - img^2).  A
-// block takes kWR output rows of one image; a thread owns 4 channels and
-// walks whole rows (rows strip, strip + S, ... of the block), sliding a
-// 3x3 window of a (4 channels per position) in registers: one new column
-// of 3 loads per pixel feeds 108 FMAs.  The S strips then combine in a
-// fixed order through LDS, one output channel at a time, into the block's
+//   dW[co][r][s][c] = sum_p dt[p][co] a[p + (r - 1, s - 1)][c] = sum_q a[q][c] G[q][n],
+//   G[q][co * 9 + r * 3 + s] = dt[q - (r - 1, s - 1)][co],  db[co] = sum_p dt[p][co],
+// with a = relu(bn(x)) recomputed from x and dt = dimg (1 - img^2): the
+// positions q are the K side of a (C x 32) product on the fp32 matrix cores.
+// A block takes ghead_wrows(W) rows of one image.  dt of those rows plus a
+// one-pixel zero frame is staged in LDS, so the 27 columns of G are plain
+// reads from it; each wave takes 16-position chunks of a, normalised once
+// into its LDS tile [position][channel] (the channel is the M side of the
+// product).  The 4 waves' sums combine in wave order into the block's
 // partial; blocks are summed in order by k_ghead_fin.
-constexpr int kWR = 16;    // output rows per block
+constexpr int kWC = 16;   // positions per wave chunk
+constexpr size_t kWgLds = 64 * 1024;
+static size_t ghead_lds_at(int tr, int W, int Cp) {
+  return ((size_t)(tr + 2) * (W + 2) * 3 + 3) / 4 * 16 + (size_t)4 * kWC * (Cp + 4) * 4 + 3 * (size_t)Cp * 4 + 768 * 4;
+}
+// rows per weight-gradient block: about 2048 positions, fewer if the LDS tile would not fit
+static int ghead_wrows(int W, int Cp) {
+  int tr = std::max(1, std::min(16, 2048 / W));
+  while (tr > 1 && ghead_lds_at(tr, W, Cp) > kWgLds) --tr;
+  return tr;
+}
+static size_t ghead_wgrad_lds(int W, int Cp) { return ghead_lds_at(ghead_wrows(W, Cp), W, Cp); }
 
-__global__ __launch_bounds__(256) void k_ghead_wgrad(const float* __restrict__ dimg, int ldd,
-                                                     const float* __restrict__ img, const bf16_t* __restrict__ x,
-                                                     int B, int H, int W, int C, int Cp,
-                                                     const float* __restrict__ mean, const float* __restrict__ scale,
-                                                     const float* __restrict__ shift, float* __restrict__ part) {
-  extern __shared__ float red[];      // [S][9 * Cp] strip partials of one output channel
-  const int ncg = Cp >> 2;
-  const int S = 256 / ncg;            // strips (threads beyond S * ncg idle)
-  const int tiles_h = (H + kWR - 1) / kWR;
-  const int b = blockIdx.x / tiles_h, h0 = (blockIdx.x % tiles_h) * kWR;
-  const int h1 = min(H, h0 + kWR);
-  const int t = threadIdx.x;
-  const int cg = t % ncg, strip = t / ncg;
-  const bool active = strip < S;
-  const int c = 4 * cg;
-  float mu[4], sc[4], sh[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const bool ok = active && c + e < C;
-    mu[e] = ok ? mean[c + e] : 0.f;
-    sc[e] = ok ? scale[c + e] : 0.f;   // zero scale and shift: a = 0 for padded channels
-    sh[e] = ok ? shift[c + e] : 0.f;
+bool ghead_shape_ok(int W, int C) {
+  const int Cp = (int)cpad(C);
+  return C >= 1 && Cp <= 128 && W >= 4 && W % 4 == 0 && ghead_wgrad_lds(W, Cp) <= kWgLds;
+}
+
+template <int CT>   // CT = Cp / 32
+__global__ __launch_bounds__(256, 2) void k_ghead_wgrad(const float* __restrict__ dimg, int ldd,
+                                                        const float* __restrict__ img, const bf16_t* __restrict__ x,
+                                                        int H, int W, int C, int TRW,
+                                                        const float* __restrict__ mean, const float* __restrict__ scale,
+                                                        const float* __restrict__ shift, float* __restrict__ part) {
+  constexpr int Cp = 32 * CT, AS = Cp + 4;
+  extern __shared__ float4 sm4[];
+  const int W2 = W + 2;
+  float* const dts = reinterpret_cast<float*>(sm4);                  // [(rows + 2) * W2][3]
+  float* const As = dts + ((TRW + 2) * W2 * 3 + 3) / 4 * 4;         // [4][kWC][AS]
+  float* const cst = As + 4 * kWC * AS;                              // [3][Cp]
+  float* const sb = cst + 3 * Cp;                                    // [256][3] bias partials
+  const int nrb = (H + TRW - 1) / TRW;
+  const int b = blockIdx.x / nrb, h0 = (blockIdx.x % nrb) * TRW;
+  const int nr = min(TRW, H - h0);
+  const int tid = threadIdx.x, lane = tid & 63, kh = lane >> 5, ln = lane & 31;
+  const int wv = tid >> 6;
+  for (int c = tid; c < Cp; c += 256) {
+    const bool ok = c < C;
+    cst[c] = ok ? mean[c] : 0.f;
+    cst[Cp + c] = ok ? scale[c] : 0.f;
+    cst[2 * Cp + c] = ok ? shift[c] : 0.f;
   }
-  float acc[3][9][4];
+  float bs[3] = {0.f, 0.f, 0.f};
+  for (int i = tid; i < (nr + 2) * W2; i += 256) {
+    const int rr = i / W2, cc = i - rr * W2;
+    const int h = h0 - 1 + rr, w = cc - 1;
+    float d[3] = {0.f, 0.f, 0.f};
+    if ((unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W) {
+      const int64_t q = ((int64_t)b * H + h) * W + w;
 #pragma unroll
-  for (int co = 0; co < 3; ++co)
-#pragma unroll
-    for (int k = 0; k < 9; ++k)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) acc[co][k][e] = 0.f;
-  float bsum[3] = {0.f, 0.f, 0.f};
-  // a at (row, col) for this thread's 4 channels (zero outside the image)
-  auto load_a = [&](int row, int col, float* v) {
-    if ((unsigned)row < (unsigned)H && (unsigned)col < (unsigned)W) {
-      const uint2 q = *reinterpret_cast<const uint2*>(x + (((int64_t)b * H + row) * W + col) * Cp + c);
-      const float f[4] = {__uint_as_float(q.x << 16), __uint_as_float(q.x & 0xffff0000u),
-                          __uint_as_float(q.y << 16), __uint_as_float(q.y & 0xffff0000u)};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = fmaxf((f[e] - mu[e]) * sc[e] + sh[e], 0.f);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) v[e] = 0.f;
-    }
-  };
-  if (active) {
-    for (int h = h0 + strip; h < h1; h += S) {
-      // window columns w-1, w, w+1 of rows h-1, h, h+1
-      float win[3][3][4];
-#pragma unroll
-      for (int r = 0; r < 3; ++r) {
-        load_a(h + r - 1, -1, win[r][0]);
-        load_a(h + r - 1, 0, win[r][1]);
+      for (int co = 0; co < 3; ++co) {
+        const float y = img[q * 3 + co];
+        d[co] = dimg[q * ldd + co] * (1.f - y * y);
       }
-      for (int w = 0; w < W; ++w) {
+      if (rr >= 1 && rr <= nr) {
 #pragma unroll
-        for (int r = 0; r < 3; ++r) load_a(h + r - 1, w + 1, win[r][2]);
-        const int64_t q = ((int64_t)b * H + h) * W + w;
-        float dt[3];
+        for (int co = 0; co < 3; ++co) bs[co] += d[co];
+      }
+    }
 #pragma unroll
-        for (int co = 0; co < 3; ++co) {
-          const float y = img[q * 3 + co];
-          dt[co] = dimg[q * ldd + co] * (1.f - y * y);
-          bsum[co] += dt[co];
+    for (int co = 0; co < 3; ++co) dts[3 * i + co] = d[co];
+  }
+  // G column of this lane: dts offset relative to ((h - h0) * W2 + w) * 3
+  const bool nok = ln < 27;
+  const int co_n = ln / 9, tap = ln - 9 * co_n, tr = tap / 3, ts = tap - 3 * tr;
+  const int boff = ((2 - tr) * W2 + (2 - ts)) * 3 + co_n;
+  // staging role: position si of the chunk, channels 32 j + 8 sq + 0..7
+  const int si = lane & 15, sq = lane >> 4;
+  const int P = nr * W;
+  const int nch = (P + kWC - 1) / kWC, iters = (nch + 3) / 4;
+  uint4 xr[CT];
+  auto fetch = [&](int k) {
+    const int p = k * kWC + si;
+    const bool ok = k < nch && p < P;
+    int64_t off = 0;
+    if (ok) {
+      const int h = p / W;
+      off = (((int64_t)b * H + h0 + h) * W + (p - h * W)) * Cp + 8 * sq;
+    }
+#pragma unroll
+    for (int j = 0; j < CT; ++j)
+      xr[j] = ok ? *reinterpret_cast<const uint4*>(x + off + 32 * j) : make_uint4(0u, 0u, 0u, 0u);
+  };
+  f32x16 acc[CT];
+#pragma unroll
+  for (int ct = 0; ct < CT; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[ct][r] = 0.f;
+  fetch(wv);
+  __syncthreads();
+  float* const as = As + wv * kWC * AS;
+  for (int it = 0; it < iters; ++it) {
+    const int k = wv + 4 * it;
+    {
+      const int p = k * kWC + si;
+      const bool ok = k < nch && p < P;
+#pragma unroll
+      for (int j = 0; j < CT; ++j) {
+        float v[8];
+        unpack8(xr[j], v);
+        const int c0 = 32 * j + 8 * sq;
+        float a[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          a[e] = ok ? fmaxf((v[e] - cst[c0 + e]) * cst[Cp + c0 + e] + cst[2 * Cp + c0 + e], 0.f) : 0.f;
+        *reinterpret_cast<float4*>(as + si * AS + c0) = make_float4(a[0], a[1], a[2], a[3]);
+        *reinterpret_cast<float4*>(as + si * AS + c0 + 4) = make_float4(a[4], a[5], a[6], a[7]);
+      }
+    }
+    if (it + 1 < iters) fetch(k + 4);
+    __syncthreads();
+    if (k < nch) {
+#pragma unroll
+      for (int s = 0; s < kWC / 2; ++s) {
+        const int pl = 2 * s + kh, p = k * kWC + pl;
+        float bv = 0.f;
+        if (nok && p < P) {
+          const int h = p / W;
+          bv = dts[(h * W2 + (p - h * W)) * 3 + boff];
         }
 #pragma unroll
-        for (int co = 0; co < 3; ++co)
-#pragma unroll
-          for (int r = 0; r < 3; ++r)
-#pragma unroll
-            for (int s_ = 0; s_ < 3; ++s_)
-#pragma unroll
-              for (int e = 0; e < 4; ++e)
-                acc[co][r * 3 + s_][e] = fmaf(dt[co], win[r][s_][e], acc[co][r * 3 + s_][e]);
-#pragma unroll
-        for (int r = 0; r < 3; ++r)
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            win[r][0][e] = win[r][1][e];
-            win[r][1][e] = win[r][2][e];
-          }
+        for (int ct = 0; ct < CT; ++ct) acc[ct] = mfma_f32(as[pl * AS + 32 * ct + ln], bv, acc[ct]);
       }
     }
+    __syncthreads();
   }
-  const int nout = 27 * C + 3;
-  float* out = part + (int64_t)blockIdx.x * nout;
+  // waves combine in order 0..3 (As is free after the loop's last barrier)
+  float* const red = As;
+  for (int w_ = 0; w_ < 4; ++w_) {
+    if (wv == w_) {
 #pragma unroll
-  for (int co = 0; co < 3; ++co) {
-    __syncthreads();
-    if (active)
+      for (int ct = 0; ct < CT; ++ct)
 #pragma unroll
-      for (int k = 0; k < 9; ++k)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) red[strip * 9 * Cp + k * Cp + c + e] = acc[co][k][e];
-    __syncthreads();
-    for (int i = t; i < 9 * C; i += 256) {
-      const int k = i / C, cc = i - k * C;
-      float v = 0.f;
-      for (int j = 0; j < S; ++j) v += red[j * 9 * Cp + k * Cp + cc];
-      out[(co * 9 + k) * C + cc] = v;
+        for (int r = 0; r < 16; ++r) {
+          const int i = (ct * 16 + r) * 64 + lane;
+          red[i] = w_ == 0 ? acc[ct][r] : red[i] + acc[ct][r];
+        }
     }
+    __syncthreads();
   }
-  // bias: every strip's lane cg == 0 holds its rows' sums
-  __syncthreads();
-  if (active && cg == 0) {
-    red[strip * 3] = bsum[0];
-    red[strip * 3 + 1] = bsum[1];
-    red[strip * 3 + 2] = bsum[2];
+  float* const out = part + (int64_t)blockIdx.x * (27 * C + 3);
+  for (int i = tid; i < CT * 1024; i += 256) {
+    const int l = i & 63, r = (i >> 6) & 15, ct = i >> 10;
+    const int n = l & 31, c = 32 * ct + 8 * (r >> 2) + 4 * (l >> 5) + (r & 3);
+    if (n < 27 && c < C) out[n * C + c] = red[i];
   }
+  // bias: thread partials in thread order
+#pragma unroll
+  for (int co = 0; co < 3; ++co) sb[3 * tid + co] = bs[co];
   __syncthreads();
-  if (t < 3) {
+  if (tid < 3) {
     float v = 0.f;
-    for (int j = 0; j < S; ++j) v += red[j * 3 + t];
-    out[27 * C + t] = v;
+    for (int j = 0; j < 256; ++j) v += sb[3 * j + tid];
+    out[27 * C + tid] = v;
   }
 }
 
@@ -381,34 +439,53 @@ __global__ __launch_bounds__(1024) void k_ghead_fin(const float* part, int nch, 
   }
 }
 
-static int64_t ghead_wgrad_blocks(int B, int H) { return (int64_t)B * cdiv(H, kWR); }
+static int64_t ghead_wgrad_blocks(int B, int H, int W, int Cp) { return (int64_t)B * cdiv(H, ghead_wrows(W, Cp)); }
 
-size_t ghead_ws_bytes(int B, int H, int C) { return align256((size_t)ghead_wgrad_blocks(B, H) * (27 * C + 3) * 4); }
+size_t ghead_ws_bytes(int B, int H, int W, int C) {
+  return align256((size_t)ghead_wgrad_blocks(B, H, W, (int)cpad(C)) * (27 * C + 3) * 4);
+}
 
 void ghead_fwd(hipStream_t st, const void* x, int B, int H, int W, int C, int Cp, const float* mean,
                const float* scale, const float* shift, const float* Wt, const float* sigma, const float* bias,
                float* img) {
-  const int64_t blocks = (int64_t)B * cdiv(H, kFR) * cdiv(W, kFC);
-  PG_CHECK(blocks < (1LL << 31) && Cp % 8 == 0 && C <= Cp && C <= 512, "ghead_fwd: shape");
-  hipLaunchKernelGGL(k_ghead_fwd, dim3((unsigned)blocks), dim3(256), 28 * C * sizeof(float), st, (const bf16_t*)x,
-                     B, H, W, C, Cp, mean, scale, shift, Wt, sigma, bias, img);
+  const int TC = ghead_cols(W);
+  const int64_t blocks = (int64_t)B * cdiv(H, kHR) * cdiv(W, TC);
+  PG_CHECK(blocks < (1LL << 31) && Cp == cpad(C) && ghead_shape_ok(W, C), "ghead_fwd: shape");
+  const bf16_t* xb = (const bf16_t*)x;
+#define PG_GHF(CK)                                                                                              \
+  hipLaunchKernelGGL(k_ghead_fwd<CK>, dim3((unsigned)blocks), dim3(256), 0, st, xb, H, W, C, TC, mean, scale, \
+                     shift, Wt, sigma, bias, img)
+  switch (Cp / 32) {
+    case 1: PG_GHF(2); break;
+    case 2: PG_GHF(4); break;
+    case 3: PG_GHF(6); break;
+    default: PG_GHF(8); break;
+  }
+#undef PG_GHF
   PG_LAUNCH_CHECK();
 }
 
 void ghead_bwd(hipStream_t st, const float* dimg, int ldd, const float* img, const void* x, int B, int H, int W,
                int C, int Cp, const float* mean, const float* scale, const float* shift, const float* Wt,
                const float* sigma, float* da, float* dwsn, float* dbias, void* ws) {
-  PG_CHECK(W % 4 == 0 && Cp % 4 == 0 && C <= Cp && Cp <= 1024, "ghead_bwd: shape");
   const int64_t dblocks = (int64_t)B * cdiv(H, kDR) * cdiv(W, kDC);
-  PG_CHECK(dblocks < (1LL << 31), "ghead_bwd: shape");
+  PG_CHECK(dblocks < (1LL << 31) && Cp == cpad(C) && ghead_shape_ok(W, C) && ldd >= 3, "ghead_bwd: shape");
+  const int TRW = ghead_wrows(W, Cp);
+  const size_t lds = ghead_wgrad_lds(W, Cp);
+  const int nch = (int)ghead_wgrad_blocks(B, H, W, Cp);
   hipLaunchKernelGGL(k_ghead_dgrad, dim3((unsigned)dblocks), dim3(256), 27 * Cp * sizeof(float), st, dimg, ldd,
                      img, B, H, W, C, Cp, Wt, sigma, da);
-  const int nch = (int)ghead_wgrad_blocks(B, H);
-  const int S = 256 / (Cp / 4);
-  const size_t red_bytes = (size_t)S * 9 * Cp * sizeof(float);
-  PG_CHECK(S >= 1 && red_bytes <= 64 * 1024, "ghead_bwd: channels");
-  hipLaunchKernelGGL(k_ghead_wgrad, dim3(nch), dim3(256), red_bytes, st, dimg, ldd, img, (const bf16_t*)x, B, H, W,
-                     C, Cp, mean, scale, shift, (float*)ws);
+  const bf16_t* xb = (const bf16_t*)x;
+#define PG_GHW(CT)                                                                                                   \
+  hipLaunchKernelGGL(k_ghead_wgrad<CT>, dim3(nch), dim3(256), lds, st, dimg, ldd, img, xb, H, W, C, TRW, mean, scale, \
+                     shift, (float*)ws)
+  switch (Cp / 32) {
+    case 1: PG_GHW(1); break;
+    case 2: PG_GHW(2); break;
+    case 3: PG_GHW(3); break;
+    default: PG_GHW(4); break;
+  }
+#undef PG_GHW
   hipLaunchKernelGGL(k_ghead_fin, dim3((unsigned)cdiv(27 * C + 3, 64)), dim3(1024), 0, st, (const float*)ws, nch,
                      27 * C + 3, dwsn, dbias);
   PG_LAUNCH_CHECK();

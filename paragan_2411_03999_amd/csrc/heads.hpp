@@ -9,7 +9,10 @@ namespace pg {
 void img_to_bf16(hipStream_t st, const float* img, int64_t npix, int Cp, void* out);
 
 // generator output layer (fp32): img = tanh(conv3x3(relu(bn(x))) + b)
-size_t ghead_ws_bytes(int B, int H, int C);
+// Shapes the kernels take: cpad(C) <= 128, W a multiple of 4, and the
+// weight-gradient tile (one image row plus a frame) within 64 KB of LDS.
+bool ghead_shape_ok(int W, int C);
+size_t ghead_ws_bytes(int B, int H, int W, int C);
 void ghead_fwd(hipStream_t st, const void* x, int B, int H, int W, int C, int Cp, const float* mean,
                const float* scale, const float* shift, const float* Wt, const float* sigma, const float* bias,
                float* img);

@@ -77,6 +77,8 @@ void check_arch(const paragan_biggan_desc* d) {
   for (int i = 0; i < a.n_g; ++i)
     if ((4 << (i + 1)) == a.attn_res)
       PG_CHECK(attn_width_ok(a.g_mult[i + 1] * a.ch), "biggan: unsupported G attention width");
+  PG_CHECK(ghead_shape_ok(a.img, a.g_mult[a.n_g] * a.ch),
+           "biggan: the generator output layer takes at most 128 (padded) input channels");
 }
 
 Layout g_layout(const Arch& a) {
@@ -90,11 +92,7 @@ Layout g_layout(const Arch& a) {
     L.add_prefixed("g" + std::to_string(i) + ".", gblock_layout(a.g_mult[i] * a.ch, cout, a.dc));
     if ((4 << (i + 1)) == a.attn_res) L.add_prefixed("attn.", attn_layout(cout));
   }
-  const int c = a.g_mult[a.n_g] * a.ch;
-  L.add("out_bn.gain", {c}, false);
-  L.add("out_bn.bias", {c}, false);
-  L.add("out_conv.w", {3, 3, 3, c}, true);
-  L.add("out_conv.b", {3}, false);
+  L.add_prefixed("", gout_layout(a.g_mult[a.n_g] * a.ch));
   return L;
 }
 
@@ -153,16 +151,16 @@ void GNet::plan_saved(Arena& s) {
     }
     in_.push_back(i == attn_after_ ? attn_out_ : act_[i + 1]);
   }
-  const int c = a.g_mult[a.n_g] * a.ch;
-  const int cp = (int)cpad(c);
-  mean_ = s.f32(cp); rstd_ = s.f32(cp); gain_ = s.f32(cp); bias_ = s.f32(cp); scale_ = s.f32(cp);
-  plan_slot(s, out_, 3, 27LL * c);
+  head_.B = B_; head_.H = a.img; head_.W = a.img; head_.C = a.g_mult[a.n_g] * a.ch;
+  head_.npi = a.npi; head_.bn_eps = a.bn_eps; head_.sn_eps = a.sn_eps;
+  head_.plan_saved(s);
 }
 
 struct GNetWs {
   void *g0, *g1;       // ping-pong activation gradients (bf16)
-  float *da, *dw, *dlin, *dcond, *part;
-  void* head;
+  float *dlin, *dcond, *part;
+  void* head;          // output layer workspace
+  size_t head_bytes;
   void* blk;           // block workspace
   size_t blk_bytes;
 };
@@ -180,17 +178,16 @@ static GNetWs gnet_carve(const Arch& a, int B, const std::vector<GBlock>& blocks
   }
   if (attn) blk = std::max(blk, attn->ws_size(n_cu));
   const int c0 = a.g_mult[0] * a.ch;
-  const int c = a.g_mult[a.n_g] * a.ch;
-  const int64_t M = (int64_t)B * a.img * a.img;
-  blk = std::max({blk, sn_ws_bytes(16LL * c0, a.zc), sn_ws_bytes(3, 27LL * c), bn_stats_ws_bytes(M, c)});
+  blk = std::max(blk, sn_ws_bytes(16LL * c0, a.zc));
   r.g0 = w.bytes(maxact * 2);
   r.g1 = w.bytes(maxact * 2);
-  r.da = w.f32((size_t)M * cpad(c));
-  r.dw = w.f32(27LL * c);
   r.dlin = w.f32(16LL * c0 * a.zc);
   r.dcond = w.f32((size_t)B * a.dc);
   r.part = w.f32(256);
-  r.head = w.bytes(std::max(ghead_ws_bytes(B, a.img, c), bn_bwd_ws_bytes(B, a.img * a.img, c)));
+  GOut head;
+  head.B = B; head.H = a.img; head.W = a.img; head.C = a.g_mult[a.n_g] * a.ch;
+  r.head_bytes = head.ws_size();
+  r.head = w.bytes(r.head_bytes);
   r.blk_bytes = blk;
   r.blk = w.bytes(blk);
   return r;
@@ -220,14 +217,7 @@ void GNet::fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y
       h = attn_out_;
     }
   }
-  const int c = a.g_mult[a.n_g] * a.ch, cp = (int)cpad(c);
-  const int64_t M = (int64_t)B_ * a.img * a.img;
-  bn_stats(ex.st, false, h, M, c, cp, a.bn_eps, mean_, rstd_, r.blk);
-  cbn_tables(ex.st, nullptr, 0, nullptr, nullptr, nullptr, nullptr, P.w("out_bn.gain"), P.w("out_bn.bias"), rstd_,
-             1, c, cp, gain_, bias_, scale_);
-  sn_forward(eb, P, "out_conv.w", out_, a.npi, a.sn_eps);
-  ghead_fwd(ex.st, h, B_, a.img, a.img, c, cp, mean_, scale_, bias_, P.w("out_conv.w"), out_.sigma,
-            P.w("out_conv.b"), img);
+  head_.fwd(Exec{ex.st, ex.n_cu, r.head, r.head_bytes}, P, h, img);
   img_ = img;
 }
 
@@ -236,16 +226,9 @@ void GNet::bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y
   Arena w(ex.ws);
   GNetWs r = gnet_carve(a, B_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
   Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
-  const int c = a.g_mult[a.n_g] * a.ch, cp = (int)cpad(c);
-  const void* x5 = in_[a.n_g];
-  ghead_bwd(ex.st, dimg, ldd, img_, x5, B_, a.img, a.img, c, cp, mean_, scale_, bias_, P.w("out_conv.w"),
-            out_.sigma, r.da, r.dw, P.gr("out_conv.b"), r.head);
-  sn_bwd(ex.st, r.dw, P.w("out_conv.w"), out_.u, out_.v, out_.sigma, 3, c, 3, c, nullptr, P.gr("out_conv.w"),
-         r.part);
   void* gcur = r.g0;
   void* gnext = r.g1;
-  bn_bwd(ex.st, false, r.da, false, x5, B_, a.img, a.img, c, cp, mean_, rstd_, gain_, bias_, 0, nullptr, gcur,
-         P.gr("out_bn.gain"), P.gr("out_bn.bias"), 0, r.head);
+  head_.bwd(Exec{ex.st, ex.n_cu, r.head, r.head_bytes}, P, in_[a.n_g], img_, dimg, ldd, gcur);
   for (int i = a.n_g - 1; i >= 0; --i) {
     if (i == attn_after_) {
       attn_.bwd(eb, sub(P, "attn."), act_[i + 1], gcur, gnext);
@@ -260,6 +243,71 @@ void GNet::bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y
   sn_bwd(ex.st, r.dlin, P.w("linear.w"), lin_.u, lin_.v, lin_.sigma, 16 * c0, a.zc, 1, a.zc, nullptr,
          P.gr("linear.w"), r.part);
   shared_grad(ex.st, r.dcond, a.dc, y, B_, a.n_classes, a.sd, P.gr("shared"));
+}
+
+// ============================================================ G output layer
+Layout gout_layout(int C) {
+  Layout L;
+  L.add("out_bn.gain", {C}, false);
+  L.add("out_bn.bias", {C}, false);
+  L.add("out_conv.w", {3, 3, 3, C}, true);
+  L.add("out_conv.b", {3}, false);
+  return L;
+}
+
+void GOut::plan_saved(Arena& s) {
+  const int cp = (int)cpad(C);
+  mean_ = s.f32(cp); rstd_ = s.f32(cp); gain_ = s.f32(cp); bias_ = s.f32(cp); scale_ = s.f32(cp);
+  plan_slot(s, sn_, 3, 27LL * C);
+}
+
+struct GOutWs {
+  float *da, *dw, *part;
+  void* red;           // reductions, the SN iteration and the weight-gradient partials, in turn
+  size_t red_bytes;
+};
+
+static GOutWs gout_carve(const GOut& g, Arena& w) {
+  const int64_t M = (int64_t)g.B * g.H * g.W;
+  GOutWs r;
+  r.da = w.f32((size_t)M * cpad(g.C));
+  r.dw = w.f32(27LL * g.C);
+  r.part = w.f32(256);
+  r.red_bytes = std::max({ghead_ws_bytes(g.B, g.H, g.W, g.C), bn_bwd_ws_bytes(g.B, g.H * g.W, g.C),
+                          bn_stats_ws_bytes(M, g.C), sn_ws_bytes(3, 27LL * g.C)});
+  r.red = w.bytes(r.red_bytes);
+  return r;
+}
+
+size_t GOut::ws_size() const {
+  Arena w(nullptr);
+  gout_carve(*this, w);
+  return w.off;
+}
+
+void GOut::fwd(const Exec& ex, const Params& P, const void* x, float* img) {
+  Arena w(ex.ws);
+  const GOutWs r = gout_carve(*this, w);
+  PG_CHECK(w.off <= ex.ws_bytes, "output layer: workspace too small");
+  const int cp = (int)cpad(C);
+  bn_stats(ex.st, false, x, (int64_t)B * H * W, C, cp, bn_eps, mean_, rstd_, r.red);
+  cbn_tables(ex.st, nullptr, 0, nullptr, nullptr, nullptr, nullptr, P.w("out_bn.gain"), P.w("out_bn.bias"), rstd_,
+             1, C, cp, gain_, bias_, scale_);
+  sn_forward(Exec{ex.st, ex.n_cu, r.red, r.red_bytes}, P, "out_conv.w", sn_, npi, sn_eps);
+  ghead_fwd(ex.st, x, B, H, W, C, cp, mean_, scale_, bias_, P.w("out_conv.w"), sn_.sigma, P.w("out_conv.b"), img);
+}
+
+void GOut::bwd(const Exec& ex, const Params& P, const void* x, const float* img, const float* dimg, int ldd,
+               void* dx) {
+  Arena w(ex.ws);
+  const GOutWs r = gout_carve(*this, w);
+  PG_CHECK(w.off <= ex.ws_bytes, "output layer: workspace too small");
+  const int cp = (int)cpad(C);
+  ghead_bwd(ex.st, dimg, ldd, img, x, B, H, W, C, cp, mean_, scale_, bias_, P.w("out_conv.w"), sn_.sigma, r.da,
+            r.dw, P.gr("out_conv.b"), r.red);
+  sn_bwd(ex.st, r.dw, P.w("out_conv.w"), sn_.u, sn_.v, sn_.sigma, 3, C, 3, C, nullptr, P.gr("out_conv.w"), r.part);
+  bn_bwd(ex.st, false, r.da, false, x, B, H, W, C, cp, mean_, rstd_, gain_, bias_, 0, nullptr, dx,
+         P.gr("out_bn.gain"), P.gr("out_bn.bias"), 0, r.red);
 }
 
 // =================================================================== D

@@ -25,6 +25,28 @@ struct DSpec {
 };
 std::vector<DSpec> d_specs(const Arch& a);
 
+// Generator output layer, fp32 arithmetic: BN with batch statistics and an
+// affine gain / bias -> ReLU -> SN conv3x3 (C -> 3, bias) -> tanh.
+// Parameters (named): out_bn.gain out_bn.bias out_conv.w out_conv.b.
+class GOut {
+ public:
+  int B = 0, H = 0, W = 0, C = 0, npi = 1;
+  float bn_eps = 1e-5f, sn_eps = 1e-12f;
+  void plan_saved(Arena& s);
+  size_t ws_size() const;
+  // x: bf16 [B][H][W][cpad(C)]; img: fp32 [B][H][W][3]
+  void fwd(const Exec& ex, const Params& P, const void* x, float* img);
+  // img: this layer's forward output; dimg: fp32 [B][H][W][ldd];
+  // dx: bf16 [B][H][W][cpad(C)]
+  void bwd(const Exec& ex, const Params& P, const void* x, const float* img, const float* dimg, int ldd,
+           void* dx);
+
+ private:
+  SNSlot sn_;
+  float *mean_ = nullptr, *rstd_ = nullptr, *gain_ = nullptr, *bias_ = nullptr, *scale_ = nullptr;
+};
+Layout gout_layout(int C);
+
 class GNet {
  public:
   GNet(const Arch& a, int B) : a_(a), B_(B) {}
@@ -45,8 +67,8 @@ class GNet {
   std::vector<void*> in_;      // in_[i]: input of block i (attention output after the attention block)
   void* attn_out_ = nullptr;
   std::vector<float*> cond_;
-  SNSlot lin_, out_;
-  float *mean_, *rstd_, *gain_, *bias_, *scale_;
+  SNSlot lin_;
+  GOut head_;
   float* img_ = nullptr;
 };
 

@@ -45,6 +45,11 @@ class AttnDesc(C.Structure):
                 ("n_power_iter", C.c_int32), ("sn_eps", C.c_float)]
 
 
+class GoutDesc(C.Structure):
+    _fields_ = [("B", C.c_int32), ("H", C.c_int32), ("W", C.c_int32), ("C", C.c_int32),
+                ("n_power_iter", C.c_int32), ("bn_eps", C.c_float), ("sn_eps", C.c_float)]
+
+
 class BigganDesc(C.Structure):
     _fields_ = [("img", C.c_int32), ("ch", C.c_int32), ("n_g", C.c_int32), ("g_mult", C.c_int32 * 10),
                 ("n_d", C.c_int32), ("d_mult", C.c_int32 * 10), ("d_down", C.c_int32 * 10),
@@ -99,6 +104,12 @@ _SIGS = {
     "paragan_attn_check": (C.c_int, [_P]),
     "paragan_attn_fwd": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
     "paragan_attn_bwd": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "paragan_gout_layout": (C.c_int, [_P, _P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int64),
+                                      C.POINTER(C.c_int64)]),
+    "paragan_gout_sizes": (C.c_int, [_P, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]),
+    "paragan_gout_check": (C.c_int, [_P]),
+    "paragan_gout_fwd": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
+    "paragan_gout_bwd": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "paragan_net_layout": (C.c_int, [_P, C.c_int32, _P, C.c_int32, C.POINTER(C.c_int32),
                                      C.POINTER(C.c_int64), C.POINTER(C.c_int64)]),
     "paragan_biggan_check": (C.c_int, [_P]),
@@ -274,6 +285,28 @@ def paragan_attn_fwd(ctx, desc, params, u, x, y, saved, ws):
 def paragan_attn_bwd(ctx, desc, params, x, saved, dy, dx, grads, ws):
     return ctx.check(load().paragan_attn_bwd(ctx.h, C.byref(desc), _ptr(params), _ptr(x), _ptr(saved),
                                              _ptr(dy), _ptr(dx), _ptr(grads), _ptr(ws)))
+
+
+def paragan_gout_layout(desc):
+    return _layout(load().paragan_gout_layout, C.byref(desc))
+
+
+def paragan_gout_sizes(desc):
+    return _sizes(load().paragan_gout_sizes, desc)
+
+
+def paragan_gout_check(desc):
+    return load().paragan_gout_check(C.byref(desc))
+
+
+def paragan_gout_fwd(ctx, desc, params, u, x, img, saved, ws):
+    return ctx.check(load().paragan_gout_fwd(ctx.h, C.byref(desc), _ptr(params), _ptr(u), _ptr(x), _ptr(img),
+                                             _ptr(saved), _ptr(ws)))
+
+
+def paragan_gout_bwd(ctx, desc, params, x, img, saved, dimg, dx, grads, ws):
+    return ctx.check(load().paragan_gout_bwd(ctx.h, C.byref(desc), _ptr(params), _ptr(x), _ptr(img),
+                                             _ptr(saved), _ptr(dimg), _ptr(dx), _ptr(grads), _ptr(ws)))
 
 
 def paragan_net_layout(desc, which):

@@ -123,3 +123,27 @@ def test_biggan_validation(L):
     assert lib.paragan_biggan_check(d) == lib.EINVAL          # z does not split evenly
     d = _desc(a)
     assert lib.paragan_train_step_ws_size(d) > 0
+
+
+def test_gout_validation_and_layout(L):
+    ok = lib.GoutDesc(2, 128, 128, 96, 1, 1e-5, 1e-12)
+    assert lib.paragan_gout_check(ok) == lib.OK
+    assert lib.paragan_gout_check(lib.GoutDesc(1, 8, 8, 129, 1, 1e-5, 1e-12)) == lib.EINVAL    # cpad(C) = 160
+    assert lib.paragan_gout_check(lib.GoutDesc(1, 8, 10, 8, 1, 1e-5, 1e-12)) == lib.EINVAL     # W % 4 != 0
+    assert lib.paragan_gout_check(lib.GoutDesc(1, 8, 2048, 96, 1, 1e-5, 1e-12)) == lib.EINVAL  # tile too wide
+    assert lib.paragan_gout_check(lib.GoutDesc(1, 8, 704, 128, 1, 1e-5, 1e-12)) == lib.OK
+    assert lib.paragan_gout_check(lib.GoutDesc(0, 8, 8, 8, 1, 1e-5, 1e-12)) == lib.EINVAL
+    ents, npar, nu = lib.paragan_gout_layout(ok)
+    lay, sn = O.g_layout(O.biggan128())
+    out = [(k, v) for k, v in lay.items() if k.startswith("out_")]
+    assert [(e["name"], e["shape"]) for e in ents] == out
+    assert [e["name"] for e in ents if e["u_offset"] >= 0] == ["out_conv.w"] and nu == 3
+    s, w = lib.paragan_gout_sizes(ok)
+    assert s > 0 and w > 0
+
+
+def test_biggan_rejects_wide_output_layer(L):
+    a = O.biggan128()
+    d = _desc(a)
+    d.g_mult[a.n_g] = 2        # output layer input 192 channels
+    assert lib.paragan_biggan_check(d) == lib.EINVAL
