@@ -96,6 +96,7 @@ __global__ __launch_bounds__(256, 2) void k_ghead_fwd(const bf16_t* __restrict__
   const bool col_ok = zw < zc1;
   uint4 xr[CK];
   auto fetch = [&](int zr) {
+    // columns past zc1 read zeros; their Z values are never gathered
     const bool ok = col_ok && zr >= 0 && zr < H;
     const int64_t off = ok ? (((int64_t)b * H + zr) * W + zw) * Cp + 8 * kh : 0;
 #pragma unroll
@@ -105,7 +106,27 @@ __global__ __launch_bounds__(256, 2) void k_ghead_fwd(const bf16_t* __restrict__
   const float inv = 1.f / *sigma;
   const int nz = h1 - h0 + 2;   // Z rows h0 - 1 .. h1
   fetch(h0 - 1);
+  // ring indices 0 and w1 - w0 + 1 are columns w0 - 1 and w1: outside the
+  // image (zeros, set once) when the block touches the left or right edge,
+  // otherwise written with every Z row
+  for (int i = tid; i < 6 * kZS; i += 256) {
+    const int side = i / (3 * kZS), k = i - side * 3 * kZS;
+    if (side == 0 ? w0 == 0 : w1 == W) Zs[k / kZS][side == 0 ? 0 : w1 - w0 + 1][k % kZS] = 0.f;
+  }
   __syncthreads();
+  // the B operand of every k-step stays in registers for the whole block
+  float wr[CK * 8];
+#pragma unroll
+  for (int i = 0; i < CK * 8; ++i) wr[i] = Wl[((2 * (i >> 3) + kh) * 8 + (i & 7)) * 32 + ln];
+  // BN constants of chunk j for this lane's 8 channels (16 j + 8 kh ..)
+  auto ldc = [&](int j, float4 (&c)[6]) {
+    const int q4 = 4 * j + 2 * kh;
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+      c[2 * a] = cst[a][q4];
+      c[2 * a + 1] = cst[a][q4 + 1];
+    }
+  };
   for (int t = 0; t < nz; ++t) {
     const int zr = h0 - 1 + t;
     uint4 cur[CK];
@@ -116,51 +137,58 @@ __global__ __launch_bounds__(256, 2) void k_ghead_fwd(const bf16_t* __restrict__
       f32x16 acc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      float4 cc[6], cn[6];
+      ldc(0, cc);
 #pragma unroll
       for (int j = 0; j < CK; ++j) {
+        if (j + 1 < CK) ldc(j + 1, cn);
         float v[8];
         unpack8(cur[j], v);
-        const int q4 = 4 * j + 2 * kh;   // float4 index of channel 16 j + 8 kh
-        const float4 m0 = cst[0][q4], m1 = cst[0][q4 + 1];
-        const float4 s0 = cst[1][q4], s1 = cst[1][q4 + 1];
-        const float4 f0 = cst[2][q4], f1 = cst[2][q4 + 1];
-        const float mu[8] = {m0.x, m0.y, m0.z, m0.w, m1.x, m1.y, m1.z, m1.w};
-        const float sc[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
-        const float sh[8] = {f0.x, f0.y, f0.z, f0.w, f1.x, f1.y, f1.z, f1.w};
+        const float mu[8] = {cc[0].x, cc[0].y, cc[0].z, cc[0].w, cc[1].x, cc[1].y, cc[1].z, cc[1].w};
+        const float sc[8] = {cc[2].x, cc[2].y, cc[2].z, cc[2].w, cc[3].x, cc[3].y, cc[3].z, cc[3].w};
+        const float sh[8] = {cc[4].x, cc[4].y, cc[4].z, cc[4].w, cc[5].x, cc[5].y, cc[5].z, cc[5].w};
 #pragma unroll
-        for (int s = 0; s < 8; ++s) {
-          const float a = col_ok ? fmaxf((v[s] - mu[s]) * sc[s] + sh[s], 0.f) : 0.f;
-          acc = mfma_f32(a, Wl[((2 * j + kh) * 8 + s) * 32 + ln], acc);
-        }
+        for (int s = 0; s < 8; ++s) acc = mfma_f32(fmaxf((v[s] - mu[s]) * sc[s] + sh[s], 0.f), wr[8 * j + s], acc);
+#pragma unroll
+        for (int i = 0; i < 6; ++i) cc[i] = cn[i];
       }
-      // lane: Z[position row 8 (r / 4) + 4 kh + r % 4 of the tile][n = ln]
+      // lane: Z[position row 8 (r / 4) + 4 kh + r % 4 of the tile][n = ln].  Ring
+      // index w - w0 + 1 stays below kZP for every position of the tiles;
+      // columns >= W get zeros (the zero padding the gather reads)
       float* zs = &Zs[t % 3][0][0];
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int w = zc0 + 32 * wv + 8 * (r >> 2) + 4 * kh + (r & 3);
-        if (w < zc1) zs[(w - w0 + 1) * kZS + ln] = acc[r];
+        zs[(w - w0 + 1) * kZS + ln] = w < W ? acc[r] : 0.f;
       }
+    } else if (zr < 0 || zr >= H) {
+      // a Z row outside the image: zeros wherever the gather reads
+      float* zs = &Zs[t % 3][0][0];
+      for (int i = tid; i < kZP * kZS; i += 256) zs[i] = 0.f;
     }
     if (t >= 2) {
-      // output row oh = zr - 1: its Z rows oh - 1 .. oh + 1 sit in ring slots (t - 2 .. t) % 3
+      // output row oh = zr - 1: its Z rows oh - 1 .. oh + 1 sit in ring slots
+      // (t - 2 .. t) % 3; every read below lands on a computed or zeroed entry
       __syncthreads();
       const int oh = zr - 1, ncol = w1 - w0;
+      const float* z0 = &Zs[(t - 2) % 3][0][0];
+      const float* z1 = &Zs[(t - 1) % 3][0][0];
+      const float* z2 = &Zs[t % 3][0][0];
+      float* const orow = img + (((int64_t)b * H + oh) * W + w0) * 3;
       for (int it = tid; it < 3 * ncol; it += 256) {
-        const int co = it / ncol, pc = it - co * ncol;
-        const int ow = w0 + pc;
+        const int pc = it / 3, co = it - 3 * pc;
+        const int base = pc * kZS + co * 9;   // ring index of column ow - 1 is pc
         float sum = 0.f;
 #pragma unroll
-        for (int r = 0; r < 3; ++r) {
-          const int ih = oh - 1 + r;
-          if ((unsigned)ih >= (unsigned)H) continue;
-          const float* zs = &Zs[(t - 2 + r) % 3][0][0];
+        for (int s = 0; s < 3; ++s) sum += z0[base + s * kZS + s];
 #pragma unroll
-          for (int s = 0; s < 3; ++s) {
-            const int iw = ow - 1 + s;
-            if ((unsigned)iw < (unsigned)W) sum += zs[(iw - w0 + 1) * kZS + co * 9 + r * 3 + s];
-          }
-        }
-        img[(((int64_t)b * H + oh) * W + ow) * 3 + co] = tanhf(sum * inv + bias[co]);
+        for (int s = 0; s < 3; ++s) sum += z1[base + s * kZS + 3 + s];
+#pragma unroll
+        for (int s = 0; s < 3; ++s) sum += z2[base + s * kZS + 6 + s];
+        // tanh(y) = 1 - 2 / (exp(2 y) + 1): exact at the saturated ends,
+        // absolute error about 1e-7 elsewhere
+        const float e = __expf(2.f * (sum * inv + bias[co]));
+        orow[it] = 1.f - __fdividef(2.f, e + 1.f);
       }
       __syncthreads();
     }
@@ -285,7 +313,7 @@ bool ghead_shape_ok(int W, int C) {
 template <int CT>   // CT = Cp / 32
 __global__ __launch_bounds__(256, 2) void k_ghead_wgrad(const float* __restrict__ dimg, int ldd,
                                                         const float* __restrict__ img, const bf16_t* __restrict__ x,
-                                                        int H, int W, int C, int TRW,
+                                                        int H, int W, FastDiv fdW, int C, int TRW,
                                                         const float* __restrict__ mean, const float* __restrict__ scale,
                                                         const float* __restrict__ shift, float* __restrict__ part) {
   constexpr int Cp = 32 * CT, AS = Cp + 4;
@@ -293,8 +321,8 @@ __global__ __launch_bounds__(256, 2) void k_ghead_wgrad(const float* __restrict_
   const int W2 = W + 2;
   float* const dts = reinterpret_cast<float*>(sm4);                  // [(rows + 2) * W2][3]
   float* const As = dts + ((TRW + 2) * W2 * 3 + 3) / 4 * 4;         // [4][kWC][AS]
-  float* const cst = As + 4 * kWC * AS;                              // [3][Cp]
-  float* const sb = cst + 3 * Cp;                                    // [256][3] bias partials
+  float4* const cst = reinterpret_cast<float4*>(As + 4 * kWC * AS);  // [3][Cp / 4]
+  float* const sb = reinterpret_cast<float*>(cst + 3 * Cp / 4);      // [256][3] bias partials
   const int nrb = (H + TRW - 1) / TRW;
   const int b = blockIdx.x / nrb, h0 = (blockIdx.x % nrb) * TRW;
   const int nr = min(TRW, H - h0);
@@ -302,9 +330,10 @@ __global__ __launch_bounds__(256, 2) void k_ghead_wgrad(const float* __restrict_
   const int wv = tid >> 6;
   for (int c = tid; c < Cp; c += 256) {
     const bool ok = c < C;
-    cst[c] = ok ? mean[c] : 0.f;
-    cst[Cp + c] = ok ? scale[c] : 0.f;
-    cst[2 * Cp + c] = ok ? shift[c] : 0.f;
+    float* const cf = reinterpret_cast<float*>(cst);
+    cf[c] = ok ? mean[c] : 0.f;
+    cf[Cp + c] = ok ? scale[c] : 0.f;
+    cf[2 * Cp + c] = ok ? shift[c] : 0.f;
   }
   float bs[3] = {0.f, 0.f, 0.f};
   for (int i = tid; i < (nr + 2) * W2; i += 256) {
@@ -335,12 +364,13 @@ __global__ __launch_bounds__(256, 2) void k_ghead_wgrad(const float* __restrict_
   const int P = nr * W;
   const int nch = (P + kWC - 1) / kWC, iters = (nch + 3) / 4;
   uint4 xr[CT];
+  // positions past P stage zeros (and meet a zero G row below)
   auto fetch = [&](int k) {
     const int p = k * kWC + si;
     const bool ok = k < nch && p < P;
     int64_t off = 0;
     if (ok) {
-      const int h = p / W;
+      const int h = (int)fdiv((uint32_t)p, fdW);
       off = (((int64_t)b * H + h0 + h) * W + (p - h * W)) * Cp + 8 * sq;
     }
 #pragma unroll
@@ -357,36 +387,44 @@ __global__ __launch_bounds__(256, 2) void k_ghead_wgrad(const float* __restrict_
   float* const as = As + wv * kWC * AS;
   for (int it = 0; it < iters; ++it) {
     const int k = wv + 4 * it;
-    {
-      const int p = k * kWC + si;
-      const bool ok = k < nch && p < P;
 #pragma unroll
-      for (int j = 0; j < CT; ++j) {
-        float v[8];
-        unpack8(xr[j], v);
-        const int c0 = 32 * j + 8 * sq;
-        float a[8];
+    for (int j = 0; j < CT; ++j) {
+      const int q4 = 8 * j + 2 * sq;   // float4 index of channel 32 j + 8 sq
+      float4 c[6];
 #pragma unroll
-        for (int e = 0; e < 8; ++e)
-          a[e] = ok ? fmaxf((v[e] - cst[c0 + e]) * cst[Cp + c0 + e] + cst[2 * Cp + c0 + e], 0.f) : 0.f;
-        *reinterpret_cast<float4*>(as + si * AS + c0) = make_float4(a[0], a[1], a[2], a[3]);
-        *reinterpret_cast<float4*>(as + si * AS + c0 + 4) = make_float4(a[4], a[5], a[6], a[7]);
+      for (int a = 0; a < 3; ++a) {
+        c[2 * a] = cst[a * (Cp / 4) + q4];
+        c[2 * a + 1] = cst[a * (Cp / 4) + q4 + 1];
       }
+      const float mu[8] = {c[0].x, c[0].y, c[0].z, c[0].w, c[1].x, c[1].y, c[1].z, c[1].w};
+      const float sc[8] = {c[2].x, c[2].y, c[2].z, c[2].w, c[3].x, c[3].y, c[3].z, c[3].w};
+      const float sh[8] = {c[4].x, c[4].y, c[4].z, c[4].w, c[5].x, c[5].y, c[5].z, c[5].w};
+      float v[8], a[8];
+      unpack8(xr[j], v);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[e] = fmaxf((v[e] - mu[e]) * sc[e] + sh[e], 0.f);
+      *reinterpret_cast<float4*>(as + si * AS + 32 * j + 8 * sq) = make_float4(a[0], a[1], a[2], a[3]);
+      *reinterpret_cast<float4*>(as + si * AS + 32 * j + 8 * sq + 4) = make_float4(a[4], a[5], a[6], a[7]);
     }
     if (it + 1 < iters) fetch(k + 4);
     __syncthreads();
     if (k < nch) {
+      // every operand of the chunk's k-steps first, then the products
+      float av[kWC / 2][CT], bv[kWC / 2];
 #pragma unroll
       for (int s = 0; s < kWC / 2; ++s) {
         const int pl = 2 * s + kh, p = k * kWC + pl;
-        float bv = 0.f;
-        if (nok && p < P) {
-          const int h = p / W;
-          bv = dts[(h * W2 + (p - h * W)) * 3 + boff];
-        }
+        const int pc = min(p, P - 1);
+        const int h = (int)fdiv((uint32_t)pc, fdW);
+        const float g = dts[(h * W2 + (pc - h * W)) * 3 + boff];
+        bv[s] = nok && p < P ? g : 0.f;
 #pragma unroll
-        for (int ct = 0; ct < CT; ++ct) acc[ct] = mfma_f32(as[pl * AS + 32 * ct + ln], bv, acc[ct]);
+        for (int ct = 0; ct < CT; ++ct) av[s][ct] = as[pl * AS + 32 * ct + ln];
       }
+#pragma unroll
+      for (int s = 0; s < kWC / 2; ++s)
+#pragma unroll
+        for (int ct = 0; ct < CT; ++ct) acc[ct] = mfma_f32(av[s][ct], bv[s], acc[ct]);
     }
     __syncthreads();
   }
@@ -473,12 +511,13 @@ void ghead_bwd(hipStream_t st, const float* dimg, int ldd, const float* img, con
   const int TRW = ghead_wrows(W, Cp);
   const size_t lds = ghead_wgrad_lds(W, Cp);
   const int nch = (int)ghead_wgrad_blocks(B, H, W, Cp);
+  const FastDiv fdW = make_fastdiv((uint32_t)W);
   hipLaunchKernelGGL(k_ghead_dgrad, dim3((unsigned)dblocks), dim3(256), 27 * Cp * sizeof(float), st, dimg, ldd,
                      img, B, H, W, C, Cp, Wt, sigma, da);
   const bf16_t* xb = (const bf16_t*)x;
 #define PG_GHW(CT)                                                                                                   \
-  hipLaunchKernelGGL(k_ghead_wgrad<CT>, dim3(nch), dim3(256), lds, st, dimg, ldd, img, xb, H, W, C, TRW, mean, scale, \
-                     shift, (float*)ws)
+  hipLaunchKernelGGL(k_ghead_wgrad<CT>, dim3(nch), dim3(256), lds, st, dimg, ldd, img, xb, H, W, fdW, C, TRW, mean,  \
+                     scale, shift, (float*)ws)
   switch (Cp / 32) {
     case 1: PG_GHW(1); break;
     case 2: PG_GHW(2); break;
