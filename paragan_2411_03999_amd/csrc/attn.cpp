@@ -55,7 +55,7 @@ static AWsB a_carve_b(const Attn& t, Arena& a, int n_cu) {
   w.Dv = a.f32((size_t)t.B * d.HWp);
   w.dwq = a.f32((size_t)t.Nqkv * t.Cp);
   w.dwo = a.f32((size_t)t.Cp * t.dv);
-  w.part = a.f32(256 * kSnGroupMax);
+  w.part = a.f32((size_t)kSnbParts * kSnGroupMax);
   w.wg_bytes = std::max(conv_wgrad_ws(false, M, 1, t.dv, t.Cp, n_cu), conv_wgrad_ws(false, M, 1, t.Cp, t.Nqkv, n_cu));
   w.wg = a.bytes(w.wg_bytes);
   return w;

@@ -165,7 +165,7 @@ static GWsB g_carve_b(const GBlock& g, Arena& a, int n_cu) {
   w.dh1 = a.bytes((size_t)M2 * g.Cop * e);
   w.dg1 = a.f32((size_t)g.B * g.Cip); w.db1 = a.f32((size_t)g.B * g.Cip);
   w.dg2 = a.f32((size_t)g.B * g.Cop); w.db2 = a.f32((size_t)g.B * g.Cop);
-  w.part = a.f32(256 * kSnGroupMax);
+  w.part = a.f32((size_t)kSnbParts * kSnGroupMax);
   w.lin = (float*)a.bytes(cbn_linear_bwd_ws_bytes(g.B, g.dc));
   w.bnb = a.bytes(std::max(bn_bwd_ws_bytes(g.B, 4 * g.H * g.W, g.cout), bn_bwd_ws_bytes(g.B, g.H * g.W, g.cin)));
   return w;
@@ -371,7 +371,7 @@ static DWsB d_carve_b(const DBlock& d, Arena& a, int n_cu) {
   w.cs = a.bytes(colsum_ws_bytes(M, d.Cop));
   w.dh = a.bytes((size_t)M * d.Cop * e);
   w.dxs = d.lsc ? a.f32((size_t)Mo * d.Cip) : nullptr;
-  w.part = a.f32(256 * kSnGroupMax);
+  w.part = a.f32((size_t)kSnbParts * kSnGroupMax);
   return w;
 }
 

@@ -38,18 +38,23 @@ PG_DEV double block_sum_d(double v, double* sh) {
 // kSnGroupMax), each launch finding its weight from a block-offset table
 // passed by value with the job descriptors.
 //   phase 1  part[j][c] = sum_{r in row chunk j} W[r][c] u[r]
-//   phase 2  t[c] = sum_j part[j][c] (in order), and per-block partials of |t|^2
+//   phase 2  t[c] = sum_j part[j][c] (fixed order), and per-block partials of |t|^2
 //   phase 3  s'[r] = W[r] . t                                              (a wave per row)
 //   phase 4  (a block per weight) v = t / max(|t|, eps), s = s' / max(|t|, eps),
 //            u = s / max(|s|, eps), sigma = u . s
 // (W v = (W t) / max(|t|, eps) exactly; only the rounding order differs from
-// normalising t first.)  Row chunks are sized so that phase 2 sums at most
-// 16 partials per column.
+// normalising t first.)  Phase 1 tiles W as (row chunk) x (cw columns): a
+// block's threads are P = 256 / cw row lanes of cw columns, so a matrix with
+// few columns (a linear map from a 20-d z chunk) still reads whole rows per
+// step; the P lane sums combine in order through LDS.  Row chunks are many
+// for narrow matrices (about 1024 blocks in all), so phase 2 splits each
+// column's chunk sum over L = 256 / cw2 lanes, combined in lane order (cw2
+// = 64 columns per block when there are more than 32 chunks, else 256).
 struct SnJobK {
   const float* W;
   float *u, *v, *sigma, *u_save, *part, *s;
-  double* tsq;          // per-block partials of |t|^2 (ceil(cols / 256))
-  int rows, cols, rchunk, nrc;
+  double* tsq;          // per-block partials of |t|^2 (ceil(cols / cw2))
+  int rows, cols, rchunk, nrc, cw, P, cw2;
 };
 struct SnGroupK {
   SnJobK j[kSnGroupMax];
@@ -64,41 +69,65 @@ PG_DEV int find_job(const int* off, int n, int bid) {
 }
 
 __global__ __launch_bounds__(256) void k_sng_wtu(SnGroupK g) {
+  __shared__ float sh[256];
   const int i = find_job(g.off, g.n, blockIdx.x);
   const SnJobK& J = g.j[i];
   const int lb = blockIdx.x - g.off[i];
-  const int cb = (J.cols + 255) >> 8;
+  const int cb = (J.cols + J.cw - 1) / J.cw;
   const int rc = lb / cb;
-  const int c = (lb - rc * cb) * 256 + threadIdx.x;
-  if (c >= J.cols) return;
+  const int cc = (int)threadIdx.x % J.cw, ro = (int)threadIdx.x / J.cw;
+  const int c = (lb - rc * cb) * J.cw + cc;
+  const bool on = ro < J.P && c < J.cols;
   const int r0 = rc * J.rchunk, r1 = min(r0 + J.rchunk, J.rows);
-  const float* W = J.W + (int64_t)r0 * J.cols + c;
-  const int64_t ld = J.cols;
-  // four independent chains: four rows in flight per thread
-  float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
-  int r = r0;
-  for (; r + 4 <= r1; r += 4, W += 4 * ld) {
-    s0 = fmaf(W[0], J.u[r], s0);
-    s1 = fmaf(W[ld], J.u[r + 1], s1);
-    s2 = fmaf(W[2 * ld], J.u[r + 2], s2);
-    s3 = fmaf(W[3 * ld], J.u[r + 3], s3);
+  float acc = 0.f;
+  if (on) {
+    const int64_t ld = J.cols, st = (int64_t)J.P * ld;
+    const float* W = J.W + (int64_t)(r0 + ro) * ld + c;
+    // four independent chains: four rows in flight per thread
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+    int r = r0 + ro;
+    for (; r + 3 * J.P < r1; r += 4 * J.P, W += 4 * st) {
+      s0 = fmaf(W[0], J.u[r], s0);
+      s1 = fmaf(W[st], J.u[r + J.P], s1);
+      s2 = fmaf(W[2 * st], J.u[r + 2 * J.P], s2);
+      s3 = fmaf(W[3 * st], J.u[r + 3 * J.P], s3);
+    }
+    for (; r < r1; r += J.P, W += st) s0 = fmaf(W[0], J.u[r], s0);
+    acc = (s0 + s1) + (s2 + s3);
   }
-  for (; r < r1; ++r, W += ld) s0 = fmaf(W[0], J.u[r], s0);
-  J.part[(int64_t)rc * J.cols + c] = (s0 + s1) + (s2 + s3);
+  if (J.P == 1) {
+    if (on) J.part[(int64_t)rc * J.cols + c] = acc;
+    return;
+  }
+  sh[threadIdx.x] = acc;
+  __syncthreads();
+  if (ro == 0 && c < J.cols) {
+    float t = 0.f;
+    for (int k = 0; k < J.P; ++k) t += sh[k * J.cw + cc];
+    J.part[(int64_t)rc * J.cols + c] = t;
+  }
 }
 
 __global__ __launch_bounds__(256) void k_sng_t(SnGroupK g) {
-  __shared__ double sh[4];
+  __shared__ float sh[256];
+  __shared__ double shd[4];
   const int i = find_job(g.off, g.n, blockIdx.x);
   const SnJobK& J = g.j[i];
   const int lb = blockIdx.x - g.off[i];
-  const int c = lb * 256 + threadIdx.x;
+  const int cw2 = J.cw2, L = 256 / cw2;
+  const int cc = (int)threadIdx.x % cw2, ln = (int)threadIdx.x / cw2;
+  const int c = lb * cw2 + cc;
   float t = 0.f;
-  if (c < J.cols) {
-    for (int j = 0; j < J.nrc; ++j) t += J.part[(int64_t)j * J.cols + c];
-    J.v[c] = t;
+  if (ln < L && c < J.cols)
+    for (int j = ln; j < J.nrc; j += L) t += J.part[(int64_t)j * J.cols + c];
+  sh[threadIdx.x] = t;
+  __syncthreads();
+  float tc = 0.f;
+  if (ln == 0 && c < J.cols) {
+    for (int k = 0; k < L; ++k) tc += sh[k * cw2 + cc];
+    J.v[c] = tc;
   }
-  const double ss = block_sum_d<256>((double)t * t, sh);
+  const double ss = block_sum_d<256>((double)tc * tc, shd);
   if (threadIdx.x == 0) J.tsq[lb] = ss;
 }
 
@@ -126,11 +155,12 @@ __global__ __launch_bounds__(1024) void k_sng_u(SnGroupK g, float eps) {
   __shared__ double sh[16];
   __shared__ float inv_t_sh;
   const SnJobK& J = g.j[blockIdx.x];
-  if (threadIdx.x == 0) {
+  {
+    const int nb = (J.cols + J.cw2 - 1) / J.cw2;
     double tt = 0.0;
-    const int nb = (J.cols + 255) >> 8;
-    for (int b = 0; b < nb; ++b) tt += J.tsq[b];
-    inv_t_sh = 1.f / fmaxf((float)sqrt(tt), eps);
+    for (int b = threadIdx.x; b < nb; b += 1024) tt += J.tsq[b];
+    tt = block_sum_d<1024>(tt, sh);
+    if (threadIdx.x == 0) inv_t_sh = 1.f / fmaxf((float)sqrt(tt), eps);
   }
   __syncthreads();
   const float inv_t = inv_t_sh;
@@ -154,16 +184,27 @@ __global__ __launch_bounds__(1024) void k_sng_u(SnGroupK g, float eps) {
   if (threadIdx.x == 0) *J.sigma = (float)sgt;
 }
 
-static void sn_chunks(int64_t rows, int& rchunk, int& nrc) {
-  nrc = (int)std::min<int64_t>(16, cdiv(rows, 16));
-  rchunk = (int)cdiv(rows, nrc);
-  nrc = (int)cdiv(rows, rchunk);
+// phase-1 tiling: cw columns x P row lanes per block, nrc row chunks of rchunk rows
+struct SnTiling {
+  int cw, P, rchunk, nrc, cw2;
+};
+static SnTiling sn_tiling(int64_t rows, int64_t cols) {
+  SnTiling t;
+  t.cw = (int)std::min<int64_t>(cols, 256);
+  t.P = 256 / t.cw;
+  const int64_t cb = cdiv(cols, (int64_t)t.cw);
+  // at least 8 rows per lane; about 1024 blocks over the column tiles
+  const int64_t want = std::max<int64_t>(16, 1024 / cb);
+  t.nrc = (int)std::max<int64_t>(1, std::min<int64_t>({want, 256, cdiv(rows, (int64_t)t.P * 8)}));
+  t.rchunk = (int)cdiv(rows, (int64_t)t.nrc);
+  t.nrc = (int)cdiv(rows, (int64_t)t.rchunk);
+  t.cw2 = (int)std::min<int64_t>(cols, t.nrc > 32 ? 64 : 256);
+  return t;
 }
 
 static size_t sn_job_ws(int64_t rows, int64_t cols) {
-  int rc, nrc;
-  sn_chunks(rows, rc, nrc);
-  return align256((size_t)nrc * cols * 4) + align256((size_t)rows * 4) + align256((size_t)cdiv(cols, 256) * 8);
+  const SnTiling t = sn_tiling(rows, cols);
+  return align256((size_t)t.nrc * cols * 4) + align256((size_t)rows * 4) + align256((size_t)cdiv(cols, (int64_t)t.cw2) * 8);
 }
 
 size_t sn_ws_bytes(int64_t rows, int64_t cols) { return sn_job_ws(rows, cols); }
@@ -185,7 +226,8 @@ void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, f
     SnJobK& k = g.j[i];
     k.W = a.W; k.u = a.u; k.v = a.v; k.sigma = a.sigma; k.u_save = nullptr;
     k.rows = (int)a.rows; k.cols = (int)a.cols;
-    sn_chunks(a.rows, k.rchunk, k.nrc);
+    const SnTiling tl = sn_tiling(a.rows, a.cols);
+    k.cw = tl.cw; k.P = tl.P; k.rchunk = tl.rchunk; k.nrc = tl.nrc; k.cw2 = tl.cw2;
     k.part = (float*)w;
     k.s = (float*)(w + align256((size_t)k.nrc * a.cols * 4));
     k.tsq = (double*)(w + align256((size_t)k.nrc * a.cols * 4) + align256((size_t)a.rows * 4));
@@ -197,8 +239,8 @@ void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, f
     o1[i] = b1;
     o2[i] = b2;
     o3[i] = b3;
-    b1 += (int)cdiv(g.j[i].cols, 256) * g.j[i].nrc;
-    b2 += (int)cdiv(g.j[i].cols, 256);
+    b1 += (int)cdiv(g.j[i].cols, g.j[i].cw) * g.j[i].nrc;
+    b2 += (int)cdiv(g.j[i].cols, g.j[i].cw2);
     b3 += (int)cdiv(g.j[i].rows, 4);
   }
   o1[n] = b1;
@@ -501,14 +543,14 @@ void fold_pool4_wgrad(hipStream_t st, const float* dw4, int Np, int Cp, float* d
 // in the padded forward layout [Np][R][R][Cp]; W: master [Cout][R][R][Cin].
 //   dW = (s dWsn - s <dWsn, W/sigma> u v^T) / sigma,  s = *scale (1 if null),
 // v indexed by (r, s, c).  Launch 1 forms fixed-order block partials of
-// <dWsn, W>; launch 2 sums a weight's partials (the same order in every
-// block) and applies the update elementwise.
-constexpr int kSnbParts = 256;
-
+// <dWsn, W> (up to kSnbParts blocks per weight); launch 2 sums a weight's
+// partials (the same order in every block) and applies the update.  Both
+// take 4 consecutive elements of a row (tap) per thread when Cin % 4 == 0
+// (16-byte accesses, one division per 4 elements), else one.
 struct SnBwdJobK {
   const float *dwp, *W, *u, *v, *sigma, *scale;
   float *dW, *part;
-  int Cout, Cin, RR, Cp, nparts;
+  int Cout, Cin, RR, Cp, nparts, vec;
 };
 struct SnBwdGroupK {
   SnBwdJobK j[kSnGroupMax];
@@ -523,10 +565,27 @@ __global__ __launch_bounds__(256) void k_sngb_dot(SnBwdGroupK g) {
   const int lb = blockIdx.x - g.off[i];
   const int total = J.Cout * J.RR * J.Cin;      // < 2^31 (host-checked)
   float acc = 0.f;
-  for (int e = lb * 256 + (int)threadIdx.x; e < total; e += J.nparts * 256) {
-    const int t = e / J.Cin;
-    const int c = e - t * J.Cin;
-    acc = fmaf(J.dwp[(int64_t)t * J.Cp + c], J.W[e], acc);
+  if (J.vec) {
+    const int q = total >> 2;                   // groups of 4 (Cin % 4 == 0)
+    float a1 = 0.f;
+    int e4 = lb * 256 + (int)threadIdx.x;
+    const int step = J.nparts * 256;
+    for (; e4 < q; e4 += step) {
+      const int e = 4 * e4, t = e / J.Cin, c = e - t * J.Cin;
+      const float4 d = *reinterpret_cast<const float4*>(J.dwp + (int64_t)t * J.Cp + c);
+      const float4 w = *reinterpret_cast<const float4*>(J.W + e);
+      acc = fmaf(d.x, w.x, acc);
+      a1 = fmaf(d.y, w.y, a1);
+      acc = fmaf(d.z, w.z, acc);
+      a1 = fmaf(d.w, w.w, a1);
+    }
+    acc += a1;
+  } else {
+    for (int e = lb * 256 + (int)threadIdx.x; e < total; e += J.nparts * 256) {
+      const int t = e / J.Cin;
+      const int c = e - t * J.Cin;
+      acc = fmaf(J.dwp[(int64_t)t * J.Cp + c], J.W[e], acc);
+    }
   }
   const float s = block_sum<256>(acc, sh);
   if (threadIdx.x == 0) J.part[lb] = s;
@@ -537,19 +596,32 @@ __global__ __launch_bounds__(256) void k_sngb_apply(SnBwdGroupK g) {
   const int i = find_job(g.off, g.n, blockIdx.x);
   const SnBwdJobK& J = g.j[i];
   const int lb = blockIdx.x - g.off[i];
-  const float p = (int)threadIdx.x < J.nparts ? J.part[threadIdx.x] : 0.f;
+  float p = 0.f;
+  for (int k = (int)threadIdx.x; k < J.nparts; k += 256) p += J.part[k];
   const float sig = *J.sigma;
   const float extra = J.scale ? *J.scale : 1.f;
   const float dot = block_sum<256>(p, sh) / sig * extra;   // s <dWsn, W/sigma>
   const float inv = 1.f / sig;
   const int total = J.Cout * J.RR * J.Cin;
-  const int e = lb * 256 + (int)threadIdx.x;
-  if (e >= total) return;
-  const int t = e / J.Cin;        // n * RR + tap
-  const int c = e - t * J.Cin;
-  const int n = t / J.RR;
-  const int k = e - n * J.RR * J.Cin;   // column index (tap, c)
-  J.dW[e] = (extra * J.dwp[(int64_t)t * J.Cp + c] - dot * J.u[n] * J.v[k]) * inv;
+  const int per = J.vec ? 4 : 1;
+  const int units = total / per;
+  const int nb = g.off[i + 1] - g.off[i];
+  for (int q = lb * 256 + (int)threadIdx.x; q < units; q += nb * 256) {
+    const int e = q * per;
+    const int t = e / J.Cin;        // n * RR + tap
+    const int c = e - t * J.Cin;
+    const int n = t / J.RR;
+    const int k = e - n * J.RR * J.Cin;   // column index (tap, c)
+    const float un = dot * J.u[n];
+    if (J.vec) {
+      const float4 d = *reinterpret_cast<const float4*>(J.dwp + (int64_t)t * J.Cp + c);
+      const float4 v = *reinterpret_cast<const float4*>(J.v + k);
+      *reinterpret_cast<float4*>(J.dW + e) = make_float4((extra * d.x - un * v.x) * inv, (extra * d.y - un * v.y) * inv,
+                                                         (extra * d.z - un * v.z) * inv, (extra * d.w - un * v.w) * inv);
+    } else {
+      J.dW[e] = (extra * J.dwp[(int64_t)t * J.Cp + c] - un * J.v[k]) * inv;
+    }
+  }
 }
 
 void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part) {
@@ -563,9 +635,13 @@ void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part) {
     const SnBwdJob& a = jobs[i];
     const int64_t total = (int64_t)a.Cout * a.R * a.R * a.Cin;
     PG_CHECK(total < (1LL << 31) && (int64_t)a.Cout * a.R * a.R * a.Cp < (1LL << 40), "sn bwd group: shape");
-    const int np = (int)std::max<int64_t>(1, std::min<int64_t>(kSnbParts, cdiv(total, 256 * 16)));
+    // 4-wide when rows are whole float4s in both layouts and every buffer is 16-byte aligned
+    const bool vec = a.Cin % 4 == 0 && a.Cp % 4 == 0 && (((uintptr_t)a.dwp | (uintptr_t)a.W | (uintptr_t)a.v |
+                                                          (uintptr_t)a.dW) & 15) == 0;
+    const int64_t units = vec ? total / 4 : total;
+    const int np = (int)std::max<int64_t>(1, std::min<int64_t>(kSnbParts, cdiv(units, 256 * 8)));
     g.j[i] = SnBwdJobK{a.dwp, a.W, a.u, a.v, a.sigma, a.scale, a.dW, part + (int64_t)i * kSnbParts,
-                       a.Cout, a.Cin, a.R * a.R, a.Cp, np};
+                       a.Cout, a.Cin, a.R * a.R, a.Cp, np, vec ? 1 : 0};
     g.off[i] = b1;
     b1 += np;
   }
@@ -573,7 +649,8 @@ void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part) {
   g2 = g;
   for (int i = 0; i < n; ++i) {
     g2.off[i] = (int)b2;
-    b2 += cdiv((int64_t)g.j[i].Cout * g.j[i].RR * g.j[i].Cin, 256);
+    const int64_t total = (int64_t)g.j[i].Cout * g.j[i].RR * g.j[i].Cin;
+    b2 += cdiv(g.j[i].vec ? total / 4 : total, 256 * 8);   // up to 8 units per thread
   }
   g2.off[n] = (int)b2;
   PG_CHECK(b2 < (1LL << 31), "sn bwd group: too large");
@@ -584,7 +661,7 @@ void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part) {
 
 void sn_bwd(hipStream_t st, const float* dwp, const float* W, const float* u, const float* v,
             const float* sigma, int Cout, int Cin, int R, int Cp, const float* scale, float* dW,
-            float* part /* >= 256 floats */) {
+            float* part /* kSnbParts floats */) {
   const SnBwdJob j{dwp, W, u, v, sigma, scale, dW, Cout, Cin, R, Cp};
   sn_bwd_group(st, &j, 1, part);
 }

@@ -49,7 +49,8 @@ struct SnBwdJob {
   float* dW;
   int Cout, Cin, R, Cp;
 };
-// part: >= 256 floats per job
+// part: kSnbParts floats per job (the fixed-order partials of <dWsn, W>)
+constexpr int kSnbParts = 1024;
 void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part);
 // dw[n][r][s][c] (3x3) = 1/4 sum_{a,b in {0,1}} dw4[n][r+a][s+b][c]: the gradient
 // of a 3x3 filter from that of its pooled stride-2 4x4 form

@@ -183,7 +183,7 @@ static GNetWs gnet_carve(const Arch& a, int B, const std::vector<GBlock>& blocks
   r.g1 = w.bytes(maxact * 2);
   r.dlin = w.f32(16LL * c0 * a.zc);
   r.dcond = w.f32((size_t)B * a.dc);
-  r.part = w.f32(256);
+  r.part = w.f32(kSnbParts);
   GOut head;
   head.B = B; head.H = a.img; head.W = a.img; head.C = a.g_mult[a.n_g] * a.ch;
   r.head_bytes = head.ws_size();
@@ -272,7 +272,7 @@ static GOutWs gout_carve(const GOut& g, Arena& w) {
   GOutWs r;
   r.da = w.f32((size_t)M * cpad(g.C));
   r.dw = w.f32(27LL * g.C);
-  r.part = w.f32(256);
+  r.part = w.f32(kSnbParts);
   r.red_bytes = std::max({ghead_ws_bytes(g.B, g.H, g.W, g.C), bn_bwd_ws_bytes(g.B, g.H * g.W, g.C),
                           bn_stats_ws_bytes(M, g.C), sn_ws_bytes(3, 27LL * g.C)});
   r.red = w.bytes(r.red_bytes);
@@ -362,7 +362,7 @@ static DNetWs dnet_carve(const Arch& a, int N, const std::vector<DBlock>& blocks
   r.g1 = w.bytes(maxact * 2);
   r.dw = w.f32(c);
   r.dE = w.f32((size_t)a.n_classes * c);
-  r.part = w.f32(256);
+  r.part = w.f32(kSnbParts);
   r.blk_bytes = blk;
   r.blk = w.bytes(blk);
   return r;

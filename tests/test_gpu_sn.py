@@ -18,6 +18,7 @@ SHAPES = [
     (512, 2304), (192, 1728),              # config-2 conv1, a 64x64 G conv
     (1536, 13824),                         # the largest 3x3 conv (1536 -> 1536)
     (1000, 1536), (24, 192),               # class embedding, attention theta
+    (24576, 20), (3000, 5), (1000, 70),    # the z linear (16*1536 x 20), narrow tiles with idle lanes
 ]
 
 
