@@ -288,6 +288,7 @@ struct PackJobK {
   const float* sigma;
   void* dst;
   int Cout, Cin, R, Np, Cp, mode;
+  int wvec;   // filter rows are whole float4s (Cin % 4 == 0)
 };
 struct PackGroupK {
   PackJobK j[kSnGroupMax];
@@ -318,6 +319,21 @@ PG_DEV void store4f<float>(float* p, const float* v) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
+// four consecutive channels c .. c + 3 of filter row `row` (zeros past Cin):
+// one 16-byte load when the rows are whole float4s.  A tensor of the flat
+// parameter buffer starts at any float offset; global memory accepts the
+// unaligned vector access.
+PG_DEV void ld4w(const float* W, int64_t row, int Cin, int c, bool wvec, float* v) {
+  const float* p = W + row * Cin + c;
+  if (wvec && c + 4 <= Cin) {
+    const float4 f = *reinterpret_cast<const float4*>(p);
+    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+  } else {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) v[q] = c + q < Cin ? p[q] : 0.f;
+  }
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
   __shared__ float tile[64][65];
@@ -334,20 +350,24 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     const int t = e / J.Cp;     // n * 16 + u * 4 + v
     const int c = e - t * J.Cp;
     const int n = t >> 4, u = (t >> 2) & 3, v = t & 3;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    if (n < J.Cout && c < J.Cin) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float acc = 0.f;
-      if (n < J.Cout && c + q < J.Cin) {
+      for (int a = 0; a < 2; ++a)
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+        for (int b2 = 0; b2 < 2; ++b2) {
+          const int r = u - a, s_ = v - b2;
+          if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) {
+            float w4[4];
+            ld4w(J.W, (int64_t)n * 9 + r * 3 + s_, J.Cin, c, J.wvec, w4);
 #pragma unroll
-          for (int b2 = 0; b2 < 2; ++b2) {
-            const int r = u - a, s_ = v - b2;
-            if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) acc += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + c + q];
+            for (int q = 0; q < 4; ++q) acc[q] += w4[q];
           }
-      }
-      st<T>(dst, (int64_t)e + q, acc * (0.25f * inv));
+        }
     }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[q] *= 0.25f * inv;
+    store4f<T>(dst + e, acc);
     return;
   }
   if (J.mode == kPackSub) {
@@ -360,14 +380,18 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     const int p = pn / J.Np, n = pn - p * J.Np;
     const int a = p >> 1, b2 = p & 1;
     const int r0 = du ? 1 + a : 0, r1 = du ? 2 : a, s0 = dv ? 1 + b2 : 0, s1 = dv ? 2 : b2;
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    if (n < J.Cout && c < J.Cin)
+      for (int r = r0; r <= r1; ++r)
+        for (int s_ = s0; s_ <= s1; ++s_) {
+          float w4[4];
+          ld4w(J.W, (int64_t)n * 9 + r * 3 + s_, J.Cin, c, J.wvec, w4);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      float acc = 0.f;
-      if (n < J.Cout && c + q < J.Cin)
-        for (int r = r0; r <= r1; ++r)
-          for (int s_ = s0; s_ <= s1; ++s_) acc += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + c + q];
-      st<T>(dst, (int64_t)e + q, acc * inv);
-    }
+          for (int q = 0; q < 4; ++q) acc[q] += w4[q];
+        }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc[q] *= inv;
+    store4f<T>(dst + e, acc);
     return;
   }
   if (J.mode == kPackFwd) {
@@ -379,7 +403,7 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     const int n = t / RR;
     const float* src = J.W + (int64_t)t * J.Cin;
     float v[8];
-    if (n < J.Cout && (J.Cin & 3) == 0 && c + 8 <= J.Cin) {
+    if (n < J.Cout && J.wvec && c + 8 <= J.Cin) {
       const float4 a = *reinterpret_cast<const float4*>(src + c), b = *reinterpret_cast<const float4*>(src + c + 4);
       v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
     } else {
@@ -409,28 +433,34 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     float val[4] = {0.f, 0.f, 0.f, 0.f};
     if (n < J.Cout) {
       if (J.mode == kPackDgradSum4) {
+        if (cb < J.Cin)
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (cb + q < J.Cin)
+          for (int a = 0; a < 2; ++a)
 #pragma unroll
-            for (int a = 0; a < 2; ++a)
+            for (int b2 = 0; b2 < 2; ++b2) {
+              const int r = 2 - u + a, s_ = 2 - v + b2;
+              if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) {
+                float w4[4];
+                ld4w(J.W, (int64_t)n * 9 + r * 3 + s_, J.Cin, cb, J.wvec, w4);
 #pragma unroll
-              for (int b2 = 0; b2 < 2; ++b2) {
-                const int r = 2 - u + a, s_ = 2 - v + b2;
-                if (r >= 0 && r < 3 && s_ >= 0 && s_ < 3) val[q] += J.W[((int64_t)n * 9 + r * 3 + s_) * J.Cin + cb + q];
+                for (int q = 0; q < 4; ++q) val[q] += w4[q];
               }
+            }
       } else if (J.mode == kPackSubDgrad) {
         const int a = p >> 1, b2 = p & 1;
         const int r0 = u ? 1 + a : 0, r1 = u ? 2 : a, s0 = v ? 1 + b2 : 0, s1 = v ? 2 : b2;
+        if (cb < J.Cin)
+          for (int r = r0; r <= r1; ++r)
+            for (int s_ = s0; s_ <= s1; ++s_) {
+              float w4[4];
+              ld4w(J.W, (int64_t)n * 9 + (2 - r) * 3 + (2 - s_), J.Cin, cb, J.wvec, w4);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (cb + q < J.Cin)
-            for (int r = r0; r <= r1; ++r)
-              for (int s_ = s0; s_ <= s1; ++s_) val[q] += J.W[((int64_t)n * 9 + (2 - r) * 3 + (2 - s_)) * J.Cin + cb + q];
+              for (int q = 0; q < 4; ++q) val[q] += w4[q];
+            }
       } else {
         const int ftap = J.mode == kPackDgradRep4 ? 0 : (J.R - 1 - u) * J.R + (J.R - 1 - v);
         const float* src = J.W + ((int64_t)n * RR + ftap) * J.Cin + cb;
-        if ((J.Cin & 3) == 0 && cb + 4 <= J.Cin) {
+        if (J.wvec && cb + 4 <= J.Cin) {
           const float4 f = *reinterpret_cast<const float4*>(src);
           val[0] = f.x; val[1] = f.y; val[2] = f.z; val[3] = f.w;
         } else {
@@ -461,7 +491,7 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
   int64_t b = 0;
   for (int i = 0; i < n; ++i) {
     const PackJob& a = jobs[i];
-    g.j[i] = PackJobK{a.W, a.sigma, a.dst, a.Cout, a.Cin, a.R, a.Np, a.Cp, a.mode};
+    g.j[i] = PackJobK{a.W, a.sigma, a.dst, a.Cout, a.Cin, a.R, a.Np, a.Cp, a.mode, a.Cin % 4 == 0 ? 1 : 0};
     g.off[i] = (int)b;
     const int RR = a.R * a.R;
     const bool four = a.mode == kPackPool4 || a.mode == kPackDgradSum4;
@@ -635,9 +665,10 @@ void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part) {
     const SnBwdJob& a = jobs[i];
     const int64_t total = (int64_t)a.Cout * a.R * a.R * a.Cin;
     PG_CHECK(total < (1LL << 31) && (int64_t)a.Cout * a.R * a.R * a.Cp < (1LL << 40), "sn bwd group: shape");
-    // 4-wide when rows are whole float4s in both layouts and every buffer is 16-byte aligned
-    const bool vec = a.Cin % 4 == 0 && a.Cp % 4 == 0 && (((uintptr_t)a.dwp | (uintptr_t)a.W | (uintptr_t)a.v |
-                                                          (uintptr_t)a.dW) & 15) == 0;
+    // 4-wide when rows are whole float4s in both layouts and the workspace
+    // operands (dwp, v) are 16-byte aligned; W and dW sit in the flat
+    // parameter buffers at any float offset (unaligned vector accesses)
+    const bool vec = a.Cin % 4 == 0 && a.Cp % 4 == 0 && (((uintptr_t)a.dwp | (uintptr_t)a.v) & 15) == 0;
     const int64_t units = vec ? total / 4 : total;
     const int np = (int)std::max<int64_t>(1, std::min<int64_t>(kSnbParts, cdiv(units, 256 * 8)));
     g.j[i] = SnBwdJobK{a.dwp, a.W, a.u, a.v, a.sigma, a.scale, a.dW, part + (int64_t)i * kSnbParts,
