@@ -1,6 +1,7 @@
 // Residual-block executors: the order of kernel launches for the BigGAN
 // generator and discriminator blocks, forward and backward.
 #include "blocks.hpp"
+#include "heads.hpp"
 
 namespace pg {
 
@@ -311,7 +312,8 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
 // discriminator block
 // ======================================================================
 void DBlock::plan_saved(Arena& a) {
-  Cip = (int)cpad(cin);
+  PG_CHECK(!im2col || (9 * cin <= 32 && !f32 && !preact), "dblock: 3x3-patch input needs 9 cin <= 32, bf16, no ReLU");
+  Cip = (int)cpad(im2col ? 9 * cin : cin);
   Cop = (int)cpad(cout);
   Ho = down ? H / 2 : H;
   Wo = down ? W / 2 : W;
@@ -341,6 +343,7 @@ struct DWsB {
   void* dh;
   float* dxs;
   float* part;
+  float* dcol;   // im2col: gradient of the 3x3 patches
 };
 
 static DWsF d_carve_f(const DBlock& d, Arena& a) {
@@ -372,6 +375,7 @@ static DWsB d_carve_b(const DBlock& d, Arena& a, int n_cu) {
   w.dh = a.bytes((size_t)M * d.Cop * e);
   w.dxs = d.lsc ? a.f32((size_t)Mo * d.Cip) : nullptr;
   w.part = a.f32((size_t)kSnbParts * kSnGroupMax);
+  w.dcol = d.im2col ? a.f32((size_t)M * d.Cip) : nullptr;
   return w;
 }
 
@@ -389,16 +393,20 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   const SnJob jobs[3] = {sn_job(P, "conv1.w", sn[0]), sn_job(P, "conv2.w", sn[1]),
                          lsc ? sn_job(P, "sc.w", sn[2]) : SnJob{}};
   sn_power_iter_group(ex.st, jobs, nsn, npi, sn_eps, w.sn);
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, wp1, cout, cin, 3, Cop, Cip, kPackFwd},
+  // with 3x3-patch input, conv1 is a 1x1 filter over the 9 cin patch
+  // channels (the [Cout][3][3][cin] weight read as [Cout][9 cin]) and the
+  // skip's 1x1 filter sits on the centre tap's channels 4 cin ..
+  const int R1 = im2col ? 1 : 3, K1 = im2col ? 9 * cin : cin, ksc = im2col ? 4 * cin : 0;
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, wp1, cout, K1, R1, Cop, Cip, kPackFwd},
                          {P.w("conv2.w"), sn[1].sigma, wp2, cout, cout, 3, Cop, Cop, s2conv() ? kPackPool4 : kPackFwd},
-                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
+                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd, ksc}};
   pack_group(ex.st, f32, pk, nsn);
   // h = conv3x3([relu](x)) + b1
   ConvIn i1;
-  i1.x = x; i1.B = B; i1.Hx = H; i1.Wx = W; i1.C = Cip; i1.relu = preact; i1.c_real = cin;
+  i1.x = x; i1.B = B; i1.Hx = H; i1.Wx = W; i1.C = Cip; i1.relu = preact; i1.c_real = K1;
   ConvOut o1;
   o1.y = h; o1.y_f32 = f32; o1.yC = Cop; o1.n_real = cout; o1.bias = P.w("conv1.b");
-  conv_fwd(ex.st, f32, i1, H, W, 3, wp1, Cop, o1);
+  conv_fwd(ex.st, f32, i1, H, W, R1, wp1, Cop, o1);
   // skip = conv1x1([avgpool](x)) + bsc, fp32
   if (lsc) {
     ConvIn si;
@@ -434,10 +442,11 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   Arena a(ex.ws);
   DWsB w = d_carve_b(*this, a, ex.n_cu);
   const int64_t M = (int64_t)B * H * W, Mo = (int64_t)B * Ho * Wo;
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, w.wd1, cout, cin, 3, Cop, Cip, kPackDgrad},
+  const int R1 = im2col ? 1 : 3, K1 = im2col ? 9 * cin : cin, ksc = im2col ? 4 * cin : 0;
+  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, w.wd1, cout, K1, R1, Cop, Cip, kPackDgrad},
                          {P.w("conv2.w"), sn[1].sigma, w.wd2, cout, cout, 3, Cop, Cop,
                           subdgrad() ? kPackSubDgrad : kPackDgrad},
-                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, w.wdsc, cout, cin, 1, Cop, Cip, kPackDgrad}};
+                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, w.wdsc, cout, cin, 1, Cop, Cip, kPackDgrad, ksc}};
   pack_group(ex.st, f32, pk, lsc ? 3 : 2);
   // conv2 (its output gradient is dy, or dy/4 spread over 2x2 when pooled)
   GradIn g2;
@@ -478,9 +487,9 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   GradIn g1;
   g1.g = w.dh; g1.Hs = H; g1.Ws = W; g1.C = Cop;
   ConvIn a1;
-  a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.relu = preact; a1.c_real = cin;
+  a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.relu = preact; a1.c_real = K1;
   if (wgrad) {
-    conv_wgrad(ex.st, f32, g1, a1, H, W, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+    conv_wgrad(ex.st, f32, g1, a1, H, W, R1, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
     colsum(ex.st, f32, w.dh, M, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
   }
   // skip
@@ -499,7 +508,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
       ConvIn ds;
       ds.x = dy; ds.B = B; ds.Hx = Ho; ds.Wx = Wo; ds.C = Cop;
       ConvOut dso;
-      dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = cin;
+      dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = ksc + cin;
       conv_fwd(ex.st, f32, ds, Ho, Wo, 1, w.wdsc, Cip, dso);
     }
   }
@@ -507,7 +516,9 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     ConvIn d1;
     d1.x = w.dh; d1.B = B; d1.Hx = H; d1.Wx = W; d1.C = Cop;
     ConvOut d1o;
-    d1o.y = dx; d1o.y_f32 = dx_f32 || f32; d1o.yC = Cip; d1o.n_real = cin;
+    // with 3x3-patch input: the patch gradient (fp32), folded onto the image after
+    d1o.y = im2col ? (void*)w.dcol : dx; d1o.y_f32 = dx_f32 || f32 || im2col; d1o.yC = Cip;
+    d1o.n_real = im2col ? K1 : cin;
     if (preact) { d1o.mask = x; d1o.mask_f32 = f32; d1o.maskC = Cip; }
     if (lsc) {
       d1o.res = w.dxs; d1o.res_f32 = 1; d1o.resC = Cip;
@@ -516,12 +527,13 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     } else {
       d1o.res = dy; d1o.res_f32 = f32; d1o.resC = Cop; d1o.res_mode = R_SAME;
     }
-    conv_fwd(ex.st, f32, d1, H, W, 3, w.wd1, Cip, d1o);
+    conv_fwd(ex.st, f32, d1, H, W, R1, w.wd1, Cip, d1o);
+    if (im2col) im2col_grad(ex.st, w.dcol, B, H, W, (float*)dx);
   }
   if (!wgrad) return;
-  const SnBwdJob jobs[3] = {sn_bwd_job(P, "conv1.w", sn[0], w.dwp1, 3, Cip, nullptr),
+  const SnBwdJob jobs[3] = {sn_bwd_job(P, "conv1.w", sn[0], w.dwp1, R1, Cip, nullptr),
                             sn_bwd_job(P, "conv2.w", sn[1], w.dwp2, 3, Cop, nullptr),
-                            lsc ? sn_bwd_job(P, "sc.w", sn[2], w.dwpsc, 1, Cip, nullptr) : SnBwdJob{}};
+                            lsc ? sn_bwd_job(P, "sc.w", sn[2], w.dwpsc + ksc, 1, Cip, nullptr) : SnBwdJob{}};
   sn_bwd_group(ex.st, jobs, lsc ? 3 : 2, w.part);
 }
 

@@ -107,6 +107,10 @@ struct GBlock {
 struct DBlock {
   int B, H, W, cin, cout, npi;
   bool preact, down, lsc, f32;
+  // the input is an image in 3x3-patch form (img_to_im2col, 9 cin <= 32
+  // channels): conv1 runs as a 1x1 conv over the patches, the skip reads
+  // the centre tap, and dx is the fp32 image gradient [B][H][W][4]
+  bool im2col = false;
   float sn_eps;
   int Cip, Cop, Ho, Wo;
   SNSlot sn[3];

@@ -9,25 +9,111 @@
 
 namespace pg {
 
-// fp32 [N][H][W][3] images -> bf16 [N][H][W][Cp] (channels >= 3 zero)
-// one thread per 16-byte chunk (8 channels) of a pixel: the first chunk
-// holds the three colours, the rest are zeros
-__global__ void k_img_to_bf16(const float* img, int64_t npix, int q, bf16_t* out) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= npix * q) return;
-  const int64_t p = i / q;
-  uint4 v = make_uint4(0u, 0u, 0u, 0u);
-  if (i == p * q) {
-    v.x = f2bf2(img[p * 3], img[p * 3 + 1]);
-    v.y = f2bf2(img[p * 3 + 2], 0.f);
+// fp32 [N][H][W][3] images -> bf16 [N][H][W][32] 3x3 patches: channel
+// (r * 3 + s) * 3 + c holds img[h + r - 1][w + s - 1][c] (zero outside the
+// image), channels 27..31 zero.  The discriminator's first 3x3 conv is then
+// a 1x1 conv over 27 real channels instead of 9 taps over 3 of 32.  Both
+// this and its adjoint take kPR rows x kPC columns of one image per block:
+// the rows it needs, with a one-pixel zero frame, are staged in LDS with
+// coalesced loads, then a thread per pixel gathers from LDS.
+constexpr int kPR = 2, kPC = 128;
+
+__global__ __launch_bounds__(256) void k_img_im2col(const float* __restrict__ img, int H, int W,
+                                                    bf16_t* __restrict__ out) {
+  __shared__ float sx[kPR + 2][kPC + 2][3];
+  const int ncb = (W + kPC - 1) / kPC, nrb = (H + kPR - 1) / kPR;
+  int bid = blockIdx.x;
+  const int cb = bid % ncb;
+  bid /= ncb;
+  const int h0 = (bid % nrb) * kPR, n = bid / nrb, w0 = cb * kPC;
+  const float* im = img + (int64_t)n * H * W * 3;
+  constexpr int kNS = (kPR + 2) * (kPC + 2) * 3;
+#pragma unroll
+  for (int k = 0; k < (kNS + 255) / 256; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    if (i < kNS) {
+      const int c = i % 3, q = i / 3, col = q % (kPC + 2), row = q / (kPC + 2);
+      const int h = h0 - 1 + row, w = w0 - 1 + col;
+      (&sx[0][0][0])[i] =
+          (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W ? im[((int64_t)h * W + w) * 3 + c] : 0.f;
+    }
   }
-  reinterpret_cast<uint4*>(out)[i] = v;
+  __syncthreads();
+  // 16-byte chunk j of the block's output: pixel j / 4, channels 8 (j % 4) ..;
+  // consecutive lanes store consecutive chunks
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int j = threadIdx.x + 256 * k, px = j >> 2, qd = j & 3;
+    const int lr = px / kPC, lc = px % kPC;
+    const int h = h0 + lr, w = w0 + lc;
+    if (h >= H || w >= W) continue;
+    float v[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int ch = 8 * qd + e, tap = ch / 3, c = ch - 3 * tap;
+      v[e] = ch < 27 ? sx[lr + tap / 3][lc + tap % 3][c] : 0.f;
+    }
+    reinterpret_cast<uint4*>(out + (((int64_t)n * H + h) * W + w) * 32)[qd] = pack8(v);
+  }
 }
-void img_to_bf16(hipStream_t st, const float* img, int64_t npix, int Cp, void* out) {
-  PG_CHECK(Cp % 8 == 0 && Cp >= 8 && ((uintptr_t)out & 15) == 0, "img_to_bf16: layout");
-  const int q = Cp / 8;
-  hipLaunchKernelGGL(k_img_to_bf16, dim3((unsigned)cdiv(npix * q, 256)), dim3(256), 0, st, img, npix, q,
-                     (bf16_t*)out);
+void img_to_im2col(hipStream_t st, const float* img, int N, int H, int W, void* out) {
+  PG_CHECK(N >= 1 && H >= 1 && W >= 1 && ((uintptr_t)out & 15) == 0, "img_to_im2col: shape");
+  const int64_t blocks = (int64_t)N * cdiv(H, kPR) * cdiv(W, kPC);
+  PG_CHECK(blocks < (1LL << 31), "img_to_im2col: too many pixels");
+  hipLaunchKernelGGL(k_img_im2col, dim3((unsigned)blocks), dim3(256), 0, st, img, H, W, (bf16_t*)out);
+  PG_LAUNCH_CHECK();
+}
+
+// The adjoint: dimg[p][c] = sum_{r,s} dcol[p - (r - 1, s - 1)][(r * 3 + s) * 3 + c]
+// over the patches that contain p; dcol fp32 [N][H][W][32], dimg fp32
+// [N][H][W][4] (channel 3 written as 0).  The staged patch gradients keep
+// channels 0..27 (28 floats per pixel: a stride that spreads the lanes of a
+// gather over the LDS banks).
+constexpr int kPS = 28;
+__global__ __launch_bounds__(256) void k_im2col_grad(const float* __restrict__ dcol, int H, int W,
+                                                     float* __restrict__ dimg) {
+  __shared__ float4 sd[(kPR + 2) * (kPC + 2) * kPS / 4];
+  const int ncb = (W + kPC - 1) / kPC, nrb = (H + kPR - 1) / kPR;
+  int bid = blockIdx.x;
+  const int cb = bid % ncb;
+  bid /= ncb;
+  const int h0 = (bid % nrb) * kPR, n = bid / nrb, w0 = cb * kPC;
+  const float* dc = dcol + (int64_t)n * H * W * 32;
+  constexpr int kNS = (kPR + 2) * (kPC + 2) * (kPS / 4);
+#pragma unroll
+  for (int k = 0; k < (kNS + 255) / 256; ++k) {
+    const int i = threadIdx.x + 256 * k;
+    if (i < kNS) {
+      const int j = i % (kPS / 4), q = i / (kPS / 4), col = q % (kPC + 2), row = q / (kPC + 2);
+      const int h = h0 - 1 + row, w = w0 - 1 + col;
+      sd[i] = (unsigned)h < (unsigned)H && (unsigned)w < (unsigned)W
+                  ? *reinterpret_cast<const float4*>(dc + ((int64_t)h * W + w) * 32 + 4 * j)
+                  : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+  __syncthreads();
+  const int lr = threadIdx.x / kPC, lc = threadIdx.x % kPC;
+  const int h = h0 + lr, w = w0 + lc;
+  if (h >= H || w >= W) return;
+  const float* sf = reinterpret_cast<const float*>(sd);
+  float d[3] = {0.f, 0.f, 0.f};
+#pragma unroll
+  for (int r = 0; r < 3; ++r)
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      // the patch centred at (h - r + 1, w - s + 1) holds this pixel at tap (r, s)
+      const float* src = sf + ((lr + 2 - r) * (kPC + 2) + (lc + 2 - s)) * kPS + (r * 3 + s) * 3;
+#pragma unroll
+      for (int c = 0; c < 3; ++c) d[c] += src[c];
+    }
+  reinterpret_cast<float4*>(dimg)[((int64_t)n * H + h) * W + w] = make_float4(d[0], d[1], d[2], 0.f);
+}
+void im2col_grad(hipStream_t st, const float* dcol, int N, int H, int W, float* dimg) {
+  PG_CHECK(N >= 1 && H >= 1 && W >= 1 && ((uintptr_t)dimg & 15) == 0 && ((uintptr_t)dcol & 15) == 0,
+           "im2col_grad: shape");
+  const int64_t blocks = (int64_t)N * cdiv(H, kPR) * cdiv(W, kPC);
+  PG_CHECK(blocks < (1LL << 31), "im2col_grad: too many pixels");
+  hipLaunchKernelGGL(k_im2col_grad, dim3((unsigned)blocks), dim3(256), 0, st, dcol, H, W, dimg);
   PG_LAUNCH_CHECK();
 }
 

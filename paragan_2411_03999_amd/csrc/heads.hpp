@@ -6,7 +6,10 @@
 
 namespace pg {
 
-void img_to_bf16(hipStream_t st, const float* img, int64_t npix, int Cp, void* out);
+// fp32 [N][H][W][3] images -> bf16 [N][H][W][32] 3x3 patches (channel (r*3+s)*3+c)
+void img_to_im2col(hipStream_t st, const float* img, int N, int H, int W, void* out);
+// its adjoint: fp32 patch gradients [N][H][W][32] -> fp32 image gradient [N][H][W][4]
+void im2col_grad(hipStream_t st, const float* dcol, int N, int H, int W, float* dimg);
 
 // generator output layer (fp32): img = tanh(conv3x3(relu(bn(x))) + b)
 // Shapes the kernels take: cpad(C) <= 128, W a multiple of 4, and the

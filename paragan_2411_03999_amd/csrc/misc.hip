@@ -288,7 +288,8 @@ struct PackJobK {
   const float* sigma;
   void* dst;
   int Cout, Cin, R, Np, Cp, mode;
-  int wvec;   // filter rows are whole float4s (Cin % 4 == 0)
+  int wvec;   // filter rows are whole float4s (Cin % 4 == 0, koff % 4 == 0)
+  int koff;   // destination channel of input channel 0 (fwd and dgrad modes)
 };
 struct PackGroupK {
   PackJobK j[kSnGroupMax];
@@ -402,13 +403,14 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     const int c = e - t * J.Cp;
     const int n = t / RR;
     const float* src = J.W + (int64_t)t * J.Cin;
+    const int cs = c - J.koff;   // source channel of destination channel c
     float v[8];
-    if (n < J.Cout && J.wvec && c + 8 <= J.Cin) {
-      const float4 a = *reinterpret_cast<const float4*>(src + c), b = *reinterpret_cast<const float4*>(src + c + 4);
+    if (n < J.Cout && J.wvec && cs >= 0 && cs + 8 <= J.Cin) {
+      const float4 a = *reinterpret_cast<const float4*>(src + cs), b = *reinterpret_cast<const float4*>(src + cs + 4);
       v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
     } else {
 #pragma unroll
-      for (int q = 0; q < 8; ++q) v[q] = (n < J.Cout && c + q < J.Cin) ? src[c + q] : 0.f;
+      for (int q = 0; q < 8; ++q) v[q] = (n < J.Cout && cs + q >= 0 && cs + q < J.Cin) ? src[cs + q] : 0.f;
     }
 #pragma unroll
     for (int q = 0; q < 8; ++q) v[q] *= inv;
@@ -459,13 +461,14 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
             }
       } else {
         const int ftap = J.mode == kPackDgradRep4 ? 0 : (J.R - 1 - u) * J.R + (J.R - 1 - v);
-        const float* src = J.W + ((int64_t)n * RR + ftap) * J.Cin + cb;
-        if (J.wvec && cb + 4 <= J.Cin) {
+        const int cs = cb - J.koff;   // source channel of destination channel cb
+        const float* src = J.W + ((int64_t)n * RR + ftap) * J.Cin + cs;
+        if (J.wvec && cs >= 0 && cs + 4 <= J.Cin) {
           const float4 f = *reinterpret_cast<const float4*>(src);
           val[0] = f.x; val[1] = f.y; val[2] = f.z; val[3] = f.w;
         } else {
 #pragma unroll
-          for (int q = 0; q < 4; ++q) val[q] = cb + q < J.Cin ? src[q] : 0.f;
+          for (int q = 0; q < 4; ++q) val[q] = cs + q >= 0 && cs + q < J.Cin ? src[q] : 0.f;
         }
       }
     }
@@ -491,7 +494,10 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
   int64_t b = 0;
   for (int i = 0; i < n; ++i) {
     const PackJob& a = jobs[i];
-    g.j[i] = PackJobK{a.W, a.sigma, a.dst, a.Cout, a.Cin, a.R, a.Np, a.Cp, a.mode, a.Cin % 4 == 0 ? 1 : 0};
+    PG_CHECK(a.koff == 0 || ((a.mode == kPackFwd || a.mode == kPackDgrad) && a.koff > 0 && a.koff + a.Cin <= a.Cp),
+             "pack group: channel offset (fwd and dgrad modes, within Cp)");
+    g.j[i] = PackJobK{a.W, a.sigma, a.dst, a.Cout, a.Cin, a.R, a.Np, a.Cp, a.mode,
+                      a.Cin % 4 == 0 && a.koff % 4 == 0 ? 1 : 0, a.koff};
     g.off[i] = (int)b;
     const int RR = a.R * a.R;
     const bool four = a.mode == kPackPool4 || a.mode == kPackDgradSum4;

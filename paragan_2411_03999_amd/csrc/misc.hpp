@@ -42,6 +42,7 @@ struct PackJob {
   void* dst;
   int Cout, Cin, R, Np, Cp;
   int mode;
+  int koff = 0;   // kPackFwd / kPackDgrad: input channel c lands at channel koff + c of dst
 };
 void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n);
 struct SnBwdJob {

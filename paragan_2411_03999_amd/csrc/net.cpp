@@ -323,6 +323,7 @@ void DNet::plan_saved(Arena& s) {
     DBlock b;
     b.B = N_; b.H = sp.H; b.W = sp.W; b.cin = sp.cin; b.cout = sp.cout; b.npi = a.npi;
     b.preact = sp.preact; b.down = sp.down; b.lsc = sp.lsc; b.f32 = false; b.sn_eps = a.sn_eps;
+    b.im2col = j == 0;   // the image enters as 3x3 patches
     b.plan_saved(s);
     blocks_.push_back(b);
     act_.push_back(s.bytes((size_t)N_ * b.Ho * b.Wo * cpad(sp.cout) * 2));
@@ -379,7 +380,7 @@ void DNet::fwd(const Exec& ex, const Params& P, const float* x, const int32_t* y
   Arena w(ex.ws);
   DNetWs r = dnet_carve(a, N_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
   Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
-  img_to_bf16(ex.st, x, (int64_t)N_ * a.img * a.img, 32, act_[0]);
+  img_to_im2col(ex.st, x, N_, a.img, a.img, act_[0]);
   const void* h = act_[0];
   for (int j = 0; j < (int)blocks_.size(); ++j) {
     blocks_[j].fwd(eb, sub(P, "d" + std::to_string(j) + "."), h, act_[j + 1]);
@@ -449,7 +450,7 @@ static StepWs step_carve(const Arch& a, int B, Arena& w, GNet& g, DNet& d2, DNet
   r.ylab = (int32_t*)w.bytes((size_t)2 * B * 4);
   r.logits = w.f32(2 * B);
   r.dout = w.f32(2 * B);
-  r.dimg = w.f32((size_t)B * pix * 32);
+  r.dimg = w.f32((size_t)B * pix * 4);
   r.dloss = w.f32(64);
   r.net_bytes = std::max({g.ws_size(n_cu), d2.ws_size(n_cu), d1.ws_size(n_cu)});
   r.net = w.bytes(r.net_bytes);
@@ -495,7 +496,7 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
   d1.fwd(ex, PD, r.ximg, in->y_g, r.logits);
   hinge(st, r.logits, 0, B, true, r.dout, r.dloss + n_D);
   d1.bwd(ex, PD, in->y_g, r.dout, r.dimg, false);
-  g.bwd(ex, PG, in->z_g, in->y_g, r.dimg, 32);
+  g.bwd(ex, PG, in->z_g, in->y_g, r.dimg, 4);
   G->adam_t += 1;
   adam(st, G->params, G->grads, G->adam_m, G->adam_v, LG.n_params, d->beta1, d->beta2, d->lr_g, d->adam_eps,
        G->adam_t);

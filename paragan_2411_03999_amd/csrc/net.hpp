@@ -79,7 +79,7 @@ class DNet {
   size_t ws_size(int n_cu);
   // x: fp32 images [N][img][img][3]; out: fp32 logits [N]
   void fwd(const Exec& ex, const Params& P, const float* x, const int32_t* y, float* out);
-  // wgrad = false: input gradient only (dimg fp32 [N][img][img][32])
+  // wgrad = false: input gradient only (dimg fp32 [N][img][img][4], channels 0..2)
   void bwd(const Exec& ex, const Params& P, const int32_t* y, const float* dout, float* dimg, bool wgrad);
 
  private:
