@@ -119,9 +119,10 @@ struct DBlock {
   void* xp = nullptr;   // 2x2 average of the input (downsampling learnable skip)
   // conv2 + 2x2 average pool as one stride-2 4x4 conv (bf16 downsampling blocks)
   bool s2conv() const { return down && !f32; }
-  // its data gradient as four sub-pixel 2x2 convs (K = 4 Cout; below 192
-  // channels the short K loses to the 3x3 form over the upsampled gradient)
-  bool subdgrad() const { return s2conv() && cout >= 192; }
+  // its data gradient as four sub-pixel 2x2 convs (K = 4 Cout; below 96
+  // channels, where no sub-pixel halo tile applies, the short K loses to the
+  // 3x3 form over the upsampled gradient)
+  bool subdgrad() const { return s2conv() && cout >= 96; }
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);
