@@ -236,32 +236,54 @@ __global__ __launch_bounds__(WM * WN * 64, 8 / (WM * WN)) void k_wgrad_tr(WgTrK 
     }
 }
 
-// dw = scale * sum over splits, in split order (few splits: a thread per output)
-__global__ void k_wgtr_reduce(const float* part, int splits, int64_t n, float scale, float* out) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  float s = 0.f;
-  for (int j = 0; j < splits; ++j) s += part[(int64_t)j * n + i];
-  out[i] = s * scale;
+// dw = scale * sum over splits, each output's splits added in split order.
+// Up to 32 splits: a thread per 4 outputs (16-byte loads, four splits in
+// flight); more: 256 outputs per block, 16 waves each summing every 16th
+// split, then the 16 sums in wave order.  n is a multiple of 4 (Kdim is).
+__global__ __launch_bounds__(256) void k_wgtr_reduce(const float* __restrict__ part, int splits, int64_t n4,
+                                                     float scale, float* __restrict__ out) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n4) return;
+  const float4* p = reinterpret_cast<const float4*>(part) + i;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  int j = 0;
+  for (; j + 4 <= splits; j += 4) {
+    float4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = p[(int64_t)(j + u) * n4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      s.x += v[u].x; s.y += v[u].y; s.z += v[u].z; s.w += v[u].w;
+    }
+  }
+  for (; j < splits; ++j) {
+    const float4 v = p[(int64_t)j * n4];
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  reinterpret_cast<float4*>(out)[i] = make_float4(s.x * scale, s.y * scale, s.z * scale, s.w * scale);
 }
 
-// Many splits: 64 outputs per block, 16 waves each summing every 16th split,
-// then the 16 sums in wave order (a fixed order, as above).
-__global__ __launch_bounds__(1024) void k_wgtr_reduce_wide(const float* part, int splits, int64_t n, float scale,
-                                                           float* out) {
-  __shared__ float sh[16][64];
+__global__ __launch_bounds__(1024) void k_wgtr_reduce_wide(const float* __restrict__ part, int splits, int64_t n4,
+                                                           float scale, float* __restrict__ out) {
+  __shared__ float4 sh[16][64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int64_t i = (int64_t)blockIdx.x * 64 + lane;
-  float s = 0.f;
-  if (i < n)
-    for (int j = wv; j < splits; j += 16) s += part[(int64_t)j * n + i];
+  const float4* p = reinterpret_cast<const float4*>(part) + i;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i < n4)
+    for (int j = wv; j < splits; j += 16) {
+      const float4 v = p[(int64_t)j * n4];
+      s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+    }
   sh[wv][lane] = s;
   __syncthreads();
-  if (wv == 0 && i < n) {
-    float t = 0.f;
+  if (wv == 0 && i < n4) {
+    float4 t = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-    for (int w = 0; w < 16; ++w) t += sh[w][lane];
-    out[i] = t * scale;
+    for (int w = 0; w < 16; ++w) {
+      t.x += sh[w][lane].x; t.y += sh[w][lane].y; t.z += sh[w][lane].z; t.w += sh[w][lane].w;
+    }
+    reinterpret_cast<float4*>(out)[i] = make_float4(t.x * scale, t.y * scale, t.z * scale, t.w * scale);
   }
 }
 
@@ -397,6 +419,8 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   k.tiles_k = p.tiles_k;
   const int64_t nout = (int64_t)Np * k.Kdim;
   if (p.splits > 1 && (size_t)p.splits * nout * 4 > ws_bytes) throw Error{-3, "conv_wgrad: workspace too small"};
+  PG_CHECK(p.splits == 1 || (nout % 4 == 0 && (((uintptr_t)ws | (uintptr_t)dw) & 15) == 0),
+           "conv_wgrad: split partials must be 16-byte aligned rows of whole float4s");
   // a single split writes the scaled result itself; several leave unscaled partials
   k.part = p.splits == 1 ? dw : (float*)ws;
   k.scale = p.splits == 1 ? g.gscale : 1.f;
@@ -417,12 +441,13 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   prof.done(name, flops, k.M, Np, k.Kdim);
   if (p.splits > 1) {
     ProfScope pr(s);
-    if (p.splits <= 8)
-      hipLaunchKernelGGL(k_wgtr_reduce, dim3((unsigned)cdiv(nout, 256)), dim3(256), 0, s, k.part, p.splits, nout,
+    const int64_t n4 = nout / 4;
+    if (p.splits <= 32)
+      hipLaunchKernelGGL(k_wgtr_reduce, dim3((unsigned)cdiv(n4, 256)), dim3(256), 0, s, k.part, p.splits, n4,
                          g.gscale, dw);
     else
-      hipLaunchKernelGGL(k_wgtr_reduce_wide, dim3((unsigned)cdiv(nout, 64)), dim3(1024), 0, s, k.part, p.splits,
-                         nout, g.gscale, dw);
+      hipLaunchKernelGGL(k_wgtr_reduce_wide, dim3((unsigned)cdiv(n4, 64)), dim3(1024), 0, s, k.part, p.splits, n4,
+                         g.gscale, dw);
     PG_LAUNCH_CHECK();
     pr.done("k_wgtr_reduce", 0.0);
   }
