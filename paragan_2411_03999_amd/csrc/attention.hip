@@ -152,7 +152,7 @@ __global__ void k_attn_pool(const bf16_t* qkv, int B, int H, int W, int Nqkv, in
 template <int DV>
 __global__ __launch_bounds__(256, 2) void k_attn_fwd(const bf16_t* qkv, int Nqkv, const bf16_t* kp,
                                                      const bf16_t* vp, int HW, int L, int Lp, int HWp, bf16_t* o,
-                                                     float* lse2) {
+                                                     float* o32, float* lse2) {
   constexpr int DK = 32, NT = DV / 32, NCV = DV / 8, QT = 2;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][32 * DK];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][32 * DV];
@@ -260,31 +260,38 @@ __global__ __launch_bounds__(256, 2) void k_attn_fwd(const bf16_t* qkv, int Nqkv
     const int q = qw + 32 * u + lq;
     const float lt = l[u] + __shfl_xor(l[u], 32, 64);
     const float inv = 1.f / lt;
-    if (q < HW) {
-      bf16_t* orow = o + ((int64_t)b * HW + q) * DV;
+    // fp32 copy in register layout: 32-query tile, then (j, i), then lane:
+    // every store is 64 lanes x 16 contiguous bytes
+    float4* const t32 = o32 && qw + 32 * u < HWp
+                            ? reinterpret_cast<float4*>(o32 + ((int64_t)b * (HWp / 32) + (qw + 32 * u) / 32) * DV * 32)
+                            : nullptr;
+    bf16_t* orow = o + ((int64_t)b * HW + q) * DV;
 #pragma unroll
-      for (int j = 0; j < NT; ++j)
+    for (int j = 0; j < NT; ++j)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const f32x16& a = acc[u][j];
-          const uint2 v = make_uint2(f2bf2(a[4 * i] * inv, a[4 * i + 1] * inv), f2bf2(a[4 * i + 2] * inv, a[4 * i + 3] * inv));
-          *reinterpret_cast<uint2*>(orow + 32 * j + 8 * i + 4 * g) = v;
-        }
-    }
+      for (int i = 0; i < 4; ++i) {
+        const f32x16& a = acc[u][j];
+        const float4 f = make_float4(a[4 * i] * inv, a[4 * i + 1] * inv, a[4 * i + 2] * inv, a[4 * i + 3] * inv);
+        if (q < HW) *reinterpret_cast<uint2*>(orow + 32 * j + 8 * i + 4 * g) = make_uint2(f2bf2(f.x, f.y), f2bf2(f.z, f.w));
+        if (t32) t32[(j * 4 + i) * 64 + lane] = f;
+      }
     if (g == 0 && q < HWp) lse2[(int64_t)b * HWp + q] = q < HW ? m2[u] + __log2f(lt) : INFINITY;
   }
 }
 
 // ------------------------------------------------------------- dQ (query-owned)
-// Pass 1: Dv[q] = sum_k P dP (the softmax backward's row term, by its
-// definition, from the same P and dP that pass 2 uses); pass 2: dQ^T = K^T dS^T.
+// One pass over the keys: dS = P (dP - Dv) and dQ^T = K^T dS^T, where the
+// softmax backward's row term Dv[q] = sum_k P dP = dO[q] . O[q] is the dot
+// product of the query's output gradient with the forward's fp32 output row
+// (normalised accumulators, before bf16 rounding), formed in the prologue.
 template <int DV>
 constexpr int dq_tiles() { return DV >= 96 ? 1 : 2; }   // query tiles per wave (register budget)
 
 template <int DV>
 __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv, const bf16_t* kp,
-                                                    const bf16_t* vp, const bf16_t* dO, const float* lse2, float* Dv,
-                                                    int HW, int L, int Lp, int HWp, bf16_t* dqkv) {
+                                                    const bf16_t* vp, const bf16_t* dO, const float* O32,
+                                                    const float* lse2, float* Dv, int HW, int L, int Lp, int HWp,
+                                                    bf16_t* dqkv) {
   constexpr int DK = 32, NCV = DV / 8, QT = dq_tiles<DV>();
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][32 * DK];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][32 * DV];
@@ -295,6 +302,7 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
   const bf16_t* K = kp + (int64_t)b * Lp * DK;
   const bf16_t* V = vp + (int64_t)b * Lp * DV;
   const bf16_t* DO = dO + (int64_t)b * HW * DV;
+  const float4* OO = reinterpret_cast<const float4*>(O32 + (int64_t)b * HWp * DV);
   bf16x8 qb[QT][2], db[QT][DV / 16];
   float lq2[QT], dd[QT];
   bool qv[QT];
@@ -304,10 +312,25 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
     qv[u] = q < HW;
 #pragma unroll
     for (int t = 0; t < 2; ++t) qb[u][t] = qv[u] ? ld8g(Q + (int64_t)q * Nqkv + 16 * t + 8 * g) : zero8();
-#pragma unroll
-    for (int t = 0; t < DV / 16; ++t) db[u][t] = qv[u] ? ld8g(DO + (int64_t)q * DV + 16 * t + 8 * g) : zero8();
-    lq2[u] = qv[u] ? lse2[(int64_t)b * HWp + q] : 0.f;
     dd[u] = 0.f;
+#pragma unroll
+    for (int t = 0; t < DV / 16; ++t) {
+      db[u][t] = qv[u] ? ld8g(DO + (int64_t)q * DV + 16 * t + 8 * g) : zero8();
+      // this lane's half of dO[q] . O[q] (channels 16 t + 8 g ..)
+      if (qv[u]) {
+        // channels 16 t + 8 g + 0..7 of query q: in the forward's register
+        // layout (j, i) = (t / 2, 2 (t % 2) + g), lanes lq and 32 + lq
+        float a[8];
+        unpack8(__builtin_bit_cast(uint4, db[u][t]), a);
+        const float4* tile = OO + (int64_t)((qw + 32 * u) / 32) * DV * 8;
+        const int ji = (t / 2) * 4 + 2 * (t % 2) + g;
+        const float4 o0 = tile[ji * 64 + lq], o1 = tile[ji * 64 + 32 + lq];
+        const float o[8] = {o0.x, o0.y, o0.z, o0.w, o1.x, o1.y, o1.z, o1.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) dd[u] = fmaf(a[e], o[e], dd[u]);
+      }
+    }
+    lq2[u] = qv[u] ? lse2[(int64_t)b * HWp + q] : 0.f;
   }
   f32x16 acc[QT];
 #pragma unroll
@@ -317,10 +340,8 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
 
   Stager<4, 1> sk;
   Stager<NCV, (32 * NCV + 255) / 256> sv;
-  // one 32-key block of a pass; PASS and TAIL are compile-time so the
-  // per-element work has no branches
-  auto block = [&](auto pass_c, auto tail_c, const bf16_t* ks, const bf16_t* vs, int k0) {
-    constexpr int PASS = decltype(pass_c)::value;
+  // one 32-key block; TAIL is compile-time so the per-element work has no branches
+  auto block = [&](auto tail_c, const bf16_t* ks, const bf16_t* vs, int k0) {
     constexpr bool TAIL = decltype(tail_c)::value;
     f32x16 s[QT], dp[QT];
 #pragma unroll
@@ -345,21 +366,18 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
       for (int r = 0; r < 16; ++r) {
         float p = exp2_(fmaf(s[u][r], kL2E, -lq2[u]));
         if (TAIL) p = k0 + acc_row(r, g) < L ? p : 0.f;
-        if (PASS == 0) dd[u] = fmaf(p, dp[u][r], dd[u]);
-        else s[u][r] = p * (dp[u][r] - dd[u]);
+        s[u][r] = p * (dp[u][r] - dd[u]);
       }
     }
-    if (PASS == 1) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const bf16x8 ka = ld_tr<4>(ks, t, 0, lane);
+    for (int t = 0; t < 2; ++t) {
+      const bf16x8 ka = ld_tr<4>(ks, t, 0, lane);
 #pragma unroll
-        for (int u = 0; u < QT; ++u)
-          acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, pack_regs(s[u], t), acc[u], 0, 0, 0);
-      }
+      for (int u = 0; u < QT; ++u)
+        acc[u] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, pack_regs(s[u], t), acc[u], 0, 0, 0);
     }
   };
-  auto run = [&](auto pass_c) {
+  auto run = [&]() {
     sk.load(K, DK, 0, Lp, tid);
     sv.load(V, DV, 0, Lp, tid);
     __syncthreads();
@@ -374,9 +392,9 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
         sv.load(V, DV, k0 + 32, Lp, tid);
       }
       if (k0 + 32 > L)
-        block(pass_c, std::integral_constant<bool, true>(), Ks[buf], Vs[buf], k0);
+        block(std::integral_constant<bool, true>(), Ks[buf], Vs[buf], k0);
       else
-        block(pass_c, std::integral_constant<bool, false>(), Ks[buf], Vs[buf], k0);
+        block(std::integral_constant<bool, false>(), Ks[buf], Vs[buf], k0);
       if (more) {
         sk.store(Ks[buf ^ 1], tid);
         sv.store(Vs[buf ^ 1], tid);
@@ -387,14 +405,13 @@ __global__ __launch_bounds__(256, 2) void k_attn_dq(const bf16_t* qkv, int Nqkv,
   };
   // invalid queries have zero Q and dO rows and lse2 0: their dS rows are
   // dropped at the store and their Dv is written as 0
-  run(std::integral_constant<int, 0>());
 #pragma unroll
   for (int u = 0; u < QT; ++u) {
     dd[u] = dd[u] + __shfl_xor(dd[u], 32, 64);
     const int q = qw + 32 * u + lq;
     if (g == 0 && q < HWp) Dv[(int64_t)b * HWp + q] = qv[u] ? dd[u] : 0.f;
   }
-  run(std::integral_constant<int, 1>());
+  run();
 #pragma unroll
   for (int u = 0; u < QT; ++u) {
     const int q = qw + 32 * u + lq;
@@ -599,33 +616,34 @@ static void check_dims(const AttnDims& a) {
 }
 
 void attn_fwd_core(hipStream_t st, const AttnDims& a, const void* qkv, const void* kp, const void* vp, void* o,
-                   float* lse2) {
+                   float* o32, float* lse2) {
   check_dims(a);
   dim3 grid((unsigned)cdiv(a.HWp, 256), a.B);
   ProfScope prof(st);
   PG_DV_DISPATCH(a.dv, hipLaunchKernelGGL(k_attn_fwd<DVc>, grid, dim3(256), 0, st, (const bf16_t*)qkv, a.Nqkv,
                                           (const bf16_t*)kp, (const bf16_t*)vp, a.HW, a.L, a.Lp, a.HWp,
-                                          (bf16_t*)o, lse2));
+                                          (bf16_t*)o, o32, lse2));
   PG_LAUNCH_CHECK();
   prof.done("k_attn_fwd<" + std::to_string(a.dv) + ">", 2.0 * a.B * (double)a.HW * a.L * (a.dk + a.dv));
 }
 
-void attn_bwd_core(hipStream_t st, const AttnDims& a, const void* qkv, const void* dO, const void* kp,
-                   const void* vp, const float* lse2, float* Dv, void* dk, void* dvv, void* dqkv) {
+void attn_bwd_core(hipStream_t st, const AttnDims& a, const void* qkv, const void* dO, const float* o32,
+                   const void* kp, const void* vp, const float* lse2, float* Dv, void* dk, void* dvv, void* dqkv) {
   check_dims(a);
   dim3 gk((unsigned)cdiv(a.Lp, 128), a.B);
   ProfScope prof(st);
   PG_DV_DISPATCH(a.dv, {
     dim3 gq((unsigned)cdiv(a.HWp, 128 * dq_tiles<DVc>()), a.B);
     hipLaunchKernelGGL(k_attn_dq<DVc>, gq, dim3(256), 0, st, (const bf16_t*)qkv, a.Nqkv, (const bf16_t*)kp,
-                       (const bf16_t*)vp, (const bf16_t*)dO, lse2, Dv, a.HW, a.L, a.Lp, a.HWp, (bf16_t*)dqkv);
+                       (const bf16_t*)vp, (const bf16_t*)dO, o32, lse2, Dv, a.HW, a.L, a.Lp, a.HWp,
+                       (bf16_t*)dqkv);
     hipLaunchKernelGGL(k_attn_dkv<DVc>, gk, dim3(256), 0, st, (const bf16_t*)qkv, a.Nqkv, (const bf16_t*)kp,
                        (const bf16_t*)vp, (const bf16_t*)dO, lse2, Dv, a.HW, a.L, a.Lp, a.HWp, (bf16_t*)dk,
                        (bf16_t*)dvv);
   });
-  // dQ: 2 passes of S and dP plus dQ; dK/dV: S, dP, dV, dK
+  // executed: dQ pass S, dP, dQ; dK/dV pass S, dP, dV, dK
   prof.done("k_attn_bwd<" + std::to_string(a.dv) + ">",
-            2.0 * a.B * (double)a.HW * a.L * (3 * a.dk + 4 * a.dv));
+            2.0 * a.B * (double)a.HW * a.L * (4 * a.dk + 3 * a.dv));
   const int64_t n = (int64_t)a.B * a.L * ((a.dk + a.dv) / 8);
   PG_CHECK(a.dv % 8 == 0 && n < (1LL << 31) && (int64_t)a.B * a.H * a.W * a.Nqkv < (1LL << 31),
            "attention pool: size");

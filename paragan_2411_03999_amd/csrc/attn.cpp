@@ -33,6 +33,7 @@ void Attn::plan_saved(Arena& a) {
   kp = a.bytes((size_t)B * d.Lp * dk * 2);
   vp = a.bytes((size_t)B * d.Lp * dv * 2);
   o = a.bytes((size_t)B * d.HW * dv * 2);
+  o32 = a.f32((size_t)B * d.HWp * dv);
   lse = a.f32((size_t)B * d.HWp);
 }
 
@@ -71,7 +72,7 @@ size_t Attn::ws_size(int n_cu) const {
 
 static const char* kASN[4] = {"theta", "phi", "g", "o"};
 
-void Attn::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
+void Attn::fwd(const Exec& ex, const Params& P, const void* x, void* y, bool for_bwd) {
   const AttnDims d = dims(*this);
   SnJob jobs[4];
   for (int i = 0; i < 4; ++i) jobs[i] = sn_job(P, kASN[i], sn[i]);
@@ -87,7 +88,7 @@ void Attn::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   po.y = qkv; po.yC = Nqkv; po.n_real = Nqkv;
   conv_fwd(ex.st, false, in, H, W, 1, wqkv, Nqkv, po);
   attn_pool(ex.st, d, qkv, kp, vp);
-  attn_fwd_core(ex.st, d, qkv, kp, vp, o, lse);
+  attn_fwd_core(ex.st, d, qkv, kp, vp, o, for_bwd ? o32 : nullptr, lse);
   ConvIn oi;
   oi.x = o; oi.B = B; oi.Hx = H; oi.Wx = W; oi.C = dv;
   ConvOut oo;
@@ -118,7 +119,7 @@ void Attn::bwd(const Exec& ex, const Params& P, const void* x, const void* dy, v
   ConvOut dOo;
   dOo.y = w.dO; dOo.yC = dv; dOo.n_real = dv; dOo.acc_scale = gamma;
   conv_fwd(ex.st, false, di, H, W, 1, w.wdo, dv, dOo);
-  attn_bwd_core(ex.st, d, qkv, w.dO, kp, vp, lse, w.Dv, w.dk, w.dvv, w.dqkv);
+  attn_bwd_core(ex.st, d, qkv, w.dO, o32, kp, vp, lse, w.Dv, w.dk, w.dvv, w.dqkv);
   // projections
   GradIn gq;
   gq.g = w.dqkv; gq.Hs = H; gq.Ws = W; gq.C = Nqkv;

@@ -142,10 +142,13 @@ struct Attn {
   void *qkv = nullptr;       // [B][H][W][Nqkv] bf16 projections (pre-pool)
   void *kp = nullptr, *vp = nullptr;   // pooled keys / values
   void *o = nullptr;         // attention output [B][HW][dv] bf16
+  float* o32 = nullptr;      // the same in fp32 for the backward's row term dO . O, in the
+                             // attention kernels' register layout ([B][HWp / 32][dv / 32][4][64][4])
   float* lse = nullptr;      // [B][HWp] log2-sum-exp2 of the scores
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
-  void fwd(const Exec& ex, const Params& P, const void* x, void* y);
+  // for_bwd = false: no backward will follow (o32 is not written)
+  void fwd(const Exec& ex, const Params& P, const void* x, void* y, bool for_bwd = true);
   void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool wgrad = true);
 };
 

@@ -199,7 +199,7 @@ size_t GNet::ws_size(int n_cu) {
   return w.off;
 }
 
-void GNet::fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img) {
+void GNet::fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img, bool for_bwd) {
   const Arch& a = a_;
   Arena w(ex.ws);
   GNetWs r = gnet_carve(a, B_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
@@ -213,7 +213,7 @@ void GNet::fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y
     blocks_[i].fwd(eb, sub(P, "g" + std::to_string(i) + "."), h, cond_[i], act_[i + 1]);
     h = act_[i + 1];
     if (i == attn_after_) {
-      attn_.fwd(eb, sub(P, "attn."), h, attn_out_);
+      attn_.fwd(eb, sub(P, "attn."), h, attn_out_, for_bwd);
       h = attn_out_;
     }
   }
@@ -484,7 +484,7 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
     PG_HIP(hipMemcpyAsync(r.ximg, in->x_real[k], (size_t)B * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
     PG_HIP(hipMemcpyAsync(r.ylab, in->y_real[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
     PG_HIP(hipMemcpyAsync(r.ylab + B, in->y_fake[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
-    g.fwd(ex, PG, in->z_fake[k], in->y_fake[k], r.ximg + (size_t)B * pix * 3);
+    g.fwd(ex, PG, in->z_fake[k], in->y_fake[k], r.ximg + (size_t)B * pix * 3, false);
     d2.fwd(ex, PD, r.ximg, r.ylab, r.logits);
     hinge(st, r.logits, B, B, false, r.dout, r.dloss + k);
     d2.bwd(ex, PD, r.ylab, r.dout, nullptr, true);

@@ -53,7 +53,8 @@ class GNet {
   void plan_saved(Arena& s);
   size_t ws_size(int n_cu);
   // img: fp32 [B][img][img][3]
-  void fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img);
+  // for_bwd = false: no backward will follow this forward
+  void fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img, bool for_bwd = true);
   // dimg: fp32 [B][img][img][ldd]
   void bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, const float* dimg, int ldd);
 
