@@ -934,45 +934,63 @@ void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc
 // activation type: the BN(+ReLU) operand of the next convolution, computed
 // once per element instead of once per filter tap.  Padded channels get 0.
 // One thread per (pixel, 8 channels): 16-byte loads and stores.
+// Block layout of the elementwise BN passes: P = 256 / CC row lanes of CC
+// 8-channel groups (a pixel's 16-byte chunks in lane order, so a row lane
+// reads whole pixel rows), each thread walking kBnRows rows P apart; the
+// per-channel constants stay in registers, the per-image tables are reloaded
+// only when a row starts a new image.
+constexpr int kBnRows = 4;
+
 template <typename T>
-__global__ __launch_bounds__(256) void k_bn_apply(const T* x, int64_t n8, int CC, FastDiv fdCC, FastDiv fdHW,
-                                                  int C, const float* mean, const float* scale,
-                                                  const float* shift, int tab_stride, int relu, T* out) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n8) return;
-  const int p = (int)fdiv((uint32_t)i, fdCC);
-  const int c0 = ((int)i - p * CC) * 8;
-  const int b = (int)fdiv((uint32_t)p, fdHW);
-  float v[8], mu[8], sc[8], sh[8];
-  load8f<T>(x + i * 8, v);
-  const int64_t tb = (int64_t)b * tab_stride;
+__global__ __launch_bounds__(256) void k_bn_apply(const T* x, int64_t M, int CC, FastDiv fdHW, int C, int Cp,
+                                                  const float* mean, const float* scale, const float* shift,
+                                                  int tab_stride, int relu, T* out) {
+  const int P = 256 / CC;
+  const int cg = (int)threadIdx.x % CC, ro = (int)threadIdx.x / CC;
+  if (ro >= P) return;
+  const int c0 = cg * 8;
+  const int64_t r0 = (int64_t)blockIdx.x * P * kBnRows + ro;
+  float mu[8], sc[8], sh[8];
   load8f<float>(mean + c0, mu);
-  load8f<float>(scale + tb + c0, sc);
-  load8f<float>(shift + tb + c0, sh);
+  int bcur = -1;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    float y = (v[e] - mu[e]) * sc[e] + sh[e];
-    if (relu) y = fmaxf(y, 0.f);
-    v[e] = c0 + e < C ? y : 0.f;
+  for (int k = 0; k < kBnRows; ++k) {
+    const int64_t p = r0 + (int64_t)k * P;
+    if (p >= M) break;
+    const int b = (int)fdiv((uint32_t)p, fdHW);
+    if (b != bcur) {
+      const int64_t tb = (int64_t)b * tab_stride;
+      load8f<float>(scale + tb + c0, sc);
+      load8f<float>(shift + tb + c0, sh);
+      bcur = b;
+    }
+    float v[8];
+    load8f<T>(x + p * Cp + c0, v);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float y = (v[e] - mu[e]) * sc[e] + sh[e];
+      if (relu) y = fmaxf(y, 0.f);
+      v[e] = c0 + e < C ? y : 0.f;
+    }
+    store8f<T>(out + p * Cp + c0, v);
   }
-  store8f<T>(out + i * 8, v);
 }
 
 void bn_apply(hipStream_t st, bool f32, const void* x, int64_t M, int HW, int C, int Cp, const float* mean,
               const float* scale, const float* shift, int tab_stride, bool relu, void* out) {
   const int CC = Cp / 8;
-  const int64_t n8 = M * CC;
-  if (n8 == 0) return;
-  PG_CHECK(Cp % 8 == 0 && tab_stride % 8 == 0 && n8 < (1LL << 31), "bn_apply: shape");
+  if (M == 0) return;
+  PG_CHECK(Cp % 8 == 0 && CC <= 256 && tab_stride % 8 == 0 && M * CC < (1LL << 31), "bn_apply: shape");
   PG_CHECK(((uintptr_t)mean | (uintptr_t)scale | (uintptr_t)shift) % 16 == 0, "bn_apply: table alignment");
-  const FastDiv fdCC = make_fastdiv(CC), fdHW = make_fastdiv(HW);
-  dim3 g((unsigned)cdiv(n8, 256));
+  const FastDiv fdHW = make_fastdiv(HW);
+  const int64_t rows_blk = (int64_t)(256 / CC) * kBnRows;
+  dim3 g((unsigned)cdiv(M, rows_blk));
   if (f32)
-    hipLaunchKernelGGL(k_bn_apply<float>, g, dim3(256), 0, st, (const float*)x, n8, CC, fdCC, fdHW, C, mean,
-                       scale, shift, tab_stride, (int)relu, (float*)out);
+    hipLaunchKernelGGL(k_bn_apply<float>, g, dim3(256), 0, st, (const float*)x, M, CC, fdHW, C, Cp, mean, scale,
+                       shift, tab_stride, (int)relu, (float*)out);
   else
-    hipLaunchKernelGGL(k_bn_apply<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, n8, CC, fdCC, fdHW, C, mean,
-                       scale, shift, tab_stride, (int)relu, (bf16_t*)out);
+    hipLaunchKernelGGL(k_bn_apply<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, M, CC, fdHW, C, Cp, mean, scale,
+                       shift, tab_stride, (int)relu, (bf16_t*)out);
   PG_LAUNCH_CHECK();
 }
 
@@ -1323,41 +1341,52 @@ __global__ __launch_bounds__(1024) void k_bnb_fin2(const float* p1, const float*
   }
 }
 
-// pass 3: dx = rstd * (gain * dz - A - xhat * Bc) (+ res, at the same pixel);
-// a thread per (pixel, 8 channels), 16-byte loads and stores.
+// pass 3: dx = rstd * (gain * dz - A - xhat * Bc) (+ res, at the same pixel),
+// in the block layout of k_bn_apply (16-byte loads and stores).
 template <typename T>
-__global__ __launch_bounds__(256) void k_bnb_apply(const float* g, int g_up2, const T* x, int64_t n8, int CC,
-                                                   FastDiv fdCC, FastDiv fdHW, FastDiv fdW, int HW, int H, int W,
-                                                   int C, int Cp, const float* mean, const float* rstd,
-                                                   const float* gain, const float* bias, int tab_stride,
-                                                   const float* A, const float* Bc, const float* res, T* dx) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n8) return;
-  const int p = (int)fdiv((uint32_t)i, fdCC);
-  const int c0 = ((int)i - p * CC) * 8;
-  const int b = (int)fdiv((uint32_t)p, fdHW);
-  const int r = p - b * HW;
-  float xv[8], gv[8], mu[8], rs[8], ga[8], be[8], aa[8], bb[8];
-  load8f<T>(x + (int64_t)p * Cp + c0, xv);
-  load_g8(g, g_up2, p, b, r, fdW, H, W, Cp, c0, gv);
+__global__ __launch_bounds__(256) void k_bnb_apply(const float* g, int g_up2, const T* x, int64_t M, int CC,
+                                                   FastDiv fdHW, FastDiv fdW, int HW, int H, int W, int C, int Cp,
+                                                   const float* mean, const float* rstd, const float* gain,
+                                                   const float* bias, int tab_stride, const float* A,
+                                                   const float* Bc, const float* res, T* dx) {
+  const int P = 256 / CC;
+  const int cg = (int)threadIdx.x % CC, ro = (int)threadIdx.x / CC;
+  if (ro >= P) return;
+  const int c0 = cg * 8;
+  const int64_t r0 = (int64_t)blockIdx.x * P * kBnRows + ro;
+  float mu[8], rs[8], aa[8], bb[8], ga[8], be[8];
   load8f<float>(mean + c0, mu);
   load8f<float>(rstd + c0, rs);
-  load8f<float>(gain + (int64_t)b * tab_stride + c0, ga);
-  load8f<float>(bias + (int64_t)b * tab_stride + c0, be);
   load8f<float>(A + c0, aa);
   load8f<float>(Bc + c0, bb);
-  float rv[8];
-  if (res) load8f<float>(res + (int64_t)p * Cp + c0, rv);
-  float out[8];
+  int bcur = -1;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const float xh = (xv[e] - mu[e]) * rs[e];
-    const float dz = (ga[e] * xh + be[e] > 0.f) ? gv[e] : 0.f;
-    float o = rs[e] * (ga[e] * dz - aa[e] - xh * bb[e]);
-    if (res) o += rv[e];
-    out[e] = c0 + e < C ? o : 0.f;
+  for (int k = 0; k < kBnRows; ++k) {
+    const int64_t p = r0 + (int64_t)k * P;
+    if (p >= M) break;
+    const int b = (int)fdiv((uint32_t)p, fdHW);
+    if (b != bcur) {
+      load8f<float>(gain + (int64_t)b * tab_stride + c0, ga);
+      load8f<float>(bias + (int64_t)b * tab_stride + c0, be);
+      bcur = b;
+    }
+    const int r = (int)(p - (int64_t)b * HW);
+    float xv[8], gv[8];
+    load8f<T>(x + p * Cp + c0, xv);
+    load_g8(g, g_up2, p, b, r, fdW, H, W, Cp, c0, gv);
+    float rv[8];
+    if (res) load8f<float>(res + p * Cp + c0, rv);
+    float out[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float xh = (xv[e] - mu[e]) * rs[e];
+      const float dz = (ga[e] * xh + be[e] > 0.f) ? gv[e] : 0.f;
+      float o = rs[e] * (ga[e] * dz - aa[e] - xh * bb[e]);
+      if (res) o += rv[e];
+      out[e] = c0 + e < C ? o : 0.f;
+    }
+    store8f<T>(dx + p * Cp + c0, out);
   }
-  store8f<T>(dx + (int64_t)p * Cp + c0, out);
 }
 
 size_t bn_bwd_ws_bytes(int B, int HW, int C) {
@@ -1393,16 +1422,15 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
                      tab_stride, (int64_t)B * HW, dgain, dbias, A, Bc, dg_stride);
   const int64_t M = (int64_t)B * HW;
   const int CC = Cp / 8;
-  const int64_t n8 = M * CC;
-  PG_CHECK(n8 < (1LL << 31) && M < (1LL << 31), "bn_bwd: too large");
-  dim3 g3((unsigned)cdiv(n8, 256));
-  const FastDiv fdCC = make_fastdiv(CC), fdHW = make_fastdiv(HW);
+  PG_CHECK(M * CC < (1LL << 31) && M < (1LL << 31) && CC <= 256, "bn_bwd: too large");
+  dim3 g3((unsigned)cdiv(M, (int64_t)(256 / CC) * kBnRows));
+  const FastDiv fdHW = make_fastdiv(HW);
   if (f32)
-    hipLaunchKernelGGL(k_bnb_apply<float>, g3, dim3(256), 0, st, g, (int)g_up2, (const float*)x, n8, CC, fdCC,
-                       fdHW, fdW, HW, H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (float*)dx);
+    hipLaunchKernelGGL(k_bnb_apply<float>, g3, dim3(256), 0, st, g, (int)g_up2, (const float*)x, M, CC, fdHW, fdW,
+                       HW, H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (float*)dx);
   else
-    hipLaunchKernelGGL(k_bnb_apply<bf16_t>, g3, dim3(256), 0, st, g, (int)g_up2, (const bf16_t*)x, n8, CC, fdCC,
-                       fdHW, fdW, HW, H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (bf16_t*)dx);
+    hipLaunchKernelGGL(k_bnb_apply<bf16_t>, g3, dim3(256), 0, st, g, (int)g_up2, (const bf16_t*)x, M, CC, fdHW,
+                       fdW, HW, H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (bf16_t*)dx);
   PG_LAUNCH_CHECK();
 }
 
