@@ -157,7 +157,8 @@ static GWsB g_carve_b(const GBlock& g, Arena& a, int n_cu) {
   for (int i = 0; i < 4; ++i) w.dlin[i] = a.f32((size_t)(i < 2 ? g.cin : g.cout) * g.dc);
   w.wg_bytes = std::max({conv_wgrad_ws(g.f32, M2, 3, g.Cip, g.Cop, n_cu),
                          conv_wgrad_ws(g.f32, M2, 3, g.Cop, g.Cop, n_cu),
-                         conv_wgrad_ws(g.f32, M2, 1, g.Cip, g.Cop, n_cu)});
+                         conv_wgrad_ws(g.f32, M2, 1, g.Cip, g.Cop, n_cu),
+                         g.f32 ? (size_t)0 : wgrad_sub_ws(M1, g.Cip, g.Cop, n_cu)});
   w.wg = a.bytes(w.wg_bytes);
   w.cs = a.bytes(colsum_ws_bytes(M2, g.Cop));
   w.dxs = a.f32((size_t)M1 * g.Cip);
@@ -273,7 +274,14 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   gdh.g = w.dh1; gdh.Hs = H2; gdh.Ws = W2; gdh.C = Cop;
   ConvIn ia1;
   ia1.x = a1; ia1.B = B; ia1.Hx = H; ia1.Wx = W; ia1.C = Cip; ia1.gather = G_UP2;
-  conv_wgrad(ex.st, f32, gdh, ia1, H2, W2, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+  if (!f32) {
+    // bf16: the four sub-pixel 2x2 forms over a1 itself, folded onto the 3x3 filter
+    ConvIn src = ia1;
+    src.gather = G_DIRECT;
+    wgrad_sub(ex.st, gdh, src, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+  } else {
+    conv_wgrad(ex.st, f32, gdh, ia1, H2, W2, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+  }
   colsum(ex.st, f32, w.dh1, M2, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
   // da1 = the 2x2 sum (the upsample's adjoint) of conv1^T dh1: in bf16 one
   // stride-2 4x4 conv straight to the low resolution; in fp32 at 2x

@@ -88,6 +88,16 @@ void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in,
 // upsampled operands without a BN-affine prologue.  wgrad_tr_ok tells whether
 // a call qualifies; conv_wgrad dispatches to it.
 bool wgrad_tr_ok(const GradIn& g, const ConvIn& in, int H, int W, int R, int Np);
+
+// bf16 weight gradient of a 3x3 conv over a nearest 2x upsample of in (the
+// source, [B][Hx][Wx][C], direct gather) against g ([B][2 Hx][2 Wx][g.C]),
+// through the four sub-pixel 2x2 forms and a fold onto the 3x3 filter:
+// dw fp32 [Np][3][3][in.C] = g.gscale * the same sums as conv_wgrad over the
+// upsampled operand.  ws: wgrad_sub_ws bytes (per-class partials).
+bool wgrad_sub_ok(const GradIn& g, const ConvIn& in, int Np);
+size_t wgrad_sub_ws(int64_t Msrc, int Cin, int Np, int n_cu);
+void wgrad_sub(hipStream_t s, const GradIn& g, const ConvIn& in, int Np, float* dw, void* ws, size_t ws_bytes,
+               int n_cu);
 size_t wgrad_tr_ws(int64_t M, int R, int Cin, int Np, int n_cu);
 void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, int R, int Np, float* dw,
               void* ws, size_t ws_bytes, int n_cu, double flops);

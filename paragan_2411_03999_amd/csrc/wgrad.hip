@@ -5,8 +5,10 @@
 // where X~ is the im2col view of the activation (direct, a nearest 2x
 // upsample of a half-resolution tensor, or read at stride 2 for a 4x4 filter
 // over a tensor of twice the grid's size; optionally ReLU'd) and dY the
-// output gradient (direct, or a nearest 2x upsample of a half-resolution
-// gradient).
+// output gradient (direct, a nearest 2x upsample of a half-resolution
+// gradient, or one parity class (2i + a, 2j + b) of a double-resolution
+// gradient: the sub-pixel form of a 3x3 conv over a 2x upsample, see
+// wgrad_sub).
 // The reduction runs over pixels, which are the rows of both operands in
 // memory, so each MFMA operand is a transposed tile.  Here both tiles are
 // copied row-major into LDS unchanged (16-byte loads and stores) and the
@@ -61,10 +63,13 @@ struct WgTrK {
   int Hs, Ws;        // gradient source dims (upsampled gradient)
   int M;             // conv-grid pixels
   FastDiv fdW, fdH, fdC, fdR;
-  int m_per_split, tiles_n, tiles_k;
+  int m_per_split, tiles_n, tiles_k, splits;
   float scale;       // applied to the sums written (1 when splits are reduced later)
-  float* part;       // [splits][Np][Kdim]
+  float* part;       // [splits][Np][Kdim]; parity mode: [4][splits][Np][Kdim]
 };
+
+// gradient operand modes
+constexpr int kGDirect = 0, kGUp2 = 1, kGParity = 2;
 
 PG_DEV int remap_block(int bid, int total) {
   // Blocks go round-robin to the 8 XCDs; give each XCD a contiguous run of
@@ -77,7 +82,7 @@ PG_DEV int remap_block(int bid, int total) {
   return bid;
 }
 
-template <int WM, int WN, int TM, int TN, bool GUP, int XG, bool RELU>
+template <int WM, int WN, int TM, int TN, int GM, int XG, bool RELU>
 __global__ __launch_bounds__(WM * WN * 64, 8 / (WM * WN)) void k_wgrad_tr(WgTrK k) {
   constexpr int NT = WM * WN * 64;   // 4 or 8 waves
   constexpr int BN = WM * TM * 32, BK = WN * TN * 32;
@@ -96,6 +101,11 @@ __global__ __launch_bounds__(WM * WN * 64, 8 / (WM * WN)) void k_wgrad_tr(WgTrK 
   const int mend = min(mbeg + k.m_per_split, k.M);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
+  // parity mode: class (pa, pb) of the gradient's pixels; the 2x2 filter's
+  // tap (r, s) reads the source at (i + r - 1 + pa, j + s - 1 + pb)
+  const int par = GM == kGParity ? (int)blockIdx.y : 0;
+  const int pa = par >> 1, pb = par & 1;
+  const int pad_r = GM == kGParity ? 1 - pa : k.pad, pad_s = GM == kGParity ? 1 - pb : k.pad;
 
   // ---- per-thread load slots (fixed across stages)
   int g_row[GIT], g_col[GIT], g_lds[GIT];
@@ -123,7 +133,7 @@ __global__ __launch_bounds__(WM * WN * 64, 8 / (WM * WN)) void k_wgrad_tr(WgTrK 
     x_row[i] = row;
     // tap offsets relative to the padding; an off slot gets an offset that
     // fails every bounds check
-    x_rs[i] = on ? (((r - k.pad) & 0xffff) | ((s - k.pad) << 16)) : (0x4000 | (0x4000 << 16));
+    x_rs[i] = on ? (((r - pad_r) & 0xffff) | ((s - pad_s) << 16)) : (0x4000 | (0x4000 << 16));
     x_c[i] = c;
     x_lds[i] = lds_off<BK>(row < kMS ? row : 0, ch * 8);
   }
@@ -136,14 +146,15 @@ __global__ __launch_bounds__(WM * WN * 64, 8 / (WM * WN)) void k_wgrad_tr(WgTrK 
     for (int i = 0; i < GIT; ++i) {
       const int m = mb + g_row[i];
       int off;
-      if (!GUP) {
+      if (GM == kGDirect) {
         off = m * k.gC + g_col[i];
       } else {
         const int t = (int)fdiv((uint32_t)m, k.fdW);
         const int ow = m - t * k.W;
         const int b = (int)fdiv((uint32_t)t, k.fdH);
         const int oh = t - b * k.H;
-        off = ((b * k.Hs + (oh >> 1)) * k.Ws + (ow >> 1)) * k.gC + g_col[i];
+        off = GM == kGUp2 ? ((b * k.Hs + (oh >> 1)) * k.Ws + (ow >> 1)) * k.gC + g_col[i]
+                          : ((b * k.Hs + 2 * oh + pa) * k.Ws + 2 * ow + pb) * k.gC + g_col[i];
       }
       rg[i] = buf_ld16(gr, g_on[i] && m < mend ? 2u * (uint32_t)off : kOOB);
     }
@@ -221,7 +232,7 @@ __global__ __launch_bounds__(WM * WN * 64, 8 / (WM * WN)) void k_wgrad_tr(WgTrK 
     buf ^= 1;
   }
 
-  float* part = k.part + (int64_t)split * k.Np * k.Kdim;
+  float* part = k.part + ((int64_t)par * k.splits + split) * k.Np * k.Kdim;
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -285,6 +296,35 @@ __global__ __launch_bounds__(1024) void k_wgtr_reduce_wide(const float* __restri
     }
     reinterpret_cast<float4*>(out)[i] = make_float4(t.x * scale, t.y * scale, t.z * scale, t.w * scale);
   }
+}
+
+// Fold of the sub-pixel weight gradients onto the 3x3 filter:
+//   dw[n][r][s][c] = scale * sum over parities (a, b), then splits, of
+//                    part[(2a + b) * splits + sp][n][(D_a(r) * 2 + D_b(s)) * C + c],
+// D_0 = (0, 1, 1), D_1 = (0, 0, 1): the 2x2 tap that 3x3 tap r feeds in
+// parity class a.  Four consecutive channels per thread (C % 4 == 0).
+__global__ __launch_bounds__(256) void k_wgrad_fold_sub(const float* __restrict__ part, int splits, int Np, int C,
+                                                        float scale, float* __restrict__ dw) {
+  const int C4 = C / 4;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)Np * 9 * C4) return;
+  const int c4 = (int)(i % C4);
+  const int64_t t = i / C4;
+  const int tap = (int)(t % 9), n = (int)(t / 9);
+  const int r = tap / 3, s_ = tap % 3;
+  const int64_t plane = (int64_t)Np * 4 * C;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int ab = 0; ab < 4; ++ab) {
+    const int a = ab >> 1, b = ab & 1;
+    const int du = a == 0 ? (r > 0) : (r == 2), dv = b == 0 ? (s_ > 0) : (s_ == 2);
+    const float* src = part + (int64_t)ab * splits * plane + ((int64_t)n * 4 + du * 2 + dv) * C + 4 * c4;
+    for (int sp = 0; sp < splits; ++sp) {
+      const float4 v = *reinterpret_cast<const float4*>(src + sp * plane);
+      acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+    }
+  }
+  reinterpret_cast<float4*>(dw)[i] = make_float4(acc.x * scale, acc.y * scale, acc.z * scale, acc.w * scale);
 }
 
 struct TrCfg {
@@ -353,21 +393,35 @@ TrPlan tr_plan(int64_t M, int R, int Cin, int Np, int n_cu) {
 }
 
 template <int WM, int WN, int TM, int TN>
-std::string launch_tr(hipStream_t s, const WgTrK& k, int blocks, bool gup, int xg, bool relu) {
-#define PG_WTR_CASE(GU, XG, RL)                                                                    \
-  if (gup == GU && xg == XG && relu == RL) {                                                       \
-    hipLaunchKernelGGL((k_wgrad_tr<WM, WN, TM, TN, GU, XG, RL>), dim3(blocks), dim3(64 * WM * WN), 0, s, k); \
-    return "k_wgrad_tr<" + std::to_string(WM * TM * 32) + "x" + std::to_string(WN * TN * 32) +    \
-           "," #GU "," #XG "," #RL ">";                                                            \
+std::string launch_tr(hipStream_t s, const WgTrK& k, int blocks, int gm, int xg, bool relu) {
+#define PG_WTR_CASE(GM, XG, RL, NAME)                                                                      \
+  if (gm == GM && xg == XG && relu == RL) {                                                                \
+    hipLaunchKernelGGL((k_wgrad_tr<WM, WN, TM, TN, GM, XG, RL>), dim3(blocks, GM == kGParity ? 4 : 1),      \
+                       dim3(64 * WM * WN), 0, s, k);                                                       \
+    return "k_wgrad_tr<" + std::to_string(WM * TM * 32) + "x" + std::to_string(WN * TN * 32) + "," NAME "," \
+           #XG "," #RL ">";                                                                                \
   }
-  PG_WTR_CASE(false, G_DIRECT, false)
-  PG_WTR_CASE(false, G_DIRECT, true)
-  PG_WTR_CASE(true, G_DIRECT, false)
-  PG_WTR_CASE(true, G_DIRECT, true)
-  PG_WTR_CASE(false, G_UP2, false)
-  PG_WTR_CASE(false, G_S2, true)
+  PG_WTR_CASE(kGDirect, G_DIRECT, false, "false")
+  PG_WTR_CASE(kGDirect, G_DIRECT, true, "false")
+  PG_WTR_CASE(kGUp2, G_DIRECT, false, "true")
+  PG_WTR_CASE(kGUp2, G_DIRECT, true, "true")
+  PG_WTR_CASE(kGDirect, G_UP2, false, "false")
+  PG_WTR_CASE(kGDirect, G_S2, true, "false")
+  PG_WTR_CASE(kGParity, G_DIRECT, false, "SUB")
 #undef PG_WTR_CASE
   throw Error{-2, "wgrad_tr: unsupported gather combination"};
+}
+
+std::string launch_cfg_tr(hipStream_t s, int cfg, const WgTrK& k, int blocks, int gm, int xg, bool relu) {
+  switch (cfg) {
+    case 0: return launch_tr<2, 2, 4, 2>(s, k, blocks, gm, xg, relu);
+    case 1: return launch_tr<2, 2, 2, 4>(s, k, blocks, gm, xg, relu);
+    case 2: return launch_tr<2, 2, 3, 3>(s, k, blocks, gm, xg, relu);
+    case 3: return launch_tr<1, 4, 3, 2>(s, k, blocks, gm, xg, relu);
+    case 4: return launch_tr<1, 4, 3, 3>(s, k, blocks, gm, xg, relu);
+    case 5: return launch_tr<2, 2, 2, 2>(s, k, blocks, gm, xg, relu);
+    default: return launch_tr<4, 2, 2, 4>(s, k, blocks, gm, xg, relu);
+  }
 }
 
 }  // namespace
@@ -417,6 +471,7 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   k.m_per_split = p.m_per_split;
   k.tiles_n = p.tiles_n;
   k.tiles_k = p.tiles_k;
+  k.splits = p.splits;
   const int64_t nout = (int64_t)Np * k.Kdim;
   if (p.splits > 1 && (size_t)p.splits * nout * 4 > ws_bytes) throw Error{-3, "conv_wgrad: workspace too small"};
   PG_CHECK(p.splits == 1 || (nout % 4 == 0 && (((uintptr_t)ws | (uintptr_t)dw) & 15) == 0),
@@ -425,18 +480,10 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   k.part = p.splits == 1 ? dw : (float*)ws;
   k.scale = p.splits == 1 ? g.gscale : 1.f;
   const int blocks = p.splits * p.tiles_n * p.tiles_k;
-  const bool gup = g.gather == G_UP2;
+  const int gm = g.gather == G_UP2 ? kGUp2 : kGDirect;
   std::string name;
   ProfScope prof(s);
-  switch (p.cfg) {
-    case 0: name = launch_tr<2, 2, 4, 2>(s, k, blocks, gup, in.gather, in.relu); break;
-    case 1: name = launch_tr<2, 2, 2, 4>(s, k, blocks, gup, in.gather, in.relu); break;
-    case 2: name = launch_tr<2, 2, 3, 3>(s, k, blocks, gup, in.gather, in.relu); break;
-    case 3: name = launch_tr<1, 4, 3, 2>(s, k, blocks, gup, in.gather, in.relu); break;
-    case 4: name = launch_tr<1, 4, 3, 3>(s, k, blocks, gup, in.gather, in.relu); break;
-    case 5: name = launch_tr<2, 2, 2, 2>(s, k, blocks, gup, in.gather, in.relu); break;
-    default: name = launch_tr<4, 2, 2, 4>(s, k, blocks, gup, in.gather, in.relu); break;
-  }
+  name = launch_cfg_tr(s, p.cfg, k, blocks, gm, in.gather, in.relu);
   PG_LAUNCH_CHECK();
   prof.done(name, flops, k.M, Np, k.Kdim);
   if (p.splits > 1) {
@@ -451,6 +498,83 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
     PG_LAUNCH_CHECK();
     pr.done("k_wgtr_reduce", 0.0);
   }
+}
+
+// ---- sub-pixel weight gradient of a 3x3 conv over a nearest 2x upsample
+// The forward runs that conv as four 2x2 convs over the source grid, one per
+// parity class (a, b) of the output pixels, each with the filter sums
+//   W_ab[n][du][dv] = sum of W[n][r][s] over r in S(a, du), s in S(b, dv)
+// (S(a, 0) = [0, a], S(a, 1) = [1 + a, 2]).  Each 3x3 tap sits in exactly one
+// sum per class, so dW[n][r][s] = sum over (a, b) of dW_ab[n][D_a(r)][D_b(s)],
+// and dW_ab = sum over the class's pixels of dY (x) (the 2x2 window of the
+// source): 4/9 of the upsampled form's MACs, on the unexpanded source.
+static TrPlan sub_plan(int64_t Msrc, int Cin, int Np, int n_cu) {
+  // four parity classes share the CUs
+  return tr_plan(Msrc, 2, Cin, Np, std::max(1, n_cu / 4));
+}
+
+size_t wgrad_sub_ws(int64_t Msrc, int Cin, int Np, int n_cu) {
+  const TrPlan p = sub_plan(Msrc, Cin, Np, n_cu);
+  return align256((size_t)4 * p.splits * Np * 4 * Cin * 4);
+}
+
+bool wgrad_sub_ok(const GradIn& g, const ConvIn& in, int Np) {
+  if (in.mean || in.relu || in.gather != G_DIRECT || g.gather != G_DIRECT || in.gscale != 1.f) return false;
+  const int64_t xs = (int64_t)in.B * in.Hx * in.Wx * in.C;
+  const int64_t gs = (int64_t)in.B * g.Hs * g.Ws * g.C;
+  return g.Hs == 2 * in.Hx && g.Ws == 2 * in.Wx && xs < (1LL << 31) && gs < (1LL << 31) && 2 * xs < kBufMax &&
+         2 * gs < kBufMax && in.C % 8 == 0 && g.C % 8 == 0 && Np % 8 == 0;
+}
+
+void wgrad_sub(hipStream_t s, const GradIn& g, const ConvIn& in, int Np, float* dw, void* ws, size_t ws_bytes,
+               int n_cu) {
+  PG_CHECK(wgrad_sub_ok(g, in, Np), "wgrad_sub: operands");
+  const int H = in.Hx, W = in.Wx;
+  WgTrK k;
+  k.g = (const bf16_t*)g.g;
+  k.x = (const bf16_t*)in.x;
+  k.x_bytes = 2LL * in.B * H * W * in.C;
+  k.g_bytes = 2LL * in.B * g.Hs * g.Ws * g.C;
+  k.gC = g.C;
+  k.Np = Np;
+  k.Kdim = 4 * in.C;
+  k.C = in.C;
+  k.R = 2;
+  k.pad = 0;   // per parity in the kernel
+  k.H = H;
+  k.W = W;
+  k.Hx = H;
+  k.Wx = W;
+  k.Hs = g.Hs;
+  k.Ws = g.Ws;
+  k.M = (int)((int64_t)in.B * H * W);
+  k.fdW = make_fastdiv(W);
+  k.fdH = make_fastdiv(H);
+  k.fdC = make_fastdiv(in.C);
+  k.fdR = make_fastdiv(2);
+  const TrPlan p = sub_plan(k.M, in.C, Np, n_cu);
+  k.m_per_split = p.m_per_split;
+  k.tiles_n = p.tiles_n;
+  k.tiles_k = p.tiles_k;
+  k.splits = p.splits;
+  const size_t need = (size_t)4 * p.splits * Np * k.Kdim * 4;
+  if (need > ws_bytes) throw Error{-3, "wgrad_sub: workspace too small"};
+  PG_CHECK(in.C % 4 == 0 && (((uintptr_t)ws | (uintptr_t)dw) & 15) == 0, "wgrad_sub: alignment");
+  k.part = (float*)ws;
+  k.scale = 1.f;
+  const int blocks = p.splits * p.tiles_n * p.tiles_k;
+  ProfScope prof(s);
+  const std::string name = launch_cfg_tr(s, p.cfg, k, blocks, kGParity, G_DIRECT, false);
+  PG_LAUNCH_CHECK();
+  // executed MACs: four classes of M source pixels x 4 taps
+  const double flops = 2.0 * 4.0 * k.M * (g.n_real ? g.n_real : Np) * 4.0 * (in.c_real ? in.c_real : in.C);
+  prof.done(name, flops, 4LL * k.M, Np, k.Kdim);
+  ProfScope pr(s);
+  const int64_t n4 = (int64_t)Np * 9 * in.C / 4;
+  hipLaunchKernelGGL(k_wgrad_fold_sub, dim3((unsigned)cdiv(n4, 256)), dim3(256), 0, s, (const float*)k.part,
+                     p.splits, Np, in.C, g.gscale, dw);
+  PG_LAUNCH_CHECK();
+  pr.done("k_wgrad_fold_sub", 0.0);
 }
 
 }  // namespace pg
