@@ -228,14 +228,17 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
   bf16_t(*const Xs)[BM * KS] = reinterpret_cast<bf16_t(*)[BM * KS]>(lds);
   bf16_t(*const Ws)[WR * KS] = reinterpret_cast<bf16_t(*)[WR * KS]>(lds + NS * BM * KS);
 
-  const int bid = remap_tile2(blockIdx.x, k.tiles_m * k.tiles_n);
+  // sub-pixel gather: the parity class (a, b) of this block's output pixels
+  // varies fastest, so the four classes of a tile run back to back on one
+  // XCD and their interleaved output pixels meet in its L2
+  const int lin = remap_tile2(blockIdx.x, k.tiles_m * k.tiles_n * (GATHER == G_SUB ? 4 : 1));
+  const int par = GATHER == G_SUB ? (lin & 3) : 0;
+  const int bid = GATHER == G_SUB ? (lin >> 2) : lin;
   const int tmi = bid / k.tiles_n, tni = bid - tmi * k.tiles_n;
   const int m0 = tmi * BM, n0 = tni * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave / WM, wm = wave % WM;
-  // sub-pixel parity class (a, b) of this block's output pixels
-  const int par = GATHER == G_SUB ? (int)blockIdx.y : 0;
   const int pa = par >> 1, pb = par & 1;
   const int C = k.C, R = k.R, pad = k.pad;
 
@@ -387,14 +390,15 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
   constexpr int EPI = NW * 32 * SROW * 2 + 2 * BN;
   __shared__ __attribute__((aligned(16))) bf16_t lds[RING > EPI ? RING : EPI];
 
-  const int bid = remap_tile2(blockIdx.x, k.tiles_m * k.tiles_n);
+  // sub-pixel gather: parity class fastest (as in k_conv_fwd)
+  const int lin = remap_tile2(blockIdx.x, k.tiles_m * k.tiles_n * (GK == G_SUB ? 4 : 1));
+  const int par = GK == G_SUB ? (lin & 3) : 0;
+  const int bid = GK == G_SUB ? (lin >> 2) : lin;
   const int tmi = bid / k.tiles_n, tni = bid - tmi * k.tiles_n;
   const int m0 = tmi * BM, n0 = tni * BN;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wn = wave / WM, wm = wave % WM;
-  // sub-pixel parity class (a, b) of this block's output pixels
-  const int par = GK == G_SUB ? (int)blockIdx.y : 0;
   const int pa = par >> 1, pb = par & 1;
   const int C = k.C, H = k.H, W = k.W, PC = W + 2;
   // the tile: rows tr0 .. tr0 + TR - 1 of image b (the host checks that W
@@ -525,7 +529,7 @@ std::string launch_halo(hipStream_t s, CfK& k, bool relu) {
   k.tiles_m = (int)cdiv(k.M, BM);
   k.tiles_n = (int)cdiv(k.Np, BN);
   k.ksteps = (GK == G_SUB ? 4 : 9) * (k.C / 32);
-  dim3 grid(k.tiles_m * k.tiles_n, GK == G_SUB ? 4 : 1), block(64 * WN * WM);
+  dim3 grid(k.tiles_m * k.tiles_n * (GK == G_SUB ? 4 : 1)), block(64 * WN * WM);
   const std::string name = "k_conv_halo<" + std::to_string(BN) + "x" + std::to_string(BM) +
                            (GK == G_SUB ? ",G_SUB" : "") + (relu ? ",true>" : ",false>");
   if constexpr (GK == G_DIRECT) {
@@ -552,7 +556,7 @@ std::string launch_cfg(hipStream_t s, CfK& k, int gather, bool relu) {
   k.ksteps = k.R * k.R * (k.C / KS);
   k.tiles_m = (int)cdiv(k.M, BM);
   k.tiles_n = (int)cdiv(k.Np, BN);
-  dim3 grid(k.tiles_m * k.tiles_n, gather == G_SUB ? 4 : 1), block(64 * WN * WM);
+  dim3 grid(k.tiles_m * k.tiles_n * (gather == G_SUB ? 4 : 1)), block(64 * WN * WM);
 #define PG_CF_CASE(G, R_)                                                             \
   if (gather == G && relu == R_) {                                                    \
     hipLaunchKernelGGL((k_conv_fwd<WN, WM, TN, TM, NS, KS, G, R_>), grid, block, 0, s, k); \
