@@ -128,8 +128,63 @@ PG_DEV void conv_epilogue(const CfK& k, f32x16 (&acc)[TN][TM], bf16_t* lds, int 
   float* const bsh = reinterpret_cast<float*>(lds) + NW * 32 * SROW;
   const int nw = n0 + wn * TN * 32;
   const float* const bw = bsh + wn * TN * 32;
+  // raw 16-byte words of a mask / residual chunk: bf16 (one word) or fp32 (two)
+  auto ld_raw = [](const void* base, bool f32, int i, uint4* w) {
+    if (f32) {
+      w[0] = *reinterpret_cast<const uint4*>((const float*)base + i);
+      w[1] = *reinterpret_cast<const uint4*>((const float*)base + i + 4);
+    } else {
+      w[0] = *reinterpret_cast<const uint4*>((const bf16_t*)base + i);
+    }
+  };
+  // the mask and residual words of output row m (at output pixel mo), channel n
+  auto load_mr = [&](int m, int mo, int n, uint4* mwt, uint4* rwt) {
+    if (o.mask) ld_raw(o.mask, o.mask_f32, mo * o.maskC + n, mwt);
+    if (o.res_mode != R_NONE) {
+      int ridx = mo;
+      if (o.res_mode == R_HALF) {
+        int bb, oh, ow;
+        pix_of(k, m, bb, oh, ow);
+        ridx = (bb * (k.H >> 1) + (oh >> 1)) * (k.W >> 1) + (ow >> 1);
+      }
+      ld_raw(o.res, o.res_f32, ridx * o.resC + n, rwt);
+    }
+  };
+  auto unpack_raw = [](const uint4* w, bool f32, float* v) {
+    if (f32) {
+      const float4 a = __builtin_bit_cast(float4, w[0]), b = __builtin_bit_cast(float4, w[1]);
+      v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w; v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+    } else {
+      unpack8(w[0], v);
+    }
+  };
+  // up to 12 chunks per pixel (TN <= 3) the mask / residual words of a pass
+  // fit in registers beside the accumulators; wider tiles load them in place
+  constexpr bool PF = TN <= 3;
 #pragma unroll
   for (int j = 0; j < TM; ++j) {
+    // this lane's chunks of the pass: output index (-1: none), and the mask
+    // and residual words, loaded before the staging barriers so that their
+    // latency overlaps the staging
+    const int mb = m0 + (wm * TM + j) * 32;
+    int yo[NQ / 2];
+    uint4 mw[NQ / 2][2], rw[NQ / 2][2];
+#pragma unroll
+    for (int t = 0; t < NQ / 2; ++t) {
+      const int c = 64 * t + lane, p = c / NQ, q = c - p * NQ;
+      const int m = mb + p, n = nw + 8 * q;
+      yo[t] = -1;
+      if (m >= k.M || n >= o.yC) continue;
+      int mo = m;
+      if (GATHER == G_SUB) {
+        // source-grid pixel (b, i, j) -> output pixel (b, 2i + a, 2j + b) of the 2x grid
+        int bb, ii, jj;
+        pix_of(k, m, bb, ii, jj);
+        mo = (bb * 2 * k.H + 2 * ii + pa) * (2 * k.W) + 2 * jj + pb;
+      }
+      yo[t] = mo * o.yC + n;
+      if (PF) load_mr(m, mo, n, mw[t], rw[t]);
+    }
     // (first pass: every wave is done with the ring; later: this wave has
     // read back the previous pass)
     __syncthreads();
@@ -142,12 +197,12 @@ PG_DEV void conv_epilogue(const CfK& k, f32x16 (&acc)[TN][TM], bf16_t* lds, int 
         *reinterpret_cast<float4*>(stg + lr * SROW + i * 32 + 8 * g4 + 4 * h) =
             make_float4(acc[i][j][4 * g4], acc[i][j][4 * g4 + 1], acc[i][j][4 * g4 + 2], acc[i][j][4 * g4 + 3]);
     __syncthreads();
-    const int mb = m0 + (wm * TM + j) * 32;
 #pragma unroll
     for (int t = 0; t < NQ / 2; ++t) {
+      if (yo[t] < 0) continue;
       const int c = 64 * t + lane, p = c / NQ, q = c - p * NQ;
-      const int m = mb + p, n = nw + 8 * q;
-      if (m >= k.M || n >= o.yC) continue;
+      const int n = nw + 8 * q;
+      if (!PF) load_mr(mb + p, yo[t] / o.yC, n, mw[t], rw[t]);
       float v[8];
       {
         const float4 a = *reinterpret_cast<const float4*>(stg + p * SROW + 8 * q);
@@ -162,28 +217,15 @@ PG_DEV void conv_epilogue(const CfK& k, f32x16 (&acc)[TN][TM], bf16_t* lds, int 
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = v[e] * accs + bv[e];
       }
-      int mo = m;
-      if (GATHER == G_SUB) {
-        // source-grid pixel (b, i, j) -> output pixel (b, 2i + a, 2j + b) of the 2x grid
-        int bb, ii, jj;
-        pix_of(k, m, bb, ii, jj);
-        mo = (bb * 2 * k.H + 2 * ii + pa) * (2 * k.W) + 2 * jj + pb;
-      }
       if (o.mask) {
         float mk[8];
-        load8(o.mask, o.mask_f32, mo * o.maskC + n, mk);
+        unpack_raw(mw[t], o.mask_f32, mk);
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] = mk[e] > 0.f ? v[e] : 0.f;
       }
       if (o.res_mode != R_NONE) {
-        int ridx = mo;
-        if (o.res_mode == R_HALF) {
-          int bb, oh, ow;
-          pix_of(k, m, bb, oh, ow);
-          ridx = (bb * (k.H >> 1) + (oh >> 1)) * (k.W >> 1) + (ow >> 1);
-        }
         float rv8[8];
-        load8(o.res, o.res_f32, ridx * o.resC + n, rv8);
+        unpack_raw(rw[t], o.res_f32, rv8);
 #pragma unroll
         for (int e = 0; e < 8; ++e) v[e] += o.res_scale * rv8[e];
       }
@@ -192,13 +234,12 @@ PG_DEV void conv_epilogue(const CfK& k, f32x16 (&acc)[TN][TM], bf16_t* lds, int 
         for (int e = 0; e < 8; ++e)
           if (n + e >= o.n_real) v[e] = 0.f;
       }
-      const int yo = mo * o.yC + n;
       if (o.y_f32) {
-        float* yp = (float*)o.y + yo;
+        float* yp = (float*)o.y + yo[t];
         *reinterpret_cast<float4*>(yp) = make_float4(v[0], v[1], v[2], v[3]);
         *reinterpret_cast<float4*>(yp + 4) = make_float4(v[4], v[5], v[6], v[7]);
       } else {
-        *reinterpret_cast<uint4*>((bf16_t*)o.y + yo) =
+        *reinterpret_cast<uint4*>((bf16_t*)o.y + yo[t]) =
             make_uint4(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]), f2bf2(v[4], v[5]), f2bf2(v[6], v[7]));
       }
     }
