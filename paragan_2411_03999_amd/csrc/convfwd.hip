@@ -414,11 +414,23 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_fwd(CfK k)
 // ring of NSW stages as in k_conv_fwd; T is a multiple of NSW, so the stage
 // of tap t is t % NSW.  Patch rows keep the 64-byte row layout and swizzle
 // of k_conv_fwd, indexed by patch pixel.
+// compile-time loop: f(std::integral_constant<int, I>) for I = B .. E - 1
+template <int B, int E, typename F>
+PG_DEV void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 template <int WN, int WM, int TN, int TM, int PPX, int GK, bool RELU>
 __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k) {
   static_assert(GK == G_DIRECT || GK == G_SUB, "halo gathers");
   constexpr int T = GK == G_SUB ? 4 : 9;       // taps per chunk
-  constexpr int NSW = GK == G_SUB ? 2 : 3;     // weight ring stages
+  // weight ring stages of one tap each: each tap's weights are issued two
+  // steps ahead (measured: for the four-tap sub-pixel chunks, two stages
+  // leave the waits exposed; deeper rings gain nothing on the nine-tap ones)
+  constexpr int NSW = 3;
   constexpr int NW = WN * WM;
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
   constexpr int RG = 16 * NW;                  // rows covered by one load of every wave
@@ -517,31 +529,31 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
   // Issue order: P(0) W(0) .. W(NSW - 2), then at step s W(s + NSW - 1)
   // and, at a chunk's first tap, P(c + 1).  Step s waits until W(s) -- and
   // with it every earlier load, P(c) among them -- has landed; still in
-  // flight may be W(s + 1) .. W(s + NSW - 2) and, at taps 1 .. NSW - 1,
-  // P(c + 1).  The barrier then also guarantees that no wave reads weight
-  // stage (s - 1) % NSW or patch buffer (c + 1) % 2 (last read in chunk
-  // c - 1) any more before they refill.
-  static_assert(T % NSW == 0 && NSW <= 3, "ring stage of a tap");
+  // flight may be W(s + 1) .. W(s + NSW - 2) (those that exist) and, at taps
+  // 1 .. NSW - 1, P(c + 1).  The barrier then also guarantees that no wave
+  // reads weight stage (s - 1) % NSW or patch buffer (c + 1) % 2 (last read
+  // in chunk c - 1) any more before they refill.
+  static_assert(NSW >= 2 && NSW <= T, "the next patch is issued within a chunk");
   const int nch = C / 32, S = T * nch;
   issue_patch(0, 0);
 #pragma unroll
   for (int st = 0; st < NSW - 1; ++st)
     if (st < S) issue_w(st, st);
+  int sb = 0;   // ring stage of the chunk's first tap, (T c) % NSW
   for (int c = 0; c < nch; ++c) {
     const bf16_t* Pc = lds + (c & 1) * PATCH;
-#pragma unroll
-    for (int t = 0; t < T; ++t) {
+    const bool more = c + 1 < nch;
+    static_for<0, T>([&](auto tc) {
+      constexpr int t = decltype(tc)::value;
+      constexpr int wfly = (NSW - 2) * BP + (t >= 1 && t <= NSW - 1 ? PLW : 0);
+      constexpr int wlast = (NSW - 2 < T - 1 - t ? NSW - 2 : T - 1 - t) * BP;
       const int s = T * c + t;
-      const bool wmore = NSW == 3 && s + 1 < S;
-      const bool pmore = t >= 1 && t <= NSW - 1 && c + 1 < nch;
-      if (wmore && pmore) wait_barrier<vm_cap(BP + PLW)>();
-      else if (wmore) wait_barrier<BP>();
-      else if (pmore) wait_barrier<PLW>();
-      else wait_barrier<0>();
-      if (s + NSW - 1 < S) issue_w((t + NSW - 1) % NSW, s + NSW - 1);
-      if (t == 0 && c + 1 < nch) issue_patch((c + 1) & 1, c + 1);
+      if (more) wait_barrier<vm_cap(wfly)>();
+      else wait_barrier<vm_cap(wlast)>();
+      if (s + NSW - 1 < S) issue_w((sb + t + NSW - 1) % NSW, s + NSW - 1);
+      if (t == 0 && more) issue_patch((c + 1) & 1, c + 1);
       const int qoff = GK == G_SUB ? ((t >> 1) + pa) * PC + (t & 1) + pb : (t / 3) * PC + (t % 3);
-      const bf16_t* Wt = lds + 2 * PATCH + (t % NSW) * WST;
+      const bf16_t* Wt = lds + 2 * PATCH + ((sb + t) % NSW) * WST;
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
         bf16x8 wv[TN], xv[TM];
@@ -559,7 +571,8 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
           for (int j = 0; j < TM; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[i], xv[j], acc[i][j], 0, 0, 0);
       }
-    }
+    });
+    sb = (sb + T) % NSW;
   }
   conv_epilogue<WN, WM, TN, TM, GK>(k, acc, lds, m0, n0, wn, wm, wave, lane, pa, pb);
 }

@@ -225,3 +225,20 @@ def test_gblock_bf16_ragged():
 
 def test_gblock_bf16_wide():
     run_gblock(B=2, H=4, W=4, cin=384, cout=192, dc=148, dtype=lib.BF16, seed=105)
+
+
+def test_gblock_biggan128_last_block():
+    """BigGAN-128's last G block, 192 -> 96 channels, 64x64 -> 128x128, bf16,
+    batch 2: the 96-channel kernels of the full model (its conv1 as four
+    sub-pixel convs over the 64x64 source, conv2 a 3x3 conv over four-row
+    tiles of the 128-wide image) at their real image shapes."""
+    run_gblock(B=2, H=64, W=64, cin=192, cout=96, dc=148, dtype=lib.BF16, seed=106)
+
+
+def test_dblock_biggan128_first_resolution():
+    """A 96 -> 96 channel D block at 128x128 -> 64x64, bf16, batch 2: the
+    stride-2 conv2 and its data gradient as four sub-pixel 2x2 convs with 96
+    output channels over the 64x64 grid, the shapes of BigGAN-128's first D
+    block after its image layer."""
+    run_dblock(B=2, H=128, W=128, cin=96, cout=96, preact=True, down=True, lsc=True, dtype=lib.BF16,
+               seed=107)
