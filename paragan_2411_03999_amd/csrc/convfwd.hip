@@ -425,8 +425,12 @@ PG_DEV void static_for(F&& f) {
 
 template <int WN, int WM, int TN, int TM, int PPX, int GK, bool RELU>
 __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k) {
-  static_assert(GK == G_DIRECT || GK == G_SUB, "halo gathers");
-  constexpr int T = GK == G_SUB ? 4 : 9;       // taps per chunk
+  static_assert(GK == G_DIRECT || GK == G_SUB || GK == G_S2, "halo gathers");
+  // Chunks: 32 channels of the source (direct, sub-pixel), or for the
+  // stride-2 4x4 filter 32 channels of one parity class (a, b) of the
+  // source pixels (2i + a, 2j + b) -- chunk c: slice c / 4, class c % 4 --
+  // a 2x2 conv over that class with the taps (2 dr + 1 - a, 2 ds + 1 - b).
+  constexpr int T = GK == G_DIRECT ? 9 : 4;    // taps per chunk
   // weight ring stages of one tap each: each tap's weights are issued two
   // steps ahead (measured: for the four-tap sub-pixel chunks, two stages
   // leave the waits exposed; deeper rings gain nothing on the nine-tap ones)
@@ -473,22 +477,29 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
     const int pr = q / PC, pc = q - pr * PC;
     const int ih = tr0 - 1 + pr, iw = pc - 1;
     const bool ok = q < npx && (unsigned)ih < (unsigned)H && (unsigned)iw < (unsigned)W;
-    poff[j] = ok ? (uint32_t)(((b * H + ih) * W + iw) * C) * 2u + 16u * lchunk : kOOB;
+    // (stride 2: the class (0, 0) pixel of the source's 2x2 window; the
+    // chunk's class adds its offset)
+    const int pix = GK == G_S2 ? (b * k.Hx + 2 * ih) * k.Wx + 2 * iw : (b * H + ih) * W + iw;
+    poff[j] = ok ? (uint32_t)(pix * C) * 2u + 16u * lchunk : kOOB;
   }
   uint32_t woff[BP];
 #pragma unroll
   for (int j = 0; j < BP; ++j) {
     const int row = 16 * (NW * j + wave) + lrow;
     const int n = n0 + row;
-    // (the sub-pixel filters are [4][Np][2][2][C], one per parity)
-    woff[j] = row < BN && n < k.Np ? (uint32_t)((par * k.Np + n) * T * C) * 2u + 16u * lchunk : kOOB;
+    // (the sub-pixel filters are [4][Np][2][2][C], one per parity; the
+    // stride-2 ones [Np][4][4][C])
+    const int wrow = GK == G_S2 ? n * 16 : (par * k.Np + n) * T;
+    woff[j] = row < BN && n < k.Np ? (uint32_t)(wrow * C) * 2u + 16u * lchunk : kOOB;
   }
   const __amdgpu_buffer_rsrc_t xr = make_rsrc(k.x, k.x_bytes);
   const __amdgpu_buffer_rsrc_t wr = make_rsrc(k.w, k.w_bytes);
   const uint32_t pl0 = lds_addr(lds + 16 * wave * 32), wl0 = lds_addr(lds + 2 * PATCH + 16 * wave * 32);
   // chunk c's patch into buffer buf
   auto issue_patch = [&](int buf, int c) {
-    const uint32_t coff = __builtin_amdgcn_readfirstlane(64u * (uint32_t)c);
+    const uint32_t coff = __builtin_amdgcn_readfirstlane(
+        GK == G_S2 ? 64u * (uint32_t)(c >> 2) + (uint32_t)((((c >> 1) & 1) * k.Wx + (c & 1)) * C) * 2u
+                   : 64u * (uint32_t)c);
     const uint32_t pl = pl0 + (uint32_t)buf * (PATCH * 2);
 #pragma unroll
     for (int j = 0; j < PLW; ++j) lds_load16(pl + j * (NW * 1024u), poff[j], coff, xr);
@@ -496,7 +507,10 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
   // weights of step s (chunk s / T, tap s % T) into stage st
   auto issue_w = [&](int st, int step) {
     const int c = step / T, t = step - T * c;
-    const uint32_t wk = __builtin_amdgcn_readfirstlane(2u * (uint32_t)(t * C + 32 * c));
+    // stride 2: tap (r, s) = (2 dr + 1 - a, 2 ds + 1 - b) of the 4x4 filter
+    const int wtap = GK == G_S2 ? (2 * (t >> 1) + 1 - ((c >> 1) & 1)) * 4 + 2 * (t & 1) + 1 - (c & 1) : t;
+    const int wch = GK == G_S2 ? 32 * (c >> 2) : 32 * c;
+    const uint32_t wk = __builtin_amdgcn_readfirstlane(2u * (uint32_t)(wtap * C + wch));
     const uint32_t wl = wl0 + (uint32_t)st * (WST * 2);
 #pragma unroll
     for (int j = 0; j < BP; ++j) lds_load16(wl + j * (NW * 1024u), woff[j], wk, wr);
@@ -534,7 +548,7 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
   // reads weight stage (s - 1) % NSW or patch buffer (c + 1) % 2 (last read
   // in chunk c - 1) any more before they refill.
   static_assert(NSW >= 2 && NSW <= T, "the next patch is issued within a chunk");
-  const int nch = C / 32, S = T * nch;
+  const int nch = (GK == G_S2 ? 4 : 1) * (C / 32), S = T * nch;
   issue_patch(0, 0);
 #pragma unroll
   for (int st = 0; st < NSW - 1; ++st)
@@ -543,6 +557,8 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
   for (int c = 0; c < nch; ++c) {
     const bf16_t* Pc = lds + (c & 1) * PATCH;
     const bool more = c + 1 < nch;
+    // the patch offset of tap (dr, ds) is (dr + ca) PC + ds + cb
+    const int ca = GK == G_S2 ? 1 - ((c >> 1) & 1) : pa, cb = GK == G_S2 ? 1 - (c & 1) : pb;
     static_for<0, T>([&](auto tc) {
       constexpr int t = decltype(tc)::value;
       constexpr int wfly = (NSW - 2) * BP + (t >= 1 && t <= NSW - 1 ? PLW : 0);
@@ -552,7 +568,7 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
       else wait_barrier<vm_cap(wlast)>();
       if (s + NSW - 1 < S) issue_w((sb + t + NSW - 1) % NSW, s + NSW - 1);
       if (t == 0 && more) issue_patch((c + 1) & 1, c + 1);
-      const int qoff = GK == G_SUB ? ((t >> 1) + pa) * PC + (t & 1) + pb : (t / 3) * PC + (t % 3);
+      const int qoff = GK != G_DIRECT ? ((t >> 1) + ca) * PC + (t & 1) + cb : (t / 3) * PC + (t % 3);
       const bf16_t* Wt = lds + 2 * PATCH + ((sb + t) % NSW) * WST;
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
@@ -574,7 +590,7 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
     });
     sb = (sb + T) % NSW;
   }
-  conv_epilogue<WN, WM, TN, TM, GK>(k, acc, lds, m0, n0, wn, wm, wave, lane, pa, pb);
+  conv_epilogue<WN, WM, TN, TM, GK == G_SUB ? G_SUB : G_DIRECT>(k, acc, lds, m0, n0, wn, wm, wave, lane, pa, pb);
 }
 
 template <int WN, int WM, int TN, int TM, int PPX, int GK>
@@ -582,15 +598,15 @@ std::string launch_halo(hipStream_t s, CfK& k, bool relu) {
   constexpr int BN = WN * TN * 32, BM = WM * TM * 32;
   k.tiles_m = (int)cdiv(k.M, BM);
   k.tiles_n = (int)cdiv(k.Np, BN);
-  k.ksteps = (GK == G_SUB ? 4 : 9) * (k.C / 32);
+  k.ksteps = (GK == G_DIRECT ? 9 : GK == G_S2 ? 16 : 4) * (k.C / 32);
   dim3 grid(k.tiles_m * k.tiles_n * (GK == G_SUB ? 4 : 1)), block(64 * WN * WM);
   const std::string name = "k_conv_halo<" + std::to_string(BN) + "x" + std::to_string(BM) +
-                           (GK == G_SUB ? ",G_SUB" : "") + (relu ? ",true>" : ",false>");
-  if constexpr (GK == G_DIRECT) {
+                           (GK == G_SUB ? ",G_SUB" : GK == G_S2 ? ",G_S2" : "") + (relu ? ",true>" : ",false>");
+  if constexpr (GK != G_SUB) {
     if (relu)
-      hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, G_DIRECT, true>), grid, block, 0, s, k);
+      hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, GK, true>), grid, block, 0, s, k);
     else
-      hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, G_DIRECT, false>), grid, block, 0, s, k);
+      hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, GK, false>), grid, block, 0, s, k);
   } else {
     if (relu) throw Error{-2, "conv_fwd: no ReLU'd operand for the sub-pixel gather"};
     hipLaunchKernelGGL((k_conv_halo<WN, WM, TN, TM, PPX, GK, false>), grid, block, 0, s, k);
@@ -710,6 +726,14 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   if (Np % 192 == 0 && in.C >= (Np % 128 == 0 ? 768 : 384) && fits_sub(128, 320))
     return launch_halo<2, 2, 3, 2, 320, G_SUB>(s, k, false);
   if (Np == 96 && fits_sub(256, 448)) return launch_halo<1, 4, 3, 2, 448, G_SUB>(s, k, false);
+  // the stride-2 4x4 filter (pooled D conv2): a patch per parity class of the source
+  const bool hs2 = in.gather == G_S2 && R == 4;
+  auto fits_s2 = [&](int bm, int ppx) {
+    const int np = halo_patch(bm, H, W);
+    return hs2 && np > 0 && np <= ppx;
+  };
+  if (Np % 192 == 0 && fits_s2(128, 320)) return launch_halo<2, 2, 3, 2, 320, G_S2>(s, k, in.relu);
+  if (Np == 96 && fits_s2(256, 448)) return launch_halo<1, 4, 3, 2, 448, G_S2>(s, k, in.relu);
   if (Np == 128) return launch_cfg<2, 2, 2, 2>(s, k, in.gather, in.relu);
   if (Np % 128 == 0) return launch_cfg<2, 2, 2, 4>(s, k, in.gather, in.relu);
   if (Np % 192 == 0) return launch_cfg<2, 2, 3, 2>(s, k, in.gather, in.relu);

@@ -242,3 +242,11 @@ def test_dblock_biggan128_first_resolution():
     block after its image layer."""
     run_dblock(B=2, H=128, W=128, cin=96, cout=96, preact=True, down=True, lsc=True, dtype=lib.BF16,
                seed=107)
+
+
+def test_dblock_biggan128_second_resolution():
+    """BigGAN-128's second D block, 96 -> 192 channels, 64x64 -> 32x32, bf16,
+    batch 2: its stride-2 conv2 with 192 output channels over four-row tiles
+    of the 32-wide output."""
+    run_dblock(B=2, H=64, W=64, cin=96, cout=192, preact=True, down=True, lsc=True, dtype=lib.BF16,
+               seed=108)
