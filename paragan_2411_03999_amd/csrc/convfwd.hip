@@ -734,6 +734,14 @@ std::string conv_fwd_mfma(hipStream_t s, const ConvIn& in, int H, int W, int R, 
   };
   if (Np % 192 == 0 && fits_s2(128, 320)) return launch_halo<2, 2, 3, 2, 320, G_S2>(s, k, in.relu);
   if (Np == 96 && fits_s2(256, 448)) return launch_halo<1, 4, 3, 2, 448, G_S2>(s, k, in.relu);
+  // eight waves on 192 x 256 where those tiles come in whole rounds over
+  // the CUs and the four-wave tiles would not
+  if (Np % 192 == 0) {
+    const int64_t t6 = cdiv(k.M, 256) * (Np / 192) * (in.gather == G_SUB ? 4 : 1), l6 = t6 % 256;
+    const int64_t t4 = cdiv(k.M, Np % 128 == 0 ? 256 : 128) * (Np % 128 == 0 ? Np / 128 : Np / 192) *
+                       (in.gather == G_SUB ? 4 : 1), l4 = t4 % 512;
+    if (t6 >= 192 && (l6 == 0 || l6 >= 192) && l4 != 0 && l4 < 384) return launch_cfg<2, 4, 3, 2>(s, k, in.gather, in.relu);
+  }
   if (Np == 128) return launch_cfg<2, 2, 2, 2>(s, k, in.gather, in.relu);
   if (Np % 128 == 0) return launch_cfg<2, 2, 2, 4>(s, k, in.gather, in.relu);
   if (Np % 192 == 0) return launch_cfg<2, 2, 3, 2>(s, k, in.gather, in.relu);

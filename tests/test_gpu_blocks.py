@@ -250,3 +250,11 @@ def test_dblock_biggan128_second_resolution():
     of the 32-wide output."""
     run_dblock(B=2, H=64, W=64, cin=96, cout=192, preact=True, down=True, lsc=True, dtype=lib.BF16,
                seed=108)
+
+
+def test_dblock_deep_resolution_768():
+    """A 768-channel D block at 8x8 (no pooling, identity skip), bf16, batch
+    192: 12288-pixel convs with 768 outputs, the shape class of BigGAN-128's
+    deep layers whose tiles fill the CUs in whole rounds only at 192 x 256."""
+    run_dblock(B=192, H=8, W=8, cin=768, cout=768, preact=True, down=False, lsc=False, dtype=lib.BF16,
+               seed=109)
