@@ -60,7 +60,16 @@ int paragan_create(paragan_ctx** out, void* hip_stream) {
   }
 }
 
-void paragan_destroy(paragan_ctx* ctx) { delete ctx; }
+void paragan_destroy(paragan_ctx* ctx) {
+  if (!ctx) return;
+  if (ctx->side) {
+    (void)hipStreamSynchronize(ctx->side);
+    (void)hipStreamDestroy(ctx->side);
+  }
+  for (hipEvent_t e : ctx->ev)
+    if (e) (void)hipEventDestroy(e);
+  delete ctx;
+}
 
 const char* paragan_last_error(const paragan_ctx* ctx) {
   return ctx ? ctx->err.c_str() : g_create_err.c_str();

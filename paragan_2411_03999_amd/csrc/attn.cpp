@@ -72,16 +72,20 @@ size_t Attn::ws_size(int n_cu) const {
 
 static const char* kASN[4] = {"theta", "phi", "g", "o"};
 
-void Attn::fwd(const Exec& ex, const Params& P, const void* x, void* y, bool for_bwd) {
-  const AttnDims d = dims(*this);
+void Attn::prep(hipStream_t st, const Params& P, void* sn_ws) {
   SnJob jobs[4];
   for (int i = 0; i < 4; ++i) jobs[i] = sn_job(P, kASN[i], sn[i]);
-  sn_power_iter_group(ex.st, jobs, 4, npi, sn_eps, ex.ws);
+  sn_power_iter_group(st, jobs, 4, npi, sn_eps, sn_ws);
   const PackJob pk[4] = {{P.w("theta"), sn[0].sigma, wqkv, C / 8, C, 1, dk, Cp, kPackFwd},
                          {P.w("phi"), sn[1].sigma, (char*)wqkv + (size_t)dk * Cp * 2, C / 8, C, 1, dk, Cp, kPackFwd},
                          {P.w("g"), sn[2].sigma, (char*)wqkv + (size_t)2 * dk * Cp * 2, C / 2, C, 1, dv, Cp, kPackFwd},
                          {P.w("o"), sn[3].sigma, wo, C, C / 2, 1, Cp, dv, kPackFwd}};
-  pack_group(ex.st, false, pk, 4);
+  pack_group(st, false, pk, 4);
+}
+
+void Attn::fwd(const Exec& ex, const Params& P, const void* x, void* y, bool for_bwd) {
+  const AttnDims d = dims(*this);
+  if (!prepped) prep(ex.st, P, ex.ws);
   ConvIn in;
   in.x = x; in.B = B; in.Hx = H; in.Wx = W; in.C = Cp;
   ConvOut po;

@@ -65,6 +65,13 @@ SnJob sn_job(const Params& P, const std::string& name, SNSlot& s) {
   return SnJob{P.p + e.offset, e.shape[0], cols_of(e), P.u + e.u_offset, s.v, s.sigma, s.u};
 }
 
+size_t sn_ws_all(const Layout& L) {
+  size_t t = 0;
+  for (const Entry& e : L.e)
+    if (e.sn) t += sn_ws_bytes(e.shape[0], cols_of(e));
+  return t;
+}
+
 size_t sn_group_ws(const int64_t (*rc)[2], int n) {
   size_t t = 0;
   for (int i = 0; i < n; ++i) t += sn_ws_bytes(rc[i][0], rc[i][1]);
@@ -180,16 +187,20 @@ size_t GBlock::ws_size(int n_cu) const {
   return std::max(a.off, b.off);
 }
 
-void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y) {
-  Arena a(ex.ws);
-  GWsF w = g_carve_f(*this, a);
+void GBlock::prep(hipStream_t st, const Params& P, void* sn_ws) {
   SnJob jobs[7];
   for (int i = 0; i < 7; ++i) jobs[i] = sn_job(P, kGSN[i], sn[i]);
-  sn_power_iter_group(ex.st, jobs, 7, npi, sn_eps, w.sn);
+  sn_power_iter_group(st, jobs, 7, npi, sn_eps, sn_ws);
   const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, wp1, cout, cin, 3, Cop, Cip, f32 ? kPackFwd : kPackSub},
                          {P.w("conv2.w"), sn[5].sigma, wp2, cout, cout, 3, Cop, Cop, kPackFwd},
                          {P.w("sc.w"), sn[6].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
-  pack_group(ex.st, f32, pk, 3);
+  pack_group(st, f32, pk, 3);
+}
+
+void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y) {
+  Arena a(ex.ws);
+  GWsF w = g_carve_f(*this, a);
+  if (!prepped) prep(ex.st, P, w.sn);
   const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
   // cBN1 statistics and tables
   bn_stats(ex.st, f32, x, M1, cin, Cip, bn_eps, mean1, rstd1, w.bn);
@@ -394,13 +405,11 @@ size_t DBlock::ws_size(int n_cu) const {
   return std::max(a.off, b.off);
 }
 
-void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
-  Arena a(ex.ws);
-  DWsF w = d_carve_f(*this, a);
+void DBlock::prep(hipStream_t st, const Params& P, void* sn_ws) {
   const int nsn = lsc ? 3 : 2;
   const SnJob jobs[3] = {sn_job(P, "conv1.w", sn[0]), sn_job(P, "conv2.w", sn[1]),
                          lsc ? sn_job(P, "sc.w", sn[2]) : SnJob{}};
-  sn_power_iter_group(ex.st, jobs, nsn, npi, sn_eps, w.sn);
+  sn_power_iter_group(st, jobs, nsn, npi, sn_eps, sn_ws);
   // with 3x3-patch input, conv1 is a 1x1 filter over the 9 cin patch
   // channels (the [Cout][3][3][cin] weight read as [Cout][9 cin]) and the
   // skip's 1x1 filter sits on the centre tap's channels 4 cin ..
@@ -408,7 +417,14 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, wp1, cout, K1, R1, Cop, Cip, kPackFwd},
                          {P.w("conv2.w"), sn[1].sigma, wp2, cout, cout, 3, Cop, Cop, s2conv() ? kPackPool4 : kPackFwd},
                          {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd, ksc}};
-  pack_group(ex.st, f32, pk, nsn);
+  pack_group(st, f32, pk, nsn);
+}
+
+void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
+  Arena a(ex.ws);
+  DWsF w = d_carve_f(*this, a);
+  if (!prepped) prep(ex.st, P, w.sn);
+  const int R1 = im2col ? 1 : 3, K1 = im2col ? 9 * cin : cin, ksc = im2col ? 4 * cin : 0;
   // h = conv3x3([relu](x)) + b1
   ConvIn i1;
   i1.x = x; i1.B = B; i1.Hx = H; i1.Wx = W; i1.C = Cip; i1.relu = preact; i1.c_real = K1;

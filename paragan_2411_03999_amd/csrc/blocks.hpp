@@ -97,6 +97,11 @@ struct GBlock {
   void *a1 = nullptr, *a2 = nullptr;   // relu(cbn1(x)), relu(cbn2(h1)): conv operands
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
+  // The forward's SN power iterations and weight packing: fwd runs them
+  // itself unless prepped is set (then prep ran them before, e.g. on
+  // another stream; sn_ws: sn_ws_all of the layout, or the block's share)
+  bool prepped = false;
+  void prep(hipStream_t st, const Params& P, void* sn_ws);
   void fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y);
   // dcond_accumulate: add to dcond instead of overwriting it
   void bwd(const Exec& ex, const Params& P, const void* x, const float* cond, const void* dy, void* dx,
@@ -125,6 +130,11 @@ struct DBlock {
   bool subdgrad() const { return s2conv() && cout >= 96; }
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
+  // The forward's SN power iterations and weight packing: fwd runs them
+  // itself unless prepped is set (then prep ran them before, e.g. on
+  // another stream; sn_ws: sn_ws_all of the layout, or the block's share)
+  bool prepped = false;
+  void prep(hipStream_t st, const Params& P, void* sn_ws);
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);
   // dx may be null; dx_f32 writes an unrounded fp32 input gradient;
   // wgrad = false computes the input gradient only (no parameter gradients).
@@ -148,6 +158,11 @@ struct Attn {
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   // for_bwd = false: no backward will follow (o32 is not written)
+  // The forward's SN power iterations and weight packing: fwd runs them
+  // itself unless prepped is set (then prep ran them before, e.g. on
+  // another stream; sn_ws: sn_ws_all of the layout, or the block's share)
+  bool prepped = false;
+  void prep(hipStream_t st, const Params& P, void* sn_ws);
   void fwd(const Exec& ex, const Params& P, const void* x, void* y, bool for_bwd = true);
   void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool wgrad = true);
 };
@@ -163,5 +178,7 @@ SnBwdJob sn_bwd_job(const Params& P, const std::string& name, const SNSlot& s, c
                     const float* scale);
 // workspace of a group of (rows, cols) weights
 size_t sn_group_ws(const int64_t (*rc)[2], int n);
+// workspace for any group of a layout's SN weights
+size_t sn_ws_all(const Layout& L);
 
 }  // namespace pg

@@ -154,6 +154,11 @@ struct ProfScope {
 
 struct paragan_ctx {
   hipStream_t stream = nullptr;
+  // a second stream (default priority) for work that overlaps the caller's
+  // stream inside one call, and events to order the two; created on first
+  // use, released with the context
+  hipStream_t side = nullptr;
+  hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
   int device = 0;
   int n_cu = 0;
   std::string err;

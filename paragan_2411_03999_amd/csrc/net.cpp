@@ -199,13 +199,30 @@ size_t GNet::ws_size(int n_cu) {
   return w.off;
 }
 
+void GNet::prep(hipStream_t st, const Params& P, void* sn_ws) {
+  const Arch& a = a_;
+  const Exec e{st, 0, sn_ws, 0};
+  sn_forward(e, P, "linear.w", lin_, a.npi, a.sn_eps);
+  for (int i = 0; i < a.n_g; ++i) {
+    blocks_[i].prep(st, sub(P, "g" + std::to_string(i) + "."), sn_ws);
+    blocks_[i].prepped = true;
+  }
+  if (attn_after_ >= 0) {
+    attn_.prep(st, sub(P, "attn."), sn_ws);
+    attn_.prepped = true;
+  }
+  sn_forward(e, P, "out_conv.w", head_.sn_slot(), head_.npi, head_.sn_eps);
+  head_.prepped = true;
+  prepped_ = true;
+}
+
 void GNet::fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img, bool for_bwd) {
   const Arch& a = a_;
   Arena w(ex.ws);
   GNetWs r = gnet_carve(a, B_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
   Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
   const int c0 = a.g_mult[0] * a.ch;
-  sn_forward(eb, P, "linear.w", lin_, a.npi, a.sn_eps);
+  if (!prepped_) sn_forward(eb, P, "linear.w", lin_, a.npi, a.sn_eps);
   glin_fwd(ex.st, z, a.dz, a.zc, P.w("linear.w"), lin_.sigma, P.w("linear.b"), B_, c0, (int)cpad(c0), act_[0]);
   const void* h = act_[0];
   for (int i = 0; i < a.n_g; ++i) {
@@ -219,6 +236,9 @@ void GNet::fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y
   }
   head_.fwd(Exec{ex.st, ex.n_cu, r.head, r.head_bytes}, P, h, img);
   img_ = img;
+  // a later forward runs its own SN and packing unless prepped again
+  for (GBlock& g : blocks_) g.prepped = false;
+  attn_.prepped = head_.prepped = prepped_ = false;
 }
 
 void GNet::bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, const float* dimg, int ldd) {
@@ -293,7 +313,7 @@ void GOut::fwd(const Exec& ex, const Params& P, const void* x, float* img) {
   bn_stats(ex.st, false, x, (int64_t)B * H * W, C, cp, bn_eps, mean_, rstd_, r.red);
   cbn_tables(ex.st, nullptr, 0, nullptr, nullptr, nullptr, nullptr, P.w("out_bn.gain"), P.w("out_bn.bias"), rstd_,
              1, C, cp, gain_, bias_, scale_);
-  sn_forward(Exec{ex.st, ex.n_cu, r.red, r.red_bytes}, P, "out_conv.w", sn_, npi, sn_eps);
+  if (!prepped) sn_forward(Exec{ex.st, ex.n_cu, r.red, r.red_bytes}, P, "out_conv.w", sn_, npi, sn_eps);
   ghead_fwd(ex.st, x, B, H, W, C, cp, mean_, scale_, bias_, P.w("out_conv.w"), sn_.sigma, P.w("out_conv.b"), img);
 }
 
@@ -375,6 +395,22 @@ size_t DNet::ws_size(int n_cu) {
   return w.off;
 }
 
+void DNet::prep(hipStream_t st, const Params& P, void* sn_ws) {
+  const Arch& a = a_;
+  const Exec e{st, 0, sn_ws, 0};
+  for (int j = 0; j < (int)blocks_.size(); ++j) {
+    blocks_[j].prep(st, sub(P, "d" + std::to_string(j) + "."), sn_ws);
+    blocks_[j].prepped = true;
+  }
+  if (attn_after_ >= 0) {
+    attn_.prep(st, sub(P, "attn."), sn_ws);
+    attn_.prepped = true;
+  }
+  sn_forward(e, P, "head.w", head_, a.npi, a.sn_eps);
+  sn_forward(e, P, "embed", emb_, a.npi, a.sn_eps);
+  prepped_ = true;
+}
+
 void DNet::fwd(const Exec& ex, const Params& P, const float* x, const int32_t* y, float* out) {
   const Arch& a = a_;
   Arena w(ex.ws);
@@ -391,8 +427,12 @@ void DNet::fwd(const Exec& ex, const Params& P, const float* x, const int32_t* y
     }
   }
   const DBlock& last = blocks_.back();
-  sn_forward(eb, P, "head.w", head_, a.npi, a.sn_eps);
-  sn_forward(eb, P, "embed", emb_, a.npi, a.sn_eps);
+  if (!prepped_) {
+    sn_forward(eb, P, "head.w", head_, a.npi, a.sn_eps);
+    sn_forward(eb, P, "embed", emb_, a.npi, a.sn_eps);
+  }
+  for (DBlock& b : blocks_) b.prepped = false;
+  attn_.prepped = prepped_ = false;
   dhead_fwd(ex.st, h, N_, last.Ho * last.Wo, last.cout, last.Cop, y, P.w("head.w"), head_.sigma, P.w("head.b"),
             P.w("embed"), emb_.sigma, hs_, out);
 }
@@ -434,6 +474,7 @@ struct StepWs {
   int32_t* ylab;
   void* net;
   size_t net_bytes;
+  void* side;          // SN workspace of the second stream's weight preparation
 };
 
 static StepWs step_carve(const Arch& a, int B, Arena& w, GNet& g, DNet& d2, DNet& d1, int n_cu) {
@@ -454,6 +495,7 @@ static StepWs step_carve(const Arch& a, int B, Arena& w, GNet& g, DNet& d2, DNet
   r.dloss = w.f32(64);
   r.net_bytes = std::max({g.ws_size(n_cu), d2.ws_size(n_cu), d1.ws_size(n_cu)});
   r.net = w.bytes(r.net_bytes);
+  r.side = w.bytes(std::max(sn_ws_all(g_layout(a)), sn_ws_all(d_layout(a))));
   return r;
 }
 
@@ -480,11 +522,38 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
   Params PG{&LG, "", G->params, G->u, G->grads};
   Params PD{&LD, "", D->params, D->u, D->grads};
   const int64_t pix = (int64_t)a.img * a.img;
+  // The forwards' SN power iterations and weight packing (which read only
+  // parameters) run on a second stream, each network's ahead of its forward
+  // and behind the work that last used its packed weights or changed its
+  // parameters: D's behind the previous Adam step (overlapping G's forward),
+  // G's behind the previous G forward (overlapping D's forward and backward).
+  if (!ctx->side) {
+    PG_HIP(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking));
+    for (hipEvent_t& e : ctx->ev) PG_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  }
+  hipStream_t sd = ctx->side;
+  hipEvent_t ev_main = ctx->ev[0], ev_main2 = ctx->ev[1], ev_g = ctx->ev[2], ev_d = ctx->ev[3];
+  auto side_after_main = [&](hipEvent_t e) {
+    PG_HIP(hipEventRecord(e, st));
+    PG_HIP(hipStreamWaitEvent(sd, e, 0));
+  };
+  auto main_after = [&](hipEvent_t e) { PG_HIP(hipStreamWaitEvent(st, e, 0)); };
+  side_after_main(ev_main2);
+  g.prep(sd, PG, r.side);
+  PG_HIP(hipEventRecord(ev_g, sd));
   for (int k = 0; k < n_D; ++k) {
+    side_after_main(ev_main);
+    d2.prep(sd, PD, r.side);
+    PG_HIP(hipEventRecord(ev_d, sd));
     PG_HIP(hipMemcpyAsync(r.ximg, in->x_real[k], (size_t)B * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
     PG_HIP(hipMemcpyAsync(r.ylab, in->y_real[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
     PG_HIP(hipMemcpyAsync(r.ylab + B, in->y_fake[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
+    main_after(ev_g);
     g.fwd(ex, PG, in->z_fake[k], in->y_fake[k], r.ximg + (size_t)B * pix * 3, false);
+    side_after_main(ev_main2);
+    g.prep(sd, PG, r.side);   // for the next D step's or the G step's forward
+    PG_HIP(hipEventRecord(ev_g, sd));
+    main_after(ev_d);
     d2.fwd(ex, PD, r.ximg, r.ylab, r.logits);
     hinge(st, r.logits, B, B, false, r.dout, r.dloss + k);
     d2.bwd(ex, PD, r.ylab, r.dout, nullptr, true);
@@ -492,7 +561,12 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
     adam(st, D->params, D->grads, D->adam_m, D->adam_v, LD.n_params, d->beta1, d->beta2, d->lr_d, d->adam_eps,
          D->adam_t);
   }
+  side_after_main(ev_main);
+  d1.prep(sd, PD, r.side);
+  PG_HIP(hipEventRecord(ev_d, sd));
+  main_after(ev_g);
   g.fwd(ex, PG, in->z_g, in->y_g, r.ximg);
+  main_after(ev_d);
   d1.fwd(ex, PD, r.ximg, in->y_g, r.logits);
   hinge(st, r.logits, 0, B, true, r.dout, r.dloss + n_D);
   d1.bwd(ex, PD, in->y_g, r.dout, r.dimg, false);

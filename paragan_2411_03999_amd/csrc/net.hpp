@@ -36,6 +36,9 @@ class GOut {
   size_t ws_size() const;
   // x: bf16 [B][H][W][cpad(C)]; img: fp32 [B][H][W][3]
   void fwd(const Exec& ex, const Params& P, const void* x, float* img);
+  // prepped: the SN of out_conv.w already ran (GNet::prep, into sn_slot())
+  bool prepped = false;
+  SNSlot& sn_slot() { return sn_; }
   // img: this layer's forward output; dimg: fp32 [B][H][W][ldd];
   // dx: bf16 [B][H][W][cpad(C)]
   void bwd(const Exec& ex, const Params& P, const void* x, const float* img, const float* dimg, int ldd,
@@ -54,12 +57,16 @@ class GNet {
   size_t ws_size(int n_cu);
   // img: fp32 [B][img][img][3]
   // for_bwd = false: no backward will follow this forward
+  // The forward's SN power iterations and weight packing of every layer on
+  // stream st (sn_ws: sn_ws_all of the layout); the next fwd then skips them
+  void prep(hipStream_t st, const Params& P, void* sn_ws);
   void fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img, bool for_bwd = true);
   // dimg: fp32 [B][img][img][ldd]
   void bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, const float* dimg, int ldd);
 
  private:
   Arch a_;
+  bool prepped_ = false;
   int B_;
   std::vector<GBlock> blocks_;
   Attn attn_;
@@ -79,12 +86,14 @@ class DNet {
   void plan_saved(Arena& s);
   size_t ws_size(int n_cu);
   // x: fp32 images [N][img][img][3]; out: fp32 logits [N]
+  void prep(hipStream_t st, const Params& P, void* sn_ws);   // as GNet::prep
   void fwd(const Exec& ex, const Params& P, const float* x, const int32_t* y, float* out);
   // wgrad = false: input gradient only (dimg fp32 [N][img][img][4], channels 0..2)
   void bwd(const Exec& ex, const Params& P, const int32_t* y, const float* dout, float* dimg, bool wgrad);
 
  private:
   Arch a_;
+  bool prepped_ = false;
   int N_;
   std::vector<DBlock> blocks_;
   Attn attn_;
