@@ -109,6 +109,11 @@ void GBlock::plan_saved(Arena& a) {
   wp1 = a.bytes((size_t)Cop * (f32 ? 9 : 16) * Cip * e);
   wp2 = a.bytes((size_t)Cop * 9 * Cop * e);
   wpsc = a.bytes((size_t)Cop * Cip * e);
+  if (keep_dgrad) {
+    wd1s = a.bytes((size_t)Cip * (f32 ? 9 : 16) * Cop * e);
+    wd2s = a.bytes((size_t)Cop * 9 * Cop * e);
+    wdscs = a.bytes((size_t)Cip * Cop * e * (f32 ? 1 : 4));
+  }
   mean1 = a.f32(Cip); rstd1 = a.f32(Cip);
   gain1 = a.f32((size_t)B * Cip); bias1 = a.f32((size_t)B * Cip); scale1 = a.f32((size_t)B * Cip);
   mean2 = a.f32(Cop); rstd2 = a.f32(Cop);
@@ -187,7 +192,17 @@ size_t GBlock::ws_size(int n_cu) const {
   return std::max(a.off, b.off);
 }
 
-void GBlock::prep(hipStream_t st, const Params& P, void* sn_ws) {
+// the data-gradient weight packs of a G block into (wd1, wd2, wdsc)
+static void g_pack_dgrad(const GBlock& g, hipStream_t st, const Params& P, void* wd1, void* wd2, void* wdsc) {
+  const PackJob pk[3] = {{P.w("conv1.w"), g.sn[2].sigma, wd1, g.cout, g.cin, 3, g.Cop, g.Cip,
+                          g.f32 ? kPackDgrad : kPackDgradSum4},
+                         {P.w("conv2.w"), g.sn[5].sigma, wd2, g.cout, g.cout, 3, g.Cop, g.Cop, kPackDgrad},
+                         {P.w("sc.w"), g.sn[6].sigma, wdsc, g.cout, g.cin, 1, g.Cop, g.Cip,
+                          g.f32 ? kPackDgrad : kPackDgradRep4}};
+  pack_group(st, g.f32, pk, 3);
+}
+
+void GBlock::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   SnJob jobs[7];
   for (int i = 0; i < 7; ++i) jobs[i] = sn_job(P, kGSN[i], sn[i]);
   sn_power_iter_group(st, jobs, 7, npi, sn_eps, sn_ws);
@@ -195,6 +210,10 @@ void GBlock::prep(hipStream_t st, const Params& P, void* sn_ws) {
                          {P.w("conv2.w"), sn[5].sigma, wp2, cout, cout, 3, Cop, Cop, kPackFwd},
                          {P.w("sc.w"), sn[6].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
   pack_group(st, f32, pk, 3);
+  if (for_bwd && keep_dgrad) {
+    g_pack_dgrad(*this, st, P, wd1s, wd2s, wdscs);
+    dgrad_ready = true;
+  }
 }
 
 void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y) {
@@ -245,12 +264,14 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   GWsB w = g_carve_b(*this, a, ex.n_cu);
   const int64_t M1 = (int64_t)B * H * W, M2 = 4 * M1;
   const int H2 = 2 * H, W2 = 2 * W;
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, w.wd1, cout, cin, 3, Cop, Cip,
-                          f32 ? kPackDgrad : kPackDgradSum4},
-                         {P.w("conv2.w"), sn[5].sigma, w.wd2, cout, cout, 3, Cop, Cop, kPackDgrad},
-                         {P.w("sc.w"), sn[6].sigma, w.wdsc, cout, cin, 1, Cop, Cip,
-                          f32 ? kPackDgrad : kPackDgradRep4}};
-  pack_group(ex.st, f32, pk, 3);
+  // the data-gradient weights: packed by prep, or here
+  void *wd1 = w.wd1, *wd2 = w.wd2, *wdsc = w.wdsc;
+  if (dgrad_ready) {
+    wd1 = wd1s; wd2 = wd2s; wdsc = wdscs;
+    dgrad_ready = false;
+  } else {
+    g_pack_dgrad(*this, ex.st, P, wd1, wd2, wdsc);
+  }
   // conv2: dW2, db2
   GradIn gdy;
   gdy.g = dy; gdy.Hs = H2; gdy.Ws = W2; gdy.C = Cop;
@@ -270,13 +291,13 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   dsp.x = dy; dsp.B = B; dsp.Hx = H2; dsp.Wx = W2; dsp.C = Cop; dsp.gather = f32 ? G_POOL2 : G_S2;
   ConvOut dso;
   dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = cin;
-  conv_fwd(ex.st, f32, dsp, H, W, f32 ? 1 : 2, w.wdsc, Cip, dso);
+  conv_fwd(ex.st, f32, dsp, H, W, f32 ? 1 : 2, wdsc, Cip, dso);
   // da2 = conv2^T dy (fp32)
   ConvIn d2;
   d2.x = dy; d2.B = B; d2.Hx = H2; d2.Wx = W2; d2.C = Cop;
   ConvOut d2o;
   d2o.y = w.da2; d2o.y_f32 = 1; d2o.yC = Cop; d2o.n_real = cout;
-  conv_fwd(ex.st, f32, d2, H2, W2, 3, w.wd2, Cop, d2o);
+  conv_fwd(ex.st, f32, d2, H2, W2, 3, wd2, Cop, d2o);
   // cBN2 backward (through the ReLU) -> dh1
   bn_bwd(ex.st, f32, w.da2, false, h1, B, H2, W2, cout, Cop, mean2, rstd2, gain2, bias2, Cop, nullptr, w.dh1,
          w.dg2, w.db2, Cop, w.bnb);
@@ -303,9 +324,9 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   d1o.y = w.da1; d1o.y_f32 = 1; d1o.yC = Cip; d1o.n_real = cin;
   if (!f32) {
     d1.gather = G_S2;
-    conv_fwd(ex.st, f32, d1, H, W, 4, w.wd1, Cip, d1o);
+    conv_fwd(ex.st, f32, d1, H, W, 4, wd1, Cip, d1o);
   } else {
-    conv_fwd(ex.st, f32, d1, H2, W2, 3, w.wd1, Cip, d1o);
+    conv_fwd(ex.st, f32, d1, H2, W2, 3, wd1, Cip, d1o);
   }
   bn_bwd(ex.st, f32, w.da1, f32, x, B, H, W, cin, Cip, mean1, rstd1, gain1, bias1, Cip, w.dxs, dx, w.dg1,
          w.db1, Cip, w.bnb);
@@ -343,6 +364,11 @@ void DBlock::plan_saved(Arena& a) {
   wp1 = a.bytes((size_t)Cop * 9 * Cip * e);
   // a downsampling bf16 block keeps conv2 as the pre-pooled stride-2 4x4 filter
   wp2 = a.bytes((size_t)Cop * (s2conv() ? 16 : 9) * Cop * e);
+  if (keep_dgrad) {
+    wd1s = a.bytes((size_t)Cip * 9 * Cop * e);
+    wd2s = a.bytes((size_t)Cop * (subdgrad() ? 16 : 9) * Cop * e);
+    wdscs = lsc ? a.bytes((size_t)Cip * Cop * e) : nullptr;
+  }
   if (lsc) wpsc = a.bytes((size_t)Cop * Cip * e);
   h = a.bytes((size_t)B * H * W * Cop * e);
   // the pooled block input, operand of the downsampling 1x1 skip
@@ -405,7 +431,18 @@ size_t DBlock::ws_size(int n_cu) const {
   return std::max(a.off, b.off);
 }
 
-void DBlock::prep(hipStream_t st, const Params& P, void* sn_ws) {
+// the data-gradient weight packs of a D block into (wd1, wd2, wdsc)
+static void d_pack_dgrad(const DBlock& d, hipStream_t st, const Params& P, void* wd1, void* wd2, void* wdsc) {
+  const int R1 = d.im2col ? 1 : 3, K1 = d.im2col ? 9 * d.cin : d.cin, ksc = d.im2col ? 4 * d.cin : 0;
+  const PackJob pk[3] = {{P.w("conv1.w"), d.sn[0].sigma, wd1, d.cout, K1, R1, d.Cop, d.Cip, kPackDgrad},
+                         {P.w("conv2.w"), d.sn[1].sigma, wd2, d.cout, d.cout, 3, d.Cop, d.Cop,
+                          d.subdgrad() ? kPackSubDgrad : kPackDgrad},
+                         {d.lsc ? P.w("sc.w") : nullptr, d.sn[2].sigma, wdsc, d.cout, d.cin, 1, d.Cop, d.Cip,
+                          kPackDgrad, ksc}};
+  pack_group(st, d.f32, pk, d.lsc ? 3 : 2);
+}
+
+void DBlock::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   const int nsn = lsc ? 3 : 2;
   const SnJob jobs[3] = {sn_job(P, "conv1.w", sn[0]), sn_job(P, "conv2.w", sn[1]),
                          lsc ? sn_job(P, "sc.w", sn[2]) : SnJob{}};
@@ -418,6 +455,10 @@ void DBlock::prep(hipStream_t st, const Params& P, void* sn_ws) {
                          {P.w("conv2.w"), sn[1].sigma, wp2, cout, cout, 3, Cop, Cop, s2conv() ? kPackPool4 : kPackFwd},
                          {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd, ksc}};
   pack_group(st, f32, pk, nsn);
+  if (for_bwd && keep_dgrad) {
+    d_pack_dgrad(*this, st, P, wd1s, wd2s, wdscs);
+    dgrad_ready = true;
+  }
 }
 
 void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
@@ -467,11 +508,14 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   DWsB w = d_carve_b(*this, a, ex.n_cu);
   const int64_t M = (int64_t)B * H * W, Mo = (int64_t)B * Ho * Wo;
   const int R1 = im2col ? 1 : 3, K1 = im2col ? 9 * cin : cin, ksc = im2col ? 4 * cin : 0;
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, w.wd1, cout, K1, R1, Cop, Cip, kPackDgrad},
-                         {P.w("conv2.w"), sn[1].sigma, w.wd2, cout, cout, 3, Cop, Cop,
-                          subdgrad() ? kPackSubDgrad : kPackDgrad},
-                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, w.wdsc, cout, cin, 1, Cop, Cip, kPackDgrad, ksc}};
-  pack_group(ex.st, f32, pk, lsc ? 3 : 2);
+  // the data-gradient weights: packed by prep, or here
+  void *wd1 = w.wd1, *wd2 = w.wd2, *wdsc = w.wdsc;
+  if (dgrad_ready) {
+    wd1 = wd1s; wd2 = wd2s; wdsc = wdscs;
+    dgrad_ready = false;
+  } else {
+    d_pack_dgrad(*this, ex.st, P, wd1, wd2, wdsc);
+  }
   // conv2 (its output gradient is dy, or dy/4 spread over 2x2 when pooled)
   GradIn g2;
   g2.g = dy; g2.Hs = Ho; g2.Ws = Wo; g2.C = Cop;
@@ -503,9 +547,9 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   if (subdgrad()) {
     // conv2^T over up2(dy) / 4 as the four sub-pixel 2x2 convs over dy
     d2.gather = G_SUB;
-    conv_fwd(ex.st, f32, d2, Ho, Wo, 2, w.wd2, Cop, d2o);
+    conv_fwd(ex.st, f32, d2, Ho, Wo, 2, wd2, Cop, d2o);
   } else {
-    conv_fwd(ex.st, f32, d2, H, W, 3, w.wd2, Cop, d2o);
+    conv_fwd(ex.st, f32, d2, H, W, 3, wd2, Cop, d2o);
   }
   // conv1
   GradIn g1;
@@ -533,7 +577,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
       ds.x = dy; ds.B = B; ds.Hx = Ho; ds.Wx = Wo; ds.C = Cop;
       ConvOut dso;
       dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = ksc + cin;
-      conv_fwd(ex.st, f32, ds, Ho, Wo, 1, w.wdsc, Cip, dso);
+      conv_fwd(ex.st, f32, ds, Ho, Wo, 1, wdsc, Cip, dso);
     }
   }
   if (dx) {
@@ -551,7 +595,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     } else {
       d1o.res = dy; d1o.res_f32 = f32; d1o.resC = Cop; d1o.res_mode = R_SAME;
     }
-    conv_fwd(ex.st, f32, d1, H, W, R1, w.wd1, Cip, d1o);
+    conv_fwd(ex.st, f32, d1, H, W, R1, wd1, Cip, d1o);
     if (im2col) im2col_grad(ex.st, w.dcol, B, H, W, (float*)dx);
   }
   if (!wgrad) return;

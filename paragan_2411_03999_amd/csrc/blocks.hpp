@@ -101,7 +101,11 @@ struct GBlock {
   // itself unless prepped is set (then prep ran them before, e.g. on
   // another stream; sn_ws: sn_ws_all of the layout, or the block's share)
   bool prepped = false;
-  void prep(hipStream_t st, const Params& P, void* sn_ws);
+  // keep_dgrad (set before plan_saved): prep(for_bwd) also packs the
+  // data-gradient weights, into saved buffers the next bwd uses
+  bool keep_dgrad = false, dgrad_ready = false;
+  void *wd1s = nullptr, *wd2s = nullptr, *wdscs = nullptr;
+  void prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd = false);
   void fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y);
   // dcond_accumulate: add to dcond instead of overwriting it
   void bwd(const Exec& ex, const Params& P, const void* x, const float* cond, const void* dy, void* dx,
@@ -134,7 +138,9 @@ struct DBlock {
   // itself unless prepped is set (then prep ran them before, e.g. on
   // another stream; sn_ws: sn_ws_all of the layout, or the block's share)
   bool prepped = false;
-  void prep(hipStream_t st, const Params& P, void* sn_ws);
+  bool keep_dgrad = false, dgrad_ready = false;   // as in GBlock
+  void *wd1s = nullptr, *wd2s = nullptr, *wdscs = nullptr;
+  void prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd = false);
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);
   // dx may be null; dx_f32 writes an unrounded fp32 input gradient;
   // wgrad = false computes the input gradient only (no parameter gradients).

@@ -139,6 +139,7 @@ void GNet::plan_saved(Arena& s) {
     GBlock g;
     g.B = B_; g.H = res; g.W = res; g.cin = a.g_mult[i] * a.ch; g.cout = a.g_mult[i + 1] * a.ch;
     g.dc = a.dc; g.npi = a.npi; g.f32 = false; g.bn_eps = a.bn_eps; g.sn_eps = a.sn_eps;
+    g.keep_dgrad = true;
     g.plan_saved(s);
     blocks_.push_back(g);
     res *= 2;
@@ -199,12 +200,12 @@ size_t GNet::ws_size(int n_cu) {
   return w.off;
 }
 
-void GNet::prep(hipStream_t st, const Params& P, void* sn_ws) {
+void GNet::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   const Arch& a = a_;
   const Exec e{st, 0, sn_ws, 0};
   sn_forward(e, P, "linear.w", lin_, a.npi, a.sn_eps);
   for (int i = 0; i < a.n_g; ++i) {
-    blocks_[i].prep(st, sub(P, "g" + std::to_string(i) + "."), sn_ws);
+    blocks_[i].prep(st, sub(P, "g" + std::to_string(i) + "."), sn_ws, for_bwd);
     blocks_[i].prepped = true;
   }
   if (attn_after_ >= 0) {
@@ -344,6 +345,7 @@ void DNet::plan_saved(Arena& s) {
     b.B = N_; b.H = sp.H; b.W = sp.W; b.cin = sp.cin; b.cout = sp.cout; b.npi = a.npi;
     b.preact = sp.preact; b.down = sp.down; b.lsc = sp.lsc; b.f32 = false; b.sn_eps = a.sn_eps;
     b.im2col = j == 0;   // the image enters as 3x3 patches
+    b.keep_dgrad = true;
     b.plan_saved(s);
     blocks_.push_back(b);
     act_.push_back(s.bytes((size_t)N_ * b.Ho * b.Wo * cpad(sp.cout) * 2));
@@ -395,11 +397,11 @@ size_t DNet::ws_size(int n_cu) {
   return w.off;
 }
 
-void DNet::prep(hipStream_t st, const Params& P, void* sn_ws) {
+void DNet::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   const Arch& a = a_;
   const Exec e{st, 0, sn_ws, 0};
   for (int j = 0; j < (int)blocks_.size(); ++j) {
-    blocks_[j].prep(st, sub(P, "d" + std::to_string(j) + "."), sn_ws);
+    blocks_[j].prep(st, sub(P, "d" + std::to_string(j) + "."), sn_ws, for_bwd);
     blocks_[j].prepped = true;
   }
   if (attn_after_ >= 0) {
@@ -539,11 +541,11 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
   };
   auto main_after = [&](hipEvent_t e) { PG_HIP(hipStreamWaitEvent(st, e, 0)); };
   side_after_main(ev_main2);
-  g.prep(sd, PG, r.side);
+  g.prep(sd, PG, r.side, n_D == 0);
   PG_HIP(hipEventRecord(ev_g, sd));
   for (int k = 0; k < n_D; ++k) {
     side_after_main(ev_main);
-    d2.prep(sd, PD, r.side);
+    d2.prep(sd, PD, r.side, true);
     PG_HIP(hipEventRecord(ev_d, sd));
     PG_HIP(hipMemcpyAsync(r.ximg, in->x_real[k], (size_t)B * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
     PG_HIP(hipMemcpyAsync(r.ylab, in->y_real[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
@@ -551,7 +553,7 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
     main_after(ev_g);
     g.fwd(ex, PG, in->z_fake[k], in->y_fake[k], r.ximg + (size_t)B * pix * 3, false);
     side_after_main(ev_main2);
-    g.prep(sd, PG, r.side);   // for the next D step's or the G step's forward
+    g.prep(sd, PG, r.side, k == n_D - 1);   // for the next D step's or the G step's forward
     PG_HIP(hipEventRecord(ev_g, sd));
     main_after(ev_d);
     d2.fwd(ex, PD, r.ximg, r.ylab, r.logits);
@@ -562,7 +564,7 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
          D->adam_t);
   }
   side_after_main(ev_main);
-  d1.prep(sd, PD, r.side);
+  d1.prep(sd, PD, r.side, true);
   PG_HIP(hipEventRecord(ev_d, sd));
   main_after(ev_g);
   g.fwd(ex, PG, in->z_g, in->y_g, r.ximg);

@@ -58,8 +58,9 @@ class GNet {
   // img: fp32 [B][img][img][3]
   // for_bwd = false: no backward will follow this forward
   // The forward's SN power iterations and weight packing of every layer on
-  // stream st (sn_ws: sn_ws_all of the layout); the next fwd then skips them
-  void prep(hipStream_t st, const Params& P, void* sn_ws);
+  // stream st (sn_ws: sn_ws_all of the layout); the next fwd then skips them.
+  // for_bwd: the blocks' data-gradient weights too, for the next bwd.
+  void prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd = false);
   void fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img, bool for_bwd = true);
   // dimg: fp32 [B][img][img][ldd]
   void bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, const float* dimg, int ldd);
@@ -86,7 +87,7 @@ class DNet {
   void plan_saved(Arena& s);
   size_t ws_size(int n_cu);
   // x: fp32 images [N][img][img][3]; out: fp32 logits [N]
-  void prep(hipStream_t st, const Params& P, void* sn_ws);   // as GNet::prep
+  void prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd = false);   // as GNet::prep
   void fwd(const Exec& ex, const Params& P, const float* x, const int32_t* y, float* out);
   // wgrad = false: input gradient only (dimg fp32 [N][img][img][4], channels 0..2)
   void bwd(const Exec& ex, const Params& P, const int32_t* y, const float* dout, float* dimg, bool wgrad);
