@@ -68,6 +68,11 @@ ARCHS = {
 }
 
 
+# (lr, beta1, beta2, eps) of the generator's AdaBelief and the discriminator's Adam
+OPT_G = (1e-4, 0.5, 0.999, 1e-12)
+OPT_D = (4e-4, 0.0, 0.999, 1e-6)
+
+
 def make_desc(lib, arch, B):
     img, ch, gm, dm, dd, attn, ncls, dz, sd = ARCHS[arch]
     d = lib.BigganDesc()
@@ -78,7 +83,9 @@ def make_desc(lib, arch, B):
         d.d_mult[j], d.d_down[j] = m, dn
     d.attn_res, d.n_classes, d.dz, d.shared_dim, d.B = attn, ncls, dz, sd, B
     d.n_power_iter, d.bn_eps, d.sn_eps = 1, 1e-5, 1e-12
-    d.lr_g, d.lr_d, d.beta1, d.beta2, d.adam_eps = 1e-4, 4e-4, 0.0, 0.999, 1e-6
+    # the paper's asymmetric policy: AdaBelief for G, Adam for D
+    d.opt_g = lib.Optim(lib.ADABELIEF, *OPT_G)
+    d.opt_d = lib.Optim(lib.ADAM, *OPT_D)
     return d
 
 
@@ -118,7 +125,7 @@ def model_flops(arch):
 
 
 def device_net(torch, lib, ents, npar, nu, gen):
-    """Seeded random parameters, u vectors and zeroed Adam state on the GPU."""
+    """Seeded random parameters, u vectors and zeroed optimiser state on the GPU."""
     P = torch.empty(npar, dtype=torch.float32, device="cuda")
     for e in ents:
         n = 1
@@ -160,8 +167,8 @@ def cpu_baseline(arch, B=1, n_D=2):
     d_in = [(s.uniform((B, img, img, 3)), s.labels(B, ncls), s.normal((B, dz)), s.labels(B, ncls))
             for _ in range(n_D)]
     g_in = (s.normal((B, dz)), s.labels(B, ncls))
-    hp = O.HParams()
-    optG, optD = O.adam_init(gp), O.adam_init(dp)
+    hp = O.HParams(opt_g=O.OptSpec("adabelief", *OPT_G), opt_d=O.OptSpec("adam", *OPT_D))
+    optG, optD = O.opt_init(gp), O.opt_init(dp)
     t0 = time.perf_counter()
     _, _, losses, _, _ = O.train_step(a, hp, (gp, gu), (dp, du), optG, optD, d_in, g_in)
     dt = time.perf_counter() - t0

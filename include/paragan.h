@@ -16,7 +16,8 @@
  *   on error nothing has been launched and paragan_last_error() names the
  *   problem.  No C++ exception crosses the ABI.
  * - Streams: all device work is enqueued on the hipStream_t given to
- *   paragan_create(), in order.  Calls are asynchronous unless stated.
+ *   paragan_create(), in order (paragan_train_step also uses a second
+ *   stream of its own, see there).  Calls are asynchronous unless stated.
  * - Memory: every device buffer is allocated and owned by the caller and
  *   passed as a plain device pointer.  The library never allocates device
  *   memory.  Sizes of the "saved" (forward -> backward) and "ws" (scratch)
@@ -91,6 +92,9 @@ typedef struct {
  * paragan_sn_ws_size() bytes, 256-byte aligned.
  * ------------------------------------------------------------------- */
 int paragan_sn_ws_size(int64_t rows, int64_t cols, size_t* ws_bytes);
+/* Validation only (no device work): the checks paragan_sn_power_iter makes
+ * of its sizes and scalars. */
+int paragan_sn_check(int64_t rows, int64_t cols, int n_iter, float eps);
 int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t rows,
                           int64_t cols, float* u, float* v, float* sigma,
                           int n_iter, float eps, void* ws);
@@ -132,7 +136,9 @@ int paragan_gblock_bwd(paragan_ctx* ctx, const paragan_gblock_desc* d,
                        float* dcond, float* grads, void* ws);
 
 /* ---------------------------------------------------------------------
- * BigGAN discriminator residual block:
+ * BigGAN discriminator residual block (the benchmark model's
+ * discriminator, Evaluation "Experiment Setup"; its size pinned by Table
+ * tab:GAN's 158.42M parameters):
  *   h = conv3x3([ReLU](x)) + b1,  main = [avgpool2](conv3x3(ReLU(h)) + b2),
  *   y = main + skip,  skip = conv1x1([avgpool2](x)) + bsc (learnable) or x.
  * x: [B][H][W][cpad(cin)] (bf16, or fp32 images when cin <= 4 and
@@ -164,7 +170,9 @@ int paragan_dblock_bwd(paragan_ctx* ctx, const paragan_dblock_desc* d,
                        const void* dy, void* dx, float* grads, void* ws);
 
 /* ---------------------------------------------------------------------
- * Self-attention block (bf16 only):
+ * Self-attention block of the benchmark BigGAN (Evaluation, "Experiment
+ * Setup"; one per network at 64x64, counted in Table tab:GAN's 158.42M),
+ * bf16 only:
  *   theta = x Wt^T (C/8), phi = maxpool2(x Wp^T) (C/8), g = maxpool2(x Wg^T)
  *   (C/2), P = softmax over keys of theta phi^T (no scaling),
  *   y = x + gamma * (P g) Wo^T.  SN on Wt Wp Wg Wo; gamma has none.
@@ -226,15 +234,33 @@ int paragan_gout_bwd(paragan_ctx* ctx, const paragan_gout_desc* d,
                      float* grads, void* ws);
 
 /* ---------------------------------------------------------------------
- * Full BigGAN G+D train step.  The architecture is given by channel
- * multipliers (BigGAN-128: ch 96, G 16,16,8,4,2,1, D 1,2,4,8,16,16 with the
- * last D block not pooling, attention at 64x64, 1000 classes, z 120 split
- * into 6 chunks of 20, shared class embedding 128).  One call runs n_D
- * discriminator steps, each on concat(real_k, G(z_k, y_k)) with labels
- * concat(yr_k, yf_k) (inputs sharing a weight are batched, Implementation
- * "Hardware-Aware Layout Transformation"), then one generator step on
- * (z_g, y_g); the D:G ratio n_D is the caller's (Numerical Optimizations,
- * "Asynchronous Update Scheme").  Hinge loss, Adam on fp32 master weights.
+ * Optimisers.  The paper trains the two networks with different optimisers
+ * (Numerical Optimizations, "Asymmetric Optimization Policy": AdaBelief for
+ * the generator and Adam for the discriminator converge to the better
+ * equilibrium).  Each network carries its own optimiser, on fp32 master
+ * weights, with bias correction and no weight decay; t counts the steps
+ * taken (the update computes step t + 1):
+ *   Adam:       m = b1 m + (1 - b1) g,  v = b2 v + (1 - b2) g^2,
+ *               p -= lr (m / (1 - b1^t)) / (sqrt(v / (1 - b2^t)) + eps)
+ *   AdaBelief (Zhuang et al., NeurIPS 2020, the method the paper cites):
+ *               m = b1 m + (1 - b1) g,  s = b2 s + (1 - b2) (g - m)^2 + eps,
+ *               p -= lr (m / (1 - b1^t)) / (sqrt(s / (1 - b2^t)) + eps)
+ * ------------------------------------------------------------------- */
+enum { PARAGAN_ADAM = 0, PARAGAN_ADABELIEF = 1 };
+
+typedef struct {
+  int32_t kind;         /* PARAGAN_ADAM or PARAGAN_ADABELIEF */
+  float lr, beta1, beta2, eps;   /* lr >= 0, 0 <= beta < 1, eps > 0 */
+} paragan_optim;
+
+/* ---------------------------------------------------------------------
+ * Full BigGAN networks and the G+D training iteration.  The architecture
+ * is given by channel multipliers (BigGAN-128: ch 96, G 16,16,8,4,2,1, D
+ * 1,2,4,8,16,16 with the last D block not pooling, attention at 64x64, 1000
+ * classes, z 120 split into 6 chunks of 20, shared class embedding 128;
+ * Evaluation, "Experiment Setup").  Hinge loss:
+ *   L_D = mean relu(1 - D(x_real, y_real)) + mean relu(1 + D(x_fake, y_fake)),
+ *   L_G = -mean D(G(z, y), y).
  * ------------------------------------------------------------------- */
 typedef struct {
   int32_t img;          /* output resolution */
@@ -249,7 +275,7 @@ typedef struct {
   int32_t B;            /* per-GPU batch (D steps see 2B images) */
   int32_t n_power_iter;
   float bn_eps, sn_eps;
-  float lr_g, lr_d, beta1, beta2, adam_eps;
+  paragan_optim opt_g, opt_d;   /* the generator's and the discriminator's */
 } paragan_biggan_desc;
 
 /* which = 0: generator, 1: discriminator. */
@@ -257,16 +283,44 @@ int paragan_net_layout(const paragan_biggan_desc* d, int32_t which,
                        paragan_tensor_info* out, int32_t cap, int32_t* count,
                        int64_t* n_params, int64_t* n_u);
 int paragan_biggan_check(const paragan_biggan_desc* d);
+/* Workspace of every step call below (one size serves them all). */
 int paragan_train_step_ws_size(const paragan_biggan_desc* d, size_t* ws_bytes);
 
 typedef struct {
-  float* params;   /* flat fp32 master weights (updated by Adam) */
+  float* params;   /* flat fp32 master weights (updated by the optimiser) */
   float* u;        /* flat SN vectors (updated by every forward) */
   float* grads;    /* flat fp32: the last gradient computed (overwritten) */
-  float* adam_m;   /* flat fp32 Adam moments */
-  float* adam_v;
-  int64_t adam_t;  /* Adam steps taken so far (host; incremented) */
+  float* opt_m;    /* flat fp32 first moments */
+  float* opt_v;    /* flat fp32 second moments (Adam's v, AdaBelief's s) */
+  int64_t opt_t;   /* optimiser steps taken so far (host; incremented) */
 } paragan_net_state;
+
+/* Generator forward in training mode (batch statistics, SN u updated):
+ * img (fp32 [B][img][img][3], in [-1, 1]) = G(z, y); z fp32 [B][dz], y [B].
+ * No parameter changes other than u. */
+int paragan_g_sample(paragan_ctx* ctx, const paragan_biggan_desc* d,
+                     paragan_net_state* G, const float* z, const int32_t* y,
+                     float* img, void* ws);
+
+/* One discriminator step on supplied images: D forward, hinge, backward on
+ * the batch concat(x_real, x_fake) with labels concat(y_real, y_fake)
+ * (inputs sharing a weight are batched, Implementation "Hardware-Aware
+ * Layout Transformation"), then D's optimiser.  x_real, x_fake: fp32
+ * [B][img][img][3].  Writes D's gradients and L_D (loss_host, one float);
+ * synchronises the stream at the end.  Returns PARAGAN_ENONFINITE (after
+ * finishing the step) if L_D is not finite. */
+int paragan_d_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
+                   paragan_net_state* D, const float* x_real,
+                   const int32_t* y_real, const float* x_fake,
+                   const int32_t* y_fake, void* ws, float* loss_host);
+
+/* One generator step: G forward on (z, y), D forward (D's u updated, its
+ * weights and optimiser state untouched), hinge L_G, D backward for the
+ * input gradient only, G backward, G's optimiser.  Writes G's gradients and
+ * L_G (loss_host); synchronises at the end; PARAGAN_ENONFINITE as above. */
+int paragan_g_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
+                   paragan_net_state* G, paragan_net_state* D, const float* z,
+                   const int32_t* y, void* ws, float* loss_host);
 
 typedef struct {
   /* n_D entries each: */
@@ -278,9 +332,18 @@ typedef struct {
   const int32_t* y_g;           /* [B] */
 } paragan_step_inputs;
 
-/* Runs the step on the context's stream and synchronises once at the end.
- * losses_host: n_D + 1 floats (L_D per D step, then L_G).  Returns
- * PARAGAN_ENONFINITE (after finishing the step) if a loss is not finite. */
+/* One training iteration: n_D discriminator steps, each on
+ * concat(real_k, G(z_k, y_k)) with labels concat(y_real_k, y_fake_k) -- the
+ * same as paragan_g_sample followed by paragan_d_step -- then one generator
+ * step on (z_g, y_g) as paragan_g_step; the D:G ratio n_D (1..63) is the
+ * caller's (Numerical Optimizations, "Asynchronous Update Scheme": the
+ * ratio is adjustable).  The results equal that sequence of calls bit for
+ * bit.  Besides the context's stream the call uses a second stream of the
+ * context (default priority), ordered by events, for the forwards' SN power
+ * iterations and weight packing, which read only parameters; both streams
+ * are idle when the call returns, also on error.  losses_host: n_D + 1
+ * floats (L_D per D step, then L_G).  Returns PARAGAN_ENONFINITE (after
+ * finishing the step) if a loss is not finite. */
 int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
                        paragan_net_state* G, paragan_net_state* D,
                        const paragan_step_inputs* in, int32_t n_D, void* ws,

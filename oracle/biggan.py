@@ -18,7 +18,9 @@ train step  n_D discriminator steps on concat(real, fake) (inputs that
             share a weight are batched, Implementation "Hardware-Aware
             Layout Transformation"), then one generator step; the D:G
             ratio is adjustable (Numerical Optimizations, "Asynchronous
-            Update Scheme").  Hinge loss; Adam for both networks.
+            Update Scheme").  Hinge loss; each network has its own
+            optimiser (Numerical Optimizations, "Asymmetric Optimization
+            Policy": AdaBelief for G with Adam for D is the paper's pick).
 """
 from dataclasses import dataclass, field
 
@@ -67,15 +69,36 @@ def biggan512():
 
 
 @dataclass
+class OptSpec:
+    """One network's optimiser: kind "adam" or "adabelief"."""
+    kind: str = "adam"
+    lr: float = 1e-4
+    beta1: float = 0.0
+    beta2: float = 0.999
+    eps: float = 1e-6
+
+
+def adam_g():
+    return OptSpec("adam", 1e-4, 0.0, 0.999, 1e-6)
+
+
+def adam_d():
+    return OptSpec("adam", 4e-4, 0.0, 0.999, 1e-6)
+
+
+def adabelief_g():
+    """AdaBelief for the generator.  beta1 > 0 is required: with beta1 = 0
+    the running mean equals the gradient and the belief term vanishes."""
+    return OptSpec("adabelief", 1e-4, 0.5, 0.999, 1e-12)
+
+
+@dataclass
 class HParams:
     bn_eps: float = 1e-5
     sn_eps: float = 1e-12
     n_power_iter: int = 1
-    lr_g: float = 1e-4
-    lr_d: float = 4e-4
-    beta1: float = 0.0
-    beta2: float = 0.999
-    adam_eps: float = 1e-6
+    opt_g: OptSpec = field(default_factory=adam_g)
+    opt_d: OptSpec = field(default_factory=adam_d)
     bf16: bool = True
     frozen: dict = None          # test hook, see BlockCfg.frozen
 
@@ -330,39 +353,50 @@ def d_bwd(a, hp, p, dout, cache, need_dx):
 # train step
 # --------------------------------------------------------------------------
 @dataclass
-class AdamState:
+class OptState:
     m: dict
     v: dict
     t: int = 0
 
 
-def adam_init(p):
-    return AdamState({k: np.zeros_like(v) for k, v in p.items()},
+def opt_init(p):
+    return OptState({k: np.zeros_like(v) for k, v in p.items()},
                      {k: np.zeros_like(v) for k, v in p.items()}, 0)
 
 
-def adam_update(p, grads, st, lr, hp):
+def opt_update(p, grads, st, spec):
+    """One optimiser step of every parameter (step t = st.t + 1)."""
     st.t += 1
+    step = {"adam": L.adam, "adabelief": L.adabelief}[spec.kind]
     newp = {}
     for k in p:
-        newp[k], st.m[k], st.v[k] = L.adam(p[k], grads[k], st.m[k], st.v[k], st.t,
-                                           lr, hp.beta1, hp.beta2, hp.adam_eps)
+        newp[k], st.m[k], st.v[k] = step(p[k], grads[k], st.m[k], st.v[k], st.t,
+                                         spec.lr, spec.beta1, spec.beta2, spec.eps)
     return newp
 
 
-def d_step(a, hp, G, D, optD, x_real, y_real, z, y_fake):
-    """One discriminator step: G forward (no grad), D on concat(real, fake)."""
-    gp, gu = G
+def d_step_images(a, hp, D, optD, x_real, y_real, x_fake, y_fake):
+    """One discriminator step on given images: D forward on
+    concat(real, fake) with labels concat(y_real, y_fake), hinge, backward,
+    D's optimiser.  Returns (D, L_D, D's gradients)."""
     dp, du = D
-    fake, gu, _ = g_fwd(a, hp, gp, gu, z, y_fake)
     b = x_real.shape[0]
-    x = np.concatenate([x_real, fake], axis=0)
+    x = np.concatenate([x_real, x_fake], axis=0)
     yy = np.concatenate([y_real, y_fake], axis=0)
     out, du, cache = d_fwd(a, hp, dp, du, x, yy)
     loss, dr, df = L.hinge_d(out[:b], out[b:])
     _, grads = d_bwd(a, hp, dp, np.concatenate([dr, df]), cache, need_dx=False)
-    dp = adam_update(dp, grads, optD, hp.lr_d, hp)
-    return (gp, gu), (dp, du), loss, grads
+    dp = opt_update(dp, grads, optD, hp.opt_d)
+    return (dp, du), loss, grads
+
+
+def d_step(a, hp, G, D, optD, x_real, y_real, z, y_fake):
+    """One discriminator step: G forward (no gradient; G's u advances),
+    then the D step on concat(real, G(z, y_fake))."""
+    gp, gu = G
+    fake, gu, _ = g_fwd(a, hp, gp, gu, z, y_fake)
+    D, loss, grads = d_step_images(a, hp, D, optD, x_real, y_real, fake, y_fake)
+    return (gp, gu), D, loss, grads
 
 
 def g_step(a, hp, G, D, optG, z, y):
@@ -373,7 +407,7 @@ def g_step(a, hp, G, D, optG, z, y):
     loss, dout = L.hinge_g(out)
     dimg, _ = d_bwd(a, hp, dp, dout, dcache, need_dx=True)
     grads = g_bwd(a, hp, gp, dimg, gcache)
-    gp = adam_update(gp, grads, optG, hp.lr_g, hp)
+    gp = opt_update(gp, grads, optG, hp.opt_g)
     return (gp, gu), (dp, du), loss, grads
 
 

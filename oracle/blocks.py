@@ -18,12 +18,25 @@ Class-conditional BN: gain = 1 + cond W_g^T, bias = cond W_b^T with SN,
 bias-free linears; batch statistics; eps from the config.
 
 Precision (Implementation, "Mixed-Precision Training"): with
-`cfg.bf16` set, every tensor the GPU stores in bfloat16 is rounded here at
-the same point: block outputs, the intermediate conv output, every conv
-operand after its prologue (BN/ReLU/pooling), the packed SN weights and the
+`cfg.bf16` set, every tensor stored in bfloat16 is rounded here at that
+point: block outputs, the intermediate conv output, every conv operand after
+its prologue (BN/ReLU/pooling), the SN-normalised weight operands and the
 activation gradients.  Accumulation, statistics, SN, softmax and weight
 gradients stay in float64.  With `cfg.bf16` unset nothing is rounded (the
 fp32 path, compared at 1e-4).
+
+The spectral normalisation of a block convolution is applied to its
+accumulated product: conv(a, W / sigma) is evaluated as conv(a, W) / sigma,
+the stored weight operand being the master filter itself, so that its bf16
+rounding does not depend on sigma (sigma stays in float64 here, fp32 on the
+GPU).  Two convolutions sit next to a 2x resampling: the generator's conv1
+reads the nearest upsample, the pooling discriminator block's conv2 feeds
+the 2x2 average.  Their weight operand is the folded filter
+(layers.up2_conv_fold, layers.pool2_conv_fold: the 3x3 taps that meet one
+input pixel added), so under bf16 it is the folded filter that is rounded,
+once.  In exact arithmetic all of this equals the plain compositions with
+the normalised 3x3 filter (pinned in the layer and block tests), and the
+weight gradients are those of the plain filter.
 """
 from dataclasses import dataclass
 
@@ -99,19 +112,21 @@ def gblock_fwd(x, cond, p, u, cfg):
     b1 = cond @ ws["bn1.bias"].T
     bn1, c1 = L.cbn_fwd(x, g1, b1, cfg.bn_eps)
     a1 = R(L.relu(bn1))
-    w1 = R(ws["conv1.w"])
-    h1 = R(L.conv2d(L.up2(a1), w1, p["conv1.b"]))
+    s1, s2, ssc = (st[k][2] for k in ("conv1.w", "conv2.w", "sc.w"))
+    f1 = R(L.up2_conv_fold(p["conv1.w"]))      # conv3x3 over up2, folded
+    h1 = R(L.up2_conv(a1, f1) / s1 + p["conv1.b"])
     g2 = 1.0 + cond @ ws["bn2.gain"].T
     b2 = cond @ ws["bn2.bias"].T
     bn2, c2 = L.cbn_fwd(h1, g2, b2, cfg.bn_eps)
     a2 = R(L.relu(bn2))
-    w2 = R(ws["conv2.w"])
-    wsc = R(ws["sc.w"])
+    w2 = R(p["conv2.w"])
+    wsc = R(p["sc.w"])
     # conv1x1(up2(x)) == up2(conv1x1(x)) exactly; the skip is summed unrounded
-    skip = L.up2(L.conv2d(x, wsc, p["sc.b"]))
-    y = R(L.conv2d(a2, w2, p["conv2.b"]) + skip)
-    cache = dict(x=x, cond=cond, ws=ws, st=st, bn1=bn1, c1=c1, a1=a1, w1=w1,
-                 h1=h1, bn2=bn2, c2=c2, a2=a2, w2=w2, wsc=wsc)
+    skip = L.up2(L.conv2d(x, wsc) / ssc + p["sc.b"])
+    y = R(L.conv2d(a2, w2) / s2 + p["conv2.b"] + skip)
+    cache = dict(x=x, cond=cond, ws=ws, st=st, bn1=bn1, c1=c1, a1=a1, f1=f1,
+                 h1=h1, bn2=bn2, c2=c2, a2=a2, w2=w2, wsc=wsc, s1=s1, s2=s2,
+                 ssc=ssc)
     return y, u_new, cache
 
 
@@ -125,14 +140,14 @@ def gblock_bwd(dy, cache, cfg):
     dys = L.up2_bwd(dy)                       # skip gradient at low resolution
     dws["sc.w"] = L.conv2d_wgrad(dys, c["x"], 1)
     grads["sc.b"] = L.bias_grad(dys)
-    dx_skip = L.conv2d_dgrad(R(dys), c["wsc"])
-    da2 = L.conv2d_dgrad(dy, c["w2"])
+    dx_skip = L.conv2d_dgrad(R(dys), c["wsc"]) / c["ssc"]
+    da2 = L.conv2d_dgrad(dy, c["w2"]) / c["s2"]
     dbn2 = da2 * (c["bn2"] > 0)
     dh1, dg2, db2 = L.cbn_bwd(dbn2, c["c2"])
     dh1 = R(dh1)
     dws["conv1.w"] = L.conv2d_wgrad(dh1, L.up2(c["a1"]), 3)
     grads["conv1.b"] = L.bias_grad(dh1)
-    da1 = L.up2_bwd(L.conv2d_dgrad(dh1, c["w1"]))
+    da1 = L.up2_conv_dgrad(dh1, c["f1"]) / c["s1"]
     dbn1 = da1 * (c["bn1"] > 0)
     dx1, dg1, db1 = L.cbn_bwd(dbn1, c["c1"])
     dx = R(dx1 + dx_skip)
@@ -166,18 +181,26 @@ def dblock_fwd(x, p, u, cfg, preact, down, learnable_sc):
     ws, st = _sn_all(p, u, keys, cfg, u_new)
     x = R(x)                                  # operand precision of the input
     a0 = L.relu(x) if preact else x
-    w1, w2 = R(ws["conv1.w"]), R(ws["conv2.w"])
-    h = R(L.conv2d(a0, w1, p["conv1.b"]))
+    s1, s2 = st["conv1.w"][2], st["conv2.w"][2]
+    w1 = R(p["conv1.w"])
+    h = R(L.conv2d(a0, w1) / s1 + p["conv1.b"])
     a1 = L.relu(h)
-    c2 = L.conv2d(a1, w2, p["conv2.b"])
-    main = L.avgpool2(c2) if down else c2
-    cache = dict(x=x, a0=a0, h=h, a1=a1, w1=w1, w2=w2, ws=ws, st=st)
+    if down:
+        # avgpool2(conv3x3): one stride-2 4x4 filter, folded
+        w2 = R(L.pool2_conv_fold(p["conv2.w"]))
+        main = L.pool2_conv(a1, w2) / s2 + p["conv2.b"]
+    else:
+        w2 = R(p["conv2.w"])
+        main = L.conv2d(a1, w2) / s2 + p["conv2.b"]
+    cache = dict(x=x, a0=a0, h=h, a1=a1, w1=w1, w2=w2, s1=s1, s2=s2, ws=ws,
+                 st=st)
     if learnable_sc:
         # avgpool and conv1x1 commute exactly; pool first, operand in bf16
         xs = R(L.avgpool2(x)) if down else x
-        wsc = R(ws["sc.w"])
-        sc = L.conv2d(xs, wsc, p["sc.b"])
-        cache.update(xs=xs, wsc=wsc)
+        wsc = R(p["sc.w"])
+        ssc = st["sc.w"][2]
+        sc = L.conv2d(xs, wsc) / ssc + p["sc.b"]
+        cache.update(xs=xs, wsc=wsc, ssc=ssc)
     else:
         sc = x
     y = R(main + sc)
@@ -193,16 +216,17 @@ def dblock_bwd(dy, cache, cfg, preact, down, learnable_sc, dx_f32=False):
     dc2 = L.avgpool2_bwd(dy) if down else dy
     dws["conv2.w"] = L.conv2d_wgrad(dc2, c["a1"], 3)
     grads["conv2.b"] = L.bias_grad(dc2)
-    dh = R(L.conv2d_dgrad(dc2, c["w2"]) * (c["h"] > 0))
+    da1 = (L.pool2_conv_dgrad(dy, c["w2"]) if down else L.conv2d_dgrad(dy, c["w2"])) / c["s2"]
+    dh = R(da1 * (c["h"] > 0))
     dws["conv1.w"] = L.conv2d_wgrad(dh, c["a0"], 3)
     grads["conv1.b"] = L.bias_grad(dh)
-    dxm = L.conv2d_dgrad(dh, c["w1"])
+    dxm = L.conv2d_dgrad(dh, c["w1"]) / c["s1"]
     if preact:
         dxm = dxm * (c["x"] > 0)
     if learnable_sc:
         dws["sc.w"] = L.conv2d_wgrad(dy, c["xs"], 1)
         grads["sc.b"] = L.bias_grad(dy)
-        dxs = L.conv2d_dgrad(dy, c["wsc"])
+        dxs = L.conv2d_dgrad(dy, c["wsc"]) / c["ssc"]
         dxsc = L.avgpool2_bwd(dxs) if down else dxs
     else:
         dxsc = dy

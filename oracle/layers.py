@@ -66,6 +66,113 @@ def bias_grad(dy):
 
 
 # --------------------------------------------------------------------------
+# a 3x3 convolution fused with the 2x resampling next to it.  The 3x3 taps
+# that meet the same input pixel are added first; in exact arithmetic this is
+# the plain composition (the tests pin both identities).  Under bfloat16
+# storage the folded filter, not the 3x3 one, is the stored weight operand.
+# --------------------------------------------------------------------------
+def up2_conv_fold(w):
+    """Sub-pixel filters of conv3x3(up2(x), w).
+
+    Output pixel (2i + a, 2j + b) with tap (r, s) reads the upsampled pixel
+    (2i + a + r - 1, 2j + b + s - 1), i.e. the source pixel
+    (i + (a + r - 1) // 2, j + (b + s - 1) // 2).  For parity a that row
+    offset is a - 1 + t with t in {0, 1}.  Returns F of shape
+    (2, 2, Cout, 2, 2, Cin): F[a, b][:, t, u, :] is the sum of the taps
+    (r, s) whose source pixel is (i + a - 1 + t, j + b - 1 + u)."""
+    co, r_, s_, ci = w.shape
+    assert r_ == 3 and s_ == 3
+    F = np.zeros((2, 2, co, 2, 2, ci))
+    for a in range(2):
+        for b in range(2):
+            for r in range(3):
+                for s in range(3):
+                    t = (a + r - 1) // 2 - (a - 1)
+                    u = (b + s - 1) // 2 - (b - 1)
+                    F[a, b, :, t, u, :] += w[:, r, s, :]
+    return F
+
+
+def up2_conv(x, F, b=None):
+    """y (N, 2H, 2W, Cout): y[n, 2i+a, 2j+b] = b + sum over t, u in {0, 1} of
+    xpad[n, i+a+t, j+b+u] . F[a, b][:, t, u, :], xpad = x zero-padded by one
+    pixel.  Equals conv2d(up2(x), w, b) for F = up2_conv_fold(w)."""
+    n, h, wd, _ = x.shape
+    co = F.shape[2]
+    xp = _pad(x, 1)
+    y = np.zeros((n, 2 * h, 2 * wd, co))
+    for a in range(2):
+        for bb in range(2):
+            acc = np.zeros((n, h, wd, co))
+            for t in range(2):
+                for u in range(2):
+                    acc += xp[:, a + t:a + t + h, bb + u:bb + u + wd, :] @ F[a, bb, :, t, u, :].T
+            y[:, a::2, bb::2, :] = acc
+    if b is not None:
+        y += b
+    return y
+
+
+def up2_conv_dgrad(dy, F):
+    """Adjoint of up2_conv in x: dx (N, H, W, Cin) from dy (N, 2H, 2W, Cout)."""
+    n, h2, w2, _ = dy.shape
+    h, wd = h2 // 2, w2 // 2
+    ci = F.shape[-1]
+    dxp = np.zeros((n, h + 2, wd + 2, ci))
+    for a in range(2):
+        for bb in range(2):
+            g = dy[:, a::2, bb::2, :]
+            for t in range(2):
+                for u in range(2):
+                    dxp[:, a + t:a + t + h, bb + u:bb + u + wd, :] += g @ F[a, bb, :, t, u, :]
+    return dxp[:, 1:h + 1, 1:wd + 1, :]
+
+
+def pool2_conv_fold(w):
+    """Stride-2 4x4 filter of avgpool2(conv3x3(x, w)).
+
+    Pooled pixel (i, j) averages the conv outputs (2i + a, 2j + b), whose
+    tap (r, s) reads xpad[2i + a + r, 2j + b + s]; with t = a + r and
+    u = b + s in 0..3, P[:, t, u, :] = 1/4 of the sum of w[:, t - a, u - b, :]
+    over a, b in {0, 1} with the tap inside the 3x3 filter."""
+    co, r_, s_, ci = w.shape
+    assert r_ == 3 and s_ == 3
+    P = np.zeros((co, 4, 4, ci))
+    for a in range(2):
+        for b in range(2):
+            P[:, a:a + 3, b:b + 3, :] += w
+    return 0.25 * P
+
+
+def pool2_conv(x, P, b=None):
+    """y (N, H/2, W/2, Cout): y[n, i, j] = b + sum over t, u in 0..3 of
+    xpad[n, 2i+t, 2j+u] . P[:, t, u, :], xpad = x zero-padded by one pixel.
+    Equals avgpool2(conv2d(x, w, b)) for P = pool2_conv_fold(w)."""
+    n, h, wd, _ = x.shape
+    ho, wo = h // 2, wd // 2
+    co = P.shape[0]
+    xp = _pad(x, 1)
+    y = np.zeros((n, ho, wo, co))
+    for t in range(4):
+        for u in range(4):
+            y += xp[:, t:t + 2 * ho:2, u:u + 2 * wo:2, :] @ P[:, t, u, :].T
+    if b is not None:
+        y += b
+    return y
+
+
+def pool2_conv_dgrad(dy, P):
+    """Adjoint of pool2_conv in x: dx (N, 2Ho, 2Wo, Cin) from dy (N, Ho, Wo, Cout)."""
+    n, ho, wo, _ = dy.shape
+    ci = P.shape[-1]
+    dxp = np.zeros((n, 2 * ho + 2, 2 * wo + 2, ci))
+    for t in range(4):
+        for u in range(4):
+            dxp[:, t:t + 2 * ho:2, u:u + 2 * wo:2, :] += dy @ P[:, t, u, :]
+    return dxp[:, 1:2 * ho + 1, 1:2 * wo + 1, :]
+
+
+# --------------------------------------------------------------------------
 # resampling
 # --------------------------------------------------------------------------
 def up2(x):
@@ -220,6 +327,20 @@ def hinge_g(out_fake):
     """L_G = -mean D(G(z))."""
     b = out_fake.shape[0]
     return float(-out_fake.mean()), np.full(out_fake.shape, -1.0 / b)
+
+
+def adabelief(p, g, m, s, t, lr, beta1, beta2, eps):
+    """AdaBelief step t (t >= 1), the optimiser the paper pairs with the
+    generator (Numerical Optimizations, "Asymmetric Optimization Policy"),
+    as its authors define it (Zhuang et al., NeurIPS 2020): the second
+    moment tracks the squared deviation of the gradient from its running
+    mean (the "belief"), eps inside the moment and in the denominator,
+    bias-corrected, no weight decay."""
+    m = beta1 * m + (1.0 - beta1) * g
+    s = beta2 * s + (1.0 - beta2) * (g - m) ** 2 + eps
+    mhat = m / (1.0 - beta1 ** t)
+    shat = s / (1.0 - beta2 ** t)
+    return p - lr * mhat / (np.sqrt(shat) + eps), m, s
 
 
 def adam(p, g, m, v, t, lr, beta1, beta2, eps):

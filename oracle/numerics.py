@@ -15,22 +15,28 @@ _OVERFLOW = (2.0 - 2.0 ** -8) * 2.0 ** 127      # rounds up to inf at/after this
 
 
 def bf16(x):
-    """Round float64 values to bfloat16 (round to nearest, ties to even)."""
+    """Round float64 values to bfloat16 (round to nearest, ties to even).
+
+    A normal bfloat16 keeps 8 significant bits, i.e. the top 7 of float64's
+    52 stored fraction bits: rounding to nearest even at bit 45 of the
+    float64 pattern (add half the dropped range, minus one unless the kept
+    last bit is odd, then clear the dropped bits) gives it exactly, a carry
+    into the exponent included.  Below 2**-126 bfloat16 has a fixed quantum
+    of 2**-133; from _OVERFLOW on the result is +-inf; NaN stays NaN."""
     x = np.asarray(x, dtype=np.float64)
-    out = np.empty_like(x)
+    bits = np.ascontiguousarray(x).view(np.uint64)
+    odd = (bits >> np.uint64(45)) & np.uint64(1)
+    r = (bits + (np.uint64((1 << 44) - 1) + odd)) & ~np.uint64((1 << 45) - 1)
+    out = r.view(np.float64).reshape(x.shape)
     ax = np.abs(x)
-    finite = np.isfinite(x)
-    normal = finite & (ax >= 2.0 ** -126)
-    # normal range: x = m * 2**e with 0.5 <= |m| < 1; keep 8 significant bits
-    m, e = np.frexp(np.where(normal, x, 1.0))
-    q = np.round(m * 256.0)                      # numpy rounds half to even
-    out[...] = np.ldexp(q, e - 8)
-    # subnormal range: fixed quantum 2**-133
-    sub = finite & ~normal
-    out[sub] = np.round(x[sub] * 2.0 ** 133) * 2.0 ** -133
-    over = finite & (ax >= _OVERFLOW)
-    out[over] = np.copysign(np.inf, x[over])
-    out[~finite] = x[~finite]
+    sub = ax < 2.0 ** -126
+    if sub.any():
+        out = out.copy()
+        out[sub] = np.round(x[sub] * 2.0 ** 133) * 2.0 ** -133
+    big = ~(ax < _OVERFLOW)                      # overflow, inf and NaN
+    if big.any():
+        out = out.copy() if not sub.any() else out
+        out[big] = np.where(np.isnan(x[big]), x[big], np.copysign(np.inf, x[big]))
     return out
 
 

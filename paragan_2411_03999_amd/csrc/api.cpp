@@ -305,6 +305,17 @@ extern "C" int paragan_sn_ws_size(int64_t rows, int64_t cols, size_t* ws_bytes) 
   })
 }
 
+static void sn_check(int64_t rows, int64_t cols, int n_iter, float eps) {
+  PG_CHECK(rows >= 1 && cols >= 1, "sn_power_iter: rows and cols must be >= 1");
+  PG_CHECK(n_iter >= 1, "sn_power_iter: n_iter must be >= 1");
+  PG_CHECK(eps > 0.f, "sn_power_iter: eps must be > 0");
+  PG_CHECK(rows < (1LL << 31) && cols < (1LL << 31), "sn_power_iter: matrix too large");
+}
+
+extern "C" int paragan_sn_check(int64_t rows, int64_t cols, int n_iter, float eps) {
+  PG_TRY(nullptr, sn_check(rows, cols, n_iter, eps))
+}
+
 extern "C" int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t rows, int64_t cols, float* u,
                                      float* v, float* sigma, int n_iter, float eps, void* ws) {
   if (!ctx) return PARAGAN_EINVAL;
@@ -312,10 +323,7 @@ extern "C" int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t r
   PG_TRY(ctx, {
     need(W, "W"); need(u, "u"); need(v, "v"); need(sigma, "sigma"); need(ws, "ws");
     aligned(ws, "ws");
-    PG_CHECK(rows >= 1 && cols >= 1, "sn_power_iter: rows and cols must be >= 1");
-    PG_CHECK(n_iter >= 1, "sn_power_iter: n_iter must be >= 1");
-    PG_CHECK(eps > 0.f, "sn_power_iter: eps must be > 0");
-    PG_CHECK(rows < (1LL << 31) && cols < (1LL << 31), "sn_power_iter: matrix too large");
+    sn_check(rows, cols, n_iter, eps);
     sn_power_iter(ctx->stream, W, rows, cols, u, v, sigma, n_iter, eps, ws);
   })
 }
@@ -503,8 +511,67 @@ extern "C" int paragan_train_step_ws_size(const paragan_biggan_desc* d, size_t* 
 static void need_state(const paragan_net_state* s, const char* who) {
   need(s, who);
   need(s->params, "params"); need(s->u, "u"); need(s->grads, "grads");
-  need(s->adam_m, "adam_m"); need(s->adam_v, "adam_v");
-  PG_CHECK(s->adam_t >= 0, "adam_t must be >= 0");
+  need(s->opt_m, "opt_m"); need(s->opt_v, "opt_v");
+  PG_CHECK(s->opt_t >= 0, "opt_t must be >= 0");
+}
+
+static int finish_losses(paragan_ctx* ctx, const float* losses, int n, const char* who) {
+  for (int k = 0; k < n; ++k)
+    if (!std::isfinite(losses[k])) return fail(ctx, PARAGAN_ENONFINITE, std::string(who) + ": non-finite loss");
+  return PARAGAN_OK;
+}
+
+#define PG_STEP_TRY(ctx, ...)                              \
+  try {                                                    \
+    __VA_ARGS__;                                           \
+  } catch (const ::pg::Error& e) {                         \
+    return fail(ctx, e.code, e.msg);                       \
+  } catch (const std::exception& e) {                      \
+    return fail(ctx, PARAGAN_EINVAL, e.what());            \
+  }
+
+extern "C" int paragan_g_sample(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G,
+                                const float* z, const int32_t* y, float* img, void* ws) {
+  if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
+  PG_TRY(ctx, {
+    check_arch(d);
+    need_state(G, "G");
+    need(z, "z"); need(y, "y"); need(img, "img"); need(ws, "ws");
+    aligned(ws, "ws");
+    g_sample(ctx, d, G, z, y, img, ws);
+  })
+}
+
+extern "C" int paragan_d_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* D,
+                              const float* x_real, const int32_t* y_real, const float* x_fake,
+                              const int32_t* y_fake, void* ws, float* loss_host) {
+  if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
+  PG_STEP_TRY(ctx, {
+    check_arch(d);
+    need_state(D, "D");
+    need(x_real, "x_real"); need(y_real, "y_real"); need(x_fake, "x_fake"); need(y_fake, "y_fake");
+    need(ws, "ws"); need(loss_host, "loss_host");
+    aligned(ws, "ws");
+    d_step(ctx, d, D, x_real, y_real, x_fake, y_fake, ws, loss_host);
+  })
+  return finish_losses(ctx, loss_host, 1, "d_step");
+}
+
+extern "C" int paragan_g_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G,
+                              paragan_net_state* D, const float* z, const int32_t* y, void* ws, float* loss_host) {
+  if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
+  PG_STEP_TRY(ctx, {
+    check_arch(d);
+    need_state(G, "G");
+    need_state(D, "D");
+    need(z, "z"); need(y, "y"); need(ws, "ws"); need(loss_host, "loss_host");
+    aligned(ws, "ws");
+    g_step(ctx, d, G, D, z, y, ws, loss_host);
+  })
+  return finish_losses(ctx, loss_host, 1, "g_step");
 }
 
 extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G,
@@ -512,7 +579,7 @@ extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d
                                   float* losses_host) {
   if (!ctx) return PARAGAN_EINVAL;
   ProfBind pb(ctx);
-  try {
+  PG_STEP_TRY(ctx, {
     check_arch(d);
     need_state(G, "G");
     need_state(D, "D");
@@ -526,14 +593,8 @@ extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d
     }
     need(in->z_g, "z_g"); need(in->y_g, "y_g");
     train_step(ctx, d, G, D, in, n_D, ws, losses_host);
-    for (int k = 0; k <= n_D; ++k)
-      if (!std::isfinite(losses_host[k])) return fail(ctx, PARAGAN_ENONFINITE, "train_step: non-finite loss");
-    return PARAGAN_OK;
-  } catch (const Error& e) {
-    return fail(ctx, e.code, e.msg);
-  } catch (const std::exception& e) {
-    return fail(ctx, PARAGAN_EINVAL, e.what());
-  }
+  })
+  return finish_losses(ctx, losses_host, n_D + 1, "train_step");
 }
 
 // ------------------------------------------------------------ profiler

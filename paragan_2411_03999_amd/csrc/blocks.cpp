@@ -194,10 +194,11 @@ size_t GBlock::ws_size(int n_cu) const {
 
 // the data-gradient weight packs of a G block into (wd1, wd2, wdsc)
 static void g_pack_dgrad(const GBlock& g, hipStream_t st, const Params& P, void* wd1, void* wd2, void* wdsc) {
-  const PackJob pk[3] = {{P.w("conv1.w"), g.sn[2].sigma, wd1, g.cout, g.cin, 3, g.Cop, g.Cip,
+  // unnormalised: the data-gradient convs divide by sigma
+  const PackJob pk[3] = {{P.w("conv1.w"), nullptr, wd1, g.cout, g.cin, 3, g.Cop, g.Cip,
                           g.f32 ? kPackDgrad : kPackDgradSum4},
-                         {P.w("conv2.w"), g.sn[5].sigma, wd2, g.cout, g.cout, 3, g.Cop, g.Cop, kPackDgrad},
-                         {P.w("sc.w"), g.sn[6].sigma, wdsc, g.cout, g.cin, 1, g.Cop, g.Cip,
+                         {P.w("conv2.w"), nullptr, wd2, g.cout, g.cout, 3, g.Cop, g.Cop, kPackDgrad},
+                         {P.w("sc.w"), nullptr, wdsc, g.cout, g.cin, 1, g.Cop, g.Cip,
                           g.f32 ? kPackDgrad : kPackDgradRep4}};
   pack_group(st, g.f32, pk, 3);
 }
@@ -206,9 +207,11 @@ void GBlock::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   SnJob jobs[7];
   for (int i = 0; i < 7; ++i) jobs[i] = sn_job(P, kGSN[i], sn[i]);
   sn_power_iter_group(st, jobs, 7, npi, sn_eps, sn_ws);
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[2].sigma, wp1, cout, cin, 3, Cop, Cip, f32 ? kPackFwd : kPackSub},
-                         {P.w("conv2.w"), sn[5].sigma, wp2, cout, cout, 3, Cop, Cop, kPackFwd},
-                         {P.w("sc.w"), sn[6].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
+  // the filters are packed unnormalised (the stored bf16 values do not
+  // depend on sigma); each conv divides its accumulator by its sigma
+  const PackJob pk[3] = {{P.w("conv1.w"), nullptr, wp1, cout, cin, 3, Cop, Cip, f32 ? kPackFwd : kPackSub},
+                         {P.w("conv2.w"), nullptr, wp2, cout, cout, 3, Cop, Cop, kPackFwd},
+                         {P.w("sc.w"), nullptr, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
   pack_group(st, f32, pk, 3);
   if (for_bwd && keep_dgrad) {
     g_pack_dgrad(*this, st, P, wd1s, wd2s, wdscs);
@@ -230,7 +233,7 @@ void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* co
   ConvIn in;
   in.x = a1; in.B = B; in.Hx = H; in.Wx = W; in.C = Cip; in.gather = G_UP2;
   ConvOut o;
-  o.y = h1; o.y_f32 = f32; o.yC = Cop; o.n_real = cout; o.bias = P.w("conv1.b");
+  o.y = h1; o.y_f32 = f32; o.yC = Cop; o.n_real = cout; o.bias = P.w("conv1.b"); o.acc_div = sn[2].sigma;
   if (!f32) {
     // bf16: the four sub-pixel 2x2 convs over a1 itself
     in.gather = G_SUB;
@@ -246,14 +249,14 @@ void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* co
   ConvIn si;
   si.x = x; si.B = B; si.Hx = H; si.Wx = W; si.C = Cip;
   ConvOut so;
-  so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b");
+  so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b"); so.acc_div = sn[6].sigma;
   conv_fwd(ex.st, f32, si, H, W, 1, wpsc, Cop, so);
   // y = conv3x3(a2) + b2 + up2(skip), a2 = relu(cbn2(h1))
   bn_apply(ex.st, f32, h1, M2, 4 * H * W, cout, Cop, mean2, scale2, bias2, Cop, true, a2);
   ConvIn i2;
   i2.x = a2; i2.B = B; i2.Hx = 2 * H; i2.Wx = 2 * W; i2.C = Cop;
   ConvOut o2;
-  o2.y = y; o2.y_f32 = f32; o2.yC = Cop; o2.n_real = cout; o2.bias = P.w("conv2.b");
+  o2.y = y; o2.y_f32 = f32; o2.yC = Cop; o2.n_real = cout; o2.bias = P.w("conv2.b"); o2.acc_div = sn[5].sigma;
   o2.res = w.skip; o2.res_f32 = 1; o2.res_mode = R_HALF; o2.resC = Cop;
   conv_fwd(ex.st, f32, i2, 2 * H, 2 * W, 3, wp2, Cop, o2);
 }
@@ -290,13 +293,13 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   ConvIn dsp;
   dsp.x = dy; dsp.B = B; dsp.Hx = H2; dsp.Wx = W2; dsp.C = Cop; dsp.gather = f32 ? G_POOL2 : G_S2;
   ConvOut dso;
-  dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = cin;
+  dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = cin; dso.acc_div = sn[6].sigma;
   conv_fwd(ex.st, f32, dsp, H, W, f32 ? 1 : 2, wdsc, Cip, dso);
   // da2 = conv2^T dy (fp32)
   ConvIn d2;
   d2.x = dy; d2.B = B; d2.Hx = H2; d2.Wx = W2; d2.C = Cop;
   ConvOut d2o;
-  d2o.y = w.da2; d2o.y_f32 = 1; d2o.yC = Cop; d2o.n_real = cout;
+  d2o.y = w.da2; d2o.y_f32 = 1; d2o.yC = Cop; d2o.n_real = cout; d2o.acc_div = sn[5].sigma;
   conv_fwd(ex.st, f32, d2, H2, W2, 3, wd2, Cop, d2o);
   // cBN2 backward (through the ReLU) -> dh1
   bn_bwd(ex.st, f32, w.da2, false, h1, B, H2, W2, cout, Cop, mean2, rstd2, gain2, bias2, Cop, nullptr, w.dh1,
@@ -321,7 +324,7 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   ConvIn d1;
   d1.x = w.dh1; d1.B = B; d1.Hx = H2; d1.Wx = W2; d1.C = Cop;
   ConvOut d1o;
-  d1o.y = w.da1; d1o.y_f32 = 1; d1o.yC = Cip; d1o.n_real = cin;
+  d1o.y = w.da1; d1o.y_f32 = 1; d1o.yC = Cip; d1o.n_real = cin; d1o.acc_div = sn[2].sigma;
   if (!f32) {
     d1.gather = G_S2;
     conv_fwd(ex.st, f32, d1, H, W, 4, wd1, Cip, d1o);
@@ -434,10 +437,11 @@ size_t DBlock::ws_size(int n_cu) const {
 // the data-gradient weight packs of a D block into (wd1, wd2, wdsc)
 static void d_pack_dgrad(const DBlock& d, hipStream_t st, const Params& P, void* wd1, void* wd2, void* wdsc) {
   const int R1 = d.im2col ? 1 : 3, K1 = d.im2col ? 9 * d.cin : d.cin, ksc = d.im2col ? 4 * d.cin : 0;
-  const PackJob pk[3] = {{P.w("conv1.w"), d.sn[0].sigma, wd1, d.cout, K1, R1, d.Cop, d.Cip, kPackDgrad},
-                         {P.w("conv2.w"), d.sn[1].sigma, wd2, d.cout, d.cout, 3, d.Cop, d.Cop,
+  // unnormalised: the data-gradient convs divide by sigma
+  const PackJob pk[3] = {{P.w("conv1.w"), nullptr, wd1, d.cout, K1, R1, d.Cop, d.Cip, kPackDgrad},
+                         {P.w("conv2.w"), nullptr, wd2, d.cout, d.cout, 3, d.Cop, d.Cop,
                           d.subdgrad() ? kPackSubDgrad : kPackDgrad},
-                         {d.lsc ? P.w("sc.w") : nullptr, d.sn[2].sigma, wdsc, d.cout, d.cin, 1, d.Cop, d.Cip,
+                         {d.lsc ? P.w("sc.w") : nullptr, nullptr, wdsc, d.cout, d.cin, 1, d.Cop, d.Cip,
                           kPackDgrad, ksc}};
   pack_group(st, d.f32, pk, d.lsc ? 3 : 2);
 }
@@ -451,9 +455,10 @@ void DBlock::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   // channels (the [Cout][3][3][cin] weight read as [Cout][9 cin]) and the
   // skip's 1x1 filter sits on the centre tap's channels 4 cin ..
   const int R1 = im2col ? 1 : 3, K1 = im2col ? 9 * cin : cin, ksc = im2col ? 4 * cin : 0;
-  const PackJob pk[3] = {{P.w("conv1.w"), sn[0].sigma, wp1, cout, K1, R1, Cop, Cip, kPackFwd},
-                         {P.w("conv2.w"), sn[1].sigma, wp2, cout, cout, 3, Cop, Cop, s2conv() ? kPackPool4 : kPackFwd},
-                         {lsc ? P.w("sc.w") : nullptr, sn[2].sigma, wpsc, cout, cin, 1, Cop, Cip, kPackFwd, ksc}};
+  // packed unnormalised; each conv divides its accumulator by its sigma
+  const PackJob pk[3] = {{P.w("conv1.w"), nullptr, wp1, cout, K1, R1, Cop, Cip, kPackFwd},
+                         {P.w("conv2.w"), nullptr, wp2, cout, cout, 3, Cop, Cop, s2conv() ? kPackPool4 : kPackFwd},
+                         {lsc ? P.w("sc.w") : nullptr, nullptr, wpsc, cout, cin, 1, Cop, Cip, kPackFwd, ksc}};
   pack_group(st, f32, pk, nsn);
   if (for_bwd && keep_dgrad) {
     d_pack_dgrad(*this, st, P, wd1s, wd2s, wdscs);
@@ -470,7 +475,7 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   ConvIn i1;
   i1.x = x; i1.B = B; i1.Hx = H; i1.Wx = W; i1.C = Cip; i1.relu = preact; i1.c_real = K1;
   ConvOut o1;
-  o1.y = h; o1.y_f32 = f32; o1.yC = Cop; o1.n_real = cout; o1.bias = P.w("conv1.b");
+  o1.y = h; o1.y_f32 = f32; o1.yC = Cop; o1.n_real = cout; o1.bias = P.w("conv1.b"); o1.acc_div = sn[0].sigma;
   conv_fwd(ex.st, f32, i1, H, W, R1, wp1, Cop, o1);
   // skip = conv1x1([avgpool](x)) + bsc, fp32
   if (lsc) {
@@ -481,7 +486,7 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
       si.x = xp; si.Hx = Ho; si.Wx = Wo;
     }
     ConvOut so;
-    so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b");
+    so.y = w.skip; so.y_f32 = 1; so.yC = Cop; so.n_real = cout; so.bias = P.w("sc.b"); so.acc_div = sn[2].sigma;
     conv_fwd(ex.st, f32, si, Ho, Wo, 1, wpsc, Cop, so);
   }
   // y = [avgpool](conv3x3(relu(h)) + b2) + skip; with downsampling in bf16 the
@@ -490,6 +495,7 @@ void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {
   i2.x = h; i2.B = B; i2.Hx = H; i2.Wx = W; i2.C = Cop; i2.relu = 1;
   ConvOut o2;
   o2.y = y; o2.y_f32 = f32; o2.yC = Cop; o2.n_real = cout; o2.bias = P.w("conv2.b"); o2.pool = down;
+  o2.acc_div = sn[1].sigma;
   o2.res_mode = R_SAME; o2.resC = Cop;
   if (lsc) { o2.res = w.skip; o2.res_f32 = 1; }
   else { o2.res = x; o2.res_f32 = f32; }
@@ -542,7 +548,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   d2.x = dy; d2.B = B; d2.Hx = Ho; d2.Wx = Wo; d2.C = Cop;
   if (down) { d2.gather = G_UP2; d2.gscale = 0.25f; }
   ConvOut d2o;
-  d2o.y = w.dh; d2o.y_f32 = f32; d2o.yC = Cop; d2o.n_real = cout;
+  d2o.y = w.dh; d2o.y_f32 = f32; d2o.yC = Cop; d2o.n_real = cout; d2o.acc_div = sn[1].sigma;
   d2o.mask = h; d2o.mask_f32 = f32; d2o.maskC = Cop;
   if (subdgrad()) {
     // conv2^T over up2(dy) / 4 as the four sub-pixel 2x2 convs over dy
@@ -576,7 +582,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
       ConvIn ds;
       ds.x = dy; ds.B = B; ds.Hx = Ho; ds.Wx = Wo; ds.C = Cop;
       ConvOut dso;
-      dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = ksc + cin;
+      dso.y = w.dxs; dso.y_f32 = 1; dso.yC = Cip; dso.n_real = ksc + cin; dso.acc_div = sn[2].sigma;
       conv_fwd(ex.st, f32, ds, Ho, Wo, 1, wdsc, Cip, dso);
     }
   }
@@ -586,6 +592,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     ConvOut d1o;
     // with 3x3-patch input: the patch gradient (fp32), folded onto the image after
     d1o.y = im2col ? (void*)w.dcol : dx; d1o.y_f32 = dx_f32 || f32 || im2col; d1o.yC = Cip;
+    d1o.acc_div = sn[0].sigma;
     d1o.n_real = im2col ? K1 : cin;
     if (preact) { d1o.mask = x; d1o.mask_f32 = f32; d1o.maskC = Cip; }
     if (lsc) {

@@ -128,10 +128,10 @@ struct DBlock {
   void* xp = nullptr;   // 2x2 average of the input (downsampling learnable skip)
   // conv2 + 2x2 average pool as one stride-2 4x4 conv (bf16 downsampling blocks)
   bool s2conv() const { return down && !f32; }
-  // its data gradient as four sub-pixel 2x2 convs (K = 4 Cout; below 96
-  // channels, where no sub-pixel halo tile applies, the short K loses to the
-  // 3x3 form over the upsampled gradient)
-  bool subdgrad() const { return s2conv() && cout >= 96; }
+  // its data gradient as four sub-pixel 2x2 convs (K = 4 Cout) at every
+  // width, so that forward and data gradient use the same bf16 folded taps
+  // (the 3x3 form over the upsampled gradient would round the 3x3 taps)
+  bool subdgrad() const { return s2conv(); }
   void plan_saved(Arena& a);
   size_t ws_size(int n_cu) const;
   // The forward's SN power iterations and weight packing: fwd runs them

@@ -281,7 +281,7 @@ __global__ __launch_bounds__(256, 2) void k_conv_mfma(ConvK k) {
   }
 
   // epilogue
-  const float accs = (k.o.acc_scale ? *k.o.acc_scale : 1.f) * k.o.acc_mul;
+  const float accs = (k.o.acc_scale ? *k.o.acc_scale : 1.f) * k.o.acc_mul / (k.o.acc_div ? *k.o.acc_div : 1.f);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -371,7 +371,7 @@ __global__ __launch_bounds__(256) void k_conv_simt(ConvK k) {
     }
     __syncthreads();
   }
-  const float accs = (k.o.acc_scale ? *k.o.acc_scale : 1.f) * k.o.acc_mul;
+  const float accs = (k.o.acc_scale ? *k.o.acc_scale : 1.f) * k.o.acc_mul / (k.o.acc_div ? *k.o.acc_div : 1.f);
   for (int j = 0; j < 4; ++j) {
     const int col = n0 + tx * 4 + j;
     if (col >= k.o.yC) continue;

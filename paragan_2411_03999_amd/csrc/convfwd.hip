@@ -122,7 +122,7 @@ PG_DEV void conv_epilogue(const CfK& k, f32x16 (&acc)[TN][TM], bf16_t* lds, int 
   const int tid = wave * 64 + lane, lr = lane & 31, h = lane >> 5;
   constexpr int NQ = TN * 4;                   // 8-channel chunks per pixel
   const ConvOut& o = k.o;
-  const float accs = (o.acc_scale ? *o.acc_scale : 1.f) * o.acc_mul;
+  const float accs = (o.acc_scale ? *o.acc_scale : 1.f) * o.acc_mul / (o.acc_div ? *o.acc_div : 1.f);
   float* const stg = reinterpret_cast<float*>(lds) + wave * 32 * SROW;
   // the block's bias, past every wave's staging rows
   float* const bsh = reinterpret_cast<float*>(lds) + NW * 32 * SROW;

@@ -884,45 +884,60 @@ void shared_grad(hipStream_t st, const float* dcond, int dc, const int32_t* y, i
   PG_LAUNCH_CHECK();
 }
 
-// --------------------------------------------------- Adam
-// m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2;  p -= lr_t m / (sqrt(v c2) + eps)
+// --------------------------------------------------- optimisers
+// Adam:      m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2;  p -= lr_t m / (sqrt(v c2) + eps)
+// AdaBelief: m = b1 m + (1-b1) g;  s = b2 s + (1-b2) (g - m)^2 + eps;
+//            p -= lr_t m / (sqrt(s c2) + eps)
 // with lr_t = lr / (1 - b1^t) and c2 = 1 / (1 - b2^t) (bias corrections).
-// one element; four per thread through 16-byte accesses where aligned
-PG_DEV void adam1(float& p, float g, float& m, float& v, float b1, float b2, float lr_t, float c2, float eps) {
+// One element; four per thread through 16-byte accesses (28 bytes of HBM
+// traffic per parameter either way).
+template <int KIND>
+PG_DEV void optim1(float& p, float g, float& m, float& v, float b1, float b2, float lr_t, float c2, float eps) {
   m = b1 * m + (1.f - b1) * g;
-  v = b2 * v + (1.f - b2) * g * g;
+  if (KIND == 0) {
+    v = b2 * v + (1.f - b2) * g * g;
+  } else {
+    const float d = g - m;
+    v = b2 * v + (1.f - b2) * d * d + eps;
+  }
   p -= lr_t * m / (sqrtf(v * c2) + eps);
 }
-__global__ void k_adam(float* p, const float* g, float* m, float* v, int64_t n, float b1, float b2, float lr_t,
-                       float c2, float eps) {
+template <int KIND>
+__global__ void k_optim(float* p, const float* g, float* m, float* v, int64_t n, float b1, float b2, float lr_t,
+                        float c2, float eps) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t n4 = n >> 2;
   if (i < n4) {
     float4 pp = reinterpret_cast<float4*>(p)[i], mm = reinterpret_cast<float4*>(m)[i];
     float4 vv = reinterpret_cast<float4*>(v)[i];
     const float4 gg = reinterpret_cast<const float4*>(g)[i];
-    adam1(pp.x, gg.x, mm.x, vv.x, b1, b2, lr_t, c2, eps);
-    adam1(pp.y, gg.y, mm.y, vv.y, b1, b2, lr_t, c2, eps);
-    adam1(pp.z, gg.z, mm.z, vv.z, b1, b2, lr_t, c2, eps);
-    adam1(pp.w, gg.w, mm.w, vv.w, b1, b2, lr_t, c2, eps);
+    optim1<KIND>(pp.x, gg.x, mm.x, vv.x, b1, b2, lr_t, c2, eps);
+    optim1<KIND>(pp.y, gg.y, mm.y, vv.y, b1, b2, lr_t, c2, eps);
+    optim1<KIND>(pp.z, gg.z, mm.z, vv.z, b1, b2, lr_t, c2, eps);
+    optim1<KIND>(pp.w, gg.w, mm.w, vv.w, b1, b2, lr_t, c2, eps);
     reinterpret_cast<float4*>(p)[i] = pp;
     reinterpret_cast<float4*>(m)[i] = mm;
     reinterpret_cast<float4*>(v)[i] = vv;
   } else if (i < n4 + (n & 3)) {
     const int64_t j = 4 * n4 + (i - n4);
-    adam1(p[j], g[j], m[j], v[j], b1, b2, lr_t, c2, eps);
+    optim1<KIND>(p[j], g[j], m[j], v[j], b1, b2, lr_t, c2, eps);
   }
 }
 
-void adam(hipStream_t st, float* p, const float* g, float* m, float* v, int64_t n, float b1, float b2, float lr,
-          float eps, int64_t t) {
+void optim_step(hipStream_t st, int kind, float* p, const float* g, float* m, float* v, int64_t n, float b1,
+                float b2, float lr, float eps, int64_t t) {
   if (n <= 0) return;
-  PG_CHECK((((uintptr_t)p | (uintptr_t)g | (uintptr_t)m | (uintptr_t)v) & 15) == 0, "adam: 16-byte aligned buffers");
+  PG_CHECK((((uintptr_t)p | (uintptr_t)g | (uintptr_t)m | (uintptr_t)v) & 15) == 0,
+           "optimiser: 16-byte aligned buffers");
+  PG_CHECK(kind == 0 || kind == 1, "optimiser: unknown kind");
   const double lr_t = (double)lr / (1.0 - std::pow((double)b1, (double)t));
   const double c2 = 1.0 / (1.0 - std::pow((double)b2, (double)t));
   const int64_t threads = (n >> 2) + (n & 3);
-  hipLaunchKernelGGL(k_adam, dim3((unsigned)cdiv(threads, 256)), dim3(256), 0, st, p, g, m, v, n, b1, b2,
-                     (float)lr_t, (float)c2, eps);
+  const dim3 grid((unsigned)cdiv(threads, 256));
+  if (kind == 0)
+    hipLaunchKernelGGL(k_optim<0>, grid, dim3(256), 0, st, p, g, m, v, n, b1, b2, (float)lr_t, (float)c2, eps);
+  else
+    hipLaunchKernelGGL(k_optim<1>, grid, dim3(256), 0, st, p, g, m, v, n, b1, b2, (float)lr_t, (float)c2, eps);
   PG_LAUNCH_CHECK();
 }
 

@@ -43,7 +43,8 @@ void glin_bwd(hipStream_t st, const void* dh0, const float* z, int dz, int zc, i
 void shared_grad(hipStream_t st, const float* dcond, int dc, const int32_t* y, int B, int n_classes, int sd,
                  float* dshared);
 
-void adam(hipStream_t st, float* p, const float* g, float* m, float* v, int64_t n, float b1, float b2, float lr,
-          float eps, int64_t t);
+// One optimiser step t (>= 1) over n fp32 parameters: kind 0 Adam, 1 AdaBelief.
+void optim_step(hipStream_t st, int kind, float* p, const float* g, float* m, float* v, int64_t n, float b1,
+                float b2, float lr, float eps, int64_t t);
 
 }  // namespace pg

@@ -335,6 +335,29 @@ PG_DEV void ld4w(const float* W, int64_t row, int Cin, int c, bool wvec, float* 
   }
 }
 
+// A folded tap (a sum of up to four fp32 filter taps, times an optional
+// 1/sigma and 1/4) rounded once to the stored type: the sum is formed in
+// double, where it is exact, and rounded from there, so the stored value is
+// the correctly rounded folded tap.  bf16: round to nearest even at bit 45
+// of the double pattern (8 significant bits kept; a carry into the exponent
+// is the next power of two); below bf16's normal range (no filter tap of
+// these models) through fp32.
+template <typename T>
+PG_DEV float round_fold(double v);
+template <>
+PG_DEV float round_fold<float>(double v) {
+  return (float)v;
+}
+template <>
+PG_DEV float round_fold<bf16_t>(double v) {
+  unsigned long long b = (unsigned long long)__double_as_longlong(v);
+  const unsigned e = (unsigned)((b >> 52) & 0x7ff);
+  if (e == 0x7ff || e < 1023 - 126) return bf2f(f2bf((float)v));
+  b += ((1ull << 44) - 1) + ((b >> 45) & 1ull);
+  b &= ~((1ull << 45) - 1);
+  return (float)__longlong_as_double((long long)b);
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
   __shared__ float tile[64][65];
@@ -342,7 +365,9 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
   const PackJobK& J = g.j[i];
   const int lb = blockIdx.x - g.off[i];
   const int RR = J.R * J.R;
-  const float inv = 1.f / *J.sigma;
+  // a null sigma packs the filter unnormalised (the convolution then
+  // divides its accumulator by sigma)
+  const float inv = J.sigma ? 1.f / *J.sigma : 1.f;
   T* dst = (T*)J.dst;
   if (J.mode == kPackPool4) {
     // four consecutive channels of one (n, u, v) per thread
@@ -351,7 +376,7 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     const int t = e / J.Cp;     // n * 16 + u * 4 + v
     const int c = e - t * J.Cp;
     const int n = t >> 4, u = (t >> 2) & 3, v = t & 3;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
     if (n < J.Cout && c < J.Cin) {
 #pragma unroll
       for (int a = 0; a < 2; ++a)
@@ -362,13 +387,14 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
             float w4[4];
             ld4w(J.W, (int64_t)n * 9 + r * 3 + s_, J.Cin, c, J.wvec, w4);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) acc[q] += w4[q];
+            for (int q = 0; q < 4; ++q) acc[q] += (double)w4[q];
           }
         }
     }
+    float out[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[q] *= 0.25f * inv;
-    store4f<T>(dst + e, acc);
+    for (int q = 0; q < 4; ++q) out[q] = round_fold<T>(acc[q] * 0.25 * (double)inv);
+    store4f<T>(dst + e, out);
     return;
   }
   if (J.mode == kPackSub) {
@@ -381,18 +407,19 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
     const int p = pn / J.Np, n = pn - p * J.Np;
     const int a = p >> 1, b2 = p & 1;
     const int r0 = du ? 1 + a : 0, r1 = du ? 2 : a, s0 = dv ? 1 + b2 : 0, s1 = dv ? 2 : b2;
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    double acc[4] = {0.0, 0.0, 0.0, 0.0};
     if (n < J.Cout && c < J.Cin)
       for (int r = r0; r <= r1; ++r)
         for (int s_ = s0; s_ <= s1; ++s_) {
           float w4[4];
           ld4w(J.W, (int64_t)n * 9 + r * 3 + s_, J.Cin, c, J.wvec, w4);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) acc[q] += w4[q];
+          for (int q = 0; q < 4; ++q) acc[q] += (double)w4[q];
         }
+    float out[4];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) acc[q] *= inv;
-    store4f<T>(dst + e, acc);
+    for (int q = 0; q < 4; ++q) out[q] = round_fold<T>(acc[q] * (double)inv);
+    store4f<T>(dst + e, out);
     return;
   }
   if (J.mode == kPackFwd) {
@@ -432,7 +459,7 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int n = n0 + ty + 16 * k, cb = c0 + 4 * tx;
-    float val[4] = {0.f, 0.f, 0.f, 0.f};
+    double val[4] = {0.0, 0.0, 0.0, 0.0};
     if (n < J.Cout) {
       if (J.mode == kPackDgradSum4) {
         if (cb < J.Cin)
@@ -445,7 +472,7 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
                 float w4[4];
                 ld4w(J.W, (int64_t)n * 9 + r * 3 + s_, J.Cin, cb, J.wvec, w4);
 #pragma unroll
-                for (int q = 0; q < 4; ++q) val[q] += w4[q];
+                for (int q = 0; q < 4; ++q) val[q] += (double)w4[q];
               }
             }
       } else if (J.mode == kPackSubDgrad) {
@@ -457,7 +484,7 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
               float w4[4];
               ld4w(J.W, (int64_t)n * 9 + (2 - r) * 3 + (2 - s_), J.Cin, cb, J.wvec, w4);
 #pragma unroll
-              for (int q = 0; q < 4; ++q) val[q] += w4[q];
+              for (int q = 0; q < 4; ++q) val[q] += (double)w4[q];
             }
       } else {
         const int ftap = J.mode == kPackDgradRep4 ? 0 : (J.R - 1 - u) * J.R + (J.R - 1 - v);
@@ -472,8 +499,12 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
         }
       }
     }
+    // a single tap is an fp32 value already (times an fp32 1/sigma); a sum
+    // of taps is rounded once from its exact double value
+    const bool folded = J.mode == kPackDgradSum4 || J.mode == kPackSubDgrad;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) tile[ty + 16 * k][4 * tx + q] = val[q] * inv;
+    for (int q = 0; q < 4; ++q)
+      tile[ty + 16 * k][4 * tx + q] = folded ? round_fold<T>(val[q] * (double)inv) : (float)val[q] * inv;
   }
   __syncthreads();
 #pragma unroll

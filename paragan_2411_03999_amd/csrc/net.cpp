@@ -63,9 +63,11 @@ void check_arch(const paragan_biggan_desc* d) {
   PG_CHECK(d->dz >= d->n_g + 1 && d->dz % (d->n_g + 1) == 0, "biggan: dz must split into n_g + 1 equal chunks");
   for (int i = 0; i <= d->n_g; ++i) PG_CHECK(d->g_mult[i] >= 1, "biggan: g_mult entries must be >= 1");
   for (int j = 0; j < d->n_d; ++j) PG_CHECK(d->d_mult[j] >= 1, "biggan: d_mult entries must be >= 1");
-  PG_CHECK(d->n_power_iter >= 1 && d->bn_eps > 0 && d->sn_eps > 0 && d->adam_eps > 0, "biggan: bad eps / n_power_iter");
-  PG_CHECK(d->lr_g >= 0 && d->lr_d >= 0 && d->beta1 >= 0 && d->beta1 < 1 && d->beta2 >= 0 && d->beta2 < 1,
-           "biggan: bad optimiser settings");
+  PG_CHECK(d->n_power_iter >= 1 && d->bn_eps > 0 && d->sn_eps > 0, "biggan: bad eps / n_power_iter");
+  for (const paragan_optim* o : {&d->opt_g, &d->opt_d})
+    PG_CHECK((o->kind == PARAGAN_ADAM || o->kind == PARAGAN_ADABELIEF) && o->lr >= 0 && o->beta1 >= 0 &&
+                 o->beta1 < 1 && o->beta2 >= 0 && o->beta2 < 1 && o->eps > 0,
+             "biggan: bad optimiser settings (kind Adam or AdaBelief, lr >= 0, 0 <= beta < 1, eps > 0)");
   PG_CHECK((int64_t)2 * d->B * d->img * d->img < (1LL << 31), "biggan: batch too large");
   const Arch a = arch_from(d);
   int res = a.img;
@@ -510,74 +512,142 @@ size_t train_step_ws(const paragan_biggan_desc* d, int n_cu) {
   return w.off;
 }
 
+namespace {
+// The pieces of a training iteration over one workspace: the generator
+// (batch B), the discriminator on the 2B batch of a D step and on the B
+// images of a G step (their saved buffers share one region).
+struct StepRun {
+  Arch a;
+  int B;
+  hipStream_t st;
+  GNet g;
+  DNet d2, d1;
+  StepWs r;
+  Exec ex;
+  Layout LG, LD;
+  Params PG, PD;
+  int64_t pix;
+  StepRun(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D, void* ws)
+      : a(arch_from(d)), B(d->B), st(ctx->stream), g(a, B), d2(a, 2 * B), d1(a, B) {
+    Arena w(ws);
+    r = step_carve(a, B, w, g, d2, d1, ctx->n_cu);
+    ex = Exec{st, ctx->n_cu, r.net, r.net_bytes};
+    LG = g_layout(a);
+    LD = d_layout(a);
+    PG = Params{&LG, "", G ? G->params : nullptr, G ? G->u : nullptr, G ? G->grads : nullptr};
+    PD = Params{&LD, "", D ? D->params : nullptr, D ? D->u : nullptr, D ? D->grads : nullptr};
+    pix = (int64_t)a.img * a.img;
+  }
+  static void optimise(hipStream_t st, const paragan_optim& o, paragan_net_state* N, int64_t n) {
+    N->opt_t += 1;
+    optim_step(st, o.kind, N->params, N->grads, N->opt_m, N->opt_v, n, o.beta1, o.beta2, o.lr, o.eps, N->opt_t);
+  }
+  // D step on the batch already in r.ximg / r.ylab: forward, hinge (L_D to
+  // *loss), backward with weight gradients, D's optimiser
+  void d_update(const paragan_biggan_desc* d, paragan_net_state* D, float* loss) {
+    d2.fwd(ex, PD, r.ximg, r.ylab, r.logits);
+    hinge(st, r.logits, B, B, false, r.dout, loss);
+    d2.bwd(ex, PD, r.ylab, r.dout, nullptr, true);
+    optimise(st, d->opt_d, D, LD.n_params);
+  }
+  void stage_real(const float* x_real, const int32_t* y_real, const int32_t* y_fake) {
+    PG_HIP(hipMemcpyAsync(r.ximg, x_real, (size_t)B * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(r.ylab, y_real, (size_t)B * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(r.ylab + B, y_fake, (size_t)B * 4, hipMemcpyDeviceToDevice, st));
+  }
+  float* fake_half() { return r.ximg + (size_t)B * pix * 3; }
+  // G step: G forward, D forward (u updated), hinge (L_G to *loss), D input
+  // gradient, G backward, G's optimiser
+  void g_update(const paragan_biggan_desc* d, paragan_net_state* G, const float* z, const int32_t* y,
+                float* loss) {
+    g.fwd(ex, PG, z, y, r.ximg);
+    d1.fwd(ex, PD, r.ximg, y, r.logits);
+    hinge(st, r.logits, 0, B, true, r.dout, loss);
+    d1.bwd(ex, PD, y, r.dout, r.dimg, false);
+    g.bwd(ex, PG, z, y, r.dimg, 4);
+    optimise(st, d->opt_g, G, LG.n_params);
+  }
+  void losses_to_host(float* host, int n) {
+    PG_HIP(hipMemcpyAsync(host, r.dloss, (size_t)n * 4, hipMemcpyDeviceToHost, st));
+    PG_HIP(hipStreamSynchronize(st));
+  }
+};
+}  // namespace
+
+void g_sample(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, const float* z,
+              const int32_t* y, float* img, void* ws) {
+  StepRun R(ctx, d, G, nullptr, ws);
+  R.g.fwd(R.ex, R.PG, z, y, img, false);
+}
+
+void d_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* D, const float* x_real,
+            const int32_t* y_real, const float* x_fake, const int32_t* y_fake, void* ws, float* loss_host) {
+  StepRun R(ctx, d, nullptr, D, ws);
+  R.stage_real(x_real, y_real, y_fake);
+  PG_HIP(hipMemcpyAsync(R.fake_half(), x_fake, (size_t)R.B * R.pix * 3 * 4, hipMemcpyDeviceToDevice, R.st));
+  R.d_update(d, D, R.r.dloss);
+  R.losses_to_host(loss_host, 1);
+}
+
+void g_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
+            const float* z, const int32_t* y, void* ws, float* loss_host) {
+  StepRun R(ctx, d, G, D, ws);
+  R.g_update(d, G, z, y, R.r.dloss);
+  R.losses_to_host(loss_host, 1);
+}
+
 void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
                 const paragan_step_inputs* in, int n_D, void* ws, float* losses_host) {
-  const Arch a = arch_from(d);
-  const int B = d->B;
-  hipStream_t st = ctx->stream;
-  GNet g(a, B);
-  DNet d2(a, 2 * B), d1(a, B);
-  Arena w(ws);
-  StepWs r = step_carve(a, B, w, g, d2, d1, ctx->n_cu);
-  Exec ex{st, ctx->n_cu, r.net, r.net_bytes};
-  const Layout LG = g_layout(a), LD = d_layout(a);
-  Params PG{&LG, "", G->params, G->u, G->grads};
-  Params PD{&LD, "", D->params, D->u, D->grads};
-  const int64_t pix = (int64_t)a.img * a.img;
+  StepRun R(ctx, d, G, D, ws);
+  hipStream_t st = R.st;
   // The forwards' SN power iterations and weight packing (which read only
   // parameters) run on a second stream, each network's ahead of its forward
   // and behind the work that last used its packed weights or changed its
-  // parameters: D's behind the previous Adam step (overlapping G's forward),
-  // G's behind the previous G forward (overlapping D's forward and backward).
+  // parameters: D's behind the previous optimiser step (overlapping G's
+  // forward), G's behind the previous G forward (overlapping D's forward and
+  // backward).  The kernels are the same as on the one-stream path, so the
+  // results are too.
   if (!ctx->side) {
     PG_HIP(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking));
     for (hipEvent_t& e : ctx->ev) PG_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
   }
   hipStream_t sd = ctx->side;
-  hipEvent_t ev_main = ctx->ev[0], ev_main2 = ctx->ev[1], ev_g = ctx->ev[2], ev_d = ctx->ev[3];
-  auto side_after_main = [&](hipEvent_t e) {
-    PG_HIP(hipEventRecord(e, st));
-    PG_HIP(hipStreamWaitEvent(sd, e, 0));
-  };
-  auto main_after = [&](hipEvent_t e) { PG_HIP(hipStreamWaitEvent(st, e, 0)); };
-  side_after_main(ev_main2);
-  g.prep(sd, PG, r.side, n_D == 0);
-  PG_HIP(hipEventRecord(ev_g, sd));
-  for (int k = 0; k < n_D; ++k) {
-    side_after_main(ev_main);
-    d2.prep(sd, PD, r.side, true);
-    PG_HIP(hipEventRecord(ev_d, sd));
-    PG_HIP(hipMemcpyAsync(r.ximg, in->x_real[k], (size_t)B * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
-    PG_HIP(hipMemcpyAsync(r.ylab, in->y_real[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
-    PG_HIP(hipMemcpyAsync(r.ylab + B, in->y_fake[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
-    main_after(ev_g);
-    g.fwd(ex, PG, in->z_fake[k], in->y_fake[k], r.ximg + (size_t)B * pix * 3, false);
+  try {
+    hipEvent_t ev_main = ctx->ev[0], ev_main2 = ctx->ev[1], ev_g = ctx->ev[2], ev_d = ctx->ev[3];
+    auto side_after_main = [&](hipEvent_t e) {
+      PG_HIP(hipEventRecord(e, st));
+      PG_HIP(hipStreamWaitEvent(sd, e, 0));
+    };
+    auto main_after = [&](hipEvent_t e) { PG_HIP(hipStreamWaitEvent(st, e, 0)); };
     side_after_main(ev_main2);
-    g.prep(sd, PG, r.side, k == n_D - 1);   // for the next D step's or the G step's forward
+    R.g.prep(sd, R.PG, R.r.side, false);
     PG_HIP(hipEventRecord(ev_g, sd));
+    for (int k = 0; k < n_D; ++k) {
+      side_after_main(ev_main);
+      R.d2.prep(sd, R.PD, R.r.side, true);
+      PG_HIP(hipEventRecord(ev_d, sd));
+      R.stage_real(in->x_real[k], in->y_real[k], in->y_fake[k]);
+      main_after(ev_g);
+      R.g.fwd(R.ex, R.PG, in->z_fake[k], in->y_fake[k], R.fake_half(), false);
+      side_after_main(ev_main2);
+      R.g.prep(sd, R.PG, R.r.side, k == n_D - 1);   // for the next D step's or the G step's forward
+      PG_HIP(hipEventRecord(ev_g, sd));
+      main_after(ev_d);
+      R.d_update(d, D, R.r.dloss + k);
+    }
+    side_after_main(ev_main);
+    R.d1.prep(sd, R.PD, R.r.side, true);
+    PG_HIP(hipEventRecord(ev_d, sd));
+    main_after(ev_g);
     main_after(ev_d);
-    d2.fwd(ex, PD, r.ximg, r.ylab, r.logits);
-    hinge(st, r.logits, B, B, false, r.dout, r.dloss + k);
-    d2.bwd(ex, PD, r.ylab, r.dout, nullptr, true);
-    D->adam_t += 1;
-    adam(st, D->params, D->grads, D->adam_m, D->adam_v, LD.n_params, d->beta1, d->beta2, d->lr_d, d->adam_eps,
-         D->adam_t);
+    R.g_update(d, G, in->z_g, in->y_g, R.r.dloss + n_D);
+    R.losses_to_host(losses_host, n_D + 1);
+  } catch (...) {
+    // leave neither stream running on the caller's buffers
+    (void)hipStreamSynchronize(sd);
+    (void)hipStreamSynchronize(st);
+    throw;
   }
-  side_after_main(ev_main);
-  d1.prep(sd, PD, r.side, true);
-  PG_HIP(hipEventRecord(ev_d, sd));
-  main_after(ev_g);
-  g.fwd(ex, PG, in->z_g, in->y_g, r.ximg);
-  main_after(ev_d);
-  d1.fwd(ex, PD, r.ximg, in->y_g, r.logits);
-  hinge(st, r.logits, 0, B, true, r.dout, r.dloss + n_D);
-  d1.bwd(ex, PD, in->y_g, r.dout, r.dimg, false);
-  g.bwd(ex, PG, in->z_g, in->y_g, r.dimg, 4);
-  G->adam_t += 1;
-  adam(st, G->params, G->grads, G->adam_m, G->adam_v, LG.n_params, d->beta1, d->beta2, d->lr_g, d->adam_eps,
-       G->adam_t);
-  PG_HIP(hipMemcpyAsync(losses_host, r.dloss, (size_t)(n_D + 1) * 4, hipMemcpyDeviceToHost, st));
-  PG_HIP(hipStreamSynchronize(st));
 }
 
 }  // namespace pg

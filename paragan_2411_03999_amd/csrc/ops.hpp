@@ -38,8 +38,10 @@ struct ConvIn {
   int c_real = 0;                     // real input channels (0: = C); for FLOP counts
 };
 
-// Epilogue: v = (acc * (*acc_scale) + bias[n]) * (mask > 0) + res_scale * res,
+// Epilogue: v = (acc * (*acc_scale) * acc_mul / (*acc_div) + bias[n]) * (mask > 0)
+//              + res_scale * res,
 // optionally 2x2 average-pooled (the output rows are then the pooled pixels).
+// acc_div carries the spectral norm sigma of a filter packed unnormalised.
 struct ConvOut {
   void* y = nullptr;
   int y_f32 = 0;
@@ -48,6 +50,7 @@ struct ConvOut {
   const float* bias = nullptr;
   const float* acc_scale = nullptr;   // device scalar
   float acc_mul = 1.f;                // host scalar (also multiplies acc)
+  const float* acc_div = nullptr;     // device scalar dividing acc (sigma)
   int pool = 0;
   const void* res = nullptr;
   int res_f32 = 0, res_mode = R_NONE, resC = 0;

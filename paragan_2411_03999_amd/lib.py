@@ -14,6 +14,7 @@ LIB_PATH = os.path.join(_HERE, "libparagan.so")
 
 OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ENONFINITE = 0, -1, -2, -3, -4, -5
 F32, BF16 = 0, 1
+ADAM, ADABELIEF = 0, 1
 
 
 class ParaganError(RuntimeError):
@@ -50,18 +51,22 @@ class GoutDesc(C.Structure):
                 ("n_power_iter", C.c_int32), ("bn_eps", C.c_float), ("sn_eps", C.c_float)]
 
 
+class Optim(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("lr", C.c_float), ("beta1", C.c_float), ("beta2", C.c_float),
+                ("eps", C.c_float)]
+
+
 class BigganDesc(C.Structure):
     _fields_ = [("img", C.c_int32), ("ch", C.c_int32), ("n_g", C.c_int32), ("g_mult", C.c_int32 * 10),
                 ("n_d", C.c_int32), ("d_mult", C.c_int32 * 10), ("d_down", C.c_int32 * 10),
                 ("attn_res", C.c_int32), ("n_classes", C.c_int32), ("dz", C.c_int32),
                 ("shared_dim", C.c_int32), ("B", C.c_int32), ("n_power_iter", C.c_int32),
-                ("bn_eps", C.c_float), ("sn_eps", C.c_float), ("lr_g", C.c_float), ("lr_d", C.c_float),
-                ("beta1", C.c_float), ("beta2", C.c_float), ("adam_eps", C.c_float)]
+                ("bn_eps", C.c_float), ("sn_eps", C.c_float), ("opt_g", Optim), ("opt_d", Optim)]
 
 
 class NetState(C.Structure):
     _fields_ = [("params", C.c_void_p), ("u", C.c_void_p), ("grads", C.c_void_p),
-                ("adam_m", C.c_void_p), ("adam_v", C.c_void_p), ("adam_t", C.c_int64)]
+                ("opt_m", C.c_void_p), ("opt_v", C.c_void_p), ("opt_t", C.c_int64)]
 
 
 class StepInputs(C.Structure):
@@ -86,6 +91,7 @@ _SIGS = {
     "paragan_cpad": (C.c_int64, [C.c_int64]),
     "paragan_sn_ws_size": (C.c_int, [C.c_int64, C.c_int64, C.POINTER(C.c_size_t)]),
     "paragan_sn_power_iter": (C.c_int, [_P, _P, C.c_int64, C.c_int64, _P, _P, _P, C.c_int, C.c_float, _P]),
+    "paragan_sn_check": (C.c_int, [C.c_int64, C.c_int64, C.c_int, C.c_float]),
     "paragan_gblock_layout": (C.c_int, [_P, _P, C.c_int32, C.POINTER(C.c_int32), C.POINTER(C.c_int64),
                                         C.POINTER(C.c_int64)]),
     "paragan_gblock_sizes": (C.c_int, [_P, C.POINTER(C.c_size_t), C.POINTER(C.c_size_t)]),
@@ -115,6 +121,9 @@ _SIGS = {
     "paragan_biggan_check": (C.c_int, [_P]),
     "paragan_train_step_ws_size": (C.c_int, [_P, C.POINTER(C.c_size_t)]),
     "paragan_train_step": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, _P]),
+    "paragan_g_sample": (C.c_int, [_P, _P, _P, _P, _P, _P, _P]),
+    "paragan_d_step": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P]),
+    "paragan_g_step": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
 }
 
 _lib = None
@@ -327,6 +336,22 @@ def paragan_train_step(ctx, desc, G, D, inputs, n_D, ws, losses):
     """G, D: NetState; inputs: StepInputs; losses: ctypes float array (n_D+1)."""
     return load().paragan_train_step(ctx.h, C.byref(desc), C.byref(G), C.byref(D), C.byref(inputs), n_D,
                                      _ptr(ws), losses)
+
+
+def paragan_g_sample(ctx, desc, G, z, y, img, ws):
+    """G: NetState; z, y, img, ws: device tensors.  Returns the status."""
+    return load().paragan_g_sample(ctx.h, C.byref(desc), C.byref(G), _ptr(z), _ptr(y), _ptr(img), _ptr(ws))
+
+
+def paragan_d_step(ctx, desc, D, x_real, y_real, x_fake, y_fake, ws, loss):
+    """loss: ctypes float array (1).  Returns the status."""
+    return load().paragan_d_step(ctx.h, C.byref(desc), C.byref(D), _ptr(x_real), _ptr(y_real), _ptr(x_fake),
+                                 _ptr(y_fake), _ptr(ws), loss)
+
+
+def paragan_g_step(ctx, desc, G, D, z, y, ws, loss):
+    """loss: ctypes float array (1).  Returns the status."""
+    return load().paragan_g_step(ctx.h, C.byref(desc), C.byref(G), C.byref(D), _ptr(z), _ptr(y), _ptr(ws), loss)
 
 
 def paragan_profile(ctx, enable):

@@ -11,6 +11,8 @@ from oracle import biggan as O
 from oracle import blocks as OB
 from paragan_2411_03999_amd import lib
 
+from .parity import biggan_desc
+
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
@@ -34,6 +36,14 @@ def test_exports_every_declared_function(L):
     for n in names:
         assert hasattr(L, n), n
         assert n in lib.exported_symbols(), n
+
+
+def test_sn_validation(L):
+    assert L.paragan_sn_check(1536, 13824, 1, 1e-12) == lib.OK
+    assert L.paragan_sn_check(0, 4, 1, 1e-12) == lib.EINVAL
+    assert L.paragan_sn_check(4, 4, 0, 1e-12) == lib.EINVAL
+    assert L.paragan_sn_check(4, 4, 1, 0.0) == lib.EINVAL
+    assert L.paragan_sn_check(1 << 31, 4, 1, 1e-12) == lib.EINVAL
 
 
 def test_cpad():
@@ -85,16 +95,7 @@ def test_sizes_queries_need_no_gpu(L):
 
 
 def _desc(a, B=2):
-    d = lib.BigganDesc()
-    d.img, d.ch, d.n_g, d.n_d = a.img, a.ch, a.n_g, len(a.d_mult)
-    for i, m in enumerate(a.g_mult):
-        d.g_mult[i] = m
-    for j, (m, dn) in enumerate(zip(a.d_mult, a.d_down)):
-        d.d_mult[j], d.d_down[j] = m, dn
-    d.attn_res, d.n_classes, d.dz, d.shared_dim, d.B = a.attn_res, a.n_classes, a.dz, a.shared_dim, B
-    d.n_power_iter, d.bn_eps, d.sn_eps = 1, 1e-5, 1e-12
-    d.lr_g, d.lr_d, d.beta1, d.beta2, d.adam_eps = 1e-4, 4e-4, 0.0, 0.999, 1e-6
-    return d
+    return biggan_desc(a, B, O.HParams(opt_g=O.adabelief_g()))
 
 
 @pytest.mark.parametrize("arch", [O.biggan128, O.biggan512])
@@ -123,6 +124,11 @@ def test_biggan_validation(L):
     assert lib.paragan_biggan_check(d) == lib.EINVAL          # z does not split evenly
     d = _desc(a)
     assert lib.paragan_train_step_ws_size(d) > 0
+    for field, bad in (("kind", 2), ("lr", -1.0), ("beta1", 1.0), ("beta2", -0.1), ("eps", 0.0)):
+        for net in ("opt_g", "opt_d"):
+            d = _desc(a)
+            setattr(getattr(d, net), field, bad)
+            assert lib.paragan_biggan_check(d) == lib.EINVAL, (net, field)
 
 
 def test_gout_validation_and_layout(L):

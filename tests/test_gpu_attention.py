@@ -7,7 +7,7 @@ from oracle.numerics import bf16
 from paragan_2411_03999_amd import lib
 from paragan_2411_03999_amd.synth import Stream, init_params, init_u
 
-from .parity import Report, check, need_gpu
+from .parity import Report, check, need_gpu, context, harvest
 
 pytestmark = pytest.mark.gpu
 
@@ -32,7 +32,7 @@ def run_attn(B, H, W, C, seed, gamma=0.7, weights="gaussian"):
     ents, npar, nu = lib.paragan_attn_layout(d)
     assert [(e["name"], e["shape"]) for e in ents] == list(shapes.items())
     sb, wb = lib.paragan_attn_sizes(d)
-    ctx = lib.Context()
+    ctx = context()
     P = lib.flat_from_named(ents, npar, p)
     U = lib.u_from_named(ents, nu, u)
     X = lib.to_device_nhwc(x, lib.BF16)
@@ -43,6 +43,7 @@ def run_attn(B, H, W, C, seed, gamma=0.7, weights="gaussian"):
     G = torch.zeros(npar, dtype=torch.float32, device="cuda")
     lib.paragan_attn_bwd(ctx, d, P, X, saved, lib.to_device_nhwc(dy, lib.BF16), DX, G, ws)
     torch.cuda.synchronize()
+    harvest(ctx)
     rep = Report()
     check("y", lib.from_device_nhwc(Y, C), y_r, True, rep)
     # the attention contribution alone (y - x), a sharper view of the core

@@ -2,23 +2,49 @@
 
 Calls go through the C ABI (ctypes binding).  Inputs are seeded synthetic
 tensors; the oracle sees exactly the values the GPU sees (bf16 inputs are
-rounded before both).
+rounded before both).  bf16 gradients are held to the 2e-2 bar plus an
+element-wise bound on what ambiguous ReLU / rounding decisions can change,
+computed from the oracle alone (tests/bounds.py); elements away from every
+ambiguous decision get no slack.
 """
 import numpy as np
 import pytest
 
 from oracle import blocks as OB
-from oracle import layers as OL
 from oracle.numerics import bf16
 from paragan_2411_03999_amd import lib
 from paragan_2411_03999_amd.synth import Stream, init_params, init_u
 
-from .parity import TOL_BF16, Report, check, check_cancelling_sum, check_with_bound, need_gpu, norm_maxabs
+from .bounds import dblock_bounds, gblock_bounds
+from .parity import (Report, check, check_cancelling_sum, check_with_bound, context, harvest,
+                     need_gpu)
 
 pytestmark = pytest.mark.gpu
 
 
-def run_dblock(B, H, W, cin, cout, preact, down, lsc, dtype, seed, weights="orthogonal", want_dx=True):
+def worst_copy(dev_t, ref, copies, c):
+    """A GPU output over a batch of `copies` copies of the oracle's batch,
+    reduced to the oracle's shape: at every element the value of the copy
+    farthest from the oracle's (ref: the oracle's output for one copy;
+    dev_t: [copies * N, ..., >= c channels], channels past c ignored)."""
+    torch = need_gpu()
+    t = dev_t[..., :c].float().reshape((copies,) + ref.shape)
+    r = torch.from_numpy(np.ascontiguousarray(ref, dtype=np.float32)).cuda()
+    d = t - r
+    pick = d.abs().argmax(dim=0, keepdim=True)
+    return ref + torch.gather(d, 0, pick)[0].double().cpu().numpy()
+
+
+def tile_batch(a, copies):
+    return np.concatenate([a] * copies, axis=0) if copies > 1 else a
+
+
+def run_dblock(B, H, W, cin, cout, preact, down, lsc, dtype, seed, weights="orthogonal", want_dx=True,
+               copies=1):
+    """copies > 1: the GPU runs a batch of `copies` copies of the B images
+    (the launch configuration of copies * B images; no op couples the batch,
+    so every copy's outputs are the oracle's for the B images, and each
+    weight gradient is copies times the oracle's)."""
     torch = need_gpu()
     s = Stream(seed)
     shapes = OB.dblock_param_shapes(cin, cout, lsc)
@@ -31,59 +57,52 @@ def run_dblock(B, H, W, cin, cout, preact, down, lsc, dtype, seed, weights="orth
     Ho, Wo = (H // 2, W // 2) if down else (H, W)
     dy = R(s.normal((B, Ho, Wo, cout)))
     print("dblock case", dict(B=B, H=H, W=W, cin=cin, cout=cout, preact=preact, down=down, lsc=lsc,
-                              dtype=dtype, seed=seed), flush=True)
+                              dtype=dtype, seed=seed, copies=copies), flush=True)
     # oracle
     cfg = OB.BlockCfg(bf16=is_bf)
     y_r, u_r, cache = OB.dblock_fwd(x, p, u, cfg, preact, down, lsc)
     dx_r, g_r = OB.dblock_bwd(dy, cache, cfg, preact, down, lsc)
+    bnd, info = dblock_bounds(cache, dy, down, preact) if is_bf else ({}, {"counts": {}})
     # GPU
-    d = lib.DBlockDesc(B, H, W, cin, cout, int(preact), int(down), int(lsc), dtype, 1, 1e-12)
+    Bg = B * copies
+    d = lib.DBlockDesc(Bg, H, W, cin, cout, int(preact), int(down), int(lsc), dtype, 1, 1e-12)
     ents, npar, nu = lib.paragan_dblock_layout(d)
     assert [e["name"] for e in ents] == list(shapes)
     saved_b, ws_b = lib.paragan_dblock_sizes(d)
-    ctx = lib.Context()
+    ctx = context()
     P = lib.flat_from_named(ents, npar, p)
     U = lib.u_from_named(ents, nu, u)
-    X = lib.to_device_nhwc(x, dtype)
-    Y = lib.empty_nhwc(B, Ho, Wo, cout, dtype)
+    X = lib.to_device_nhwc(tile_batch(x, copies), dtype)
+    Y = lib.empty_nhwc(Bg, Ho, Wo, cout, dtype)
     saved = lib.workspace(saved_b)
     ws = lib.workspace(ws_b)
     lib.paragan_dblock_fwd(ctx, d, P, U, X, Y, saved, ws)
-    DY = lib.to_device_nhwc(dy, dtype)
-    DX = lib.empty_nhwc(B, H, W, cin, dtype) if want_dx else None
+    DY = lib.to_device_nhwc(tile_batch(dy, copies), dtype)
+    DX = lib.empty_nhwc(Bg, H, W, cin, dtype) if want_dx else None
     G = torch.zeros(npar, dtype=torch.float32, device="cuda")
     lib.paragan_dblock_bwd(ctx, d, P, X, saved, DY, DX, G, ws)
     torch.cuda.synchronize()
+    harvest(ctx)
     rep = Report()
-    check("y", lib.from_device_nhwc(Y, cout), y_r, is_bf, rep)
+    rep.err.update(info["counts"])
+    check("y", worst_copy(Y, y_r, copies, cout), y_r, is_bf, rep)
     gu = lib.named_u_from_flat(ents, U)
     for k in keys:
         check("u." + k, gu[k], u_r[k], False, rep)
     gg = lib.named_from_flat(ents, G)
-    # dh = (conv2^T dc2) * [h > 0]: where |h| is within fp32 summation error
-    # of zero the two sides may disagree on the mask; bound what that moves
-    b_dh = dblock_mask_bound(cache, dy, down)
     for k in shapes:
-        if k == "conv1.w":
-            bw = OL.conv2d_wgrad(b_dh, np.abs(cache["a0"]), 3)
-            check_with_bound("grad." + k, gg[k], g_r[k], np.abs(bw) / cache["st"]["conv1.w"][2],
-                             is_bf, rep)
+        if is_bf and k in bnd:
+            check_with_bound("grad." + k, gg[k], copies * g_r[k], copies * bnd[k], True, rep)
         else:
-            check("grad." + k, gg[k], g_r[k], is_bf, rep)
+            check("grad." + k, gg[k], copies * g_r[k], is_bf, rep)
     if want_dx:
-        bdx = OL.conv2d_dgrad(b_dh, np.abs(cache["w1"]))
-        check_with_bound("dx", lib.from_device_nhwc(DX, cin), dx_r, bdx, is_bf, rep)
+        got = worst_copy(DX, dx_r, copies, cin)
+        if is_bf:
+            check_with_bound("dx", got, dx_r, bnd["dx"], True, rep)
+        else:
+            check("dx", got, dx_r, False, rep)
     rep.done()
     return rep
-
-
-def dblock_mask_bound(cache, dy, down):
-    """|change of dh| allowed by ReLU-mask ambiguity of h, elementwise."""
-    dc2 = OL.avgpool2_bwd(dy) if down else dy
-    da = OL.conv2d_dgrad(dc2, cache["w2"])
-    absum = OL.conv2d(np.abs(cache["a0"]), np.abs(cache["w1"]))     # sum |a w|
-    ambiguous = np.abs(cache["h"]) <= 2.0 ** -16 * absum
-    return np.where(ambiguous, np.abs(da), 0.0)
 
 
 @pytest.mark.parametrize("preact,down,lsc", [(True, True, True), (False, True, True),
@@ -112,7 +131,11 @@ def test_dblock_config2_full():
 
 
 # ----------------------------------------------------------------- G block
-def run_gblock(B, H, W, cin, cout, dc, dtype, seed, weights="orthogonal", n_classes=None):
+def run_gblock(B, H, W, cin, cout, dc, dtype, seed, weights="orthogonal", n_classes=None, copies=1):
+    """copies > 1: the GPU runs a batch of `copies` copies of the B samples.
+    Batch statistics of copies equal those of the B samples, so every copy's
+    outputs are the oracle's for the B samples and each weight gradient is
+    copies times the oracle's."""
     torch = need_gpu()
     s = Stream(seed)
     shapes = OB.gblock_param_shapes(cin, cout, dc)
@@ -128,82 +151,68 @@ def run_gblock(B, H, W, cin, cout, dc, dtype, seed, weights="orthogonal", n_clas
         cond = s.normal((B, dc))
     cond = cond.astype(np.float32).astype(np.float64)
     dy = R(s.normal((B, 2 * H, 2 * W, cout)))
-    print("gblock case", dict(B=B, H=H, W=W, cin=cin, cout=cout, dc=dc, dtype=dtype, seed=seed), flush=True)
+    print("gblock case", dict(B=B, H=H, W=W, cin=cin, cout=cout, dc=dc, dtype=dtype, seed=seed, copies=copies),
+          flush=True)
     cfg = OB.BlockCfg(bf16=is_bf)
     y_r, u_r, cache = OB.gblock_fwd(x, cond, p, u, cfg)
     dx_r, dc_r, g_r = OB.gblock_bwd(dy, cache, cfg)
-    sens = conv1_rounding_sensitivity(x, cond, p, u, dy, cfg, g_r, dx_r, dc_r, seed) if is_bf else {}
-    d = lib.GBlockDesc(B, H, W, cin, cout, dc, dtype, 1, 1e-5, 1e-12)
+    Bg = B * copies
+    d = lib.GBlockDesc(Bg, H, W, cin, cout, dc, dtype, 1, 1e-5, 1e-12)
     ents, npar, nu = lib.paragan_gblock_layout(d)
     assert [e["name"] for e in ents] == list(shapes)
     saved_b, ws_b = lib.paragan_gblock_sizes(d)
-    ctx = lib.Context()
+    ctx = context()
     P = lib.flat_from_named(ents, npar, p)
     U = lib.u_from_named(ents, nu, u)
-    X = lib.to_device_nhwc(x, dtype)
-    COND = torch.from_numpy(cond.astype(np.float32)).cuda()
-    Y = lib.empty_nhwc(B, 2 * H, 2 * W, cout, dtype)
+    X = lib.to_device_nhwc(tile_batch(x, copies), dtype)
+    COND = torch.from_numpy(tile_batch(cond, copies).astype(np.float32)).cuda()
+    Y = lib.empty_nhwc(Bg, 2 * H, 2 * W, cout, dtype)
     saved = lib.workspace(saved_b)
     ws = lib.workspace(ws_b)
     lib.paragan_gblock_fwd(ctx, d, P, U, X, COND, Y, saved, ws)
-    DY = lib.to_device_nhwc(dy, dtype)
-    DX = lib.empty_nhwc(B, H, W, cin, dtype)
-    DC = torch.zeros((B, dc), dtype=torch.float32, device="cuda")
+    DY = lib.to_device_nhwc(tile_batch(dy, copies), dtype)
+    DX = lib.empty_nhwc(Bg, H, W, cin, dtype)
+    DC = torch.zeros((Bg, dc), dtype=torch.float32, device="cuda")
     G = torch.zeros(npar, dtype=torch.float32, device="cuda")
     lib.paragan_gblock_bwd(ctx, d, P, X, COND, saved, DY, DX, DC, G, ws)
     torch.cuda.synchronize()
+    harvest(ctx)
     rep = Report()
-    check("y", lib.from_device_nhwc(Y, cout), y_r, is_bf, rep)
+    check("y", worst_copy(Y, y_r, copies, cout), y_r, is_bf, rep)
     gu = lib.named_u_from_flat(ents, U)
     for k in OB.GBLOCK_SN:
         check("u." + k, gu[k], u_r[k], False, rep)
     gg = lib.named_from_flat(ents, G)
-
-    def chk(name, got, ref):
-        if name in sens:
-            # bf16: conv1 runs as sub-pixel 2x2 filters whose taps sum 3x3
-            # taps and round once; cBN2's ReLU masks near zero may flip
-            assert np.all(np.isfinite(got)), name
-            rep.add(name, norm_maxabs(got, ref), max(TOL_BF16, 3 * sens[name]))
-            rep.err[name + ".sens"] = sens[name]
-        else:
-            check(name, got, ref, is_bf, rep)
-
+    bnd = {}
+    if is_bf:
+        bnd, info = gblock_bounds(p, cache, dy)
+        rep.err.update(info["counts"])
+    dh1 = cache_dh1(cache, dy, cfg)
     for k in shapes:
         if k == "conv1.b":
             # conv1's bias feeds a batch-statistics BN: its gradient is
             # identically zero and both sides return summation noise
-            l1 = np.abs(cache_dh1(cache, dy, cfg)).sum(axis=(0, 1, 2))
-            check_cancelling_sum("grad." + k, gg[k], g_r[k], l1, is_bf, rep)
+            l1 = np.abs(dh1).sum(axis=(0, 1, 2)) + (bnd["conv1.b_l1"] if is_bf else 0.0)
+            check_cancelling_sum("grad." + k, gg[k], copies * g_r[k], copies * l1, is_bf, rep)
+        elif k in bnd:
+            check_with_bound("grad." + k, gg[k], copies * g_r[k], copies * bnd[k], True, rep)
         else:
-            chk("grad." + k, gg[k], g_r[k])
-    chk("dx", lib.from_device_nhwc(DX, cin), dx_r)
-    chk("dcond", DC.cpu().numpy(), dc_r)
+            check("grad." + k, gg[k], copies * g_r[k], is_bf, rep)
+    for name, got, ref in (("dx", worst_copy(DX, dx_r, copies, cin), dx_r),
+                           ("dcond", worst_copy(DC, dc_r, copies, dc), dc_r)):
+        if is_bf:
+            check_with_bound(name, got, ref, bnd[name], True, rep)
+        else:
+            check(name, got, ref, False, rep)
     rep.done()
     return rep
-
-
-def conv1_rounding_sensitivity(x, cond, p, u, dy, cfg, g_r, dx_r, dc_r, seed):
-    """The oracle's own movement (max-abs metric) when conv1's filter moves
-    by the rounding of the GPU's sub-pixel form: each 2x2 sub-pixel tap sums
-    up to four 3x3 taps and is rounded to bf16 once (relative error up to
-    2^-8); moving each 3x3 tap by a relative uniform +-2^-7 covers that."""
-    rng = np.random.default_rng(seed)
-    p2 = dict(p)
-    p2["conv1.w"] = p["conv1.w"] * (1 + 2.0 ** -7 * rng.uniform(-1, 1, p["conv1.w"].shape))
-    _, _, cache2 = OB.gblock_fwd(x, cond, p2, u, cfg)
-    dx2, dc2, g2 = OB.gblock_bwd(dy, cache2, cfg)
-    out = {"grad." + k: norm_maxabs(g2[k], g_r[k]) for k in g_r}
-    out["dx"] = norm_maxabs(dx2, dx_r)
-    out["dcond"] = norm_maxabs(dc2, dc_r)
-    return out
 
 
 def cache_dh1(cache, dy, cfg):
     """The oracle's gradient at conv1's output (the terms of conv1.b's sum)."""
     from oracle import layers as L
     from oracle.numerics import rounder
-    da2 = L.conv2d_dgrad(dy, cache["w2"])
+    da2 = L.conv2d_dgrad(dy, cache["w2"]) / cache["s2"]
     dh1, _, _ = L.cbn_bwd(da2 * (cache["bn2"] > 0), cache["c2"])
     return rounder(cfg.bf16)(dh1)
 
@@ -227,12 +236,50 @@ def test_gblock_bf16_wide():
     run_gblock(B=2, H=4, W=4, cin=384, cout=192, dc=148, dtype=lib.BF16, seed=105)
 
 
-def test_gblock_biggan128_last_block():
-    """BigGAN-128's last G block, 192 -> 96 channels, 64x64 -> 128x128, bf16,
-    batch 2: the 96-channel kernels of the full model (its conv1 as four
-    sub-pixel convs over the 64x64 source, conv2 a 3x3 conv over four-row
-    tiles of the 128-wide image) at their real image shapes."""
-    run_gblock(B=2, H=64, W=64, cin=192, cout=96, dc=148, dtype=lib.BF16, seed=106)
+# --------------------------------------------- BigGAN-128's own block shapes
+# (Evaluation, "Experiment Setup": ch = 96, G multipliers 16,16,8,4,2,1, D
+# multipliers 1,2,4,8,16,16; conditioning c = 128-d shared embedding + 20-d
+# z chunk.)  Batches are smaller than the train step's, sized so the oracle
+# finishes in seconds.
+@pytest.mark.parametrize("blk,B", [(0, 8), (1, 4), (2, 4), (3, 2), (4, 2)])
+def test_gblock_biggan128(blk, B):
+    mult = (16, 16, 8, 4, 2, 1)
+    res = 4 << blk
+    run_gblock(B=B, H=res, W=res, cin=96 * mult[blk], cout=96 * mult[blk + 1], dc=148, dtype=lib.BF16,
+               seed=120 + blk, weights="gaussian")
+
+
+@pytest.mark.parametrize("blk,B", [(1, 2), (2, 8), (3, 8), (4, 8), (5, 16)])
+def test_dblock_biggan128(blk, B):
+    mult = (1, 2, 4, 8, 16, 16)
+    res = 128 >> blk
+    down = blk < 5
+    run_dblock(B=B, H=res, W=res, cin=96 * mult[blk - 1], cout=96 * mult[blk], preact=True, down=down,
+               lsc=down, dtype=lib.BF16, seed=130 + blk, weights="gaussian")
+
+
+# ---------------- BigGAN-128's blocks in the benchmark's launch configuration
+# The train step at batch 256 runs the generator blocks on 256 samples and
+# the discriminator blocks on 512 (a D step's real + fake) and 256 (the G
+# step's fakes).  Kernel tiles are chosen from the GEMM shapes, which depend
+# on the batch, not on the data: a batch of copies of two samples takes the
+# benchmark's exact kernel instances and launch grids, and the oracle needs
+# only the two samples.
+@pytest.mark.parametrize("blk", [0, 1, 2, 3, 4])
+def test_gblock_biggan128_benchmark_batch(blk):
+    mult = (16, 16, 8, 4, 2, 1)
+    res = 4 << blk
+    run_gblock(B=2, H=res, W=res, cin=96 * mult[blk], cout=96 * mult[blk + 1], dc=148, dtype=lib.BF16,
+               seed=140 + blk, weights="gaussian", copies=128)
+
+
+@pytest.mark.parametrize("blk,n", [(b, n) for b in (1, 2, 3, 4, 5) for n in (512, 256)])
+def test_dblock_biggan128_benchmark_batch(blk, n):
+    mult = (1, 2, 4, 8, 16, 16)
+    res = 128 >> blk
+    down = blk < 5
+    run_dblock(B=2, H=res, W=res, cin=96 * mult[blk - 1], cout=96 * mult[blk], preact=True, down=down,
+               lsc=down, dtype=lib.BF16, seed=150 + blk, weights="gaussian", copies=n // 2)
 
 
 def test_dblock_biggan128_first_resolution():
@@ -242,14 +289,6 @@ def test_dblock_biggan128_first_resolution():
     block after its image layer."""
     run_dblock(B=2, H=128, W=128, cin=96, cout=96, preact=True, down=True, lsc=True, dtype=lib.BF16,
                seed=107)
-
-
-def test_dblock_biggan128_second_resolution():
-    """BigGAN-128's second D block, 96 -> 192 channels, 64x64 -> 32x32, bf16,
-    batch 2: its stride-2 conv2 with 192 output channels over four-row tiles
-    of the 32-wide output."""
-    run_dblock(B=2, H=64, W=64, cin=96, cout=192, preact=True, down=True, lsc=True, dtype=lib.BF16,
-               seed=108)
 
 
 def test_dblock_deep_resolution_768():

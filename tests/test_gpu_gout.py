@@ -11,7 +11,7 @@ from oracle.numerics import bf16
 from paragan_2411_03999_amd import lib
 from paragan_2411_03999_amd.synth import Stream, init_params, init_u
 
-from .parity import Report, check, need_gpu, norm_maxabs
+from .parity import Report, check, need_gpu, norm_maxabs, context, harvest
 
 pytestmark = pytest.mark.gpu
 
@@ -40,7 +40,7 @@ def run_gout(B, H, W, C, seed):
     ents, npar, nu = lib.paragan_gout_layout(d)
     assert [(e["name"], tuple(e["shape"])) for e in ents] == list(shapes.items())
     sb, wb = lib.paragan_gout_sizes(d)
-    ctx = lib.Context()
+    ctx = context()
     P = lib.flat_from_named(ents, npar, p)
     U = lib.u_from_named(ents, nu, u)
     X = lib.to_device_nhwc(x, lib.BF16)
@@ -52,6 +52,7 @@ def run_gout(B, H, W, C, seed):
     DIMG = torch.from_numpy(dimg.astype(np.float32)).cuda()
     lib.paragan_gout_bwd(ctx, d, P, X, IMG, saved, DIMG, DX, G, ws)
     torch.cuda.synchronize()
+    harvest(ctx)
 
     rep = Report()
     check("img", IMG.cpu().numpy().astype(np.float64), img_r, False, rep)

@@ -1,5 +1,26 @@
-"""GPU parity: the full G+D train step (n_D discriminator steps, one
-generator step, hinge loss, Adam) on a small BigGAN vs the oracle."""
+"""GPU parity: the BigGAN training iteration (Numerical Optimizations: n_D
+discriminator steps per generator step; hinge loss; AdaBelief for G and Adam
+for D) against the oracle.
+
+Each piece is checked on its own, from the same state on both sides (the
+GPU is given the oracle's state; nothing flows the other way): the generator
+forward (paragan_g_sample), the discriminator step on given images
+(paragan_d_step, the config of a D step with 32 real + 32 fake images), and
+the generator step (paragan_g_step).  The fused iteration is then pinned to
+the pieces bit for bit on the GPU, and is deterministic.  The optimiser
+updates are checked from a smooth optimiser state (t > 1, moments set), where
+the step is a smooth function of the gradient.
+
+Bars.  Inside a network every block's input already carries the rounding of
+the blocks before it, so its ReLU, max-pool and hinge decisions near a tie
+come out differently far more often than at a block's exact inputs (where
+the block tests hold every element to 2e-2 plus a bound on exactly those
+flips, at every BigGAN-128 block shape and launch configuration).  A deep
+network is therefore held, module by module (a residual block, the
+attention block, each head), to a relative L2 error of its whole gradient and
+update of at most 2e-2; the per-tensor max-abs errors are reported.  The
+minimal network (one block each) is held element-wise, tensor by tensor.
+"""
 import ctypes as C
 
 import numpy as np
@@ -9,7 +30,7 @@ from oracle import biggan as O
 from paragan_2411_03999_amd import lib
 from paragan_2411_03999_amd.synth import Stream, init_params, init_u
 
-from .parity import TOL_BF16, Report, check, need_gpu, norm_maxabs
+from .parity import TOL_BF16, Report, biggan_desc, check, context, harvest, need_gpu, norm_maxabs
 
 pytestmark = pytest.mark.gpu
 
@@ -21,18 +42,16 @@ def small_arch():
                   attn_res=16, n_classes=10, dz=20, shared_dim=16)
 
 
-def desc_of(a, B, hp):
-    d = lib.BigganDesc()
-    d.img, d.ch, d.n_g, d.n_d = a.img, a.ch, a.n_g, len(a.d_mult)
-    for i, m in enumerate(a.g_mult):
-        d.g_mult[i] = m
-    for j, (m, dn) in enumerate(zip(a.d_mult, a.d_down)):
-        d.d_mult[j], d.d_down[j] = m, dn
-    d.attn_res, d.n_classes, d.dz, d.shared_dim, d.B = a.attn_res, a.n_classes, a.dz, a.shared_dim, B
-    d.n_power_iter = hp.n_power_iter
-    d.bn_eps, d.sn_eps, d.lr_g, d.lr_d = hp.bn_eps, hp.sn_eps, hp.lr_g, hp.lr_d
-    d.beta1, d.beta2, d.adam_eps = hp.beta1, hp.beta2, hp.adam_eps
-    return d
+def minimal_arch():
+    # one G block (4 -> 8), one pooling D block (8 -> 4), no attention
+    return O.Arch(img=8, ch=16, g_mult=(2, 1), d_mult=(2,), d_down=(1,), attn_res=0, n_classes=5, dz=8,
+                  shared_dim=8)
+
+
+def hparams():
+    """The paper's policy: AdaBelief for the generator, Adam for the
+    discriminator (Numerical Optimizations, "Asymmetric Optimization Policy")."""
+    return O.HParams(opt_g=O.adabelief_g(), opt_d=O.adam_d())
 
 
 def f32(d):
@@ -40,191 +59,382 @@ def f32(d):
 
 
 class NetDev:
-    """Device buffers of one network (params, u, grads, Adam state)."""
+    """Device state of one network (params, u, grads, optimiser moments)."""
 
-    def __init__(self, torch, ents, npar, nu, p, u):
+    def __init__(self, torch, ents, npar, nu, p, u, opt=None):
         self.ents = ents
         self.P = lib.flat_from_named(ents, npar, p)
         self.U = lib.u_from_named(ents, nu, u)
         self.G = torch.zeros(npar, dtype=torch.float32, device="cuda")
-        self.M = torch.zeros(npar, dtype=torch.float32, device="cuda")
-        self.V = torch.zeros(npar, dtype=torch.float32, device="cuda")
+        if opt is None:
+            self.M = torch.zeros(npar, dtype=torch.float32, device="cuda")
+            self.V = torch.zeros(npar, dtype=torch.float32, device="cuda")
+            t = 0
+        else:
+            self.M = lib.flat_from_named(ents, npar, opt.m)
+            self.V = lib.flat_from_named(ents, npar, opt.v)
+            t = opt.t
         self.state = lib.NetState(self.P.data_ptr(), self.U.data_ptr(), self.G.data_ptr(), self.M.data_ptr(),
-                                  self.V.data_ptr(), 0)
+                                  self.V.data_ptr(), t)
+
+    def clone(self, torch):
+        c = object.__new__(NetDev)
+        c.ents = self.ents
+        c.P, c.U, c.G, c.M, c.V = (t.clone() for t in (self.P, self.U, self.G, self.M, self.V))
+        c.state = lib.NetState(c.P.data_ptr(), c.U.data_ptr(), c.G.data_ptr(), c.M.data_ptr(), c.V.data_ptr(),
+                               self.state.opt_t)
+        return c
+
+    def tensors(self):
+        return (self.P, self.U, self.G, self.M, self.V)
 
 
-def make_inputs(torch, s, a, B, n_D):
-    xs, yrs, zs, yfs = [], [], [], []
-    for _ in range(n_D):
-        xs.append(s.uniform((B, a.img, a.img, 3)).astype(np.float32))
-        yrs.append(s.labels(B, a.n_classes))
-        zs.append(s.normal((B, a.dz)).astype(np.float32))
-        yfs.append(s.labels(B, a.n_classes))
-    zg = s.normal((B, a.dz)).astype(np.float32)
-    yg = s.labels(B, a.n_classes)
-    dev = lambda v: torch.from_numpy(np.ascontiguousarray(v)).cuda()
-    keep = [dev(v) for v in xs + yrs + zs + yfs] + [dev(zg), dev(yg)]
-    ptrs = [t.data_ptr() for t in keep]
-    arr = lambda lst: (C.c_void_p * n_D)(*lst)
-    inp = lib.StepInputs(arr(ptrs[0:n_D]), arr(ptrs[n_D:2 * n_D]), arr(ptrs[2 * n_D:3 * n_D]),
-                         arr(ptrs[3 * n_D:4 * n_D]), ptrs[4 * n_D], ptrs[4 * n_D + 1])
-    d_in = [(x.astype(np.float64), yr, z.astype(np.float64), yf) for x, yr, z, yf in zip(xs, yrs, zs, yfs)]
-    g_in = (zg.astype(np.float64), yg)
-    return inp, keep, d_in, g_in
-
-
-def check_adam_step(name, p_new, p_old, g_ref, p_new_ref, lr, rep):
-    """Sign-aware check of one Adam step (beta1 = 0, t = 1: the step is
-    lr * g / (|g| + eps), nearly lr * sign(g)).  Where the oracle's gradient
-    is large enough that the bf16-path gradient tolerance cannot flip its
-    sign, the step must match; elsewhere it must stay within one step."""
-    d_gpu = p_new - p_old
-    d_ref = p_new_ref - p_old
-    g = np.abs(g_ref)
-    firm = g >= 5 * TOL_BF16 * g.max() if g.size else g
-    e = np.abs(d_gpu - d_ref)[firm].max() / lr if firm.any() else 0.0
-    rep.add("step." + name, e, 2e-2)
-    over = np.abs(d_gpu).max() / lr if d_gpu.size else 0.0
-    rep.add("step_bound." + name, over - 1.0, 1e-3)
-
-
-def zero_by_bn(a, name):
-    """Biases whose gradient is identically zero: each feeds only a batch-
-    statistics BN (conv1 -> bn2 in every G block; the last G block's
-    conv2 / skip -> the output BN).  Both sides return rounding noise."""
-    last = "g%d." % (a.n_g - 1)
-    return name.endswith("conv1.b") and name.startswith("g") or name in (last + "conv2.b", last + "sc.b")
-
-
-def rel_l2(g, r):
-    return float(np.linalg.norm(np.asarray(g) - np.asarray(r)) / max(np.linalg.norm(np.asarray(r)), 1e-30))
-
-
-def folded_filters_perturbed(a, gp, dp, seed):
-    """The weights with every filter the GPU folds before rounding moved by
-    that rounding.  The folded filters are each pooling D block's conv2 (the
-    2x2 average folded in: a stride-2 4x4 filter) and each G block's conv1
-    (the nearest upsample folded in: four 2x2 sub-pixel filters).  Each
-    folded tap sums up to four 3x3 taps and is rounded to bf16 once (relative
-    error up to 2^-8, bf16 having 8 significant bits), where the definition
-    rounds the 3x3 filter; moving each 3x3 tap by a relative uniform +-2^-7
-    gives the folded taps at least that spread."""
-    rng = np.random.default_rng(seed)
-    g2, d2 = dict(gp), dict(dp)
-    for j, down in enumerate(a.d_down):
-        if down:
-            w = dp["d%d.conv2.w" % j]
-            d2["d%d.conv2.w" % j] = w * (1 + 2.0 ** -7 * rng.uniform(-1, 1, w.shape))
-    for i in range(a.n_g):
-        w = gp["g%d.conv1.w" % i]
-        g2["g%d.conv1.w" % i] = w * (1 + 2.0 ** -7 * rng.uniform(-1, 1, w.shape))
-    return g2, d2
-
-
-def run_step(a, B, n_D, seed, calibrated):
-    torch = need_gpu()
-    hp = O.HParams()
+def make_nets(torch, a, B, seed, hp, smooth_opt=False):
+    """Seeded parameters (f32-representable) on both sides; with smooth_opt
+    the optimiser state is a seeded t = 7 history on both sides."""
     s = Stream(seed)
     glay, gsn = O.g_layout(a)
     dlay, dsn = O.d_layout(a)
-    gp, gu = f32(init_params(glay, s)), f32(init_u(glay, gsn, s))
-    dp, du = f32(init_params(dlay, s)), f32(init_u(dlay, dsn, s))
-    d = desc_of(a, B, hp)
+    gp, gu = f32(init_params(glay, s, weights="gaussian")), f32(init_u(glay, gsn, s))
+    dp, du = f32(init_params(dlay, s, weights="gaussian")), f32(init_u(dlay, dsn, s))
+    optG, optD = O.opt_init(gp), O.opt_init(dp)
+    if smooth_opt:
+        for opt, lay in ((optG, glay), (optD, dlay)):
+            opt.t = 7
+            for k, shp in lay.items():
+                opt.m[k] = f32({k: 1e-3 * s.normal(shp)})[k]
+                opt.v[k] = f32({k: 1e-6 * (1.0 + s.uniform(shp, 0.0, 1.0))})[k]
+    d = biggan_desc(a, B, hp)
     assert lib.paragan_biggan_check(d) == lib.OK
     gents, gn, gnu = lib.paragan_net_layout(d, 0)
     dents, dn, dnu = lib.paragan_net_layout(d, 1)
     assert [(e["name"], e["shape"]) for e in gents] == list(glay.items())
     assert [(e["name"], e["shape"]) for e in dents] == list(dlay.items())
-    ctx = lib.Context()
-    G = NetDev(torch, gents, gn, gnu, gp, gu)
-    D = NetDev(torch, dents, dn, dnu, dp, du)
-    inp, keep, d_in, g_in = make_inputs(torch, s, a, B, n_D)
+    G = NetDev(torch, gents, gn, gnu, gp, gu, optG if smooth_opt else None)
+    D = NetDev(torch, dents, dn, dnu, dp, du, optD if smooth_opt else None)
+    return d, s, (gp, gu, glay, gsn, optG), (dp, du, dlay, dsn, optD), G, D
+
+
+def dev(torch, v):
+    return torch.from_numpy(np.ascontiguousarray(v)).cuda()
+
+
+def zero_by_bn(a, name):
+    """Generator biases whose gradient is identically zero: each feeds only a
+    batch-statistics BN (conv1 -> bn2 in every G block; the last G block's
+    conv2 / skip -> the output BN).  Both sides return rounding noise."""
+    last = "g%d." % (a.n_g - 1)
+    return (name.endswith("conv1.b") and name.startswith("g")) or name in (last + "conv2.b", last + "sc.b")
+
+
+def module_of(name):
+    return name.split(".")[0]
+
+
+def check_net(rep, tag, a, got, ref, keys, gen, strict):
+    """strict: every tensor at 2e-2 normalised max-abs.  Otherwise every
+    module's concatenated tensors at 2e-2 relative L2 (max-abs reported)."""
+    mods = {}
+    for k in keys:
+        assert np.all(np.isfinite(got[k])), tag + k
+        if gen and zero_by_bn(a, k):
+            continue
+        e = norm_maxabs(got[k], ref[k])
+        if strict:
+            rep.add(tag + k, e, TOL_BF16)
+        else:
+            rep.err[tag + k + ".maxabs"] = e
+            g, r = mods.setdefault(module_of(k), ([], []))
+            g.append(np.ravel(got[k]))
+            r.append(np.ravel(ref[k]))
+    for m, (g, r) in mods.items():
+        g, r = np.concatenate(g), np.concatenate(r)
+        rep.add(tag + m + ".l2", float(np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-30)), TOL_BF16)
+
+
+def check_grads(rep, tag, a, got, ref, lay, gen, strict=False):
+    check_net(rep, tag, a, got, ref, list(lay), gen, strict)
+
+
+def check_update(rep, tag, a, p_new, p_old, p_ref, keys, gen, strict=False):
+    """The optimiser's change of every tensor, against the oracle's change
+    from the same state (smooth in the gradient for t > 1)."""
+    check_net(rep, tag, a, {k: p_new[k] - p_old[k] for k in keys}, {k: p_ref[k] - p_old[k] for k in keys},
+              keys, gen, strict)
+
+
+def loss_err(got, ref):
+    return abs(got - ref) / max(abs(ref), 1e-3)
+
+
+# ------------------------------------------------------------ generator forward
+@pytest.mark.parametrize("arch,B", [("small", 4), ("biggan128", 2)])
+def test_g_sample(arch, B):
+    torch = need_gpu()
+    a = small_arch() if arch == "small" else O.biggan128()
+    hp = hparams()
+    d, s, (gp, gu, glay, gsn, _), _, G, _ = make_nets(torch, a, B, 401, hp)
+    z, y = f32({"z": s.normal((B, a.dz))})["z"], s.labels(B, a.n_classes)
+    print("g_sample case", arch, B, flush=True)
+    ctx = context()
     ws = lib.workspace(lib.paragan_train_step_ws_size(d))
-    losses = (C.c_float * (n_D + 1))()
-    print("train step case", dict(arch=a, B=B, n_D=n_D, seed=seed), flush=True)
-    rc = lib.paragan_train_step(ctx, d, G.state, D.state, inp, n_D, ws, losses)
-    assert rc == lib.OK, lib.load().paragan_last_error(ctx.h)
+    img = torch.empty((B, a.img, a.img, 3), dtype=torch.float32, device="cuda")
+    ctx.check(lib.paragan_g_sample(ctx, d, G.state, dev(torch, z.astype(np.float32)), dev(torch, y), img, ws))
     torch.cuda.synchronize()
-    assert G.state.adam_t == 1 and D.state.adam_t == n_D
-    optG, optD = O.adam_init(gp), O.adam_init(dp)
-    Gr, Dr, loss_r, gd_r, gg_r = O.train_step(a, hp, (gp, gu), (dp, du), optG, optD, d_in, g_in)
-    sens = {}
-    # ReLU masks near zero may flip between the two rounding points of the
-    # filters the GPU folds: the oracle's own movement when they move by that
-    # rounding bounds what a flip can do (max-abs metric for the strict
-    # checks, relative L2 for the calibrated ones)
-    metric = rel_l2 if calibrated else norm_maxabs
-    gp2, dp2 = folded_filters_perturbed(a, gp, dp, seed)
-    optG2, optD2 = O.adam_init(gp2), O.adam_init(dp2)
-    _, _, _, gd2, gg2 = O.train_step(a, hp, (gp2, gu), (dp2, du), optG2, optD2, d_in, g_in)
-    sens.update({"gG." + k: metric(gg2[k], gg_r[k]) for k in glay})
-    sens.update({"gD." + k: metric(gd2[k], gd_r[k]) for k in dlay})
-    if calibrated:
-        # and its movement when its real images move by 1e-5 (about one bf16
-        # flip in 300 values): the chaos floor of this net; the larger counts
-        rng = np.random.default_rng(seed)
-        d_in2 = [(x * (1 + 1e-5 * rng.standard_normal(x.shape)), yr, z, yf) for x, yr, z, yf in d_in]
-        optG2, optD2 = O.adam_init(gp), O.adam_init(dp)
-        _, _, _, gd2, gg2 = O.train_step(a, hp, (gp, gu), (dp, du), optG2, optD2, d_in2, g_in)
-        for k in glay:
-            sens["gG." + k] = max(sens["gG." + k], rel_l2(gg2[k], gg_r[k]))
-        for k in dlay:
-            sens["gD." + k] = max(sens["gD." + k], rel_l2(gd2[k], gd_r[k]))
+    harvest(ctx)
+    img_r, u_r, _ = O.g_fwd(a, hp, gp, gu, z, y)
     rep = Report()
-    lg = np.array(list(losses))
-    print("losses gpu", lg, "oracle", loss_r, flush=True)
-    rep.add("losses", float(np.abs(lg - np.array(loss_r)).max() / max(np.abs(loss_r).max(), 1e-6)), TOL_BF16)
-    ggrad = lib.named_from_flat(gents, G.G)
-    dgrad = lib.named_from_flat(dents, D.G)
-    for tag, got, ref, lay in (("gG.", ggrad, gg_r, glay), ("gD.", dgrad, gd_r, dlay)):
-        for k in lay:
-            if tag == "gG." and zero_by_bn(a, k):
-                continue
-            if calibrated:
-                tol = max(TOL_BF16, 3 * sens[tag + k])
-                rep.add(tag + k, rel_l2(got[k], ref[k]), tol)
-            else:
-                assert np.all(np.isfinite(got[k])), tag + k
-                rep.add(tag + k, norm_maxabs(got[k], ref[k]), max(TOL_BF16, 3 * sens[tag + k]))
-                rep.err[tag + k + ".sens"] = sens[tag + k]
-    gu_new = lib.named_u_from_flat(gents, G.U)
+    got = img.cpu().numpy()
+    rep.err["img.maxabs"] = norm_maxabs(got, img_r)
+    rep.add("img.l2", float(np.linalg.norm(got - img_r) / np.linalg.norm(img_r)), TOL_BF16)
+    gu_new = lib.named_u_from_flat(G.ents, G.U)
     for k in gsn:
-        check("uG." + k, gu_new[k], Gr[1][k], False, rep)
-    if not calibrated:
-        # D's final u comes from the generator step's D forward, which runs on
-        # the Adam-updated D weights: bf16-gradient precision
-        du_new = lib.named_u_from_flat(dents, D.U)
-        for k in dsn:
-            check("uD." + k, du_new[k], Dr[1][k], True, rep)
-        gp_new = lib.named_from_flat(gents, G.P)
-        for k in glay:
-            if not zero_by_bn(a, k):
-                check_adam_step("G." + k, gp_new[k], gp[k], gg_r[k], Gr[0][k], hp.lr_g, rep)
-        if n_D == 1:
-            dp_new = lib.named_from_flat(dents, D.P)
-            for k in dlay:
-                check_adam_step("D." + k, dp_new[k], dp[k], gd_r[k], Dr[0][k], hp.lr_d, rep)
+        check("u." + k, gu_new[k], u_r[k], False, rep)
+    assert np.array_equal(lib.named_from_flat(G.ents, G.P)["linear.w"], gp["linear.w"].astype(np.float32))
     rep.done()
 
 
-def minimal_arch():
-    # one G block (4 -> 8), one pooling D block (8 -> 4), no attention
-    return O.Arch(img=8, ch=16, g_mult=(2, 1), d_mult=(2,), d_down=(1,), attn_res=0, n_classes=5, dz=8,
-                  shared_dim=8)
+# ------------------------------------------------------ discriminator step
+@pytest.mark.parametrize("arch,B", [("minimal", 8), ("small", 4), ("biggan128", 2)])
+def test_d_step_images(arch, B):
+    """One D step on B real + B given fake images (uniform in [-1, 1]) with
+    Adam from a smooth state: L_D, every D gradient, D's u and its update."""
+    torch = need_gpu()
+    a = {"minimal": minimal_arch, "small": small_arch, "biggan128": O.biggan128}[arch]()
+    hp = hparams()
+    d, s, _, (dp, du, dlay, dsn, optD), _, D = make_nets(torch, a, B, 402, hp, smooth_opt=True)
+    xr = s.uniform((B, a.img, a.img, 3)).astype(np.float32)
+    # fakes with other statistics than the real images, as a generator's
+    # are (with both from one distribution the real and fake halves' terms
+    # of every D gradient nearly cancel, which no summation order resolves)
+    xf = (0.5 * s.uniform((B, a.img, a.img, 3)) + 0.25).astype(np.float32)
+    yr, yf = s.labels(B, a.n_classes), s.labels(B, a.n_classes)
+    print("d_step case", arch, B, flush=True)
+    ctx = context()
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+    loss = (C.c_float * 1)()
+    rc = lib.paragan_d_step(ctx, d, D.state, dev(torch, xr), dev(torch, yr), dev(torch, xf), dev(torch, yf), ws,
+                            loss)
+    assert rc == lib.OK, lib.load().paragan_last_error(ctx.h)
+    torch.cuda.synchronize()
+    harvest(ctx)
+    assert D.state.opt_t == 8
+    (dp_r, du_r), loss_r, gd_r = O.d_step_images(a, hp, (dp, du), optD, xr.astype(np.float64), yr,
+                                                 xf.astype(np.float64), yf)
+    rep = Report()
+    rep.add("L_D", loss_err(loss[0], loss_r), TOL_BF16)
+    strict = arch == "minimal"
+    check_grads(rep, "gD.", a, lib.named_from_flat(D.ents, D.G), gd_r, dlay, False, strict)
+    du_new = lib.named_u_from_flat(D.ents, D.U)
+    for k in dsn:
+        check("uD." + k, du_new[k], du_r[k], False, rep)
+    check_update(rep, "stepD.", a, lib.named_from_flat(D.ents, D.P), dp, dp_r, list(dlay), False, strict)
+    rep.done()
 
 
-@pytest.mark.parametrize("n_D", [1, 2])
-def test_train_step_minimal_strict(n_D):
-    """Heads, hinge, Adam, z-linear, conditioning and the class-embedding
-    gradient at the 2e-2 bar (a network shallow enough that bf16 rounding
-    flips cannot move its gradients by more than that), widened only to 3x
-    the oracle's own movement when its pooled conv2 filter moves by the
-    rounding the GPU's pooled-filter evaluation introduces."""
-    run_step(minimal_arch(), B=16, n_D=n_D, seed=310 + n_D, calibrated=False)
+# ------------------------------------------------------------ generator step
+@pytest.mark.parametrize("arch,B", [("minimal", 8), ("small", 4), ("biggan128", 2)])
+def test_g_step(arch, B):
+    """One G step with AdaBelief from a smooth state against a fixed D: L_G,
+    every G gradient, both nets' u, G's update; D's parameters and optimiser
+    state stay untouched, bit for bit."""
+    torch = need_gpu()
+    a = {"minimal": minimal_arch, "small": small_arch, "biggan128": O.biggan128}[arch]()
+    hp = hparams()
+    d, s, (gp, gu, glay, gsn, optG), (dp, du, dlay, dsn, _), G, D = make_nets(torch, a, B, 403, hp,
+                                                                              smooth_opt=True)
+    z, y = f32({"z": s.normal((B, a.dz))})["z"], s.labels(B, a.n_classes)
+    print("g_step case", arch, B, flush=True)
+    keepD = [t.clone() for t in (D.P, D.M, D.V)]
+    ctx = context()
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+    loss = (C.c_float * 1)()
+    rc = lib.paragan_g_step(ctx, d, G.state, D.state, dev(torch, z.astype(np.float32)), dev(torch, y), ws, loss)
+    assert rc == lib.OK, lib.load().paragan_last_error(ctx.h)
+    torch.cuda.synchronize()
+    harvest(ctx)
+    assert G.state.opt_t == 8 and D.state.opt_t == 7
+    for before, after in zip(keepD, (D.P, D.M, D.V)):
+        assert torch.equal(before, after)
+    (gp_r, gu_r), (_, du_r), loss_r, gg_r = O.g_step(a, hp, (gp, gu), (dp, du), optG, z, y)
+    rep = Report()
+    rep.add("L_G", loss_err(loss[0], loss_r), TOL_BF16)
+    strict = arch == "minimal"
+    check_grads(rep, "gG.", a, lib.named_from_flat(G.ents, G.G), gg_r, glay, True, strict)
+    gu_new = lib.named_u_from_flat(G.ents, G.U)
+    for k in gsn:
+        check("uG." + k, gu_new[k], gu_r[k], False, rep)
+    du_new = lib.named_u_from_flat(D.ents, D.U)
+    for k in dsn:
+        check("uD." + k, du_new[k], du_r[k], False, rep)
+    check_update(rep, "stepG.", a, lib.named_from_flat(G.ents, G.P), gp, gp_r, list(glay), True, strict)
+    rep.done()
 
 
-def test_train_step_small_biggan_calibrated():
-    """Every component (attention in both nets, identity skips) at a
-    tolerance calibrated by the oracle's own chaos floor and its movement
-    under the folded filters' rounding (see run_step)."""
-    run_step(small_arch(), B=4, n_D=2, seed=302, calibrated=True)
+# ---------------------------------------------------- the fused iteration
+def step_inputs(torch, s, a, B, n_D):
+    xs = [s.uniform((B, a.img, a.img, 3)).astype(np.float32) for _ in range(n_D)]
+    yrs = [s.labels(B, a.n_classes) for _ in range(n_D)]
+    zs = [s.normal((B, a.dz)).astype(np.float32) for _ in range(n_D)]
+    yfs = [s.labels(B, a.n_classes) for _ in range(n_D)]
+    zg, yg = s.normal((B, a.dz)).astype(np.float32), s.labels(B, a.n_classes)
+    keep = [dev(torch, v) for v in xs + yrs + zs + yfs] + [dev(torch, zg), dev(torch, yg)]
+    ptrs = [t.data_ptr() for t in keep]
+    arr = lambda lst: (C.c_void_p * n_D)(*lst)
+    inp = lib.StepInputs(arr(ptrs[0:n_D]), arr(ptrs[n_D:2 * n_D]), arr(ptrs[2 * n_D:3 * n_D]),
+                         arr(ptrs[3 * n_D:4 * n_D]), ptrs[4 * n_D], ptrs[4 * n_D + 1])
+    return inp, keep
+
+
+def run_train_step(torch, d, G, D, inp, n_D, ws, ctx):
+    losses = (C.c_float * (n_D + 1))()
+    rc = lib.paragan_train_step(ctx, d, G.state, D.state, inp, n_D, ws, losses)
+    assert rc == lib.OK, lib.load().paragan_last_error(ctx.h)
+    torch.cuda.synchronize()
+    return list(losses)
+
+
+def test_train_step_equals_its_pieces_and_is_deterministic():
+    """paragan_train_step (two streams, prepared weights) equals
+    g_sample + d_step per D step and then g_step, bit for bit, and two runs
+    from the same state are bit-identical."""
+    torch = need_gpu()
+    a, B, n_D = small_arch(), 4, 2
+    hp = hparams()
+    d, s, _, _, G0, D0 = make_nets(torch, a, B, 404, hp)
+    inp, keep = step_inputs(torch, s, a, B, n_D)
+    ctx = context()
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+    runs = []
+    for _ in range(2):
+        G, D = G0.clone(torch), D0.clone(torch)
+        losses = run_train_step(torch, d, G, D, inp, n_D, ws, ctx)
+        runs.append((losses, G, D))
+    # the pieces
+    G, D = G0.clone(torch), D0.clone(torch)
+    img = torch.empty((B, a.img, a.img, 3), dtype=torch.float32, device="cuda")
+    pl = []
+    for k in range(n_D):
+        ctx.check(lib.paragan_g_sample(ctx, d, G.state, keep[2 * n_D + k], keep[3 * n_D + k], img, ws))
+        loss = (C.c_float * 1)()
+        ctx.check(lib.paragan_d_step(ctx, d, D.state, keep[k], keep[n_D + k], img, keep[3 * n_D + k], ws, loss))
+        pl.append(loss[0])
+    loss = (C.c_float * 1)()
+    ctx.check(lib.paragan_g_step(ctx, d, G.state, D.state, keep[4 * n_D], keep[4 * n_D + 1], ws, loss))
+    pl.append(loss[0])
+    torch.cuda.synchronize()
+    harvest(ctx)
+    (l1, G1, D1), (l2, G2, D2) = runs
+    assert l1 == l2 == pl, (l1, l2, pl)
+    for X, Y in ((G1, G2), (D1, D2), (G1, G), (D1, D)):
+        for t1, t2 in zip(X.tensors(), Y.tensors()):
+            assert torch.equal(t1, t2)
+        assert X.state.opt_t == Y.state.opt_t
+
+
+def test_train_step_minimal_vs_oracle():
+    """The whole iteration against the oracle's, end to end, on a network
+    shallow enough that no decision inside it is near a tie: every loss,
+    the last D step's and the G step's gradients at the bf16 bar."""
+    torch = need_gpu()
+    a, B, n_D = minimal_arch(), 16, 2
+    hp = hparams()
+    d, s, (gp, gu, glay, gsn, optG), (dp, du, dlay, dsn, optD), G, D = make_nets(torch, a, B, 405, hp)
+    inp, keep = step_inputs(torch, s, a, B, n_D)
+    ctx = context()
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+    losses = run_train_step(torch, d, G, D, inp, n_D, ws, ctx)
+    harvest(ctx)
+    host = [t.cpu().numpy() for t in keep]
+    d_in = [(host[k].astype(np.float64), host[n_D + k], host[2 * n_D + k].astype(np.float64), host[3 * n_D + k])
+            for k in range(n_D)]
+    g_in = (host[4 * n_D].astype(np.float64), host[4 * n_D + 1])
+    Gr, Dr, loss_r, gd_r, gg_r = O.train_step(a, hp, (gp, gu), (dp, du), optG, optD, d_in, g_in)
+    rep = Report()
+    for k in range(n_D + 1):
+        rep.add("loss%d" % k, loss_err(losses[k], loss_r[k]), TOL_BF16)
+    check_grads(rep, "gD.", a, lib.named_from_flat(D.ents, D.G), gd_r, dlay, False, True)
+    check_grads(rep, "gG.", a, lib.named_from_flat(G.ents, G.G), gg_r, glay, True, True)
+    gu_new = lib.named_u_from_flat(G.ents, G.U)
+    for k in gsn:
+        check("uG." + k, gu_new[k], Gr[1][k], False, rep)
+    rep.done()
+
+
+# ---------------------------------------- a D step of 32 + 32 images, full size
+def test_d_step_biggan128_32_plus_32_batch_additive():
+    """BigGAN-128's D step at its full 32 real + 32 fake size.  The
+    discriminator has no batch coupling, so the step's loss and gradient are
+    the means of those of four 8 + 8 steps from the same state (a property
+    that holds at any size; the 2 + 2 step is held to the oracle above)."""
+    torch = need_gpu()
+    a, hp = O.biggan128(), hparams()
+    hp.opt_d = O.OptSpec("adam", 0.0, 0.0, 0.999, 1e-6)        # parameters stay put
+    d32, s, _, _, _, D0 = make_nets(torch, a, 32, 406, hp)
+    d8 = biggan_desc(a, 8, hp)
+    xr = dev(torch, s.uniform((32, a.img, a.img, 3)).astype(np.float32))
+    xf = dev(torch, s.uniform((32, a.img, a.img, 3)).astype(np.float32))
+    yr, yf = dev(torch, s.labels(32, a.n_classes)), dev(torch, s.labels(32, a.n_classes))
+    ctx = context()
+    ws = lib.workspace(max(lib.paragan_train_step_ws_size(d32), lib.paragan_train_step_ws_size(d8)))
+    D = D0.clone(torch)
+    loss = (C.c_float * 1)()
+    ctx.check(lib.paragan_d_step(ctx, d32, D.state, xr, yr, xf, yf, ws, loss))
+    torch.cuda.synchronize()
+    full_loss, full_g, full_u = loss[0], D.G.clone(), D.U.clone()
+    parts, gsum = [], torch.zeros_like(full_g)
+    for i in range(4):
+        D = D0.clone(torch)
+        sl = slice(8 * i, 8 * i + 8)
+        ctx.check(lib.paragan_d_step(ctx, d8, D.state, xr[sl].contiguous(), yr[sl].contiguous(), xf[sl].contiguous(),
+                                     yf[sl].contiguous(), ws, loss))
+        torch.cuda.synchronize()
+        parts.append(loss[0])
+        gsum += D.G
+        assert torch.equal(D.U, full_u) or torch.allclose(D.U, full_u, rtol=1e-5, atol=1e-6)
+    harvest(ctx)
+    rep = Report()
+    rep.add("L_D", abs(full_loss - np.mean(parts)) / max(abs(full_loss), 1e-3), 1e-3)
+    ents = D0.ents
+    got, ref = lib.named_from_flat(ents, full_g), lib.named_from_flat(ents, gsum / 4)
+    for k in got:
+        rep.add("gD." + k, norm_maxabs(got[k], ref[k]), TOL_BF16)
+    rep.done()
+
+
+# ------------------------------------------------------------ error paths
+def test_nonfinite_loss_reports_enonfinite():
+    """A NaN in the discriminator's output bias makes every logit and L_D
+    NaN: the D step finishes and returns PARAGAN_ENONFINITE (no GPU fault:
+    the NaN only flows through arithmetic).  (A NaN in an image need not
+    reach the loss: the ReLU on bf16 operands, a signed-integer max of the
+    bit patterns, maps a NaN whose sign bit is set to 0.)"""
+    torch = need_gpu()
+    a, B = minimal_arch(), 4
+    hp = hparams()
+    d, s, _, _, _, D = make_nets(torch, a, B, 407, hp)
+    hb = [e for e in D.ents if e["name"] == "head.b"][0]
+    D.P[hb["offset"]] = float("nan")
+    xr = s.uniform((B, a.img, a.img, 3)).astype(np.float32)
+    xf = s.uniform((B, a.img, a.img, 3)).astype(np.float32)
+    y = s.labels(B, a.n_classes)
+    ctx = context()
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+    loss = (C.c_float * 1)()
+    rc = lib.paragan_d_step(ctx, d, D.state, dev(torch, xr), dev(torch, y), dev(torch, xf), dev(torch, y), ws, loss)
+    assert rc == lib.ENONFINITE and not np.isfinite(loss[0])
+    assert "non-finite" in lib.load().paragan_last_error(ctx.h).decode()
+
+
+def test_train_step_rejects_n_d_zero_before_launching():
+    torch = need_gpu()
+    a, B = minimal_arch(), 4
+    d, s, _, _, G, D = make_nets(torch, a, B, 408, hparams())
+    inp, keep = step_inputs(torch, s, a, B, 1)
+    ctx = context()
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+    before = [t.clone() for t in G.tensors() + D.tensors()]
+    losses = (C.c_float * 2)()
+    assert lib.paragan_train_step(ctx, d, G.state, D.state, inp, 0, ws, losses) == lib.EINVAL
+    torch.cuda.synchronize()
+    assert all(torch.equal(x, y) for x, y in zip(before, G.tensors() + D.tensors()))

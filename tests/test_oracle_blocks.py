@@ -211,7 +211,7 @@ def test_train_step_runs_and_updates():
     gp, gu, _, s = _net(a, "g", 31, weights="orthogonal")
     dp, du, _, _ = _net(a, "d", 32, weights="orthogonal")
     hp = O.HParams()
-    optG, optD = O.adam_init(gp), O.adam_init(dp)
+    optG, optD = O.opt_init(gp), O.opt_init(dp)
     d_in = [(s.uniform((2, 16, 16, 3)), s.labels(2, 5), s.normal((2, a.dz)), s.labels(2, 5))
             for _ in range(2)]
     g_in = (s.normal((2, a.dz)), s.labels(2, 5))
@@ -221,5 +221,152 @@ def test_train_step_runs_and_updates():
     for k in gp:
         assert G[0][k].shape == gp[k].shape
     # Adam with beta1 = 0 moves each parameter by at most lr per step (|g|/(|g|+eps) < 1)
-    assert max(np.abs(G[0][k] - gp[k]).max() for k in gp) <= hp.lr_g * (1 + 1e-9)
-    assert max(np.abs(D[0][k] - dp[k]).max() for k in dp) <= 2 * hp.lr_d * (1 + 1e-9) * 1.5
+    assert max(np.abs(G[0][k] - gp[k]).max() for k in gp) <= hp.opt_g.lr * (1 + 1e-9)
+    assert max(np.abs(D[0][k] - dp[k]).max() for k in dp) <= 2 * hp.opt_d.lr * (1 + 1e-9) * 1.5
+
+
+# ------------------------------------------------ ambiguity bounds of the parity tests
+def _flip_where(arr, mask):
+    """A copy of arr with the sign of the masked elements flipped (a zero
+    becomes a tiny positive value): every ReLU decision there reverses."""
+    out = arr.copy()
+    out[mask] = np.where(arr[mask] > 0, -arr[mask], np.abs(arr[mask]) + 1e-300)
+    return out
+
+
+def _assert_within(name, diff, bound, scale):
+    """|diff| <= bound, up to float64 noise."""
+    excess = np.abs(diff) - bound * (1 + 1e-9) - 1e-12 * scale
+    assert excess.max() <= 0, (name, float(excess.max()), float(np.abs(diff).max()))
+
+
+def test_gblock_bounds_cover_mask_flips(monkeypatch):
+    """The element-wise bound used by the G-block parity test covers every
+    combination of ReLU flips it marks as ambiguous: with the bands widened
+    so that many elements are marked, the oracle's own backward with all of
+    those masks reversed stays inside the bound, tensor by tensor.  Run
+    without bf16 rounding, so that the difference is exactly the flips'."""
+    import tests.bounds as TB
+    monkeypatch.setattr(TB, "SUM_EPS", 2.0 ** -9)
+    monkeypatch.setattr(TB, "BN_EPS", 2.0 ** -6)
+    s = Stream(77)
+    shapes = B.gblock_param_shapes(12, 8, 6)
+    p = init_params(shapes, s, weights="gaussian")
+    u = init_u(shapes, B.GBLOCK_SN, s)
+    x = s.normal((3, 4, 5, 12))
+    cond = s.normal((3, 6))
+    dy = s.normal((3, 8, 10, 8))
+    cfg = B.BlockCfg(bf16=False)
+    _, _, cache = B.gblock_fwd(x, cond, p, u, cfg)
+    dx, dc, g = B.gblock_bwd(dy, cache, cfg)
+    bnd, info = TB.gblock_bounds(p, cache, dy)
+    counts = info["counts"]
+    assert counts["amb_bn2"] > 20 and counts["amb_bn1"] > 5, counts
+    flipped = dict(cache)
+    flipped["bn2"] = _flip_where(cache["bn2"], info["masks"]["bn2"])
+    flipped["bn1"] = _flip_where(cache["bn1"], info["masks"]["bn1"])
+    dx2, dc2, g2 = B.gblock_bwd(dy, flipped, cfg)
+    for k in ("conv1.w", "bn1.gain", "bn1.bias", "bn2.gain", "bn2.bias"):
+        _assert_within(k, g2[k] - g[k], bnd[k], np.abs(g[k]).max())
+    _assert_within("dx", dx2 - dx, bnd["dx"], np.abs(dx).max())
+    _assert_within("dcond", dc2 - dc, bnd["dcond"], np.abs(dc).max())
+    _assert_within("conv1.b", g2["conv1.b"] - g["conv1.b"], bnd["conv1.b_l1"], 1.0)
+    # and the flips do move the gradients (the pin has teeth)
+    assert np.abs(g2["conv1.w"] - g["conv1.w"]).max() > 1e-3 * np.abs(g["conv1.w"]).max()
+
+
+def test_dblock_bounds_cover_mask_flips(monkeypatch):
+    import tests.bounds as TB
+    monkeypatch.setattr(TB, "SUM_EPS", 2.0 ** -9)
+    s = Stream(78)
+    shapes = B.dblock_param_shapes(8, 12, True)
+    p = init_params(shapes, s, weights="gaussian")
+    u = init_u(shapes, ("conv1.w", "conv2.w", "sc.w"), s)
+    x = s.normal((2, 6, 8, 8))
+    dy = s.normal((2, 3, 4, 12))
+    cfg = B.BlockCfg(bf16=False)
+    _, _, cache = B.dblock_fwd(x, p, u, cfg, True, True, True)
+    dx, g = B.dblock_bwd(dy, cache, cfg, True, True, True)
+    bnd, info = TB.dblock_bounds(cache, dy, True, True)
+    assert info["counts"]["amb_h"] > 10, info["counts"]
+    flipped = dict(cache)
+    flipped["h"] = _flip_where(cache["h"], info["masks"]["h"])
+    dx2, g2 = B.dblock_bwd(dy, flipped, cfg, True, True, True)
+    for k in ("conv1.w", "conv1.b"):
+        _assert_within(k, g2[k] - g[k], bnd[k], np.abs(g[k]).max())
+    _assert_within("dx", dx2 - dx, bnd["dx"], np.abs(dx).max())
+    assert np.abs(g2["conv1.w"] - g["conv1.w"]).max() > 1e-3 * np.abs(g["conv1.w"]).max()
+
+
+# ------------------------------------------------------ the train step's logic
+def _tiny():
+    return O.Arch(img=8, ch=8, g_mult=(2, 1), d_mult=(1, 2), d_down=(1, 0), attn_res=0, n_classes=4, dz=8,
+                  shared_dim=4)
+
+
+def _advance(p, u, sn_keys, k):
+    """u of every SN weight after k power iterations (one per forward)."""
+    return {key: (L.sn_power_iter(p[key].reshape(p[key].shape[0], -1), u[key], k, 1e-12)[0] if k else u[key])
+            for key in sn_keys}
+
+
+def _setup(seed, bf=False):
+    a = _tiny()
+    s = Stream(seed)
+    glay, gsn = O.g_layout(a)
+    dlay, dsn = O.d_layout(a)
+    gp, gu = init_params(glay, s, weights="gaussian"), init_u(glay, gsn, s)
+    dp, du = init_params(dlay, s, weights="gaussian"), init_u(dlay, dsn, s)
+    B = 3
+    d_in = [(s.uniform((B, 8, 8, 3)), s.labels(B, 4), s.normal((B, 8)), s.labels(B, 4)) for _ in range(2)]
+    g_in = (s.normal((B, 8)), s.labels(B, 4))
+    return a, (glay, gsn, gp, gu), (dlay, dsn, dp, du), d_in, g_in
+
+
+def test_train_step_losses_from_separate_forwards():
+    """With zero learning rates the step's losses equal the hinge of D
+    forwards computed on their own: the real half with the real labels, the
+    fake half G(z, y_fake) with y_fake, every SN vector advanced by exactly
+    one power iteration per training forward (D's concat batch is one
+    forward), and the G step seeing the u left by the n_D D steps."""
+    a, (glay, gsn, gp, gu), (dlay, dsn, dp, du), d_in, g_in = _setup(41)
+    hp = O.HParams(bf16=False, opt_g=O.OptSpec("adam", 0.0), opt_d=O.OptSpec("adam", 0.0))
+    G, D, losses, _, _ = O.train_step(a, hp, (gp, gu), (dp, du), O.opt_init(gp), O.opt_init(dp), d_in, g_in)
+    n_D = len(d_in)
+    for k, (xr, yr, z, yf) in enumerate(d_in):
+        guk, duk = _advance(gp, gu, gsn, k), _advance(dp, du, dsn, k)
+        fake, _, _ = O.g_fwd(a, hp, gp, guk, z, yf)
+        out_r, _, _ = O.d_fwd(a, hp, dp, duk, xr, yr)
+        out_f, _, _ = O.d_fwd(a, hp, dp, duk, fake, yf)
+        want = np.maximum(1 - out_r, 0).mean() + np.maximum(1 + out_f, 0).mean()
+        assert np.isclose(losses[k], want, rtol=1e-12), (k, losses[k], want)
+    fake, _, _ = O.g_fwd(a, hp, gp, _advance(gp, gu, gsn, n_D), *g_in)
+    out, _, _ = O.d_fwd(a, hp, dp, _advance(dp, du, dsn, n_D), fake, g_in[1])
+    assert np.isclose(losses[n_D], -out.mean(), rtol=1e-12)
+    # and every u advanced once per forward: n_D + 1 forwards of each net
+    for key in gsn:
+        np.testing.assert_allclose(G[1][key], _advance(gp, gu, gsn, n_D + 1)[key], rtol=1e-10, atol=1e-12)
+    for key in dsn:
+        np.testing.assert_allclose(D[1][key], _advance(dp, du, dsn, n_D + 1)[key], rtol=1e-10, atol=1e-12)
+
+
+def test_each_step_updates_only_its_network():
+    """The D step changes D's parameters and optimiser state and only G's u;
+    the G step changes G's and only D's u."""
+    a, (glay, gsn, gp, gu), (dlay, dsn, dp, du), d_in, g_in = _setup(42)
+    hp = O.HParams(bf16=False, opt_g=O.adabelief_g())
+    optG, optD = O.opt_init(gp), O.opt_init(dp)
+    G1, D1, _, gd = O.d_step(a, hp, (gp, gu), (dp, du), optD, *d_in[0])
+    assert all(np.array_equal(G1[0][k], gp[k]) for k in gp) and optG.t == 0 and optD.t == 1
+    assert any(not np.array_equal(D1[0][k], dp[k]) for k in dp)
+    assert any(not np.allclose(G1[1][k], gu[k]) for k in gsn)
+    mD = {k: v.copy() for k, v in optD.m.items()}
+    G2, D2, _, gg = O.g_step(a, hp, G1, D1, optG, *g_in)
+    assert all(np.array_equal(D2[0][k], D1[0][k]) for k in dp) and optD.t == 1 and optG.t == 1
+    assert all(np.array_equal(optD.m[k], mD[k]) for k in dp)
+    assert any(not np.array_equal(G2[0][k], G1[0][k]) for k in gp)
+    assert any(not np.allclose(D2[1][k], D1[1][k]) for k in dsn)
+    # the optimiser moved each network by its own rule from its own gradients
+    st = O.opt_init(gp)
+    want = O.opt_update(G1[0], gg, st, hp.opt_g)
+    assert all(np.allclose(G2[0][k], want[k], rtol=0, atol=1e-15) for k in gp)

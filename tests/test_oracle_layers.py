@@ -120,6 +120,98 @@ def test_resampling_adjoints():
     assert np.count_nonzero(g) == d2.size
 
 
+# ------------------------------------------- convolutions fused with resampling
+def test_up2_conv_fold_equals_conv_over_upsample():
+    """conv3x3(up2(x)) with the taps that meet one source pixel added first:
+    equal to torch's conv over torch's nearest upsample, forward and data
+    gradient, on an odd ragged shape."""
+    x = RNG.standard_normal((2, 3, 5, 4))
+    w = RNG.standard_normal((6, 3, 3, 4))
+    b = RNG.standard_normal(6)
+    dy = RNG.standard_normal((2, 6, 10, 6))
+    Fw = L.up2_conv_fold(w)
+    xt = nchw(x).requires_grad_()
+    up = F.interpolate(xt, scale_factor=2, mode="nearest")
+    ref = F.conv2d(up, t(w.transpose(0, 3, 1, 2)), t(b), padding=1)
+    ref.backward(nchw(dy))
+    np.testing.assert_allclose(L.up2_conv(x, Fw, b), nhwc(ref), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(L.up2_conv_dgrad(dy, Fw), nhwc(xt.grad), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(L.up2_conv_dgrad(dy, Fw), L.up2_bwd(L.conv2d_dgrad(dy, w)), rtol=1e-12,
+                               atol=1e-12)
+
+
+def test_up2_conv_fold_taps():
+    """Each parity class's folded taps add up to the whole 3x3 filter; a single
+    1 at tap (r, s) lands at the documented (t, u) = source offset - (a - 1)."""
+    w = RNG.standard_normal((2, 3, 3, 3))
+    Fw = L.up2_conv_fold(w)
+    for a in range(2):
+        for b in range(2):
+            np.testing.assert_allclose(Fw[a, b].sum(axis=(1, 2)), w.sum(axis=(1, 2)), rtol=1e-13)
+    one = np.zeros((1, 3, 3, 1))
+    one[0, 0, 2, 0] = 1.0        # r = 0, s = 2
+    Fo = L.up2_conv_fold(one)
+    # a = 0: row offset -1 -> t = 0; a = 1: offset 0 -> t = 0.  b = 0: column
+    # offset 0 -> u = 1; b = 1: offset +1 -> u = 1.
+    for a in range(2):
+        for b in range(2):
+            nz = np.argwhere(Fo[a, b, 0, :, :, 0] != 0).tolist()
+            assert nz == [[0, 1]], (a, b, nz)
+
+
+def test_up2_conv_brute_force():
+    x = RNG.standard_normal((1, 2, 3, 2))
+    w = RNG.standard_normal((2, 3, 3, 2))
+    up = np.zeros((1, 4, 6, 2))
+    for h in range(4):
+        for q in range(6):
+            up[0, h, q] = x[0, h // 2, q // 2]
+    ref = np.zeros((1, 4, 6, 2))
+    for h in range(4):
+        for q in range(6):
+            for o in range(2):
+                acc = 0.0
+                for r in range(3):
+                    for s in range(3):
+                        hh, qq = h + r - 1, q + s - 1
+                        if 0 <= hh < 4 and 0 <= qq < 6:
+                            acc += float(up[0, hh, qq] @ w[o, r, s])
+                ref[0, h, q, o] = acc
+    np.testing.assert_allclose(L.up2_conv(x, L.up2_conv_fold(w)), ref, rtol=1e-13, atol=1e-13)
+
+
+def test_pool2_conv_fold_equals_pooled_conv():
+    """avgpool2(conv3x3(x)) as one stride-2 4x4 conv: equal to torch's pooled
+    conv, forward and data gradient."""
+    x = RNG.standard_normal((2, 6, 8, 3))
+    w = RNG.standard_normal((5, 3, 3, 3))
+    b = RNG.standard_normal(5)
+    dy = RNG.standard_normal((2, 3, 4, 5))
+    P = L.pool2_conv_fold(w)
+    xt = nchw(x).requires_grad_()
+    ref = F.avg_pool2d(F.conv2d(xt, t(w.transpose(0, 3, 1, 2)), t(b), padding=1), 2)
+    ref.backward(nchw(dy))
+    np.testing.assert_allclose(L.pool2_conv(x, P, b), nhwc(ref), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(L.pool2_conv_dgrad(dy, P), nhwc(xt.grad), rtol=1e-12, atol=1e-12)
+    # the 4x4 taps sum to the 3x3 filter's total; the corners hold w / 4
+    np.testing.assert_allclose(P.sum(axis=(1, 2)), w.sum(axis=(1, 2)), rtol=1e-13)
+    np.testing.assert_allclose(P[:, 0, 0], w[:, 0, 0] / 4, rtol=1e-15)
+    np.testing.assert_allclose(P[:, 3, 3], w[:, 2, 2] / 4, rtol=1e-15)
+
+
+def test_fused_resample_conv_adjointness():
+    x = RNG.standard_normal((2, 4, 6, 3))
+    w = RNG.standard_normal((4, 3, 3, 3))
+    d_up = RNG.standard_normal((2, 8, 12, 4))
+    Fw = L.up2_conv_fold(w)
+    lhs = (L.up2_conv(x, Fw) * d_up).sum()
+    assert abs(lhs - (x * L.up2_conv_dgrad(d_up, Fw)).sum()) < 1e-10 * abs(lhs)
+    d_pool = RNG.standard_normal((2, 2, 3, 4))
+    P = L.pool2_conv_fold(w)
+    lhs = (L.pool2_conv(x, P) * d_pool).sum()
+    assert abs(lhs - (x * L.pool2_conv_dgrad(d_pool, P)).sum()) < 1e-10 * abs(lhs)
+
+
 def test_maxpool_tie_rule():
     x = np.zeros((1, 2, 2, 3))
     x[0, :, :, 0] = [[1.0, 1.0], [1.0, 1.0]]      # all tied -> (0, 0)
@@ -277,3 +369,44 @@ def test_adam_closed_form_steps():
     # beta1 > 0: bias-corrected momentum, closed form at step 1 is the same
     p1b, _, _ = L.adam(p, g, np.zeros(3), np.zeros(3), 1, lr, 0.9, 0.999, eps)
     np.testing.assert_allclose(p1b, p1, rtol=1e-12)
+
+
+def test_adabelief_worked_first_step():
+    """Hand-computed first step from zero state: g = 2, beta1 = 1/2,
+    beta2 = 3/4, eps = 0: m = 1, s = (1/4)(2 - 1)^2 = 1/4, mhat = 2,
+    shat = 1, so the parameter moves by -2 lr."""
+    p1, m, s = L.adabelief(np.array([5.0]), np.array([2.0]), np.zeros(1), np.zeros(1), 1, 0.1, 0.5, 0.75, 0.0)
+    assert m[0] == 1.0 and s[0] == 0.25
+    assert np.isclose(p1[0], 5.0 - 0.2, rtol=0, atol=1e-15)
+
+
+def test_adabelief_constant_gradient_limit():
+    """With a constant gradient the bias-corrected mean is exactly g at every
+    step, the deviation g - m decays as beta1^t, so the second moment tends
+    to eps / (1 - beta2) (the belief in a steady gradient): the step grows
+    monotonically towards lr g / (sqrt(eps / (1 - beta2)) + eps)."""
+    g, lr, b1, b2, eps = 0.3, 1e-3, 0.5, 0.9, 1e-8
+    p, m, s = np.zeros(1), np.zeros(1), np.zeros(1)
+    steps = []
+    for t in range(1, 400):
+        p_new, m, s = L.adabelief(p, np.array([g]), m, s, t, lr, b1, b2, eps)
+        steps.append(float(p[0] - p_new[0]))
+        p = p_new
+        assert np.isclose(m[0] / (1 - b1 ** t), g, rtol=1e-12)
+    assert all(b >= a * (1 - 1e-12) for a, b in zip(steps, steps[1:]))
+    limit = lr * g / (np.sqrt(eps / (1 - b2)) + eps)
+    assert np.isclose(steps[-1], limit, rtol=1e-6)
+
+
+def test_adabelief_scale_invariant_without_eps():
+    """At eps = 0 the step depends on the gradient's direction history, not
+    its scale: m scales by k and (g - m)^2 by k^2."""
+    rng = np.random.default_rng(5)
+    gs = rng.standard_normal((6, 4))
+    out = []
+    for k in (1.0, 1e-3):
+        p, m, s = np.zeros(4), np.zeros(4), np.zeros(4)
+        for t, g in enumerate(gs, start=1):
+            p, m, s = L.adabelief(p, k * g, m, s, t, 1e-2, 0.9, 0.999, 0.0)
+        out.append(p)
+    np.testing.assert_allclose(out[0], out[1], rtol=1e-10)
