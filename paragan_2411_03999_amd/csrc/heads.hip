@@ -645,14 +645,17 @@ __global__ void k_hinge(const float* out, int nr, int nf, int mode, float* dout,
   __shared__ double sh[4];
   double s = 0.0;
   const int n = mode == 0 ? nr + nf : nf;
+  // relu(t) as (t > 0 ? t : 0) would drop a NaN logit; a NaN propagates
+  // into the loss instead, so that a diverged discriminator is reported
+  auto relu_nan = [](float t) { return t > 0.f || t != t ? t : 0.f; };
   for (int i = threadIdx.x; i < n; i += 256) {
     const float v = out[i];
     if (mode == 0) {
       if (i < nr) {
-        s += (double)fmaxf(1.f - v, 0.f) / nr;
+        s += (double)relu_nan(1.f - v) / nr;
         dout[i] = v < 1.f ? -1.f / nr : 0.f;
       } else {
-        s += (double)fmaxf(1.f + v, 0.f) / nf;
+        s += (double)relu_nan(1.f + v) / nf;
         dout[i] = v > -1.f ? 1.f / nf : 0.f;
       }
     } else {

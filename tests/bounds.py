@@ -25,9 +25,8 @@ bf16's half spacing for the sums here and would mark nearly every element;
 the estimate instead models each accumulator rounding as an independent
 error of at most 2^-24 of the running sum, whose total over n roundings has
 standard deviation below 2^-24 sqrt(n) times the root-sum-square of the
-terms.  SUM_EPS = 2^-19 takes 32 such standard deviations with n = K
-(measured on the GPU: at 8 a few flips of the BigGAN-128 block tests fell
-outside the band): band = SUM_EPS * sqrt(K) * sqrt(sum of squared terms).  A BN output
+terms.  SUM_EPS = 2^-19 takes 32 such standard deviations with n = K:
+band = SUM_EPS * sqrt(K) * sqrt(sum of squared terms).  A BN output
 gain * xhat + bias comes from fp32 statistics and tables after a handful of
 roundings: BN_EPS = 2^-20 of its absolute terms.  The spectral norm sigma is
 an fp32 power iteration on the GPU: SIGMA_EPS = 2^-16 of every value it
@@ -45,7 +44,7 @@ SIGMA_EPS = 2.0 ** -16
 
 
 def conv_band(l2sq, k):
-    """Summation band of conv outputs with squared-term sums l2sq over k terms."""
+    """Summation band of conv outputs whose k terms have squared sum l2sq."""
     return SUM_EPS * np.sqrt(k) * np.sqrt(l2sq)
 
 

@@ -35,29 +35,45 @@ def worst_copy(dev_t, ref, copies, c):
     return ref + torch.gather(d, 0, pick)[0].double().cpu().numpy()
 
 
+def f32(d):
+    """The values as the GPU holds them: fp32 master parameters."""
+    return {k: np.asarray(v, np.float32).astype(np.float64) for k, v in d.items()}
+
+
 def tile_batch(a, copies):
     return np.concatenate([a] * copies, axis=0) if copies > 1 else a
 
 
 def run_dblock(B, H, W, cin, cout, preact, down, lsc, dtype, seed, weights="orthogonal", want_dx=True,
                copies=1):
-    """copies > 1: the GPU runs a batch of `copies` copies of the B images
-    (the launch configuration of copies * B images; no op couples the batch,
-    so every copy's outputs are the oracle's for the B images, and each
-    weight gradient is copies times the oracle's)."""
-    torch = need_gpu()
     s = Stream(seed)
     shapes = OB.dblock_param_shapes(cin, cout, lsc)
     keys = [k for k in ("conv1.w", "conv2.w", "sc.w") if k in shapes]
     p = init_params(shapes, s, weights=weights)
     u = init_u(shapes, keys, s)
-    is_bf = dtype == lib.BF16
-    R = bf16 if is_bf else (lambda a: a)
+    R = bf16 if dtype == lib.BF16 else (lambda a: a)
     x = R(s.normal((B, H, W, cin)))
     Ho, Wo = (H // 2, W // 2) if down else (H, W)
     dy = R(s.normal((B, Ho, Wo, cout)))
     print("dblock case", dict(B=B, H=H, W=W, cin=cin, cout=cout, preact=preact, down=down, lsc=lsc,
                               dtype=dtype, seed=seed, copies=copies), flush=True)
+    return compare_dblock(x, p, u, dy, cout, preact, down, lsc, dtype, want_dx, copies)
+
+
+def compare_dblock(x, p, u, dy, cout, preact, down, lsc, dtype, want_dx=True, copies=1):
+    """The D block on the GPU against the oracle on given inputs (x, dy in
+    the storage precision; p, u fp32-representable).  copies > 1: the GPU
+    runs a batch of `copies` copies of x (the launch configuration of
+    copies * B images; no op couples the batch, so every copy's outputs are
+    the oracle's for x, and each weight gradient is copies times the
+    oracle's)."""
+    torch = need_gpu()
+    p, u = f32(p), f32(u)
+    B, H, W, cin = x.shape
+    shapes = OB.dblock_param_shapes(cin, cout, lsc)
+    keys = [k for k in ("conv1.w", "conv2.w", "sc.w") if k in shapes]
+    is_bf = dtype == lib.BF16
+    Ho, Wo = (H // 2, W // 2) if down else (H, W)
     # oracle
     cfg = OB.BlockCfg(bf16=is_bf)
     y_r, u_r, cache = OB.dblock_fwd(x, p, u, cfg, preact, down, lsc)
@@ -132,11 +148,6 @@ def test_dblock_config2_full():
 
 # ----------------------------------------------------------------- G block
 def run_gblock(B, H, W, cin, cout, dc, dtype, seed, weights="orthogonal", n_classes=None, copies=1):
-    """copies > 1: the GPU runs a batch of `copies` copies of the B samples.
-    Batch statistics of copies equal those of the B samples, so every copy's
-    outputs are the oracle's for the B samples and each weight gradient is
-    copies times the oracle's."""
-    torch = need_gpu()
     s = Stream(seed)
     shapes = OB.gblock_param_shapes(cin, cout, dc)
     p = init_params(shapes, s, weights=weights)
@@ -153,6 +164,22 @@ def run_gblock(B, H, W, cin, cout, dc, dtype, seed, weights="orthogonal", n_clas
     dy = R(s.normal((B, 2 * H, 2 * W, cout)))
     print("gblock case", dict(B=B, H=H, W=W, cin=cin, cout=cout, dc=dc, dtype=dtype, seed=seed, copies=copies),
           flush=True)
+    return compare_gblock(x, cond, p, u, dy, dtype, copies)
+
+
+def compare_gblock(x, cond, p, u, dy, dtype, copies=1):
+    """The G block on the GPU against the oracle on given inputs (x, dy in
+    the storage precision; cond, p, u fp32-representable).  copies > 1: the
+    GPU runs a batch of `copies` copies of the B samples.  Batch statistics
+    of copies equal those of the B samples, so every copy's outputs are the
+    oracle's for the B samples and each weight gradient is copies times the
+    oracle's."""
+    torch = need_gpu()
+    p, u = f32(p), f32(u)
+    B, H, W, cin = x.shape
+    cout, dc = p["conv1.w"].shape[0], cond.shape[1]
+    shapes = OB.gblock_param_shapes(cin, cout, dc)
+    is_bf = dtype == lib.BF16
     cfg = OB.BlockCfg(bf16=is_bf)
     y_r, u_r, cache = OB.gblock_fwd(x, cond, p, u, cfg)
     dx_r, dc_r, g_r = OB.gblock_bwd(dy, cache, cfg)

@@ -13,13 +13,21 @@ the step is a smooth function of the gradient.
 
 Bars.  Inside a network every block's input already carries the rounding of
 the blocks before it, so its ReLU, max-pool and hinge decisions near a tie
-come out differently far more often than at a block's exact inputs (where
-the block tests hold every element to 2e-2 plus a bound on exactly those
-flips, at every BigGAN-128 block shape and launch configuration).  A deep
-network is therefore held, module by module (a residual block, the
-attention block, each head), to a relative L2 error of its whole gradient and
-update of at most 2e-2; the per-tensor max-abs errors are reported.  The
-minimal network (one block each) is held element-wise, tensor by tensor.
+come out differently far more often than at a block's exact inputs.  The
+oracle itself, rerun with noise of 2^-20 of a value before each bf16
+rounding (a summation-order difference), moves its generator-step gradients
+by 1.5-9 % (the small network) and 4-12 % (BigGAN-128) in relative L2 per
+module.  So the element-wise bar (2e-2 plus a bound on exactly those flips)
+is applied block by block, to every block of BigGAN-128 in its place in the
+D and G steps, from the oracle's own inputs (tests/test_gpu_network_blocks.py),
+and at every block shape and launch configuration of the benchmark
+(tests/test_gpu_blocks.py).  Here the minimal network (one block each) is
+held element-wise, tensor by tensor, at 2e-2; deeper networks are held, as a
+check of how the blocks are composed, to a relative L2 error of at most
+TOL_NET = 0.25 per module (a residual block, the attention block, each head),
+twice the spread measured above, where a composition fault (a block, label,
+latent chunk or weight wired wrongly) moves a module by order 1; the
+per-tensor max-abs errors are reported.
 """
 import ctypes as C
 
@@ -33,6 +41,8 @@ from paragan_2411_03999_amd.synth import Stream, init_params, init_u
 from .parity import TOL_BF16, Report, biggan_desc, check, context, harvest, need_gpu, norm_maxabs
 
 pytestmark = pytest.mark.gpu
+
+TOL_NET = 0.25
 
 
 def small_arch():
@@ -133,7 +143,7 @@ def module_of(name):
 
 def check_net(rep, tag, a, got, ref, keys, gen, strict):
     """strict: every tensor at 2e-2 normalised max-abs.  Otherwise every
-    module's concatenated tensors at 2e-2 relative L2 (max-abs reported)."""
+    module's concatenated tensors at TOL_NET relative L2 (max-abs reported)."""
     mods = {}
     for k in keys:
         assert np.all(np.isfinite(got[k])), tag + k
@@ -149,7 +159,7 @@ def check_net(rep, tag, a, got, ref, keys, gen, strict):
             r.append(np.ravel(ref[k]))
     for m, (g, r) in mods.items():
         g, r = np.concatenate(g), np.concatenate(r)
-        rep.add(tag + m + ".l2", float(np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-30)), TOL_BF16)
+        rep.add(tag + m + ".l2", float(np.linalg.norm(g - r) / max(np.linalg.norm(r), 1e-30)), TOL_NET)
 
 
 def check_grads(rep, tag, a, got, ref, lay, gen, strict=False):
@@ -186,7 +196,7 @@ def test_g_sample(arch, B):
     rep = Report()
     got = img.cpu().numpy()
     rep.err["img.maxabs"] = norm_maxabs(got, img_r)
-    rep.add("img.l2", float(np.linalg.norm(got - img_r) / np.linalg.norm(img_r)), TOL_BF16)
+    rep.add("img.l2", float(np.linalg.norm(got - img_r) / np.linalg.norm(img_r)), TOL_NET)
     gu_new = lib.named_u_from_flat(G.ents, G.U)
     for k in gsn:
         check("u." + k, gu_new[k], u_r[k], False, rep)
@@ -414,7 +424,7 @@ def test_nonfinite_loss_reports_enonfinite():
     hp = hparams()
     d, s, _, _, _, D = make_nets(torch, a, B, 407, hp)
     hb = [e for e in D.ents if e["name"] == "head.b"][0]
-    D.P[hb["offset"]] = float("nan")
+    D.P[hb["offset"]] = float("nan")           # every logit NaN
     xr = s.uniform((B, a.img, a.img, 3)).astype(np.float32)
     xf = s.uniform((B, a.img, a.img, 3)).astype(np.float32)
     y = s.labels(B, a.n_classes)

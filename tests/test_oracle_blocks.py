@@ -370,3 +370,34 @@ def test_each_step_updates_only_its_network():
     st = O.opt_init(gp)
     want = O.opt_update(G1[0], gg, st, hp.opt_g)
     assert all(np.allclose(G2[0][k], want[k], rtol=0, atol=1e-15) for k in gp)
+
+
+def test_generator_step_spread_under_rounding_noise(monkeypatch):
+    """The premise of the network-level bars: a whole generator step is
+    sensitive to rounding.  Rerun with noise of 2^-20 of every value before
+    its bf16 rounding (a summation-order difference), the oracle's own
+    per-module gradients of a 3-block network move by more than the 2e-2
+    block bar somewhere, and by less than half the 0.25 composition bar."""
+    import oracle.numerics as N
+    a = O.Arch(img=32, ch=8, g_mult=(4, 4, 2, 1), d_mult=(1, 2, 4, 4), d_down=(1, 1, 1, 0), attn_res=16,
+               n_classes=10, dz=20, shared_dim=16)
+    hp = O.HParams(opt_g=O.adabelief_g())
+    s = Stream(403)
+    glay, gsn = O.g_layout(a)
+    dlay, dsn = O.d_layout(a)
+    gp, gu = init_params(glay, s, weights="gaussian"), init_u(glay, gsn, s)
+    dp, du = init_params(dlay, s, weights="gaussian"), init_u(dlay, dsn, s)
+    z, y = s.normal((4, a.dz)), s.labels(4, a.n_classes)
+    _, _, _, g0 = O.g_step(a, hp, (gp, gu), (dp, du), O.opt_init(gp), z, y)
+    rng = np.random.default_rng(0)
+    exact = N.bf16
+    monkeypatch.setattr(N, "bf16", lambda x: exact(np.asarray(x) * (1 + 2.0 ** -20 * rng.standard_normal(np.shape(x)))))
+    _, _, _, g1 = O.g_step(a, hp, (gp, gu), (dp, du), O.opt_init(gp), z, y)
+    spread = {}
+    for k in g0:
+        m = k.split(".")[0]
+        d, r = spread.get(m, (0.0, 0.0))
+        spread[m] = (d + float(((g1[k] - g0[k]) ** 2).sum()), r + float((g0[k] ** 2).sum()))
+    rel = {m: (d / r) ** 0.5 for m, (d, r) in spread.items()}
+    assert max(rel.values()) > 2e-2, rel
+    assert max(rel.values()) < 0.125, rel
