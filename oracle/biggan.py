@@ -424,3 +424,40 @@ def train_step(a, hp, G, D, optG, optD, d_inputs, g_inputs):
     G, D, lg, gg = g_step(a, hp, G, D, optG, *g_inputs)
     losses.append(lg)
     return G, D, losses, gd, gg
+
+
+def async_step(a, hp, G, D, optG, optD, d_inputs, g_inputs, img_buff, lab_buff):
+    """One iteration of the asynchronous update scheme (Numerical
+    Optimizations, "Asynchronous Update Scheme"), written sequentially: the
+    two halves below read disjoint state, so running them one after the
+    other or side by side gives the same numbers.
+
+    * The generator half takes a snapshot of D as it is at the start of the
+      iteration and makes one generator step of batch len(z) against it
+      (the snapshot's SN vectors advance and are dropped with the snapshot).
+      Its samples, their labels and the snapshot's predictions on them are
+      what goes into img_buff / lab_buff / pred_buff for the next iteration.
+    * The discriminator half makes len(d_inputs) D steps; step k sees the
+      real batch d_inputs[k] = (x_real, y_real) and the k-th len(x_real)
+      images and labels of img_buff / lab_buff, the samples of the previous
+      iteration's generator.
+
+    Returns (G, D, losses [L_D ..., L_G], img_buff, lab_buff, pred_buff,
+    last D grads, G grads)."""
+    z, y = g_inputs
+    snapshot = (dict(D[0]), dict(D[1]))
+    gp, gu = G
+    fake, gu, gcache = g_fwd(a, hp, gp, gu, z, y)
+    pred, _, dcache = d_fwd(a, hp, snapshot[0], snapshot[1], fake, y)
+    lg, dout = L.hinge_g(pred)
+    dimg, _ = d_bwd(a, hp, snapshot[0], dout, dcache, need_dx=True)
+    gg = g_bwd(a, hp, gp, dimg, gcache)
+    gp = opt_update(gp, gg, optG, hp.opt_g)
+    losses, gd = [], None
+    for k, (xr, yr) in enumerate(d_inputs):
+        b = xr.shape[0]
+        D, ld, gd = d_step_images(a, hp, D, optD, xr, yr, img_buff[k * b:(k + 1) * b],
+                                  lab_buff[k * b:(k + 1) * b])
+        losses.append(ld)
+    losses.append(lg)
+    return (gp, gu), D, losses, fake, np.array(y), pred, gd, gg
