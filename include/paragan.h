@@ -350,6 +350,50 @@ int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
                        float* losses_host);
 
 /* ---------------------------------------------------------------------
+ * The asynchronous update scheme (Numerical Optimizations, "Asynchronous
+ * Update Scheme"), on one GPU.  One call is one iteration:
+ *   1. the discriminator's parameters and SN vectors are copied to a
+ *      snapshot held in the workspace;
+ *   2. on the context's second stream: a generator step of batch n_D * B on
+ *      (z, y) against the snapshot, as paragan_g_step (the snapshot's SN
+ *      vectors advance and are discarded with it); its samples G(z, y),
+ *      their labels and the snapshot's predictions D_snap(G(z, y)) are kept;
+ *   3. concurrently on the context's stream: n_D discriminator steps, step k
+ *      as paragan_d_step on x_real[k], y_real[k] and the k-th B samples and
+ *      labels of img_buff / lab_buff -- the previous iteration's samples, so
+ *      the discriminator sees fakes one generator update stale;
+ *   4. after both: img_buff, lab_buff and pred_buff are replaced with this
+ *      iteration's samples, labels and predictions.
+ * The caller fills img_buff / lab_buff before the first iteration (e.g.
+ * with paragan_g_sample).  Together the two sides need about the memory of
+ * two generator steps and one discriminator step.
+ *   x_real, y_real: n_D device pointers each (fp32 [B][img][img][3], [B]);
+ *   z, y:           fp32 [n_D B][dz] and [n_D B] (the generator's batch);
+ *   img_buff:       fp32 [n_D B][img][img][3], read then replaced;
+ *   lab_buff:       [n_D B], read then replaced;
+ *   pred_buff:      fp32 [n_D B], written.
+ * losses_host: n_D + 1 floats (L_D per D step, then L_G against the
+ * snapshot).  Both streams are idle when the call returns, also on error;
+ * PARAGAN_ENONFINITE (after finishing the iteration) if a loss is not
+ * finite.  ws: paragan_async_ws_size() bytes, 256-byte aligned.
+ * ------------------------------------------------------------------- */
+typedef struct {
+  const float* const* x_real;
+  const int32_t* const* y_real;
+  const float* z;
+  const int32_t* y;
+  float* img_buff;
+  int32_t* lab_buff;
+  float* pred_buff;
+} paragan_async_inputs;
+
+int paragan_async_ws_size(const paragan_biggan_desc* d, int32_t n_D, size_t* ws_bytes);
+int paragan_async_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
+                       paragan_net_state* G, paragan_net_state* D,
+                       const paragan_async_inputs* in, int32_t n_D, void* ws,
+                       float* losses_host);
+
+/* ---------------------------------------------------------------------
  * Launch profiler (instrumentation for the roofline report).  When enabled,
  * every convolution, weight-gradient and attention launch on the context's
  * stream is bracketed by a HIP event pair and tagged with its kernel

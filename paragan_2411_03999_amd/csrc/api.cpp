@@ -597,6 +597,37 @@ extern "C" int paragan_train_step(paragan_ctx* ctx, const paragan_biggan_desc* d
   return finish_losses(ctx, losses_host, n_D + 1, "train_step");
 }
 
+extern "C" int paragan_async_ws_size(const paragan_biggan_desc* d, int32_t n_D, size_t* ws_bytes) {
+  PG_TRY(nullptr, {
+    check_arch(d);
+    need(ws_bytes, "ws_bytes");
+    PG_CHECK(n_D >= 1 && n_D <= 63, "async_ws_size: n_D must be in [1, 63]");
+    *ws_bytes = async_step_ws(d, n_D, device_cus());
+  })
+}
+
+extern "C" int paragan_async_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G,
+                                  paragan_net_state* D, const paragan_async_inputs* in, int32_t n_D, void* ws,
+                                  float* losses_host) {
+  if (!ctx) return PARAGAN_EINVAL;
+  ProfBind pb(ctx);
+  PG_STEP_TRY(ctx, {
+    check_arch(d);
+    need_state(G, "G");
+    need_state(D, "D");
+    need(in, "inputs"); need(ws, "ws"); need(losses_host, "losses_host");
+    aligned(ws, "ws");
+    PG_CHECK(n_D >= 1 && n_D <= 63, "async_step: n_D must be in [1, 63]");
+    PG_CHECK((int64_t)n_D * d->B * d->img * d->img < (1LL << 31), "async_step: generator batch n_D * B too large");
+    need(in->x_real, "x_real"); need(in->y_real, "y_real");
+    for (int k = 0; k < n_D; ++k) { need(in->x_real[k], "x_real[k]"); need(in->y_real[k], "y_real[k]"); }
+    need(in->z, "z"); need(in->y, "y");
+    need(in->img_buff, "img_buff"); need(in->lab_buff, "lab_buff"); need(in->pred_buff, "pred_buff");
+    async_step(ctx, d, G, D, in, n_D, ws, losses_host);
+  })
+  return finish_losses(ctx, losses_host, n_D + 1, "async_step");
+}
+
 // ------------------------------------------------------------ profiler
 extern "C" int paragan_profile(paragan_ctx* ctx, int enable) {
   if (!ctx) return PARAGAN_EINVAL;

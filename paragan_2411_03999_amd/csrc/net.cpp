@@ -650,4 +650,133 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
   }
 }
 
+// =================================================================== async
+// The asynchronous update scheme (Numerical Optimizations, "Asynchronous
+// Update Scheme"): within one iteration the generator step runs against a
+// snapshot of the discriminator taken at the iteration's start, on the
+// context's second stream, while the n_D discriminator steps run on the
+// caller's stream on the previous iteration's generator samples (img_buff,
+// one iteration stale).  The two sides share no state until the join at the
+// end, where this iteration's samples replace img_buff.
+struct AsyncWs {
+  void *gsaved, *ssaved, *dsaved;     // G (batch n_D B), the snapshot D (n_D B), the stepping D (2B)
+  float *snap_p, *snap_u;             // the snapshot's parameters and SN vectors
+  float *gimg, *glog, *gdout, *gdimg, *gloss;
+  float *dimg, *dlog, *ddout, *dloss;
+  int32_t* dlab;
+  void *gnet, *dnet;
+  size_t gnet_bytes, dnet_bytes;
+};
+
+template <typename Net>
+static void* carve_saved(Arena& w, Net& net) {
+  Arena s(w.base ? w.base + w.off : nullptr);
+  net.plan_saved(s);
+  return w.bytes(s.off);
+}
+
+static AsyncWs async_carve(const Arch& a, int B, int n_D, Arena& w, GNet& g, DNet& ds, DNet& d2, int n_cu) {
+  AsyncWs r;
+  const int BG = n_D * B;
+  const int64_t pix = (int64_t)a.img * a.img;
+  r.gsaved = carve_saved(w, g);
+  r.ssaved = carve_saved(w, ds);
+  r.dsaved = carve_saved(w, d2);
+  const Layout LD = d_layout(a);
+  r.snap_p = w.f32(LD.n_params);
+  r.snap_u = w.f32(std::max<int64_t>(LD.n_u, 1));
+  r.gimg = w.f32((size_t)BG * pix * 3);
+  r.glog = w.f32(BG);
+  r.gdout = w.f32(BG);
+  r.gdimg = w.f32((size_t)BG * pix * 4);
+  r.gloss = w.f32(64);
+  r.dimg = w.f32((size_t)2 * B * pix * 3);
+  r.dlab = (int32_t*)w.bytes((size_t)2 * B * 4);
+  r.dlog = w.f32(2 * B);
+  r.ddout = w.f32(2 * B);
+  r.dloss = w.f32(64);
+  r.gnet_bytes = std::max(g.ws_size(n_cu), ds.ws_size(n_cu));
+  r.gnet = w.bytes(r.gnet_bytes);
+  r.dnet_bytes = d2.ws_size(n_cu);
+  r.dnet = w.bytes(r.dnet_bytes);
+  return r;
+}
+
+size_t async_step_ws(const paragan_biggan_desc* d, int n_D, int n_cu) {
+  const Arch a = arch_from(d);
+  GNet g(a, n_D * d->B);
+  DNet ds(a, n_D * d->B), d2(a, 2 * d->B);
+  Arena w(nullptr);
+  async_carve(a, d->B, n_D, w, g, ds, d2, n_cu);
+  return w.off;
+}
+
+void async_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
+                const paragan_async_inputs* in, int n_D, void* ws, float* losses_host) {
+  const Arch a = arch_from(d);
+  const int B = d->B, BG = n_D * B;
+  GNet g(a, BG);
+  DNet ds(a, BG), d2(a, 2 * B);
+  Arena w(ws);
+  const AsyncWs r = async_carve(a, B, n_D, w, g, ds, d2, ctx->n_cu);
+  hipStream_t st = ctx->stream;
+  if (!ctx->side) {
+    PG_HIP(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking));
+    for (hipEvent_t& e : ctx->ev) PG_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+  }
+  hipStream_t sg = ctx->side;
+  const Layout LG = g_layout(a), LD = d_layout(a);
+  const Params PG{&LG, "", G->params, G->u, G->grads};
+  const Params PD{&LD, "", D->params, D->u, D->grads};
+  const Params PS{&LD, "", r.snap_p, r.snap_u, nullptr};
+  const int64_t pix = (int64_t)a.img * a.img;
+  try {
+    // the snapshot of D at the start of the iteration
+    PG_HIP(hipMemcpyAsync(r.snap_p, D->params, (size_t)LD.n_params * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(r.snap_u, D->u, (size_t)LD.n_u * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipEventRecord(ctx->ev[0], st));
+    PG_HIP(hipStreamWaitEvent(sg, ctx->ev[0], 0));
+    // generator side: samples, the snapshot's predictions (pred_buff),
+    // L_G, the input gradient through the snapshot, G's backward and step
+    const Exec eg{sg, ctx->n_cu, r.gnet, r.gnet_bytes};
+    g.fwd(eg, PG, in->z, in->y, r.gimg);
+    ds.fwd(eg, PS, r.gimg, in->y, r.glog);
+    hinge(sg, r.glog, 0, BG, true, r.gdout, r.gloss);
+    ds.bwd(eg, PS, in->y, r.gdout, r.gdimg, false);
+    g.bwd(eg, PG, in->z, in->y, r.gdimg, 4);
+    G->opt_t += 1;
+    optim_step(sg, d->opt_g.kind, G->params, G->grads, G->opt_m, G->opt_v, LG.n_params, d->opt_g.beta1,
+               d->opt_g.beta2, d->opt_g.lr, d->opt_g.eps, G->opt_t);
+    PG_HIP(hipEventRecord(ctx->ev[1], sg));
+    // discriminator side: step k on B real images and the k-th B of the
+    // previous iteration's samples
+    const Exec ed{st, ctx->n_cu, r.dnet, r.dnet_bytes};
+    for (int k = 0; k < n_D; ++k) {
+      PG_HIP(hipMemcpyAsync(r.dimg, in->x_real[k], (size_t)B * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
+      PG_HIP(hipMemcpyAsync(r.dimg + (size_t)B * pix * 3, in->img_buff + (size_t)k * B * pix * 3,
+                            (size_t)B * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
+      PG_HIP(hipMemcpyAsync(r.dlab, in->y_real[k], (size_t)B * 4, hipMemcpyDeviceToDevice, st));
+      PG_HIP(hipMemcpyAsync(r.dlab + B, in->lab_buff + (size_t)k * B, (size_t)B * 4, hipMemcpyDeviceToDevice, st));
+      d2.fwd(ed, PD, r.dimg, r.dlab, r.dlog);
+      hinge(st, r.dlog, B, B, false, r.ddout, r.dloss + k);
+      d2.bwd(ed, PD, r.dlab, r.ddout, nullptr, true);
+      D->opt_t += 1;
+      optim_step(st, d->opt_d.kind, D->params, D->grads, D->opt_m, D->opt_v, LD.n_params, d->opt_d.beta1,
+                 d->opt_d.beta2, d->opt_d.lr, d->opt_d.eps, D->opt_t);
+    }
+    // join, then this iteration's samples become the next one's img_buff
+    PG_HIP(hipStreamWaitEvent(st, ctx->ev[1], 0));
+    PG_HIP(hipMemcpyAsync(in->img_buff, r.gimg, (size_t)BG * pix * 3 * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(in->lab_buff, in->y, (size_t)BG * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(in->pred_buff, r.glog, (size_t)BG * 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(r.dloss + n_D, r.gloss, 4, hipMemcpyDeviceToDevice, st));
+    PG_HIP(hipMemcpyAsync(losses_host, r.dloss, (size_t)(n_D + 1) * 4, hipMemcpyDeviceToHost, st));
+    PG_HIP(hipStreamSynchronize(st));
+  } catch (...) {
+    (void)hipStreamSynchronize(sg);
+    (void)hipStreamSynchronize(st);
+    throw;
+  }
+}
+
 }  // namespace pg

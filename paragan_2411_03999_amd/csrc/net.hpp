@@ -113,6 +113,9 @@ void d_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* D
             const int32_t* y_real, const float* x_fake, const int32_t* y_fake, void* ws, float* loss_host);
 void g_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
             const float* z, const int32_t* y, void* ws, float* loss_host);
+size_t async_step_ws(const paragan_biggan_desc* d, int n_D, int n_cu);
+void async_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
+                const paragan_async_inputs* in, int n_D, void* ws, float* losses_host);
 void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
                 const paragan_step_inputs* in, int n_D, void* ws, float* losses_host);
 

@@ -75,6 +75,12 @@ class StepInputs(C.Structure):
                 ("z_g", C.c_void_p), ("y_g", C.c_void_p)]
 
 
+class AsyncInputs(C.Structure):
+    _fields_ = [("x_real", C.POINTER(C.c_void_p)), ("y_real", C.POINTER(C.c_void_p)),
+                ("z", C.c_void_p), ("y", C.c_void_p), ("img_buff", C.c_void_p),
+                ("lab_buff", C.c_void_p), ("pred_buff", C.c_void_p)]
+
+
 class KernelStat(C.Structure):
     _fields_ = [("name", C.c_char * 64), ("launches", C.c_int64), ("total_ms", C.c_double),
                 ("flops", C.c_double)]
@@ -124,6 +130,8 @@ _SIGS = {
     "paragan_g_sample": (C.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "paragan_d_step": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "paragan_g_step": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
+    "paragan_async_ws_size": (C.c_int, [_P, C.c_int32, C.POINTER(C.c_size_t)]),
+    "paragan_async_step": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, _P]),
 }
 
 _lib = None
@@ -352,6 +360,18 @@ def paragan_d_step(ctx, desc, D, x_real, y_real, x_fake, y_fake, ws, loss):
 def paragan_g_step(ctx, desc, G, D, z, y, ws, loss):
     """loss: ctypes float array (1).  Returns the status."""
     return load().paragan_g_step(ctx.h, C.byref(desc), C.byref(G), C.byref(D), _ptr(z), _ptr(y), _ptr(ws), loss)
+
+
+def paragan_async_ws_size(desc, n_D):
+    n = C.c_size_t()
+    _check_static(load().paragan_async_ws_size(C.byref(desc), int(n_D), C.byref(n)))
+    return n.value
+
+
+def paragan_async_step(ctx, desc, G, D, inputs, n_D, ws, losses):
+    """inputs: AsyncInputs; losses: ctypes float array (n_D+1).  Returns the status."""
+    return load().paragan_async_step(ctx.h, C.byref(desc), C.byref(G), C.byref(D), C.byref(inputs), n_D,
+                                     _ptr(ws), losses)
 
 
 def paragan_profile(ctx, enable):
