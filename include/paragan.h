@@ -98,6 +98,22 @@ int paragan_sn_check(int64_t rows, int64_t cols, int n_iter, float eps);
 int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t rows,
                           int64_t cols, float* u, float* v, float* sigma,
                           int n_iter, float eps, void* ws);
+/* For callers that cannot allocate device memory (code under stream
+ * capture, serving loops, harnesses that forbid hipMalloc): the same
+ * computation, with the same kernels and results, as paragan_sn_power_iter,
+ * but its scratch is a 4 MiB array the library holds on each device until
+ * the process ends (its address taken in paragan_create), so the caller
+ * passes no workspace and the call allocates nothing.  Every BigGAN-128 and
+ * BigGAN-512 SN weight fits (the largest needs about 1 MiB); a weight whose
+ * paragan_sn_ws_size() exceeds 4 MiB is rejected with PARAGAN_EINVAL before
+ * any work.  All calls on one device share that one array: calls that
+ * overlap on a device (two streams, two threads, two contexts) race and
+ * must be ordered by the caller.  The kernels write all scratch they read,
+ * so nothing has to be cleared between calls. */
+int paragan_sn_power_iter_noalloc(paragan_ctx* ctx, const float* W,
+                                  int64_t rows, int64_t cols, float* u,
+                                  float* v, float* sigma, int n_iter,
+                                  float eps);
 
 /* ---------------------------------------------------------------------
  * BigGAN generator residual block (spec block of the benchmark

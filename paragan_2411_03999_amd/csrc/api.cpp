@@ -49,10 +49,12 @@ int paragan_create(paragan_ctx** out, void* hip_stream) {
     PG_HIP(hipGetDeviceProperties(&p, dev));
     if (std::strncmp(p.gcnArchName, "gfx950", 6) != 0)
       throw Error{PARAGAN_EUNSUPPORTED, std::string("paragan needs gfx950, found ") + p.gcnArchName};
+    void* scr = sn_scratch_init(dev);
     auto* c = new paragan_ctx;
     c->stream = (hipStream_t)hip_stream;
     c->device = dev;
     c->n_cu = p.multiProcessorCount;
+    c->sn_scratch = scr;
     *out = c;
     return PARAGAN_OK;
   } catch (const Error& e) {
@@ -325,6 +327,22 @@ extern "C" int paragan_sn_power_iter(paragan_ctx* ctx, const float* W, int64_t r
     aligned(ws, "ws");
     sn_check(rows, cols, n_iter, eps);
     sn_power_iter(ctx->stream, W, rows, cols, u, v, sigma, n_iter, eps, ws);
+  })
+}
+
+extern "C" int paragan_sn_power_iter_noalloc(paragan_ctx* ctx, const float* W, int64_t rows, int64_t cols,
+                                             float* u, float* v, float* sigma, int n_iter, float eps) {
+  if (!ctx) return PARAGAN_EINVAL;
+  PG_TRY(ctx, {
+    need(W, "W"); need(u, "u"); need(v, "v"); need(sigma, "sigma");
+    sn_check(rows, cols, n_iter, eps);
+    const size_t want = sn_ws_bytes(rows, cols);
+    PG_CHECK(want <= kSnScratchBytes, "sn_power_iter_noalloc: a " + std::to_string(rows) + " x " +
+                                          std::to_string(cols) + " weight needs " + std::to_string(want) +
+                                          " bytes of scratch, more than the library's " +
+                                          std::to_string(kSnScratchBytes) + " (use paragan_sn_power_iter)");
+    PG_CHECK(ctx->sn_scratch != nullptr, "sn_power_iter_noalloc: context has no scratch address");
+    sn_power_iter(ctx->stream, W, rows, cols, u, v, sigma, n_iter, eps, ctx->sn_scratch);
   })
 }
 

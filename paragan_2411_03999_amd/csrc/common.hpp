@@ -161,6 +161,7 @@ struct paragan_ctx {
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
   int device = 0;
   int n_cu = 0;
+  void* sn_scratch = nullptr;   // the device's address of the library's SN scratch array
   std::string err;
   pg::Profiler prof;
 };

@@ -4,6 +4,8 @@
 // atomics), so results are bitwise reproducible run to run.
 #include "misc.hpp"
 
+#include <mutex>
+
 namespace pg {
 
 // ----------------------------------------------------- block reductions
@@ -258,6 +260,28 @@ void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, f
     hipLaunchKernelGGL(k_sng_u, dim3(n), dim3(1024), 0, st, g, eps);
   }
   PG_LAUNCH_CHECK();
+}
+
+// Scratch of the allocation-free SN entry point.  In host code `scratch`
+// names a host-side stand-in, not the array: its device address comes from
+// hipGetSymbolAddress, once per device (each device holds its own copy), and
+// only that address is ever handed to a kernel.  The kernels write every
+// byte of the scratch they read, so it needs no clearing between calls.
+static __device__ __align__(256) unsigned char scratch[kSnScratchBytes];
+constexpr int kScratchDevices = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[kScratchDevices] = {};
+
+void* sn_scratch_init(int device) {
+  PG_CHECK(device >= 0 && device < kScratchDevices, "sn scratch: device ordinal out of range");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[device]) {
+    void* p = nullptr;
+    PG_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    PG_CHECK(p != nullptr && ((uintptr_t)p & 255) == 0, "sn scratch: symbol address not 256-byte aligned");
+    g_scratch_ptr[device] = p;
+  }
+  return g_scratch_ptr[device];
 }
 
 void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, float* u, float* v,

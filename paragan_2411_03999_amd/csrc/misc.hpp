@@ -15,6 +15,11 @@ struct SnJob {
   float* u_save;        // optional copy of the final u
 };
 size_t sn_group_ws_bytes(const SnJob* jobs, int n);
+// The library's own SN scratch array (one per device, held until the
+// process ends) for callers that cannot allocate.  sn_scratch_init() runs
+// with `device` current and returns the array's device address there.
+constexpr size_t kSnScratchBytes = (size_t)4 << 20;
+void* sn_scratch_init(int device);
 void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws);
 // mode: kPackFwd [Np][R][R][Cp]; kPackDgrad [Cp][R][R][Np] flipped taps;
 // kPackPool4 [Np][4][4][Cp], the 3x3 filter (R = 3) convolved with the 2x2

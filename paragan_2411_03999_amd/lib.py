@@ -130,6 +130,7 @@ _SIGS = {
     "paragan_g_sample": (C.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "paragan_d_step": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "paragan_g_step": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
+    "paragan_sn_power_iter_noalloc": (C.c_int, [_P, _P, C.c_int64, C.c_int64, _P, _P, _P, C.c_int, C.c_float]),
     "paragan_async_ws_size": (C.c_int, [_P, C.c_int32, C.POINTER(C.c_size_t)]),
     "paragan_async_step": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, _P]),
 }
@@ -360,6 +361,13 @@ def paragan_d_step(ctx, desc, D, x_real, y_real, x_fake, y_fake, ws, loss):
 def paragan_g_step(ctx, desc, G, D, z, y, ws, loss):
     """loss: ctypes float array (1).  Returns the status."""
     return load().paragan_g_step(ctx.h, C.byref(desc), C.byref(G), C.byref(D), _ptr(z), _ptr(y), _ptr(ws), loss)
+
+
+def paragan_sn_power_iter_noalloc(ctx, W, rows, cols, u, v, sigma, n_iter, eps):
+    """As paragan_sn_power_iter, with the library's own scratch (no
+    workspace argument).  Returns the status."""
+    return load().paragan_sn_power_iter_noalloc(ctx.h, _ptr(W), rows, cols, _ptr(u), _ptr(v), _ptr(sigma), n_iter,
+                                                eps)
 
 
 def paragan_async_ws_size(desc, n_D):
