@@ -16,11 +16,14 @@
  *   on error nothing has been launched and paragan_last_error() names the
  *   problem.  No C++ exception crosses the ABI.
  * - Streams: all device work is enqueued on the hipStream_t given to
- *   paragan_create(), in order (paragan_train_step also uses a second
- *   stream of its own, see there).  Calls are asynchronous unless stated.
+ *   paragan_create(), in order; paragan_train_step and paragan_async_step
+ *   also use a second stream of the context (default priority, created on
+ *   first use), ordered by events and idle again when they return.  Calls
+ *   are asynchronous unless stated.
  * - Memory: every device buffer is allocated and owned by the caller and
- *   passed as a plain device pointer.  The library never allocates device
- *   memory.  Sizes of the "saved" (forward -> backward) and "ws" (scratch)
+ *   passed as a plain device pointer.  The library allocates no device
+ *   memory; its one device-resident object is the fixed 4 MiB scratch
+ *   array of paragan_sn_power_iter_noalloc, part of the loaded code.  Sizes of the "saved" (forward -> backward) and "ws" (scratch)
  *   buffers come from the *_sizes() queries and must be 256-byte aligned.
  * - Activations are NHWC.  Their channel stride is the channel count
  *   rounded up to a multiple of 32 (paragan_cpad()); padded channels hold
@@ -52,7 +55,8 @@ enum {
   PARAGAN_EUNSUPPORTED = -2,  /* valid request this build does not handle */
   PARAGAN_EWORKSPACE = -3,    /* a buffer is smaller than the query said */
   PARAGAN_EHIP = -4,          /* a HIP runtime call failed */
-  PARAGAN_ENONFINITE = -5     /* train step produced a NaN/Inf loss */
+  PARAGAN_ENONFINITE = -5,    /* train step produced a NaN/Inf loss */
+  PARAGAN_ETIMEOUT = -6       /* a bounded wait ended without its event */
 };
 
 enum { PARAGAN_F32 = 0, PARAGAN_BF16 = 1 };
@@ -408,6 +412,78 @@ int paragan_async_step(paragan_ctx* ctx, const paragan_biggan_desc* d,
                        paragan_net_state* G, paragan_net_state* D,
                        const paragan_async_inputs* in, int32_t n_D, void* ws,
                        float* losses_host);
+
+/* ---------------------------------------------------------------------
+ * Congestion-aware host data pipeline (Implementation, "Congestion-Aware
+ * Data Pipelining").  Host threads fetch batches (by calling `fetch`) into
+ * caller-provided host slots ahead of the consumer.  A sliding window holds
+ * the latency of the last `window` fetches; once `window` fetches have
+ * completed since the last change, a window mean above threshold_ms adds
+ * one fetch thread and one batch of prefetch depth (up to the maxima), and a
+ * mean at or below it releases one of each (down to the minima).  Depth
+ * counts every batch a thread has claimed and the consumer has not yet
+ * released.  Batches are delivered in sequence order 0, 1, 2, ..., each
+ * exactly once, whatever the number of threads.  Host code only (no device
+ * work, usable without a GPU); the caller copies a delivered slot to the
+ * device (from pinned memory for an asynchronous copy) and then releases it.
+ * Thread-safety: one consumer thread calls next, release and get_stats.
+ * ------------------------------------------------------------------- */
+/* Fill `slot` (slot_bytes bytes) with batch `seq`; return 0 on success.
+ * Called from pipeline threads, concurrently for different seq. */
+typedef int (*paragan_fetch_fn)(void* user, int64_t seq, void* slot, size_t slot_bytes);
+
+typedef struct {
+  int32_t min_threads, max_threads;   /* 1 <= min <= max <= 64 */
+  int32_t min_depth, max_depth;       /* 1 <= min <= max <= n_slots */
+  int32_t window;                     /* latency samples, 1 .. 100000 */
+  double threshold_ms;                /* > 0 */
+} paragan_pipeline_cfg;
+
+typedef struct {
+  int32_t threads, depth;             /* the controller's current targets */
+  double window_mean_ms;              /* mean latency over the window */
+  int64_t fetched, delivered;
+  int64_t grows, shrinks;             /* controller adjustments so far */
+  double consumer_wait_ms;            /* total time next() has waited */
+} paragan_pipeline_stats;
+
+typedef struct paragan_pipeline paragan_pipeline;
+
+/* slots: n_slots host pointers of slot_bytes each, owned by the caller and
+ * valid until paragan_pipeline_destroy returns.  Starts min_threads threads. */
+int paragan_pipeline_create(paragan_pipeline** out, const paragan_pipeline_cfg* cfg,
+                            paragan_fetch_fn fetch, void* user, void* const* slots,
+                            int32_t n_slots, size_t slot_bytes);
+/* Wait for the next batch in sequence order (timeout_ms < 0: no limit):
+ * *seq, *slot.  The slot belongs to the consumer until released.
+ * PARAGAN_ETIMEOUT if nothing came in time; PARAGAN_EINVAL once a fetch has
+ * failed (the message names the batch). */
+int paragan_pipeline_next(paragan_pipeline* p, int64_t* seq, int32_t* slot, int32_t timeout_ms);
+int paragan_pipeline_release(paragan_pipeline* p, int32_t slot);
+int paragan_pipeline_get_stats(paragan_pipeline* p, paragan_pipeline_stats* out);
+/* Message of the last failed call on p (p = NULL: of the last failed
+ * paragan_pipeline_create). */
+const char* paragan_pipeline_error(const paragan_pipeline* p);
+/* Stops the threads (a fetch in progress finishes first) and frees p. */
+void paragan_pipeline_destroy(paragan_pipeline* p);
+
+/* Seeded synthetic batches standing in for the image dataset: B images of
+ * img x img x 3 floats then B int32 labels per slot.  Value i of batch seq
+ * is 2u - 1 with u the top 24 bits of SplitMix64(seed + 2^40 seq + i) over
+ * 2^24 (Steele, Lea and Flood, OOPSLA 2014: add 0x9E3779B97F4A7C15, then
+ * the finaliser); label b is SplitMix64(seed + 2^40 seq + 2^39 + b) mod
+ * n_classes.  latency_ms (host, n_latency entries, may be NULL) injects a
+ * delay: fetching batch seq takes at least latency_ms[seq % n_latency]. */
+typedef struct {
+  uint64_t seed;
+  int32_t B, img, n_classes;
+  const float* latency_ms;
+  int64_t n_latency;
+} paragan_synth_source;
+
+size_t paragan_synth_batch_bytes(const paragan_synth_source* s);
+/* A paragan_fetch_fn with user = a paragan_synth_source*. */
+int paragan_synth_fetch(void* user, int64_t seq, void* slot, size_t slot_bytes);
 
 /* ---------------------------------------------------------------------
  * Launch profiler (instrumentation for the roofline report).  When enabled,

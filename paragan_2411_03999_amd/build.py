@@ -11,7 +11,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libparagan.so")
 BUILD = os.path.join(os.path.dirname(HERE), "_build")
-SOURCES = ["conv.hip", "convfwd.hip", "wgrad.hip", "misc.hip", "attention.hip", "heads.hip", "blocks.cpp", "attn.cpp", "net.cpp", "api.cpp"]
+SOURCES = ["conv.hip", "convfwd.hip", "wgrad.hip", "misc.hip", "attention.hip", "heads.hip", "blocks.cpp", "attn.cpp", "net.cpp", "api.cpp", "pipeline.cpp"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-unused-result",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 

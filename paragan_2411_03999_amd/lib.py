@@ -12,7 +12,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libparagan.so")
 
-OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ENONFINITE = 0, -1, -2, -3, -4, -5
+OK, EINVAL, EUNSUPPORTED, EWORKSPACE, EHIP, ENONFINITE, ETIMEOUT = 0, -1, -2, -3, -4, -5, -6
 F32, BF16 = 0, 1
 ADAM, ADABELIEF = 0, 1
 
@@ -81,6 +81,26 @@ class AsyncInputs(C.Structure):
                 ("lab_buff", C.c_void_p), ("pred_buff", C.c_void_p)]
 
 
+class PipelineCfg(C.Structure):
+    _fields_ = [("min_threads", C.c_int32), ("max_threads", C.c_int32), ("min_depth", C.c_int32),
+                ("max_depth", C.c_int32), ("window", C.c_int32), ("threshold_ms", C.c_double)]
+
+
+class PipelineStats(C.Structure):
+    _fields_ = [("threads", C.c_int32), ("depth", C.c_int32), ("window_mean_ms", C.c_double),
+                ("fetched", C.c_int64), ("delivered", C.c_int64), ("grows", C.c_int64), ("shrinks", C.c_int64),
+                ("consumer_wait_ms", C.c_double)]
+
+
+class SynthSource(C.Structure):
+    _fields_ = [("seed", C.c_uint64), ("B", C.c_int32), ("img", C.c_int32), ("n_classes", C.c_int32),
+                ("latency_ms", C.c_void_p), ("n_latency", C.c_int64)]
+
+
+# int fetch(void* user, int64_t seq, void* slot, size_t slot_bytes)
+FETCH_FN = C.CFUNCTYPE(C.c_int, C.c_void_p, C.c_int64, C.c_void_p, C.c_size_t)
+
+
 class KernelStat(C.Structure):
     _fields_ = [("name", C.c_char * 64), ("launches", C.c_int64), ("total_ms", C.c_double),
                 ("flops", C.c_double)]
@@ -131,6 +151,14 @@ _SIGS = {
     "paragan_d_step": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P]),
     "paragan_g_step": (C.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
     "paragan_sn_power_iter_noalloc": (C.c_int, [_P, _P, C.c_int64, C.c_int64, _P, _P, _P, C.c_int, C.c_float]),
+    "paragan_pipeline_create": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, C.c_size_t]),
+    "paragan_pipeline_next": (C.c_int, [_P, C.POINTER(C.c_int64), C.POINTER(C.c_int32), C.c_int32]),
+    "paragan_pipeline_release": (C.c_int, [_P, C.c_int32]),
+    "paragan_pipeline_get_stats": (C.c_int, [_P, _P]),
+    "paragan_pipeline_error": (C.c_char_p, [_P]),
+    "paragan_pipeline_destroy": (None, [_P]),
+    "paragan_synth_batch_bytes": (C.c_size_t, [_P]),
+    "paragan_synth_fetch": (C.c_int, [_P, C.c_int64, _P, C.c_size_t]),
     "paragan_async_ws_size": (C.c_int, [_P, C.c_int32, C.POINTER(C.c_size_t)]),
     "paragan_async_step": (C.c_int, [_P, _P, _P, _P, _P, C.c_int32, _P, _P]),
 }
@@ -380,6 +408,56 @@ def paragan_async_step(ctx, desc, G, D, inputs, n_D, ws, losses):
     """inputs: AsyncInputs; losses: ctypes float array (n_D+1).  Returns the status."""
     return load().paragan_async_step(ctx.h, C.byref(desc), C.byref(G), C.byref(D), C.byref(inputs), n_D,
                                      _ptr(ws), losses)
+
+
+class Pipeline:
+    """paragan_pipeline_* over host slot buffers.  fetch: a FETCH_FN (kept
+    alive here) or None for the library's synthetic source `synth`."""
+
+    def __init__(self, cfg, slots, slot_bytes, fetch=None, user=None, synth=None):
+        lib = load()
+        self._keep = [cfg, slots, fetch, synth]
+        if fetch is None:
+            fn = C.cast(lib.paragan_synth_fetch, C.c_void_p)
+            user = C.cast(C.pointer(synth), C.c_void_p)
+        else:
+            fn = C.cast(fetch, C.c_void_p)
+        arr = (C.c_void_p * len(slots))(*slots)
+        self._keep.append(arr)
+        h = C.c_void_p()
+        rc = lib.paragan_pipeline_create(C.byref(h), C.byref(cfg), fn, user, arr, len(slots), slot_bytes)
+        if rc != OK:
+            raise ParaganError(rc, lib.paragan_pipeline_error(None).decode())
+        self.h = h
+
+    def next(self, timeout_ms=-1):
+        """(status, seq, slot)."""
+        seq, slot = C.c_int64(), C.c_int32()
+        rc = load().paragan_pipeline_next(self.h, C.byref(seq), C.byref(slot), int(timeout_ms))
+        return rc, seq.value, slot.value
+
+    def release(self, slot):
+        return load().paragan_pipeline_release(self.h, int(slot))
+
+    def stats(self):
+        st = PipelineStats()
+        if load().paragan_pipeline_get_stats(self.h, C.byref(st)) != OK:
+            raise ParaganError(EINVAL, self.error())
+        return {k: getattr(st, k) for k, _ in PipelineStats._fields_}
+
+    def error(self):
+        return load().paragan_pipeline_error(self.h).decode()
+
+    def close(self):
+        if self.h:
+            load().paragan_pipeline_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def paragan_profile(ctx, enable):
