@@ -3,10 +3,11 @@
 
 One step = one paragan_train_step call: n_D = 2 discriminator updates on
 concat(real, fake) batches of 2 x 256 images and one generator update on
-256 images (hinge loss, Adam), the configuration the paper trains BigGAN
-with at 2048 images per step over 8 accelerators (Evaluation, Table
-tab:abl_study).  images/sec = batch x steps / seconds (the generator batch,
-one step per generator update).
+256 images (hinge loss; AdaBelief for G, Adam for D, the paper's asymmetric
+policy), the configuration the paper trains BigGAN with at 2048 images per
+step over 8 accelerators (Evaluation, Table tab:abl_study).  images/sec =
+batch x steps / seconds (the generator batch, one step per generator
+update).
 
 Inputs are synthetic and seeded (real images uniform in [-1, 1], z ~ N(0, 1),
 labels uniform over 1000 classes), generated on the GPU and resident in HBM
@@ -20,7 +21,12 @@ The JSON line also carries:
                 the bf16 dense MFMA peak;
   conv_mfma     all implicit-GEMM convolution launches together;
   cpu_baseline  the float64 CPU oracle timed on this host on a bounded
-                sample (one train step at batch 1 on the same architecture).
+                sample (one train step at batch 1 on the same architecture);
+  extras        the other workloads, each timed the same way after the main
+                one: the BigGAN-128 discriminator step on 32 real + 32 fake
+                images (paragan_d_step), the asynchronous update scheme at
+                B = 256, n_D = 2 (generator batch 512, paragan_async_step),
+                and the BigGAN-512 train step at batch 16, n_D = 2.
 """
 import argparse
 import json
@@ -150,6 +156,106 @@ def device_net(torch, lib, ents, npar, nu, gen):
     return dict(P=P, U=U, G=G, M=M, V=V, state=st)
 
 
+def timed(torch, fn, steps, warmup):
+    """Milliseconds per call of fn over `steps` calls after `warmup`, on the
+    device clock, bracketed by synchronisations."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
+def extras(torch, lib, C, ctx, gen, Dn, real, labels, steps=5):
+    """The discriminator step (32 + 32), the asynchronous iteration and the
+    BigGAN-512 step; each from its own seeded state."""
+    out = {}
+    # BigGAN-128 D step on 32 real + 32 fake images
+    d32 = make_desc(lib, "biggan128", 32)
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d32))
+    xr, xf = real[0][:32].contiguous(), real[1][:32].contiguous()
+    yr, yf = labels[0][:32].contiguous(), labels[1][:32].contiguous()
+    loss = (C.c_float * 1)()
+
+    def dstep():
+        ctx.check(lib.paragan_d_step(ctx, d32, Dn["state"], xr, yr, xf, yf, ws, loss))
+    ms = timed(torch, dstep, 4 * steps, 2)
+    out["d_step_32_32"] = {"workload": "BigGAN-128 discriminator step, 32 real + 32 fake images",
+                           "ms_per_step": ms, "images_per_sec": 64 / (ms / 1e3)}
+    del ws
+    # the asynchronous update scheme at B = 256, n_D = 2 (generator batch 512)
+    B, n_D = 256, 2
+    d = make_desc(lib, "biggan128", B)
+    gents, gn, gnu = lib.paragan_net_layout(d, 0)
+    dents, dn, dnu = lib.paragan_net_layout(d, 1)
+    Ga = device_net(torch, lib, gents, gn, gnu, gen)
+    Da = device_net(torch, lib, dents, dn, dnu, gen)
+    z = torch.randn((n_D * B, d.dz), device="cuda", generator=gen)
+    y = torch.randint(0, d.n_classes, (n_D * B,), device="cuda", generator=gen, dtype=torch.int32)
+    img = torch.rand((n_D * B, d.img, d.img, 3), device="cuda", generator=gen) * 2 - 1
+    lab = torch.randint(0, d.n_classes, (n_D * B,), device="cuda", generator=gen, dtype=torch.int32)
+    pred = torch.empty(n_D * B, device="cuda")
+    arr = lambda lst: (C.c_void_p * n_D)(*[t.data_ptr() for t in lst])
+    inp = lib.AsyncInputs(arr(real[:n_D]), arr(labels[:n_D]), z.data_ptr(), y.data_ptr(), img.data_ptr(),
+                          lab.data_ptr(), pred.data_ptr())
+    ws = lib.workspace(lib.paragan_async_ws_size(d, n_D))
+    losses = (C.c_float * (n_D + 1))()
+
+    def astep():
+        ctx.check(lib.paragan_async_step(ctx, d, Ga["state"], Da["state"], inp, n_D, ws, losses))
+    ms = timed(torch, astep, steps, 1)
+    out["async"] = {"workload": "BigGAN-128 asynchronous iteration: G step on 512 images against a D snapshot "
+                                "(second stream) beside 2 D steps of 256 + 256 on the previous samples",
+                    "ms_per_iteration": ms, "g_images_per_sec": n_D * B / (ms / 1e3),
+                    "d_images_per_sec": 2 * n_D * B / (ms / 1e3)}
+    del ws, Ga, Da, img
+    torch.cuda.empty_cache()
+    # BigGAN-512 train step at batch 16, n_D = 2
+    B = 16
+    d = make_desc(lib, "biggan512", B)
+    gents, gn, gnu = lib.paragan_net_layout(d, 0)
+    dents, dn, dnu = lib.paragan_net_layout(d, 1)
+    G5 = device_net(torch, lib, gents, gn, gnu, gen)
+    D5 = device_net(torch, lib, dents, dn, dnu, gen)
+    keep = [torch.rand((B, d.img, d.img, 3), device="cuda", generator=gen) * 2 - 1 for _ in range(n_D)]
+    keep += [torch.randint(0, d.n_classes, (B,), device="cuda", generator=gen, dtype=torch.int32)
+             for _ in range(n_D)]
+    keep += [torch.randn((B, d.dz), device="cuda", generator=gen) for _ in range(n_D)]
+    keep += [torch.randint(0, d.n_classes, (B,), device="cuda", generator=gen, dtype=torch.int32)
+             for _ in range(n_D)]
+    keep += [torch.randn((B, d.dz), device="cuda", generator=gen),
+             torch.randint(0, d.n_classes, (B,), device="cuda", generator=gen, dtype=torch.int32)]
+    ptr = [t.data_ptr() for t in keep]
+    arr = lambda lst: (C.c_void_p * n_D)(*lst)
+    inp5 = lib.StepInputs(arr(ptr[0:n_D]), arr(ptr[n_D:2 * n_D]), arr(ptr[2 * n_D:3 * n_D]),
+                          arr(ptr[3 * n_D:4 * n_D]), ptr[4 * n_D], ptr[4 * n_D + 1])
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+
+    def step5():
+        ctx.check(lib.paragan_train_step(ctx, d, G5["state"], D5["state"], inp5, n_D, ws, losses))
+    ms = timed(torch, step5, steps, 1)
+    out["biggan512"] = {"workload": "BigGAN-512 G+D train step, batch 16, 2 D steps per G step",
+                        "ms_per_step": ms, "images_per_sec": B / (ms / 1e3)}
+    return out
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(arch, B=1, n_D=2):
     """Time the oracle (float64 numpy) on one train step at batch B."""
     import numpy as np
@@ -174,6 +280,7 @@ def cpu_baseline(arch, B=1, n_D=2):
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": B / dt, "unit": "images/sec", "cores": int(threads), "kind": "oracle",
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count(),
             "sample": "one %s G+D train step (n_D=%d) at batch %d, float64 numpy, %.1f s; finite losses: %s"
                       % (arch, n_D, B, dt, bool(np.all(np.isfinite(losses))))}
 
@@ -188,6 +295,7 @@ def main():
     ap.add_argument("--arch", default="biggan128", choices=sorted(ARCHS))
     ap.add_argument("--seed", type=int, default=1004)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="skip the D-step, async and BigGAN-512 timings")
     ap.add_argument("--cpu-batch", type=int, default=1)
     ap.add_argument("--kernels-out", default=None, help="write the per-kernel table (JSON) here")
     ap.add_argument("--copy-probe", action="store_true",
@@ -323,6 +431,12 @@ def main():
                   model_tf / PEAK_BF16_TFLOPS, "conv_gflop_per_image": conv_per_img / 1e9,
                   "conv_tflops": conv_model_tf, "conv_frac_of_peak": conv_model_tf / PEAK_BF16_TFLOPS},
     }
+    if not args.no_extras and args.arch == "biggan128" and B >= 32 and n_D >= 2:
+        print("bench: timing the extra workloads ...", file=sys.stderr, flush=True)
+        del ws
+        torch.cuda.empty_cache()
+        out["extras"] = extras(torch, lib, C, ctx, gen, Dn, keep[0:n_D], keep[n_D:2 * n_D])
+        print("bench: extras %s" % json.dumps(out["extras"]), file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle sample ...", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(args.arch, B=args.cpu_batch, n_D=n_D)
