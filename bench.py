@@ -20,6 +20,12 @@ The JSON line also carries:
                 algorithmic FLOPs (real channels) / its launch time, against
                 the bf16 dense MFMA peak;
   conv_mfma     all implicit-GEMM convolution launches together;
+  bandwidth     the bandwidth-bound kernel families (SN power iteration
+                and backward, weight packing, BN statistics / apply /
+                backward, column sums, pooling, optimisers): algorithmic
+                bytes / launch time against the 8 TB/s HBM peak (the SN and
+                packing launches run on the second stream beside the
+                convolutions, so theirs include waiting for CUs);
   cpu_baseline  the float64 CPU oracle timed on this host on a bounded
                 sample (one train step at batch 1 on the same architecture);
   extras        the other workloads, each timed the same way after the main
@@ -39,6 +45,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA (published)
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E (published)
 
 # HBM bytes per launch of a kernel, from two rocprofv3 --pmc passes over
 # "bench.py --steps 1 --warmup 1 --no-cpu-baseline --copy-probe" (FETCH_SIZE,
@@ -381,20 +388,29 @@ def main():
           file=sys.stderr, flush=True)
 
     stats.sort(key=lambda s: -s["total_ms"])
-    dom = stats[0]
+    # the dominant kernel: most time among the MFMA (FLOP-tagged) launches
+    dom = next(s for s in stats if s["flops"] > 0)
     achieved = dom["flops"] / (dom["total_ms"] / 1e3) / 1e12
     conv = [s for s in stats if s["name"].startswith(("k_conv_", "k_wgrad_")) and s["flops"] > 0
             and "simt" not in s["name"]]
     conv_ms = sum(s["total_ms"] for s in conv)
     conv_tf = sum(s["flops"] for s in conv) / (conv_ms / 1e3) / 1e12 if conv_ms else 0.0
     all_ms = sum(s["total_ms"] for s in stats)
+    bw = {}
+    for s in stats:
+        if s.get("bytes", 0) > 0:
+            gbs = s["bytes"] / (s["total_ms"] / 1e3) / 1e9
+            bw[s["name"]] = {"GB_per_s": gbs, "frac_of_hbm": gbs / PEAK_HBM_GBS,
+                             "ms_per_step": s["total_ms"] / args.steps, "launches_per_step": s["launches"] / args.steps,
+                             "bytes_per_launch": s["bytes"] / s["launches"]}
     if args.kernels_out:
         with open(args.kernels_out, "w") as f:
             json.dump(stats, f, indent=1)
-    for s in stats[:(60 if args.detail else 12)]:
-        print("bench: %-62s %6d launches %9.2f ms %8.1f TFLOP/s" % (
-            s["name"], s["launches"], s["total_ms"], s["flops"] / max(s["total_ms"], 1e-9) / 1e9),
-            file=sys.stderr)
+    for s in stats[:(60 if args.detail else 16)]:
+        rate = ("%8.1f TFLOP/s" % (s["flops"] / max(s["total_ms"], 1e-9) / 1e9) if s["flops"] > 0 else
+                "%8.1f GB/s" % (s.get("bytes", 0) / max(s["total_ms"], 1e-9) / 1e6))
+        print("bench: %-62s %6d launches %9.2f ms %s" % (s["name"], s["launches"], s["total_ms"], rate),
+              file=sys.stderr)
     # model FLOPs of one step per image: G fwd in each D step and in the G
     # step, G bwd (2x fwd); D fwd+bwd on 2 images per D step, D fwd + input
     # gradient (1x fwd) in the G step
@@ -427,6 +443,7 @@ def main():
         "conv_mfma": {"achieved": conv_tf, "unit": "TFLOP/s", "frac_of_peak": conv_tf / PEAK_BF16_TFLOPS,
                       "share_of_profiled_time": conv_ms / max(all_ms, 1e-9),
                       "flops": "executed (the folded pool / upsample filters do fewer MACs than the model)"},
+        "bandwidth": bw,
         "model": {"gflop_per_image": per_img / 1e9, "step_tflops": model_tf, "step_frac_of_peak":
                   model_tf / PEAK_BF16_TFLOPS, "conv_gflop_per_image": conv_per_img / 1e9,
                   "conv_tflops": conv_model_tf, "conv_frac_of_peak": conv_model_tf / PEAK_BF16_TFLOPS},

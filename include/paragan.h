@@ -487,9 +487,14 @@ int paragan_synth_fetch(void* user, int64_t seq, void* slot, size_t slot_bytes);
 
 /* ---------------------------------------------------------------------
  * Launch profiler (instrumentation for the roofline report).  When enabled,
- * every convolution, weight-gradient and attention launch on the context's
- * stream is bracketed by a HIP event pair and tagged with its kernel
- * template instance and algorithmic FLOPs (real, unpadded channels).
+ * every convolution, weight-gradient and attention launch is bracketed by a
+ * HIP event pair on the stream it runs on and tagged with its kernel
+ * template instance and algorithmic FLOPs (real, unpadded channels); the
+ * bandwidth-bound launches (SN power iteration and backward, weight packing,
+ * BN statistics / apply / backward, column sums, pooling, the optimisers)
+ * are tagged with their algorithmic HBM bytes instead.  Launches on the
+ * context's second stream overlap the first, so their times include waiting
+ * for CUs the other stream holds.
  * paragan_profile_read synchronises the stream, aggregates the records by
  * kernel name into `out` (up to `cap` entries; *count = number of kernels)
  * and clears them.  Off by default; costs two event records per launch.
@@ -503,6 +508,8 @@ typedef struct {
   int64_t launches;
   double total_ms;
   double flops;
+  double bytes;     /* algorithmic HBM bytes of the bandwidth-bound launches
+                       (SN, packing, BN, column sums, pooling, optimiser) */
 } paragan_kernel_stat;
 
 int paragan_profile(paragan_ctx* ctx, int enable);

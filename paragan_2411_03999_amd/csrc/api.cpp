@@ -674,6 +674,7 @@ extern "C" int paragan_profile_read(paragan_ctx* ctx, paragan_kernel_stat* out, 
       k->launches += 1;
       k->total_ms += ms;
       k->flops += r.flops;
+      k->bytes += r.bytes;
       ctx->prof.pool.push_back(r.a);
       ctx->prof.pool.push_back(r.b);
     }

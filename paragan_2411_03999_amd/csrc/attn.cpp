@@ -72,15 +72,24 @@ size_t Attn::ws_size(int n_cu) const {
 
 static const char* kASN[4] = {"theta", "phi", "g", "o"};
 
+void Attn::sn_jobs(const Params& P, std::vector<SnJob>& out) {
+  for (int i = 0; i < 4; ++i) out.push_back(sn_job(P, kASN[i], sn[i]));
+}
+
+void Attn::pack_jobs(const Params& P, std::vector<PackJob>& out) {
+  out.push_back({P.w("theta"), sn[0].sigma, wqkv, C / 8, C, 1, dk, Cp, kPackFwd});
+  out.push_back({P.w("phi"), sn[1].sigma, (char*)wqkv + (size_t)dk * Cp * 2, C / 8, C, 1, dk, Cp, kPackFwd});
+  out.push_back({P.w("g"), sn[2].sigma, (char*)wqkv + (size_t)2 * dk * Cp * 2, C / 2, C, 1, dv, Cp, kPackFwd});
+  out.push_back({P.w("o"), sn[3].sigma, wo, C, C / 2, 1, Cp, dv, kPackFwd});
+}
+
 void Attn::prep(hipStream_t st, const Params& P, void* sn_ws) {
-  SnJob jobs[4];
-  for (int i = 0; i < 4; ++i) jobs[i] = sn_job(P, kASN[i], sn[i]);
-  sn_power_iter_group(st, jobs, 4, npi, sn_eps, sn_ws);
-  const PackJob pk[4] = {{P.w("theta"), sn[0].sigma, wqkv, C / 8, C, 1, dk, Cp, kPackFwd},
-                         {P.w("phi"), sn[1].sigma, (char*)wqkv + (size_t)dk * Cp * 2, C / 8, C, 1, dk, Cp, kPackFwd},
-                         {P.w("g"), sn[2].sigma, (char*)wqkv + (size_t)2 * dk * Cp * 2, C / 2, C, 1, dv, Cp, kPackFwd},
-                         {P.w("o"), sn[3].sigma, wo, C, C / 2, 1, Cp, dv, kPackFwd}};
-  pack_group(st, false, pk, 4);
+  std::vector<SnJob> sj;
+  sn_jobs(P, sj);
+  sn_power_iter_all(st, sj.data(), (int)sj.size(), npi, sn_eps, sn_ws);
+  std::vector<PackJob> pk;
+  pack_jobs(P, pk);
+  pack_all(st, false, pk.data(), (int)pk.size());
 }
 
 void Attn::fwd(const Exec& ex, const Params& P, const void* x, void* y, bool for_bwd) {

@@ -193,30 +193,42 @@ size_t GBlock::ws_size(int n_cu) const {
 }
 
 // the data-gradient weight packs of a G block into (wd1, wd2, wdsc)
-static void g_pack_dgrad(const GBlock& g, hipStream_t st, const Params& P, void* wd1, void* wd2, void* wdsc) {
+static void g_pack_dgrad_jobs(const GBlock& g, const Params& P, void* wd1, void* wd2, void* wdsc,
+                              std::vector<PackJob>& out) {
   // unnormalised: the data-gradient convs divide by sigma
-  const PackJob pk[3] = {{P.w("conv1.w"), nullptr, wd1, g.cout, g.cin, 3, g.Cop, g.Cip,
-                          g.f32 ? kPackDgrad : kPackDgradSum4},
-                         {P.w("conv2.w"), nullptr, wd2, g.cout, g.cout, 3, g.Cop, g.Cop, kPackDgrad},
-                         {P.w("sc.w"), nullptr, wdsc, g.cout, g.cin, 1, g.Cop, g.Cip,
-                          g.f32 ? kPackDgrad : kPackDgradRep4}};
-  pack_group(st, g.f32, pk, 3);
+  out.push_back({P.w("conv1.w"), nullptr, wd1, g.cout, g.cin, 3, g.Cop, g.Cip, g.f32 ? kPackDgrad : kPackDgradSum4});
+  out.push_back({P.w("conv2.w"), nullptr, wd2, g.cout, g.cout, 3, g.Cop, g.Cop, kPackDgrad});
+  out.push_back({P.w("sc.w"), nullptr, wdsc, g.cout, g.cin, 1, g.Cop, g.Cip, g.f32 ? kPackDgrad : kPackDgradRep4});
+}
+static void g_pack_dgrad(const GBlock& g, hipStream_t st, const Params& P, void* wd1, void* wd2, void* wdsc) {
+  std::vector<PackJob> pk;
+  g_pack_dgrad_jobs(g, P, wd1, wd2, wdsc, pk);
+  pack_all(st, g.f32, pk.data(), (int)pk.size());
+}
+
+void GBlock::sn_jobs(const Params& P, std::vector<SnJob>& out) {
+  for (int i = 0; i < 7; ++i) out.push_back(sn_job(P, kGSN[i], sn[i]));
+}
+
+void GBlock::pack_jobs(const Params& P, bool for_bwd, std::vector<PackJob>& out) {
+  // the filters are packed unnormalised (the stored bf16 values do not
+  // depend on sigma); each conv divides its accumulator by its sigma
+  out.push_back({P.w("conv1.w"), nullptr, wp1, cout, cin, 3, Cop, Cip, f32 ? kPackFwd : kPackSub});
+  out.push_back({P.w("conv2.w"), nullptr, wp2, cout, cout, 3, Cop, Cop, kPackFwd});
+  out.push_back({P.w("sc.w"), nullptr, wpsc, cout, cin, 1, Cop, Cip, kPackFwd});
+  if (for_bwd && keep_dgrad) {
+    g_pack_dgrad_jobs(*this, P, wd1s, wd2s, wdscs, out);
+    dgrad_ready = true;
+  }
 }
 
 void GBlock::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
-  SnJob jobs[7];
-  for (int i = 0; i < 7; ++i) jobs[i] = sn_job(P, kGSN[i], sn[i]);
-  sn_power_iter_group(st, jobs, 7, npi, sn_eps, sn_ws);
-  // the filters are packed unnormalised (the stored bf16 values do not
-  // depend on sigma); each conv divides its accumulator by its sigma
-  const PackJob pk[3] = {{P.w("conv1.w"), nullptr, wp1, cout, cin, 3, Cop, Cip, f32 ? kPackFwd : kPackSub},
-                         {P.w("conv2.w"), nullptr, wp2, cout, cout, 3, Cop, Cop, kPackFwd},
-                         {P.w("sc.w"), nullptr, wpsc, cout, cin, 1, Cop, Cip, kPackFwd}};
-  pack_group(st, f32, pk, 3);
-  if (for_bwd && keep_dgrad) {
-    g_pack_dgrad(*this, st, P, wd1s, wd2s, wdscs);
-    dgrad_ready = true;
-  }
+  std::vector<SnJob> sj;
+  sn_jobs(P, sj);
+  sn_power_iter_all(st, sj.data(), (int)sj.size(), npi, sn_eps, sn_ws);
+  std::vector<PackJob> pk;
+  pack_jobs(P, for_bwd, pk);
+  pack_all(st, f32, pk.data(), (int)pk.size());
 }
 
 void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y) {
@@ -435,35 +447,49 @@ size_t DBlock::ws_size(int n_cu) const {
 }
 
 // the data-gradient weight packs of a D block into (wd1, wd2, wdsc)
-static void d_pack_dgrad(const DBlock& d, hipStream_t st, const Params& P, void* wd1, void* wd2, void* wdsc) {
+static void d_pack_dgrad_jobs(const DBlock& d, const Params& P, void* wd1, void* wd2, void* wdsc,
+                              std::vector<PackJob>& out) {
   const int R1 = d.im2col ? 1 : 3, K1 = d.im2col ? 9 * d.cin : d.cin, ksc = d.im2col ? 4 * d.cin : 0;
   // unnormalised: the data-gradient convs divide by sigma
-  const PackJob pk[3] = {{P.w("conv1.w"), nullptr, wd1, d.cout, K1, R1, d.Cop, d.Cip, kPackDgrad},
-                         {P.w("conv2.w"), nullptr, wd2, d.cout, d.cout, 3, d.Cop, d.Cop,
-                          d.subdgrad() ? kPackSubDgrad : kPackDgrad},
-                         {d.lsc ? P.w("sc.w") : nullptr, nullptr, wdsc, d.cout, d.cin, 1, d.Cop, d.Cip,
-                          kPackDgrad, ksc}};
-  pack_group(st, d.f32, pk, d.lsc ? 3 : 2);
+  out.push_back({P.w("conv1.w"), nullptr, wd1, d.cout, K1, R1, d.Cop, d.Cip, kPackDgrad});
+  out.push_back({P.w("conv2.w"), nullptr, wd2, d.cout, d.cout, 3, d.Cop, d.Cop,
+                 d.subdgrad() ? kPackSubDgrad : kPackDgrad});
+  if (d.lsc) out.push_back({P.w("sc.w"), nullptr, wdsc, d.cout, d.cin, 1, d.Cop, d.Cip, kPackDgrad, ksc});
+}
+static void d_pack_dgrad(const DBlock& d, hipStream_t st, const Params& P, void* wd1, void* wd2, void* wdsc) {
+  std::vector<PackJob> pk;
+  d_pack_dgrad_jobs(d, P, wd1, wd2, wdsc, pk);
+  pack_all(st, d.f32, pk.data(), (int)pk.size());
 }
 
-void DBlock::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
-  const int nsn = lsc ? 3 : 2;
-  const SnJob jobs[3] = {sn_job(P, "conv1.w", sn[0]), sn_job(P, "conv2.w", sn[1]),
-                         lsc ? sn_job(P, "sc.w", sn[2]) : SnJob{}};
-  sn_power_iter_group(st, jobs, nsn, npi, sn_eps, sn_ws);
+void DBlock::sn_jobs(const Params& P, std::vector<SnJob>& out) {
+  out.push_back(sn_job(P, "conv1.w", sn[0]));
+  out.push_back(sn_job(P, "conv2.w", sn[1]));
+  if (lsc) out.push_back(sn_job(P, "sc.w", sn[2]));
+}
+
+void DBlock::pack_jobs(const Params& P, bool for_bwd, std::vector<PackJob>& out) {
   // with 3x3-patch input, conv1 is a 1x1 filter over the 9 cin patch
   // channels (the [Cout][3][3][cin] weight read as [Cout][9 cin]) and the
   // skip's 1x1 filter sits on the centre tap's channels 4 cin ..
   const int R1 = im2col ? 1 : 3, K1 = im2col ? 9 * cin : cin, ksc = im2col ? 4 * cin : 0;
   // packed unnormalised; each conv divides its accumulator by its sigma
-  const PackJob pk[3] = {{P.w("conv1.w"), nullptr, wp1, cout, K1, R1, Cop, Cip, kPackFwd},
-                         {P.w("conv2.w"), nullptr, wp2, cout, cout, 3, Cop, Cop, s2conv() ? kPackPool4 : kPackFwd},
-                         {lsc ? P.w("sc.w") : nullptr, nullptr, wpsc, cout, cin, 1, Cop, Cip, kPackFwd, ksc}};
-  pack_group(st, f32, pk, nsn);
+  out.push_back({P.w("conv1.w"), nullptr, wp1, cout, K1, R1, Cop, Cip, kPackFwd});
+  out.push_back({P.w("conv2.w"), nullptr, wp2, cout, cout, 3, Cop, Cop, s2conv() ? kPackPool4 : kPackFwd});
+  if (lsc) out.push_back({P.w("sc.w"), nullptr, wpsc, cout, cin, 1, Cop, Cip, kPackFwd, ksc});
   if (for_bwd && keep_dgrad) {
-    d_pack_dgrad(*this, st, P, wd1s, wd2s, wdscs);
+    d_pack_dgrad_jobs(*this, P, wd1s, wd2s, wdscs, out);
     dgrad_ready = true;
   }
+}
+
+void DBlock::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
+  std::vector<SnJob> sj;
+  sn_jobs(P, sj);
+  sn_power_iter_all(st, sj.data(), (int)sj.size(), npi, sn_eps, sn_ws);
+  std::vector<PackJob> pk;
+  pack_jobs(P, for_bwd, pk);
+  pack_all(st, f32, pk.data(), (int)pk.size());
 }
 
 void DBlock::fwd(const Exec& ex, const Params& P, const void* x, void* y) {

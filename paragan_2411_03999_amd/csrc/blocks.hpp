@@ -106,6 +106,11 @@ struct GBlock {
   bool keep_dgrad = false, dgrad_ready = false;
   void *wd1s = nullptr, *wd2s = nullptr, *wdscs = nullptr;
   void prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd = false);
+  // prep's work as job lists, for a network to launch all of its modules'
+  // SN weights and packs together (pack_jobs with for_bwd marks the
+  // data-gradient packs ready)
+  void sn_jobs(const Params& P, std::vector<SnJob>& out);
+  void pack_jobs(const Params& P, bool for_bwd, std::vector<PackJob>& out);
   void fwd(const Exec& ex, const Params& P, const void* x, const float* cond, void* y);
   // dcond_accumulate: add to dcond instead of overwriting it
   void bwd(const Exec& ex, const Params& P, const void* x, const float* cond, const void* dy, void* dx,
@@ -141,6 +146,8 @@ struct DBlock {
   bool keep_dgrad = false, dgrad_ready = false;   // as in GBlock
   void *wd1s = nullptr, *wd2s = nullptr, *wdscs = nullptr;
   void prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd = false);
+  void sn_jobs(const Params& P, std::vector<SnJob>& out);                       // as in GBlock
+  void pack_jobs(const Params& P, bool for_bwd, std::vector<PackJob>& out);
   void fwd(const Exec& ex, const Params& P, const void* x, void* y);
   // dx may be null; dx_f32 writes an unrounded fp32 input gradient;
   // wgrad = false computes the input gradient only (no parameter gradients).
@@ -169,6 +176,10 @@ struct Attn {
   // another stream; sn_ws: sn_ws_all of the layout, or the block's share)
   bool prepped = false;
   void prep(hipStream_t st, const Params& P, void* sn_ws);
+  // as in GBlock; the attention packs divide by sigma, so they must follow
+  // the SN launches of sn_jobs on the stream
+  void sn_jobs(const Params& P, std::vector<SnJob>& out);
+  void pack_jobs(const Params& P, std::vector<PackJob>& out);
   void fwd(const Exec& ex, const Params& P, const void* x, void* y, bool for_bwd = true);
   void bwd(const Exec& ex, const Params& P, const void* x, const void* dy, void* dx, bool wgrad = true);
 };

@@ -106,6 +106,7 @@ struct ProfRec {
   std::string name;
   double flops;
   hipEvent_t a, b;
+  double bytes = 0.0;   // algorithmic HBM bytes (bandwidth-bound kernels)
 };
 struct Profiler {
   bool on = false;
@@ -136,13 +137,15 @@ struct ProfScope {
       (void)hipEventRecord(a, st);
     }
   }
-  void done(const std::string& name, double flops) {
+  void done(const std::string& name, double flops, double bytes = 0.0) {
     if (!a) return;
     hipEvent_t b = p->ev();
     (void)hipEventRecord(b, st);
-    p->recs.push_back(ProfRec{name, flops, a, b});
+    p->recs.push_back(ProfRec{name, flops, a, b, bytes});
     a = nullptr;
   }
+  // a bandwidth-bound launch: its algorithmic bytes instead of FLOPs
+  void done_bytes(const std::string& name, double bytes) { done(name, 0.0, bytes); }
   // as done(), with the launch's GEMM shape appended in detail mode
   void done(const std::string& name, double flops, int64_t m, int64_t n, int64_t k) {
     if (!a) return;

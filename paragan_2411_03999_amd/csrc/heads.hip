@@ -937,10 +937,13 @@ void optim_step(hipStream_t st, int kind, float* p, const float* g, float* m, fl
   const double c2 = 1.0 / (1.0 - std::pow((double)b2, (double)t));
   const int64_t threads = (n >> 2) + (n & 3);
   const dim3 grid((unsigned)cdiv(threads, 256));
+  ProfScope ps(st);
   if (kind == 0)
     hipLaunchKernelGGL(k_optim<0>, grid, dim3(256), 0, st, p, g, m, v, n, b1, b2, (float)lr_t, (float)c2, eps);
   else
     hipLaunchKernelGGL(k_optim<1>, grid, dim3(256), 0, st, p, g, m, v, n, b1, b2, (float)lr_t, (float)c2, eps);
+  // p, g, m, v read; p, m, v written
+  ps.done_bytes(kind == 0 ? "k_optim<adam>" : "k_optim<adabelief>", 28.0 * n);
   PG_LAUNCH_CHECK();
 }
 

@@ -218,7 +218,7 @@ size_t sn_group_ws_bytes(const SnJob* jobs, int n) {
 }
 
 void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws) {
-  PG_CHECK(n >= 1 && n <= kSnGroupMax, "sn group: 1..8 weights");
+  PG_CHECK(n >= 1 && n <= kSnGroupMax, "sn group: 1.." + std::to_string(kSnGroupMax) + " weights");
   SnGroupK g{};
   g.n = n;
   char* w = (char*)ws;
@@ -248,16 +248,39 @@ void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, f
   o1[n] = b1;
   o2[n] = b2;
   o3[n] = b3;
+  // algorithmic bytes: each matvec streams W once (plus its vectors); the
+  // normalisations move only vectors
+  double wbytes = 0.0, vbytes = 0.0;
+  for (int i = 0; i < n; ++i) {
+    wbytes += 4.0 * ((double)jobs[i].rows * jobs[i].cols + jobs[i].rows + jobs[i].cols);
+    vbytes += 4.0 * (2.0 * jobs[i].rows + 2.0 * jobs[i].cols);
+  }
   for (int it = 0; it < n_iter; ++it) {
     if (it + 1 == n_iter)
       for (int i = 0; i < n; ++i) g.j[i].u_save = jobs[i].u_save;
     std::copy(o1, o1 + n + 1, g.off);
-    hipLaunchKernelGGL(k_sng_wtu, dim3(b1), dim3(256), 0, st, g);
+    {
+      ProfScope ps(st);
+      hipLaunchKernelGGL(k_sng_wtu, dim3(b1), dim3(256), 0, st, g);
+      ps.done_bytes("k_sng_wtu", wbytes);
+    }
     std::copy(o2, o2 + n + 1, g.off);
-    hipLaunchKernelGGL(k_sng_t, dim3(b2), dim3(256), 0, st, g);
+    {
+      ProfScope ps(st);
+      hipLaunchKernelGGL(k_sng_t, dim3(b2), dim3(256), 0, st, g);
+      ps.done_bytes("k_sng_t", vbytes);
+    }
     std::copy(o3, o3 + n + 1, g.off);
-    hipLaunchKernelGGL(k_sng_wv, dim3(b3), dim3(256), 0, st, g);
-    hipLaunchKernelGGL(k_sng_u, dim3(n), dim3(1024), 0, st, g, eps);
+    {
+      ProfScope ps(st);
+      hipLaunchKernelGGL(k_sng_wv, dim3(b3), dim3(256), 0, st, g);
+      ps.done_bytes("k_sng_wv", wbytes);
+    }
+    {
+      ProfScope ps(st);
+      hipLaunchKernelGGL(k_sng_u, dim3(n), dim3(1024), 0, st, g, eps);
+      ps.done_bytes("k_sng_u", vbytes);
+    }
   }
   PG_LAUNCH_CHECK();
 }
@@ -282,6 +305,14 @@ void* sn_scratch_init(int device) {
     g_scratch_ptr[device] = p;
   }
   return g_scratch_ptr[device];
+}
+
+void sn_power_iter_all(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws) {
+  for (int i = 0; i < n; i += kSnGroupMax) {
+    const int k = std::min(kSnGroupMax, n - i);
+    sn_power_iter_group(st, jobs + i, k, n_iter, eps, ws);
+    ws = (char*)ws + sn_group_ws_bytes(jobs + i, k);
+  }
 }
 
 void sn_power_iter(hipStream_t st, const float* W, int64_t rows, int64_t cols, float* u, float* v,
@@ -542,8 +573,12 @@ __global__ __launch_bounds__(256) void k_pack_group(PackGroupK g) {
   }
 }
 
+void pack_all(hipStream_t st, bool f32, const PackJob* jobs, int n) {
+  for (int i = 0; i < n; i += kSnGroupMax) pack_group(st, f32, jobs + i, std::min(kSnGroupMax, n - i));
+}
+
 void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
-  PG_CHECK(n >= 1 && n <= kSnGroupMax, "pack group: 1..8 weights");
+  PG_CHECK(n >= 1 && n <= kSnGroupMax, "pack group: 1.." + std::to_string(kSnGroupMax) + " weights");
   PackGroupK g{};
   g.n = n;
   int64_t b = 0;
@@ -571,10 +606,21 @@ void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n) {
     PG_CHECK(b < (1LL << 31), "pack group: too large");
   }
   g.off[n] = (int)b;
+  // algorithmic bytes: the fp32 master weights read, the packed operand written
+  double bytes = 0.0;
+  for (int i = 0; i < n; ++i) {
+    const PackJob& a = jobs[i];
+    const bool four = a.mode == kPackPool4 || a.mode == kPackDgradSum4;
+    const bool sub = a.mode == kPackSub || a.mode == kPackSubDgrad;
+    const int RRd = four || sub ? 16 : (a.mode == kPackDgradRep4 ? 4 : a.R * a.R);
+    bytes += 4.0 * a.Cout * a.R * a.R * a.Cin + (f32 ? 4.0 : 2.0) * a.Np * RRd * a.Cp;
+  }
+  ProfScope ps(st);
   if (f32)
     hipLaunchKernelGGL(k_pack_group<float>, dim3((unsigned)b), dim3(256), 0, st, g);
   else
     hipLaunchKernelGGL(k_pack_group<bf16_t>, dim3((unsigned)b), dim3(256), 0, st, g);
+  ps.done_bytes("k_pack_group", bytes);
   PG_LAUNCH_CHECK();
 }
 
@@ -716,7 +762,7 @@ __global__ __launch_bounds__(256) void k_sngb_apply(SnBwdGroupK g) {
 }
 
 void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part) {
-  PG_CHECK(n >= 1 && n <= kSnGroupMax, "sn bwd group: 1..8 weights");
+  PG_CHECK(n >= 1 && n <= kSnGroupMax, "sn bwd group: 1.." + std::to_string(kSnGroupMax) + " weights");
   SnBwdGroupK g{};
   g.n = n;
   SnBwdGroupK g2;
@@ -746,8 +792,20 @@ void sn_bwd_group(hipStream_t st, const SnBwdJob* jobs, int n, float* part) {
   }
   g2.off[n] = (int)b2;
   PG_CHECK(b2 < (1LL << 31), "sn bwd group: too large");
-  hipLaunchKernelGGL(k_sngb_dot, dim3(b1), dim3(256), 0, st, g);
-  hipLaunchKernelGGL(k_sngb_apply, dim3((unsigned)b2), dim3(256), 0, st, g2);
+  // algorithmic bytes: <dW, W> reads both; the projection reads the raw
+  // gradient and writes the parameter gradient
+  double bytes = 0.0;
+  for (int i = 0; i < n; ++i) bytes += 8.0 * jobs[i].Cout * jobs[i].R * jobs[i].R * jobs[i].Cin;
+  {
+    ProfScope ps(st);
+    hipLaunchKernelGGL(k_sngb_dot, dim3(b1), dim3(256), 0, st, g);
+    ps.done_bytes("k_sngb_dot", bytes);
+  }
+  {
+    ProfScope ps(st);
+    hipLaunchKernelGGL(k_sngb_apply, dim3((unsigned)b2), dim3(256), 0, st, g2);
+    ps.done_bytes("k_sngb_apply", bytes);
+  }
   PG_LAUNCH_CHECK();
 }
 
@@ -909,6 +967,7 @@ void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, 
   PG_CHECK(ldc >= cpad(C) && ldc % 8 == 0, "colsum: channel stride");
   const int nch = (int)cdiv(M, sh.rows_blk);
   float* part = (float*)ws;
+  ProfScope ps(st);
   if (f32)
     hipLaunchKernelGGL((k_colred<float, false>), dim3(nch), dim3(256), 0, st, (const float*)x, M, C, ldc, sh, part,
                        nullptr);
@@ -916,6 +975,7 @@ void colsum(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc, 
     hipLaunchKernelGGL((k_colred<bf16_t, false>), dim3(nch), dim3(256), 0, st, (const bf16_t*)x, M, C, ldc, sh,
                        part, nullptr);
   hipLaunchKernelGGL(k_colsum_fin, dim3((unsigned)cdiv(C, 16)), dim3(1024), 0, st, part, nch, C, scale, out);
+  ps.done_bytes("colsum", (double)M * C * (f32 ? 4 : 2));
   PG_LAUNCH_CHECK();
 }
 
@@ -974,6 +1034,7 @@ void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc
   const int nch = (int)cdiv(M, sh.rows_blk);
   float* pmean = (float*)ws;
   float* pm2 = (float*)((char*)ws + align256((size_t)nch * C * 4));
+  ProfScope ps(st);
   if (f32)
     hipLaunchKernelGGL((k_colred<float, true>), dim3(nch), dim3(256), 0, st, (const float*)x, M, C, ldc, sh, pmean,
                        pm2);
@@ -982,6 +1043,7 @@ void bn_stats(hipStream_t st, bool f32, const void* x, int64_t M, int C, int ldc
                        pmean, pm2);
   hipLaunchKernelGGL(k_bn_fin, dim3((unsigned)cdiv(C, 16)), dim3(1024), 0, st, pmean, pm2, nch, sh.rows_blk, M, C,
                      eps, mean, rstd);
+  ps.done_bytes("bn_stats", (double)M * C * (f32 ? 4 : 2));
   PG_LAUNCH_CHECK();
 }
 
@@ -1040,12 +1102,14 @@ void bn_apply(hipStream_t st, bool f32, const void* x, int64_t M, int HW, int C,
   const FastDiv fdHW = make_fastdiv(HW);
   const int64_t rows_blk = (int64_t)(256 / CC) * kBnRows;
   dim3 g((unsigned)cdiv(M, rows_blk));
+  ProfScope ps(st);
   if (f32)
     hipLaunchKernelGGL(k_bn_apply<float>, g, dim3(256), 0, st, (const float*)x, M, CC, fdHW, C, Cp, mean, scale,
                        shift, tab_stride, (int)relu, (float*)out);
   else
     hipLaunchKernelGGL(k_bn_apply<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, M, CC, fdHW, C, Cp, mean, scale,
                        shift, tab_stride, (int)relu, (bf16_t*)out);
+  ps.done_bytes("bn_apply", 2.0 * M * Cp * (f32 ? 4 : 2));
   PG_LAUNCH_CHECK();
 }
 
@@ -1465,6 +1529,10 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
   float* Bc = (float*)((char*)A + align256((size_t)cpad(C) * 4));
   const FastDiv fdW = make_fastdiv(W);
   dim3 g1(nch, B);
+  // algorithmic bytes: x and the fp32 output gradient (at its own
+  // resolution) read for the statistics, then again with dx written
+  const double gbytes = 4.0 * (double)B * HW * C / (g_up2 ? 4 : 1), xbytes = (double)B * HW * Cp * (f32 ? 4 : 2);
+  ProfScope ps(st);
   if (f32)
     hipLaunchKernelGGL(k_bnb_reduce<float>, g1, dim3(256), 0, st, g, (int)g_up2, (const float*)x, HW, H, W, fdW,
                        C, Cp, mean, rstd, gain, bias, tab_stride, sh, p1, p2);
@@ -1475,17 +1543,20 @@ void bn_bwd(hipStream_t st, bool f32, const float* g, bool g_up2, const void* x,
                      dgain, dbias, dg_stride);
   hipLaunchKernelGGL(k_bnb_fin2, dim3((unsigned)cdiv(C, 64)), dim3(1024), 0, st, p1, p2, nch, B, C, gain,
                      tab_stride, (int64_t)B * HW, dgain, dbias, A, Bc, dg_stride);
+  ps.done_bytes("bn_bwd_stats", gbytes + xbytes);
   const int64_t M = (int64_t)B * HW;
   const int CC = Cp / 8;
   PG_CHECK(M * CC < (1LL << 31) && M < (1LL << 31) && CC <= 256, "bn_bwd: too large");
   dim3 g3((unsigned)cdiv(M, (int64_t)(256 / CC) * kBnRows));
   const FastDiv fdHW = make_fastdiv(HW);
+  ProfScope ps2(st);
   if (f32)
     hipLaunchKernelGGL(k_bnb_apply<float>, g3, dim3(256), 0, st, g, (int)g_up2, (const float*)x, M, CC, fdHW, fdW,
                        HW, H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (float*)dx);
   else
     hipLaunchKernelGGL(k_bnb_apply<bf16_t>, g3, dim3(256), 0, st, g, (int)g_up2, (const bf16_t*)x, M, CC, fdHW,
                        fdW, HW, H, W, C, Cp, mean, rstd, gain, bias, tab_stride, A, Bc, res, (bf16_t*)dx);
+  ps2.done_bytes("bn_bwd_apply", gbytes + 2.0 * xbytes + (res ? 4.0 * (double)M * C : 0.0));
   PG_LAUNCH_CHECK();
 }
 
@@ -1542,12 +1613,14 @@ void avgpool2(hipStream_t st, bool f32, const void* x, int B, int H, int W, int 
   PG_CHECK(n8 < (1LL << 31), "avgpool2: size");
   const FastDiv fdCC = make_fastdiv(CC), fdWo = make_fastdiv(Wo);
   dim3 g((unsigned)cdiv(n8, 256));
+  ProfScope ps(st);
   if (f32)
     hipLaunchKernelGGL(k_avgpool2<float>, g, dim3(256), 0, st, (const float*)x, n8, CC, fdCC, fdWo, Ho, Wo,
                        (float*)out);
   else
     hipLaunchKernelGGL(k_avgpool2<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, n8, CC, fdCC, fdWo, Ho, Wo,
                        (bf16_t*)out);
+  ps.done_bytes("avgpool2", 5.0 * 8.0 * n8 * (f32 ? 4 : 2));
   PG_LAUNCH_CHECK();
 }
 

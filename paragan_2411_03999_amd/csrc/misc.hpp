@@ -6,8 +6,9 @@ namespace pg {
 
 // spectral normalisation
 size_t sn_ws_bytes(int64_t rows, int64_t cols);
-// Grouped forms: every SN weight of a module through one launch per phase.
-constexpr int kSnGroupMax = 8;
+// Grouped forms: up to kSnGroupMax SN weights through one launch per phase
+// (the job table travels in the kernel arguments, 2.3 KB at 24 jobs).
+constexpr int kSnGroupMax = 24;
 struct SnJob {
   const float* W;       // [rows][cols] fp32
   int64_t rows, cols;
@@ -21,6 +22,9 @@ size_t sn_group_ws_bytes(const SnJob* jobs, int n);
 constexpr size_t kSnScratchBytes = (size_t)4 << 20;
 void* sn_scratch_init(int device);
 void sn_power_iter_group(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws);
+// Any number of jobs, in groups of kSnGroupMax; ws holds every job's
+// partials (sn_group_ws_bytes of all of them).
+void sn_power_iter_all(hipStream_t st, const SnJob* jobs, int n, int n_iter, float eps, void* ws);
 // mode: kPackFwd [Np][R][R][Cp]; kPackDgrad [Cp][R][R][Np] flipped taps;
 // kPackPool4 [Np][4][4][Cp], the 3x3 filter (R = 3) convolved with the 2x2
 // averaging box: the stride-2 filter of conv3x3 followed by avgpool2;
@@ -50,6 +54,8 @@ struct PackJob {
   int koff = 0;   // kPackFwd / kPackDgrad: input channel c lands at channel koff + c of dst
 };
 void pack_group(hipStream_t st, bool f32, const PackJob* jobs, int n);
+// any number of jobs, in groups of kSnGroupMax
+void pack_all(hipStream_t st, bool f32, const PackJob* jobs, int n);
 struct SnBwdJob {
   const float *dwp, *W, *u, *v, *sigma, *scale;
   float* dW;

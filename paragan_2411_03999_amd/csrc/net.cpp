@@ -202,19 +202,30 @@ size_t GNet::ws_size(int n_cu) {
   return w.off;
 }
 
+// Every SN weight of the network through one group of launches per power
+// iteration phase (kSnGroupMax weights a launch), then every weight pack
+// through one group of launches: the same kernels, per weight, as each
+// module's own prep, so the results are identical, in a few launches
+// instead of four per module.
 void GNet::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   const Arch& a = a_;
-  const Exec e{st, 0, sn_ws, 0};
-  sn_forward(e, P, "linear.w", lin_, a.npi, a.sn_eps);
+  std::vector<SnJob> sj;
+  std::vector<PackJob> pk;
+  sj.push_back(sn_job(P, "linear.w", lin_));
+  for (int i = 0; i < a.n_g; ++i) blocks_[i].sn_jobs(sub(P, "g" + std::to_string(i) + "."), sj);
+  if (attn_after_ >= 0) attn_.sn_jobs(sub(P, "attn."), sj);
+  sj.push_back(sn_job(P, "out_conv.w", head_.sn_slot()));
+  sn_power_iter_all(st, sj.data(), (int)sj.size(), a.npi, a.sn_eps, sn_ws);
   for (int i = 0; i < a.n_g; ++i) {
-    blocks_[i].prep(st, sub(P, "g" + std::to_string(i) + "."), sn_ws, for_bwd);
+    blocks_[i].pack_jobs(sub(P, "g" + std::to_string(i) + "."), for_bwd, pk);
     blocks_[i].prepped = true;
   }
+  // (the attention packs divide by sigma: after the SN launches above)
   if (attn_after_ >= 0) {
-    attn_.prep(st, sub(P, "attn."), sn_ws);
+    attn_.pack_jobs(sub(P, "attn."), pk);
     attn_.prepped = true;
   }
-  sn_forward(e, P, "out_conv.w", head_.sn_slot(), head_.npi, head_.sn_eps);
+  pack_all(st, false, pk.data(), (int)pk.size());
   head_.prepped = true;
   prepped_ = true;
 }
@@ -401,17 +412,22 @@ size_t DNet::ws_size(int n_cu) {
 
 void DNet::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   const Arch& a = a_;
-  const Exec e{st, 0, sn_ws, 0};
+  std::vector<SnJob> sj;
+  std::vector<PackJob> pk;
+  for (int j = 0; j < (int)blocks_.size(); ++j) blocks_[j].sn_jobs(sub(P, "d" + std::to_string(j) + "."), sj);
+  if (attn_after_ >= 0) attn_.sn_jobs(sub(P, "attn."), sj);
+  sj.push_back(sn_job(P, "head.w", head_));
+  sj.push_back(sn_job(P, "embed", emb_));
+  sn_power_iter_all(st, sj.data(), (int)sj.size(), a.npi, a.sn_eps, sn_ws);
   for (int j = 0; j < (int)blocks_.size(); ++j) {
-    blocks_[j].prep(st, sub(P, "d" + std::to_string(j) + "."), sn_ws, for_bwd);
+    blocks_[j].pack_jobs(sub(P, "d" + std::to_string(j) + "."), for_bwd, pk);
     blocks_[j].prepped = true;
   }
   if (attn_after_ >= 0) {
-    attn_.prep(st, sub(P, "attn."), sn_ws);
+    attn_.pack_jobs(sub(P, "attn."), pk);
     attn_.prepped = true;
   }
-  sn_forward(e, P, "head.w", head_, a.npi, a.sn_eps);
-  sn_forward(e, P, "embed", emb_, a.npi, a.sn_eps);
+  pack_all(st, false, pk.data(), (int)pk.size());
   prepped_ = true;
 }
 

@@ -103,7 +103,7 @@ FETCH_FN = C.CFUNCTYPE(C.c_int, C.c_void_p, C.c_int64, C.c_void_p, C.c_size_t)
 
 class KernelStat(C.Structure):
     _fields_ = [("name", C.c_char * 64), ("launches", C.c_int64), ("total_ms", C.c_double),
-                ("flops", C.c_double)]
+                ("flops", C.c_double), ("bytes", C.c_double)]
 
 
 _P = C.c_void_p
@@ -471,7 +471,7 @@ def paragan_profile_read(ctx, cap=1024):
     arr = (KernelStat * cap)()
     n = C.c_int32()
     ctx.check(load().paragan_profile_read(ctx.h, arr, cap, C.byref(n)))
-    return [dict(name=a.name.decode(), launches=a.launches, total_ms=a.total_ms, flops=a.flops)
+    return [dict(name=a.name.decode(), launches=a.launches, total_ms=a.total_ms, flops=a.flops, bytes=a.bytes)
             for a in arr[:min(n.value, cap)]]
 
 
