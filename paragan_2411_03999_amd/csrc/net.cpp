@@ -207,7 +207,7 @@ size_t GNet::ws_size(int n_cu) {
 // through one group of launches: the same kernels, per weight, as each
 // module's own prep, so the results are identical, in a few launches
 // instead of four per module.
-void GNet::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
+void GNet::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd, bool pack) {
   const Arch& a = a_;
   std::vector<SnJob> sj;
   std::vector<PackJob> pk;
@@ -217,10 +217,11 @@ void GNet::prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd) {
   sj.push_back(sn_job(P, "out_conv.w", head_.sn_slot()));
   sn_power_iter_all(st, sj.data(), (int)sj.size(), a.npi, a.sn_eps, sn_ws);
   for (int i = 0; i < a.n_g; ++i) {
-    blocks_[i].pack_jobs(sub(P, "g" + std::to_string(i) + "."), for_bwd, pk);
+    if (pack) blocks_[i].pack_jobs(sub(P, "g" + std::to_string(i) + "."), for_bwd, pk);
     blocks_[i].prepped = true;
   }
-  // (the attention packs divide by sigma: after the SN launches above)
+  // (the attention packs divide by sigma, so they are redone after every
+  // SN update, and after the SN launches above)
   if (attn_after_ >= 0) {
     attn_.pack_jobs(sub(P, "attn."), pk);
     attn_.prepped = true;
@@ -574,9 +575,13 @@ struct StepRun {
   float* fake_half() { return r.ximg + (size_t)B * pix * 3; }
   // G step: G forward, D forward (u updated), hinge (L_G to *loss), D input
   // gradient, G backward, G's optimiser
+  // (between_fwds runs after G's forward, before D's: the point where the
+  // fused step waits for D's preparation)
+  template <typename F>
   void g_update(const paragan_biggan_desc* d, paragan_net_state* G, const float* z, const int32_t* y,
-                float* loss) {
+                float* loss, F&& between_fwds) {
     g.fwd(ex, PG, z, y, r.ximg);
+    between_fwds();
     d1.fwd(ex, PD, r.ximg, y, r.logits);
     hinge(st, r.logits, 0, B, true, r.dout, loss);
     d1.bwd(ex, PD, y, r.dout, r.dimg, false);
@@ -608,7 +613,7 @@ void d_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* D
 void g_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_state* G, paragan_net_state* D,
             const float* z, const int32_t* y, void* ws, float* loss_host) {
   StepRun R(ctx, d, G, D, ws);
-  R.g_update(d, G, z, y, R.r.dloss);
+  R.g_update(d, G, z, y, R.r.dloss, [] {});
   R.losses_to_host(loss_host, 1);
 }
 
@@ -618,11 +623,14 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
   hipStream_t st = R.st;
   // The forwards' SN power iterations and weight packing (which read only
   // parameters) run on a second stream, each network's ahead of its forward
-  // and behind the work that last used its packed weights or changed its
+  // and behind the work that last used its SN state or changed its
   // parameters: D's behind the previous optimiser step (overlapping G's
   // forward), G's behind the previous G forward (overlapping D's forward and
-  // backward).  The kernels are the same as on the one-stream path, so the
-  // results are too.
+  // backward).  G's parameters do not change before the G step's optimiser,
+  // so its weights are packed once per step (forward and data-gradient
+  // packs), and its later preparations run only the SN power iterations.
+  // The G step waits for D's preparation only after G's forward.  The
+  // kernels are the same as on the one-stream path, so the results are too.
   if (!ctx->side) {
     PG_HIP(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking));
     for (hipEvent_t& e : ctx->ev) PG_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
@@ -636,7 +644,7 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
     };
     auto main_after = [&](hipEvent_t e) { PG_HIP(hipStreamWaitEvent(st, e, 0)); };
     side_after_main(ev_main2);
-    R.g.prep(sd, R.PG, R.r.side, false);
+    R.g.prep(sd, R.PG, R.r.side, true);
     PG_HIP(hipEventRecord(ev_g, sd));
     for (int k = 0; k < n_D; ++k) {
       side_after_main(ev_main);
@@ -646,7 +654,7 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
       main_after(ev_g);
       R.g.fwd(R.ex, R.PG, in->z_fake[k], in->y_fake[k], R.fake_half(), false);
       side_after_main(ev_main2);
-      R.g.prep(sd, R.PG, R.r.side, k == n_D - 1);   // for the next D step's or the G step's forward
+      R.g.prep(sd, R.PG, R.r.side, false, false);   // SN for the next D step's or the G step's forward
       PG_HIP(hipEventRecord(ev_g, sd));
       main_after(ev_d);
       R.d_update(d, D, R.r.dloss + k);
@@ -655,8 +663,7 @@ void train_step(paragan_ctx* ctx, const paragan_biggan_desc* d, paragan_net_stat
     R.d1.prep(sd, R.PD, R.r.side, true);
     PG_HIP(hipEventRecord(ev_d, sd));
     main_after(ev_g);
-    main_after(ev_d);
-    R.g_update(d, G, in->z_g, in->y_g, R.r.dloss + n_D);
+    R.g_update(d, G, in->z_g, in->y_g, R.r.dloss + n_D, [&] { main_after(ev_d); });
     R.losses_to_host(losses_host, n_D + 1);
   } catch (...) {
     // leave neither stream running on the caller's buffers

@@ -60,7 +60,10 @@ class GNet {
   // The forward's SN power iterations and weight packing of every layer on
   // stream st (sn_ws: sn_ws_all of the layout); the next fwd then skips them.
   // for_bwd: the blocks' data-gradient weights too, for the next bwd.
-  void prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd = false);
+  // pack = false: the SN power iterations only, the packed weights of the
+  // last packing prep being still those of the parameters (the packs hold
+  // unnormalised weights; sigma enters in the conv epilogues)
+  void prep(hipStream_t st, const Params& P, void* sn_ws, bool for_bwd = false, bool pack = true);
   void fwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, float* img, bool for_bwd = true);
   // dimg: fp32 [B][img][img][ldd]
   void bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y, const float* dimg, int ldd);
