@@ -48,15 +48,15 @@ PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA (published)
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E (published)
 
 # HBM bytes per launch of a kernel, from two rocprofv3 --pmc passes over
-# "bench.py --steps 1 --warmup 1 --no-cpu-baseline --copy-probe" (FETCH_SIZE,
+# "bench.py --steps 1 --warmup 1 --no-cpu-baseline --no-extras --copy-probe" (FETCH_SIZE,
 # then WRITE_SIZE, KiB per dispatch, averaged over the kernel's dispatches),
 # each scaled by what the counter reads for the 1 GiB copy probe (FETCH_SIZE
 # reads 0.5 GiB for it: x2.0; WRITE_SIZE reads 1 GiB: x1.0).  Valid only for
 # the kernel source they were taken on (sha1 prefix of the file).
 TRAFFIC = {
-    "k_conv_halo<192x128,false>": {"fetch": 2.0 * 297642.0 * 1024, "write": 263315.0 * 1024,
+    "k_conv_halo<192x128,false>": {"fetch": 2.0 * 297649.0 * 1024, "write": 263315.0 * 1024,
                                    "source": "paragan_2411_03999_amd/csrc/convfwd.hip",
-                                   "sha1": "4cb8c19c47d9"},
+                                   "sha1": "aea6e3f37613"},
 }
 
 
