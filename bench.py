@@ -373,12 +373,18 @@ def main():
     lib.paragan_profile(ctx, 2 if args.detail else 1)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
+    # an event after every step as well (each step ends with its losses on
+    # the host), for the spread of the step time
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ev0.record()
     t0 = time.perf_counter()
     for i in range(args.steps):
         step()
+        evs[i].record()
     ev1.record()
     torch.cuda.synchronize()
+    step_ms = sorted([ev0.elapsed_time(evs[0])] + [evs[i - 1].elapsed_time(evs[i]) for i in range(1, args.steps)])
+    pct = lambda q: step_ms[min(len(step_ms) - 1, int(round(q * (len(step_ms) - 1))))]
     wall = time.perf_counter() - t0
     lib.paragan_profile(ctx, False)
     stats = lib.paragan_profile_read(ctx)
@@ -392,7 +398,7 @@ def main():
     dom = next(s for s in stats if s["flops"] > 0)
     achieved = dom["flops"] / (dom["total_ms"] / 1e3) / 1e12
     conv = [s for s in stats if s["name"].startswith(("k_conv_", "k_wgrad_")) and s["flops"] > 0
-            and "simt" not in s["name"]]
+            and "f32mfma" not in s["name"]]
     conv_ms = sum(s["total_ms"] for s in conv)
     conv_tf = sum(s["flops"] for s in conv) / (conv_ms / 1e3) / 1e12 if conv_ms else 0.0
     all_ms = sum(s["total_ms"] for s in stats)
@@ -427,6 +433,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": gpu_ms / args.steps,
+        "step_ms": {"median": pct(0.5), "p10": pct(0.1), "p90": pct(0.9)},
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,

@@ -311,9 +311,17 @@ __global__ __launch_bounds__(256, 2) void k_conv_mfma(ConvK k) {
   }
 }
 
-// ------------------------------------------------------------ fp32 SIMT conv
+// ------------------------------------------------------ fp32 MFMA conv
+// The fp32 path (exact-fp32 configurations) on the fp32 matrix cores:
+// 64 x 64 tiles (pixels x output channels), 16-deep K steps staged in LDS
+// k-major, four waves each owning a 32 x 32 quarter through
+// v_mfma_f32_32x32x2_f32 (a lane supplies one value of each operand per
+// instruction: row lane % 32 at K index lane / 32).  Weights are the A
+// operand (rows = output channels), pixels the B operand, so a lane ends
+// with one pixel (lane % 32) and the 16 channels (r % 4) + 8 (r / 4) +
+// 4 (lane / 32) of its wave's 32.
 template <int GATHER, bool AFF, bool RELU>
-__global__ __launch_bounds__(256) void k_conv_simt(ConvK k) {
+__global__ __launch_bounds__(256) void k_conv_f32mfma(ConvK k) {
   __shared__ float As[16][68];
   __shared__ float Bs[16][68];
   const AOp& a = k.a;
@@ -321,7 +329,8 @@ __global__ __launch_bounds__(256) void k_conv_simt(ConvK k) {
   const int tmi = bid / k.tiles_n, tni = bid - tmi * k.tiles_n;
   const int64_t m0 = (int64_t)tmi * 64;
   const int n0 = tni * 64;
-  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, kh = lane >> 5;
+  const int wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
   const int arow = tid >> 2, c4 = (tid & 3) * 4;
   const int64_t am = m0 + arow;
   const bool arv = am < a.M;
@@ -330,7 +339,9 @@ __global__ __launch_bounds__(256) void k_conv_simt(ConvK k) {
   const float* X = (const float*)a.x;
   const float* Wt = (const float*)k.w;
   const int RR = a.R * a.R;
-  float acc[4][4] = {};
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
   for (int ks = 0; ks < k.ksteps; ++ks) {
     const int tap = ks / k.cchunks;
     const int c0 = (ks - tap * k.cchunks) * 16;
@@ -360,29 +371,29 @@ __global__ __launch_bounds__(256) void k_conv_simt(ConvK k) {
     Bs[c4 + 0][arow] = wv.x; Bs[c4 + 1][arow] = wv.y; Bs[c4 + 2][arow] = wv.z; Bs[c4 + 3][arow] = wv.w;
     __syncthreads();
 #pragma unroll
-    for (int kk = 0; kk < 16; ++kk) {
-      float av[4], bv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { av[i] = As[kk][ty * 4 + i]; bv[i] = Bs[kk][tx * 4 + i]; }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    for (int t = 0; t < 8; ++t) {
+      const float wa = Bs[2 * t + kh][wn * 32 + l32];
+      const float xb = As[2 * t + kh][wm * 32 + l32];
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(wa, xb, acc, 0, 0, 0);
     }
     __syncthreads();
   }
   const float accs = (k.o.acc_scale ? *k.o.acc_scale : 1.f) * k.o.acc_mul / (k.o.acc_div ? *k.o.acc_div : 1.f);
-  for (int j = 0; j < 4; ++j) {
-    const int col = n0 + tx * 4 + j;
-    if (col >= k.o.yC) continue;
+  const int64_t m = m0 + wm * 32 + l32;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int col = n0 + wn * 32 + (r & 3) + 8 * (r >> 2) + 4 * kh;
     const float bias = (k.o.bias && col < k.o.n_real) ? k.o.bias[col] : 0.f;
-    const int64_t m = m0 + ty * 4;
     if (!k.o.pool) {
-      for (int i = 0; i < 4; ++i)
-        if (m + i < a.M) epi_store(k, m + i, col, acc[i][j] * accs + bias, a.H, a.W);
-    } else if (m < a.M) {
-      const float v = 0.25f * ((acc[0][j] + acc[1][j]) + (acc[2][j] + acc[3][j]));
-      epi_store(k, m >> 2, col, v * accs + bias, a.H, a.W);
+      if (col < k.o.yC && m < a.M) epi_store(k, m, col, acc[r] * accs + bias, a.H, a.W);
+    } else {
+      // pooled output: the 2 x 2 window is four consecutive rows m (tiles
+      // hold whole windows), here four consecutive lanes, summed in the
+      // order (m0 + m1) + (m2 + m3)
+      float v = acc[r];
+      v += __shfl_xor(v, 1);
+      v += __shfl_xor(v, 2);
+      if ((lane & 3) == 0 && col < k.o.yC && m < a.M) epi_store(k, m >> 2, col, 0.25f * v * accs + bias, a.H, a.W);
     }
   }
 }
@@ -442,20 +453,20 @@ void conv_fwd(hipStream_t s, bool f32, const ConvIn& in, int H, int W, int R,
     k.tiles_m = (int)cdiv(k.a.M, 64);
     k.tiles_n = (int)cdiv(Np, 64);
     dim3 grid(k.tiles_m * k.tiles_n), block(256);
-#define PG_SIMT_CASE(G, A_, R_)                                                     \
+#define PG_F32_CASE(G, A_, R_)                                                     \
   if (in.gather == G && aff == A_ && (bool)in.relu == R_) {                         \
-    hipLaunchKernelGGL((k_conv_simt<G, A_, R_>), grid, block, 0, s, k);             \
+    hipLaunchKernelGGL((k_conv_f32mfma<G, A_, R_>), grid, block, 0, s, k);             \
     PG_LAUNCH_CHECK();                                                              \
-    prof.done(kname("k_conv_simt", {G, A_, R_}), flops);                            \
+    prof.done(kname("k_conv_f32mfma", {G, A_, R_}), flops);                            \
     return;                                                                         \
   }
-    PG_SIMT_CASE(G_DIRECT, false, false)
-    PG_SIMT_CASE(G_DIRECT, false, true)
-    PG_SIMT_CASE(G_DIRECT, true, true)
-    PG_SIMT_CASE(G_UP2, false, false)
-    PG_SIMT_CASE(G_UP2, true, true)
-    PG_SIMT_CASE(G_POOL2, false, false)
-#undef PG_SIMT_CASE
+    PG_F32_CASE(G_DIRECT, false, false)
+    PG_F32_CASE(G_DIRECT, false, true)
+    PG_F32_CASE(G_DIRECT, true, true)
+    PG_F32_CASE(G_UP2, false, false)
+    PG_F32_CASE(G_UP2, true, true)
+    PG_F32_CASE(G_POOL2, false, false)
+#undef PG_F32_CASE
     throw Error{-2, "conv(f32): unsupported prologue combination"};
   }
   k.cchunks = in.C / 32;
@@ -684,9 +695,12 @@ __global__ __launch_bounds__(256, 2) void k_wgrad_mfma(WgK k) {
     }
 }
 
-// fp32 SIMT weight gradient: 64 (n) x 64 (k) tile, 16 pixels per step.
+// fp32 weight gradient on the fp32 matrix cores: 64 (n) x 64 (k) tile, 16
+// pixels per step staged in LDS, four waves each owning a 32 x 32 quarter
+// through v_mfma_f32_32x32x2_f32 (the gradient is the A operand, rows =
+// output channels; the gathered activation the B operand, columns = K).
 template <int GATHER, bool AFF, bool RELU>
-__global__ __launch_bounds__(256) void k_wgrad_simt(WgK k) {
+__global__ __launch_bounds__(256) void k_wgrad_f32mfma(WgK k) {
   __shared__ float Gs[16][68];
   __shared__ float Xs[16][68];
   const AOp& a = k.a;
@@ -698,11 +712,14 @@ __global__ __launch_bounds__(256) void k_wgrad_simt(WgK k) {
   const int64_t mbeg = (int64_t)split * k.m_per_split;
   int64_t mend = mbeg + k.m_per_split;
   if (mend > a.M) mend = a.M;
-  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, kh = lane >> 5;
+  const int wave = tid >> 6, wn = wave >> 1, wk = wave & 1;
   const int lrow = tid >> 4, lc4 = (tid & 15) * 4;   // 16 pixels x 64 columns
   const float* G = (const float*)k.g;
   const float* X = (const float*)a.x;
-  float acc[4][4] = {};
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
   for (int64_t mc = mbeg; mc < mend; mc += 16) {
     const int64_t m = mc + lrow;
     float gv[4] = {0.f, 0.f, 0.f, 0.f}, xv[4] = {0.f, 0.f, 0.f, 0.f};
@@ -742,25 +759,19 @@ __global__ __launch_bounds__(256) void k_wgrad_simt(WgK k) {
     for (int i = 0; i < 4; ++i) { Gs[lrow][lc4 + i] = gv[i]; Xs[lrow][lc4 + i] = xv[i]; }
     __syncthreads();
 #pragma unroll
-    for (int mm = 0; mm < 16; ++mm) {
-      float av[4], bv[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) { av[i] = Gs[mm][ty * 4 + i]; bv[i] = Xs[mm][tx * 4 + i]; }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+    for (int t = 0; t < 8; ++t) {
+      const float ga = Gs[2 * t + kh][wn * 32 + l32];
+      const float xb = Xs[2 * t + kh][wk * 32 + l32];
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(ga, xb, acc, 0, 0, 0);
     }
     __syncthreads();
   }
   float* part = k.part + (int64_t)split * k.Np * k.Kdim;
-  for (int i = 0; i < 4; ++i) {
-    const int n = n0 + ty * 4 + i;
-    if (n >= k.Np) continue;
-    for (int j = 0; j < 4; ++j) {
-      const int kc = k0 + tx * 4 + j;
-      if (kc < k.Kdim) part[(int64_t)n * k.Kdim + kc] = acc[i][j];
-    }
+  const int kc = k0 + wk * 32 + l32;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int n = n0 + wn * 32 + (r & 3) + 8 * (r >> 2) + 4 * kh;
+    if (n < k.Np && kc < k.Kdim) part[(int64_t)n * k.Kdim + kc] = acc[r];
   }
 }
 
@@ -833,10 +844,10 @@ void conv_wgrad(hipStream_t s, bool f32, const GradIn& g, const ConvIn& in, int 
 #define PG_WG_CASE(G, A_, R_)                                                   \
   if (!done && in.gather == G && aff == A_ && (bool)in.relu == R_) {            \
     if (f32)                                                                    \
-      hipLaunchKernelGGL((k_wgrad_simt<G, A_, R_>), grid, block, 0, s, k);      \
+      hipLaunchKernelGGL((k_wgrad_f32mfma<G, A_, R_>), grid, block, 0, s, k);      \
     else                                                                        \
       hipLaunchKernelGGL((k_wgrad_mfma<G, A_, R_>), grid, block, 0, s, k);      \
-    name = kname(f32 ? "k_wgrad_simt" : "k_wgrad_mfma", {G, A_, R_});            \
+    name = kname(f32 ? "k_wgrad_f32mfma" : "k_wgrad_mfma", {G, A_, R_});            \
     done = true;                                                                \
   }
   PG_WG_CASE(G_DIRECT, false, false)
