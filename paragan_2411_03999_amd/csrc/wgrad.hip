@@ -247,6 +247,172 @@ __global__ __launch_bounds__(WM * WN * 64, 8 / (WM * WN)) void k_wgrad_tr(WgTrK 
     }
 }
 
+
+// ---- row-tap form of the direct 3x3 weight gradient
+// For a 3x3, pad-1 conv over an image whose rows are multiples of 32 pixels
+// wide, a 32-pixel stage lies in one image row, and the three taps (r, 0),
+// (r, 1), (r, 2) of one filter row read that row's input at the 34 pixels
+// ow0 - 1 .. ow0 + 32 shifted by 0, 1, 2.  A block here owns, for one filter
+// row r and one 64-channel chunk, the 192 K columns (r, s, c0 .. c0 + 63),
+// s = 0, 1, 2, and stages that 34 x 64 input segment once per 32 pixels: tap
+// s's B operand is rows s .. s + 31 of it.  The activation bytes staged per
+// MFMA drop to 34 / 96 of the tap-per-block form, whose operand loads bound
+// it.  Gradient tile, transpose reads and fixed-order split reduction as in
+// k_wgrad_tr.
+template <int WM, int TM, int GM, bool RELU>
+__global__ __launch_bounds__(WM * 2 * 64, 8 / (WM * 2)) void k_wgrad_row3(WgTrK k) {
+  constexpr int WN = 2, TN = 3;
+  constexpr int NT = WM * WN * 64;
+  constexpr int BN = WM * TM * 32;
+  constexpr int XR = 34, XC = 64;              // staged input rows (pixels) x channels
+  constexpr int GCH = BN / 8;
+  constexpr int GIT = (kMS * GCH + NT - 1) / NT, XIT = (XR * (XC / 8) + NT - 1) / NT;
+  __shared__ __attribute__((aligned(16))) bf16_t Gs[2][kMS * BN];
+  __shared__ __attribute__((aligned(16))) bf16_t Xs[2][36 * XC];
+
+  const int cch = k.C / XC;                    // 64-channel chunks
+  const int tiles = k.tiles_n * k.tiles_k;     // tiles_k = 3 filter rows x cch
+  const int bid = remap_block(blockIdx.x, gridDim.x);
+  const int split = bid / tiles;
+  const int tile = bid - split * tiles;
+  const int tni = tile / k.tiles_k, tki = tile - tni * k.tiles_k;
+  const int fr = tki / cch, c0 = (tki - fr * cch) * XC;
+  const int n0 = tni * BN;
+  const int mbeg = split * k.m_per_split;
+  const int mend = min(mbeg + k.m_per_split, k.M);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+
+  int g_row[GIT], g_col[GIT], g_lds[GIT];
+  bool g_on[GIT];
+#pragma unroll
+  for (int i = 0; i < GIT; ++i) {
+    const int id = tid + NT * i;
+    const int row = id / GCH, ch = id - (id / GCH) * GCH;
+    g_on[i] = id < kMS * GCH && n0 + ch * 8 < k.Np;
+    g_row[i] = row;
+    g_col[i] = n0 + ch * 8;
+    g_lds[i] = lds_off<BN>(row < kMS ? row : 0, ch * 8);
+  }
+  int x_row[XIT], x_ch[XIT], x_lds[XIT];
+  bool x_on[XIT];
+#pragma unroll
+  for (int i = 0; i < XIT; ++i) {
+    const int id = tid + NT * i;
+    const int row = id / (XC / 8), ch = id - row * (XC / 8);
+    x_on[i] = id < XR * (XC / 8);
+    x_row[i] = row;
+    x_ch[i] = ch;
+    x_lds[i] = lds_off<XC>(x_on[i] ? row : 0, ch * 8);
+  }
+
+  uint4 rg[GIT], rx[XIT];
+  const __amdgpu_buffer_rsrc_t gr = make_rsrc(k.g, k.g_bytes);
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(k.x, k.x_bytes);
+  auto load = [&](int mb) {
+#pragma unroll
+    for (int i = 0; i < GIT; ++i) {
+      const int m = mb + g_row[i];
+      int off;
+      if (GM == kGDirect) {
+        off = m * k.gC + g_col[i];
+      } else {
+        const int t = (int)fdiv((uint32_t)m, k.fdW);
+        const int ow = m - t * k.W;
+        const int b = (int)fdiv((uint32_t)t, k.fdH);
+        const int oh = t - b * k.H;
+        off = ((b * k.Hs + (oh >> 1)) * k.Ws + (ow >> 1)) * k.gC + g_col[i];
+      }
+      rg[i] = buf_ld16(gr, g_on[i] && m < mend ? 2u * (uint32_t)off : kOOB);
+    }
+    // the stage's 32 pixels share one image row (b, oh), from column ow0
+    const int t = (int)fdiv((uint32_t)mb, k.fdW);
+    const int ow0 = mb - t * k.W;
+    const int b = (int)fdiv((uint32_t)t, k.fdH);
+    const int ih = t - b * k.H + fr - 1;
+#pragma unroll
+    for (int i = 0; i < XIT; ++i) {
+      const int iw = ow0 - 1 + x_row[i];
+      const bool ok = x_on[i] && (unsigned)ih < (unsigned)k.H && (unsigned)iw < (unsigned)k.W;
+      rx[i] = buf_ld16(xr, ok ? 2u * (uint32_t)(((b * k.H + ih) * k.W + iw) * k.C + c0 + 8 * x_ch[i]) : kOOB);
+    }
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < GIT; ++i)
+      if (tid + NT * i < kMS * GCH) *reinterpret_cast<uint4*>(&Gs[buf][g_lds[i]]) = rg[i];
+#pragma unroll
+    for (int i = 0; i < XIT; ++i)
+      if (x_on[i]) *reinterpret_cast<uint4*>(&Xs[buf][x_lds[i]]) = RELU ? relu8_bits(rx[i]) : rx[i];
+  };
+
+  // transpose-read offsets as in k_wgrad_tr; B fragment j of this wave is
+  // K columns 32 jj .. + 31 of the 192, jj = 3 wn + j: tap s = jj / 2,
+  // channels 32 (jj % 2) .. of the chunk, read at rows shifted by s
+  const int rA = 8 * (lane >> 5) + ((lane & 15) >> 2);
+  const int cA = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  int a_off[TM], b_off[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) a_off[i] = lds_off<BN>(rA, (wm * TM + i) * 32 + cA);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int jj = wn * TN + j;
+    b_off[j] = lds_off<XC>(rA + (jj >> 1), 32 * (jj & 1) + cA);
+  }
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+  const int nst = (mend - mbeg + kMS - 1) / kMS;
+  if (nst > 0) {
+    load(mbeg);
+    store(0);
+  }
+  __syncthreads();
+  int buf = 0;
+  for (int st = 0; st < nst; ++st) {
+    const bool more = st + 1 < nst;
+    if (more) load(mbeg + (st + 1) * kMS);
+    const bf16_t* gb = Gs[buf];
+    const bf16_t* xb = Xs[buf];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8 av[TM], bv[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) av[i] = tr_pair(gb, a_off[i] + kk * 16 * BN, a_off[i] + (kk * 16 + 4) * BN);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bv[j] = tr_pair(xb, b_off[j] + kk * 16 * XC, b_off[j] + (kk * 16 + 4) * XC);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+    if (more) store(buf ^ 1);
+    __syncthreads();
+    buf ^= 1;
+  }
+
+  float* part = k.part + (int64_t)split * k.Np * k.Kdim;
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int jj = wn * TN + j;
+    const int kc = (fr * 3 + (jj >> 1)) * k.C + c0 + 32 * (jj & 1) + (lane & 31);
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int n = n0 + (wm * TM + i) * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        if (n < k.Np) part[(int64_t)n * k.Kdim + kc] = acc[i][j][r] * k.scale;
+      }
+  }
+}
+
 // dw = scale * sum over splits, each output's splits added in split order.
 // Up to 32 splits: a thread per 4 outputs (16-byte loads, four splits in
 // flight); more: 256 outputs per block, 16 waves each summing every 16th
@@ -412,6 +578,22 @@ std::string launch_tr(hipStream_t s, const WgTrK& k, int blocks, int gm, int xg,
   throw Error{-2, "wgrad_tr: unsupported gather combination"};
 }
 
+// the row-tap kernel: 192 or 256 output channels per block
+template <int WM, int TM>
+std::string launch_row3(hipStream_t s, const WgTrK& k, int blocks, int gm, bool relu) {
+#define PG_ROW3_CASE(GM, RL, GNAME)                                                                    \
+  if (gm == GM && relu == RL) {                                                                        \
+    hipLaunchKernelGGL((k_wgrad_row3<WM, TM, GM, RL>), dim3(blocks), dim3(64 * WM * 2), 0, s, k);     \
+    return "k_wgrad_row3<" + std::to_string(WM * TM * 32) + "x192," GNAME "," #RL ">";                \
+  }
+  PG_ROW3_CASE(kGDirect, false, "false")
+  PG_ROW3_CASE(kGDirect, true, "false")
+  PG_ROW3_CASE(kGUp2, false, "true")
+  PG_ROW3_CASE(kGUp2, true, "true")
+#undef PG_ROW3_CASE
+  throw Error{-2, "wgrad_row3: unsupported gradient gather"};
+}
+
 std::string launch_cfg_tr(hipStream_t s, int cfg, const WgTrK& k, int blocks, int gm, int xg, bool relu) {
   switch (cfg) {
     case 0: return launch_tr<2, 2, 4, 2>(s, k, blocks, gm, xg, relu);
@@ -472,6 +654,15 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   k.tiles_n = p.tiles_n;
   k.tiles_k = p.tiles_k;
   k.splits = p.splits;
+  // the row-tap form (k_wgrad_row3): a direct 3x3 conv over images whose
+  // rows are whole 32-pixel stages, 64-channel chunks, 192 / 256-channel
+  // output tiles; same splits (so the same partial buffer)
+  const bool row3 = R == 3 && in.gather == G_DIRECT && W % 32 == 0 && in.C % 64 == 0 &&
+                    (Np % 256 == 0 || Np % 192 == 0) && k.M % 32 == 0;
+  if (row3) {
+    k.tiles_n = Np / (Np % 256 == 0 ? 256 : 192);
+    k.tiles_k = 3 * (in.C / 64);
+  }
   const int64_t nout = (int64_t)Np * k.Kdim;
   if (p.splits > 1 && (size_t)p.splits * nout * 4 > ws_bytes) throw Error{-3, "conv_wgrad: workspace too small"};
   PG_CHECK(p.splits == 1 || (nout % 4 == 0 && (((uintptr_t)ws | (uintptr_t)dw) & 15) == 0),
@@ -479,11 +670,14 @@ void wgrad_tr(hipStream_t s, const GradIn& g, const ConvIn& in, int H, int W, in
   // a single split writes the scaled result itself; several leave unscaled partials
   k.part = p.splits == 1 ? dw : (float*)ws;
   k.scale = p.splits == 1 ? g.gscale : 1.f;
-  const int blocks = p.splits * p.tiles_n * p.tiles_k;
+  const int blocks = p.splits * k.tiles_n * k.tiles_k;
   const int gm = g.gather == G_UP2 ? kGUp2 : kGDirect;
   std::string name;
   ProfScope prof(s);
-  name = launch_cfg_tr(s, p.cfg, k, blocks, gm, in.gather, in.relu);
+  if (row3)
+    name = Np % 256 == 0 ? launch_row3<4, 2>(s, k, blocks, gm, in.relu) : launch_row3<2, 3>(s, k, blocks, gm, in.relu);
+  else
+    name = launch_cfg_tr(s, p.cfg, k, blocks, gm, in.gather, in.relu);
   PG_LAUNCH_CHECK();
   prof.done(name, flops, k.M, Np, k.Kdim);
   if (p.splits > 1) {
