@@ -456,8 +456,9 @@ int paragan_pipeline_create(paragan_pipeline** out, const paragan_pipeline_cfg* 
                             int32_t n_slots, size_t slot_bytes);
 /* Wait for the next batch in sequence order (timeout_ms < 0: no limit):
  * *seq, *slot.  The slot belongs to the consumer until released.
- * PARAGAN_ETIMEOUT if nothing came in time; PARAGAN_EINVAL once a fetch has
- * failed (the message names the batch). */
+ * PARAGAN_ETIMEOUT if nothing came in time; PARAGAN_EINVAL when the batch
+ * due is one whose fetch failed (the batches before it are delivered first;
+ * nothing after it is fetched; the message names the batch). */
 int paragan_pipeline_next(paragan_pipeline* p, int64_t* seq, int32_t* slot, int32_t timeout_ms);
 int paragan_pipeline_release(paragan_pipeline* p, int32_t slot);
 int paragan_pipeline_get_stats(paragan_pipeline* p, paragan_pipeline_stats* out);

@@ -9,6 +9,7 @@
 // dataset: every value is a function of (seed, batch, index) through the
 // SplitMix64 finaliser, so a batch is the same whichever thread makes it.
 #include <algorithm>
+#include <cstdint>
 #include <chrono>
 #include <condition_variable>
 #include <mutex>
@@ -95,7 +96,8 @@ struct paragan_pipeline {
   double wait_ms = 0.0;
   int live_threads = 0;               // running workers
   bool stop = false;
-  std::string err;                    // first fetch failure (sticky)
+  std::string err;                    // the failure of the lowest failed batch (sticky)
+  int64_t err_seq = INT64_MAX;        // that batch; the batches before it are still delivered
   std::string last_err;               // last failed call's message
   std::vector<std::thread> workers;
 
@@ -125,7 +127,12 @@ struct paragan_pipeline {
       const double ms = ms_since(t0);
       lk.lock();
       if (rc != 0) {
-        if (err.empty()) err = "fetch callback returned " + std::to_string(rc) + " for batch " + std::to_string(seq);
+        // every batch before seq was claimed before it, so those still
+        // arrive and are delivered; nothing after it is claimed any more
+        if (seq < err_seq) {
+          err_seq = seq;
+          err = "fetch callback returned " + std::to_string(rc) + " for batch " + std::to_string(seq);
+        }
         state[(size_t)slot] = kFree;
         free_slots.push_back(slot);
         --outstanding;
@@ -213,7 +220,7 @@ int paragan_pipeline_next(paragan_pipeline* p, int64_t* seq, int32_t* slot, int3
   int s = -1;
   auto ready = [&] {
     s = p->find_ready_locked(p->next_deliver);
-    return s >= 0 || !p->err.empty();
+    return s >= 0 || p->err_seq <= p->next_deliver;
   };
   bool ok;
   if (timeout_ms < 0) {
@@ -223,7 +230,7 @@ int paragan_pipeline_next(paragan_pipeline* p, int64_t* seq, int32_t* slot, int3
     ok = p->cv_ready.wait_for(lk, std::chrono::milliseconds(timeout_ms), ready);
   }
   p->wait_ms += ms_since(t0);
-  if (s < 0 && !p->err.empty()) return bad(p, "pipeline_next: " + p->err);
+  if (s < 0 && p->err_seq <= p->next_deliver) return bad(p, "pipeline_next: " + p->err);
   if (!ok || s < 0) {
     p->last_err = "pipeline_next: no batch within the timeout";
     return PARAGAN_ETIMEOUT;
