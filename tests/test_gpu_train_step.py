@@ -455,3 +455,43 @@ def test_train_step_rejects_n_d_zero_before_launching():
     assert lib.paragan_train_step(ctx, d, G.state, D.state, inp, 0, ws, losses) == lib.EINVAL
     torch.cuda.synchronize()
     assert all(torch.equal(x, y) for x, y in zip(before, G.tensors() + D.tensors()))
+
+
+# ------------------------------------------------------ checkpoint / resume
+def test_resume_from_host_checkpoint_is_bit_identical():
+    """The whole training state is the caller's buffers: two steps in a row
+    equal one step, a round trip of every buffer through host memory into
+    fresh device buffers (and a fresh context and workspace), then the
+    second step -- bit for bit."""
+    torch = need_gpu()
+    a, B, n_D = small_arch(), 4, 2
+    hp = hparams()
+    d, s, _, _, G0, D0 = make_nets(torch, a, B, 407, hp)
+    inp1, keep1 = step_inputs(torch, s, a, B, n_D)
+    inp2, keep2 = step_inputs(torch, s, a, B, n_D)
+    ctx = context()
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+    G, D = G0.clone(torch), D0.clone(torch)
+    l1 = run_train_step(torch, d, G, D, inp1, n_D, ws, ctx)
+    l2 = run_train_step(torch, d, G, D, inp2, n_D, ws, ctx)
+    # resume: the state after step 1 to host and back into new buffers
+    Gr, Dr = G0.clone(torch), D0.clone(torch)
+    m1 = run_train_step(torch, d, Gr, Dr, inp1, n_D, ws, ctx)
+    saved = [[t.cpu().numpy().copy() for t in N.tensors()] + [N.state.opt_t] for N in (Gr, Dr)]
+    del Gr, Dr
+    fresh = []
+    for N0, host in zip((G0, D0), saved):
+        N = N0.clone(torch)
+        assert len(N.tensors()) == len(host) - 1
+        for t, h in zip(N.tensors(), host[:-1]):
+            t.copy_(torch.from_numpy(h))
+        N.state.opt_t = host[-1]
+        fresh.append(N)
+    ctx2 = context()
+    ws2 = lib.workspace(lib.paragan_train_step_ws_size(d))
+    m2 = run_train_step(torch, d, fresh[0], fresh[1], inp2, n_D, ws2, ctx2)
+    assert (m1, m2) == (l1, l2), ((m1, m2), (l1, l2))
+    for X, Y in ((G, fresh[0]), (D, fresh[1])):
+        for t1, t2 in zip(X.tensors(), Y.tensors()):
+            assert torch.equal(t1, t2)
+        assert X.state.opt_t == Y.state.opt_t
