@@ -559,6 +559,26 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
     const bool more = c + 1 < nch;
     // the patch offset of tap (dr, ds) is (dr + ca) PC + ds + cb
     const int ca = GK == G_S2 ? 1 - ((c >> 1) & 1) : pa, cb = GK == G_S2 ? 1 - (c & 1) : pb;
+    // activation fragments (both 16-channel halves) of tap t at patch offset qo
+    auto read_x = [&](int qo, uint4 (&xr)[2][TM]) {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int j = 0; j < TM; ++j) {
+          const int q = q0[j] + qo;
+          xr[kk][j] = *reinterpret_cast<const uint4*>(Pc + q * 32 + 8 * ((2 * kk + h) ^ ((q >> 2) & 3)));
+        }
+    };
+    auto tap_off = [&](int t) {
+      return GK != G_DIRECT ? ((t >> 1) + ca) * PC + (t & 1) + cb : (t / 3) * PC + (t % 3);
+    };
+    // Per tap: all operand reads first, then the MFMAs (the compiler would
+    // otherwise interleave them two by two, waiting on each read).  The
+    // activation fragments of the next tap of the chunk come from the same
+    // patch buffer, which no load touches during the chunk, so they are read
+    // as soon as this tap's MFMAs are issued, ahead of the next barrier;
+    // after it only the weight reads are left.
+    uint4 xnext[2][TM];
     static_for<0, T>([&](auto tc) {
       constexpr int t = decltype(tc)::value;
       constexpr int wfly = (NSW - 2) * BP + (t >= 1 && t <= NSW - 1 ? PLW : 0);
@@ -568,25 +588,33 @@ __global__ __launch_bounds__(WN * WM * 64, 8 / (WN * WM)) void k_conv_halo(CfK k
       else wait_barrier<vm_cap(wlast)>();
       if (s + NSW - 1 < S) issue_w((sb + t + NSW - 1) % NSW, s + NSW - 1);
       if (t == 0 && more) issue_patch((c + 1) & 1, c + 1);
-      const int qoff = GK != G_DIRECT ? ((t >> 1) + ca) * PC + (t & 1) + cb : (t / 3) * PC + (t % 3);
       const bf16_t* Wt = lds + 2 * PATCH + ((sb + t) % NSW) * WST;
+      bf16x8 wv[2][TN];
+      uint4 xr[2][TM];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int i = 0; i < TN; ++i) wv[kk][i] = *reinterpret_cast<const bf16x8*>(Wt + wbase + i * 32 * 32 + rdw[kk]);
+      if (t == 0) read_x(tap_off(0), xr);
+      else {
+#pragma unroll
+        for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+          for (int j = 0; j < TM; ++j) xr[kk][j] = xnext[kk][j];
+      }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk) {
-        bf16x8 wv[TN], xv[TM];
+        bf16x8 xv[TM];
 #pragma unroll
-        for (int i = 0; i < TN; ++i) wv[i] = *reinterpret_cast<const bf16x8*>(Wt + wbase + i * 32 * 32 + rdw[kk]);
-#pragma unroll
-        for (int j = 0; j < TM; ++j) {
-          const int q = q0[j] + qoff;
-          const uint4 v = *reinterpret_cast<const uint4*>(Pc + q * 32 + 8 * ((2 * kk + h) ^ ((q >> 2) & 3)));
-          xv[j] = __builtin_bit_cast(bf16x8, RELU ? relu8_bits(v) : v);
-        }
+        for (int j = 0; j < TM; ++j) xv[j] = __builtin_bit_cast(bf16x8, RELU ? relu8_bits(xr[kk][j]) : xr[kk][j]);
 #pragma unroll
         for (int i = 0; i < TN; ++i)
 #pragma unroll
           for (int j = 0; j < TM; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[i], xv[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wv[kk][i], xv[j], acc[i][j], 0, 0, 0);
       }
+      if (t + 1 < T) read_x(tap_off(t + 1), xnext);
     });
     sb = (sb + T) % NSW;
   }
