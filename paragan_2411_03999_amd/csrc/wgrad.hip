@@ -53,6 +53,49 @@ PG_DEV bf16x8 tr_pair(const bf16_t* base, int off_lo, int off_hi) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// One 32-deep K step of a wave's TM x TN accumulator tiles: A rows from the
+// gradient tile gb (row stride sa), B rows from the activation tile xb (row
+// stride sb), both read transposed.  With at most eight tiles every operand
+// of the step is read before the first MFMA (left to itself the compiler
+// interleaves reads and MFMAs two by two, waiting on each read); wider
+// tiles have no registers for that and take each 16-deep half in turn.
+template <int TM, int TN>
+PG_DEV void wg_step(const bf16_t* gb, const bf16_t* xb, const int (&a_off)[TM], const int (&b_off)[TN], int sa,
+                    int sb, f32x16 (&acc)[TM][TN]) {
+  if constexpr (TM * TN <= 8) {
+    bf16x8 av[2][TM], bv[2][TN];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) av[kk][i] = tr_pair(gb, a_off[i] + kk * 16 * sa, a_off[i] + (kk * 16 + 4) * sa);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bv[kk][j] = tr_pair(xb, b_off[j] + kk * 16 * sb, b_off[j] + (kk * 16 + 4) * sb);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[kk][i], bv[kk][j], acc[i][j], 0, 0, 0);
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+      bf16x8 av[TM], bv[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) av[i] = tr_pair(gb, a_off[i] + kk * 16 * sa, a_off[i] + (kk * 16 + 4) * sa);
+#pragma unroll
+      for (int j = 0; j < TN; ++j) bv[j] = tr_pair(xb, b_off[j] + kk * 16 * sb, b_off[j] + (kk * 16 + 4) * sb);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
 struct WgTrK {
   const bf16_t* g;   // gradient source, channel stride gC
   const bf16_t* x;   // activation source [B][Hx][Wx][C]
@@ -214,19 +257,7 @@ __global__ __launch_bounds__(WM * WN * 64, 8 / (WM * WN)) void k_wgrad_tr(WgTrK 
     if (more) load(mbeg + (st + 1) * kMS);
     const bf16_t* gb = Gs[buf];
     const bf16_t* xb = Xs[buf];
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      bf16x8 av[TM], bv[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) av[i] = tr_pair(gb, a_off[i] + kk * 16 * BN, a_off[i] + (kk * 16 + 4) * BN);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bv[j] = tr_pair(xb, b_off[j] + kk * 16 * BK, b_off[j] + (kk * 16 + 4) * BK);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
+    wg_step<TM, TN>(gb, xb, a_off, b_off, BN, BK, acc);
     if (more) store(buf ^ 1);
     __syncthreads();
     buf ^= 1;
@@ -380,19 +411,7 @@ __global__ __launch_bounds__(WM * 2 * 64, 8 / (WM * 2)) void k_wgrad_row3(WgTrK 
     if (more) load(mbeg + (st + 1) * kMS);
     const bf16_t* gb = Gs[buf];
     const bf16_t* xb = Xs[buf];
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      bf16x8 av[TM], bv[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) av[i] = tr_pair(gb, a_off[i] + kk * 16 * BN, a_off[i] + (kk * 16 + 4) * BN);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bv[j] = tr_pair(xb, b_off[j] + kk * 16 * XC, b_off[j] + (kk * 16 + 4) * XC);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0, 0, 0);
-    }
+    wg_step<TM, TN>(gb, xb, a_off, b_off, BN, XC, acc);
     if (more) store(buf ^ 1);
     __syncthreads();
     buf ^= 1;
