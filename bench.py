@@ -27,7 +27,7 @@ The JSON line also carries:
                 packing launches run on the second stream beside the
                 convolutions, so theirs include waiting for CUs);
   cpu_baseline  the float64 CPU oracle timed on this host on a bounded
-                sample (one train step at batch 1 on the same architecture);
+                sample (one train step at batch 2 on the same architecture);
   extras        the other workloads, each timed the same way after the main
                 one: the BigGAN-128 discriminator step on 32 real + 32 fake
                 images (paragan_d_step), the asynchronous update scheme at
@@ -355,7 +355,7 @@ def main():
     ap.add_argument("--seed", type=int, default=1004)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip the D-step, async and BigGAN-512 timings")
-    ap.add_argument("--cpu-batch", type=int, default=1)
+    ap.add_argument("--cpu-batch", type=int, default=2)
     ap.add_argument("--kernels-out", default=None, help="write the per-kernel table (JSON) here")
     ap.add_argument("--copy-probe", action="store_true",
                     help="before the timed steps, copy 1 GiB device to device once: the known-size "
