@@ -32,7 +32,9 @@ The JSON line also carries:
                 one: the BigGAN-128 discriminator step on 32 real + 32 fake
                 images (paragan_d_step), the asynchronous update scheme at
                 B = 256, n_D = 2 (generator batch 512, paragan_async_step),
-                and the BigGAN-512 train step at batch 16, n_D = 2.
+                the BigGAN-512 train step at batch 16, n_D = 2, the main
+                step fed by the host pipeline (pipeline_fed) and the main
+                step with the weight gradients overlapped (overlap_wgrad).
 """
 import argparse
 import json
@@ -509,11 +511,21 @@ def main():
     }
     if not args.no_extras and args.arch == "biggan128" and B >= 32 and n_D >= 2:
         print("bench: timing the extra workloads ...", file=sys.stderr, flush=True)
+        # the same step with the block backwards' weight gradients on a
+        # further stream beside their data gradients (opt-in; the kernel
+        # rates above are measured with it off, as they share the CUs on)
+        ctx.set_overlap_wgrad(1)
+        ms_ov = timed(torch, step, args.steps, 1)
+        ctx.set_overlap_wgrad(0)
+        overlap = {"workload": "the same train step with each block backward's weight gradients on a further "
+                               "stream beside its data gradients (paragan_set_overlap_wgrad; bit-identical)",
+                   "ms_per_step": ms_ov, "images_per_sec": B / (ms_ov / 1e3)}
         fed = pipeline_fed(torch, lib, C, step, d, keep, n_D)
         del ws
         torch.cuda.empty_cache()
         out["extras"] = extras(torch, lib, C, ctx, gen, Dn, keep[0:n_D], keep[n_D:2 * n_D])
         out["extras"]["pipeline_fed"] = fed
+        out["extras"]["overlap_wgrad"] = overlap
         print("bench: extras %s" % json.dumps(out["extras"]), file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         print("bench: timing the CPU oracle sample ...", file=sys.stderr, flush=True)

@@ -72,6 +72,18 @@ void paragan_destroy(paragan_ctx* ctx);
 const char* paragan_last_error(const paragan_ctx* ctx);
 /* Block until all work enqueued by this context has finished. */
 int paragan_sync(paragan_ctx* ctx);
+/* Off (0, the default) or on (1): whether the step calls (paragan_g_sample,
+ * paragan_d_step, paragan_g_step, paragan_train_step) run the weight
+ * gradients of each block backward -- with their bias column sums -- on a
+ * further stream of the context (default priority), beside the block's
+ * data gradients on the context's stream, ordered by events and joined
+ * before the block's SN backward; every call returns with both streams
+ * joined (also on error).  Results are bit-identical either way.  On, the
+ * data- and weight-gradient kernels share the CUs, so a step finishes
+ * sooner while each kernel's own launch takes longer: per-kernel rates
+ * measured with it on count the shared time.  Returns PARAGAN_EINVAL for
+ * other values. */
+int paragan_set_overlap_wgrad(paragan_ctx* ctx, int on);
 
 /* Channel stride of an activation tensor with c channels. */
 int64_t paragan_cpad(int64_t c);

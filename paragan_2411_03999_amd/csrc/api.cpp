@@ -21,8 +21,15 @@ struct ProfBind {
 }  // namespace
 
 static int fail(paragan_ctx* ctx, int code, const std::string& msg) {
-  if (ctx) ctx->err = msg;
-  else g_create_err = msg;
+  if (ctx) {
+    ctx->err = msg;
+    // leave no work of a failed call running on the context's own streams
+    // (it may read the caller's buffers)
+    if (ctx->side) (void)hipStreamSynchronize(ctx->side);
+    if (ctx->wside) (void)hipStreamSynchronize(ctx->wside);
+  } else {
+    g_create_err = msg;
+  }
   return code;
 }
 
@@ -68,7 +75,13 @@ void paragan_destroy(paragan_ctx* ctx) {
     (void)hipStreamSynchronize(ctx->side);
     (void)hipStreamDestroy(ctx->side);
   }
+  if (ctx->wside) {
+    (void)hipStreamSynchronize(ctx->wside);
+    (void)hipStreamDestroy(ctx->wside);
+  }
   for (hipEvent_t e : ctx->ev)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : ctx->wev)
     if (e) (void)hipEventDestroy(e);
   delete ctx;
 }
@@ -80,6 +93,13 @@ const char* paragan_last_error(const paragan_ctx* ctx) {
 int paragan_sync(paragan_ctx* ctx) {
   if (!ctx) return PARAGAN_EINVAL;
   PG_TRY(ctx, PG_HIP(hipStreamSynchronize(ctx->stream)))
+}
+
+int paragan_set_overlap_wgrad(paragan_ctx* ctx, int on) {
+  if (!ctx) return PARAGAN_EINVAL;
+  if (on != 0 && on != 1) return fail(ctx, PARAGAN_EINVAL, "paragan_set_overlap_wgrad: on must be 0 or 1");
+  ctx->overlap_wgrad = on == 1;
+  return PARAGAN_OK;
 }
 
 int64_t paragan_cpad(int64_t c) { return cpad(c); }

@@ -273,6 +273,28 @@ void GBlock::fwd(const Exec& ex, const Params& P, const void* x, const float* co
   conv_fwd(ex.st, f32, i2, 2 * H, 2 * W, 3, wp2, Cop, o2);
 }
 
+// The weight gradients of a block backward (and their bias column sums)
+// read only the output gradients and the saved activations: with ex.side
+// they run on that stream, forked from ex.st once their gradient is ready,
+// while the data gradients continue on ex.st; the join comes before the SN
+// backward, which reads them.  The kernels are the same either way, so are
+// the results.
+struct WgSide {
+  const Exec& ex;
+  hipStream_t sw;
+  explicit WgSide(const Exec& e) : ex(e), sw(e.side ? e.side : e.st) {}
+  void fork() const {
+    if (!ex.side) return;
+    PG_HIP(hipEventRecord(ex.ev_fork, ex.st));
+    PG_HIP(hipStreamWaitEvent(sw, ex.ev_fork, 0));
+  }
+  void join() const {
+    if (!ex.side) return;
+    PG_HIP(hipEventRecord(ex.ev_join, sw));
+    PG_HIP(hipStreamWaitEvent(ex.st, ex.ev_join, 0));
+  }
+};
+
 void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* cond, const void* dy, void* dx,
                  float* dcond, bool dcond_acc) {
   Arena a(ex.ws);
@@ -287,19 +309,22 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   } else {
     g_pack_dgrad(*this, ex.st, P, wd1, wd2, wdsc);
   }
+  const WgSide side(ex);
+  const hipStream_t sw = side.sw;
+  side.fork();
   // conv2: dW2, db2
   GradIn gdy;
   gdy.g = dy; gdy.Hs = H2; gdy.Ws = W2; gdy.C = Cop;
   ConvIn ia2;
   ia2.x = a2; ia2.B = B; ia2.Hx = H2; ia2.Wx = W2; ia2.C = Cop;
-  conv_wgrad(ex.st, f32, gdy, ia2, H2, W2, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
-  colsum(ex.st, f32, dy, M2, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
+  conv_wgrad(sw, f32, gdy, ia2, H2, W2, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
+  colsum(sw, f32, dy, M2, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
   // skip: dWsc at full resolution against up2(x); dbsc = db2
   ConvIn ax;
   ax.x = x; ax.B = B; ax.Hx = H; ax.Wx = W; ax.C = Cip; ax.gather = G_UP2;
-  conv_wgrad(ex.st, f32, gdy, ax, H2, W2, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
+  conv_wgrad(sw, f32, gdy, ax, H2, W2, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
   // both biases add to the block output: their gradients are the same column sum of dy
-  PG_HIP(hipMemcpyAsync(P.gr("sc.b"), P.gr("conv2.b"), (size_t)cout * 4, hipMemcpyDeviceToDevice, ex.st));
+  PG_HIP(hipMemcpyAsync(P.gr("sc.b"), P.gr("conv2.b"), (size_t)cout * 4, hipMemcpyDeviceToDevice, sw));
   // dx_skip = Wsc^T sum2x2(dy)   (low resolution, fp32); in bf16 one
   // stride-2 2x2 conv with Wsc^T on every tap
   ConvIn dsp;
@@ -316,6 +341,7 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   // cBN2 backward (through the ReLU) -> dh1
   bn_bwd(ex.st, f32, w.da2, false, h1, B, H2, W2, cout, Cop, mean2, rstd2, gain2, bias2, Cop, nullptr, w.dh1,
          w.dg2, w.db2, Cop, w.bnb);
+  side.fork();
   // conv1: dW1, db1
   GradIn gdh;
   gdh.g = w.dh1; gdh.Hs = H2; gdh.Ws = W2; gdh.C = Cop;
@@ -325,11 +351,11 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
     // bf16: the four sub-pixel 2x2 forms over a1 itself, folded onto the 3x3 filter
     ConvIn src = ia1;
     src.gather = G_DIRECT;
-    wgrad_sub(ex.st, gdh, src, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+    wgrad_sub(sw, gdh, src, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
   } else {
-    conv_wgrad(ex.st, f32, gdh, ia1, H2, W2, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+    conv_wgrad(sw, f32, gdh, ia1, H2, W2, 3, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
   }
-  colsum(ex.st, f32, w.dh1, M2, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
+  colsum(sw, f32, w.dh1, M2, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
   // da1 = the 2x2 sum (the upsample's adjoint) of conv1^T dh1: in bf16 one
   // stride-2 4x4 conv straight to the low resolution; in fp32 at 2x
   // resolution, summed by the BN backward
@@ -360,6 +386,7 @@ void GBlock::bwd(const Exec& ex, const Params& P, const void* x, const float* co
   jobs[4] = sn_bwd_job(P, "conv1.w", sn[2], w.dwp1, 3, Cip, nullptr);
   jobs[5] = sn_bwd_job(P, "conv2.w", sn[5], w.dwp2, 3, Cop, nullptr);
   jobs[6] = sn_bwd_job(P, "sc.w", sn[6], w.dwpsc, 1, Cip, nullptr);
+  side.join();
   sn_bwd_group(ex.st, jobs, 7, w.part);
 }
 
@@ -548,6 +575,9 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   } else {
     d_pack_dgrad(*this, ex.st, P, wd1, wd2, wdsc);
   }
+  const WgSide side(ex);
+  const hipStream_t sw = side.sw;
+  if (wgrad) side.fork();
   // conv2 (its output gradient is dy, or dy/4 spread over 2x2 when pooled)
   GradIn g2;
   g2.g = dy; g2.Hs = Ho; g2.Ws = Wo; g2.C = Cop;
@@ -562,12 +592,12 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
       g2s.g = dy; g2s.Hs = Ho; g2s.Ws = Wo; g2s.C = Cop;
       ConvIn a2s = a2;
       a2s.gather = G_S2;
-      conv_wgrad(ex.st, f32, g2s, a2s, Ho, Wo, 4, Cop, w.dwp2s, w.wg, w.wg_bytes, ex.n_cu);
-      fold_pool4_wgrad(ex.st, w.dwp2s, Cop, Cop, w.dwp2);
+      conv_wgrad(sw, f32, g2s, a2s, Ho, Wo, 4, Cop, w.dwp2s, w.wg, w.wg_bytes, ex.n_cu);
+      fold_pool4_wgrad(sw, w.dwp2s, Cop, Cop, w.dwp2);
     } else {
-      conv_wgrad(ex.st, f32, g2, a2, H, W, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
+      conv_wgrad(sw, f32, g2, a2, H, W, 3, Cop, w.dwp2, w.wg, w.wg_bytes, ex.n_cu);
     }
-    colsum(ex.st, f32, dy, Mo, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
+    colsum(sw, f32, dy, Mo, cout, Cop, 1.f, P.gr("conv2.b"), w.cs);
   }
   // dh = (conv2^T dc2) * [h > 0]
   ConvIn d2;
@@ -589,8 +619,9 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
   ConvIn a1;
   a1.x = x; a1.B = B; a1.Hx = H; a1.Wx = W; a1.C = Cip; a1.relu = preact; a1.c_real = K1;
   if (wgrad) {
-    conv_wgrad(ex.st, f32, g1, a1, H, W, R1, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
-    colsum(ex.st, f32, w.dh, M, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
+    side.fork();   // dh is ready
+    conv_wgrad(sw, f32, g1, a1, H, W, R1, Cop, w.dwp1, w.wg, w.wg_bytes, ex.n_cu);
+    colsum(sw, f32, w.dh, M, cout, Cop, 1.f, P.gr("conv1.b"), w.cs);
   }
   // skip
   if (lsc) {
@@ -600,9 +631,9 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     as.x = x; as.B = B; as.Hx = H; as.Wx = W; as.C = Cip; as.c_real = cin;
     if (down) { as.x = xp; as.Hx = Ho; as.Wx = Wo; }
     if (wgrad) {
-      conv_wgrad(ex.st, f32, gs, as, Ho, Wo, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
+      conv_wgrad(sw, f32, gs, as, Ho, Wo, 1, Cop, w.dwpsc, w.wg, w.wg_bytes, ex.n_cu);
       // both biases add to the block output (after the pool): the same column sum of dy
-      PG_HIP(hipMemcpyAsync(P.gr("sc.b"), P.gr("conv2.b"), (size_t)cout * 4, hipMemcpyDeviceToDevice, ex.st));
+      PG_HIP(hipMemcpyAsync(P.gr("sc.b"), P.gr("conv2.b"), (size_t)cout * 4, hipMemcpyDeviceToDevice, sw));
     }
     if (dx) {
       ConvIn ds;
@@ -632,6 +663,7 @@ void DBlock::bwd(const Exec& ex, const Params& P, const void* x, const void* dy,
     if (im2col) im2col_grad(ex.st, w.dcol, B, H, W, (float*)dx);
   }
   if (!wgrad) return;
+  side.join();
   const SnBwdJob jobs[3] = {sn_bwd_job(P, "conv1.w", sn[0], w.dwp1, R1, Cip, nullptr),
                             sn_bwd_job(P, "conv2.w", sn[1], w.dwp2, 3, Cop, nullptr),
                             lsc ? sn_bwd_job(P, "sc.w", sn[2], w.dwpsc + ksc, 1, Cip, nullptr) : SnBwdJob{}};

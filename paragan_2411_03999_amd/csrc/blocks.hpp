@@ -80,6 +80,11 @@ struct Exec {
   int n_cu;
   void* ws;           // scratch shared by the steps of one block call
   size_t ws_bytes;
+  // with side set, a block backward runs its weight gradients there, beside
+  // its data gradients on st, ordered by the two events (fork: st -> side,
+  // join: side -> st); both streams are joined when the call returns
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_join = nullptr;
 };
 
 // ----------------------------------------------------------- G block

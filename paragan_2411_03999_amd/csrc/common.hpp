@@ -162,6 +162,12 @@ struct paragan_ctx {
   // use, released with the context
   hipStream_t side = nullptr;
   hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  // a third stream (default priority) for the weight gradients of the block
+  // backwards inside the step calls, beside their data gradients, and the
+  // fork / join events that order it; created on first use
+  hipStream_t wside = nullptr;
+  hipEvent_t wev[2] = {nullptr, nullptr};
+  bool overlap_wgrad = false;   // use wside (paragan_set_overlap_wgrad)
   int device = 0;
   int n_cu = 0;
   void* sn_scratch = nullptr;   // the device's address of the library's SN scratch array

@@ -260,7 +260,7 @@ void GNet::bwd(const Exec& ex, const Params& P, const float* z, const int32_t* y
   const Arch& a = a_;
   Arena w(ex.ws);
   GNetWs r = gnet_carve(a, B_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
-  Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
+  Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes, ex.side, ex.ev_fork, ex.ev_join};
   void* gcur = r.g0;
   void* gnext = r.g1;
   head_.bwd(Exec{ex.st, ex.n_cu, r.head, r.head_bytes}, P, in_[a.n_g], img_, dimg, ldd, gcur);
@@ -462,7 +462,7 @@ void DNet::bwd(const Exec& ex, const Params& P, const int32_t* y, const float* d
   const Arch& a = a_;
   Arena w(ex.ws);
   DNetWs r = dnet_carve(a, N_, blocks_, attn_after_ >= 0 ? &attn_ : nullptr, w, ex.n_cu);
-  Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes};
+  Exec eb{ex.st, ex.n_cu, r.blk, r.blk_bytes, ex.side, ex.ev_fork, ex.ev_join};
   const DBlock& last = blocks_.back();
   const int nb = (int)blocks_.size();
   const void* xl = in_[nb];
@@ -549,6 +549,15 @@ struct StepRun {
     Arena w(ws);
     r = step_carve(a, B, w, g, d2, d1, ctx->n_cu);
     ex = Exec{st, ctx->n_cu, r.net, r.net_bytes};
+    if (ctx->overlap_wgrad) {
+      if (!ctx->wside) {
+        PG_HIP(hipStreamCreateWithFlags(&ctx->wside, hipStreamNonBlocking));
+        for (hipEvent_t& e : ctx->wev) PG_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+      }
+      ex.side = ctx->wside;
+      ex.ev_fork = ctx->wev[0];
+      ex.ev_join = ctx->wev[1];
+    }
     LG = g_layout(a);
     LD = d_layout(a);
     PG = Params{&LG, "", G ? G->params : nullptr, G ? G->u : nullptr, G ? G->grads : nullptr};

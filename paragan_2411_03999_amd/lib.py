@@ -114,6 +114,7 @@ _SIGS = {
     "paragan_destroy": (None, [_P]),
     "paragan_last_error": (C.c_char_p, [_P]),
     "paragan_sync": (C.c_int, [_P]),
+    "paragan_set_overlap_wgrad": (C.c_int, [_P, C.c_int]),
     "paragan_cpad": (C.c_int64, [C.c_int64]),
     "paragan_sn_ws_size": (C.c_int, [C.c_int64, C.c_int64, C.POINTER(C.c_size_t)]),
     "paragan_sn_power_iter": (C.c_int, [_P, _P, C.c_int64, C.c_int64, _P, _P, _P, C.c_int, C.c_float, _P]),
@@ -216,6 +217,11 @@ class Context:
         if rc != OK:
             raise ParaganError(rc, load().paragan_last_error(self.h).decode())
         return rc
+
+    def set_overlap_wgrad(self, on):
+        """Run the block backwards' weight gradients of the step calls on a
+        further stream beside their data gradients (bit-identical results)."""
+        return self.check(load().paragan_set_overlap_wgrad(self.h, int(on)))
 
     def close(self):
         if self.h:

@@ -349,6 +349,35 @@ def test_train_step_equals_its_pieces_and_is_deterministic():
         assert X.state.opt_t == Y.state.opt_t
 
 
+@pytest.mark.parametrize("arch,B", [("small", 4), ("biggan128", 2)])
+def test_overlapped_weight_gradients_are_bit_identical(arch, B):
+    """With paragan_set_overlap_wgrad on, the block backwards' weight
+    gradients run on a further stream beside the data gradients: two train
+    steps give the same losses and state, bit for bit, as with it off."""
+    torch = need_gpu()
+    a, n_D = ARCHS[arch](), 2
+    hp = hparams()
+    d, s, _, _, G0, D0 = make_nets(torch, a, B, 409, hp)
+    inp1, keep1 = step_inputs(torch, s, a, B, n_D)
+    inp2, keep2 = step_inputs(torch, s, a, B, n_D)
+    ws = lib.workspace(lib.paragan_train_step_ws_size(d))
+    print("overlap case", arch, B, flush=True)
+    runs = []
+    for on in (0, 1):
+        ctx = context()
+        ctx.set_overlap_wgrad(on)
+        G, D = G0.clone(torch), D0.clone(torch)
+        l = run_train_step(torch, d, G, D, inp1, n_D, ws, ctx) + run_train_step(torch, d, G, D, inp2, n_D, ws, ctx)
+        runs.append((l, G, D))
+    (l0, G0r, D0r), (l1, G1r, D1r) = runs
+    assert l0 == l1, (l0, l1)
+    for X, Y in ((G0r, G1r), (D0r, D1r)):
+        for t0, t1 in zip(X.tensors(), Y.tensors()):
+            assert torch.equal(t0, t1)
+    with pytest.raises(lib.ParaganError):
+        context().set_overlap_wgrad(2)
+
+
 def test_train_step_minimal_vs_oracle():
     """The whole iteration against the oracle's, end to end, on a network
     shallow enough that no decision inside it is near a tie: every loss,
