@@ -17,14 +17,17 @@
  *   problem.  No C++ exception crosses the ABI.
  * - Streams: all device work is enqueued on the hipStream_t given to
  *   paragan_create(), in order; paragan_train_step and paragan_async_step
- *   also use a second stream of the context (default priority, created on
- *   first use), ordered by events and idle again when they return.  Calls
- *   are asynchronous unless stated.
+ *   also use a second stream of the context, and with
+ *   paragan_set_overlap_wgrad on the step calls use a third (default
+ *   priority, created on first use), ordered by events and idle again when
+ *   the call returns, also on error.  Calls are asynchronous unless
+ *   stated.
  * - Memory: every device buffer is allocated and owned by the caller and
  *   passed as a plain device pointer.  The library allocates no device
  *   memory; its one device-resident object is the fixed 4 MiB scratch
- *   array of paragan_sn_power_iter_noalloc, part of the loaded code.  Sizes of the "saved" (forward -> backward) and "ws" (scratch)
- *   buffers come from the *_sizes() queries and must be 256-byte aligned.
+ *   array of paragan_sn_power_iter_noalloc, part of the loaded code.
+ *   Sizes of the "saved" (forward -> backward) and "ws" (scratch) buffers
+ *   come from the *_sizes() queries and must be 256-byte aligned.
  * - Activations are NHWC.  Their channel stride is the channel count
  *   rounded up to a multiple of 32 (paragan_cpad()); padded channels hold
  *   zeros on input and are written as zeros.  dtype PARAGAN_BF16 means
