@@ -5,7 +5,10 @@
 * every backward pass against central finite differences of its forward in
   float64 with spectral-norm u, v held fixed (the gradient's definition);
 * exact commutations the blocks rely on, the D concat(real, fake)
-  invariance, and bf16 storage emulation properties.
+  invariance, and bf16 storage emulation properties;
+* the bf16 backward's rounding points (recorded, in order) and their size
+  against the unrounded backward on the same cache, with the vanishing
+  gradient of the bias that feeds a batch norm.
 """
 import os
 
@@ -204,6 +207,100 @@ def test_bf16_emulation_rounds_block_outputs_and_stays_close():
     np.testing.assert_array_equal(bf16(y16), y16)
     np.testing.assert_array_equal(bf16(c16["h"]), c16["h"])
     assert np.abs(y16 - y64).max() / np.abs(y64).max() < 2e-2
+
+
+def _fwd_cache(block):
+    """One block forward with bf16 storage: (run_bwd, dims), where
+    run_bwd(bf16) runs the block backward on that same cache with or
+    without the backward's bf16 roundings (masks and batch statistics
+    shared, so the two differ only by those roundings)."""
+    s = Stream(25 if block == "g" else 26)
+    if block == "g":
+        n, h, w, cin, cout, dc = 3, 4, 4, 16, 8, 6
+        shapes = B.gblock_param_shapes(cin, cout, dc)
+        p = init_params(shapes, s)
+        u = init_u(shapes, ["bn1.gain", "bn1.bias", "conv1.w", "bn2.gain", "bn2.bias", "conv2.w", "sc.w"], s)
+        x, cond = bf16(s.normal((n, h, w, cin))), s.normal((n, dc))
+        _, _, cache = B.gblock_fwd(x, cond, p, u, B.BlockCfg(bf16=True))
+        dy = bf16(s.normal((n, 2 * h, 2 * w, cout)))
+
+        def run(r):
+            dx, _, g = B.gblock_bwd(dy, cache, B.BlockCfg(bf16=r))
+            return dx, g
+    else:
+        n, h, w, cin, cout = 2, 8, 8, 8, 16
+        shapes = B.dblock_param_shapes(cin, cout, True)
+        p = init_params(shapes, s)
+        u = init_u(shapes, ["conv1.w", "conv2.w", "sc.w"], s)
+        x = bf16(s.normal((n, h, w, cin)))
+        _, _, cache = B.dblock_fwd(x, p, u, B.BlockCfg(bf16=True), True, True, True)
+        dy = bf16(s.normal((n, h // 2, w // 2, cout)))
+
+        def run(r):
+            return B.dblock_bwd(dy, cache, B.BlockCfg(bf16=r), True, True, True)
+    return run, (n, h, w, cin, cout)
+
+
+def _bwd_pair(block):
+    run, _ = _fwd_cache(block)
+    dx16, g16 = run(True)
+    dx64, g64 = run(False)
+    return dx16, g16, dx64, g64
+
+
+@pytest.mark.parametrize("block", ["g", "d"])
+def test_bf16_backward_rounds_stored_gradients_only(block):
+    """Mixed precision (Implementation, "Mixed-Precision Training") stores
+    activation gradients in bf16: the bf16 backward's input gradient is
+    bf16-representable; its roundings change the result (they are there)
+    but by a few units of bf16 roundoff (2^-9) of each tensor's scale, as
+    the two or three roundings on the path (hidden gradient, skip operand,
+    output) allow; the weight and bias gradients, accumulated in float64
+    from rounded operands, move by no more."""
+    dx16, g16, dx64, g64 = _bwd_pair(block)
+    np.testing.assert_array_equal(bf16(dx16), dx16)
+    u = 2.0 ** -9
+    scale = np.abs(dx64).max()
+    assert np.abs(dx16 - dx64).max() > 0
+    assert np.abs(dx16 - dx64).max() <= 4 * u * scale, (np.abs(dx16 - dx64).max() / scale)
+    dead = set()
+    if block == "g":
+        # conv1 feeds the second batch norm, which cancels any per-channel
+        # shift: the exact gradient of conv1's bias vanishes (the bf16 value
+        # is the roundoff of summing the rounded hidden gradient)
+        assert np.abs(g64["conv1.b"]).max() <= 1e-12 * np.abs(g64["conv2.b"]).max()
+        dead.add("conv1.b")
+    for k in g64:
+        if k in dead:
+            continue
+        sc = np.abs(g64[k]).max()
+        assert np.abs(g16[k] - g64[k]).max() <= 4 * u * sc, (k, np.abs(g16[k] - g64[k]).max() / sc)
+
+
+@pytest.mark.parametrize("block", ["g", "d"])
+def test_bf16_backward_rounding_points(block, monkeypatch):
+    """Where the bf16 backward rounds: exactly the activation gradients the
+    mixed-precision path stores between kernels -- G block: the skip
+    gradient at low resolution (the operand of its data gradient), the
+    hidden gradient dh1 after the second BN backward, the input gradient;
+    D block: the hidden gradient dh after the ReLU mask, the input gradient
+    -- in that order, and nothing else (weight gradients, BN terms and the
+    fp32 skip path stay unrounded)."""
+    run, (n, h, w, cin, cout) = _fwd_cache(block)
+    seen = []
+    real = B.rounder
+
+    def recording(emulate):
+        r = real(emulate)
+        return (lambda a: (seen.append(np.shape(a)), r(a))[1]) if emulate else r
+    monkeypatch.setattr(B, "rounder", recording)
+    dx16, _ = run(True)
+    if block == "g":
+        want = [(n, h, w, cout), (n, 2 * h, 2 * w, cout), (n, h, w, cin)]
+    else:
+        want = [(n, h, w, cout), (n, h, w, cin)]
+    assert seen == want, seen
+    assert dx16.shape == want[-1]
 
 
 def test_train_step_runs_and_updates():
