@@ -70,6 +70,35 @@ def test_dblock_validation(L):
     assert lib.paragan_dblock_check(ident) == lib.EINVAL         # identity skip, cin != cout
 
 
+def test_pixel_count_limits(L):
+    """Offsets inside the kernels are 32-bit: each module's check accepts
+    the largest pixel count below 2^31 and rejects the next one (before
+    anything is launched), and the network check bounds the concatenated
+    real + fake batch the same way."""
+    big = 1 << 15                       # H = W = 2^15: 2^30 pixels per image
+    g = lib.GBlockDesc(1, big // 4, big, 64, 64, 128, lib.BF16, 1, 1e-5, 1e-12)
+    assert lib.paragan_gblock_check(g) == lib.OK                  # output pixels 4 B H W = 2^30
+    g.H = big // 2
+    assert lib.paragan_gblock_check(g) == lib.EINVAL              # 2^31
+    d = lib.DBlockDesc(1, big, big, 16, 32, 1, 1, 1, lib.BF16, 1, 1e-12)
+    assert lib.paragan_dblock_check(d) == lib.OK                  # 2^30 pixels
+    d.B = 2
+    assert lib.paragan_dblock_check(d) == lib.EINVAL              # 2^31 pixels
+    a = lib.AttnDesc(1, big, big, 64, 1, 1e-12)
+    assert lib.paragan_attn_check(a) == lib.OK
+    a.B = 2
+    assert lib.paragan_attn_check(a) == lib.EINVAL
+    o = lib.GoutDesc(1, big, 704, 96, 1, 1e-5, 1e-12)
+    assert lib.paragan_gout_check(o) == lib.OK                    # 2.3e7 pixels
+    o.B = (1 << 31) // (big * 704) + 1
+    assert lib.paragan_gout_check(o) == lib.EINVAL
+    n = _desc(O.biggan128())
+    n.B = (1 << 31) // (2 * 128 * 128)                            # 2 B img^2 = 2^31: rejected
+    assert lib.paragan_biggan_check(n) == lib.EINVAL
+    n.B -= 1
+    assert lib.paragan_biggan_check(n) == lib.OK
+
+
 def test_entry_points_reject_null_context(L):
     d = lib.DBlockDesc(2, 8, 8, 16, 32, 1, 1, 1, lib.BF16, 1, 1e-12)
     assert L.paragan_dblock_fwd(None, C.byref(d), None, None, None, None, None, None) == lib.EINVAL
